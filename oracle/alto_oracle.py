@@ -1,0 +1,430 @@
+"""CPU oracle for nested-ancestry routing and aggregation.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the CPU-baseline leg
+of the benchmark may import this module. It is a plain, slow, single-threaded
+numpy definition of what the GPU path computes, and it shares no code with it.
+
+Model (paper, Section 4.2 "Nested Ancestry" and Section 4.3 "Routing with
+Ancestry"): every fragment carries a stack of ancestry tags, one per level of
+pmap nesting. Level 1 is the request, level ``d`` the fragment itself. A pmap
+entry pushes a tag (the element's index in its parent's stream); a pmap exit pops
+one and aggregates the outputs generated under the same parent. All elements that
+share the same tags are routed to the same instance (Section 4.3, like ECMP but on
+tags). A stream that is parallelised must be put back in its original order for
+sequential consumers (Section 3.2, pmap; Section 4.1). The size of a generated
+stream is unknown until its end (Section 3.1), so every node declares its child
+count and a group is complete only when its whole subtree has arrived.
+
+Readings where the paper is silent (each is listed in the design notes):
+
+* Keys: tags are packed most-significant level first into one uint64, ``bits[l-1]``
+  bits for level ``l``; numeric key order is then the lexicographic path order,
+  the original stream order.
+* Routing hash: ``dest = ((mix64(prefix) >> 32) * D) >> 32`` where ``mix64`` is the
+  SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014) and the range
+  reduction is Lemire's multiply-shift (2019).
+* ``perm`` lists input indices ordered by (dest, key). Groups, pending groups and
+  mask nodes at a level ``L >= Lr`` are ordered by (dest, key); mask nodes above the
+  route level (``L < Lr``) span destinations and are ordered by key.
+* Completion is the recursive definition: a leaf is complete on arrival; a node
+  at level ``l`` is complete when the number of its complete children equals its
+  declared child count ``fan[l]``.
+* MEAN pools all leaves of a group (flat mean), accumulated in float64 and
+  rounded once to float32. CONCAT lists the payloads of a group's leaves in key
+  order. FIRST is the payload of the group's first leaf in key order.
+* Error priority in a batch: layout, then fan-out, then duplicate, then capacity.
+  In a stream: layout, late, fan-out, duplicate, capacity.
+
+Parity is pinned against brute force, closed forms and textbook routines in
+``tests/test_oracle_*.py``.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+OK, E_ARG, E_LAYOUT, E_DUPLICATE, E_FANOUT, E_LATE, E_CAPACITY = 0, 1, 2, 3, 4, 5, 6
+CONCAT, MEAN = "concat", "mean"
+
+U64 = np.uint64
+
+
+class OracleError(Exception):
+    def __init__(self, code: int, what: str = ""):
+        super().__init__(f"code {code}: {what}")
+        self.code = code
+
+
+# ---------------------------------------------------------------------------
+# keys (nested ancestry tags packed into one integer)
+# ---------------------------------------------------------------------------
+
+def shift_below(bits: Sequence[int], level: int) -> int:
+    """Number of key bits that belong to levels deeper than ``level`` (1-based)."""
+    return int(sum(bits[level:]))
+
+
+def prefix(keys: np.ndarray, bits: Sequence[int], level: int) -> np.ndarray:
+    """The tags of levels 1..level, as an integer (key with deeper levels dropped)."""
+    return keys >> U64(shift_below(bits, level))
+
+
+def tag(keys: np.ndarray, bits: Sequence[int], level: int) -> np.ndarray:
+    """The level-``level`` tag of each key."""
+    return prefix(keys, bits, level) & U64((1 << bits[level - 1]) - 1)
+
+
+def check_layout(bits: Sequence[int]):
+    if not (2 <= len(bits) <= 16) or any(b < 1 for b in bits) or sum(bits) > 63:
+        raise OracleError(E_ARG, "layout")
+
+
+def pack_keys(path: np.ndarray, bits: Sequence[int]) -> np.ndarray:
+    """Pack int32 tags ``path[l-1][i]`` into uint64 keys, level 1 most significant."""
+    check_layout(bits)
+    path = np.asarray(path)
+    d = len(bits)
+    if path.ndim != 2 or path.shape[0] != d:
+        raise OracleError(E_ARG, "path shape")
+    keys = np.zeros(path.shape[1], dtype=U64)
+    for level in range(1, d + 1):
+        t = path[level - 1].astype(np.int64)
+        if t.size and (t.min() < 0 or t.max() >= (1 << bits[level - 1])):
+            raise OracleError(E_LAYOUT, f"tag at level {level} does not fit")
+        keys |= t.astype(U64) << U64(shift_below(bits, level))
+    return keys
+
+
+# ---------------------------------------------------------------------------
+# routing (Section 4.3)
+# ---------------------------------------------------------------------------
+
+def mix64(x: np.ndarray) -> np.ndarray:
+    """SplitMix64 output function: two xor-shift-multiply rounds and a final xor-shift."""
+    with np.errstate(over="ignore"):
+        z = np.asarray(x, dtype=U64).copy()
+        z = (z ^ (z >> U64(30))) * U64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> U64(27))) * U64(0x94D049BB133111EB)
+        return z ^ (z >> U64(31))
+
+
+def dest_of(prefixes: np.ndarray, num_dest: int) -> np.ndarray:
+    """Destination of a tag prefix: hash, then multiply-shift range reduction."""
+    h = mix64(prefixes) >> U64(32)
+    with np.errstate(over="ignore"):
+        return ((h * U64(num_dest)) >> U64(32)).astype(np.int32)
+
+
+def route_dest(keys: np.ndarray, bits: Sequence[int], route_level: int, num_dest: int):
+    if route_level == 0:
+        return np.zeros(len(keys), dtype=np.int32)
+    return dest_of(prefix(keys, bits, route_level), num_dest)
+
+
+def _check_keys_fit(keys: np.ndarray, bits: Sequence[int]):
+    if len(keys) and int(keys.max()) >> int(sum(bits)) != 0:
+        raise OracleError(E_LAYOUT, "key wider than the layout")
+
+
+@dataclass
+class Route:
+    perm: np.ndarray          # int32 [n], input indices in (dest, key) order
+    dest_offsets: np.ndarray  # int64 [D+1]
+    dest: np.ndarray          # int32 [n], input order
+
+
+def route(keys: np.ndarray, bits: Sequence[int], route_level: int, num_dest: int) -> Route:
+    """Hash-partition fragments by their level-``route_level`` prefix, then order
+    each destination's fragments by key (the original stream order)."""
+    check_layout(bits)
+    keys = np.asarray(keys, dtype=U64)
+    if not (1 <= route_level <= len(bits)) or num_dest < 1:
+        raise OracleError(E_ARG, "route level / destinations")
+    _check_keys_fit(keys, bits)
+    if len(np.unique(keys)) != len(keys):
+        raise OracleError(E_DUPLICATE, "same key twice")
+    dest = route_dest(keys, bits, route_level, num_dest)
+    perm = np.lexsort((keys, dest)).astype(np.int32)
+    counts = np.bincount(dest, minlength=num_dest).astype(np.int64)
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+    return Route(perm, offs, dest)
+
+
+# ---------------------------------------------------------------------------
+# completion (Section 3.1 end-of-output; pmap exit in Section 4.2)
+# ---------------------------------------------------------------------------
+
+def node_fans(keys: np.ndarray, fan: np.ndarray, bits: Sequence[int], level: int):
+    """Distinct level-``level`` nodes among the keys and the child count each declares.
+
+    Raises FANOUT when the carriers of one node disagree."""
+    p = prefix(keys, bits, level)
+    nodes, inv = np.unique(p, return_inverse=True)
+    f = fan[level - 1].astype(np.int64)
+    lo = np.full(len(nodes), np.iinfo(np.int64).max)
+    hi = np.full(len(nodes), np.iinfo(np.int64).min)
+    np.minimum.at(lo, inv, f)
+    np.maximum.at(hi, inv, f)
+    if (lo != hi).any():
+        raise OracleError(E_FANOUT, f"carriers disagree at level {level}")
+    return nodes, lo
+
+
+def check_fanout(keys, fan, bits, lo_level: int):
+    """Declared child counts of levels lo_level..d-1: at least 1, larger than every
+    child index under the node, and identical on every carrier."""
+    d = len(bits)
+    for level in range(lo_level, d):
+        f = fan[level - 1].astype(np.int64)
+        if f.size and f.min() < 1:
+            raise OracleError(E_FANOUT, f"child count < 1 at level {level}")
+        if f.size and (tag(keys, bits, level + 1).astype(np.int64) >= f).any():
+            raise OracleError(E_FANOUT, f"child index >= child count at level {level}")
+        node_fans(keys, fan, bits, level)
+
+
+def completion(keys, fan, bits, lo_level: int) -> Dict[int, tuple]:
+    """For each level from d-1 down to ``lo_level``: (nodes, complete flags).
+
+    A leaf is complete; a node is complete when its complete children number
+    exactly its declared child count."""
+    d = len(bits)
+    out = {}
+    child_nodes = np.unique(keys)
+    child_complete = np.ones(len(child_nodes), dtype=bool)
+    for level in range(d - 1, lo_level - 1, -1):
+        nodes, declared = node_fans(keys, fan, bits, level)
+        parent_of_child = child_nodes >> U64(bits[level])
+        idx = np.searchsorted(nodes, parent_of_child)
+        ncomplete = np.bincount(idx, weights=child_complete.astype(np.float64),
+                                minlength=len(nodes)).astype(np.int64)
+        complete = ncomplete == declared
+        out[level] = (nodes, complete)
+        child_nodes, child_complete = nodes, complete
+    return out
+
+
+# ---------------------------------------------------------------------------
+# aggregation at pmap exit (Section 3.3 aggregate operator, Section 4.3)
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Groups:
+    key: np.ndarray                  # uint64 [G] emitted (complete) groups
+    dest: np.ndarray                 # int32 [G]
+    count: np.ndarray                # int64 [G] leaves per group
+    first_i32: Optional[np.ndarray]  # int32 [G]
+    fan_up: np.ndarray               # int32 [La-1][G]
+    tok_off: Optional[np.ndarray]    # int64 [G+1]   (concat)
+    tok: Optional[np.ndarray]        # int32 [sum]   (concat)
+    mean: Optional[np.ndarray]       # float32 [G][dim] (mean)
+    mask_key: Optional[np.ndarray]   # uint64 [M]
+    mask: Optional[np.ndarray]       # uint8 [M]
+    pend_key: np.ndarray             # uint64 [P] incomplete groups
+    pend_count: np.ndarray           # int64 [P]
+
+
+def _order_by_dest_key(keys_at_level: np.ndarray, dests: np.ndarray) -> np.ndarray:
+    return np.lexsort((keys_at_level, dests))
+
+
+def _group_payloads(members: List[np.ndarray], op: str, dim: int, payload_i32, payload_f32):
+    """Payload of each group over its leaves (``members[g]``, input indices in key order)."""
+    tok_off = tok = mean = None
+    if op == CONCAT:
+        tok_off = np.concatenate([[0], np.cumsum([len(m) for m in members])]).astype(np.int64)
+        tok = (np.concatenate([payload_i32[m] for m in members]) if members
+               else np.zeros(0)).astype(np.int32)
+    else:
+        mean = np.zeros((len(members), dim), dtype=np.float32)
+        budget = max(1, (1 << 24) // max(dim, 1))          # rows per float64 batch
+        gi = 0
+        while gi < len(members):
+            gj, rows = gi, 0
+            while gj < len(members) and (gj == gi or rows + len(members[gj]) <= budget):
+                rows += len(members[gj])
+                gj += 1
+            part = members[gi:gj]
+            x = np.asarray(payload_f32[np.concatenate(part)], dtype=np.float64)
+            starts = np.concatenate([[0], np.cumsum([len(m) for m in part])[:-1]]).astype(np.int64)
+            sums = np.add.reduceat(x, starts, axis=0)
+            cnt = np.array([len(m) for m in part], dtype=np.float64)
+            mean[gi:gj] = (sums / cnt[:, None]).astype(np.float32)
+            gi = gj
+    return tok_off, tok, mean
+
+
+def aggregate(keys, fan, bits, agg_level: int, op: str, dim: int = 1, mask_level: int = 0,
+              route_level: int = 0, num_dest: int = 1, payload_i32=None, payload_f32=None,
+              cap_groups: Optional[int] = None, cap_tokens: Optional[int] = None,
+              cap_mask: Optional[int] = None):
+    """Route a batch and aggregate it at ``agg_level``.
+
+    Returns ``(Route, Groups)``. Raises ``OracleError`` with the status code the
+    GPU path must report."""
+    check_layout(bits)
+    d = len(bits)
+    keys = np.asarray(keys, dtype=U64)
+    n = len(keys)
+    La, Lm, Lr = agg_level, mask_level, route_level
+    if not (1 <= La <= d - 1) or not (Lm == 0 or 1 <= Lm <= d - 1):
+        raise OracleError(E_ARG, "levels")
+    if not (0 <= Lr <= La) or num_dest < 1 or (Lr == 0 and num_dest != 1):
+        raise OracleError(E_ARG, "route level must not exceed the aggregation level")
+    if op not in (CONCAT, MEAN) or (op == MEAN and (payload_f32 is None or dim < 1)):
+        raise OracleError(E_ARG, "op")
+    if op == CONCAT and payload_i32 is None:
+        raise OracleError(E_ARG, "concat needs int32 payload")
+    fan = np.asarray(fan)
+    lo = min(La, Lm) if Lm else La
+    _check_keys_fit(keys, bits)
+    check_fanout(keys, fan, bits, lo)
+    if len(np.unique(keys)) != n:
+        raise OracleError(E_DUPLICATE, "same key twice")
+
+    dest = route_dest(keys, bits, Lr, num_dest)
+    perm = np.lexsort((keys, dest)).astype(np.int32)
+    offs = np.concatenate([[0], np.cumsum(np.bincount(dest, minlength=num_dest))]).astype(np.int64)
+    rt = Route(perm, offs, dest)
+
+    comp = completion(keys, fan, bits, lo)
+    gnodes, gcomplete = comp[La]                       # ascending group keys
+    # leaves of each group, in key order
+    by_key = np.argsort(keys, kind="stable")
+    gk_sorted = prefix(keys, bits, La)[by_key]
+    gstart = np.searchsorted(gk_sorted, gnodes, side="left")
+    gend = np.searchsorted(gk_sorted, gnodes, side="right")
+    gdest = route_dest(gnodes << U64(shift_below(bits, La)), bits, Lr, num_dest)
+    order = _order_by_dest_key(gnodes, gdest)
+    emit = [int(g) for g in order if gcomplete[g]]
+    pend = [int(g) for g in order if not gcomplete[g]]
+    members = [by_key[gstart[g]:gend[g]] for g in emit]
+    first = np.array([m[0] for m in members], dtype=np.int64)
+    fan_up = (np.stack([fan[l - 1][first] for l in range(1, La)]).astype(np.int32)
+              if La > 1 else np.zeros((0, len(emit)), np.int32))
+    first_i32 = payload_i32[first].astype(np.int32) if payload_i32 is not None else None
+    tok_off, tok, mean = _group_payloads(members, op, dim, payload_i32, payload_f32)
+    mask_key = mask = None
+    if Lm:
+        mnodes, mcomplete = comp[Lm]
+        if Lm >= Lr:
+            md = route_dest(mnodes << U64(shift_below(bits, Lm)), bits, Lr, num_dest)
+            o = _order_by_dest_key(mnodes, md)
+        else:
+            o = np.argsort(mnodes, kind="stable")
+        mask_key, mask = mnodes[o], mcomplete[o].astype(np.uint8)
+    gcount = (gend - gstart).astype(np.int64)
+    g = Groups(gnodes[emit], gdest[emit], gcount[emit], first_i32, fan_up, tok_off, tok, mean,
+               mask_key, mask, gnodes[pend], gcount[pend])
+    need = (len(emit), 0 if tok is None else len(tok), 0 if mask is None else len(mask), len(pend))
+    if ((cap_groups is not None and (need[0] > cap_groups or need[3] > cap_groups))
+            or (cap_tokens is not None and need[1] > cap_tokens)
+            or (cap_mask is not None and need[2] > cap_mask)):
+        err = OracleError(E_CAPACITY, "output capacity")
+        err.need = need
+        raise err
+    return rt, g
+
+
+# ---------------------------------------------------------------------------
+# streams: partial groups carried between steps
+# ---------------------------------------------------------------------------
+
+@dataclass
+class StepResult:
+    route: Route
+    groups: Groups       # emitted this step (mask and pending unused)
+
+
+class Stream:
+    """Feed a stream in steps. Each step is routed on its own; leaves of groups that
+    are not yet complete are carried; a group is emitted once, in the step that
+    completes it, with its payload computed over all of its leaves in key order."""
+
+    def __init__(self, bits, route_level: int, num_dest: int, agg_level: int, op: str,
+                 dim: int = 1):
+        check_layout(bits)
+        d = len(bits)
+        if not (1 <= agg_level <= d - 1) or not (1 <= route_level <= agg_level) or num_dest < 1:
+            raise OracleError(E_ARG, "levels")
+        self.bits, self.Lr, self.D, self.La, self.op, self.dim = tuple(bits), route_level, num_dest, agg_level, op, dim
+        self.d = d
+        self.keys = np.zeros(0, U64)                           # arrived leaves of live groups
+        self.fan = np.zeros((d - 1, 0), np.int32)
+        self.p32 = np.zeros(0, np.int32)
+        self.pf = np.zeros((0, dim), np.float32) if op == MEAN else None
+        self.emitted = set()
+        self.error = OK
+
+    def step(self, keys, fan, payload_i32=None, payload_f32=None) -> StepResult:
+        if self.error:
+            raise OracleError(self.error, "stream poisoned")
+        try:
+            return self._step(keys, fan, payload_i32, payload_f32)
+        except OracleError as e:
+            if e.code != E_ARG:
+                self.error = e.code
+            raise
+
+    def _step(self, keys, fan, payload_i32, payload_f32) -> StepResult:
+        bits, La = self.bits, self.La
+        keys = np.asarray(keys, dtype=U64)
+        fan = np.asarray(fan).astype(np.int32)
+        n = len(keys)
+        if payload_i32 is None:
+            payload_i32 = np.zeros(n, np.int32)
+        _check_keys_fit(keys, bits)
+        gk = prefix(keys, bits, La)
+        if any(int(k) in self.emitted for k in np.unique(gk)):
+            raise OracleError(E_LATE, "fragment of an emitted group")
+        all_keys = np.concatenate([self.keys, keys])
+        all_fan = np.concatenate([self.fan, fan], axis=1)
+        check_fanout(all_keys, all_fan, bits, La)
+        if len(np.unique(all_keys)) != len(all_keys):
+            raise OracleError(E_DUPLICATE, "same key twice")
+        rt = route(keys, bits, self.Lr, self.D)
+        all_p32 = np.concatenate([self.p32, np.asarray(payload_i32, np.int32)])
+        all_pf = None
+        if self.op == MEAN:
+            all_pf = np.concatenate([self.pf, np.asarray(payload_f32, np.float32).reshape(n, self.dim)])
+        # completion of the groups this step touched, over all their arrived leaves
+        touched = np.unique(gk)
+        live_gk = prefix(all_keys, bits, La)
+        sel = np.isin(live_gk, touched)
+        comp = completion(all_keys[sel], all_fan[:, sel], bits, La)
+        gnodes, gcomplete = comp[La]
+        done = gnodes[gcomplete]
+        in_done = np.isin(live_gk, done)
+        if len(done):
+            _, g = aggregate(all_keys[in_done], all_fan[:, in_done], bits, La, self.op, self.dim, 0,
+                             self.Lr, self.D, all_p32[in_done],
+                             None if all_pf is None else all_pf[in_done])
+        else:
+            g = _empty_groups(La, self.op, self.dim)
+        for k in done:
+            self.emitted.add(int(k))
+        keep = ~in_done
+        self.keys, self.fan, self.p32 = all_keys[keep], all_fan[:, keep], all_p32[keep]
+        if self.op == MEAN:
+            self.pf = all_pf[keep]
+        return StepResult(rt, g)
+
+    def pending(self):
+        """Groups with arrived leaves that never completed: (keys, counts), (dest, key) order."""
+        gk = prefix(self.keys, self.bits, self.La)
+        nodes, cnt = np.unique(gk, return_counts=True)
+        dest = route_dest(nodes << U64(shift_below(self.bits, self.La)), self.bits, self.Lr, self.D)
+        o = _order_by_dest_key(nodes, dest)
+        return nodes[o], cnt[o].astype(np.int64)
+
+
+def _empty_groups(La, op, dim):
+    z64 = np.zeros(0, U64)
+    return Groups(z64, np.zeros(0, np.int32), np.zeros(0, np.int64), np.zeros(0, np.int32),
+                  np.zeros((La - 1, 0), np.int32),
+                  np.zeros(1, np.int64) if op == CONCAT else None,
+                  np.zeros(0, np.int32) if op == CONCAT else None,
+                  np.zeros((0, dim), np.float32) if op == MEAN else None,
+                  None, None, z64, np.zeros(0, np.int64))

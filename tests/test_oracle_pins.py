@@ -1,0 +1,440 @@
+"""Pins of the CPU oracle against things other than itself: published hash outputs,
+closed forms, textbook routines and a brute-force model on tiny trees."""
+import functools
+import itertools
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import alto_oracle as O
+from paper_2403_04311_amd import workloads as W
+from tests import brute
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- hash
+
+def test_mix64_matches_published_splitmix64_outputs():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "splitmix64_seed0.txt"))
+            if l.strip() and not l.startswith("#")]
+    states = np.array([int(r[1], 16) for r in rows], dtype=np.uint64)
+    want = [int(r[2], 16) for r in rows]
+    got = [int(v) for v in O.mix64(states)]
+    assert got == want
+
+
+def test_dest_power_of_two_is_top_bits_of_hash():
+    rng = np.random.default_rng(0)
+    p = rng.integers(0, 2**62, size=10000, dtype=np.int64).astype(np.uint64)
+    h = O.mix64(p)
+    for k in range(0, 12):
+        d = O.dest_of(p, 1 << k)
+        if k == 0:
+            assert (d == 0).all()
+        else:
+            assert np.array_equal(d.astype(np.uint64), h >> np.uint64(64 - k))
+
+
+@pytest.mark.parametrize("D", [3, 7, 64, 256, 1000])
+def test_dest_range_and_balance(D):
+    p = np.arange(200000, dtype=np.uint64)
+    d = O.dest_of(p, D)
+    assert d.min() >= 0 and d.max() < D
+    c = np.bincount(d, minlength=D)
+    exp = len(p) / D
+    chi2 = ((c - exp) ** 2 / exp).sum()
+    assert chi2 < D + 6 * np.sqrt(2 * D)   # loose: a biased reduction fails by far
+
+
+def test_dest_lemire_bound_small_cases():
+    # Lemire's reduction maps the 32-bit hash x to floor(x * D / 2^32): check against
+    # exact rational arithmetic.
+    rng = np.random.default_rng(1)
+    p = rng.integers(0, 2**40, size=500).astype(np.uint64)
+    x = [int(v) >> 32 for v in O.mix64(p)]
+    for D in (5, 12, 255):
+        got = O.dest_of(p, D)
+        want = [int(Fraction(xi * D, 2**32)) for xi in x]
+        assert list(got) == want
+
+
+# ---------------------------------------------------------------- keys
+
+def test_pack_literal():
+    keys = O.pack_keys(np.array([[1, 0], [5, 7]]), (2, 3))
+    assert list(keys) == [0b01101, 0b00111]
+
+
+def test_pack_preserves_lexicographic_path_order():
+    path, fan = W.random_tree(3, 4, 12, (3, 4, 5), (31, 2, 3, 3))
+    [path], _ = W.permute([path], 4)
+    keys = O.pack_keys(path, (31, 2, 3, 3))
+    tuples = brute.leaves_of(path)
+    assert list(np.argsort(keys, kind="stable")) == sorted(range(len(tuples)), key=lambda i: tuples[i])
+    for level in range(1, 5):
+        assert list(O.tag(keys, (31, 2, 3, 3), level)) == [t[level - 1] for t in tuples]
+
+
+def test_pack_rejects_tags_that_do_not_fit():
+    with pytest.raises(O.OracleError) as e:
+        O.pack_keys(np.array([[0], [8]]), (2, 3))
+    assert e.value.code == O.E_LAYOUT
+    with pytest.raises(O.OracleError) as e:
+        O.pack_keys(np.array([[-1], [0]]), (2, 3))
+    assert e.value.code == O.E_LAYOUT
+    with pytest.raises(O.OracleError) as e:
+        O.pack_keys(np.array([[0], [0]]), (40, 24))
+    assert e.value.code == O.E_ARG
+
+
+# ---------------------------------------------------------------- route
+
+@pytest.mark.parametrize("D,Lr", [(1, 1), (3, 1), (8, 2), (256, 3), (5, 4)])
+def test_route_matches_brute_force_sort(D, Lr):
+    bits = (31, 2, 3, 4)
+    path, fan = W.random_tree(10 + D, 4, 20, (4, 8, 16), bits)
+    [path], _ = W.permute([path], D)
+    keys = O.pack_keys(path, bits)
+    r = O.route(keys, bits, Lr, D)
+    tuples = brute.leaves_of(path)
+
+    @functools.lru_cache(maxsize=None)
+    def dfn(t):
+        v = 0
+        for level, tg in enumerate(t):
+            v = (v << bits[level]) | tg
+        return int(O.dest_of(np.array([v], np.uint64), D)[0])
+
+    want = sorted(range(len(tuples)), key=lambda i: (dfn(tuples[i][:Lr]), tuples[i]))
+    assert list(r.perm) == want
+    assert list(r.dest) == [dfn(t[:Lr]) for t in tuples]
+    assert list(r.dest_offsets) == [0] + list(np.cumsum([sum(1 for t in tuples if dfn(t[:Lr]) == d)
+                                                         for d in range(D)]))
+
+
+def test_route_invariants_and_duplicate():
+    keys = np.array([5, 9, 1, 7], dtype=np.uint64)
+    r = O.route(keys, (4, 4), 2, 3)
+    assert sorted(r.perm) == [0, 1, 2, 3]
+    with pytest.raises(O.OracleError) as e:
+        O.route(np.array([5, 9, 5], np.uint64), (4, 4), 2, 3)
+    assert e.value.code == O.E_DUPLICATE
+    with pytest.raises(O.OracleError) as e:
+        O.route(np.array([5, 300], np.uint64), (4, 4), 2, 3)
+    assert e.value.code == O.E_LAYOUT
+
+
+# ---------------------------------------------------------------- aggregate vs brute force
+
+def _dest_fn(bits, D):
+    def f(prefix_tuple):
+        v = 0
+        for level, tg in enumerate(prefix_tuple):
+            v = (v << bits[level]) | tg
+        return int(O.dest_of(np.array([v], np.uint64), D)[0])
+    return f
+
+
+def _tuple_of(k, bits, level):
+    """Tag tuple of a level-``level`` prefix value (inverse of _key_of)."""
+    out = []
+    for l in range(level, 0, -1):
+        out.append(k & ((1 << bits[l - 1]) - 1))
+        k >>= bits[l - 1]
+    return tuple(reversed(out))
+
+
+def _key_of(t, bits):
+    v = 0
+    for level, tg in enumerate(t):
+        v = (v << bits[level]) | tg
+    return v
+
+
+CASES = [
+    # depth, bits, max_fan per level, La, Lm, Lr, D, drop
+    (2, (8, 4), (5,), 1, 0, 1, 3, 0.0),
+    (3, (10, 3, 3), (4, 5), 2, 1, 1, 4, 0.2),
+    (4, (31, 2, 3, 4), (4, 8, 16), 3, 0, 1, 8, 0.0),
+    (4, (31, 2, 3, 4), (3, 3, 3), 2, 3, 2, 5, 0.15),
+    (5, (6, 3, 2, 3, 5), (3, 3, 3, 6), 4, 2, 4, 16, 0.1),
+    (5, (6, 3, 2, 3, 5), (3, 2, 3, 4), 3, 1, 2, 7, 0.05),
+    (4, (5, 3, 3, 3), (3, 3, 4), 1, 2, 0, 1, 0.1),
+    (6, (3, 3, 3, 3, 3, 4), (2, 3, 2, 3, 5), 4, 2, 4, 256, 0.08),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+@pytest.mark.parametrize("op", ["concat", "mean"])
+def test_aggregate_matches_brute_force(case, op):
+    depth, bits, mf, La, Lm, Lr, D, drop = CASES[case]
+    for rep in range(3):
+        seed = 1000 * case + rep
+        path, fan = W.random_tree(seed, depth, 3 + rep, mf, bits)
+        true_leaves = brute.leaves_of(path)
+        if drop:
+            path, fan, _ = W.drop_leaves(path, fan, drop, seed + 1)
+        rng = np.random.default_rng(seed + 2)
+        n = path.shape[1]
+        p32 = rng.integers(-1000, 1000, size=n).astype(np.int32)
+        pf = (rng.integers(-64, 64, size=(n, 3)) / 16.0).astype(np.float32)   # dyadic: exact
+        (path, fan, p32, pf_t), _ = W.permute([path, fan, p32, pf.T], seed + 3)
+        pf = np.ascontiguousarray(pf_t.T)
+        keys = O.pack_keys(path, bits)
+        rt, g = O.aggregate(keys, fan, bits, La, op, 3, Lm, Lr, D, p32, pf if op == "mean" else None)
+        arrived = brute.leaves_of(path)
+        exp = brute.batch_expect(true_leaves, arrived, p32, pf if op == "mean" else None, La, Lm,
+                                 _dest_fn(bits, D), Lr)
+        assert list(rt.perm) == exp["perm"]
+        em = exp["emitted"]
+        assert [int(k) for k in g.key] == [_key_of(r["key"], bits) for r in em]
+        assert list(g.dest) == [r["dest"] for r in em]
+        assert list(g.count) == [r["count"] for r in em]
+        assert list(g.first_i32) == [r["first"] for r in em]
+        tf = brute.true_fans(path, fan)
+        for level in range(1, La):
+            assert list(g.fan_up[level - 1]) == [tf[r["key"][:level]] for r in em]
+        assert [int(k) for k in g.pend_key] == [_key_of(r["key"], bits) for r in exp["pending"]]
+        assert list(g.pend_count) == [r["count"] for r in exp["pending"]]
+        if op == "concat":
+            assert list(g.tok) == [t for r in em for t in r["tok"]]
+            assert list(g.tok_off) == [0] + list(np.cumsum([r["count"] for r in em]))
+        else:
+            want = np.array([[float(v) for v in r["mean"]] for r in em], np.float64).reshape(-1, 3)
+            assert np.array_equal(g.mean, want.astype(np.float32))
+        if Lm:
+            assert [int(k) for k in g.mask_key] == [_key_of(m, bits) for m, _ in exp["mask"]]
+            assert list(g.mask) == [int(c) for _, c in exp["mask"]]
+
+
+def test_single_batch_concat_reproduces_depth_first_payload_order():
+    # Closed form: with every leaf present, all groups are complete, and the groups'
+    # token lists in key order concatenate to the pre-shuffle (depth-first) payloads.
+    bits = (31, 2, 3, 4)
+    path, fan = W.random_tree(77, 4, 40, (4, 8, 16), bits, dense_roots=True)
+    dfs_tok = np.arange(path.shape[1], dtype=np.int32) * 3 + 1
+    (sp, sf, st), _ = W.permute([path, fan, dfs_tok], 78)
+    keys = O.pack_keys(sp, bits)
+    _, g = O.aggregate(keys, sf, bits, 3, "concat", 1, 0, 1, 8, st)
+    assert len(g.pend_key) == 0
+    o = np.argsort(g.key)
+    toks = np.concatenate([g.tok[g.tok_off[i]:g.tok_off[i + 1]] for i in o])
+    assert np.array_equal(toks, dfs_tok)
+
+
+def test_mean_is_textbook_group_mean():
+    bits = (31, 3, 2, 3, 8)
+    path, fan = W.random_tree(5, 5, 6, (8, 3, 5, 20), bits)
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal((path.shape[1], 16)).astype(np.float32)
+    (sp, sf, xt), _ = W.permute([path, fan, x.T], 7)
+    x = np.ascontiguousarray(xt.T)
+    keys = O.pack_keys(sp, bits)
+    _, g = O.aggregate(keys, sf, bits, 4, "mean", 16, 0, 2, 32, None, x)
+    gk = O.prefix(keys, bits, 4)
+    for i, k in enumerate(g.key):
+        rows = x[gk == k].astype(np.float64)
+        assert np.allclose(g.mean[i], rows.mean(axis=0).astype(np.float32), rtol=0, atol=1e-7)
+
+
+def test_arrival_permutation_invariance():
+    bits = (6, 3, 2, 3, 5)
+    path, fan = W.random_tree(9, 5, 4, (3, 3, 3, 6), bits)
+    path, fan, _ = W.drop_leaves(path, fan, 0.1, 10)
+    p32 = np.arange(path.shape[1], dtype=np.int32)
+    ref = None
+    for s in range(5):
+        (sp, sf, st), _ = W.permute([path, fan, p32], 100 + s)
+        keys = O.pack_keys(sp, bits)
+        rt, g = O.aggregate(keys, sf, bits, 3, "concat", 1, 2, 2, 7, st)
+        out = (list(g.key), list(g.tok), list(g.mask_key), list(g.mask), list(keys[rt.perm]))
+        if ref is None:
+            ref = out
+        assert out == ref
+
+
+# ---------------------------------------------------------------- error paths
+
+def _small():
+    bits = (4, 3, 3)
+    path, fan = W.random_tree(21, 3, 3, (4, 5), bits)
+    return bits, path.copy(), fan.copy()
+
+
+def test_fanout_errors():
+    bits, path, fan = _small()
+    keys = O.pack_keys(path, bits)
+    O.aggregate(keys, fan, bits, 2, "concat", payload_i32=np.zeros(len(keys), np.int32))
+    f2 = fan.copy()
+    f2[1, 0] += 1                                   # one carrier disagrees
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(keys, f2, bits, 2, "concat", payload_i32=np.zeros(len(keys), np.int32))
+    assert e.value.code == O.E_FANOUT
+    f3 = fan.copy()
+    f3[1, :] = np.maximum(f3[1, :] - 1, 0)          # child index >= declared count
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(keys, f3, bits, 2, "concat", payload_i32=np.zeros(len(keys), np.int32))
+    assert e.value.code == O.E_FANOUT
+    # levels above the aggregation level are not read
+    f4 = fan.copy()
+    f4[0, 0] = -5
+    O.aggregate(keys, f4, bits, 2, "concat", payload_i32=np.zeros(len(keys), np.int32))
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(keys, f4, bits, 2, "concat", 1, 1, payload_i32=np.zeros(len(keys), np.int32))
+    assert e.value.code == O.E_FANOUT
+
+
+def test_error_priority():
+    bits, path, fan = _small()
+    keys = O.pack_keys(path, bits)
+    dup = np.concatenate([keys, keys[:1]])
+    fdup = np.concatenate([fan, fan[:, :1]], axis=1)
+    z = np.zeros(len(dup), np.int32)
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(dup, fdup, bits, 2, "concat", payload_i32=z)
+    assert e.value.code == O.E_DUPLICATE
+    fbad = fdup.copy()
+    fbad[1, 0] += 3
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(dup, fbad, bits, 2, "concat", payload_i32=z)
+    assert e.value.code == O.E_FANOUT
+    wide = dup.copy()
+    wide[1] = np.uint64(1 << 20)
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(wide, fbad, bits, 2, "concat", payload_i32=z)
+    assert e.value.code == O.E_LAYOUT
+
+
+def test_argument_errors():
+    bits, path, fan = _small()
+    keys = O.pack_keys(path, bits)
+    z = np.zeros(len(keys), np.int32)
+    for kw in [dict(agg_level=3), dict(agg_level=1, route_level=2, num_dest=4),
+               dict(agg_level=2, route_level=0, num_dest=4)]:
+        with pytest.raises(O.OracleError) as e:
+            O.aggregate(keys, fan, bits, op="concat", payload_i32=z, **kw)
+        assert e.value.code == O.E_ARG
+
+
+def test_capacity_reports_needs():
+    bits, path, fan = _small()
+    keys = O.pack_keys(path, bits)
+    z = np.zeros(len(keys), np.int32)
+    _, g = O.aggregate(keys, fan, bits, 2, "concat", payload_i32=z)
+    with pytest.raises(O.OracleError) as e:
+        O.aggregate(keys, fan, bits, 2, "concat", payload_i32=z, cap_tokens=len(keys) - 1)
+    assert e.value.code == O.E_CAPACITY and e.value.need[1] == len(keys)
+
+
+def test_empty_batch():
+    bits = (4, 3, 3)
+    keys = np.zeros(0, np.uint64)
+    rt, g = O.aggregate(keys, np.zeros((2, 0), np.int32), bits, 2, "concat", 1, 1, 1, 4,
+                        np.zeros(0, np.int32))
+    assert len(rt.perm) == 0 and list(rt.dest_offsets) == [0] * 5
+    assert len(g.key) == 0 and len(g.tok) == 0 and list(g.tok_off) == [0] and len(g.mask) == 0
+
+
+# ---------------------------------------------------------------- streams
+
+def _run_stream(bits, Lr, D, La, op, path, fan, p32, cuts):
+    s = O.Stream(bits, Lr, D, La, op, 1)
+    keys = O.pack_keys(path, bits)
+    out = []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        r = s.step(keys[a:b], fan[:, a:b], p32[a:b], None)
+        out.append(r)
+    return s, out
+
+
+def test_stream_brute_force_all_orders_and_cuts():
+    # Every arrival order of tiny trees (sampled above 6 leaves), cut into steps at
+    # random points: each group is emitted exactly once, in the step holding its
+    # last leaf, with the same tokens whatever the order; nothing stays pending.
+    bits = (4, 2, 2, 3)
+    La, Lr, D = 2, 1, 3
+    checked = 0
+    for seed in range(40):
+        roots = 1 + seed % 2
+        path, fan = W.random_tree(300 + seed, 4, roots, (2, 2, 2), bits)
+        n = path.shape[1]
+        if n > 8:
+            continue
+        true_leaves = brute.leaves_of(path)
+        p32 = np.arange(n, dtype=np.int32) + 100
+        batch = brute.batch_expect(true_leaves, true_leaves, p32, None, La, 0,
+                                   _dest_fn(bits, D), Lr)
+        tok_of = {r["key"]: r["tok"] for r in batch["emitted"]}
+        rng = np.random.default_rng(seed)
+        if n <= 6:
+            orders = [list(o) for o in itertools.permutations(range(n))]
+        else:
+            orders = [list(rng.permutation(n)) for _ in range(150)]
+        for oi, order in enumerate(orders):
+            ncut = 1 + oi % min(n, 4)
+            cuts = [0] + sorted(rng.choice(np.arange(1, n), size=ncut - 1, replace=False).tolist()) + [n]
+            sp, sf, st = path[:, order], fan[:, order], p32[order]
+            s, res = _run_stream(bits, Lr, D, La, "concat", sp, sf, st, cuts)
+            arrival = brute.leaves_of(sp)
+            step_of = np.searchsorted(cuts, np.arange(n), side="right") - 1
+            want = brute.stream_emission_steps(true_leaves, arrival, step_of, La)
+            seen = {}
+            for si, r in enumerate(res):
+                for j, k in enumerate(r.groups.key):
+                    gt = _tuple_of(int(k), bits, La)
+                    assert gt not in seen            # emitted exactly once
+                    seen[gt] = si
+                    toks = list(r.groups.tok[r.groups.tok_off[j]:r.groups.tok_off[j + 1]])
+                    assert toks == tok_of[gt]         # arrival-order invariant content
+            assert seen == want
+            assert len(s.pending()[0]) == 0
+            checked += 1
+    assert checked > 3000
+
+
+def test_stream_late_and_duplicate():
+    bits = (4, 3, 3)
+    path, fan = W.random_tree(31, 3, 2, (3, 4), bits)
+    keys = O.pack_keys(path, bits)
+    z = np.zeros(len(keys), np.int32)
+    s = O.Stream(bits, 1, 4, 2, "concat")
+    s.step(keys, fan, z)
+    with pytest.raises(O.OracleError) as e:
+        s.step(keys[:1], fan[:, :1], z[:1])
+    assert e.value.code == O.E_LATE
+    with pytest.raises(O.OracleError) as e:               # poisoned
+        s.step(keys[:0], fan[:, :0], z[:0])
+    assert e.value.code == O.E_LATE
+    # duplicate across steps of a group that is still open
+    keep = O.prefix(keys, bits, 2) == O.prefix(keys[:1], bits, 2)[0]
+    s = O.Stream(bits, 1, 4, 2, "concat")
+    if keep.sum() >= 2:
+        first = np.nonzero(keep)[0][:1]
+        s.step(keys[first], fan[:, first], z[first])
+        with pytest.raises(O.OracleError) as e:
+            s.step(keys[first], fan[:, first], z[first])
+        assert e.value.code == O.E_DUPLICATE
+
+
+def test_config3_emission_step_closed_form():
+    # Tokens of a generator arrive in order, so a sentence is emitted in the step of
+    # its last token: floor(arrival index of the last token / step).
+    w = W.config3(generators=16, sentences=8, step=256)
+    path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
+    keys = O.pack_keys(path, w.bits)
+    s = O.Stream(w.bits, w.route_level, w.num_dest, w.agg_level, "concat")
+    got = {}
+    for si, a in enumerate(range(0, w.n, w.step)):
+        b = min(a + w.step, w.n)
+        r = s.step(keys[a:b], fan[:, a:b], tok[a:b])
+        for k in r.groups.key:
+            got[int(k)] = si
+    gk = O.prefix(keys, w.bits, 2)
+    want = {}
+    for i, k in enumerate(gk):
+        want[int(k)] = i // w.step
+    assert got == want
+    assert len(s.pending()[0]) == 0
