@@ -1,0 +1,197 @@
+/*
+ * alto.h -- C ABI of libalto: batched routing and re-aggregation of fragments that
+ * carry nested ancestry, on AMD Instinct MI355X (gfx950).
+ *
+ * Model (paper, Sections 4.1-4.3). Every fragment carries a stack of ancestry
+ * tags, one per level of pmap nesting (Section 4.2): level 1 is the request, level
+ * d the fragment itself, and levels >= 2 hold the index of the element in its
+ * parent's stream. Fragments with the same tags go to the same instance, picked by
+ * hashing the tags, like ECMP (Section 4.3). A parallelised stream is put back in
+ * its original order before sequential consumers see it (Sections 3.2 and 4.1). A
+ * pmap exit pops a level and aggregates what the call produced (Section 4.3;
+ * the aggregate operator of Section 3.3). The extent of a generated stream is known
+ * only at its end (Section 3.1), so every node declares its child count, and a group
+ * is released only when its whole subtree has arrived.
+ *
+ * Conventions for every entry point:
+ *  - Array arguments are DEVICE pointers owned by the caller. The library never
+ *    allocates device memory; temporary memory comes from a caller workspace sized
+ *    by alto_workspace_bytes(). Struct arguments (alto_layout, alto_agg,
+ *    alto_groups) are HOST pointers to structs whose array members are device
+ *    pointers.
+ *  - Calls only enqueue work on the given stream and return without synchronising.
+ *  - The return value reports host-detectable problems only: ALTO_E_ARG for bad
+ *    arguments (nothing is enqueued), ALTO_E_HIP for a failed launch.
+ *  - Data-dependent problems are written to the device word *status, which the
+ *    caller sets to 0 beforehand and reads after its own synchronisation. When
+ *    several problems are present the one reported is, in decreasing priority:
+ *    LAYOUT, LATE, FANOUT, DUPLICATE, CAPACITY. After a data error the outputs are
+ *    undefined and a stream handle is poisoned; writes always stay inside the
+ *    buffers and capacities given.
+ *  - Level-major arrays: element (l, i) of a [levels][n] array lives at
+ *    [l * ld + i] with ld >= n, so that loads across fragments are coalesced.
+ *  - n < 2^31.
+ *
+ * Orders. perm lists input indices by (destination, key). Packed keys order
+ * fragments exactly as their tag tuples, i.e. in original stream order. Groups,
+ * pending groups and mask nodes at a level >= route_level lie within one
+ * destination and are listed by (destination, key); mask nodes above the route
+ * level span destinations and are listed by key.
+ */
+#ifndef ALTO_H
+#define ALTO_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ALTO_OK = 0,
+  ALTO_E_ARG = 1,        /* bad argument (host check; nothing enqueued) */
+  ALTO_E_LAYOUT = 2,     /* a tag >= 2^bits[level] or < 0, or a key wider than the layout */
+  ALTO_E_DUPLICATE = 3,  /* the same full key twice (within a batch, or across stream steps) */
+  ALTO_E_FANOUT = 4,     /* declared child count < 1, child index >= declared count,
+                            or two carriers of one node declaring different counts */
+  ALTO_E_LATE = 5,       /* stream: fragment of a group that was already emitted */
+  ALTO_E_CAPACITY = 6,   /* an output or state capacity is too small; the sizes
+                            needed are written to counts[] */
+  ALTO_E_HIP = 7         /* a HIP launch failed */
+} alto_status;
+
+/* Key layout: depth d in [2, 16] levels; bits[l-1] >= 1 bits for level l, level 1
+ * most significant; sum(bits) <= 63 so keys are also valid non-negative int64. */
+typedef struct {
+  int32_t depth;
+  uint8_t bits[16];
+} alto_layout;
+
+enum { ALTO_CONCAT_I32 = 0, ALTO_MEAN_F32 = 1 };
+
+/* Aggregation at a pmap exit: level = La in [1, d-1] (groups are the level-La
+ * nodes); op = ALTO_CONCAT_I32 (list the int32 payloads of a group's leaves in key
+ * order) or ALTO_MEAN_F32 (flat mean of the float32 rows of all leaves, float64
+ * accumulation, one rounding to float32); dim = row width for MEAN (1 for
+ * CONCAT); mask_level = Lm in [1, d-1], or 0 for no completion mask. */
+typedef struct {
+  int32_t level;
+  int32_t op;
+  int32_t dim;
+  int32_t mask_level;
+} alto_agg;
+
+/* Outputs of an aggregation. Any array pointer may be NULL to skip that output;
+ * counts must not be NULL. Capacities bound every write. */
+typedef struct {
+  int64_t cap_groups;   /* rows of key/dest/count/first_i32/fan_up/mean/pend_* */
+  int64_t cap_tokens;   /* entries of tok */
+  int64_t cap_mask;     /* entries of mask_key/mask */
+  uint64_t *key;        /* [cap_groups] emitted (complete) group keys: the level-La prefix
+                           (key >> bits below La) */
+  int32_t *dest;        /* [cap_groups] destination of each emitted group */
+  int64_t *count;       /* [cap_groups] leaves per emitted group */
+  int32_t *first_i32;   /* [cap_groups] int32 payload of the group's first leaf in key order */
+  int32_t *fan_up;      /* [(La-1) * cap_groups] declared child counts of levels 1..La-1 of
+                           the group's ancestors, level-major with ld = cap_groups
+                           (feeds a following aggregation stage) */
+  int64_t *tok_off;     /* CONCAT: [cap_groups + 1] offsets into tok */
+  int32_t *tok;         /* CONCAT: [cap_tokens] */
+  float *mean;          /* MEAN: [cap_groups][dim] */
+  uint64_t *mask_key;   /* [cap_mask] level-Lm nodes present in the batch */
+  uint8_t *mask;        /* [cap_mask] 1 = the node's whole subtree is present */
+  uint64_t *pend_key;   /* [cap_groups] incomplete level-La groups (not emitted) */
+  int64_t *pend_count;  /* [cap_groups] leaves present per pending group */
+  int64_t *counts;      /* device [4]: emitted groups, tokens, mask nodes, pending groups
+                           (always written, also on ALTO_E_CAPACITY) */
+} alto_groups;
+
+/* Workspace bytes needed by alto_pack_keys / alto_route / alto_aggregate for up to
+ * n_max fragments with this layout, destination count and aggregation (agg may be
+ * NULL for routing only). Returns 0 for invalid arguments. */
+size_t alto_workspace_bytes(const alto_layout *layout, int64_t n_max, int32_t num_dest,
+                            const alto_agg *agg);
+
+/* Key construction (Section 4.2: the tag stack of a fragment). Packs path (int32
+ * [depth][path_ld], level-major, tag of level l at row l-1) into keys[n]
+ * (uint64), level 1 in the most significant bits. A tag outside [0, 2^bits) sets
+ * ALTO_E_LAYOUT. */
+int alto_pack_keys(const int32_t *path, int64_t path_ld, int64_t n, const alto_layout *layout,
+                   uint64_t *keys, int32_t *status, hipStream_t stream);
+
+/* Routing by ancestry (Section 4.3) and order reconstitution (Sections 3.2, 4.1).
+ * dest[i] = ((mix64(keys[i] >> bits below route_level) >> 32) * num_dest) >> 32 with
+ * mix64 the SplitMix64 output function; route_level in [1, depth], num_dest in
+ * [1, 2^24]. perm[n] (int32): input indices by (dest, key). dest_offsets[num_dest+1]
+ * (int64): start of each destination's segment of perm; dest_offsets[num_dest] = n.
+ * dest (nullable): per input fragment. Errors: LAYOUT, DUPLICATE. */
+int alto_route(const uint64_t *keys, int64_t n, const alto_layout *layout, int32_t route_level,
+               int32_t num_dest, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
+               int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Routing plus aggregation of one batch at a pmap exit (Sections 3.3 and 4.3).
+ * fan: int32 [(depth-1)][fan_ld]; row l-1 holds each fragment's level-l ancestor's
+ * declared child count. Rows of levels min(La, Lm)..depth-1 are read (checked:
+ * >= 1, > the child index under it, equal on all carriers); rows 1..La-1 of the
+ * group's first leaf are copied to fan_up. payload_i32 [n] is needed for CONCAT
+ * and for first_i32; payload_f32 [n][dim] for MEAN. route_level = 0 sends every
+ * fragment to destination 0 (num_dest must be 1); otherwise route_level must be in
+ * [1, La] so that a group never spans destinations (a stateful consumer sees all
+ * elements of its stream, Section 4.1). perm/dest_offsets/dest are as in
+ * alto_route (perm and dest_offsets nullable here). A group is complete when every
+ * node of its subtree has as many complete children as it declares (leaves are
+ * complete on arrival); complete groups are emitted, the others listed as pending.
+ * Errors: LAYOUT, FANOUT, DUPLICATE, CAPACITY. */
+int alto_aggregate(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                   const int32_t *payload_i32, const float *payload_f32, int64_t n,
+                   const alto_layout *layout, const alto_agg *agg, int32_t route_level,
+                   int32_t num_dest, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
+                   alto_groups *out, int32_t *status, void *ws, size_t ws_bytes,
+                   hipStream_t stream);
+
+/* ---- streams: partial groups carried across steps (Section 3.1: outputs stream
+ * before their inputs are complete; Section 4.2: aggregation at pmap exit) ---- */
+
+typedef struct alto_stream alto_stream; /* opaque host handle; state memory is the caller's */
+
+/* Device state bytes for a stream that holds at most max_live_leaves arrived
+ * leaves of not-yet-emitted groups and sees at most max_groups distinct level-La
+ * groups over its lifetime (emitted groups are remembered to detect late
+ * fragments). Returns 0 for invalid arguments. */
+size_t alto_stream_state_bytes(const alto_layout *layout, const alto_agg *agg,
+                               int64_t max_live_leaves, int64_t max_groups);
+
+/* Creates a handle over caller-owned device memory `state` (state_bytes from
+ * alto_stream_state_bytes with the same limits) and clears it on `stream`.
+ * route_level must be in [1, La]; mask_level must be 0. */
+int alto_stream_create(const alto_layout *layout, int32_t route_level, int32_t num_dest,
+                       const alto_agg *agg, int64_t max_live_leaves, int64_t max_groups,
+                       void *state, size_t state_bytes, hipStream_t stream, alto_stream **out);
+
+/* One step: routes the step's n fragments on their own (perm, dest_offsets, dest as
+ * in alto_route, all nullable), merges them into the carried state, and emits the
+ * groups this step completes, each once, with its payload computed over all of its
+ * leaves in key order (count, key, dest, first_i32, fan_up, tok_off/tok or mean).
+ * Emitted groups per step are at most n; emitted tokens at most max_live_leaves.
+ * Workspace: alto_workspace_bytes(layout, n_max, num_dest, agg) with n_max >= n.
+ * Errors: LAYOUT, LATE, FANOUT, DUPLICATE, CAPACITY (state full or outputs too
+ * small). A data error poisons the handle: every later step reports it again. */
+int alto_stream_step(alto_stream *s, const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                     const int32_t *payload_i32, const float *payload_f32, int64_t n,
+                     int32_t *perm, int64_t *dest_offsets, int32_t *dest, alto_groups *emitted,
+                     int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Lists the groups that have arrived leaves but never completed, by (dest, key):
+ * pend_key, pend_count and counts[3] of `out`; other members are ignored. */
+int alto_stream_pending(alto_stream *s, alto_groups *out, int32_t *status, hipStream_t stream);
+
+/* Frees the host handle (the caller frees the state memory). */
+int alto_stream_destroy(alto_stream *s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ALTO_H */

@@ -1,0 +1,313 @@
+"""Python binding of libalto (argument marshalling only).
+
+Every step of routing and aggregation runs in the HIP kernels of ``libalto.so``;
+this module only converts torch tensors (device memory) and torch's current HIP
+stream into the C ABI of ``include/alto.h``, and allocates output tensors for
+convenience. It raises if the library is missing: there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libalto.so")
+
+OK, E_ARG, E_LAYOUT, E_DUPLICATE, E_FANOUT, E_LATE, E_CAPACITY, E_HIP = range(8)
+CONCAT_I32, MEAN_F32 = 0, 1
+STATUS_NAMES = {0: "OK", 1: "ARG", 2: "LAYOUT", 3: "DUPLICATE", 4: "FANOUT", 5: "LATE",
+                6: "CAPACITY", 7: "HIP"}
+
+EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggregate",
+           "alto_stream_state_bytes", "alto_stream_create", "alto_stream_step",
+           "alto_stream_pending", "alto_stream_destroy")
+
+
+class Layout(C.Structure):
+    _fields_ = [("depth", C.c_int32), ("bits", C.c_uint8 * 16)]
+
+
+class Agg(C.Structure):
+    _fields_ = [("level", C.c_int32), ("op", C.c_int32), ("dim", C.c_int32),
+                ("mask_level", C.c_int32)]
+
+
+class Groups(C.Structure):
+    _fields_ = [("cap_groups", C.c_int64), ("cap_tokens", C.c_int64), ("cap_mask", C.c_int64),
+                ("key", C.c_void_p), ("dest", C.c_void_p), ("count", C.c_void_p),
+                ("first_i32", C.c_void_p), ("fan_up", C.c_void_p), ("tok_off", C.c_void_p),
+                ("tok", C.c_void_p), ("mean", C.c_void_p), ("mask_key", C.c_void_p),
+                ("mask", C.c_void_p), ("pend_key", C.c_void_p), ("pend_count", C.c_void_p),
+                ("counts", C.c_void_p)]
+
+
+_lib = None
+
+
+class AltoError(RuntimeError):
+    def __init__(self, code, what=""):
+        super().__init__(f"alto error {STATUS_NAMES.get(code, code)}: {what}")
+        self.code = code
+
+
+def load():
+    """Loads libalto.so (built in-tree by __graft_entry__.build())."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    lib = C.CDLL(LIB_PATH)
+    vp, i64, i32 = C.c_void_p, C.c_int64, C.c_int32
+    lib.alto_workspace_bytes.restype = C.c_size_t
+    lib.alto_workspace_bytes.argtypes = [C.POINTER(Layout), i64, i32, C.POINTER(Agg)]
+    lib.alto_pack_keys.restype = C.c_int
+    lib.alto_pack_keys.argtypes = [vp, i64, i64, C.POINTER(Layout), vp, vp, vp]
+    lib.alto_route.restype = C.c_int
+    lib.alto_route.argtypes = [vp, i64, C.POINTER(Layout), i32, i32, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.alto_aggregate.restype = C.c_int
+    lib.alto_aggregate.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
+                                   vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp]
+    if not hasattr(lib, "alto_stream_state_bytes"):
+        _lib = lib
+        return lib
+    lib.alto_stream_state_bytes.restype = C.c_size_t
+    lib.alto_stream_state_bytes.argtypes = [C.POINTER(Layout), C.POINTER(Agg), i64, i64]
+    lib.alto_stream_create.restype = C.c_int
+    lib.alto_stream_create.argtypes = [C.POINTER(Layout), i32, i32, C.POINTER(Agg), i64, i64, vp,
+                                       C.c_size_t, vp, C.POINTER(vp)]
+    lib.alto_stream_step.restype = C.c_int
+    lib.alto_stream_step.argtypes = [vp, vp, vp, i64, vp, vp, i64, vp, vp, vp, C.POINTER(Groups), vp,
+                                     vp, C.c_size_t, vp]
+    lib.alto_stream_pending.restype = C.c_int
+    lib.alto_stream_pending.argtypes = [vp, C.POINTER(Groups), vp, vp]
+    lib.alto_stream_destroy.restype = C.c_int
+    lib.alto_stream_destroy.argtypes = [vp]
+    _lib = lib
+    return lib
+
+
+def layout(bits: Sequence[int]) -> Layout:
+    l = Layout()
+    l.depth = len(bits)
+    for i, b in enumerate(bits):
+        l.bits[i] = b
+    return l
+
+
+def agg_struct(level: int, op: str, dim: int = 1, mask_level: int = 0) -> Agg:
+    a = Agg()
+    a.level, a.op, a.dim, a.mask_level = level, (MEAN_F32 if op == "mean" else CONCAT_I32), dim, mask_level
+    return a
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _check(rc, what):
+    if rc != OK:
+        raise AltoError(rc, what)
+
+
+def workspace_bytes(bits, n_max, num_dest, level=None, op="concat", dim=1, mask_level=0) -> int:
+    lib = load()
+    L = layout(bits)
+    a = None if level is None else C.byref(agg_struct(level, op, dim, mask_level))
+    return int(lib.alto_workspace_bytes(C.byref(L), int(n_max), int(num_dest), a))
+
+
+def new_workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def new_status(device="cuda") -> torch.Tensor:
+    return torch.zeros(1, dtype=torch.int32, device=device)
+
+
+def pack_keys(path: torch.Tensor, bits, keys: Optional[torch.Tensor] = None, status=None, stream=None):
+    """path: int32 [d][ld] (level-major, first n columns used)."""
+    lib = load()
+    n = path.shape[1]
+    if keys is None:
+        keys = torch.empty(n, dtype=torch.int64, device=path.device)
+    if status is None:
+        status = new_status(path.device)
+    L = layout(bits)
+    rc = lib.alto_pack_keys(_p(path), path.stride(0), n, C.byref(L), _p(keys), _p(status), _stream(stream))
+    _check(rc, "alto_pack_keys")
+    return keys, status
+
+
+def route(keys, bits, route_level, num_dest, ws=None, perm=None, dest_offsets=None, dest=None,
+          status=None, stream=None, with_dest=True):
+    lib = load()
+    n = keys.shape[0]
+    dev = keys.device
+    if ws is None:
+        ws = new_workspace(workspace_bytes(bits, n, num_dest), dev)
+    if perm is None:
+        perm = torch.empty(n, dtype=torch.int32, device=dev)
+    if dest_offsets is None:
+        dest_offsets = torch.empty(num_dest + 1, dtype=torch.int64, device=dev)
+    if dest is None and with_dest:
+        dest = torch.empty(n, dtype=torch.int32, device=dev)
+    if status is None:
+        status = new_status(dev)
+    L = layout(bits)
+    rc = lib.alto_route(_p(keys), n, C.byref(L), route_level, num_dest, _p(perm), _p(dest_offsets),
+                        _p(dest), _p(status), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "alto_route")
+    return perm, dest_offsets, dest, status
+
+
+@dataclass
+class GroupTensors:
+    key: torch.Tensor
+    dest: torch.Tensor
+    count: torch.Tensor
+    first_i32: Optional[torch.Tensor]
+    fan_up: torch.Tensor
+    tok_off: Optional[torch.Tensor]
+    tok: Optional[torch.Tensor]
+    mean: Optional[torch.Tensor]
+    mask_key: Optional[torch.Tensor]
+    mask: Optional[torch.Tensor]
+    pend_key: torch.Tensor
+    pend_count: torch.Tensor
+    counts: torch.Tensor
+    cap_groups: int
+    cap_tokens: int
+    cap_mask: int
+
+    def struct(self) -> Groups:
+        g = Groups()
+        g.cap_groups, g.cap_tokens, g.cap_mask = self.cap_groups, self.cap_tokens, self.cap_mask
+        for name in ("key", "dest", "count", "first_i32", "fan_up", "tok_off", "tok", "mean",
+                     "mask_key", "mask", "pend_key", "pend_count", "counts"):
+            t = getattr(self, name)
+            setattr(g, name, None if t is None else t.data_ptr())
+        return g
+
+
+def new_groups(cap_groups, agg_level, op, dim=1, cap_tokens=0, cap_mask=0, device="cuda",
+               with_first=True) -> GroupTensors:
+    cg = max(int(cap_groups), 0)
+    e = lambda n, dt: torch.empty(max(n, 1), dtype=dt, device=device)
+    return GroupTensors(
+        key=e(cg, torch.int64), dest=e(cg, torch.int32), count=e(cg, torch.int64),
+        first_i32=e(cg, torch.int32) if with_first else None,
+        fan_up=e((agg_level - 1) * cg, torch.int32),
+        tok_off=e(cg + 1, torch.int64) if op == "concat" else None,
+        tok=e(cap_tokens, torch.int32) if op == "concat" else None,
+        mean=torch.empty(max(cg, 1), dim, dtype=torch.float32, device=device) if op == "mean" else None,
+        mask_key=e(cap_mask, torch.int64) if cap_mask else None,
+        mask=e(cap_mask, torch.uint8) if cap_mask else None,
+        pend_key=e(cg, torch.int64), pend_count=e(cg, torch.int64),
+        counts=torch.zeros(4, dtype=torch.int64, device=device),
+        cap_groups=cg, cap_tokens=int(cap_tokens), cap_mask=int(cap_mask))
+
+
+def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0, num_dest=1,
+              payload_i32=None, payload_f32=None, ws=None, perm=None, dest_offsets=None, dest=None,
+              out: Optional[GroupTensors] = None, status=None, stream=None, n=None):
+    """Routes and aggregates one batch; returns (perm, dest_offsets, dest, groups, status)."""
+    lib = load()
+    n = keys.shape[0] if n is None else n
+    dev = keys.device
+    if ws is None:
+        ws = new_workspace(workspace_bytes(bits, n, num_dest, agg_level, op, dim, mask_level), dev)
+    if perm is None:
+        perm = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    if dest_offsets is None:
+        dest_offsets = torch.empty(num_dest + 1, dtype=torch.int64, device=dev)
+    if dest is None:
+        dest = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    if out is None:
+        out = new_groups(n, agg_level, op, dim, cap_tokens=n if op == "concat" else 0,
+                         cap_mask=n if mask_level else 0, device=dev,
+                         with_first=payload_i32 is not None)
+    if status is None:
+        status = new_status(dev)
+    L = layout(bits)
+    A = agg_struct(agg_level, op, dim, mask_level)
+    G = out.struct()
+    rc = lib.alto_aggregate(_p(keys), _p(fan), fan.stride(0), _p(payload_i32), _p(payload_f32), n,
+                            C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
+                            _p(dest), C.byref(G), _p(status), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "alto_aggregate")
+    return perm, dest_offsets, dest, out, status
+
+
+class Stream:
+    """Carried-state stream over caller-owned device memory."""
+
+    def __init__(self, bits, route_level, num_dest, agg_level, op, dim=1, max_live_leaves=1 << 16,
+                 max_groups=1 << 20, step_max=4096, device="cuda", stream=None):
+        lib = load()
+        self.lib = lib
+        self.bits, self.Lr, self.D, self.La, self.op, self.dim = tuple(bits), route_level, num_dest, agg_level, op, dim
+        self.L = layout(bits)
+        self.A = agg_struct(agg_level, op, dim, 0)
+        nbytes = lib.alto_stream_state_bytes(C.byref(self.L), C.byref(self.A), max_live_leaves, max_groups)
+        if nbytes == 0:
+            raise AltoError(E_ARG, "alto_stream_state_bytes")
+        self.state = torch.empty(int(nbytes), dtype=torch.uint8, device=device)
+        self.ws = new_workspace(lib.alto_workspace_bytes(C.byref(self.L), step_max, num_dest,
+                                                         C.byref(self.A)), device)
+        self.step_max = step_max
+        self.max_live_leaves = max_live_leaves
+        self.handle = C.c_void_p()
+        rc = lib.alto_stream_create(C.byref(self.L), route_level, num_dest, C.byref(self.A),
+                                    max_live_leaves, max_groups, _p(self.state), self.state.numel(),
+                                    _stream(stream), C.byref(self.handle))
+        _check(rc, "alto_stream_create")
+
+    def step(self, keys, fan, payload_i32=None, payload_f32=None, out: Optional[GroupTensors] = None,
+             perm=None, dest_offsets=None, dest=None, status=None, stream=None):
+        n = keys.shape[0]
+        dev = keys.device
+        if out is None:
+            out = new_groups(n, self.La, self.op, self.dim,
+                             cap_tokens=self.max_live_leaves + n if self.op == "concat" else 0,
+                             device=dev, with_first=payload_i32 is not None)
+        if status is None:
+            status = new_status(dev)
+        G = out.struct()
+        rc = self.lib.alto_stream_step(self.handle, _p(keys), _p(fan), fan.stride(0), _p(payload_i32),
+                                       _p(payload_f32), n, _p(perm), _p(dest_offsets), _p(dest),
+                                       C.byref(G), _p(status), _p(self.ws), self.ws.numel(),
+                                       _stream(stream))
+        _check(rc, "alto_stream_step")
+        return out, status
+
+    def pending(self, out: Optional[GroupTensors] = None, status=None, stream=None, cap=None):
+        dev = self.state.device
+        if out is None:
+            out = new_groups(cap or self.max_live_leaves, self.La, self.op, self.dim, device=dev)
+        if status is None:
+            status = new_status(dev)
+        G = out.struct()
+        rc = self.lib.alto_stream_pending(self.handle, C.byref(G), _p(status), _stream(stream))
+        _check(rc, "alto_stream_pending")
+        return out, status
+
+    def close(self):
+        if self.handle:
+            self.lib.alto_stream_destroy(self.handle)
+            self.handle = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,82 @@
+// Batch routing and aggregation (internal).
+#pragma once
+#include "alto_internal.h"
+#include "segment.h"
+#include "sort.h"
+
+#define MEAN_CHUNK_ROWS 1024
+
+// One unit of gather work: rows [begin, begin+len) of the sorted fragments, the
+// k-th of nch chunks of emitted group e.
+struct Chunk {
+  int64_t e;       // emitted group index
+  int64_t out;     // concat: tok offset of the chunk's first row
+  int64_t part;    // mean: first partial-sum slot of the group (-1 if one chunk)
+  int32_t begin;   // first sorted position
+  int32_t len;
+  int32_t k;
+  int32_t nch;
+  int32_t count;   // leaves of the group
+  int32_t pad;
+};
+
+// Device copy of the caller's alto_groups.
+struct GroupOut {
+  int64_t cap_groups, cap_tokens, cap_mask;
+  uint64_t* key;
+  int32_t* dest;
+  int64_t* count;
+  int32_t* first_i32;
+  int32_t* fan_up;
+  int64_t* tok_off;
+  int32_t* tok;
+  float* mean;
+  uint64_t* mask_key;
+  uint8_t* mask;
+  uint64_t* pend_key;
+  int64_t* pend_count;
+  int64_t* counts;
+};
+
+struct AggBufs {
+  SortCtl* ctl;
+  SortCtl* rctl;
+  uint64_t* fp_in;
+  uint64_t* fp_nodes;
+  int64_t* nnodes;
+  int64_t* scal;        // [8] device scalars: 0 = G+1, 1 = chunk count
+  uint64_t* tmp_keys;
+  uint32_t* tmp_vals;
+  uint64_t* sk;
+  uint32_t* perm;
+  uint32_t* perm_used;  // perm buffer the sort wrote (caller's or ours)
+  uint32_t* hist;
+  uint32_t* scan_u32;
+  int32_t* scan_i32;
+  int64_t* scan_i64;
+  int32_t* blkcnt;
+  LevelNodes lv[ALTO_MAX_LEVELS + 1];
+  int32_t* carry_fan;
+  uint64_t* rkey;
+  uint64_t* rsk;
+  uint32_t* ridx;
+  int32_t* em;
+  int64_t* tokc;
+  int64_t* nch;
+  int64_t* pch;
+  Chunk* chunks;
+  double* part;
+};
+
+void agg_levels(const KeyGeom& g, int La, int Lm, int Lr, int* Lt, int* Lseg);
+void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const alto_agg* agg, int Lr, WsCarver& c,
+                  AggBufs& b);
+int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
+              int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
+              int32_t* status, hipStream_t st);
+int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
+                  const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
+                  int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
+                  hipStream_t st);
+void empty_outputs(const GroupOut& out, int64_t* dest_offsets, int num_dest, hipStream_t st);
+void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st);

@@ -1,0 +1,565 @@
+// Routing (Section 4.3 of the paper) and aggregation at a pmap exit (Sections 3.3
+// and 4.3) of one batch: kernels and their orchestration.
+#include "aggregate.h"
+
+#include <string.h>
+
+namespace {
+
+constexpr int PREP_NT = 256;
+constexpr int GRID_CAP = 4096;
+
+__device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : h; }
+
+// Input order, one pass: layout check, destination, OR/AND of keys and
+// destinations for the sort, per-fragment fan-out checks, and the fragment side of
+// the fan fingerprint.
+__global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
+                                                  RouteGeom rg, int32_t* dest, const int32_t* __restrict__ fan,
+                                                  int64_t fan_ld, int flo, int fhi, uint64_t* fp_in, SortCtl* ctl,
+                                                  int32_t* status) {
+  uint64_t kor = 0, kand = ~0ull;
+  uint32_t dor = 0, dand = ~0u;
+  uint64_t fp[ALTO_MAX_LEVELS + 1];
+  for (int m = flo; m <= fhi; ++m) fp[m] = 0;
+  bool bad_layout = false, bad_fan = false;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = keys[i];
+    bad_layout |= (k >> g.total) != 0;
+    const uint32_t d = dest_of_key(rg, k);
+    if (dest) dest[i] = (int32_t)d;
+    kor |= k;
+    kand &= k;
+    dor |= d;
+    dand &= d;
+    for (int m = flo; m <= fhi; ++m) {
+      const int32_t f = fan[(int64_t)(m - 1) * fan_ld + i];
+      bad_fan |= (f < 1) || ((int64_t)key_tag(g, k, m + 1) >= (int64_t)f);
+      fp[m] += fan_term(m, key_prefix(k, g.shift[m]), (uint32_t)f);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kor |= __shfl_xor(kor, o);
+    kand &= __shfl_xor(kand, o);
+    dor |= __shfl_xor(dor, o);
+    dand &= __shfl_xor(dand, o);
+  }
+  for (int m = flo; m <= fhi; ++m) fp[m] = wave_sum(fp[m]);
+  if (lane_id() == 0) {
+    if (ctl) {
+      atomicOr((unsigned long long*)&ctl->key_or, (unsigned long long)kor);
+      atomicAnd((unsigned long long*)&ctl->key_and, (unsigned long long)kand);
+      atomicOr(&ctl->dest_or, dor);
+      atomicAnd(&ctl->dest_and, dand);
+    }
+    for (int m = flo; m <= fhi; ++m)
+      if (fp[m]) atomicAdd((unsigned long long*)&fp_in[m], (unsigned long long)fp[m]);
+  }
+  if (bad_layout) raise_status(status, ALTO_E_LAYOUT);
+  if (bad_fan) raise_status(status, ALTO_E_FANOUT);
+}
+
+__global__ void k_zero_u64(uint64_t* p, int count) {
+  for (int i = threadIdx.x; i < count; i += blockDim.x) p[i] = 0;
+}
+
+__global__ void k_init_ctl(SortCtl* ctl) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    ctl->key_or = 0;
+    ctl->key_and = ~0ull;
+    ctl->dest_or = 0;
+    ctl->dest_and = ~0u;
+  }
+}
+
+// dest_offsets from the sorted keys; duplicate keys are adjacent after the sort.
+__global__ __launch_bounds__(256) void k_dest_offsets(const uint64_t* __restrict__ sk, int64_t n, RouteGeom rg,
+                                                      int64_t* offs, int32_t* status) {
+  const uint32_t D = rg.num_dest;
+  bool dup = false;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = sk[j];
+    const uint32_t d = dest_of_key(rg, k);
+    uint32_t dp = 0;
+    if (j > 0) {
+      const uint64_t kp = sk[j - 1];
+      dup |= (kp == k);
+      dp = dest_of_key(rg, kp);
+    }
+    if (offs) {
+      if (j == 0) {
+        for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
+      } else if (d != dp) {
+        for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = j;
+      }
+      if (j == n - 1)
+        for (uint32_t x = d + 1; x <= D; ++x) offs[x] = n;
+    }
+  }
+  if (dup) raise_status(status, ALTO_E_DUPLICATE);
+}
+
+__global__ void k_fill_i64(int64_t* p, int64_t count, int64_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
+__global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  for (int m = flo; m <= fhi; ++m)
+    if (fp_in[m] != fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
+}
+
+// Per-group scan inputs.
+__global__ __launch_bounds__(256) void k_group_flags(LevelNodes L, const int64_t* Gp, int32_t* em, int64_t* tokc,
+                                                     int64_t* nch, int64_t* pch, int chunk_rows) {
+  const int64_t G = *Gp;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
+    const bool ok = L.ok[u];
+    const int64_t cnt = (int64_t)L.start[u + 1] - L.start[u];
+    em[u] = ok ? 1 : 0;
+    tokc[u] = ok ? cnt : 0;
+    const int64_t c = ok ? cdiv(cnt, chunk_rows) : 0;
+    nch[u] = c;
+    pch[u] = c > 1 ? c : 0;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    em[G] = 0;
+    tokc[G] = 0;
+    nch[G] = 0;
+    pch[G] = 0;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int La, LevelNodes L, const int64_t* Gp,
+                                                   const uint64_t* __restrict__ sk, const uint32_t* __restrict__ perm,
+                                                   const int32_t* em, const int64_t* tokb, const int64_t* chb,
+                                                   const int64_t* pb, const int32_t* __restrict__ fan, int64_t fan_ld,
+                                                   const int32_t* __restrict__ p32, GroupOut out, Chunk* chunks,
+                                                   int chunk_rows) {
+  const int64_t G = *Gp;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
+    const uint64_t k = sk[s];
+    const uint64_t gk = key_prefix(k, g.shift[La]);
+    if (L.ok[u]) {
+      const int64_t e = em[u];
+      if (e < out.cap_groups) {
+        if (out.key) out.key[e] = gk;
+        if (out.dest) out.dest[e] = (int32_t)dest_of_key(rg, k);
+        if (out.count) out.count[e] = cnt;
+        const uint32_t first = perm[s];
+        if (out.first_i32 && p32) out.first_i32[e] = p32[first];
+        if (out.fan_up)
+          for (int l = 1; l < La; ++l) out.fan_up[(int64_t)(l - 1) * out.cap_groups + e] = fan[(int64_t)(l - 1) * fan_ld + first];
+        if (out.tok_off) out.tok_off[e] = tokb[u];
+      }
+      const int64_t nc = chb[u + 1] - chb[u];
+      for (int64_t c = 0; c < nc; ++c) {
+        Chunk ch;
+        ch.e = e;
+        ch.begin = s + (int32_t)(c * chunk_rows);
+        ch.len = (int32_t)((cnt - c * chunk_rows) < chunk_rows ? (cnt - c * chunk_rows) : chunk_rows);
+        ch.k = (int32_t)c;
+        ch.nch = (int32_t)nc;
+        ch.count = cnt;
+        ch.part = nc > 1 ? pb[u] : -1;
+        ch.out = tokb[u] + c * chunk_rows;
+        chunks[chb[u] + c] = ch;
+      }
+    } else {
+      const int64_t p = u - em[u];
+      if (p < out.cap_groups) {
+        if (out.pend_key) out.pend_key[p] = gk;
+        if (out.pend_count) out.pend_count[p] = cnt;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks, const int64_t* nchunks,
+                                                const uint32_t* __restrict__ perm, const int32_t* __restrict__ p32,
+                                                int32_t* tok, int64_t cap_tokens) {
+  const int64_t C = *nchunks;
+  for (int64_t c = blockIdx.x; c < C; c += gridDim.x) {
+    const Chunk ch = chunks[c];
+    for (int r = threadIdx.x; r < ch.len; r += blockDim.x) {
+      const int64_t o = ch.out + r;
+      if (o < cap_tokens) tok[o] = p32[perm[ch.begin + r]];
+    }
+  }
+}
+
+// fp64 sum of the rows of one chunk of a group, in a fixed order: each lane sums
+// its rows sequentially, then lanes holding the same columns are combined in lane
+// order, then the waves in wave order. Groups of one chunk are finished here;
+// others leave a partial sum.
+template <int VEC, int CPL>
+__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks,
+                                              const uint32_t* __restrict__ perm, const float* __restrict__ pay,
+                                              int dim, int lpr, double* part, float* mean, int64_t cap_groups) {
+  constexpr int NW = 4;
+  __shared__ double red[NW][64 * CPL * VEC];
+  const int C = dim / VEC;
+  const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
+  const int rpw = ALTO_WAVE / lpr, sub = lane / lpr, cl = lane % lpr;
+  const int64_t NC = *nchunks;
+  for (int64_t c = blockIdx.x; c < NC; c += gridDim.x) {
+    const Chunk ch = chunks[c];
+    for (int col0 = 0; col0 < C; col0 += lpr * CPL) {
+      double acc[CPL][VEC];
+#pragma unroll
+      for (int q = 0; q < CPL; ++q)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[q][v] = 0.0;
+      for (int r = w * rpw + sub; r < ch.len; r += NW * rpw) {
+        const int64_t row = perm[ch.begin + r];
+        const float* src = pay + row * (int64_t)dim;
+#pragma unroll
+        for (int q = 0; q < CPL; ++q) {
+          const int col = col0 + cl + q * lpr;
+          if (col < C) {
+            if constexpr (VEC == 4) {
+              const float4 x = *reinterpret_cast<const float4*>(src + (int64_t)col * 4);
+              acc[q][0] += x.x;
+              acc[q][1] += x.y;
+              acc[q][2] += x.z;
+              acc[q][3] += x.w;
+            } else {
+              acc[q][0] += src[col];
+            }
+          }
+        }
+      }
+      // combine the sub-rows of the wave (lanes with equal cl), in a fixed order
+      for (int o = lpr; o < ALTO_WAVE; o <<= 1)
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[q][v] += __shfl_xor(acc[q][v], o);
+      if (sub == 0)
+#pragma unroll
+        for (int q = 0; q < CPL; ++q)
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) red[w][(q * lpr + cl) * VEC + v] = acc[q][v];
+      __syncthreads();
+      const int ncol = lpr * CPL * VEC;
+      for (int t = threadIdx.x; t < ncol; t += blockDim.x) {
+        const int q = t / (lpr * VEC), rem = t % (lpr * VEC);
+        const int col = col0 + q * lpr + rem / VEC;
+        if (col >= C) continue;
+        double s = 0.0;
+#pragma unroll
+        for (int ww = 0; ww < NW; ++ww) s += red[ww][t];
+        const int64_t x = (int64_t)col * VEC + rem % VEC;
+        if (ch.nch == 1) {
+          if (ch.e < cap_groups) mean[ch.e * (int64_t)dim + x] = (float)(s / (double)ch.count);
+        } else {
+          part[(ch.part + ch.k) * (int64_t)dim + x] = s;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_mean_combine(const Chunk* __restrict__ chunks, const int64_t* nchunks,
+                                                      const double* __restrict__ part, int dim, float* mean,
+                                                      int64_t cap_groups) {
+  const int64_t NC = *nchunks;
+  for (int64_t c = blockIdx.x; c < NC; c += gridDim.x) {
+    const Chunk ch = chunks[c];
+    if (ch.k != 0 || ch.nch <= 1 || ch.e >= cap_groups) continue;
+    for (int x = threadIdx.x; x < dim; x += blockDim.x) {
+      double s = 0.0;
+      for (int t = 0; t < ch.nch; ++t) s += part[(ch.part + t) * (int64_t)dim + x];
+      mean[ch.e * (int64_t)dim + x] = (float)(s / (double)ch.count);
+    }
+  }
+}
+
+__global__ void k_mask_out(LevelNodes L, const int64_t* Np, const uint64_t* __restrict__ keys, int shift,
+                           uint64_t* mask_key, uint8_t* mask, int64_t cap_mask) {
+  const int64_t N = *Np;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < N && u < cap_mask; u += (int64_t)gridDim.x * blockDim.x) {
+    if (mask_key) mask_key[u] = key_prefix(keys[L.start[u]], shift);
+    if (mask) mask[u] = L.ok[u];
+  }
+}
+
+__global__ void k_record_keys(LevelNodes L, const int64_t* Np, const uint64_t* __restrict__ sk, int shift,
+                              uint64_t* rkey) {
+  const int64_t N = *Np;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < N; u += (int64_t)gridDim.x * blockDim.x)
+    rkey[u] = key_prefix(sk[L.start[u]], shift);
+}
+
+__global__ void k_gplus1(const int64_t* Gp, int64_t* scal) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) scal[0] = *Gp + 1;
+}
+
+__global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* tokc, const int64_t* nch, const int64_t* Mp,
+                         int64_t* counts, int64_t* tok_off, GroupOut out, int64_t* scal, int32_t* status) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int64_t G = *Gp;
+  scal[1] = nch[G];
+  const int64_t E = em[G];
+  const int64_t T = tokc ? tokc[G] : 0;
+  const int64_t M = Mp ? *Mp : 0;
+  const int64_t P = G - E;
+  counts[0] = E;
+  counts[1] = T;
+  counts[2] = M;
+  counts[3] = P;
+  if (tok_off && E <= out.cap_groups) tok_off[E] = T;
+  if (E > out.cap_groups || P > out.cap_groups || T > out.cap_tokens || M > out.cap_mask)
+    raise_status(status, ALTO_E_CAPACITY);
+}
+
+inline int grid_for(int64_t n, int nt, int cap = GRID_CAP) {
+  int64_t b = cdiv(n < 1 ? 1 : n, nt);
+  return (int)(b < cap ? b : cap);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// workspace plan
+// ---------------------------------------------------------------------------
+void agg_levels(const KeyGeom& g, int La, int Lm, int Lr, int* Lt, int* Lseg) {
+  *Lt = (Lm > 0 && Lm < La) ? Lm : La;
+  *Lseg = Lr > *Lt ? Lr : *Lt;
+}
+
+void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const alto_agg* agg, int Lr, WsCarver& c,
+                  AggBufs& b) {
+  memset(&b, 0, sizeof(b));
+  const int64_t n = n_max < 1 ? 1 : n_max;
+  b.ctl = c.take<SortCtl>(1);
+  b.rctl = c.take<SortCtl>(1);
+  b.fp_in = c.take<uint64_t>(ALTO_MAX_LEVELS + 1);
+  b.fp_nodes = c.take<uint64_t>(ALTO_MAX_LEVELS + 1);
+  b.nnodes = c.take<int64_t>(ALTO_MAX_LEVELS + 1);
+  b.scal = c.take<int64_t>(8);
+  b.tmp_keys = c.take<uint64_t>(n);
+  b.tmp_vals = c.take<uint32_t>(n);
+  b.sk = c.take<uint64_t>(n);
+  b.perm = c.take<uint32_t>(n);
+  b.hist = c.take<uint32_t>((int64_t)SORT_BUCKETS * sort_hist_blocks(n));
+  b.scan_u32 = c.take<uint32_t>(SCAN_MAX_BLOCKS + 1);
+  b.scan_i32 = c.take<int32_t>(SCAN_MAX_BLOCKS + 1);
+  b.scan_i64 = c.take<int64_t>(SCAN_MAX_BLOCKS + 1);
+  if (!agg) return;
+  int Lt, Lseg;
+  agg_levels(g, agg->level, agg->mask_level, Lr, &Lt, &Lseg);
+  const int d = g.depth;
+  b.blkcnt = c.take<int32_t>((int64_t)(d - Lt) * seg_blocks(n) + 1);
+  for (int m = Lt; m < d; ++m) {
+    LevelNodes& L = b.lv[m];
+    L.start = c.take<int32_t>(n + 1);
+    L.fc = c.take<int32_t>(n + 1);
+    L.par = c.take<int32_t>(n);
+    L.nfan = c.take<int32_t>(n);
+    L.ok = c.take<uint8_t>(n);
+    L.bad = c.take<uint8_t>(n);
+  }
+  if (Lt < Lseg) {
+    b.carry_fan = c.take<int32_t>((int64_t)(Lseg - Lt) * n);
+    b.rkey = c.take<uint64_t>(n);
+    b.rsk = c.take<uint64_t>(n);
+    b.ridx = c.take<uint32_t>(n);
+  }
+  b.em = c.take<int32_t>(n + 1);
+  b.tokc = c.take<int64_t>(n + 1);
+  b.nch = c.take<int64_t>(n + 1);
+  b.pch = c.take<int64_t>(n + 1);
+  b.chunks = c.take<Chunk>(n / MEAN_CHUNK_ROWS + n + 1);
+  if (agg->op == ALTO_MEAN_F32) b.part = c.take<double>((2 * cdiv(n, MEAN_CHUNK_ROWS) + 2) * (int64_t)agg->dim);
+}
+
+// ---------------------------------------------------------------------------
+// orchestration
+// ---------------------------------------------------------------------------
+int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
+              int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
+              int32_t* status, hipStream_t st) {
+  k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
+  k_zero_u64<<<1, 64, 0, st>>>(b.fp_in, ALTO_MAX_LEVELS + 1);
+  k_zero_u64<<<1, 64, 0, st>>>(b.fp_nodes, ALTO_MAX_LEVELS + 1);
+  k_prep<<<grid_for(n, PREP_NT * 8, 2048), PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fhi, b.fp_in, b.ctl,
+                                                             status);
+  ALTO_LAUNCH_CHECK();
+  SortBufs sb;
+  sb.in_keys = keys;
+  sb.tmp_keys = b.tmp_keys;
+  sb.tmp_vals = b.tmp_vals;
+  sb.out_keys = b.sk;
+  sb.out_vals = perm_out ? reinterpret_cast<uint32_t*>(perm_out) : b.perm;
+  sb.hist = b.hist;
+  sb.scan_part = b.scan_u32;
+  sb.ctl = b.ctl;
+  b.perm_used = sb.out_vals;
+  int rc = sort_pairs(sb, n, nullptr, rg, g.total, true, st);
+  if (rc) return rc;
+  k_dest_offsets<<<grid_for(n, 256), 256, 0, st>>>(b.sk, n, rg, dest_offsets, status);
+  ALTO_LAUNCH_CHECK();
+  return ALTO_OK;
+}
+
+int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
+                  const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
+                  int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
+                  hipStream_t st) {
+  const int d = g.depth, La = agg.level, Lm = agg.mask_level;
+  int Lt, Lseg;
+  agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
+  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st);
+  if (rc) return rc;
+  const uint32_t* perm = b.perm_used;
+
+  // fragments: levels Lseg..d-1 are contiguous in (dest, key) order
+  SegJob fj;
+  memset(&fj, 0, sizeof(fj));
+  fj.keys = b.sk;
+  fj.idx = perm;
+  fj.n_host = n;
+  fj.n_max = n;
+  fj.elem_level = d;
+  fj.lo = Lseg;
+  fj.fan = fan;
+  fj.fan_ld = fan_ld;
+  fj.fan_base = 1;
+  fj.check_dup = 0;   // duplicates are reported by k_dest_offsets
+  fj.carry_lo = Lt;
+  fj.carry_fan = (Lt < Lseg) ? b.carry_fan : nullptr;
+  fj.carry_ld = n < 1 ? 1 : n;
+  for (int m = 0; m <= ALTO_MAX_LEVELS; ++m) fj.lv[m] = b.lv[m];
+  fj.nnodes = b.nnodes;
+  fj.blkcnt = b.blkcnt;
+  fj.scan_part = b.scan_i32;
+  fj.fp_nodes = b.fp_nodes;
+  fj.status = status;
+  rc = seg_run(g, fj, st);
+  if (rc) return rc;
+
+  const int64_t* Mp = nullptr;
+  if (Lm > 0 && Lm < Lseg) {
+    // mask levels above the route level: node records of level Lseg, re-sorted by key
+    const int64_t* Rp = b.nnodes + Lseg;
+    k_record_keys<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lseg], Rp, b.sk, g.shift[Lseg], b.rkey);
+    SortBufs rb;
+    rb.in_keys = b.rkey;
+    rb.tmp_keys = b.tmp_keys;
+    rb.tmp_vals = b.tmp_vals;
+    rb.out_keys = b.rsk;
+    rb.out_vals = b.ridx;
+    rb.hist = b.hist;
+    rb.scan_part = b.scan_u32;
+    rb.ctl = b.rctl;
+    RouteGeom none;
+    none.shift = 64;
+    none.num_dest = 1;
+    rc = sort_pairs(rb, n, Rp, none, g.total - g.shift[Lseg], false, st);
+    if (rc) return rc;
+    SegJob rj;
+    memset(&rj, 0, sizeof(rj));
+    rj.keys = b.rsk;
+    rj.idx = b.ridx;
+    rj.n_dev = Rp;
+    rj.n_max = n;
+    rj.elem_level = Lseg;
+    rj.lo = Lt;
+    rj.fan = b.carry_fan;
+    rj.fan_ld = n < 1 ? 1 : n;
+    rj.fan_base = Lt;
+    rj.elem_ok = b.lv[Lseg].ok;
+    rj.chain_check = 1;
+    for (int m = 0; m <= ALTO_MAX_LEVELS; ++m) rj.lv[m] = b.lv[m];
+    rj.nnodes = b.nnodes;
+    rj.blkcnt = b.blkcnt;
+    rj.scan_part = b.scan_i32;
+    rj.status = status;
+    rc = seg_run(g, rj, st);
+    if (rc) return rc;
+    Mp = b.nnodes + Lm;
+    k_mask_out<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lm], Mp, b.rsk, g.shift[Lm] - g.shift[Lseg], out.mask_key,
+                                                 out.mask, out.cap_mask);
+  } else if (Lm > 0) {
+    Mp = b.nnodes + Lm;
+    k_mask_out<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lm], Mp, b.sk, g.shift[Lm], out.mask_key, out.mask, out.cap_mask);
+  }
+  k_fp_compare<<<1, 1, 0, st>>>(b.fp_in, b.fp_nodes, Lt, d - 1, status);
+
+  // groups
+  const int64_t* Gp = b.nnodes + La;
+  const LevelNodes& GL = b.lv[La];
+  k_group_flags<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, MEAN_CHUNK_ROWS);
+  k_gplus1<<<1, 1, 0, st>>>(Gp, b.scal);
+  // exclusive scans over G+1 entries (entry G is zero): entry G receives the total
+  const int64_t* G1 = b.scal;
+  rc = scan_exclusive<int32_t>(b.em, b.em, n + 1, G1, b.scan_i32, nullptr, st);
+  if (!rc) rc = scan_exclusive<int64_t>(b.tokc, b.tokc, n + 1, G1, b.scan_i64, nullptr, st);
+  if (!rc) rc = scan_exclusive<int64_t>(b.nch, b.nch, n + 1, G1, b.scan_i64, nullptr, st);
+  if (!rc && agg.op == ALTO_MEAN_F32) rc = scan_exclusive<int64_t>(b.pch, b.pch, n + 1, G1, b.scan_i64, nullptr, st);
+  if (rc) return rc;
+  k_group_out<<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, b.sk, perm, b.em, b.tokc, b.nch, b.pch, fan, fan_ld,
+                                                p32, out, b.chunks, MEAN_CHUNK_ROWS);
+  k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, Mp, out.counts, out.tok_off,
+                            out, b.scal, status);
+  ALTO_LAUNCH_CHECK();
+  const int64_t* NCp = b.scal + 1;   // chunk count
+  if (agg.op == ALTO_CONCAT_I32) {
+    if (out.tok) k_concat<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, perm, p32, out.tok, out.cap_tokens);
+  } else if (out.mean) {
+    const int dim = agg.dim;
+    const bool v4 = (dim % 4 == 0) && ((reinterpret_cast<uintptr_t>(pf) & 15) == 0);
+    const int C = v4 ? dim / 4 : dim;
+    int lpr = 1;
+    while (lpr < C && lpr < 64) lpr <<= 1;
+    const int cpl_need = (int)cdiv(C, lpr);
+    const int cpl = cpl_need >= 4 ? 4 : cpl_need;
+    const int grid = GRID_CAP * 4;
+#define ALTO_MEAN_CASE(V, P) \
+  k_mean<V, P><<<grid, 256, 0, st>>>(b.chunks, NCp, perm, pf, dim, lpr, b.part, out.mean, out.cap_groups)
+    if (v4) {
+      if (cpl == 1) ALTO_MEAN_CASE(4, 1);
+      else if (cpl == 2) ALTO_MEAN_CASE(4, 2);
+      else if (cpl == 3) ALTO_MEAN_CASE(4, 3);
+      else ALTO_MEAN_CASE(4, 4);
+    } else {
+      if (cpl == 1) ALTO_MEAN_CASE(1, 1);
+      else if (cpl == 2) ALTO_MEAN_CASE(1, 2);
+      else if (cpl == 3) ALTO_MEAN_CASE(1, 3);
+      else ALTO_MEAN_CASE(1, 4);
+    }
+#undef ALTO_MEAN_CASE
+    k_mean_combine<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, b.part, dim, out.mean, out.cap_groups);
+  }
+  ALTO_LAUNCH_CHECK();
+  return ALTO_OK;
+}
+
+namespace {
+__global__ void k_empty(GroupOut out, int64_t* offs, int num_dest) {
+  for (int i = threadIdx.x; i <= num_dest; i += blockDim.x)
+    if (offs) offs[i] = 0;
+  if (threadIdx.x == 0) {
+    out.counts[0] = out.counts[1] = out.counts[2] = out.counts[3] = 0;
+    if (out.tok_off) out.tok_off[0] = 0;
+  }
+}
+}  // namespace
+
+void empty_outputs(const GroupOut& out, int64_t* dest_offsets, int num_dest, hipStream_t st) {
+  k_empty<<<1, 256, 0, st>>>(out, dest_offsets, num_dest);
+}
+
+namespace {
+__global__ void k_zero_offsets(int64_t* offs, int num_dest) {
+  for (int i = threadIdx.x; i <= num_dest; i += blockDim.x) offs[i] = 0;
+}
+}  // namespace
+
+void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st) {
+  if (dest_offsets) k_zero_offsets<<<1, 256, 0, st>>>(dest_offsets, num_dest);
+}

@@ -1,0 +1,155 @@
+// Internal declarations of libalto: device helpers shared by the kernels and the
+// host launchers. gfx950 (CDNA4) only: 64-lane wavefronts, 160 KB LDS per CU.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/alto.h"
+
+#define ALTO_WAVE 64
+#define ALTO_MAX_LEVELS 16
+
+// ---------------------------------------------------------------------------
+// key layout, precomputed on the host and passed by value to kernels
+// ---------------------------------------------------------------------------
+struct KeyGeom {
+  int32_t depth;
+  int32_t total;                      // sum of bits
+  int32_t shift[ALTO_MAX_LEVELS + 1]; // shift[l] = bits below level l (l = 1..depth), shift[0] = total
+  uint32_t tagmask[ALTO_MAX_LEVELS + 1];  // tagmask[l] = 2^bits[l-1] - 1
+};
+
+__host__ __device__ inline uint64_t key_prefix(uint64_t k, int sh) { return sh >= 64 ? 0ull : (k >> sh); }
+
+__host__ __device__ inline uint32_t key_tag(const KeyGeom& g, uint64_t k, int level) {
+  return (uint32_t)(key_prefix(k, g.shift[level]) & (uint64_t)g.tagmask[level]);
+}
+
+// SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014).
+__host__ __device__ inline uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Destination of a tag prefix: hash, then Lemire's multiply-shift range reduction.
+__host__ __device__ inline uint32_t dest_of_prefix(uint64_t p, uint32_t num_dest) {
+  return (uint32_t)(((mix64(p) >> 32) * (uint64_t)num_dest) >> 32);
+}
+
+struct RouteGeom {
+  int32_t shift;      // bits below the route level (64 = route everything to one place)
+  uint32_t num_dest;
+};
+
+__host__ __device__ inline uint32_t dest_of_key(const RouteGeom& r, uint64_t k) {
+  return r.shift >= 64 ? 0u : dest_of_prefix(k >> r.shift, r.num_dest);
+}
+
+// Term of the additive multiset fingerprint used to check that all carriers of a
+// node declare the same child count (sums of a random-looking function over a
+// multiset, Clarke et al., "Incremental multiset hash functions", ASIACRYPT 2003).
+__host__ __device__ inline uint64_t fan_term(int level, uint64_t node, uint32_t fan) {
+  return mix64(node * 0x9E3779B97F4A7C15ull + ((uint64_t)fan << 8) + (uint64_t)level + 0x632BE59BD9B4E019ull);
+}
+
+// ---------------------------------------------------------------------------
+// status word: the highest-priority error wins
+// ---------------------------------------------------------------------------
+__host__ __device__ inline int status_priority(int code) {
+  switch (code) {
+    case ALTO_E_LAYOUT: return 5;
+    case ALTO_E_LATE: return 4;
+    case ALTO_E_FANOUT: return 3;
+    case ALTO_E_DUPLICATE: return 2;
+    case ALTO_E_CAPACITY: return 1;
+    default: return 0;
+  }
+}
+
+__device__ inline void raise_status(int32_t* st, int code) {
+  int cur = __hip_atomic_load(st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  while (status_priority(code) > status_priority(cur)) {
+    int old = atomicCAS(st, cur, code);
+    if (old == cur) break;
+    cur = old;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// wave / block primitives
+// ---------------------------------------------------------------------------
+__device__ inline int lane_id() { return threadIdx.x & (ALTO_WAVE - 1); }
+
+__device__ inline uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+
+template <typename T>
+__device__ inline T wave_incl_scan(T v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int o = 1; o < ALTO_WAVE; o <<= 1) {
+    T u = __shfl_up(v, o, ALTO_WAVE);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+template <typename T>
+__device__ inline T wave_sum(T v) {
+#pragma unroll
+  for (int o = ALTO_WAVE / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, ALTO_WAVE);
+  return v;
+}
+
+// Exclusive scan over a block of NT threads; returns the exclusive prefix of v and
+// writes the block total to *total. `sh` holds NT / 64 entries.
+template <typename T, int NT>
+__device__ inline T block_excl_scan(T v, T* sh, T* total) {
+  constexpr int NW = NT / ALTO_WAVE;
+  const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
+  T inc = wave_incl_scan(v);
+  if (lane == ALTO_WAVE - 1) sh[w] = inc;
+  __syncthreads();
+  T off = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) {
+    T s = sh[i];
+    if (i < w) off += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return off + inc - v;
+}
+
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+#define ALTO_LAUNCH_CHECK()                                  \
+  do {                                                        \
+    if (hipGetLastError() != hipSuccess) return ALTO_E_HIP;   \
+  } while (0)
+
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Bump allocator over a caller workspace; every buffer is 256-byte aligned.
+struct WsCarver {
+  char* base;
+  size_t cap;
+  size_t off;
+  bool ok;
+  template <typename T>
+  T* take(int64_t count) {
+    size_t bytes = ((size_t)(count < 1 ? 1 : count) * sizeof(T) + 255) & ~(size_t)255;
+    if (off + bytes > cap) { ok = false; return nullptr; }
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+// Geometry helpers (host).
+KeyGeom make_geom(const alto_layout* l);
+RouteGeom make_route(const KeyGeom& g, int route_level, int num_dest);

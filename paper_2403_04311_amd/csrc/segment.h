@@ -1,0 +1,54 @@
+// Segmentation of sorted fragments into ancestry nodes and the completion cascade
+// (internal).
+#pragma once
+#include "alto_internal.h"
+
+#define SEG_NT 256
+#define SEG_IT 8
+#define SEG_TILE (SEG_NT * SEG_IT)
+#define NODE_GRID 1024
+
+// Arrays describing the nodes of one level, in element order.
+struct LevelNodes {
+  int32_t* start;   // [N+1] first element of each node; start[N] = number of elements
+  int32_t* fc;      // [N+1] id of the first child node (next level); fc[N] = child count
+  int32_t* par;     // [N] id of the parent node (previous level)
+  int32_t* nfan;    // [N] declared child count (from the node's first element)
+  uint8_t* ok;      // [N] 1 = the node's whole subtree is present
+  uint8_t* bad;     // [N] set when some child is incomplete
+};
+
+// One segmentation run over elements sorted so that every node of the levels
+// [lo, elem_level-1] is a contiguous run. Elements are either fragments
+// (elem_level = depth; their fans are read through idx from the caller's level-
+// major fan array) or node records of level elem_level (fans from rec_fan, ok flags
+// from elem_ok).
+struct SegJob {
+  const uint64_t* keys;     // sorted element keys (prefix of level elem_level)
+  const uint32_t* idx;      // element -> row in the fan source
+  const int64_t* n_dev;     // number of elements (device), or null: n_host
+  int64_t n_host;
+  int64_t n_max;
+  int32_t elem_level;
+  int32_t lo;               // segmented levels: lo .. elem_level-1
+  const int32_t* fan;       // fan source, level-major: level m at fan[(m - fan_base) * fan_ld + row]
+  int64_t fan_ld;
+  int32_t fan_base;
+  const uint8_t* elem_ok;   // records: ok flag per row (null for fragments)
+  int32_t chain_check;      // records: compare adjacent carriers' fans (exact)
+  int32_t check_dup;        // fragments: equal adjacent keys are duplicates
+  // carried levels (fragments only): fans of levels [carry_lo, lo-1] are copied
+  // from each level-lo node's first element into carry_fan[(m-carry_lo)*carry_ld + node]
+  int32_t carry_lo;
+  int32_t* carry_fan;
+  int64_t carry_ld;
+  LevelNodes lv[ALTO_MAX_LEVELS + 1];   // indexed by level
+  int64_t* nnodes;          // device [ALTO_MAX_LEVELS + 1]: node count per level
+  int32_t* blkcnt;          // [(elem_level - lo) * nblk + 1]
+  int32_t* scan_part;       // [SCAN_MAX_BLOCKS + 1]
+  uint64_t* fp_nodes;       // device [ALTO_MAX_LEVELS + 1]: fingerprint sums over nodes (fragments)
+  int32_t* status;
+};
+
+int seg_blocks(int64_t n_max);
+int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st);
