@@ -190,6 +190,18 @@ int alto_stream_pending(alto_stream *s, alto_groups *out, int32_t *status, hipSt
 /* Frees the host handle (the caller frees the state memory). */
 int alto_stream_destroy(alto_stream *s);
 
+/* ---- diagnostics: per-phase timing with HIP events on the caller's stream ----
+ * Phases: 0 input-order pass (layout check, routing hash, fan checks), 1 radix sort
+ * and destination offsets, 2 node segmentation and completion, 3 group records and
+ * chunk lists, 4 payload gathers, 5 the mean gather kernel alone, 6 whole call.
+ * alto_profile_begin creates a pool of max_records event pairs; while it is active,
+ * every entry point records one pair per phase it runs (until the pool is used
+ * up). alto_profile_end waits for the recorded events, writes the summed
+ * milliseconds and the number of records per phase (arrays of nphase entries),
+ * and destroys the pool. Host-side only; not thread-safe. */
+int alto_profile_begin(int32_t max_records);
+int alto_profile_end(float *ms, int32_t *calls, int32_t nphase);
+
 #ifdef __cplusplus
 }
 #endif

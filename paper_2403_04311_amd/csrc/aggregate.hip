@@ -1,6 +1,7 @@
 // Routing (Section 4.3 of the paper) and aggregation at a pmap exit (Sections 3.3
 // and 4.3) of one batch: kernels and their orchestration.
 #include "aggregate.h"
+#include "profile.h"
 
 #include <string.h>
 
@@ -383,12 +384,16 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
               int32_t* status, hipStream_t st) {
-  k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
-  k_zero_u64<<<1, 64, 0, st>>>(b.fp_in, ALTO_MAX_LEVELS + 1);
-  k_zero_u64<<<1, 64, 0, st>>>(b.fp_nodes, ALTO_MAX_LEVELS + 1);
-  k_prep<<<grid_for(n, PREP_NT * 8, 2048), PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fhi, b.fp_in, b.ctl,
-                                                             status);
-  ALTO_LAUNCH_CHECK();
+  {
+    ProfScope ps(PH_PREP, st);
+    k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
+    k_zero_u64<<<1, 64, 0, st>>>(b.fp_in, ALTO_MAX_LEVELS + 1);
+    k_zero_u64<<<1, 64, 0, st>>>(b.fp_nodes, ALTO_MAX_LEVELS + 1);
+    k_prep<<<grid_for(n, PREP_NT * 8, 2048), PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fhi, b.fp_in,
+                                                               b.ctl, status);
+    ALTO_LAUNCH_CHECK();
+  }
+  ProfScope ps_sort(PH_SORT, st);
   SortBufs sb;
   sb.in_keys = keys;
   sb.tmp_keys = b.tmp_keys;
@@ -413,9 +418,11 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   const int d = g.depth, La = agg.level, Lm = agg.mask_level;
   int Lt, Lseg;
   agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
+  ProfScope ps_total(PH_TOTAL, st);
   int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st);
   if (rc) return rc;
   const uint32_t* perm = b.perm_used;
+  prof_begin(PH_SEGMENT, st);
 
   // fragments: levels Lseg..d-1 are contiguous in (dest, key) order
   SegJob fj;
@@ -489,6 +496,8 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     k_mask_out<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lm], Mp, b.sk, g.shift[Lm], out.mask_key, out.mask, out.cap_mask);
   }
   k_fp_compare<<<1, 1, 0, st>>>(b.fp_in, b.fp_nodes, Lt, d - 1, status);
+  prof_end(PH_SEGMENT, st);
+  prof_begin(PH_GROUPS, st);
 
   // groups
   const int64_t* Gp = b.nnodes + La;
@@ -507,6 +516,8 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, Mp, out.counts, out.tok_off,
                             out, b.scal, status);
   ALTO_LAUNCH_CHECK();
+  prof_end(PH_GROUPS, st);
+  ProfScope ps_gather(PH_GATHER, st);
   const int64_t* NCp = b.scal + 1;   // chunk count
   if (agg.op == ALTO_CONCAT_I32) {
     if (out.tok) k_concat<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, perm, p32, out.tok, out.cap_tokens);
@@ -519,8 +530,11 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     const int cpl_need = (int)cdiv(C, lpr);
     const int cpl = cpl_need >= 4 ? 4 : cpl_need;
     const int grid = GRID_CAP * 4;
-#define ALTO_MEAN_CASE(V, P) \
-  k_mean<V, P><<<grid, 256, 0, st>>>(b.chunks, NCp, perm, pf, dim, lpr, b.part, out.mean, out.cap_groups)
+#define ALTO_MEAN_CASE(V, P)                                                                                 \
+  do {                                                                                                       \
+    ProfScope ps_mean(PH_MEAN, st);                                                                          \
+    k_mean<V, P><<<grid, 256, 0, st>>>(b.chunks, NCp, perm, pf, dim, lpr, b.part, out.mean, out.cap_groups); \
+  } while (0)
     if (v4) {
       if (cpl == 1) ALTO_MEAN_CASE(4, 1);
       else if (cpl == 2) ALTO_MEAN_CASE(4, 2);
