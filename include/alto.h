@@ -174,8 +174,9 @@ int alto_stream_create(const alto_layout *layout, int32_t route_level, int32_t n
  * in alto_route, all nullable), merges them into the carried state, and emits the
  * groups this step completes, each once, with its payload computed over all of its
  * leaves in key order (count, key, dest, first_i32, fan_up, tok_off/tok or mean).
- * Emitted groups per step are at most n; emitted tokens at most max_live_leaves.
- * Workspace: alto_workspace_bytes(layout, n_max, num_dest, agg) with n_max >= n.
+ * Emitted groups per step are at most n; emitted tokens at most max_live_leaves + n.
+ * Workspace: alto_workspace_bytes(layout, max_live_leaves + n_max, num_dest, agg)
+ * with n_max >= n (the step is merged with the carried leaves).
  * Errors: LAYOUT, LATE, FANOUT, DUPLICATE, CAPACITY (state full or outputs too
  * small). A data error poisons the handle: every later step reports it again. */
 int alto_stream_step(alto_stream *s, const uint64_t *keys, const int32_t *fan, int64_t fan_ld,

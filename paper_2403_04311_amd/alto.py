@@ -72,9 +72,6 @@ def load():
     lib.alto_aggregate.restype = C.c_int
     lib.alto_aggregate.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
                                    vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp]
-    if not hasattr(lib, "alto_stream_state_bytes"):
-        _lib = lib
-        return lib
     lib.alto_stream_state_bytes.restype = C.c_size_t
     lib.alto_stream_state_bytes.argtypes = [C.POINTER(Layout), C.POINTER(Agg), i64, i64]
     lib.alto_stream_create.restype = C.c_int
@@ -262,8 +259,9 @@ class Stream:
         if nbytes == 0:
             raise AltoError(E_ARG, "alto_stream_state_bytes")
         self.state = torch.empty(int(nbytes), dtype=torch.uint8, device=device)
-        self.ws = new_workspace(lib.alto_workspace_bytes(C.byref(self.L), step_max, num_dest,
-                                                         C.byref(self.A)), device)
+        # a step merges up to max_live_leaves carried leaves with step_max new ones
+        self.ws = new_workspace(lib.alto_workspace_bytes(C.byref(self.L), max_live_leaves + step_max,
+                                                         num_dest, C.byref(self.A)), device)
         self.step_max = step_max
         self.max_live_leaves = max_live_leaves
         self.handle = C.c_void_p()
@@ -273,8 +271,10 @@ class Stream:
         _check(rc, "alto_stream_create")
 
     def step(self, keys, fan, payload_i32=None, payload_f32=None, out: Optional[GroupTensors] = None,
-             perm=None, dest_offsets=None, dest=None, status=None, stream=None):
-        n = keys.shape[0]
+             perm=None, dest_offsets=None, dest=None, status=None, stream=None, n=None):
+        n = keys.shape[0] if n is None else n
+        if n > self.step_max:
+            raise AltoError(E_ARG, "step larger than step_max")
         dev = keys.device
         if out is None:
             out = new_groups(n, self.La, self.op, self.dim,

@@ -38,6 +38,48 @@ struct GroupOut {
   int64_t* counts;
 };
 
+// Where the fragments of the sorted element array come from. A batch reads every
+// row through perm; a stream step reads either the step's inputs (row >= 0) or
+// the carried live leaves (row = -1 - live index).
+struct BatchSrc {
+  const uint32_t* perm;
+  const int32_t* p32;
+  const int32_t* fan;
+  int64_t fan_ld;
+  const float* pf;
+  int dim;
+  __device__ int64_t row(int64_t e) const { return perm[e]; }
+  __device__ int32_t p32_of(int64_t r) const { return p32 ? p32[r] : 0; }
+  __device__ int32_t fan_of(int m, int64_t r) const { return fan[(int64_t)(m - 1) * fan_ld + r]; }
+  __device__ const float* pay_of(int64_t r) const { return pf + r * (int64_t)dim; }
+};
+
+struct MergedSrc {
+  const int32_t* src;     // merged element -> step index, or -1 - live index
+  const int32_t* sp32;
+  const int32_t* sfan;
+  int64_t sfan_ld;
+  const float* spf;
+  const int32_t* lp32;
+  const int32_t* lfan;
+  int64_t lfan_ld;
+  const int32_t* lslot;
+  const float* arena;
+  int64_t arena_rows;
+  int dim;
+  __device__ int64_t row(int64_t e) const { return src[e]; }
+  __device__ int32_t p32_of(int64_t r) const { return r >= 0 ? (sp32 ? sp32[r] : 0) : lp32[-1 - r]; }
+  __device__ int32_t fan_of(int m, int64_t r) const {
+    return r >= 0 ? sfan[(int64_t)(m - 1) * sfan_ld + r] : lfan[(int64_t)(m - 1) * lfan_ld + (-1 - r)];
+  }
+  __device__ const float* pay_of(int64_t r) const {
+    if (r >= 0) return spf + r * (int64_t)dim;
+    int64_t s = lslot[-1 - r];
+    s = (s < 0 || s >= arena_rows) ? 0 : s;   // a corrupt slot after a data error stays in bounds
+    return arena + s * (int64_t)dim;
+  }
+};
+
 struct AggBufs {
   SortCtl* ctl;
   SortCtl* rctl;
@@ -74,9 +116,16 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
               int32_t* status, hipStream_t st);
+// Groups, chunk lists, counts and payload gathers over an element array already
+// segmented at level La (nodes in b.lv[La]); elements sorted by (dest, key).
+template <typename Src>
+int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const Src& src, const uint64_t* sk,
+               int64_t n_max, AggBufs& b, const int64_t* Mp, const GroupOut& out, int32_t* status, hipStream_t st);
 int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
                   const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
                   int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
                   hipStream_t st);
 void empty_outputs(const GroupOut& out, int64_t* dest_offsets, int num_dest, hipStream_t st);
 void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st);
+void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,
+                       hipStream_t st);

@@ -132,12 +132,11 @@ __global__ __launch_bounds__(256) void k_group_flags(LevelNodes L, const int64_t
   }
 }
 
+template <typename Src>
 __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int La, LevelNodes L, const int64_t* Gp,
-                                                   const uint64_t* __restrict__ sk, const uint32_t* __restrict__ perm,
-                                                   const int32_t* em, const int64_t* tokb, const int64_t* chb,
-                                                   const int64_t* pb, const int32_t* __restrict__ fan, int64_t fan_ld,
-                                                   const int32_t* __restrict__ p32, GroupOut out, Chunk* chunks,
-                                                   int chunk_rows) {
+                                                   const uint64_t* __restrict__ sk, Src src, const int32_t* em,
+                                                   const int64_t* tokb, const int64_t* chb, const int64_t* pb,
+                                                   GroupOut out) {
   const int64_t G = *Gp;
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
     const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
@@ -149,24 +148,11 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
         if (out.key) out.key[e] = gk;
         if (out.dest) out.dest[e] = (int32_t)dest_of_key(rg, k);
         if (out.count) out.count[e] = cnt;
-        const uint32_t first = perm[s];
-        if (out.first_i32 && p32) out.first_i32[e] = p32[first];
+        const int64_t first = src.row(s);
+        if (out.first_i32) out.first_i32[e] = src.p32_of(first);
         if (out.fan_up)
-          for (int l = 1; l < La; ++l) out.fan_up[(int64_t)(l - 1) * out.cap_groups + e] = fan[(int64_t)(l - 1) * fan_ld + first];
+          for (int l = 1; l < La; ++l) out.fan_up[(int64_t)(l - 1) * out.cap_groups + e] = src.fan_of(l, first);
         if (out.tok_off) out.tok_off[e] = tokb[u];
-      }
-      const int64_t nc = chb[u + 1] - chb[u];
-      for (int64_t c = 0; c < nc; ++c) {
-        Chunk ch;
-        ch.e = e;
-        ch.begin = s + (int32_t)(c * chunk_rows);
-        ch.len = (int32_t)((cnt - c * chunk_rows) < chunk_rows ? (cnt - c * chunk_rows) : chunk_rows);
-        ch.k = (int32_t)c;
-        ch.nch = (int32_t)nc;
-        ch.count = cnt;
-        ch.part = nc > 1 ? pb[u] : -1;
-        ch.out = tokb[u] + c * chunk_rows;
-        chunks[chb[u] + c] = ch;
       }
     } else {
       const int64_t p = u - em[u];
@@ -178,15 +164,45 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
   }
 }
 
-__global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks, const int64_t* nchunks,
-                                                const uint32_t* __restrict__ perm, const int32_t* __restrict__ p32,
+// One chunk descriptor per thread: the group is found by binary search over the
+// scanned chunk counts.
+__global__ __launch_bounds__(256) void k_chunks(LevelNodes L, const int64_t* Gp, const int32_t* em, const int64_t* tokb,
+                                                const int64_t* chb, const int64_t* pb, Chunk* chunks, int chunk_rows) {
+  const int64_t G = *Gp;
+  const int64_t C = chb[G];
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < C; c += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo = 0, hi = G - 1;   // last u with chb[u] <= c
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (chb[mid] <= c) lo = mid; else hi = mid - 1;
+    }
+    const int64_t u = lo;
+    const int64_t k = c - chb[u];
+    const int64_t nc = chb[u + 1] - chb[u];
+    const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
+    Chunk ch;
+    ch.e = em[u];
+    ch.begin = s + (int32_t)(k * chunk_rows);
+    ch.len = (int32_t)((cnt - k * chunk_rows) < chunk_rows ? (cnt - k * chunk_rows) : chunk_rows);
+    ch.k = (int32_t)k;
+    ch.nch = (int32_t)nc;
+    ch.count = cnt;
+    ch.part = nc > 1 ? pb[u] : -1;
+    ch.out = tokb[u] + k * chunk_rows;
+    ch.pad = 0;
+    chunks[c] = ch;
+  }
+}
+
+template <typename Src>
+__global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src src,
                                                 int32_t* tok, int64_t cap_tokens) {
   const int64_t C = *nchunks;
   for (int64_t c = blockIdx.x; c < C; c += gridDim.x) {
     const Chunk ch = chunks[c];
     for (int r = threadIdx.x; r < ch.len; r += blockDim.x) {
       const int64_t o = ch.out + r;
-      if (o < cap_tokens) tok[o] = p32[perm[ch.begin + r]];
+      if (o < cap_tokens) tok[o] = src.p32_of(src.row(ch.begin + r));
     }
   }
 }
@@ -195,9 +211,8 @@ __global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks
 // its rows sequentially, then lanes holding the same columns are combined in lane
 // order, then the waves in wave order. Groups of one chunk are finished here;
 // others leave a partial sum.
-template <int VEC, int CPL>
-__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks,
-                                              const uint32_t* __restrict__ perm, const float* __restrict__ pay,
+template <int VEC, int CPL, typename Src>
+__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src srcp,
                                               int dim, int lpr, double* part, float* mean, int64_t cap_groups) {
   constexpr int NW = 4;
   __shared__ double red[NW][64 * CPL * VEC];
@@ -214,8 +229,7 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[q][v] = 0.0;
       for (int r = w * rpw + sub; r < ch.len; r += NW * rpw) {
-        const int64_t row = perm[ch.begin + r];
-        const float* src = pay + row * (int64_t)dim;
+        const float* src = srcp.pay_of(srcp.row(ch.begin + r));
 #pragma unroll
         for (int q = 0; q < CPL; ++q) {
           const int col = col0 + cl + q * lpr;
@@ -273,6 +287,7 @@ __global__ __launch_bounds__(256) void k_mean_combine(const Chunk* __restrict__ 
     if (ch.k != 0 || ch.nch <= 1 || ch.e >= cap_groups) continue;
     for (int x = threadIdx.x; x < dim; x += blockDim.x) {
       double s = 0.0;
+#pragma unroll 8
       for (int t = 0; t < ch.nch; ++t) s += part[(ch.part + t) * (int64_t)dim + x];
       mean[ch.e * (int64_t)dim + x] = (float)(s / (double)ch.count);
     }
@@ -315,6 +330,11 @@ __global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* to
   if (tok_off && E <= out.cap_groups) tok_off[E] = T;
   if (E > out.cap_groups || P > out.cap_groups || T > out.cap_tokens || M > out.cap_mask)
     raise_status(status, ALTO_E_CAPACITY);
+}
+
+inline bool src_rows_aligned16(const BatchSrc& s) { return (reinterpret_cast<uintptr_t>(s.pf) & 15) == 0; }
+inline bool src_rows_aligned16(const MergedSrc& s) {
+  return ((reinterpret_cast<uintptr_t>(s.spf) | reinterpret_cast<uintptr_t>(s.arena)) & 15) == 0;
 }
 
 inline int grid_for(int64_t n, int nt, int cap = GRID_CAP) {
@@ -497,22 +517,32 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   }
   k_fp_compare<<<1, 1, 0, st>>>(b.fp_in, b.fp_nodes, Lt, d - 1, status);
   prof_end(PH_SEGMENT, st);
-  prof_begin(PH_GROUPS, st);
 
   // groups
+  BatchSrc src{perm, p32, fan, fan_ld, pf, agg.dim};
+  return groups_run<BatchSrc>(g, rg, agg, src, b.sk, n, b, Mp, out, status, st);
+}
+
+template <typename Src>
+int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const Src& src, const uint64_t* sk,
+               int64_t n_max, AggBufs& b, const int64_t* Mp, const GroupOut& out, int32_t* status, hipStream_t st) {
+  const int La = agg.level;
+  const int64_t n = n_max;
+  prof_begin(PH_GROUPS, st);
   const int64_t* Gp = b.nnodes + La;
   const LevelNodes& GL = b.lv[La];
   k_group_flags<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, MEAN_CHUNK_ROWS);
   k_gplus1<<<1, 1, 0, st>>>(Gp, b.scal);
   // exclusive scans over G+1 entries (entry G is zero): entry G receives the total
   const int64_t* G1 = b.scal;
-  rc = scan_exclusive<int32_t>(b.em, b.em, n + 1, G1, b.scan_i32, nullptr, st);
+  int rc = scan_exclusive<int32_t>(b.em, b.em, n + 1, G1, b.scan_i32, nullptr, st);
   if (!rc) rc = scan_exclusive<int64_t>(b.tokc, b.tokc, n + 1, G1, b.scan_i64, nullptr, st);
   if (!rc) rc = scan_exclusive<int64_t>(b.nch, b.nch, n + 1, G1, b.scan_i64, nullptr, st);
   if (!rc && agg.op == ALTO_MEAN_F32) rc = scan_exclusive<int64_t>(b.pch, b.pch, n + 1, G1, b.scan_i64, nullptr, st);
   if (rc) return rc;
-  k_group_out<<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, b.sk, perm, b.em, b.tokc, b.nch, b.pch, fan, fan_ld,
-                                                p32, out, b.chunks, MEAN_CHUNK_ROWS);
+  k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, out);
+  k_chunks<<<grid_for(n / MEAN_CHUNK_ROWS + 1, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.chunks,
+                                                                 MEAN_CHUNK_ROWS);
   k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, Mp, out.counts, out.tok_off,
                             out, b.scal, status);
   ALTO_LAUNCH_CHECK();
@@ -520,10 +550,10 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   ProfScope ps_gather(PH_GATHER, st);
   const int64_t* NCp = b.scal + 1;   // chunk count
   if (agg.op == ALTO_CONCAT_I32) {
-    if (out.tok) k_concat<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, perm, p32, out.tok, out.cap_tokens);
+    if (out.tok) k_concat<Src><<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, src, out.tok, out.cap_tokens);
   } else if (out.mean) {
     const int dim = agg.dim;
-    const bool v4 = (dim % 4 == 0) && ((reinterpret_cast<uintptr_t>(pf) & 15) == 0);
+    const bool v4 = (dim % 4 == 0) && src_rows_aligned16(src);
     const int C = v4 ? dim / 4 : dim;
     int lpr = 1;
     while (lpr < C && lpr < 64) lpr <<= 1;
@@ -533,7 +563,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
 #define ALTO_MEAN_CASE(V, P)                                                                                 \
   do {                                                                                                       \
     ProfScope ps_mean(PH_MEAN, st);                                                                          \
-    k_mean<V, P><<<grid, 256, 0, st>>>(b.chunks, NCp, perm, pf, dim, lpr, b.part, out.mean, out.cap_groups); \
+    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NCp, src, dim, lpr, b.part, out.mean, out.cap_groups); \
   } while (0)
     if (v4) {
       if (cpl == 1) ALTO_MEAN_CASE(4, 1);
@@ -552,6 +582,12 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;
 }
+
+template int groups_run<BatchSrc>(const KeyGeom&, const RouteGeom&, const alto_agg&, const BatchSrc&, const uint64_t*,
+                                  int64_t, AggBufs&, const int64_t*, const GroupOut&, int32_t*, hipStream_t);
+template int groups_run<MergedSrc>(const KeyGeom&, const RouteGeom&, const alto_agg&, const MergedSrc&,
+                                   const uint64_t*, int64_t, AggBufs&, const int64_t*, const GroupOut&, int32_t*,
+                                   hipStream_t);
 
 namespace {
 __global__ void k_empty(GroupOut out, int64_t* offs, int num_dest) {
@@ -576,4 +612,9 @@ __global__ void k_zero_offsets(int64_t* offs, int num_dest) {
 
 void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st) {
   if (dest_offsets) k_zero_offsets<<<1, 256, 0, st>>>(dest_offsets, num_dest);
+}
+
+void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,
+                       hipStream_t st) {
+  k_fp_compare<<<1, 1, 0, st>>>(fp_in, fp_nodes, flo, fhi, status);
 }

@@ -34,6 +34,9 @@ struct SegJob {
   const int32_t* fan;       // fan source, level-major: level m at fan[(m - fan_base) * fan_ld + row]
   int64_t fan_ld;
   int32_t fan_base;
+  const int32_t* src;       // stream steps: element -> step row (>= 0) or -1 - live row;
+  const int32_t* fan2;      // the live rows' fans (same level base), used when src is set
+  int64_t fan2_ld;
   const uint8_t* elem_ok;   // records: ok flag per row (null for fragments)
   int32_t chain_check;      // records: compare adjacent carriers' fans (exact)
   int32_t check_dup;        // fragments: equal adjacent keys are duplicates

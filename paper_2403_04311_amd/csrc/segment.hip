@@ -23,6 +23,11 @@ __device__ inline int64_t nelem(const SegJob& j) { return j.n_dev ? *j.n_dev : j
 __device__ inline int es_of(const KeyGeom& g, const SegJob& j, int m) { return g.shift[m] - g.shift[j.elem_level]; }
 
 __device__ inline int32_t fan_at(const SegJob& j, int m, int64_t e) {
+  if (j.src) {
+    const int64_t r = j.src[e];
+    return r >= 0 ? j.fan[(int64_t)(m - j.fan_base) * j.fan_ld + r]
+                  : j.fan2[(int64_t)(m - j.fan_base) * j.fan2_ld + (-1 - r)];
+  }
   return j.fan[(int64_t)(m - j.fan_base) * j.fan_ld + j.idx[e]];
 }
 

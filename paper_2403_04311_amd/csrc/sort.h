@@ -9,6 +9,7 @@
 #define SORT_BUCKETS 256
 #define SORT_MAX_PASSES 12
 #define SCAN_MAX_BLOCKS 1023
+#define SORT_SMALL_MAX 4096
 
 enum { SORT_BUF_INPUT = 0, SORT_BUF_TMP = 1, SORT_BUF_FINAL = 2 };
 

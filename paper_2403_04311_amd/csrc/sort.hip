@@ -36,6 +36,9 @@ __global__ __launch_bounds__(256) void k_sort_reduce(const uint64_t* __restrict_
   const int64_t n = load_n(n_host, n_dev);
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
+  // waves with no element skip the atomics (they would only add contention)
+  const int64_t wave0 = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~(ALTO_WAVE - 1));
+  if (wave0 >= n) return;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     uint64_t k = keys[i];
     kor |= k;
@@ -313,6 +316,155 @@ __global__ __launch_bounds__(SCAN_NT) void k_scan_apply(const T* in, T* out, int
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// whole sort in one workgroup for n <= SORT_SMALL_MAX: keys stay in LDS between
+// passes; the digit windows are planned in the block from its own OR/AND.
+// ---------------------------------------------------------------------------
+constexpr int SM_NT = 1024;
+constexpr int SM_IT = SORT_SMALL_MAX / SM_NT;
+constexpr int SM_NW = SM_NT / ALTO_WAVE;
+
+__global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
+                                                      int max_key_windows, int max_dest_windows) {
+  __shared__ uint64_t s_key[SORT_SMALL_MAX];
+  __shared__ uint32_t s_val[SORT_SMALL_MAX];
+  __shared__ uint16_t s_cnt[SM_NW][SORT_BUCKETS];
+  __shared__ uint32_t s_base[SORT_BUCKETS];
+  __shared__ uint32_t s_wsum[SM_NW];
+  __shared__ uint64_t s_or[SM_NW], s_and[SM_NW];
+  __shared__ uint32_t s_dor[SM_NW], s_dand[SM_NW];
+  __shared__ int s_np;
+  __shared__ int s_lo[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
+  const int64_t n = load_n(n_host, n_dev);
+  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
+  uint64_t kor = 0, kand = ~0ull;
+  uint32_t dor = 0, dand = ~0u;
+  for (int j = 0; j < SM_IT; ++j) {
+    const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    if (e < n) {
+      const uint64_t k = b.in_keys[e];
+      s_key[e] = k;
+      s_val[e] = (uint32_t)e;
+      kor |= k;
+      kand &= k;
+      const uint32_t d = dest_of_key(rg, k);
+      dor |= d;
+      dand &= d;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kor |= __shfl_xor(kor, o);
+    kand &= __shfl_xor(kand, o);
+    dor |= __shfl_xor(dor, o);
+    dand &= __shfl_xor(dand, o);
+  }
+  if (lane == 0) {
+    s_or[w] = kor;
+    s_and[w] = kand;
+    s_dor[w] = dor;
+    s_dand[w] = dand;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t a = 0, c = ~0ull;
+    uint32_t da = 0, dc = ~0u;
+    for (int i = 0; i < SM_NW; ++i) {
+      a |= s_or[i];
+      c &= s_and[i];
+      da |= s_dor[i];
+      dc &= s_dand[i];
+    }
+    int np = 0;
+    uint64_t vk = a ^ c;
+    while (vk && np < max_key_windows) {
+      const int lo = __builtin_ctzll(vk);
+      s_lo[np] = lo;
+      s_fd[np] = 0;
+      ++np;
+      vk = (lo + SORT_RADIX >= 64) ? 0ull : (vk & ~((1ull << (lo + SORT_RADIX)) - 1ull));
+    }
+    uint32_t vd = da ^ dc;
+    const int nk = np;
+    while (vd && np < nk + max_dest_windows) {
+      const int lo = __builtin_ctz(vd);
+      s_lo[np] = lo;
+      s_fd[np] = 1;
+      ++np;
+      vd = (lo + SORT_RADIX >= 32) ? 0u : (vd & ~((1u << (lo + SORT_RADIX)) - 1u));
+    }
+    s_np = np;
+  }
+  __syncthreads();
+  const int np = s_np;
+  for (int p = 0; p < np; ++p) {
+    SortPass ps;
+    ps.from_dest = s_fd[p];
+    ps.lo = s_lo[p];
+    for (int i = threadIdx.x; i < SM_NW * SORT_BUCKETS; i += SM_NT) (&s_cnt[0][0])[i] = 0;
+    uint64_t key[SM_IT];
+    uint32_t val[SM_IT], dig[SM_IT], off[SM_IT];
+#pragma unroll
+    for (int j = 0; j < SM_IT; ++j) {
+      const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+      const bool valid = e < n;
+      key[j] = valid ? s_key[e] : 0ull;
+      val[j] = valid ? s_val[e] : 0u;
+      dig[j] = valid ? digit_of(ps, rg, key[j]) : 0u;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SM_IT; ++j) {
+      const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+      const bool valid = e < n;
+      const uint64_t peers = match_digit(dig[j], valid);
+      const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
+      uint32_t old = 0;
+      if (valid && lane == leader) {
+        old = s_cnt[w][dig[j]];
+        s_cnt[w][dig[j]] = (uint16_t)(old + (uint32_t)__popcll(peers));
+      }
+      old = __shfl(old, leader);
+      off[j] = old + (uint32_t)__popcll(peers & lanemask_lt());
+    }
+    __syncthreads();
+    if (threadIdx.x < SORT_BUCKETS) {
+      const int d = threadIdx.x;
+      uint32_t run = 0;
+      for (int ww = 0; ww < SM_NW; ++ww) {
+        const uint32_t c = s_cnt[ww][d];
+        s_cnt[ww][d] = (uint16_t)run;
+        run += c;
+      }
+      s_base[d] = run;
+    }
+    __syncthreads();
+    {
+      // every thread of the block takes part (the scan holds barriers)
+      uint32_t tot;
+      const uint32_t v = threadIdx.x < SORT_BUCKETS ? s_base[threadIdx.x] : 0u;
+      const uint32_t ex = block_excl_scan<uint32_t, SM_NT>(v, s_wsum, &tot);
+      if (threadIdx.x < SORT_BUCKETS) s_base[threadIdx.x] = ex;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SM_IT; ++j) {
+      const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+      if (e < n) {
+        const uint32_t pos = s_base[dig[j]] + (uint32_t)s_cnt[w][dig[j]] + off[j];
+        s_key[pos] = key[j];
+        s_val[pos] = val[j];
+      }
+    }
+    __syncthreads();
+  }
+  for (int e = threadIdx.x; e < n; e += SM_NT) {
+    b.out_keys[e] = s_key[e];
+    b.out_vals[e] = s_val[e];
+  }
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -347,6 +499,11 @@ int sort_max_dest_windows(const RouteGeom& rg) {
 
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
                bool ctl_has_reduction, hipStream_t st) {
+  if (n_max <= SORT_SMALL_MAX) {
+    k_sort_small<<<1, 1024, 0, st>>>(b, n_max, n_dev, rg, sort_max_key_windows(key_bits), sort_max_dest_windows(rg));
+    ALTO_LAUNCH_CHECK();
+    return ALTO_OK;
+  }
   const int nblocks = sort_hist_blocks(n_max);
   const int grid_r = (int)(n_max < 1 ? 1 : (cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048));
   if (!ctl_has_reduction) {

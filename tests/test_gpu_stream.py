@@ -1,0 +1,262 @@
+"""GPU parity of the stream path (alto_stream_*) against the oracle's Stream, step by
+step, through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import alto_oracle as O
+from paper_2403_04311_amd import alto, workloads as W
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pf, cuts, max_live=4096, max_groups=1 << 16,
+              step_max=None):
+    """Runs a stream on the GPU; returns per-step dicts of numpy outputs and statuses."""
+    step_max = step_max or max(int(np.diff(cuts).max()), 1)
+    s = alto.Stream(bits, Lr, D, La, op, dim, max_live_leaves=max_live, max_groups=max_groups,
+                    step_max=step_max)
+    dk = U.to_dev(keys.astype(np.uint64).view(np.int64))
+    dfan = U.to_dev(fan.astype(np.int32))
+    d32 = U.to_dev(p32.astype(np.int32)) if p32 is not None else None
+    dpf = U.to_dev(pf.astype(np.float32)) if pf is not None else None
+    out = []
+    cap_g = step_max
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        n = b - a
+        g = alto.new_groups(cap_g, La, op, dim, cap_tokens=max_live + step_max if op == "concat" else 0,
+                            device="cuda", with_first=p32 is not None)
+        perm = torch.empty(max(n, 1), dtype=torch.int32, device="cuda")
+        offs = torch.empty(D + 1, dtype=torch.int64, device="cuda")
+        dest = torch.empty(max(n, 1), dtype=torch.int32, device="cuda")
+        st = alto.new_status()
+        s.step(dk[a:b], dfan[:, a:b], None if d32 is None else d32[a:b], None if dpf is None else dpf[a:b],
+               out=g, perm=perm, dest_offsets=offs, dest=dest, status=st, n=n)
+        torch.cuda.synchronize()
+        E, T, _, _ = [int(x) for x in g.counts.cpu()]
+        r = {"status": int(st.item()), "E": E}
+        if r["status"] == 0:
+            r["perm"] = perm[:n].cpu().numpy()
+            r["offs"] = offs.cpu().numpy()
+            r["dest"] = dest[:n].cpu().numpy()
+            r["key"] = g.key[:E].cpu().numpy().view(np.uint64)
+            r["gdest"] = g.dest[:E].cpu().numpy()
+            r["count"] = g.count[:E].cpu().numpy()
+            if g.first_i32 is not None:
+                r["first"] = g.first_i32[:E].cpu().numpy()
+            fu = g.fan_up.cpu().numpy()
+            r["fan_up"] = (np.stack([fu[(l - 1) * cap_g:(l - 1) * cap_g + E] for l in range(1, La)])
+                           if La > 1 else None)
+            if op == "concat":
+                r["tok_off"] = g.tok_off[:E + 1].cpu().numpy()
+                r["tok"] = g.tok[:T].cpu().numpy()
+            else:
+                r["mean"] = g.mean[:E].cpu().numpy()
+        out.append(r)
+    pend, pst = s.pending(cap=max_live)
+    torch.cuda.synchronize()
+    P = int(pend.counts[3])
+    pres = {"status": int(pst.item()), "key": pend.pend_key[:P].cpu().numpy().view(np.uint64),
+            "count": pend.pend_count[:P].cpu().numpy()}
+    s.close()
+    return out, pres
+
+
+def oracle_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pf, cuts):
+    s = O.Stream(bits, Lr, D, La, op, dim)
+    res = []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        try:
+            r = s.step(keys[a:b], fan[:, a:b], None if p32 is None else p32[a:b],
+                       None if pf is None else pf[a:b])
+            res.append((O.OK, r))
+        except O.OracleError as e:
+            res.append((e.code, None))
+    pend = s.pending() if s.error == 0 else None
+    return res, pend
+
+
+def compare_steps(gpu, ora, op, La):
+    (gsteps, gpend), (osteps, opend) = gpu, ora
+    assert len(gsteps) == len(osteps)
+    for i, (g, (code, o)) in enumerate(zip(gsteps, osteps)):
+        assert g["status"] == code, (i, g["status"], code)
+        if code != O.OK:
+            continue
+        assert np.array_equal(g["perm"], o.route.perm), i
+        assert np.array_equal(g["offs"], o.route.dest_offsets), i
+        assert np.array_equal(g["dest"], o.route.dest), i
+        gr = o.groups
+        assert np.array_equal(g["key"], gr.key), i
+        assert np.array_equal(g["gdest"], gr.dest), i
+        assert np.array_equal(g["count"], gr.count), i
+        if "first" in g and gr.first_i32 is not None and len(gr.key):
+            assert np.array_equal(g["first"], gr.first_i32), i
+        if La > 1 and len(gr.key):
+            assert np.array_equal(g["fan_up"], gr.fan_up), i
+        if op == "concat":
+            assert np.array_equal(g["tok_off"], gr.tok_off), i
+            assert np.array_equal(g["tok"], gr.tok), i
+        else:
+            U.assert_mean_close(g["mean"], gr.mean)
+    if opend is not None:
+        assert gpend["status"] == O.OK
+        assert np.array_equal(gpend["key"], opend[0])
+        assert np.array_equal(gpend["count"], opend[1])
+
+
+def _tiny(seed, depth, bits, mf, roots, drop, dim):
+    path, fan = W.random_tree(seed, depth, roots, mf, bits)
+    if drop:
+        path, fan, _ = W.drop_leaves(path, fan, drop, seed + 1)
+    rng = np.random.default_rng(seed + 2)
+    n = path.shape[1]
+    p32 = rng.integers(0, 1 << 30, size=n).astype(np.int32)
+    pf = rng.standard_normal((n, dim)).astype(np.float32)
+    (path, fan, p32, pft), _ = W.permute([path, fan, p32, pf.T], seed + 3)
+    return O.pack_keys(path, bits), fan, p32, np.ascontiguousarray(pft.T)
+
+
+STREAM_CASES = [
+    # depth, bits, max_fan, roots, La, Lr, D, drop, dim, nsteps
+    (3, (10, 3, 4), (5, 9), 12, 2, 1, 4, 0.0, 4, 7),
+    (4, (31, 2, 3, 4), (4, 8, 16), 30, 3, 2, 9, 0.05, 8, 11),
+    (4, (31, 2, 3, 4), (3, 4, 6), 25, 2, 2, 64, 0.0, 16, 5),
+    (5, (31, 3, 2, 3, 8), (4, 3, 5, 20), 10, 4, 2, 32, 0.02, 768, 9),
+    (5, (31, 3, 2, 3, 8), (3, 3, 5, 10), 10, 3, 1, 7, 0.0, 12, 13),
+]
+
+
+@pytest.mark.parametrize("case", range(len(STREAM_CASES)))
+@pytest.mark.parametrize("op", ["concat", "mean"])
+def test_stream_parity(case, op):
+    depth, bits, mf, roots, La, Lr, D, drop, dim, nsteps = STREAM_CASES[case]
+    keys, fan, p32, pf = _tiny(500 + case, depth, bits, mf, roots, drop, dim)
+    n = len(keys)
+    rng = np.random.default_rng(case)
+    cuts = [0] + sorted(rng.choice(np.arange(1, n), size=nsteps - 1, replace=False).tolist()) + [n]
+    pfa = pf if op == "mean" else None
+    gpu = gpu_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pfa, cuts)
+    ora = oracle_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pfa, cuts)
+    compare_steps(gpu, ora, op, La)
+
+
+def test_config3_token_stream_full():
+    w = W.config3("cpu")
+    path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
+    keys = O.pack_keys(path, w.bits)
+    cuts = list(range(0, w.n, w.step)) + [w.n]
+    gpu = gpu_steps(w.bits, w.route_level, w.num_dest, w.agg_level, "concat", 1, keys, fan, tok, None,
+                    cuts, max_live=1 << 14, max_groups=1 << 15, step_max=w.step)
+    ora = oracle_steps(w.bits, w.route_level, w.num_dest, w.agg_level, "concat", 1, keys, fan, tok, None,
+                       cuts)
+    compare_steps(gpu, ora, "concat", w.agg_level)
+    # closed form: a sentence is emitted in the step of its last token
+    gk = O.prefix(keys, w.bits, 2)
+    want = {}
+    for i, k in enumerate(gk):
+        want[int(k)] = i // w.step
+    got = {}
+    for si, r in enumerate(gpu[0]):
+        for k in r["key"]:
+            got[int(k)] = si
+    assert got == want
+
+
+def _windowed_factool(seed, queries, W_frag, step):
+    """A small continuous FacTool-shaped stream (same construction as the 10,000-step
+    workload, fewer queries)."""
+    rng = np.random.default_rng(seed)
+    roots = W.distinct_ids(rng, queries)
+    fans = W.factool_fans(rng, roots)
+    path, fan = W.expand_tree(fans, roots)
+    docid = W.doc_ids_per_sentence(rng, fans)
+    q = W._leaves_per_root(fans)
+    qoff = np.cumsum(q) - q
+    pos = np.repeat(qoff, q) + rng.random(path.shape[1]) * W_frag
+    order = np.argsort(pos, kind="stable")
+    pf = rng.standard_normal((path.shape[1], 768)).astype(np.float32)
+    return path[:, order], fan[:, order], docid[order], pf[order]
+
+
+def test_factool_stream_two_stages():
+    path, fan, docid, pf = _windowed_factool(7, 24, 3000, 256)
+    bits = (31, 3, 2, 3, 8)
+    keys = O.pack_keys(path, bits)
+    n = len(keys)
+    cuts = list(range(0, n, 256)) + [n]
+    cuts = sorted(set(cuts))
+    gA = gpu_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, max_live=8192,
+                   max_groups=1 << 14, step_max=256)
+    oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts)
+    compare_steps(gA, oA, "mean", 4)
+    # stage B consumes stage A's emitted records step by step
+    bB = W.CONFIG2_STAGE_B["bits"]
+    kB, fB, pB, cB = [], [], [], [0]
+    for r in gA[0]:
+        kB.append(r["key"])
+        fB.append(r["fan_up"])
+        pB.append(r["first"])
+        cB.append(cB[-1] + len(r["key"]))
+    kB = np.concatenate(kB)
+    fB = np.concatenate(fB, axis=1)
+    pB = np.concatenate(pB)
+    gB = gpu_steps(bB, 2, 32, 2, "concat", 1, kB, fB, pB, None, cB, max_live=8192, max_groups=1 << 14,
+                   step_max=max(int(np.diff(cB).max()), 1))
+    oB = oracle_steps(bB, 2, 32, 2, "concat", 1, kB, fB, pB, None, cB)
+    compare_steps(gB, oB, "concat", 2)
+
+
+def _cross_step_case():
+    bits = (6, 3, 4)
+    path, fan = W.random_tree(41, 3, 6, (4, 9), bits)
+    keys = O.pack_keys(path, bits)
+    return bits, keys, fan, np.arange(len(keys), dtype=np.int32)
+
+
+@pytest.mark.parametrize("kind", ["late", "dup_across", "fan_across", "live_capacity"])
+def test_stream_errors_and_poison(kind):
+    bits, keys, fan, p32 = _cross_step_case()
+    n = len(keys)
+    gk = O.prefix(keys, bits, 2)
+    vals, cnt = np.unique(gk, return_counts=True)
+    big = vals[np.argmax(cnt)]                      # a group with several leaves
+    assert cnt.max() >= 2
+    first_group = gk == big
+    idx_g = np.nonzero(first_group)[0]
+    rest = np.nonzero(~first_group)[0]
+    max_live = 4096
+    if kind == "late":
+        # whole first group, then one of its leaves again, then anything
+        order = np.concatenate([idx_g, idx_g[:1], rest])
+        cuts = [0, len(idx_g), len(idx_g) + 1, len(order)]
+    elif kind == "dup_across":
+        # part of a group, then the same leaf again while the group is open
+        if len(idx_g) < 2:
+            pytest.skip("group too small")
+        order = np.concatenate([idx_g[:1], idx_g[:1], idx_g[1:], rest])
+        cuts = [0, 1, 2, len(order)]
+    elif kind == "fan_across":
+        if len(idx_g) < 2:
+            pytest.skip("group too small")
+        fan = fan.copy()
+        fan[1, idx_g[1]] += 1
+        order = np.concatenate([idx_g[:1], idx_g[1:], rest])
+        cuts = [0, 1, len(idx_g), len(order)]
+    else:
+        max_live = 4
+        order = np.random.default_rng(3).permutation(n)
+        cuts = [0, n // 2, n]
+    k, f, p = keys[order], fan[:, order], p32[order]
+    gpu = gpu_steps(bits, 1, 5, 2, "concat", 1, k, f, p, None, cuts, max_live=max_live, max_groups=1024)
+    ora = oracle_steps(bits, 1, 5, 2, "concat", 1, k, f, p, None, cuts)
+    codes_g = [r["status"] for r in gpu[0]]
+    codes_o = [c for c, _ in ora[0]]
+    if kind == "live_capacity":
+        assert O.E_CAPACITY in codes_g
+        first = codes_g.index(O.E_CAPACITY)
+        assert all(c == O.E_CAPACITY for c in codes_g[first:])       # poisoned
+    else:
+        assert codes_g == codes_o, (codes_g, codes_o)
+        assert codes_o[-1] != O.OK                                    # poisoned after the error
