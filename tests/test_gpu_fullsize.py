@@ -1,0 +1,185 @@
+"""Parity at the full workload sizes, in the launch configuration the benchmark
+times. Outputs the oracle can compute one by one are compared element by element;
+the rest through properties that fix them uniquely (a permutation ordered by
+(dest, key) is unique when keys are unique) and closed forms (in a stream a group
+is emitted in the step holding its last leaf)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import alto_oracle as O
+from paper_2403_04311_amd import alto, workloads as W
+from tests import gpu_util as U
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def log(msg):
+    print(f"[fullsize] {msg}", flush=True)
+
+
+def test_zipf_64M_mean_mask():
+    log("config: zipf depth-6, 2^26 fragments, 128-d mean at level 4, mask at level 2")
+    w = W.config5("cuda")
+    n = w.n
+    keys, st = alto.pack_keys(w.path, w.bits)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    hkeys = O.pack_keys(w.path.cpu().numpy(), w.bits)
+    assert np.array_equal(keys.cpu().numpy().view(np.uint64), hkeys)
+    w.path = None
+    perm = torch.empty(n, dtype=torch.int32, device="cuda")
+    offs = torch.empty(w.num_dest + 1, dtype=torch.int64, device="cuda")
+    dest = torch.empty(n, dtype=torch.int32, device="cuda")
+    out = alto.new_groups(1 << 16, w.agg_level, "mean", w.dim, cap_mask=1 << 16, with_first=False)
+    _, _, _, out, st = alto.aggregate(keys, w.fan, w.bits, w.agg_level, "mean", w.dim, w.mask_level,
+                                      w.route_level, w.num_dest, None, w.payload_f32, perm=perm,
+                                      dest_offsets=offs, dest=dest, out=out, n=n)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    log("gpu done; checking routing")
+    odest = O.route_dest(hkeys, w.bits, w.route_level, w.num_dest)
+    assert np.array_equal(dest.cpu().numpy(), odest)
+    assert np.array_equal(offs.cpu().numpy(),
+                          np.concatenate([[0], np.cumsum(np.bincount(odest, minlength=w.num_dest))]))
+    p = perm.cpu().numpy()
+    assert (np.bincount(p, minlength=n) == 1).all()                      # a permutation
+    d, k = odest[p], hkeys[p]
+    assert ((d[1:] > d[:-1]) | ((d[1:] == d[:-1]) & (k[1:] > k[:-1]))).all()   # strictly by (dest, key)
+    log("checking groups")
+    E, T, M, P = [int(x) for x in out.counts.cpu()]
+    gk = O.prefix(hkeys, w.bits, w.agg_level)
+    nodes, cnt = np.unique(gk, return_counts=True)
+    gd = O.route_dest(nodes << np.uint64(O.shift_below(w.bits, w.agg_level)), w.bits, w.route_level,
+                      w.num_dest)
+    o = np.lexsort((nodes, gd))
+    assert (E, P) == (len(nodes), 0)
+    assert np.array_equal(out.key[:E].cpu().numpy().view(np.uint64), nodes[o])
+    assert np.array_equal(out.count[:E].cpu().numpy(), cnt[o])
+    assert np.array_equal(out.dest[:E].cpu().numpy(), gd[o])
+    m2 = np.unique(O.prefix(hkeys, w.bits, w.mask_level))
+    assert M == len(m2)
+    assert np.array_equal(out.mask_key[:M].cpu().numpy().view(np.uint64), m2)
+    assert (out.mask[:M].cpu().numpy() == 1).all()
+    log("checking sampled means")
+    rng = np.random.default_rng(5)
+    order_groups = nodes[o]
+    picks = sorted(set([int(np.argmax(cnt[o])), int(np.argmin(cnt[o]))] +
+                       rng.choice(E, size=10, replace=False).tolist()))
+    gmean = out.mean[:E].cpu().numpy()
+    for i in picks:
+        rows = np.nonzero(gk == order_groups[i])[0]
+        x = w.payload_f32[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+        ref = (x.sum(axis=0) / len(rows)).astype(np.float32)
+        U.assert_mean_close(gmean[i:i + 1], ref[None])
+
+
+def test_factool_batch_two_stages():
+    log("config: FacTool depth-5, 1,024 queries, 768-d mean per doc, then doc-id concat per claim")
+    w = W.config2("cuda")
+    path, fan, docid = w.path.cpu().numpy(), w.fan.cpu().numpy(), w.payload_i32.cpu().numpy()
+    keys = O.pack_keys(path, w.bits)
+    pf = w.payload_f32.cpu().numpy()
+    code, rt, g = U.oracle_aggregate(keys, fan, w.bits, 4, "mean", 768, 0, 2, 32, docid, pf)
+    assert code == O.OK
+    res = U.run_aggregate(keys, fan, w.bits, 4, "mean", 768, 0, 2, 32, docid, pf)
+    assert res["status"] == O.OK
+    U.compare(res, rt, g, "mean", 0, 4)
+    sb = W.CONFIG2_STAGE_B
+    kB, fB, pB = res["key"], res["fan_up"], res["first_i32"]
+    code, rtB, gB = U.oracle_aggregate(kB, fB, sb["bits"], 2, "concat", 1, 0, 2, 32, pB)
+    assert code == O.OK
+    resB = U.run_aggregate(kB, fB, sb["bits"], 2, "concat", 1, 0, 2, 32, pB)
+    assert resB["status"] == O.OK
+    U.compare(resB, rtB, gB, "concat", 0, 2)
+
+
+def test_factool_stream_10000_steps():
+    log("config: FacTool windowed stream, 10,000 steps x 4,096 fragments, two chained stages")
+    w = W.config4("cuda")
+    log(f"generated: window {w.info['window']:.0f}, long-lived fraction {w.info['calibrated_frac']:.3f}")
+    step, steps = w.step, w.info["steps"]
+    ring = w.payload_f32
+    ring_rows = ring.shape[0]
+    keys_d, st = alto.pack_keys(w.path, w.bits)
+    torch.cuda.synchronize()
+    hkeys = keys_d.cpu().numpy().view(np.uint64)
+    hfan = w.fan.cpu().numpy()
+    hdoc = w.payload_i32.cpu().numpy()
+    assert np.array_equal(hkeys, O.pack_keys(w.path.cpu().numpy(), w.bits))
+    sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22, step_max=step)
+    sbB = W.CONFIG2_STAGE_B
+    sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
+                     step_max=step)
+    # expected: a document is emitted in the step of its last sentence, if all arrived
+    gk = O.prefix(hkeys, w.bits, 4)
+    stepof = np.arange(w.n) // step
+    o = np.argsort(gk, kind="stable")
+    docs, first_idx, cnt = np.unique(gk[o], return_index=True, return_counts=True)
+    last_step = np.maximum.reduceat(stepof[o], first_idx)
+    declared = hfan[3][o][first_idx]
+    complete = cnt == declared
+    want_step = dict(zip(docs[complete].tolist(), last_step[complete].tolist()))
+    rng = np.random.default_rng(9)
+    sample = set(rng.choice(docs[complete], size=12, replace=False).tolist())
+    got_step, got_first, got_count, got_mean = {}, {}, {}, {}
+    recB_keys, recB_step = [], []
+    claims_got = {}
+    gA = alto.new_groups(step, 4, "mean", 768, device="cuda")
+    gB = alto.new_groups(step, 2, "concat", 1, cap_tokens=(1 << 16) + step, device="cuda")
+    stA, stB = alto.new_status(), alto.new_status()
+    for s in range(steps):
+        a, b = s * step, (s + 1) * step
+        r0 = (s * step) % ring_rows
+        stA.zero_()
+        sA.step(keys_d[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gA, status=stA)
+        torch.cuda.synchronize()
+        assert int(stA.item()) == 0, s
+        E = int(gA.counts[0])
+        stB.zero_()
+        sB.step(gA.key[:E], gA.fan_up.view(3, -1)[:, :E], gA.first_i32[:E], None, out=gB, status=stB, n=E)
+        torch.cuda.synchronize()
+        assert int(stB.item()) == 0, s
+        ks = gA.key[:E].cpu().numpy().view(np.uint64)
+        for i, kk in enumerate(ks.tolist()):
+            got_step[kk] = s
+            if kk in sample:
+                got_mean[kk] = gA.mean[i].cpu().numpy()
+        got_first.update(zip(ks.tolist(), gA.first_i32[:E].cpu().numpy().tolist()))
+        got_count.update(zip(ks.tolist(), gA.count[:E].cpu().numpy().tolist()))
+        EB, TB = int(gB.counts[0]), int(gB.counts[1])
+        kb = gB.key[:EB].cpu().numpy().view(np.uint64)
+        toff = gB.tok_off[:EB + 1].cpu().numpy()
+        tok = gB.tok[:TB].cpu().numpy()
+        for i, kk in enumerate(kb.tolist()):
+            claims_got[kk] = (s, tok[toff[i]:toff[i + 1]].tolist())
+        if s % 1000 == 0:
+            log(f"step {s}: {E} documents, {EB} claims emitted")
+    log("checking documents")
+    assert got_step == want_step
+    doc_first = dict(zip(docs.tolist(), hdoc[o][first_idx].tolist()))
+    assert all(got_first[k] == doc_first[k] for k in got_step)
+    assert all(got_count[k] == int(c) for k, c in zip(docs[complete].tolist(), cnt[complete].tolist()))
+    for kk in sample:
+        rows = np.nonzero(gk == np.uint64(kk))[0]
+        x = ring[torch.from_numpy(rows % ring_rows).cuda()].cpu().numpy().astype(np.float64)
+        U.assert_mean_close(got_mean[kk][None], (x.sum(axis=0) / len(rows)).astype(np.float32)[None])
+    log("checking claims")
+    # a claim is emitted once all its documents were emitted, in the step of the last one
+    ck = O.prefix(docs, (31, 3, 2, 3), 2)
+    dfan = hfan[:, o][:, first_idx]            # fans of each document's first sentence
+    nsq = dfan[1]                               # search queries per claim
+    want_claims = {}
+    for c in np.unique(ck):
+        sel = np.nonzero(ck == c)[0]
+        if not complete[sel].all() or len(sel) != int(nsq[sel[0]]) * 5:
+            continue
+        want_claims[int(c)] = (int(last_step[sel].max()), [doc_first[int(d)] for d in docs[sel]])
+    assert claims_got == want_claims
+    pend, pst = sA.pending(cap=1 << 17)
+    torch.cuda.synchronize()
+    P = int(pend.counts[3])
+    pk = pend.pend_key[:P].cpu().numpy().view(np.uint64)
+    assert set(pk.tolist()) == set(docs[~complete].tolist())
+    sA.close()
+    sB.close()
