@@ -4,7 +4,7 @@
 #include "segment.h"
 #include "sort.h"
 
-#define MEAN_CHUNK_ROWS 1024
+#define MEAN_CHUNK_ROWS 4096
 
 // One unit of gather work: rows [begin, begin+len) of the sorted fragments, the
 // k-th of nch chunks of emitted group e.
@@ -80,7 +80,18 @@ struct MergedSrc {
   }
 };
 
+// Per-block record of the input-order pass.
+struct PrepPartial {
+  uint64_t kor, kand;
+  uint32_t dor, dand;
+  uint32_t flags;   // 1 layout, 2 fan, 4 flow set full
+  uint32_t pad;
+  uint64_t fp[ALTO_MAX_LEVELS];
+};
+
 struct AggBufs {
+  PrepPartial* prep_part;   // per-block records of the input-order pass
+  FlowBufs fl;          // flows of the route level (packed sort); hcap == 0 when unused
   SortCtl* ctl;
   SortCtl* rctl;
   uint64_t* fp_in;
@@ -115,7 +126,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
                   AggBufs& b);
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st);
+              int32_t* status, hipStream_t st, bool offsets_later = false);
 // Groups, chunk lists, counts and payload gathers over an element array already
 // segmented at level La (nodes in b.lv[La]); elements sorted by (dest, key).
 template <typename Src>

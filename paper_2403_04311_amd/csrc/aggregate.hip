@@ -13,30 +13,60 @@ constexpr int GRID_CAP = 4096;
 __device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : h; }
 
 // Input order, one pass: layout check, destination, OR/AND of keys and
-// destinations for the sort, per-fragment fan-out checks, and the fragment side of
-// the fan fingerprint.
+// destinations for the sort, flow-set inserts, per-fragment fan-out checks, and the
+// fragment side of the fan fingerprint. NL = number of count levels read (flo ..
+// flo + NL - 1); the per-level sums stay in registers. Each thread keeps PU elements
+// in flight; each block leaves one record of partial results (no contended atomics).
+constexpr int PU = 4;
+constexpr int PREP_GRID = 2048;
+
+template <int NL>
 __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
                                                   RouteGeom rg, int32_t* dest, const int32_t* __restrict__ fan,
-                                                  int64_t fan_ld, int flo, int fhi, uint64_t* fp_in, SortCtl* ctl,
-                                                  int32_t* status) {
+                                                  int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part) {
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
-  uint64_t fp[ALTO_MAX_LEVELS + 1];
-  for (int m = flo; m <= fhi; ++m) fp[m] = 0;
-  bool bad_layout = false, bad_fan = false;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const uint64_t k = keys[i];
-    bad_layout |= (k >> g.total) != 0;
-    const uint32_t d = dest_of_key(rg, k);
-    if (dest) dest[i] = (int32_t)d;
-    kor |= k;
-    kand &= k;
-    dor |= d;
-    dand &= d;
-    for (int m = flo; m <= fhi; ++m) {
-      const int32_t f = fan[(int64_t)(m - 1) * fan_ld + i];
-      bad_fan |= (f < 1) || ((int64_t)key_tag(g, k, m + 1) >= (int64_t)f);
-      fp[m] += fan_term(m, key_prefix(k, g.shift[m]), (uint32_t)f);
+  uint64_t fp[NL > 0 ? NL : 1];
+  int sh[NL > 0 ? NL : 1], shc[NL > 0 ? NL : 1];
+  uint32_t tm[NL > 0 ? NL : 1];
+#pragma unroll
+  for (int q = 0; q < NL; ++q) {
+    fp[q] = 0;
+    sh[q] = g.shift[flo + q];
+    shc[q] = g.shift[flo + q + 1];
+    tm[q] = g.tagmask[flo + q + 1];
+  }
+  bool bad_layout = false, bad_fan = false, flow_full = false;
+  const int total = g.total;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += stride * PU) {
+    uint64_t k[PU];
+    int32_t f[PU][NL > 0 ? NL : 1];
+#pragma unroll
+    for (int u = 0; u < PU; ++u) {
+      const int64_t i = i0 + u * stride;
+      k[u] = i < n ? keys[i] : 0ull;
+#pragma unroll
+      for (int q = 0; q < NL; ++q) f[u][q] = i < n ? fan[(int64_t)(flo + q - 1) * fan_ld + i] : 1;
+    }
+#pragma unroll
+    for (int u = 0; u < PU; ++u) {
+      const int64_t i = i0 + u * stride;
+      if (i >= n) continue;
+      bad_layout |= (k[u] >> total) != 0;
+      const uint32_t d = dest_of_key(rg, k[u]);
+      if (dest) dest[i] = (int32_t)d;
+      kor |= k[u];
+      kand &= k[u];
+      dor |= d;
+      dand &= d;
+      if (fl.hcap) flow_insert(fl, k[u] >> fl.shift, &flow_full);
+#pragma unroll
+      for (int q = 0; q < NL; ++q) {
+        const uint32_t child = (uint32_t)((k[u] >> shc[q]) & (uint64_t)tm[q]);
+        bad_fan |= (f[u][q] < 1) || ((int64_t)child >= (int64_t)f[u][q]);
+        fp[q] += fan_term(flo + q, key_prefix(k[u], sh[q]), (uint32_t)f[u][q]);
+      }
     }
   }
 #pragma unroll
@@ -46,19 +76,100 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
     dor |= __shfl_xor(dor, o);
     dand &= __shfl_xor(dand, o);
   }
-  for (int m = flo; m <= fhi; ++m) fp[m] = wave_sum(fp[m]);
+#pragma unroll
+  for (int q = 0; q < NL; ++q) fp[q] = wave_sum(fp[q]);
+  uint32_t flags = (bad_layout ? 1u : 0u) | (bad_fan ? 2u : 0u) | (flow_full ? 4u : 0u);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) flags |= __shfl_xor(flags, o);
+  __shared__ PrepPartial s_w[PREP_NT / ALTO_WAVE];
+  const int w = threadIdx.x / ALTO_WAVE;
   if (lane_id() == 0) {
-    if (ctl) {
-      atomicOr((unsigned long long*)&ctl->key_or, (unsigned long long)kor);
-      atomicAnd((unsigned long long*)&ctl->key_and, (unsigned long long)kand);
-      atomicOr(&ctl->dest_or, dor);
-      atomicAnd(&ctl->dest_and, dand);
-    }
-    for (int m = flo; m <= fhi; ++m)
-      if (fp[m]) atomicAdd((unsigned long long*)&fp_in[m], (unsigned long long)fp[m]);
+    s_w[w].kor = kor;
+    s_w[w].kand = kand;
+    s_w[w].dor = dor;
+    s_w[w].dand = dand;
+    s_w[w].flags = flags;
+#pragma unroll
+    for (int q = 0; q < NL; ++q) s_w[w].fp[q] = fp[q];
   }
-  if (bad_layout) raise_status(status, ALTO_E_LAYOUT);
-  if (bad_fan) raise_status(status, ALTO_E_FANOUT);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    PrepPartial r = s_w[0];
+    for (int ww = 1; ww < PREP_NT / ALTO_WAVE; ++ww) {
+      r.kor |= s_w[ww].kor;
+      r.kand &= s_w[ww].kand;
+      r.dor |= s_w[ww].dor;
+      r.dand &= s_w[ww].dand;
+      r.flags |= s_w[ww].flags;
+#pragma unroll
+      for (int q = 0; q < NL; ++q) r.fp[q] += s_w[ww].fp[q];
+    }
+    part[blockIdx.x] = r;
+  }
+}
+
+// Folds the per-block records of k_prep into the sort control block, the
+// fingerprint sums and the status word (strided per thread, then a wave
+// reduction, then the 4 wave results).
+__global__ __launch_bounds__(256) void k_prep_fold(const PrepPartial* part, int nblocks, int flo, int nl, SortCtl* ctl,
+                                                   uint64_t* fp_in, int32_t* status) {
+  uint64_t kor = 0, kand = ~0ull;
+  uint32_t dor = 0, dand = ~0u, flags = 0;
+  uint64_t fp[ALTO_MAX_LEVELS];
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q) fp[q] = 0;
+  for (int b = threadIdx.x; b < nblocks; b += blockDim.x) {
+    const PrepPartial& x = part[b];
+    kor |= x.kor;
+    kand &= x.kand;
+    dor |= x.dor;
+    dand &= x.dand;
+    flags |= x.flags;
+#pragma unroll
+    for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
+      if (q < nl) fp[q] += x.fp[q];
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kor |= __shfl_xor(kor, o);
+    kand &= __shfl_xor(kand, o);
+    dor |= __shfl_xor(dor, o);
+    dand &= __shfl_xor(dand, o);
+    flags |= __shfl_xor(flags, o);
+  }
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
+    if (q < nl) fp[q] = wave_sum(fp[q]);
+  __shared__ PrepPartial s_w[256 / ALTO_WAVE];
+  const int w = threadIdx.x / ALTO_WAVE;
+  if (lane_id() == 0) {
+    s_w[w].kor = kor;
+    s_w[w].kand = kand;
+    s_w[w].dor = dor;
+    s_w[w].dand = dand;
+    s_w[w].flags = flags;
+#pragma unroll
+    for (int q = 0; q < ALTO_MAX_LEVELS; ++q) s_w[w].fp[q] = fp[q];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int ww = 1; ww < 256 / ALTO_WAVE; ++ww) {
+      kor |= s_w[ww].kor;
+      kand &= s_w[ww].kand;
+      dor |= s_w[ww].dor;
+      dand &= s_w[ww].dand;
+      flags |= s_w[ww].flags;
+      for (int q = 0; q < nl; ++q) fp[q] += s_w[ww].fp[q];
+    }
+    ctl->key_or = kor;
+    ctl->key_and = kand;
+    ctl->dest_or = dor;
+    ctl->dest_and = dand;
+    if (flags & 4u) ctl->flow_overflow = 1;
+    for (int q = 0; q < nl; ++q) fp_in[flo + q] = fp[q];
+    if (flags & 1u) raise_status(status, ALTO_E_LAYOUT);
+    if (flags & 2u) raise_status(status, ALTO_E_FANOUT);
+  }
 }
 
 __global__ void k_zero_u64(uint64_t* p, int count) {
@@ -71,6 +182,10 @@ __global__ void k_init_ctl(SortCtl* ctl) {
     ctl->key_and = ~0ull;
     ctl->dest_or = 0;
     ctl->dest_and = ~0u;
+    ctl->mode = SORT_GENERAL;
+    ctl->flow_overflow = 0;
+    ctl->nflows = 0;
+    ctl->nflows_c = 0;
   }
 }
 
@@ -208,13 +323,14 @@ __global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks
 }
 
 // fp64 sum of the rows of one chunk of a group, in a fixed order: each lane sums
-// its rows sequentially, then lanes holding the same columns are combined in lane
-// order, then the waves in wave order. Groups of one chunk are finished here;
-// others leave a partial sum.
+// its rows sequentially (U independent row loads in flight), then lanes holding the
+// same columns are combined in lane order, then the waves in wave order. Groups of
+// one chunk are finished here; the others leave a partial sum per chunk.
 template <int VEC, int CPL, typename Src>
 __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src srcp,
                                               int dim, int lpr, double* part, float* mean, int64_t cap_groups) {
   constexpr int NW = 4;
+  constexpr int U = 4;
   __shared__ double red[NW][64 * CPL * VEC];
   const int C = dim / VEC;
   const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
@@ -228,23 +344,41 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
       for (int q = 0; q < CPL; ++q)
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[q][v] = 0.0;
-      for (int r = w * rpw + sub; r < ch.len; r += NW * rpw) {
-        const float* src = srcp.pay_of(srcp.row(ch.begin + r));
+      const int stride = NW * rpw;
+      for (int r0 = w * rpw + sub; r0 < ch.len; r0 += stride * U) {
+        const float* src[U];
 #pragma unroll
-        for (int q = 0; q < CPL; ++q) {
-          const int col = col0 + cl + q * lpr;
-          if (col < C) {
-            if constexpr (VEC == 4) {
-              const float4 x = *reinterpret_cast<const float4*>(src + (int64_t)col * 4);
-              acc[q][0] += x.x;
-              acc[q][1] += x.y;
-              acc[q][2] += x.z;
-              acc[q][3] += x.w;
+        for (int u = 0; u < U; ++u) {
+          const int r = r0 + u * stride;
+          src[u] = r < ch.len ? srcp.pay_of(srcp.row(ch.begin + r)) : nullptr;
+        }
+        float x[U][CPL][VEC];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int q = 0; q < CPL; ++q) {
+            const int col = col0 + cl + q * lpr;
+            if (src[u] && col < C) {
+              if constexpr (VEC == 4) {
+                const float4 t = *reinterpret_cast<const float4*>(src[u] + (int64_t)col * 4);
+                x[u][q][0] = t.x;
+                x[u][q][1] = t.y;
+                x[u][q][2] = t.z;
+                x[u][q][3] = t.w;
+              } else {
+                x[u][q][0] = src[u][col];
+              }
             } else {
-              acc[q][0] += src[col];
+#pragma unroll
+              for (int v = 0; v < VEC; ++v) x[u][q][v] = 0.f;
             }
           }
-        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+          for (int q = 0; q < CPL; ++q)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[q][v] += (double)x[u][q][v];
       }
       // combine the sub-rows of the wave (lanes with equal cl), in a fixed order
       for (int o = lpr; o < ALTO_WAVE; o <<= 1)
@@ -278,18 +412,35 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
   }
 }
 
+// Sum of a group's chunk partials in chunk order. 256 threads = SUBS chunk subsets
+// x COLS columns; each thread sums every SUBS-th chunk, then the subsets are added in
+// subset order.
 __global__ __launch_bounds__(256) void k_mean_combine(const Chunk* __restrict__ chunks, const int64_t* nchunks,
                                                       const double* __restrict__ part, int dim, float* mean,
                                                       int64_t cap_groups) {
+  constexpr int COLS = 64, SUBS = 256 / COLS;
+  __shared__ double red[SUBS][COLS];
   const int64_t NC = *nchunks;
+  const int col_l = threadIdx.x % COLS, sidx = threadIdx.x / COLS;
   for (int64_t c = blockIdx.x; c < NC; c += gridDim.x) {
     const Chunk ch = chunks[c];
-    if (ch.k != 0 || ch.nch <= 1 || ch.e >= cap_groups) continue;
-    for (int x = threadIdx.x; x < dim; x += blockDim.x) {
+    if (ch.k != 0 || ch.nch <= 1 || ch.e >= cap_groups) continue;   // uniform per block
+    for (int col0 = 0; col0 < dim; col0 += COLS) {
+      const int x = col0 + col_l;
       double s = 0.0;
-#pragma unroll 8
-      for (int t = 0; t < ch.nch; ++t) s += part[(ch.part + t) * (int64_t)dim + x];
-      mean[ch.e * (int64_t)dim + x] = (float)(s / (double)ch.count);
+      if (x < dim) {
+#pragma unroll 4
+        for (int t = sidx; t < ch.nch; t += SUBS) s += part[(ch.part + t) * (int64_t)dim + x];
+      }
+      red[sidx][col_l] = s;
+      __syncthreads();
+      if (sidx == 0 && x < dim) {
+        double tot = 0.0;
+#pragma unroll
+        for (int q = 0; q < SUBS; ++q) tot += red[q][col_l];
+        mean[ch.e * (int64_t)dim + x] = (float)(tot / (double)ch.count);
+      }
+      __syncthreads();
     }
   }
 }
@@ -362,6 +513,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   b.fp_nodes = c.take<uint64_t>(ALTO_MAX_LEVELS + 1);
   b.nnodes = c.take<int64_t>(ALTO_MAX_LEVELS + 1);
   b.scal = c.take<int64_t>(8);
+  b.prep_part = c.take<PrepPartial>(PREP_GRID);
   b.tmp_keys = c.take<uint64_t>(n);
   b.tmp_vals = c.take<uint32_t>(n);
   b.sk = c.take<uint64_t>(n);
@@ -370,6 +522,29 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   b.scan_u32 = c.take<uint32_t>(SCAN_MAX_BLOCKS + 1);
   b.scan_i32 = c.take<int32_t>(SCAN_MAX_BLOCKS + 1);
   b.scan_i64 = c.take<int64_t>(SCAN_MAX_BLOCKS + 1);
+  memset(&b.fl, 0, sizeof(b.fl));
+  if (n_max > SORT_SMALL_MAX && Lr >= 1) {
+    // flows of the route level, ranked in (dest, prefix) order (packed sort)
+    FlowBufs& f = b.fl;
+    f.fcap = n < FLOW_CAP ? n : FLOW_CAP;
+    int64_t h = 1024;
+    while (h < 2 * f.fcap) h <<= 1;
+    f.hcap = h;
+    f.shift = g.shift[Lr];
+    f.ib = bits_for(n - 1);
+    f.ht_key = c.take<uint64_t>(h);
+    f.ht_rank = c.take<uint32_t>(h);
+    f.ct_key = c.take<uint64_t>(h);
+    f.ct_rank = c.take<uint32_t>(h);
+    f.flow_key = c.take<uint64_t>(f.fcap);
+    f.flow_slot = c.take<uint32_t>(f.fcap);
+    f.flow_sorted = c.take<uint64_t>(f.fcap);
+    f.flow_order = c.take<uint32_t>(f.fcap);
+    f.ftmp_keys = c.take<uint64_t>(f.fcap);
+    f.ftmp_vals = c.take<uint32_t>(f.fcap);
+    f.fhist = c.take<uint32_t>((int64_t)SORT_BUCKETS * sort_hist_blocks(f.fcap));
+    f.fctl = c.take<SortCtl>(1);
+  }
   if (!agg) return;
   int Lt, Lseg;
   agg_levels(g, agg->level, agg->mask_level, Lr, &Lt, &Lseg);
@@ -403,18 +578,32 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 // ---------------------------------------------------------------------------
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st) {
+              int32_t* status, hipStream_t st, bool offsets_later) {
   {
     ProfScope ps(PH_PREP, st);
     k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
+    flow_clear_launch(b.fl, b.ctl, st);
     k_zero_u64<<<1, 64, 0, st>>>(b.fp_in, ALTO_MAX_LEVELS + 1);
     k_zero_u64<<<1, 64, 0, st>>>(b.fp_nodes, ALTO_MAX_LEVELS + 1);
-    k_prep<<<grid_for(n, PREP_NT * 8, 2048), PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fhi, b.fp_in,
-                                                               b.ctl, status);
+    const int nl = fhi >= flo ? fhi - flo + 1 : 0;
+    const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
+#define ALTO_PREP_CASE(NLV)                                                                                   \
+  case NLV:                                                                                                   \
+    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, b.fl, b.prep_part); \
+    break;
+    switch (nl) {
+      ALTO_PREP_CASE(0) ALTO_PREP_CASE(1) ALTO_PREP_CASE(2) ALTO_PREP_CASE(3) ALTO_PREP_CASE(4)
+      ALTO_PREP_CASE(5) ALTO_PREP_CASE(6) ALTO_PREP_CASE(7) ALTO_PREP_CASE(8) ALTO_PREP_CASE(9)
+      ALTO_PREP_CASE(10) ALTO_PREP_CASE(11) ALTO_PREP_CASE(12) ALTO_PREP_CASE(13) ALTO_PREP_CASE(14)
+      default: return ALTO_E_ARG;
+    }
+#undef ALTO_PREP_CASE
+    k_prep_fold<<<1, 256, 0, st>>>(b.prep_part, grid, flo, nl, b.ctl, b.fp_in, status);
     ALTO_LAUNCH_CHECK();
   }
   ProfScope ps_sort(PH_SORT, st);
   SortBufs sb;
+  memset(&sb, 0, sizeof(sb));
   sb.in_keys = keys;
   sb.tmp_keys = b.tmp_keys;
   sb.tmp_vals = b.tmp_vals;
@@ -423,10 +612,13 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   sb.hist = b.hist;
   sb.scan_part = b.scan_u32;
   sb.ctl = b.ctl;
+  sb.fl = b.fl;
   b.perm_used = sb.out_vals;
   int rc = sort_pairs(sb, n, nullptr, rg, g.total, true, st);
   if (rc) return rc;
-  k_dest_offsets<<<grid_for(n, 256), 256, 0, st>>>(b.sk, n, rg, dest_offsets, status);
+  // destination offsets and duplicate keys; aggregation does both in its
+  // segmentation pass over the same sorted keys
+  if (!offsets_later) k_dest_offsets<<<grid_for(n, 256), 256, 0, st>>>(b.sk, n, rg, dest_offsets, status);
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;
 }
@@ -439,7 +631,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   int Lt, Lseg;
   agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
   ProfScope ps_total(PH_TOTAL, st);
-  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st);
+  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st, true);
   if (rc) return rc;
   const uint32_t* perm = b.perm_used;
   prof_begin(PH_SEGMENT, st);
@@ -456,7 +648,9 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   fj.fan = fan;
   fj.fan_ld = fan_ld;
   fj.fan_base = 1;
-  fj.check_dup = 0;   // duplicates are reported by k_dest_offsets
+  fj.check_dup = 1;
+  fj.dest_offsets = dest_offsets;
+  fj.rg = rg;
   fj.carry_lo = Lt;
   fj.carry_fan = (Lt < Lseg) ? b.carry_fan : nullptr;
   fj.carry_ld = n < 1 ? 1 : n;
@@ -475,6 +669,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     const int64_t* Rp = b.nnodes + Lseg;
     k_record_keys<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lseg], Rp, b.sk, g.shift[Lseg], b.rkey);
     SortBufs rb;
+    memset(&rb, 0, sizeof(rb));   // no flows: records sort by key only
     rb.in_keys = b.rkey;
     rb.tmp_keys = b.tmp_keys;
     rb.tmp_vals = b.tmp_vals;

@@ -6,7 +6,7 @@
 #define SEG_NT 256
 #define SEG_IT 8
 #define SEG_TILE (SEG_NT * SEG_IT)
-#define NODE_GRID 1024
+#define NODE_GRID 512
 
 // Arrays describing the nodes of one level, in element order.
 struct LevelNodes {
@@ -51,6 +51,8 @@ struct SegJob {
   int32_t* scan_part;       // [SCAN_MAX_BLOCKS + 1]
   uint64_t* fp_nodes;       // device [ALTO_MAX_LEVELS + 1]: fingerprint sums over nodes (fragments)
   int32_t* status;
+  int64_t* dest_offsets;    // fragments sorted by (dest, key): start of each destination (nullable)
+  RouteGeom rg;
 };
 
 int seg_blocks(int64_t n_max);

@@ -52,6 +52,28 @@ __global__ __launch_bounds__(NT) void k_seg_count(KeyGeom g, SegJob j, int nblk)
     return;
   }
   load_tile(j, tile0, n, s_key);
+  if (j.dest_offsets) {
+    // destination offsets from the sorted keys: each change of destination fills
+    // the starts of the destinations it passes
+    const uint32_t D = j.rg.num_dest;
+    int64_t* offs = j.dest_offsets;
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      const int t = threadIdx.x * IT + i;
+      const int64_t e = tile0 + t;
+      if (e >= n) break;
+      const uint32_t d = dest_of_key(j.rg, s_key[t + 1]);
+      if (e == 0) {
+        for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
+      } else {
+        const uint32_t dp = dest_of_key(j.rg, s_key[t]);
+        if (d != dp)
+          for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = e;
+      }
+      if (e == n - 1)
+        for (uint32_t x = d + 1; x <= D; ++x) offs[x] = n;
+    }
+  }
   for (int m = j.lo; m < j.elem_level; ++m) {
     const int es = es_of(g, j, m);
     int32_t c = 0;
@@ -85,6 +107,7 @@ __global__ void k_seg_totals(SegJob j, int nblk, int64_t total_len) {
   }
 }
 
+template <int KM>
 __global__ __launch_bounds__(NT) void k_seg_write(KeyGeom g, SegJob j, int nblk) {
   __shared__ uint64_t s_key[TILE + 1];
   __shared__ int32_t s_w[NT / ALTO_WAVE];
@@ -92,49 +115,61 @@ __global__ __launch_bounds__(NT) void k_seg_write(KeyGeom g, SegJob j, int nblk)
   const int64_t tile0 = (int64_t)blockIdx.x * TILE;
   if (tile0 >= n) return;
   load_tile(j, tile0, n, s_key);
-  const int lo = j.lo, E = j.elem_level;
-  int32_t cur[ALTO_MAX_LEVELS + 1];
-  // per level: node id of the element before this thread's first element
-  for (int m = lo; m < E; ++m) {
-    const int es = es_of(g, j, m);
-    int32_t c = 0;
+  const int lo = j.lo, E = j.elem_level, K = E - lo;
+  // slot q holds level lo + q; every loop below is fully unrolled so that the
+  // per-level arrays stay in registers
+  int32_t cur[KM];
+  int es[KM];
 #pragma unroll
-    for (int i = 0; i < IT; ++i) {
-      int t = threadIdx.x * IT + i;
-      int64_t e = tile0 + t;
-      if (e < n) c += (e == 0) || (key_prefix(s_key[t + 1], es) != key_prefix(s_key[t], es));
+  for (int q = 0; q < KM; ++q) {
+    cur[q] = 0;
+    es[q] = q < K ? es_of(g, j, lo + q) : 64;
+  }
+  // per level: node id of the element before this thread's first element
+#pragma unroll
+  for (int q = 0; q < KM; ++q) {
+    if (q < K) {
+      int32_t c = 0;
+#pragma unroll
+      for (int i = 0; i < IT; ++i) {
+        const int t = threadIdx.x * IT + i;
+        const int64_t e = tile0 + t;
+        if (e < n) c += (e == 0) || (key_prefix(s_key[t + 1], es[q]) != key_prefix(s_key[t], es[q]));
+      }
+      int32_t tot;
+      const int32_t ex = block_excl_scan<int32_t, NT>(c, s_w, &tot);
+      const int32_t lvl_base = j.blkcnt[(int64_t)q * nblk];
+      const int32_t blk_off = j.blkcnt[(int64_t)q * nblk + blockIdx.x] - lvl_base;
+      cur[q] = blk_off + ex - 1;
     }
-    int32_t tot;
-    int32_t ex = block_excl_scan<int32_t, NT>(c, s_w, &tot);
-    const int32_t lvl_base = j.blkcnt[(int64_t)(m - lo) * nblk];
-    const int32_t blk_off = j.blkcnt[(int64_t)(m - lo) * nblk + blockIdx.x] - lvl_base;
-    cur[m] = blk_off + ex - 1;
   }
   for (int i = 0; i < IT; ++i) {
-    int t = threadIdx.x * IT + i;
-    int64_t e = tile0 + t;
+    const int t = threadIdx.x * IT + i;
+    const int64_t e = tile0 + t;
     if (e >= n) break;
     const uint64_t k = s_key[t + 1], kp = s_key[t];
     uint32_t flags = 0;
-    for (int m = lo; m < E; ++m) {
-      const int es = es_of(g, j, m);
-      bool f = (e == 0) || (key_prefix(k, es) != key_prefix(kp, es));
-      if (f) {
-        flags |= 1u << m;
-        ++cur[m];
+#pragma unroll
+    for (int q = 0; q < KM; ++q) {
+      if (q < K && ((e == 0) || (key_prefix(k, es[q]) != key_prefix(kp, es[q])))) {
+        flags |= 1u << q;
+        ++cur[q];
       }
     }
     if (j.check_dup && e > 0 && k == kp) raise_status(j.status, ALTO_E_DUPLICATE);
-    for (int m = lo; m < E; ++m) {
-      if (flags & (1u << m)) {
-        const int32_t id = cur[m];
-        LevelNodes& L = j.lv[m];
+#pragma unroll
+    for (int q = 0; q < KM; ++q) {
+      if (q >= K) continue;
+      const int m = lo + q;
+      if (flags & (1u << q)) {
+        const int32_t id = cur[q];
+        const LevelNodes& L = j.lv[m];
         L.start[id] = (int32_t)e;
-        if (m + 1 < E) L.fc[id] = cur[m + 1];
-        if (m > lo) L.par[id] = cur[m - 1];
+        if (q + 1 < K) L.fc[id] = cur[q + 1 < KM ? q + 1 : q];
+        if (q > 0) L.par[id] = cur[q > 0 ? q - 1 : 0];
         L.nfan[id] = fan_at(j, m, e);
         L.bad[id] = 0;
-        if (m == lo && j.carry_fan) {
+        if (q == 0 && j.carry_fan) {
           for (int mm = j.carry_lo; mm < lo; ++mm)
             j.carry_fan[(int64_t)(mm - j.carry_lo) * j.carry_ld + id] = fan_at(j, mm, e);
         }
@@ -161,37 +196,80 @@ __global__ __launch_bounds__(256) void k_seg_nodes(KeyGeom g, SegJob j, int m) {
   const LevelNodes L = j.lv[m];
   const bool leafy = (m + 1 == j.elem_level);
   const int es = es_of(g, j, m);
-  uint64_t fp[ALTO_MAX_LEVELS + 1];
   const int clo = (m == j.lo && j.carry_fan) ? j.carry_lo : m;
-  for (int mm = clo; mm <= m; ++mm) fp[mm] = 0;
+  const int nc = m - clo;   // carried levels handled here (clo .. m-1)
+  uint64_t fpm = 0;
+  uint64_t fpc[ALTO_MAX_LEVELS];
+  int esc[ALTO_MAX_LEVELS];
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
+    fpc[q] = 0;
+    esc[q] = q < nc ? es_of(g, j, clo + q) : 64;
+  }
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < N; u += (int64_t)gridDim.x * blockDim.x) {
     const int32_t s = L.start[u], e = L.start[u + 1];
     const int32_t cnt = e - s;
     int32_t nchild;
-    bool allok = true;
     if (leafy) {
-      nchild = cnt;
-      if (j.elem_ok)
-        for (int32_t x = s; x < e; ++x) allok = allok && j.elem_ok[j.idx[x]];
+      nchild = cnt;   // incomplete element records were pushed into bad by k_elem_bad
     } else {
       nchild = L.fc[u + 1] - L.fc[u];
     }
-    const bool ok = (nchild == L.nfan[u]) && !L.bad[u] && allok;
+    const bool ok = (nchild == L.nfan[u]) && !L.bad[u];
     L.ok[u] = ok ? 1 : 0;
     if (!ok && m > j.lo) j.lv[m - 1].bad[L.par[u]] = 1;
     if (j.fp_nodes) {
       const uint64_t k = j.keys[s];
-      fp[m] += (uint64_t)cnt * fan_term(m, key_prefix(k, es), (uint32_t)L.nfan[u]);
-      for (int mm = clo; mm < m; ++mm)
-        fp[mm] += (uint64_t)cnt * fan_term(mm, key_prefix(k, es_of(g, j, mm)),
-                                           (uint32_t)j.carry_fan[(int64_t)(mm - j.carry_lo) * j.carry_ld + u]);
+      fpm += (uint64_t)cnt * fan_term(m, key_prefix(k, es), (uint32_t)L.nfan[u]);
+#pragma unroll
+      for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
+        if (q < nc)
+          fpc[q] += (uint64_t)cnt * fan_term(clo + q, key_prefix(k, esc[q]),
+                                             (uint32_t)j.carry_fan[(int64_t)q * j.carry_ld + u]);
     }
   }
   if (j.fp_nodes) {
-    for (int mm = clo; mm <= m; ++mm) {
-      uint64_t v = wave_sum(fp[mm]);
-      if (lane_id() == 0 && v) atomicAdd((unsigned long long*)&j.fp_nodes[mm], (unsigned long long)v);
+    // block sums first: one atomic per block and level
+    __shared__ uint64_t s_fp[256 / ALTO_WAVE][ALTO_MAX_LEVELS + 1];
+    const int w = threadIdx.x / ALTO_WAVE;
+    const uint64_t v = wave_sum(fpm);
+    if (lane_id() == 0) s_fp[w][ALTO_MAX_LEVELS] = v;
+#pragma unroll
+    for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
+      if (q < nc) {
+        const uint64_t vc = wave_sum(fpc[q]);
+        if (lane_id() == 0) s_fp[w][q] = vc;
+      }
     }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t t = 0;
+      for (int ww = 0; ww < 256 / ALTO_WAVE; ++ww) t += s_fp[ww][ALTO_MAX_LEVELS];
+      if (t) atomicAdd((unsigned long long*)&j.fp_nodes[m], (unsigned long long)t);
+      for (int q = 0; q < nc; ++q) {
+        uint64_t tc = 0;
+        for (int ww = 0; ww < 256 / ALTO_WAVE; ++ww) tc += s_fp[ww][q];
+        if (tc) atomicAdd((unsigned long long*)&j.fp_nodes[clo + q], (unsigned long long)tc);
+      }
+    }
+  }
+}
+
+// Records that are themselves incomplete make their parent incomplete: one thread
+// per record finds its parent node by binary search over the node starts.
+__global__ __launch_bounds__(256) void k_elem_bad(SegJob j) {
+  const int64_t n = nelem(j);
+  const int m = j.elem_level - 1;
+  const int64_t N = j.nnodes[m];
+  const LevelNodes L = j.lv[m];
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    if (j.elem_ok[j.idx[e]]) continue;
+    int64_t lo = 0, hi = N - 1;   // last node with start <= e
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (L.start[mid] <= e) lo = mid; else hi = mid - 1;
+    }
+    if (N > 0) L.bad[lo] = 1;
   }
 }
 
@@ -209,8 +287,11 @@ int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st) {
   int rc = scan_exclusive<int32_t>(job.blkcnt, job.blkcnt, len + 1, nullptr, job.scan_part, nullptr, st);
   if (rc) return rc;
   k_seg_totals<<<1, 1, 0, st>>>(job, nblk, len);
-  k_seg_write<<<nblk, NT, 0, st>>>(g, job, nblk);
+  if (K <= 2) k_seg_write<2><<<nblk, NT, 0, st>>>(g, job, nblk);
+  else if (K <= 4) k_seg_write<4><<<nblk, NT, 0, st>>>(g, job, nblk);
+  else k_seg_write<ALTO_MAX_LEVELS><<<nblk, NT, 0, st>>>(g, job, nblk);
   k_seg_sentinels<<<1, 64, 0, st>>>(job);
+  if (job.elem_ok) k_elem_bad<<<NODE_GRID, 256, 0, st>>>(job);
   for (int m = job.elem_level - 1; m >= job.lo; --m) k_seg_nodes<<<NODE_GRID, 256, 0, st>>>(g, job, m);
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;

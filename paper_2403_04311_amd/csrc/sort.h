@@ -2,16 +2,18 @@
 #pragma once
 #include "alto_internal.h"
 
-#define SORT_NT 256
-#define SORT_IT 16
+#define SORT_NT 512
+#define SORT_IT 8
 #define SORT_TILE (SORT_NT * SORT_IT)
 #define SORT_RADIX 8
 #define SORT_BUCKETS 256
 #define SORT_MAX_PASSES 12
 #define SCAN_MAX_BLOCKS 1023
 #define SORT_SMALL_MAX 4096
+#define FLOW_CAP (1 << 15)
 
 enum { SORT_BUF_INPUT = 0, SORT_BUF_TMP = 1, SORT_BUF_FINAL = 2 };
+enum { SORT_GENERAL = 0, SORT_PACKED = 1 };
 
 struct SortPass {
   int32_t active, src, dst, from_dest, lo;
@@ -19,14 +21,47 @@ struct SortPass {
 
 struct SortPlan {
   int32_t npass;
+  int32_t idle;          // the multi-block path does nothing (sorted in one workgroup)
   SortPass pass[SORT_MAX_PASSES];
+  int64_t hist_len[SORT_MAX_PASSES];   // histogram entries to scan per pass (0 = inactive)
 };
 
 // Device control block of one sort.
 struct SortCtl {
   uint64_t key_or, key_and;
   uint32_t dest_or, dest_and;
+  int32_t mode;          // SORT_GENERAL: (key, index) pairs; SORT_PACKED: one word per element
+  int32_t ib;            // packed: bits of the input index (low bits)
+  int32_t sbits;         // packed: key bits below the route level (middle bits)
+  int32_t rbits;         // packed: bits of the flow rank (high bits)
+  int32_t flow_overflow; // the flow set filled up
+  int32_t pad;
+  int64_t nflows;        // distinct flows inserted
+  int64_t nflows_c;      // the same, clamped to the flow capacity
+  int64_t hist_len;      // histogram entries the scan covers (0 when idle)
+  int64_t ct_mask;       // packed: slots - 1 of the compact rank table
   SortPlan plan;
+};
+
+// Distinct route-level prefixes ("flows") of one batch and their rank in
+// (destination, prefix) order; used by the packed mode.
+struct FlowBufs {
+  uint64_t* ht_key;      // [hcap] open-addressing set of prefixes, ~0 = empty
+  uint32_t* ht_rank;     // [hcap] rank of the prefix held in the slot
+  uint64_t* ct_key;      // [hcap] compact rank table (power of two >= 2 x flows), ~0 = empty
+  uint32_t* ct_rank;     // [hcap]
+  int64_t hcap;          // power of two, 0 = flows not used
+  int32_t shift;         // bits below the route level
+  int32_t ib;            // bits of the largest input index
+  uint64_t* flow_key;    // [fcap] compacted prefixes
+  uint32_t* flow_slot;   // [fcap]
+  uint64_t* flow_sorted; // [fcap] prefixes in (destination, prefix) order
+  uint32_t* flow_order;  // [fcap]
+  uint64_t* ftmp_keys;   // [fcap] sort scratch
+  uint32_t* ftmp_vals;
+  uint32_t* fhist;       // [256 * sort_hist_blocks(fcap)]
+  SortCtl* fctl;
+  int64_t fcap;
 };
 
 struct SortBufs {
@@ -38,22 +73,66 @@ struct SortBufs {
   uint32_t* hist;            // [256 * sort_hist_blocks(n_max)]
   uint32_t* scan_part;       // [SCAN_MAX_BLOCKS + 1]
   SortCtl* ctl;
+  FlowBufs fl;               // hcap == 0: general mode only
 };
 
 int sort_hist_blocks(int64_t n_max);
 int sort_max_key_windows(int key_bits);
 int sort_max_dest_windows(const RouteGeom& rg);
+int bits_for(int64_t v);     // bits needed to hold values 0..v
 
 // Sorts n (= *n_dev if n_dev, else n_max) keys by (destination, key), stably.
 // key_bits bounds the width of the keys. If ctl_has_reduction, ctl already holds
-// the OR/AND of keys and destinations (see sort_reduce_launch).
+// the OR/AND of keys and destinations (see sort_reduce_launch). With b.fl.hcap > 0
+// the flow set must have been filled (flow_insert in the input pass); the sort
+// then ranks the flows and runs in packed mode when the packing fits.
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
                bool ctl_has_reduction, hipStream_t st);
 void sort_reduce_launch(const uint64_t* keys, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, SortCtl* ctl,
                         hipStream_t st);
+void flow_clear_launch(const FlowBufs& fl, SortCtl* ctl, hipStream_t st);
 
 // Exclusive scan of len (= *len_dev if len_dev, else len_max) elements; in may
 // equal out. part needs SCAN_MAX_BLOCKS + 1 entries; part[nb] and *total (if
 // non-null) receive the sum.
 template <typename T>
 int scan_exclusive(const T* in, T* out, int64_t len_max, const int64_t* len_dev, T* part, T* total, hipStream_t st);
+
+__device__ inline uint64_t flow_slot0(const FlowBufs& fl, uint64_t p) {
+  return mix64(p ^ 0xD6E8FEB86659FD93ull) & ((uint64_t)fl.hcap - 1);
+}
+
+// Insert of a route-level prefix into the flow set (called from the input pass),
+// starting at slot h whose content v the caller has already read.
+__device__ inline void flow_insert_from(const FlowBufs& fl, uint64_t p, uint64_t h, uint64_t v, bool* overflow) {
+  if (v == p) return;
+  const uint64_t mask = (uint64_t)fl.hcap - 1;
+  for (int probe = 0; probe < 256; ++probe) {
+    if (probe > 0) v = fl.ht_key[h];
+    if (v == p) return;
+    if (v == ~0ull) {
+      const uint64_t old = atomicCAS((unsigned long long*)&fl.ht_key[h], ~0ull, (unsigned long long)p);
+      if (old == ~0ull || old == p) return;
+    }
+    h = (h + 1) & mask;
+  }
+  *overflow = true;
+}
+
+// Insert of a route-level prefix into the flow set (called from the input pass).
+__device__ inline void flow_insert(const FlowBufs& fl, uint64_t p, bool* overflow) {
+  const uint64_t mask = (uint64_t)fl.hcap - 1;
+  uint64_t h = mix64(p ^ 0xD6E8FEB86659FD93ull) & mask;
+  for (int probe = 0; probe < 256; ++probe) {
+    // a plain (cached) read is enough: a slot changes once, from empty to a key,
+    // and the compare-and-swap settles a stale empty
+    const uint64_t v = fl.ht_key[h];
+    if (v == p) return;
+    if (v == ~0ull) {
+      const uint64_t old = atomicCAS((unsigned long long*)&fl.ht_key[h], ~0ull, (unsigned long long)p);
+      if (old == ~0ull || old == p) return;
+    }
+    h = (h + 1) & mask;
+  }
+  *overflow = true;
+}

@@ -12,6 +12,8 @@
 // LDS in digit order so that the global scatter writes contiguous runs.
 #include "sort.h"
 
+#include <string.h>
+
 namespace {
 
 constexpr int NT = SORT_NT;
@@ -27,6 +29,10 @@ __global__ void k_sort_init(SortCtl* ctl) {
     ctl->key_and = ~0ull;
     ctl->dest_or = 0;
     ctl->dest_and = ~0u;
+    ctl->mode = SORT_GENERAL;
+    ctl->flow_overflow = 0;
+    ctl->nflows = 0;
+    ctl->nflows_c = 0;
   }
 }
 
@@ -62,29 +68,40 @@ __global__ __launch_bounds__(256) void k_sort_reduce(const uint64_t* __restrict_
   }
 }
 
-// Greedy cover of the varying bits with 8-bit windows (optimal for fixed-width
-// interval cover), key windows first, then destination windows; then the buffer
-// ping-pong so that the last pass lands in the final buffers.
-__global__ void k_sort_plan(SortCtl* ctl, int max_key_windows, int max_dest_windows) {
+__device__ inline int greedy_windows(uint64_t v, int limit, int from_dest, SortPass* out, int np) {
+  const int start = np;
+  while (v && np < start + limit) {
+    const int lo = __builtin_ctzll(v);
+    out[np].from_dest = from_dest;
+    out[np].lo = lo;
+    ++np;
+    v = (lo + SORT_RADIX >= 64) ? 0ull : (v & ~((1ull << (lo + SORT_RADIX)) - 1ull));
+  }
+  return np;
+}
+
+// Digit windows: a greedy cover of the varying bits with 8-bit windows (optimal
+// for fixed-width interval cover). General mode: key windows, then destination
+// windows. Packed mode: windows over the (flow rank, suffix) bits. Then the buffer
+// ping-pong so that the last pass lands in the final buffers. With a device-side
+// count of at most SORT_SMALL_MAX the one-workgroup sort has done the work.
+__global__ void k_sort_plan(SortCtl* ctl, int64_t n_host, const int64_t* n_dev, int max_key_windows,
+                            int max_dest_windows, int nblocks) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const int64_t n = load_n(n_host, n_dev);
   SortPlan p;
   int np = 0;
-  uint64_t vk = ctl->key_or ^ ctl->key_and;
-  while (vk && np < max_key_windows) {
-    int lo = __builtin_ctzll(vk);
-    p.pass[np].from_dest = 0;
-    p.pass[np].lo = lo;
-    ++np;
-    vk = (lo + SORT_RADIX >= 64) ? 0ull : (vk & ~((1ull << (lo + SORT_RADIX)) - 1ull));
-  }
-  uint32_t vd = ctl->dest_or ^ ctl->dest_and;
-  int nk = np;
-  while (vd && np < nk + max_dest_windows) {
-    int lo = __builtin_ctz(vd);
-    p.pass[np].from_dest = 1;
-    p.pass[np].lo = lo;
-    ++np;
-    vd = (lo + SORT_RADIX >= 32) ? 0u : (vd & ~((1u << (lo + SORT_RADIX)) - 1u));
+  p.idle = (n_dev && n <= SORT_SMALL_MAX) ? 1 : 0;
+  if (!p.idle) {
+    if (ctl->mode == SORT_PACKED) {
+      const int S = ctl->sbits, R = ctl->rbits;
+      uint64_t vs = (ctl->key_or ^ ctl->key_and) & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
+      uint64_t vr = R > 0 ? (((1ull << R) - 1ull) << S) : 0ull;
+      np = greedy_windows(vs | vr, SORT_MAX_PASSES, 0, p.pass, np);
+    } else {
+      np = greedy_windows(ctl->key_or ^ ctl->key_and, max_key_windows, 0, p.pass, np);
+      np = greedy_windows((uint64_t)(ctl->dest_or ^ ctl->dest_and), max_dest_windows, 1, p.pass, np);
+    }
   }
   for (int k = 0; k < np; ++k) {
     p.pass[k].active = 1;
@@ -97,12 +114,135 @@ __global__ void k_sort_plan(SortCtl* ctl, int max_key_windows, int max_dest_wind
     p.pass[k].from_dest = p.pass[k].lo = 0;
   }
   p.npass = np;
+  for (int k = 0; k < SORT_MAX_PASSES; ++k) p.hist_len[k] = p.pass[k].active ? (int64_t)SORT_BUCKETS * nblocks : 0;
   ctl->plan = p;
+  ctl->hist_len = p.idle ? 0 : (int64_t)SORT_BUCKETS * nblocks;
 }
 
 __device__ inline uint32_t digit_of(const SortPass& ps, const RouteGeom& rg, uint64_t k) {
   uint64_t src = ps.from_dest ? (uint64_t)dest_of_key(rg, k) : k;
   return (uint32_t)((src >> ps.lo) & (SORT_BUCKETS - 1));
+}
+
+// ---- flows (packed mode) ----------------------------------------------------
+__global__ void k_flow_clear(FlowBufs fl) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < fl.hcap; i += (int64_t)gridDim.x * blockDim.x) {
+    fl.ht_key[i] = ~0ull;
+    fl.ct_key[i] = ~0ull;
+  }
+}
+
+// Compact rank table: the ranked flows in a table of about twice their number, so
+// that the lookups of the first pass stay in the caches.
+__global__ void k_ct_insert(FlowBufs fl, const SortCtl* ctl) {
+  const int64_t F = ctl->nflows_c;
+  const uint64_t mask = (uint64_t)ctl->ct_mask;
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < F; r += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t p = fl.flow_sorted[r];
+    uint64_t h = mix64(p ^ 0xD6E8FEB86659FD93ull) & mask;
+    for (uint64_t probe = 0; probe <= mask; ++probe) {
+      const uint64_t old = atomicCAS((unsigned long long*)&fl.ct_key[h], ~0ull, (unsigned long long)p);
+      if (old == ~0ull) {
+        fl.ct_rank[h] = (uint32_t)r;
+        break;
+      }
+      h = (h + 1) & mask;
+    }
+  }
+}
+
+// Compaction of the flow set; one atomic per wave.
+__global__ __launch_bounds__(256) void k_flow_compact(FlowBufs fl, SortCtl* ctl) {
+  for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < fl.hcap; base += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t s = base + threadIdx.x;
+    const uint64_t v = s < fl.hcap ? fl.ht_key[s] : ~0ull;
+    const bool has = v != ~0ull;
+    const uint64_t ball = __ballot(has);
+    int64_t first = 0;
+    if (lane_id() == 0 && ball) first = (int64_t)atomicAdd((unsigned long long*)&ctl->nflows, (unsigned long long)__popcll(ball));
+    first = __shfl(first, 0);
+    if (has) {
+      const int64_t i = first + __popcll(ball & lanemask_lt());
+      if (i < fl.fcap) {
+        fl.flow_key[i] = v;
+        fl.flow_slot[i] = (uint32_t)s;
+      }
+    }
+  }
+}
+
+__global__ void k_flow_count(FlowBufs fl, SortCtl* ctl) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    const int64_t F = ctl->nflows;
+    ctl->nflows_c = F < fl.fcap ? F : fl.fcap;
+    if (F > fl.fcap) ctl->flow_overflow = 1;
+  }
+}
+
+// Rank of every flow in (destination, prefix) order, and the choice of mode.
+__global__ void k_flow_rank(FlowBufs fl, SortCtl* ctl, int64_t n) {
+  const int64_t F = ctl->nflows_c;
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < F; r += (int64_t)gridDim.x * blockDim.x)
+    fl.ht_rank[fl.flow_slot[fl.flow_order[r]]] = (uint32_t)r;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    int R = 0;
+    while (R < 63 && ((int64_t)1 << R) < F) ++R;
+    const bool fits = !ctl->flow_overflow && ctl->nflows <= fl.fcap && F >= 1 && R + fl.shift + fl.ib <= 64;
+    ctl->mode = fits ? SORT_PACKED : SORT_GENERAL;
+    int64_t t = 64;
+    while (t < 2 * F && t < fl.hcap) t <<= 1;
+    ctl->ct_mask = t - 1;
+    ctl->rbits = R;
+    ctl->sbits = fl.shift;
+    ctl->ib = fl.ib;
+  }
+}
+
+// What a pass kernel needs from the control block (kept in scalars, not a copy of
+// the whole block).
+struct PassView {
+  SortPass ps;
+  int32_t mode, ib, sbits, npass;
+  uint64_t ct_mask;
+};
+
+__device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
+  PassView v;
+  v.ps = ctl->plan.pass[slot];
+  v.mode = ctl->mode;
+  v.ib = ctl->ib;
+  v.sbits = ctl->sbits;
+  v.npass = ctl->plan.npass;
+  v.ct_mask = (uint64_t)ctl->ct_mask;
+  return v;
+}
+
+__device__ inline uint64_t pack_input(const FlowBufs& fl, const PassView& c, uint64_t key, uint64_t idx) {
+  const int S = c.sbits;
+  const uint64_t p = key >> S;
+  const uint64_t mask = c.ct_mask;
+  uint64_t h = mix64(p ^ 0xD6E8FEB86659FD93ull) & mask;
+  uint32_t rank = 0;
+  for (uint64_t probe = 0; probe <= mask; ++probe) {
+    const uint64_t v = fl.ct_key[h];
+    if (v == p) {
+      rank = fl.ct_rank[h];
+      break;
+    }
+    if (v == ~0ull) break;
+    h = (h + 1) & mask;
+  }
+  const uint64_t suffix = S == 0 ? 0ull : (key & ((1ull << S) - 1ull));
+  const int hi = S + c.ib;
+  const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
+  return r | (suffix << c.ib) | idx;
+}
+
+__device__ inline uint64_t unpack_key(const FlowBufs& fl, const PassView& c, uint64_t e) {
+  const int S = c.sbits, hi = S + c.ib;
+  const uint64_t rank = hi >= 64 ? 0ull : (e >> hi);
+  const uint64_t suffix = S == 0 ? 0ull : ((e >> c.ib) & ((1ull << S) - 1ull));
+  return (fl.flow_sorted[rank] << S) | suffix;
 }
 
 struct SrcPtrs {
@@ -116,8 +256,8 @@ __device__ inline SrcPtrs pick_src(int sel, const SortBufs& b) {
   return {b.out_keys, b.out_vals};
 }
 
-// Stable in-wave ranking of one row of 64 digits: returns the rank of this lane
-// among the valid lanes holding the same digit, and the lane mask of those peers.
+// Stable in-wave ranking of one row of 64 digits: the lane mask of the valid lanes
+// holding the same digit as this lane.
 __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
   uint64_t peers = __ballot(valid);
 #pragma unroll
@@ -129,41 +269,70 @@ __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
   return peers;
 }
 
+// Loads element gi of the pass input: in packed mode one word (composed from the
+// input key on the first pass), in general mode a key and a value.
+__device__ inline void load_elem(const SortBufs& b, const PassView& c, const SortPass& ps, int64_t gi, uint64_t& key,
+                                 uint32_t& val) {
+  if (c.mode == SORT_PACKED) {
+    key = ps.src == SORT_BUF_INPUT ? pack_input(b.fl, c, b.in_keys[gi], (uint64_t)gi)
+                                   : (ps.src == SORT_BUF_TMP ? b.tmp_keys[gi] : b.out_keys[gi]);
+    val = 0;
+  } else {
+    const SrcPtrs src = pick_src(ps.src, b);
+    key = src.keys[gi];
+    val = src.vals ? src.vals[gi] : (uint32_t)gi;
+  }
+}
+
+__device__ inline uint32_t elem_digit(const PassView& c, const SortPass& ps, const RouteGeom& rg, uint64_t key) {
+  if (c.mode == SORT_PACKED) return (uint32_t)((key >> (c.ib + ps.lo)) & (SORT_BUCKETS - 1));
+  return digit_of(ps, rg, key);
+}
+
 __global__ __launch_bounds__(NT) void k_sort_upsweep(SortBufs b, int64_t n_host, const int64_t* n_dev, int slot,
                                                      RouteGeom rg, int nblocks) {
-  const SortPass ps = b.ctl->plan.pass[slot];
-  if (!ps.active) return;
+  const PassView c = read_pass(b.ctl, slot);
+  const SortPass ps = c.ps;
+  if (!ps.active || c.mode == SORT_PACKED) return;   // packed passes run k_packed_*
   const int64_t n = load_n(n_host, n_dev);
   __shared__ uint32_t s_cnt[NW][SORT_BUCKETS];
   for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
   __syncthreads();
-  const SrcPtrs src = pick_src(ps.src, b);
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-#pragma unroll 4
+#pragma unroll
   for (int j = 0; j < IT; ++j) {
     int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
     bool valid = gi < n;
-    uint32_t dig = valid ? digit_of(ps, rg, src.keys[gi]) : 0u;
+    uint32_t dig = 0;
+    if (valid) {
+      uint64_t key;
+      uint32_t val;
+      load_elem(b, c, ps, gi, key, val);
+      dig = elem_digit(c, ps, rg, key);
+    }
     uint64_t peers = match_digit(dig, valid);
     if (valid && lane == __ffsll((unsigned long long)peers) - 1) s_cnt[w][dig] += (uint32_t)__popcll(peers);
   }
   __syncthreads();
   for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) {
-    uint32_t c = 0;
+    uint32_t cnt = 0;
 #pragma unroll
-    for (int ww = 0; ww < NW; ++ww) c += s_cnt[ww][d];
-    b.hist[(int64_t)d * nblocks + blockIdx.x] = c;
+    for (int ww = 0; ww < NW; ++ww) cnt += s_cnt[ww][d];
+    b.hist[(int64_t)d * nblocks + blockIdx.x] = cnt;
   }
 }
 
 __global__ __launch_bounds__(NT) void k_sort_downsweep(SortBufs b, int64_t n_host, const int64_t* n_dev, int slot,
                                                        RouteGeom rg, int nblocks) {
-  const SortPass ps = b.ctl->plan.pass[slot];
-  if (!ps.active) return;
+  const PassView c = read_pass(b.ctl, slot);
+  const SortPass ps = c.ps;
+  if (!ps.active || c.mode == SORT_PACKED) return;   // packed passes run k_packed_*
   const int64_t n = load_n(n_host, n_dev);
   const int64_t tile0 = (int64_t)blockIdx.x * TILE;
   if (tile0 >= n) return;
+  const bool packed = false;
+  const bool last = (slot + 1 == c.npass);
   __shared__ uint32_t s_cnt[NW][SORT_BUCKETS];
   __shared__ uint32_t s_base[SORT_BUCKETS];
   __shared__ uint32_t s_gbase[SORT_BUCKETS];
@@ -174,17 +343,19 @@ __global__ __launch_bounds__(NT) void k_sort_downsweep(SortBufs b, int64_t n_hos
   for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
   for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) s_gbase[d] = b.hist[(int64_t)d * nblocks + blockIdx.x];
   __syncthreads();
-  const SrcPtrs src = pick_src(ps.src, b);
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   uint64_t key[IT];
   uint32_t val[IT], dig[IT], off[IT];
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
     int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    bool valid = gi < n;
-    key[j] = valid ? src.keys[gi] : 0ull;
-    val[j] = valid ? (src.vals ? src.vals[gi] : (uint32_t)gi) : 0u;
-    dig[j] = valid ? digit_of(ps, rg, key[j]) : 0u;
+    key[j] = 0;
+    val[j] = 0;
+    dig[j] = 0;
+    if (gi < n) {
+      load_elem(b, c, ps, gi, key[j], val[j]);
+      dig[j] = elem_digit(c, ps, rg, key[j]);
+    }
   }
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
@@ -201,20 +372,23 @@ __global__ __launch_bounds__(NT) void k_sort_downsweep(SortBufs b, int64_t n_hos
     off[j] = old + (uint32_t)__popcll(peers & lanemask_lt());
   }
   __syncthreads();
-  // per digit: exclusive prefix over waves, then exclusive scan over digits
+  // per digit: exclusive prefix over waves, then exclusive scan over digits (every
+  // thread takes part in the scan; threads past the last digit add zero)
   uint32_t tot = 0;
-  const int d = threadIdx.x;   // NT == SORT_BUCKETS
   {
+    const int d = threadIdx.x;
     uint32_t run = 0;
+    if (d < SORT_BUCKETS) {
 #pragma unroll
-    for (int ww = 0; ww < NW; ++ww) {
-      uint32_t c = s_cnt[ww][d];
-      s_cnt[ww][d] = run;
-      run += c;
+      for (int ww = 0; ww < NW; ++ww) {
+        uint32_t cc = s_cnt[ww][d];
+        s_cnt[ww][d] = run;
+        run += cc;
+      }
     }
     uint32_t btot;
     uint32_t ex = block_excl_scan<uint32_t, NT>(run, s_wsum, &btot);
-    s_base[d] = ex;
+    if (d < SORT_BUCKETS) s_base[d] = ex;
     tot = btot;
   }
   __syncthreads();
@@ -224,23 +398,216 @@ __global__ __launch_bounds__(NT) void k_sort_downsweep(SortBufs b, int64_t n_hos
     if (gi < n) {
       uint32_t pos = s_base[dig[j]] + s_cnt[w][dig[j]] + off[j];
       s_key[pos] = key[j];
-      s_val[pos] = val[j];
+      if (!packed) s_val[pos] = val[j];
       s_dig[pos] = (uint8_t)dig[j];
     }
   }
   __syncthreads();
   uint64_t* dk = (ps.dst == SORT_BUF_TMP) ? b.tmp_keys : b.out_keys;
   uint32_t* dv = (ps.dst == SORT_BUF_TMP) ? b.tmp_vals : b.out_vals;
-  for (uint32_t e = threadIdx.x; e < tot; e += NT) {
-    uint32_t dg = s_dig[e];
-    uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
-    dk[g] = s_key[e];
-    dv[g] = s_val[e];
+  if (!packed) {
+    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+      const uint32_t dg = s_dig[e];
+      const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
+      dk[g] = s_key[e];
+      dv[g] = s_val[e];
+    }
+  } else if (!last) {
+    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+      const uint32_t dg = s_dig[e];
+      dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = s_key[e];
+    }
+  } else {
+    const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
+    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+      const uint32_t dg = s_dig[e];
+      const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
+      const uint64_t el = s_key[e];
+      b.out_keys[g] = unpack_key(b.fl, c, el);
+      b.out_vals[g] = (uint32_t)(el & imask);
+    }
+  }
+}
+
+
+// ---- packed passes: one 64-bit word per element, (rank | suffix | index) --------
+// The digit is a plain bit field of the word, so LDS holds only the staged words and
+// 16-bit per-wave counters (about 38 KB, four blocks per CU).
+// The first pass composes the packed words from the input keys in its upsweep and
+// leaves them in the ping-pong buffer that the pass does not write; its downsweep
+// reads them from there.
+__device__ inline uint64_t* packed_stage(const SortBufs& b, const PassView& c) {
+  return c.ps.dst == SORT_BUF_TMP ? b.out_keys : b.tmp_keys;
+}
+
+__device__ inline uint64_t packed_load(const SortBufs& b, const PassView& c, int64_t gi) {
+  const SortPass& ps = c.ps;
+  if (ps.src == SORT_BUF_INPUT) return packed_stage(b, c)[gi];
+  return ps.src == SORT_BUF_TMP ? b.tmp_keys[gi] : b.out_keys[gi];
+}
+
+// Packs IT input keys with their ranks: the first probe of every item is issued
+// before any is resolved (independent loads), collisions are resolved afterwards.
+template <int NI>
+__device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n, uint64_t* out) {
+  const int S = c.sbits;
+  const uint64_t mask = c.ct_mask;
+  uint64_t key[NI], p[NI], h[NI], v[NI];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    p[j] = key[j] >> S;
+    h[j] = mix64(p[j] ^ 0xD6E8FEB86659FD93ull) & mask;
+  }
+#pragma unroll
+  for (int j = 0; j < NI; ++j) v[j] = b.fl.ct_key[h[j]];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    if (gi[j] >= n) {
+      out[j] = 0;
+      continue;
+    }
+    uint64_t hh = h[j], vv = v[j];
+    for (uint64_t probe = 0; vv != p[j] && vv != ~0ull && probe < mask; ++probe) {
+      hh = (hh + 1) & mask;
+      vv = b.fl.ct_key[hh];
+    }
+    const uint32_t rank = vv == p[j] ? b.fl.ct_rank[hh] : 0u;
+    const uint64_t suffix = S == 0 ? 0ull : (key[j] & ((1ull << S) - 1ull));
+    const int hi = S + c.ib;
+    const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
+    out[j] = r | (suffix << c.ib) | (uint64_t)gi[j];
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_packed_upsweep(SortBufs b, int64_t n, int slot, int nblocks) {
+  const PassView c = read_pass(b.ctl, slot);
+  if (!c.ps.active || c.mode != SORT_PACKED) return;
+  __shared__ uint32_t s_cnt[NW][SORT_BUCKETS];
+  for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
+  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
+  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
+  const int sh = c.ib + c.ps.lo;
+  uint64_t key[IT];
+  if (c.ps.src == SORT_BUF_INPUT) {
+    int64_t gi[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) gi[j] = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    pack_items<IT>(b, c, gi, n, key);
+    uint64_t* stage = packed_stage(b, c);
+#pragma unroll
+    for (int j = 0; j < IT; ++j)
+      if (gi[j] < n) stage[gi[j]] = key[j];
+  } else {
+#pragma unroll
+    for (int j = 0; j < IT; ++j) {
+      const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+      key[j] = gi < n ? packed_load(b, c, gi) : 0ull;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    const bool valid = gi < n;
+    const uint32_t dig = (uint32_t)((key[j] >> sh) & (SORT_BUCKETS - 1));
+    const uint64_t peers = match_digit(dig, valid);
+    if (valid && lane == __ffsll((unsigned long long)peers) - 1) s_cnt[w][dig] += (uint32_t)__popcll(peers);
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) {
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) cnt += s_cnt[ww][d];
+    b.hist[(int64_t)d * nblocks + blockIdx.x] = cnt;
+  }
+}
+
+__global__ __launch_bounds__(NT) void k_packed_downsweep(SortBufs b, int64_t n, int slot, int nblocks) {
+  const PassView c = read_pass(b.ctl, slot);
+  if (!c.ps.active || c.mode != SORT_PACKED) return;
+  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
+  if (tile0 >= n) return;
+  const bool last = (slot + 1 == c.npass);
+  const int sh = c.ib + c.ps.lo;
+  __shared__ uint16_t s_cnt[NW][SORT_BUCKETS];
+  __shared__ uint32_t s_base[SORT_BUCKETS];
+  __shared__ uint32_t s_gbase[SORT_BUCKETS];
+  __shared__ uint32_t s_wsum[NT / ALTO_WAVE];
+  __shared__ uint64_t s_key[TILE];
+  for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
+  for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) s_gbase[d] = b.hist[(int64_t)d * nblocks + blockIdx.x];
+  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
+  uint64_t key[IT];
+  uint32_t dig[IT], off[IT];
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    key[j] = gi < n ? packed_load(b, c, gi) : 0ull;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    const bool valid = gi < n;
+    dig[j] = (uint32_t)((key[j] >> sh) & (SORT_BUCKETS - 1));
+    const uint64_t peers = match_digit(dig[j], valid);
+    const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
+    uint32_t old = 0;
+    if (valid && lane == leader) {
+      old = s_cnt[w][dig[j]];
+      s_cnt[w][dig[j]] = (uint16_t)(old + (uint32_t)__popcll(peers));
+    }
+    old = __shfl(old, leader);
+    off[j] = old + (uint32_t)__popcll(peers & lanemask_lt());
+  }
+  __syncthreads();
+  uint32_t tot = 0;
+  {
+    const int d = threadIdx.x;
+    uint32_t run = 0;
+    if (d < SORT_BUCKETS) {
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) {
+        const uint32_t cc = s_cnt[ww][d];
+        s_cnt[ww][d] = (uint16_t)run;
+        run += cc;
+      }
+    }
+    uint32_t btot;
+    const uint32_t ex = block_excl_scan<uint32_t, NT>(run, s_wsum, &btot);
+    if (d < SORT_BUCKETS) s_base[d] = ex;
+    tot = btot;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < IT; ++j) {
+    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    if (gi < n) s_key[s_base[dig[j]] + (uint32_t)s_cnt[w][dig[j]] + off[j]] = key[j];
+  }
+  __syncthreads();
+  if (!last) {
+    uint64_t* dk = (c.ps.dst == SORT_BUF_TMP) ? b.tmp_keys : b.out_keys;
+    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+      const uint64_t el = s_key[e];
+      const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
+      dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = el;
+    }
+  } else {
+    const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
+    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+      const uint64_t el = s_key[e];
+      const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
+      const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
+      b.out_keys[g] = unpack_key(b.fl, c, el);
+      b.out_vals[g] = (uint32_t)(el & imask);
+    }
   }
 }
 
 __global__ void k_sort_identity(SortBufs b, int64_t n_host, const int64_t* n_dev) {
-  if (b.ctl->plan.npass != 0) return;
+  if (b.ctl->plan.npass != 0 || b.ctl->plan.idle) return;
   const int64_t n = load_n(n_host, n_dev);
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     b.out_keys[i] = b.in_keys[i];
@@ -337,6 +704,7 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
   __shared__ int s_np;
   __shared__ int s_lo[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
   const int64_t n = load_n(n_host, n_dev);
+  if (n > SORT_SMALL_MAX) return;   // the multi-block path sorts it
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
@@ -497,6 +865,18 @@ int sort_max_dest_windows(const RouteGeom& rg) {
   return (int)cdiv(bits, SORT_RADIX);
 }
 
+int bits_for(int64_t v) {
+  int b = 0;
+  while (b < 63 && ((int64_t)1 << b) <= v) ++b;
+  return b;
+}
+
+void flow_clear_launch(const FlowBufs& fl, SortCtl* ctl, hipStream_t st) {
+  if (fl.hcap <= 0) return;
+  const int64_t blocks = cdiv(fl.hcap, 256);
+  k_flow_clear<<<(int)(blocks < 2048 ? blocks : 2048), 256, 0, st>>>(fl);
+}
+
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
                bool ctl_has_reduction, hipStream_t st) {
   if (n_max <= SORT_SMALL_MAX) {
@@ -505,20 +885,58 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     return ALTO_OK;
   }
   const int nblocks = sort_hist_blocks(n_max);
-  const int grid_r = (int)(n_max < 1 ? 1 : (cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048));
+  const int grid_r = (int)(cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048);
+  if (n_dev) {
+    // the count is known on the device only: small counts go to one workgroup
+    k_sort_small<<<1, 1024, 0, st>>>(b, n_max, n_dev, rg, sort_max_key_windows(key_bits), sort_max_dest_windows(rg));
+  }
   if (!ctl_has_reduction) {
     k_sort_init<<<1, 1, 0, st>>>(b.ctl);
     k_sort_reduce<<<grid_r, 256, 0, st>>>(b.in_keys, n_max, n_dev, rg, b.ctl);
   }
+  if (b.fl.hcap > 0) {
+    // rank the flows in (destination, prefix) order
+    const FlowBufs& fl = b.fl;
+    const int64_t cb = cdiv(fl.hcap, 256);
+    k_flow_compact<<<(int)(cb < 2048 ? cb : 2048), 256, 0, st>>>(fl, b.ctl);
+    k_flow_count<<<1, 1, 0, st>>>(fl, b.ctl);
+    SortBufs fb;
+    memset(&fb, 0, sizeof(fb));
+    fb.in_keys = fl.flow_key;
+    fb.tmp_keys = fl.ftmp_keys;
+    fb.tmp_vals = fl.ftmp_vals;
+    fb.out_keys = fl.flow_sorted;
+    fb.out_vals = fl.flow_order;
+    fb.hist = fl.fhist;
+    fb.scan_part = b.scan_part;
+    fb.ctl = fl.fctl;
+    RouteGeom frg = rg;
+    frg.shift = 0;   // the flow keys are already prefixes of the route level
+    int rc = sort_pairs(fb, fl.fcap, &b.ctl->nflows_c, frg, key_bits - fl.shift, false, st);
+    if (rc) return rc;
+    const int64_t rb = cdiv(fl.fcap, 256);
+    k_flow_rank<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, n_max);
+    k_ct_insert<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl);
+  }
   const int mk = sort_max_key_windows(key_bits), md = sort_max_dest_windows(rg);
-  k_sort_plan<<<1, 1, 0, st>>>(b.ctl, mk, md);
+  int maxp = mk + md;
+  if (b.fl.hcap > 0) {
+    // packed windows cover at most 64 - index bits
+    const int mp = (int)cdiv(64 - b.fl.ib, SORT_RADIX);
+    if (mp > maxp) maxp = mp;
+  }
+  if (maxp > SORT_MAX_PASSES) maxp = SORT_MAX_PASSES;
+  k_sort_plan<<<1, 1, 0, st>>>(b.ctl, n_max, n_dev, mk, md, nblocks);
   ALTO_LAUNCH_CHECK();
-  for (int slot = 0; slot < mk + md; ++slot) {
+  const bool packable = b.fl.hcap > 0 && n_dev == nullptr;   // packed mode needs a host-known count
+  for (int slot = 0; slot < maxp; ++slot) {
     k_sort_upsweep<<<nblocks, NT, 0, st>>>(b, n_max, n_dev, slot, rg, nblocks);
-    int rc = scan_exclusive<uint32_t>(b.hist, b.hist, (int64_t)SORT_BUCKETS * nblocks, nullptr, b.scan_part,
-                                      nullptr, st);
+    if (packable) k_packed_upsweep<<<nblocks, NT, 0, st>>>(b, n_max, slot, nblocks);
+    int rc = scan_exclusive<uint32_t>(b.hist, b.hist, (int64_t)SORT_BUCKETS * nblocks, &b.ctl->plan.hist_len[slot],
+                                      b.scan_part, nullptr, st);
     if (rc) return rc;
     k_sort_downsweep<<<nblocks, NT, 0, st>>>(b, n_max, n_dev, slot, rg, nblocks);
+    if (packable) k_packed_downsweep<<<nblocks, NT, 0, st>>>(b, n_max, slot, nblocks);
   }
   k_sort_identity<<<grid_r, 256, 0, st>>>(b, n_max, n_dev);
   ALTO_LAUNCH_CHECK();

@@ -109,8 +109,14 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
     ctl->merged = Lc + n;
     ctl->merged1 = Lc + n + 1;
   }
-  uint64_t fp[ALTO_MAX_LEVELS + 1];
-  for (int m = flo; m <= fhi; ++m) fp[m] = 0;
+  const int nl = fhi - flo + 1;
+  uint64_t fp[ALTO_MAX_LEVELS];
+  int sh[ALTO_MAX_LEVELS];
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
+    fp[q] = 0;
+    sh[q] = q < nl ? g.shift[flo + q] : 64;
+  }
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < Lc + n; t += (int64_t)gridDim.x * blockDim.x) {
     if (t < Lc) {
       const uint64_t k = live.key[t];
@@ -121,8 +127,10 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
       }
       mkey[t + lo] = k;
       msrc[t + lo] = (int32_t)(-1 - t);
-      for (int m = flo; m <= fhi; ++m)
-        fp[m] += fan_term(m, key_prefix(k, g.shift[m]), (uint32_t)live.fan[(int64_t)(m - 1) * cap + t]);
+#pragma unroll
+      for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
+        if (q < nl)
+          fp[q] += fan_term(flo + q, key_prefix(k, sh[q]), (uint32_t)live.fan[(int64_t)(flo + q - 1) * cap + t]);
     } else {
       const int64_t j = t - Lc;
       const uint64_t k = sk[j];
@@ -135,9 +143,12 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
       msrc[j + lo] = (int32_t)sperm[j];
     }
   }
-  for (int m = flo; m <= fhi; ++m) {
-    const uint64_t v = wave_sum(fp[m]);
-    if (lane_id() == 0 && v) atomicAdd((unsigned long long*)&fp_in[m], (unsigned long long)v);
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
+    if (q < nl) {
+      const uint64_t v = wave_sum(fp[q]);
+      if (lane_id() == 0 && v) atomicAdd((unsigned long long*)&fp_in[flo + q], (unsigned long long)v);
+    }
   }
 }
 

@@ -34,6 +34,9 @@ CASES = [
     (6, (3, 3, 3, 3, 3, 4), (2, 3, 2, 3, 5), 6, 4, 2, 4, 256, 0.08, 64),
     (3, (20, 12, 12), (40, 3000), 3, 2, 0, 2, 64, 0.01, 768),      # groups span many chunks
     (4, (31, 8, 8, 10), (200, 1, 1000), 2, 1, 3, 1, 1000, 0.0, 4),  # one giant group per root
+    # mask above the route level with more than one workgroup's worth of fragments
+    (5, (6, 3, 2, 3, 8), (4, 3, 5, 60), 20, 4, 2, 3, 64, 0.02, 8),
+    (6, (3, 12, 12, 12, 12, 12), (3, 4, 30, 60, 40), 2, 4, 2, 4, 256, 0.0, 128),
 ]
 
 
