@@ -25,7 +25,7 @@
  *  - Data-dependent problems are written to the device word *status, which the
  *    caller sets to 0 beforehand and reads after its own synchronisation. When
  *    several problems are present the one reported is, in decreasing priority:
- *    LAYOUT, LATE, FANOUT, DUPLICATE, CAPACITY. After a data error the outputs are
+ *    INTERNAL, LAYOUT, LATE, FANOUT, DUPLICATE, CAPACITY. After a data error the outputs are
  *    undefined and a stream handle is poisoned; writes always stay inside the
  *    buffers and capacities given.
  *  - Level-major arrays: element (l, i) of a [levels][n] array lives at
@@ -59,7 +59,9 @@ typedef enum {
   ALTO_E_LATE = 5,       /* stream: fragment of a group that was already emitted */
   ALTO_E_CAPACITY = 6,   /* an output or state capacity is too small; the sizes
                             needed are written to counts[] */
-  ALTO_E_HIP = 7         /* a HIP launch failed */
+  ALTO_E_HIP = 7,        /* a HIP launch failed */
+  ALTO_E_INTERNAL = 8    /* a bounded device-side wait gave up (not expected in
+                            operation; outputs are invalid) */
 } alto_status;
 
 /* Key layout: depth d in [2, 16] levels; bits[l-1] >= 1 bits for level l, level 1

@@ -92,6 +92,10 @@ struct PrepPartial {
 struct AggBufs {
   PrepPartial* prep_part;   // per-block records of the input-order pass
   FlowBufs fl;          // flows of the route level (packed sort); hcap == 0 when unused
+  uint32_t* os_status;  // sort passes: [2][tiles][256] tile status words
+  uint32_t* os_ctr;     // [SORT_MAX_PASSES] tile tickets
+  uint32_t* os_hist;    // [SORT_MAX_PASSES][256] digit counts / bases
+  int64_t os_ntiles;
   SortCtl* ctl;
   SortCtl* rctl;
   uint64_t* fp_in;
@@ -103,8 +107,6 @@ struct AggBufs {
   uint64_t* sk;
   uint32_t* perm;
   uint32_t* perm_used;  // perm buffer the sort wrote (caller's or ours)
-  uint32_t* hist;
-  uint32_t* scan_u32;
   int32_t* scan_i32;
   int64_t* scan_i64;
   int32_t* blkcnt;

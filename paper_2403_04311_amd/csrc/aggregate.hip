@@ -518,8 +518,10 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   b.tmp_vals = c.take<uint32_t>(n);
   b.sk = c.take<uint64_t>(n);
   b.perm = c.take<uint32_t>(n);
-  b.hist = c.take<uint32_t>((int64_t)SORT_BUCKETS * sort_hist_blocks(n));
-  b.scan_u32 = c.take<uint32_t>(SCAN_MAX_BLOCKS + 1);
+  b.os_ntiles = sort_tiles(n);
+  b.os_status = c.take<uint32_t>(2 * b.os_ntiles * SORT_BUCKETS);
+  b.os_ctr = c.take<uint32_t>(SORT_MAX_PASSES);
+  b.os_hist = c.take<uint32_t>((int64_t)SORT_MAX_PASSES * SORT_BUCKETS);
   b.scan_i32 = c.take<int32_t>(SCAN_MAX_BLOCKS + 1);
   b.scan_i64 = c.take<int64_t>(SCAN_MAX_BLOCKS + 1);
   memset(&b.fl, 0, sizeof(b.fl));
@@ -542,7 +544,6 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
     f.flow_order = c.take<uint32_t>(f.fcap);
     f.ftmp_keys = c.take<uint64_t>(f.fcap);
     f.ftmp_vals = c.take<uint32_t>(f.fcap);
-    f.fhist = c.take<uint32_t>((int64_t)SORT_BUCKETS * sort_hist_blocks(f.fcap));
     f.fctl = c.take<SortCtl>(1);
   }
   if (!agg) return;
@@ -609,10 +610,13 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   sb.tmp_vals = b.tmp_vals;
   sb.out_keys = b.sk;
   sb.out_vals = perm_out ? reinterpret_cast<uint32_t*>(perm_out) : b.perm;
-  sb.hist = b.hist;
-  sb.scan_part = b.scan_u32;
   sb.ctl = b.ctl;
   sb.fl = b.fl;
+  sb.os_status = b.os_status;
+  sb.os_ctr = b.os_ctr;
+  sb.os_hist = b.os_hist;
+  sb.os_ntiles = b.os_ntiles;
+  sb.status = status;
   b.perm_used = sb.out_vals;
   int rc = sort_pairs(sb, n, nullptr, rg, g.total, true, st);
   if (rc) return rc;
@@ -675,9 +679,12 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     rb.tmp_vals = b.tmp_vals;
     rb.out_keys = b.rsk;
     rb.out_vals = b.ridx;
-    rb.hist = b.hist;
-    rb.scan_part = b.scan_u32;
     rb.ctl = b.rctl;
+    rb.os_status = b.os_status;
+    rb.os_ctr = b.os_ctr;
+    rb.os_hist = b.os_hist;
+    rb.os_ntiles = b.os_ntiles;
+    rb.status = status;
     RouteGeom none;
     none.shift = 64;
     none.num_dest = 1;

@@ -60,6 +60,7 @@ __host__ __device__ inline uint64_t fan_term(int level, uint64_t node, uint32_t 
 // ---------------------------------------------------------------------------
 __host__ __device__ inline int status_priority(int code) {
   switch (code) {
+    case ALTO_E_INTERNAL: return 6;
     case ALTO_E_LAYOUT: return 5;
     case ALTO_E_LATE: return 4;
     case ALTO_E_FANOUT: return 3;

@@ -23,7 +23,6 @@ struct SortPlan {
   int32_t npass;
   int32_t idle;          // the multi-block path does nothing (sorted in one workgroup)
   SortPass pass[SORT_MAX_PASSES];
-  int64_t hist_len[SORT_MAX_PASSES];   // histogram entries to scan per pass (0 = inactive)
 };
 
 // Device control block of one sort.
@@ -59,7 +58,6 @@ struct FlowBufs {
   uint32_t* flow_order;  // [fcap]
   uint64_t* ftmp_keys;   // [fcap] sort scratch
   uint32_t* ftmp_vals;
-  uint32_t* fhist;       // [256 * sort_hist_blocks(fcap)]
   SortCtl* fctl;
   int64_t fcap;
 };
@@ -70,13 +68,17 @@ struct SortBufs {
   uint32_t* tmp_vals;
   uint64_t* out_keys;        // sorted keys
   uint32_t* out_vals;        // input index of each sorted key
-  uint32_t* hist;            // [256 * sort_hist_blocks(n_max)]
-  uint32_t* scan_part;       // [SCAN_MAX_BLOCKS + 1]
   SortCtl* ctl;
   FlowBufs fl;               // hcap == 0: general mode only
+  // multi-block passes (n_max > SORT_SMALL_MAX)
+  uint32_t* os_status;       // [2][os_ntiles][256] tile status words, two alternating regions
+  uint32_t* os_ctr;          // [SORT_MAX_PASSES] tile tickets
+  uint32_t* os_hist;         // [SORT_MAX_PASSES][256] global digit counts, then bases
+  int64_t os_ntiles;         // >= sort_tiles(n_max)
+  int32_t* status;           // raised to ALTO_E_INTERNAL if a look-back wait gives up (may be null)
 };
 
-int sort_hist_blocks(int64_t n_max);
+int sort_tiles(int64_t n_max);   // tiles of SORT_TILE elements
 int sort_max_key_windows(int key_bits);
 int sort_max_dest_windows(const RouteGeom& rg);
 int bits_for(int64_t v);     // bits needed to hold values 0..v
@@ -85,7 +87,8 @@ int bits_for(int64_t v);     // bits needed to hold values 0..v
 // key_bits bounds the width of the keys. If ctl_has_reduction, ctl already holds
 // the OR/AND of keys and destinations (see sort_reduce_launch). With b.fl.hcap > 0
 // the flow set must have been filled (flow_insert in the input pass); the sort
-// then ranks the flows and runs in packed mode when the packing fits.
+// then ranks the flows and runs in packed mode when the packing fits. Returns
+// ALTO_E_ARG if n_max needs multi-block passes and the os_* buffers are missing.
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
                bool ctl_has_reduction, hipStream_t st);
 void sort_reduce_launch(const uint64_t* keys, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, SortCtl* ctl,

@@ -86,7 +86,7 @@ __device__ inline int greedy_windows(uint64_t v, int limit, int from_dest, SortP
 // ping-pong so that the last pass lands in the final buffers. With a device-side
 // count of at most SORT_SMALL_MAX the one-workgroup sort has done the work.
 __global__ void k_sort_plan(SortCtl* ctl, int64_t n_host, const int64_t* n_dev, int max_key_windows,
-                            int max_dest_windows, int nblocks) {
+                            int max_dest_windows) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   const int64_t n = load_n(n_host, n_dev);
   SortPlan p;
@@ -114,9 +114,7 @@ __global__ void k_sort_plan(SortCtl* ctl, int64_t n_host, const int64_t* n_dev, 
     p.pass[k].from_dest = p.pass[k].lo = 0;
   }
   p.npass = np;
-  for (int k = 0; k < SORT_MAX_PASSES; ++k) p.hist_len[k] = p.pass[k].active ? (int64_t)SORT_BUCKETS * nblocks : 0;
   ctl->plan = p;
-  ctl->hist_len = p.idle ? 0 : (int64_t)SORT_BUCKETS * nblocks;
 }
 
 __device__ inline uint32_t digit_of(const SortPass& ps, const RouteGeom& rg, uint64_t k) {
@@ -180,14 +178,15 @@ __global__ void k_flow_count(FlowBufs fl, SortCtl* ctl) {
 }
 
 // Rank of every flow in (destination, prefix) order, and the choice of mode.
-__global__ void k_flow_rank(FlowBufs fl, SortCtl* ctl, int64_t n) {
+__global__ void k_flow_rank(FlowBufs fl, SortCtl* ctl, int64_t n, int allow_packed) {
   const int64_t F = ctl->nflows_c;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < F; r += (int64_t)gridDim.x * blockDim.x)
     fl.ht_rank[fl.flow_slot[fl.flow_order[r]]] = (uint32_t)r;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     int R = 0;
     while (R < 63 && ((int64_t)1 << R) < F) ++R;
-    const bool fits = !ctl->flow_overflow && ctl->nflows <= fl.fcap && F >= 1 && R + fl.shift + fl.ib <= 64;
+    const bool fits = allow_packed && !ctl->flow_overflow && ctl->nflows <= fl.fcap && F >= 1 &&
+                      R + fl.shift + fl.ib <= 64;
     ctl->mode = fits ? SORT_PACKED : SORT_GENERAL;
     int64_t t = 64;
     while (t < 2 * F && t < fl.hcap) t <<= 1;
@@ -217,235 +216,45 @@ __device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
   return v;
 }
 
-__device__ inline uint64_t pack_input(const FlowBufs& fl, const PassView& c, uint64_t key, uint64_t idx) {
-  const int S = c.sbits;
-  const uint64_t p = key >> S;
-  const uint64_t mask = c.ct_mask;
-  uint64_t h = mix64(p ^ 0xD6E8FEB86659FD93ull) & mask;
-  uint32_t rank = 0;
-  for (uint64_t probe = 0; probe <= mask; ++probe) {
-    const uint64_t v = fl.ct_key[h];
-    if (v == p) {
-      rank = fl.ct_rank[h];
-      break;
-    }
-    if (v == ~0ull) break;
-    h = (h + 1) & mask;
-  }
-  const uint64_t suffix = S == 0 ? 0ull : (key & ((1ull << S) - 1ull));
-  const int hi = S + c.ib;
-  const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
-  return r | (suffix << c.ib) | idx;
-}
-
-__device__ inline uint64_t unpack_key(const FlowBufs& fl, const PassView& c, uint64_t e) {
+__device__ inline uint64_t unpack_key(const uint64_t* flow_sorted, const PassView& c, uint64_t e) {
   const int S = c.sbits, hi = S + c.ib;
   const uint64_t rank = hi >= 64 ? 0ull : (e >> hi);
   const uint64_t suffix = S == 0 ? 0ull : ((e >> c.ib) & ((1ull << S) - 1ull));
-  return (fl.flow_sorted[rank] << S) | suffix;
+  return (flow_sorted[rank] << S) | suffix;
 }
 
-struct SrcPtrs {
-  const uint64_t* keys;
-  const uint32_t* vals;   // nullptr: value = index
-};
-
-__device__ inline SrcPtrs pick_src(int sel, const SortBufs& b) {
-  if (sel == SORT_BUF_INPUT) return {b.in_keys, nullptr};
-  if (sel == SORT_BUF_TMP) return {b.tmp_keys, b.tmp_vals};
-  return {b.out_keys, b.out_vals};
+// A pointer value hidden from the optimiser: selecting between buffers of the
+// by-value argument struct then selects values, not addresses inside the struct
+// (which would force a copy of the struct into scratch memory).
+template <typename T>
+__device__ inline T* opaque(T* p) {
+  const uint64_t v = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (T*)(((uint64_t)hi << 32) | lo);
 }
 
 // Stable in-wave ranking of one row of 64 digits: the lane mask of the valid lanes
-// holding the same digit as this lane.
+// holding the same digit as this lane. Per digit bit, one ballot; each lane keeps
+// the OR over bits of (ballot XOR its own bit spread over 32 lanes), a lane whose
+// bits all agree being a peer. One v_bitop3 per half-mask (truth table 0xF6 is
+// a | (b ^ c), with the operands weighted 0xF0, 0xCC, 0xAA).
 __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
-  uint64_t peers = __ballot(valid);
+  uint32_t lo = 0, hi = 0;
 #pragma unroll
   for (int b = 0; b < SORT_RADIX; ++b) {
-    bool bit = (dig >> b) & 1u;
-    uint64_t m = __ballot(bit);
-    peers &= bit ? m : ~m;
+    const uint32_t sx = (uint32_t)((int32_t)(dig << (31 - b)) >> 31);   // 0 or ~0
+    const uint64_t m = __ballot(sx != 0);
+    lo = __builtin_amdgcn_bitop3_b32(lo, (uint32_t)m, sx, 0xF6);
+    hi = __builtin_amdgcn_bitop3_b32(hi, (uint32_t)(m >> 32), sx, 0xF6);
   }
-  return peers;
+  return __ballot(valid) & ~(((uint64_t)hi << 32) | lo);
 }
-
-// Loads element gi of the pass input: in packed mode one word (composed from the
-// input key on the first pass), in general mode a key and a value.
-__device__ inline void load_elem(const SortBufs& b, const PassView& c, const SortPass& ps, int64_t gi, uint64_t& key,
-                                 uint32_t& val) {
-  if (c.mode == SORT_PACKED) {
-    key = ps.src == SORT_BUF_INPUT ? pack_input(b.fl, c, b.in_keys[gi], (uint64_t)gi)
-                                   : (ps.src == SORT_BUF_TMP ? b.tmp_keys[gi] : b.out_keys[gi]);
-    val = 0;
-  } else {
-    const SrcPtrs src = pick_src(ps.src, b);
-    key = src.keys[gi];
-    val = src.vals ? src.vals[gi] : (uint32_t)gi;
-  }
-}
-
-__device__ inline uint32_t elem_digit(const PassView& c, const SortPass& ps, const RouteGeom& rg, uint64_t key) {
-  if (c.mode == SORT_PACKED) return (uint32_t)((key >> (c.ib + ps.lo)) & (SORT_BUCKETS - 1));
-  return digit_of(ps, rg, key);
-}
-
-__global__ __launch_bounds__(NT) void k_sort_upsweep(SortBufs b, int64_t n_host, const int64_t* n_dev, int slot,
-                                                     RouteGeom rg, int nblocks) {
-  const PassView c = read_pass(b.ctl, slot);
-  const SortPass ps = c.ps;
-  if (!ps.active || c.mode == SORT_PACKED) return;   // packed passes run k_packed_*
-  const int64_t n = load_n(n_host, n_dev);
-  __shared__ uint32_t s_cnt[NW][SORT_BUCKETS];
-  for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
-  __syncthreads();
-  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
-  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    bool valid = gi < n;
-    uint32_t dig = 0;
-    if (valid) {
-      uint64_t key;
-      uint32_t val;
-      load_elem(b, c, ps, gi, key, val);
-      dig = elem_digit(c, ps, rg, key);
-    }
-    uint64_t peers = match_digit(dig, valid);
-    if (valid && lane == __ffsll((unsigned long long)peers) - 1) s_cnt[w][dig] += (uint32_t)__popcll(peers);
-  }
-  __syncthreads();
-  for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) {
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int ww = 0; ww < NW; ++ww) cnt += s_cnt[ww][d];
-    b.hist[(int64_t)d * nblocks + blockIdx.x] = cnt;
-  }
-}
-
-__global__ __launch_bounds__(NT) void k_sort_downsweep(SortBufs b, int64_t n_host, const int64_t* n_dev, int slot,
-                                                       RouteGeom rg, int nblocks) {
-  const PassView c = read_pass(b.ctl, slot);
-  const SortPass ps = c.ps;
-  if (!ps.active || c.mode == SORT_PACKED) return;   // packed passes run k_packed_*
-  const int64_t n = load_n(n_host, n_dev);
-  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-  if (tile0 >= n) return;
-  const bool packed = false;
-  const bool last = (slot + 1 == c.npass);
-  __shared__ uint32_t s_cnt[NW][SORT_BUCKETS];
-  __shared__ uint32_t s_base[SORT_BUCKETS];
-  __shared__ uint32_t s_gbase[SORT_BUCKETS];
-  __shared__ uint32_t s_wsum[NT / ALTO_WAVE];
-  __shared__ uint64_t s_key[TILE];
-  __shared__ uint32_t s_val[TILE];
-  __shared__ uint8_t s_dig[TILE];
-  for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
-  for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) s_gbase[d] = b.hist[(int64_t)d * nblocks + blockIdx.x];
-  __syncthreads();
-  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
-  uint64_t key[IT];
-  uint32_t val[IT], dig[IT], off[IT];
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    key[j] = 0;
-    val[j] = 0;
-    dig[j] = 0;
-    if (gi < n) {
-      load_elem(b, c, ps, gi, key[j], val[j]);
-      dig[j] = elem_digit(c, ps, rg, key[j]);
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    bool valid = gi < n;
-    uint64_t peers = match_digit(dig[j], valid);
-    int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
-    uint32_t old = 0;
-    if (valid && lane == leader) {
-      old = s_cnt[w][dig[j]];
-      s_cnt[w][dig[j]] = old + (uint32_t)__popcll(peers);
-    }
-    old = __shfl(old, leader);
-    off[j] = old + (uint32_t)__popcll(peers & lanemask_lt());
-  }
-  __syncthreads();
-  // per digit: exclusive prefix over waves, then exclusive scan over digits (every
-  // thread takes part in the scan; threads past the last digit add zero)
-  uint32_t tot = 0;
-  {
-    const int d = threadIdx.x;
-    uint32_t run = 0;
-    if (d < SORT_BUCKETS) {
-#pragma unroll
-      for (int ww = 0; ww < NW; ++ww) {
-        uint32_t cc = s_cnt[ww][d];
-        s_cnt[ww][d] = run;
-        run += cc;
-      }
-    }
-    uint32_t btot;
-    uint32_t ex = block_excl_scan<uint32_t, NT>(run, s_wsum, &btot);
-    if (d < SORT_BUCKETS) s_base[d] = ex;
-    tot = btot;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    if (gi < n) {
-      uint32_t pos = s_base[dig[j]] + s_cnt[w][dig[j]] + off[j];
-      s_key[pos] = key[j];
-      if (!packed) s_val[pos] = val[j];
-      s_dig[pos] = (uint8_t)dig[j];
-    }
-  }
-  __syncthreads();
-  uint64_t* dk = (ps.dst == SORT_BUF_TMP) ? b.tmp_keys : b.out_keys;
-  uint32_t* dv = (ps.dst == SORT_BUF_TMP) ? b.tmp_vals : b.out_vals;
-  if (!packed) {
-    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
-      const uint32_t dg = s_dig[e];
-      const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
-      dk[g] = s_key[e];
-      dv[g] = s_val[e];
-    }
-  } else if (!last) {
-    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
-      const uint32_t dg = s_dig[e];
-      dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = s_key[e];
-    }
-  } else {
-    const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
-    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
-      const uint32_t dg = s_dig[e];
-      const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
-      const uint64_t el = s_key[e];
-      b.out_keys[g] = unpack_key(b.fl, c, el);
-      b.out_vals[g] = (uint32_t)(el & imask);
-    }
-  }
-}
-
 
 // ---- packed passes: one 64-bit word per element, (rank | suffix | index) --------
 // The digit is a plain bit field of the word, so LDS holds only the staged words and
-// 16-bit per-wave counters (about 38 KB, four blocks per CU).
-// The first pass composes the packed words from the input keys in its upsweep and
-// leaves them in the ping-pong buffer that the pass does not write; its downsweep
-// reads them from there.
-__device__ inline uint64_t* packed_stage(const SortBufs& b, const PassView& c) {
-  return c.ps.dst == SORT_BUF_TMP ? b.out_keys : b.tmp_keys;
-}
-
-__device__ inline uint64_t packed_load(const SortBufs& b, const PassView& c, int64_t gi) {
-  const SortPass& ps = c.ps;
-  if (ps.src == SORT_BUF_INPUT) return packed_stage(b, c)[gi];
-  return ps.src == SORT_BUF_TMP ? b.tmp_keys[gi] : b.out_keys[gi];
-}
-
+// 16-bit per-wave counters. The words are composed once from the input keys and
+// staged in the ping-pong buffer that the first pass does not write.
 // Packs IT input keys with their ranks: the first probe of every item is issued
 // before any is resolved (independent loads), collisions are resolved afterwards.
 template <int NI>
@@ -481,54 +290,143 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
   }
 }
 
-__global__ __launch_bounds__(NT) void k_packed_upsweep(SortBufs b, int64_t n, int slot, int nblocks) {
-  const PassView c = read_pass(b.ctl, slot);
-  if (!c.ps.active || c.mode != SORT_PACKED) return;
-  __shared__ uint32_t s_cnt[NW][SORT_BUCKETS];
-  for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
-  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
-  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-  const int sh = c.ib + c.ps.lo;
-  uint64_t key[IT];
-  if (c.ps.src == SORT_BUF_INPUT) {
-    int64_t gi[IT];
-#pragma unroll
-    for (int j = 0; j < IT; ++j) gi[j] = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    pack_items<IT>(b, c, gi, n, key);
-    uint64_t* stage = packed_stage(b, c);
-#pragma unroll
-    for (int j = 0; j < IT; ++j)
-      if (gi[j] < n) stage[gi[j]] = key[j];
-  } else {
-#pragma unroll
-    for (int j = 0; j < IT; ++j) {
-      const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-      key[j] = gi < n ? packed_load(b, c, gi) : 0ull;
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    const bool valid = gi < n;
-    const uint32_t dig = (uint32_t)((key[j] >> sh) & (SORT_BUCKETS - 1));
-    const uint64_t peers = match_digit(dig, valid);
-    if (valid && lane == __ffsll((unsigned long long)peers) - 1) s_cnt[w][dig] += (uint32_t)__popcll(peers);
-  }
-  __syncthreads();
-  for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) {
-    uint32_t cnt = 0;
-#pragma unroll
-    for (int ww = 0; ww < NW; ++ww) cnt += s_cnt[ww][d];
-    b.hist[(int64_t)d * nblocks + blockIdx.x] = cnt;
+// ---- single-pass passes (decoupled look-back) -----------------------------------
+// Each pass is one persistent kernel. A block takes tile tickets in order; for a
+// tile it ranks the digits locally, publishes the tile's per-digit counts, and looks
+// back over earlier tiles (whose tickets were taken before, so they are running or
+// done) for the exclusive prefix of every digit; global digit bases come from
+// counts taken for all passes in one earlier sweep over the input. Status words:
+// 0 = not yet published, bit 31 = inclusive prefix in bits 0-30, bit 30 = tile
+// count in bits 0-29. Two status regions alternate between passes; a pass clears
+// the other region at its own tiles for the next pass.
+#define OS_INC (1u << 31)
+#define OS_AGG (1u << 30)
+#define OS_SPIN_LIMIT (1 << 22)
+#define OS_LOOKBACK 4
+#define OS_GRID 1024
+
+__device__ inline uint32_t os_value(uint32_t w) { return (w & OS_INC) ? (w & ~OS_INC) : (w & (OS_AGG - 1u)); }
+
+// Counter copies of the digit counting sweep: 16-bit counters, two digits to a word,
+// `copies` copies picked by lane so that a row whose lanes share one digit (common
+// for flow-rank digits) makes at most 64 / copies same-address LDS atomics; copies
+// sit in consecutive words (banks).
+__host__ __device__ inline int os_copies(int passes) { return passes <= 7 ? 16 : 8; }
+__host__ __device__ inline int os_hist_max_tiles(int copies) { return 65535 / (SORT_TILE / copies); }
+
+__global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev) {
+  const int64_t n = load_n(n_host, n_dev);
+  const int64_t len = cdiv(n, TILE) * SORT_BUCKETS;   // status region 0
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
+    b.os_status[i] = 0;
+  if (blockIdx.x == 0) {
+    for (int i = threadIdx.x; i < SORT_MAX_PASSES * SORT_BUCKETS; i += blockDim.x) b.os_hist[i] = 0;
+    if (threadIdx.x < SORT_MAX_PASSES) b.os_ctr[threadIdx.x] = 0;
   }
 }
 
-__global__ __launch_bounds__(NT) void k_packed_downsweep(SortBufs b, int64_t n, int slot, int nblocks) {
+// Digit counts of every pass, in one sweep over the input. Packed mode also
+// composes the words and stages them for the first pass. Persistent.
+__global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
+                                                  int max_passes, int copies) {
+  const PassView c = read_pass(b.ctl, 0);
+  if (c.npass == 0) return;   // nothing varies, or sorted in one workgroup
+  const int64_t n = load_n(n_host, n_dev);
+  const int64_t ntiles = cdiv(n, TILE);
+  const bool packed = c.mode == SORT_PACKED;
+  extern __shared__ uint32_t s_hw[];
+  __shared__ int s_sh[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
+  const int np = c.npass < max_passes ? c.npass : max_passes;   // npass <= max_passes by the plan
+  const int wpp = 128 * copies;   // words per pass
+  for (int i = threadIdx.x; i < np * wpp; i += NT) s_hw[i] = 0;
+  if (threadIdx.x < SORT_MAX_PASSES) {
+    const SortPass ps = b.ctl->plan.pass[threadIdx.x];
+    s_sh[threadIdx.x] = (packed ? c.ib : 0) + ps.lo;
+    s_fd[threadIdx.x] = packed ? 0 : ps.from_dest;
+  }
+  __syncthreads();
+  bool any_dest = false;
+  for (int q = 0; q < np; ++q) any_dest |= s_fd[q] != 0;
+  uint64_t* const stage = packed ? (c.ps.dst == SORT_BUF_TMP ? opaque(b.out_keys) : opaque(b.tmp_keys)) : nullptr;
+  const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
+  const int copy = lane & (copies - 1);
+  for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int64_t tile0 = t * TILE;
+    int64_t gi[IT];
+    uint64_t key[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) gi[j] = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    if (packed) {
+      pack_items<IT>(b, c, gi, n, key);
+#pragma unroll
+      for (int j = 0; j < IT; ++j)
+        if (gi[j] < n) stage[gi[j]] = key[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < IT; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
+    }
+    uint32_t dv[IT];
+#pragma unroll
+    for (int j = 0; j < IT; ++j) dv[j] = any_dest ? dest_of_key(rg, key[j]) : 0u;
+    for (int q = 0; q < np; ++q) {
+      const int sh = s_sh[q];
+      const bool fd = s_fd[q] != 0;
+      uint32_t* hq = s_hw + q * wpp;
+#pragma unroll
+      for (int j = 0; j < IT; ++j) {
+        if (gi[j] >= n) continue;
+        const uint64_t src = fd ? (uint64_t)dv[j] : key[j];
+        const uint32_t dig = (uint32_t)((src >> sh) & (SORT_BUCKETS - 1));
+        atomicAdd(&hq[(dig >> 1) * copies + copy], (dig & 1u) ? 65536u : 1u);
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < np * SORT_BUCKETS; i += NT) {
+    const int q = i / SORT_BUCKETS, d = i % SORT_BUCKETS;
+    const uint32_t* hq = s_hw + q * wpp + (d >> 1) * copies;
+    uint32_t v = 0;
+    for (int k = 0; k < copies; ++k) v += (hq[k] >> ((d & 1) * 16)) & 0xFFFFu;
+    if (v) atomicAdd(&b.os_hist[i], v);
+  }
+}
+
+// Exclusive scan of each pass's 256 global digit counts (one wave per pass).
+__global__ void k_os_bases(SortBufs b) {
+  const int q = threadIdx.x / ALTO_WAVE, lane = lane_id();
+  if (q >= SORT_MAX_PASSES) return;
+  uint32_t* h = b.os_hist + q * SORT_BUCKETS;
+  uint32_t v[4], s = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    v[k] = h[lane * 4 + k];
+    s += v[k];
+  }
+  const uint32_t inc = wave_incl_scan(s);
+  uint32_t run = inc - s;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    h[lane * 4 + k] = run;
+    run += v[k];
+  }
+}
+
+__device__ inline uint32_t pass_digit(bool packed, const SortPass& ps, int sh, const RouteGeom& rg, uint64_t el) {
+  return packed ? (uint32_t)((el >> sh) & (SORT_BUCKETS - 1)) : digit_of(ps, rg, el);
+}
+
+// One pass over all tiles. Packed mode moves one word per element (the last pass
+// unpacks it into key and input index); general mode moves a key and a value. One
+// instantiation per mode (each exits when the device chose the other), so that the
+// packed one keeps the registers of its simpler digits.
+template <bool PACKED>
+__global__ __launch_bounds__(NT, PACKED ? 6 : 4) void k_onesweep(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
+                                                 int slot, int64_t region) {
   const PassView c = read_pass(b.ctl, slot);
-  if (!c.ps.active || c.mode != SORT_PACKED) return;
-  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-  if (tile0 >= n) return;
+  if (!c.ps.active || (c.mode == SORT_PACKED) != PACKED) return;
+  const int64_t n = load_n(n_host, n_dev);
+  const int64_t ntiles = cdiv(n, TILE);
+  constexpr bool packed = PACKED;
   const bool last = (slot + 1 == c.npass);
   const int sh = c.ib + c.ps.lo;
   __shared__ uint16_t s_cnt[NW][SORT_BUCKETS];
@@ -536,35 +434,59 @@ __global__ __launch_bounds__(NT) void k_packed_downsweep(SortBufs b, int64_t n, 
   __shared__ uint32_t s_gbase[SORT_BUCKETS];
   __shared__ uint32_t s_wsum[NT / ALTO_WAVE];
   __shared__ uint64_t s_key[TILE];
-  for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
-  for (int d = threadIdx.x; d < SORT_BUCKETS; d += NT) s_gbase[d] = b.hist[(int64_t)d * nblocks + blockIdx.x];
+  __shared__ uint16_t s_slot[TILE];   // general mode: position of the element in its tile
+  __shared__ int64_t s_tile;
+  uint32_t* st = b.os_status + (slot & 1) * region;
+  uint32_t* st_next = b.os_status + ((slot + 1) & 1) * region;
+  uint64_t* const tk = opaque(b.tmp_keys);
+  uint64_t* const ok = opaque(b.out_keys);
+  uint32_t* const tv = opaque(b.tmp_vals);
+  uint32_t* const ov = opaque(b.out_vals);
+  const uint64_t* const ik = opaque(b.in_keys);
+  // source: the input keys (general), the staged words (packed, first pass, in the
+  // buffer the pass does not write), or the previous pass's output
+  const uint64_t* sk = c.ps.src == SORT_BUF_TMP ? tk : ok;
+  const uint32_t* sv = c.ps.src == SORT_BUF_TMP ? tv : ov;
+  if (c.ps.src == SORT_BUF_INPUT) {
+    sk = packed ? (c.ps.dst == SORT_BUF_TMP ? ok : tk) : ik;
+    sv = nullptr;
+  }
+  uint64_t* const dk = c.ps.dst == SORT_BUF_TMP ? tk : ok;
+  uint32_t* const dvals = c.ps.dst == SORT_BUF_TMP ? tv : ov;
+  const uint64_t* const fsorted = opaque(b.fl.flow_sorted);
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
-  uint64_t key[IT];
-  uint32_t dig[IT], off[IT];
+  while (true) {
+    if (threadIdx.x == 0) s_tile = (int64_t)atomicAdd(&b.os_ctr[slot], 1u);
+    for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
+    __syncthreads();
+    const int64_t tile = s_tile;
+    if (tile >= ntiles) break;   // uniform across the block
+    const int64_t tile0 = tile * TILE;
+    const int rem = (int)(n - tile0 < TILE ? n - tile0 : TILE);   // elements in this tile
+    const uint64_t* const tsk = sk + tile0;
+    const int lbase = w * (IT * ALTO_WAVE) + lane;               // tile-local index of item 0
+    uint64_t key[IT];
+    uint32_t dof[IT];   // digit | in-wave offset << 8 (offsets < IT * 64)
 #pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    key[j] = gi < n ? packed_load(b, c, gi) : 0ull;
-  }
-  __syncthreads();
+    for (int j = 0; j < IT; ++j) key[j] = lbase + j * ALTO_WAVE < rem ? tsk[lbase + j * ALTO_WAVE] : 0ull;
 #pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    const bool valid = gi < n;
-    dig[j] = (uint32_t)((key[j] >> sh) & (SORT_BUCKETS - 1));
-    const uint64_t peers = match_digit(dig[j], valid);
-    const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
-    uint32_t old = 0;
-    if (valid && lane == leader) {
-      old = s_cnt[w][dig[j]];
-      s_cnt[w][dig[j]] = (uint16_t)(old + (uint32_t)__popcll(peers));
+    for (int j = 0; j < IT; ++j) {
+      const bool valid = lbase + j * ALTO_WAVE < rem;
+      const uint32_t dig = valid ? pass_digit(packed, c.ps, sh, rg, key[j]) : 0u;
+      const uint64_t peers = match_digit(dig, valid);
+      const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
+      uint32_t old = 0;
+      if (valid && lane == leader) {
+        old = s_cnt[w][dig];
+        s_cnt[w][dig] = (uint16_t)(old + (uint32_t)__popcll(peers));
+      }
+      old = __shfl(old, leader);
+      dof[j] = dig | ((old + (uint32_t)__popcll(peers & lanemask_lt())) << 8);
     }
-    old = __shfl(old, leader);
-    off[j] = old + (uint32_t)__popcll(peers & lanemask_lt());
-  }
-  __syncthreads();
-  uint32_t tot = 0;
-  {
+    __syncthreads();
+    // per-wave offsets of every digit, the tile's count published at once (so that
+    // later tiles can pass this one), then the LDS scatter; the look-back comes
+    // after it, when the elements no longer occupy registers
     const int d = threadIdx.x;
     uint32_t run = 0;
     if (d < SORT_BUCKETS) {
@@ -574,35 +496,92 @@ __global__ __launch_bounds__(NT) void k_packed_downsweep(SortBufs b, int64_t n, 
         s_cnt[ww][d] = (uint16_t)run;
         run += cc;
       }
+      __hip_atomic_store(&st[tile * SORT_BUCKETS + d], (tile == 0 ? OS_INC : OS_AGG) | run, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
     }
-    uint32_t btot;
-    const uint32_t ex = block_excl_scan<uint32_t, NT>(run, s_wsum, &btot);
-    if (d < SORT_BUCKETS) s_base[d] = ex;
-    tot = btot;
-  }
-  __syncthreads();
+    uint32_t tot;
+    {
+      const uint32_t ex = block_excl_scan<uint32_t, NT>(run, s_wsum, &tot);
+      if (d < SORT_BUCKETS) s_base[d] = ex;
+    }
+    __syncthreads();
 #pragma unroll
-  for (int j = 0; j < IT; ++j) {
-    const int64_t gi = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
-    if (gi < n) s_key[s_base[dig[j]] + (uint32_t)s_cnt[w][dig[j]] + off[j]] = key[j];
-  }
-  __syncthreads();
-  if (!last) {
-    uint64_t* dk = (c.ps.dst == SORT_BUF_TMP) ? b.tmp_keys : b.out_keys;
-    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
-      const uint64_t el = s_key[e];
-      const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
-      dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = el;
+    for (int j = 0; j < IT; ++j) {
+      if (lbase + j * ALTO_WAVE < rem) {
+        const uint32_t dg = dof[j] & 0xFFu;
+        const uint32_t r = s_base[dg] + (uint32_t)s_cnt[w][dg] + (dof[j] >> 8);
+        s_key[r] = key[j];
+        if (!packed) s_slot[r] = (uint16_t)(lbase + j * ALTO_WAVE);
+      }
     }
-  } else {
-    const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
-    for (uint32_t e = threadIdx.x; e < tot; e += NT) {
-      const uint64_t el = s_key[e];
-      const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
-      const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
-      b.out_keys[g] = unpack_key(b.fl, c, el);
-      b.out_vals[g] = (uint32_t)(el & imask);
+    if (d < SORT_BUCKETS) {
+      uint32_t excl = 0;
+      if (tile > 0) {
+        // OS_LOOKBACK earlier tiles per round trip: an unpublished tile is waited
+        // for (bounded), a tile count is added and passed, an inclusive prefix
+        // ends the walk (tile 0 always publishes one)
+        int64_t t = tile - 1;
+        bool done = false;
+        while (!done) {
+          uint32_t v[OS_LOOKBACK];
+#pragma unroll
+          for (int k = 0; k < OS_LOOKBACK; ++k)
+            v[k] = t - k >= 0 ? __hip_atomic_load(&st[(t - k) * SORT_BUCKETS + d], __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT)
+                              : OS_INC;
+#pragma unroll
+          for (int k = 0; k < OS_LOOKBACK; ++k) {
+            if (done) break;
+            uint32_t u = v[k];
+            int spin = 0;
+            while (u == 0) {
+              if (++spin > OS_SPIN_LIMIT) {
+                // give up so that the kernel ends; the outputs are then invalid
+                if (b.status) raise_status(b.status, ALTO_E_INTERNAL);
+                u = OS_INC;
+                break;
+              }
+              __builtin_amdgcn_s_sleep(1);
+              u = __hip_atomic_load(&st[(t - k) * SORT_BUCKETS + d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            excl += os_value(u);
+            if (u & OS_INC) done = true;
+          }
+          t -= OS_LOOKBACK;
+        }
+        __hip_atomic_store(&st[tile * SORT_BUCKETS + d], OS_INC | (excl + run), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+      s_gbase[d] = b.os_hist[slot * SORT_BUCKETS + d] + excl;
+      st_next[tile * SORT_BUCKETS + d] = 0;   // the next pass's status of this tile
     }
+    __syncthreads();
+    if (packed && !last) {
+      for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+        const uint64_t el = s_key[e];
+        const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
+        dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = el;
+      }
+    } else if (packed) {
+      const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
+      for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+        const uint64_t el = s_key[e];
+        const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
+        const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
+        ok[g] = unpack_key(fsorted, c, el);
+        ov[g] = (uint32_t)(el & imask);
+      }
+    } else {
+      for (uint32_t e = threadIdx.x; e < tot; e += NT) {
+        const uint64_t el = s_key[e];
+        const uint32_t dg = digit_of(c.ps, rg, el);
+        const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
+        const int64_t gi = tile0 + s_slot[e];
+        dk[g] = el;
+        dvals[g] = sv ? sv[gi] : (uint32_t)gi;
+      }
+    }
+    __syncthreads();   // LDS and the ticket are reused by the next tile
   }
 }
 
@@ -854,7 +833,7 @@ template int scan_exclusive<uint32_t>(const uint32_t*, uint32_t*, int64_t, const
 template int scan_exclusive<int32_t>(const int32_t*, int32_t*, int64_t, const int64_t*, int32_t*, int32_t*, hipStream_t);
 template int scan_exclusive<int64_t>(const int64_t*, int64_t*, int64_t, const int64_t*, int64_t*, int64_t*, hipStream_t);
 
-int sort_hist_blocks(int64_t n_max) { return (int)(n_max < 1 ? 1 : cdiv(n_max, SORT_TILE)); }
+int sort_tiles(int64_t n_max) { return (int)(n_max < 1 ? 1 : cdiv(n_max, SORT_TILE)); }
 
 int sort_max_key_windows(int key_bits) { return (int)cdiv(key_bits, SORT_RADIX); }
 
@@ -884,7 +863,8 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     ALTO_LAUNCH_CHECK();
     return ALTO_OK;
   }
-  const int nblocks = sort_hist_blocks(n_max);
+  const int nblocks = sort_tiles(n_max);
+  if (!b.os_status || !b.os_ctr || !b.os_hist || b.os_ntiles < nblocks) return ALTO_E_ARG;
   const int grid_r = (int)(cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048);
   if (n_dev) {
     // the count is known on the device only: small counts go to one workgroup
@@ -894,6 +874,8 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     k_sort_init<<<1, 1, 0, st>>>(b.ctl);
     k_sort_reduce<<<grid_r, 256, 0, st>>>(b.in_keys, n_max, n_dev, rg, b.ctl);
   }
+  // packed words need a host-known count (the index bits are fixed on the host)
+  const bool packable = b.fl.hcap > 0 && n_dev == nullptr;
   if (b.fl.hcap > 0) {
     // rank the flows in (destination, prefix) order
     const FlowBufs& fl = b.fl;
@@ -907,36 +889,45 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     fb.tmp_vals = fl.ftmp_vals;
     fb.out_keys = fl.flow_sorted;
     fb.out_vals = fl.flow_order;
-    fb.hist = fl.fhist;
-    fb.scan_part = b.scan_part;
     fb.ctl = fl.fctl;
+    fb.os_status = b.os_status;
+    fb.os_ctr = b.os_ctr;
+    fb.os_hist = b.os_hist;
+    fb.os_ntiles = b.os_ntiles;
+    fb.status = b.status;
     RouteGeom frg = rg;
     frg.shift = 0;   // the flow keys are already prefixes of the route level
     int rc = sort_pairs(fb, fl.fcap, &b.ctl->nflows_c, frg, key_bits - fl.shift, false, st);
     if (rc) return rc;
     const int64_t rb = cdiv(fl.fcap, 256);
-    k_flow_rank<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, n_max);
+    k_flow_rank<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, n_max, packable ? 1 : 0);
     k_ct_insert<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl);
   }
   const int mk = sort_max_key_windows(key_bits), md = sort_max_dest_windows(rg);
-  int maxp = mk + md;
-  if (b.fl.hcap > 0) {
-    // packed windows cover at most 64 - index bits
-    const int mp = (int)cdiv(64 - b.fl.ib, SORT_RADIX);
-    if (mp > maxp) maxp = mp;
-  }
+  int maxp = mk + md;   // general passes
   if (maxp > SORT_MAX_PASSES) maxp = SORT_MAX_PASSES;
-  k_sort_plan<<<1, 1, 0, st>>>(b.ctl, n_max, n_dev, mk, md, nblocks);
+  k_sort_plan<<<1, 1, 0, st>>>(b.ctl, n_max, n_dev, mk, md);
   ALTO_LAUNCH_CHECK();
-  const bool packable = b.fl.hcap > 0 && n_dev == nullptr;   // packed mode needs a host-known count
-  for (int slot = 0; slot < maxp; ++slot) {
-    k_sort_upsweep<<<nblocks, NT, 0, st>>>(b, n_max, n_dev, slot, rg, nblocks);
-    if (packable) k_packed_upsweep<<<nblocks, NT, 0, st>>>(b, n_max, slot, nblocks);
-    int rc = scan_exclusive<uint32_t>(b.hist, b.hist, (int64_t)SORT_BUCKETS * nblocks, &b.ctl->plan.hist_len[slot],
-                                      b.scan_part, nullptr, st);
-    if (rc) return rc;
-    k_sort_downsweep<<<nblocks, NT, 0, st>>>(b, n_max, n_dev, slot, rg, nblocks);
-    if (packable) k_packed_downsweep<<<nblocks, NT, 0, st>>>(b, n_max, slot, nblocks);
+  // passes at most: general windows, or packed windows over 64 - index bits
+  int passes = maxp;
+  if (packable) {
+    const int mp = (int)cdiv(64 - b.fl.ib, SORT_RADIX);
+    if (mp > passes) passes = mp;
+  }
+  if (passes > SORT_MAX_PASSES) passes = SORT_MAX_PASSES;
+  const int copies = os_copies(passes);
+  const int64_t g0 = cdiv(nblocks, os_hist_max_tiles(copies));
+  const int grid_h = (int)(g0 > 1024 ? g0 : (nblocks < 1024 ? nblocks : 1024));
+  const size_t lds = (size_t)passes * 128 * copies * sizeof(uint32_t);
+  const int64_t pb = cdiv((int64_t)nblocks * SORT_BUCKETS, 256);
+  k_os_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(b, n_max, n_dev);
+  k_sort_hist<<<grid_h, NT, lds, st>>>(b, n_max, n_dev, rg, passes, copies);
+  k_os_bases<<<1, SORT_MAX_PASSES * ALTO_WAVE, 0, st>>>(b);
+  const int grid_o = nblocks < OS_GRID ? nblocks : OS_GRID;
+  const int64_t region = (int64_t)b.os_ntiles * SORT_BUCKETS;
+  for (int slot = 0; slot < passes; ++slot) {
+    if (packable) k_onesweep<true><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
+    if (slot < maxp) k_onesweep<false><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
   }
   k_sort_identity<<<grid_r, 256, 0, st>>>(b, n_max, n_dev);
   ALTO_LAUNCH_CHECK();
