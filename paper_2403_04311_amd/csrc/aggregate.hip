@@ -538,6 +538,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
     f.ht_rank = c.take<uint32_t>(h);
     f.ct_key = c.take<uint64_t>(h);
     f.ct_rank = c.take<uint32_t>(h);
+    f.drank = c.take<uint16_t>((int64_t)1 << FLOW_DIRECT_BITS);
     f.flow_key = c.take<uint64_t>(f.fcap);
     f.flow_slot = c.take<uint32_t>(f.fcap);
     f.flow_sorted = c.take<uint64_t>(f.fcap);

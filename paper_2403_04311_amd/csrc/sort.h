@@ -11,6 +11,7 @@
 #define SCAN_MAX_BLOCKS 1023
 #define SORT_SMALL_MAX 4096
 #define FLOW_CAP (1 << 15)
+#define FLOW_DIRECT_BITS 12   // flow prefixes varying within this many bits: direct rank table
 
 enum { SORT_BUF_INPUT = 0, SORT_BUF_TMP = 1, SORT_BUF_FINAL = 2 };
 enum { SORT_GENERAL = 0, SORT_PACKED = 1 };
@@ -34,7 +35,7 @@ struct SortCtl {
   int32_t sbits;         // packed: key bits below the route level (middle bits)
   int32_t rbits;         // packed: bits of the flow rank (high bits)
   int32_t flow_overflow; // the flow set filled up
-  int32_t pad;
+  int32_t dlo, dbits;    // packed: rank = drank[(prefix >> dlo) & (2^dbits - 1)]; dbits < 0: hashed table
   int64_t nflows;        // distinct flows inserted
   int64_t nflows_c;      // the same, clamped to the flow capacity
   int64_t hist_len;      // histogram entries the scan covers (0 when idle)
@@ -49,6 +50,7 @@ struct FlowBufs {
   uint32_t* ht_rank;     // [hcap] rank of the prefix held in the slot
   uint64_t* ct_key;      // [hcap] compact rank table (power of two >= 2 x flows), ~0 = empty
   uint32_t* ct_rank;     // [hcap]
+  uint16_t* drank;       // [1 << FLOW_DIRECT_BITS] rank by the varying bits of the prefix
   int64_t hcap;          // power of two, 0 = flows not used
   int32_t shift;         // bits below the route level
   int32_t ib;            // bits of the largest input index

@@ -135,8 +135,13 @@ __global__ void k_flow_clear(FlowBufs fl) {
 __global__ void k_ct_insert(FlowBufs fl, const SortCtl* ctl) {
   const int64_t F = ctl->nflows_c;
   const uint64_t mask = (uint64_t)ctl->ct_mask;
+  const int dlo = ctl->dlo, dbits = ctl->dbits;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < F; r += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t p = fl.flow_sorted[r];
+    if (dbits >= 0) {
+      fl.drank[(p >> dlo) & ((1ull << dbits) - 1ull)] = (uint16_t)r;
+      continue;
+    }
     uint64_t h = mix64(p ^ 0xD6E8FEB86659FD93ull) & mask;
     for (uint64_t probe = 0; probe <= mask; ++probe) {
       const uint64_t old = atomicCAS((unsigned long long*)&fl.ct_key[h], ~0ull, (unsigned long long)p);
@@ -191,6 +196,13 @@ __global__ void k_flow_rank(FlowBufs fl, SortCtl* ctl, int64_t n, int allow_pack
     int64_t t = 64;
     while (t < 2 * F && t < fl.hcap) t <<= 1;
     ctl->ct_mask = t - 1;
+    // prefixes whose varying bits span at most FLOW_DIRECT_BITS bits index a direct
+    // table (a prefix is fixed by those bits, the others being common to all keys)
+    const uint64_t vm = fl.shift >= 64 ? 0ull : ((ctl->key_or ^ ctl->key_and) >> fl.shift);
+    const int lo = vm ? __builtin_ctzll(vm) : 0;
+    const int span = vm ? 64 - __builtin_clzll(vm) - lo : 0;
+    ctl->dlo = lo;
+    ctl->dbits = span <= FLOW_DIRECT_BITS ? span : -1;
     ctl->rbits = R;
     ctl->sbits = fl.shift;
     ctl->ib = fl.ib;
@@ -202,6 +214,7 @@ __global__ void k_flow_rank(FlowBufs fl, SortCtl* ctl, int64_t n, int allow_pack
 struct PassView {
   SortPass ps;
   int32_t mode, ib, sbits, npass;
+  int32_t dlo, dbits;
   uint64_t ct_mask;
 };
 
@@ -213,6 +226,8 @@ __device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
   v.sbits = ctl->sbits;
   v.npass = ctl->plan.npass;
   v.ct_mask = (uint64_t)ctl->ct_mask;
+  v.dlo = ctl->dlo;
+  v.dbits = ctl->dbits;
   return v;
 }
 
@@ -258,12 +273,27 @@ __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
 // Packs IT input keys with their ranks: the first probe of every item is issued
 // before any is resolved (independent loads), collisions are resolved afterwards.
 template <int NI>
-__device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n, uint64_t* out) {
+__device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n, uint64_t* out,
+                                  const uint16_t* s_drank) {
   const int S = c.sbits;
-  const uint64_t mask = c.ct_mask;
-  uint64_t key[NI], p[NI], h[NI], v[NI];
+  const int hi = S + c.ib;
+  uint64_t key[NI];
 #pragma unroll
   for (int j = 0; j < NI; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
+  if (s_drank) {
+    // direct table in LDS
+    const uint64_t dm = (1ull << c.dbits) - 1ull;
+#pragma unroll
+    for (int j = 0; j < NI; ++j) {
+      const uint32_t rank = gi[j] < n ? s_drank[((key[j] >> S) >> c.dlo) & dm] : 0u;
+      const uint64_t suffix = S == 0 ? 0ull : (key[j] & ((1ull << S) - 1ull));
+      const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
+      out[j] = gi[j] < n ? (r | (suffix << c.ib) | (uint64_t)gi[j]) : 0ull;
+    }
+    return;
+  }
+  const uint64_t mask = c.ct_mask;
+  uint64_t p[NI], h[NI], v[NI];
 #pragma unroll
   for (int j = 0; j < NI; ++j) {
     p[j] = key[j] >> S;
@@ -284,7 +314,6 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
     }
     const uint32_t rank = vv == p[j] ? b.fl.ct_rank[hh] : 0u;
     const uint64_t suffix = S == 0 ? 0ull : (key[j] & ((1ull << S) - 1ull));
-    const int hi = S + c.ib;
     const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
     out[j] = r | (suffix << c.ib) | (uint64_t)gi[j];
   }
@@ -311,7 +340,7 @@ __device__ inline uint32_t os_value(uint32_t w) { return (w & OS_INC) ? (w & ~OS
 // `copies` copies picked by lane so that a row whose lanes share one digit (common
 // for flow-rank digits) makes at most 64 / copies same-address LDS atomics; copies
 // sit in consecutive words (banks).
-__host__ __device__ inline int os_copies(int passes) { return passes <= 7 ? 16 : 8; }
+__host__ __device__ inline int os_copies(int passes) { return passes <= 6 ? 16 : 8; }
 __host__ __device__ inline int os_hist_max_tiles(int copies) { return 65535 / (SORT_TILE / copies); }
 
 __global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev) {
@@ -339,6 +368,12 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
   const int np = c.npass < max_passes ? c.npass : max_passes;   // npass <= max_passes by the plan
   const int wpp = 128 * copies;   // words per pass
   for (int i = threadIdx.x; i < np * wpp; i += NT) s_hw[i] = 0;
+  // packed mode with a direct rank table: the table follows the counters
+  uint16_t* const s_drank = (packed && c.dbits >= 0) ? reinterpret_cast<uint16_t*>(s_hw + max_passes * wpp) : nullptr;
+  if (s_drank) {
+    const uint16_t* dr = opaque(b.fl.drank);
+    for (int i = threadIdx.x; i < (1 << c.dbits); i += NT) s_drank[i] = dr[i];
+  }
   if (threadIdx.x < SORT_MAX_PASSES) {
     const SortPass ps = b.ctl->plan.pass[threadIdx.x];
     s_sh[threadIdx.x] = (packed ? c.ib : 0) + ps.lo;
@@ -357,7 +392,7 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
 #pragma unroll
     for (int j = 0; j < IT; ++j) gi[j] = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
     if (packed) {
-      pack_items<IT>(b, c, gi, n, key);
+      pack_items<IT>(b, c, gi, n, key, s_drank);
 #pragma unroll
       for (int j = 0; j < IT; ++j)
         if (gi[j] < n) stage[gi[j]] = key[j];
@@ -918,7 +953,8 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
   const int copies = os_copies(passes);
   const int64_t g0 = cdiv(nblocks, os_hist_max_tiles(copies));
   const int grid_h = (int)(g0 > 1024 ? g0 : (nblocks < 1024 ? nblocks : 1024));
-  const size_t lds = (size_t)passes * 128 * copies * sizeof(uint32_t);
+  const size_t lds = (size_t)passes * 128 * copies * sizeof(uint32_t) +
+                     (packable ? ((size_t)1 << FLOW_DIRECT_BITS) * sizeof(uint16_t) : 0);
   const int64_t pb = cdiv((int64_t)nblocks * SORT_BUCKETS, 256);
   k_os_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(b, n_max, n_dev);
   k_sort_hist<<<grid_h, NT, lds, st>>>(b, n_max, n_dev, rg, passes, copies);
