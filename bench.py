@@ -52,6 +52,9 @@ def main():
     ap.add_argument("--leaves-log2", type=int, default=26)
     ap.add_argument("--cpu-sample-log2", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB before the workload (untimed), the "
+                         "reference for scaling hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
@@ -64,6 +67,14 @@ def main():
 
     dev = "cuda"
     lib = alto.load()
+    if args.copy_calibration_mib:
+        nb = args.copy_calibration_mib << 20
+        a = torch.empty(nb, dtype=torch.uint8, device=dev)
+        b = torch.empty(nb, dtype=torch.uint8, device=dev)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log(f"calibration copy of {args.copy_calibration_mib} MiB done")
     n = 1 << args.leaves_log2
     log(f"generating workload: 2^{args.leaves_log2} fragments")
     t0 = time.time()

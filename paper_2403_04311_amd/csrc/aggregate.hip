@@ -326,11 +326,13 @@ __global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks
 // its rows sequentially (U independent row loads in flight), then lanes holding the
 // same columns are combined in lane order, then the waves in wave order. Groups of
 // one chunk are finished here; the others leave a partial sum per chunk.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 template <int VEC, int CPL, typename Src>
 __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src srcp,
                                               int dim, int lpr, double* part, float* mean, int64_t cap_groups) {
   constexpr int NW = 4;
-  constexpr int U = 4;
+  constexpr int U = 2;   // row loads in flight per lane (more lowers occupancy)
   __shared__ double red[NW][64 * CPL * VEC];
   const int C = dim / VEC;
   const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
@@ -344,41 +346,48 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
       for (int q = 0; q < CPL; ++q)
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[q][v] = 0.0;
-      const int stride = NW * rpw;
-      for (int r0 = w * rpw + sub; r0 < ch.len; r0 += stride * U) {
-        const float* src[U];
+      // each wave takes batches of 64 consecutive rows: the 64 row indices are read
+      // with one coalesced load and passed to the lanes that load the rows, so the
+      // payload loads do not wait on per-row index loads
+      for (int b0 = w * ALTO_WAVE; b0 < ch.len; b0 += NW * ALTO_WAVE) {
+        const int nr = ch.len - b0 < ALTO_WAVE ? ch.len - b0 : ALTO_WAVE;
+        const int32_t myrow = lane < nr ? (int32_t)srcp.row(ch.begin + b0 + lane) : 0;
+        for (int it0 = 0; it0 < lpr; it0 += U) {   // lpr steps of rpw rows cover the batch
+          float x[U][CPL][VEC];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int r = r0 + u * stride;
-          src[u] = r < ch.len ? srcp.pay_of(srcp.row(ch.begin + r)) : nullptr;
-        }
-        float x[U][CPL][VEC];
+          for (int u = 0; u < U; ++u) {
+            const int r = (it0 + u) * rpw + sub;
+            const int32_t row = __shfl(myrow, r & (ALTO_WAVE - 1));
+            const bool ok = (it0 + u < lpr) && r < nr;
+            const float* src = srcp.pay_of(row);
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-          for (int q = 0; q < CPL; ++q) {
-            const int col = col0 + cl + q * lpr;
-            if (src[u] && col < C) {
-              if constexpr (VEC == 4) {
-                const float4 t = *reinterpret_cast<const float4*>(src[u] + (int64_t)col * 4);
-                x[u][q][0] = t.x;
-                x[u][q][1] = t.y;
-                x[u][q][2] = t.z;
-                x[u][q][3] = t.w;
+            for (int q = 0; q < CPL; ++q) {
+              const int col = col0 + cl + q * lpr;
+              if (ok && col < C) {
+                // payload rows are read once: non-temporal loads keep them from
+                // displacing reusable lines in the caches
+                if constexpr (VEC == 4) {
+                  const f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + (int64_t)col * 4));
+                  x[u][q][0] = t[0];
+                  x[u][q][1] = t[1];
+                  x[u][q][2] = t[2];
+                  x[u][q][3] = t[3];
+                } else {
+                  x[u][q][0] = __builtin_nontemporal_load(src + col);
+                }
               } else {
-                x[u][q][0] = src[u][col];
-              }
-            } else {
 #pragma unroll
-              for (int v = 0; v < VEC; ++v) x[u][q][v] = 0.f;
+                for (int v = 0; v < VEC; ++v) x[u][q][v] = 0.f;
+              }
             }
           }
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+          for (int u = 0; u < U; ++u)
 #pragma unroll
-          for (int q = 0; q < CPL; ++q)
+            for (int q = 0; q < CPL; ++q)
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[q][v] += (double)x[u][q][v];
+              for (int v = 0; v < VEC; ++v) acc[q][v] += (double)x[u][q][v];
+        }
       }
       // combine the sub-rows of the wave (lanes with equal cl), in a fixed order
       for (int o = lpr; o < ALTO_WAVE; o <<= 1)

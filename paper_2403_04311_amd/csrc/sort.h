@@ -5,6 +5,10 @@
 #define SORT_NT 512
 #define SORT_IT 8
 #define SORT_TILE (SORT_NT * SORT_IT)
+#ifndef SORT_OS_IT
+#define SORT_OS_IT 16   // items per thread of a look-back pass
+#endif
+#define SORT_OS_TILE (SORT_NT * SORT_OS_IT)
 #define SORT_RADIX 8
 #define SORT_BUCKETS 256
 #define SORT_MAX_PASSES 12
@@ -80,7 +84,7 @@ struct SortBufs {
   int32_t* status;           // raised to ALTO_E_INTERNAL if a look-back wait gives up (may be null)
 };
 
-int sort_tiles(int64_t n_max);   // tiles of SORT_TILE elements
+int sort_tiles(int64_t n_max);   // tiles of SORT_OS_TILE elements (look-back passes)
 int sort_max_key_windows(int key_bits);
 int sort_max_dest_windows(const RouteGeom& rg);
 int bits_for(int64_t v);     // bits needed to hold values 0..v

@@ -18,6 +18,8 @@ namespace {
 
 constexpr int NT = SORT_NT;
 constexpr int IT = SORT_IT;
+constexpr int OS_IT = SORT_OS_IT;
+constexpr int OS_TILE = SORT_OS_TILE;
 constexpr int TILE = SORT_TILE;
 constexpr int NW = NT / ALTO_WAVE;
 
@@ -240,13 +242,16 @@ __device__ inline uint64_t unpack_key(const uint64_t* flow_sorted, const PassVie
 
 // A pointer value hidden from the optimiser: selecting between buffers of the
 // by-value argument struct then selects values, not addresses inside the struct
-// (which would force a copy of the struct into scratch memory).
+// (which would force a copy of the struct into scratch memory). The pointers are
+// device (global) memory.
 template <typename T>
 __device__ inline T* opaque(T* p) {
   const uint64_t v = (uint64_t)p;
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return (T*)(((uint64_t)hi << 32) | lo);
+  // rebuilt as a global-memory pointer, so that accesses stay global (not flat)
+  typedef __attribute__((address_space(1))) T GlobalT;
+  return (T*)(GlobalT*)(((uint64_t)hi << 32) | lo);
 }
 
 // Stable in-wave ranking of one row of 64 digits: the lane mask of the valid lanes
@@ -331,7 +336,9 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
 #define OS_INC (1u << 31)
 #define OS_AGG (1u << 30)
 #define OS_SPIN_LIMIT (1 << 22)
-#define OS_LOOKBACK 4
+#ifndef OS_LOOKBACK
+#define OS_LOOKBACK 1   // earlier tiles read per look-back round trip
+#endif
 #define OS_GRID 1024
 
 __device__ inline uint32_t os_value(uint32_t w) { return (w & OS_INC) ? (w & ~OS_INC) : (w & (OS_AGG - 1u)); }
@@ -345,7 +352,7 @@ __host__ __device__ inline int os_hist_max_tiles(int copies) { return 65535 / (S
 
 __global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev) {
   const int64_t n = load_n(n_host, n_dev);
-  const int64_t len = cdiv(n, TILE) * SORT_BUCKETS;   // status region 0
+  const int64_t len = cdiv(n, OS_TILE) * SORT_BUCKETS;   // status region 0
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
     b.os_status[i] = 0;
   if (blockIdx.x == 0) {
@@ -455,12 +462,12 @@ __device__ inline uint32_t pass_digit(bool packed, const SortPass& ps, int sh, c
 // instantiation per mode (each exits when the device chose the other), so that the
 // packed one keeps the registers of its simpler digits.
 template <bool PACKED>
-__global__ __launch_bounds__(NT, PACKED ? 6 : 4) void k_onesweep(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
+__global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesweep(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
                                                  int slot, int64_t region) {
   const PassView c = read_pass(b.ctl, slot);
   if (!c.ps.active || (c.mode == SORT_PACKED) != PACKED) return;
   const int64_t n = load_n(n_host, n_dev);
-  const int64_t ntiles = cdiv(n, TILE);
+  const int64_t ntiles = cdiv(n, OS_TILE);
   constexpr bool packed = PACKED;
   const bool last = (slot + 1 == c.npass);
   const int sh = c.ib + c.ps.lo;
@@ -468,8 +475,8 @@ __global__ __launch_bounds__(NT, PACKED ? 6 : 4) void k_onesweep(SortBufs b, int
   __shared__ uint32_t s_base[SORT_BUCKETS];
   __shared__ uint32_t s_gbase[SORT_BUCKETS];
   __shared__ uint32_t s_wsum[NT / ALTO_WAVE];
-  __shared__ uint64_t s_key[TILE];
-  __shared__ uint16_t s_slot[TILE];   // general mode: position of the element in its tile
+  __shared__ uint64_t s_key[OS_TILE];
+  __shared__ uint16_t s_slot[OS_TILE];   // general mode: position of the element in its tile
   __shared__ int64_t s_tile;
   uint32_t* st = b.os_status + (slot & 1) * region;
   uint32_t* st_next = b.os_status + ((slot + 1) & 1) * region;
@@ -494,18 +501,19 @@ __global__ __launch_bounds__(NT, PACKED ? 6 : 4) void k_onesweep(SortBufs b, int
     if (threadIdx.x == 0) s_tile = (int64_t)atomicAdd(&b.os_ctr[slot], 1u);
     for (int i = threadIdx.x; i < NW * SORT_BUCKETS; i += NT) (&s_cnt[0][0])[i] = 0;
     __syncthreads();
-    const int64_t tile = s_tile;
+    // uniform across the block: kept in scalar registers (scalar-based addressing)
+    const int64_t tile = (int64_t)__builtin_amdgcn_readfirstlane((uint32_t)s_tile);
     if (tile >= ntiles) break;   // uniform across the block
-    const int64_t tile0 = tile * TILE;
-    const int rem = (int)(n - tile0 < TILE ? n - tile0 : TILE);   // elements in this tile
+    const int64_t tile0 = tile * OS_TILE;
+    const int rem = (int)(n - tile0 < OS_TILE ? n - tile0 : OS_TILE);   // elements in this tile
     const uint64_t* const tsk = sk + tile0;
-    const int lbase = w * (IT * ALTO_WAVE) + lane;               // tile-local index of item 0
-    uint64_t key[IT];
-    uint32_t dof[IT];   // digit | in-wave offset << 8 (offsets < IT * 64)
+    const int lbase = w * (OS_IT * ALTO_WAVE) + lane;               // tile-local index of item 0
+    uint64_t key[OS_IT];
+    uint32_t dof[OS_IT];   // digit | in-wave offset << 8 (offsets < OS_IT * 64)
 #pragma unroll
-    for (int j = 0; j < IT; ++j) key[j] = lbase + j * ALTO_WAVE < rem ? tsk[lbase + j * ALTO_WAVE] : 0ull;
+    for (int j = 0; j < OS_IT; ++j) key[j] = lbase + j * ALTO_WAVE < rem ? tsk[lbase + j * ALTO_WAVE] : 0ull;
 #pragma unroll
-    for (int j = 0; j < IT; ++j) {
+    for (int j = 0; j < OS_IT; ++j) {
       const bool valid = lbase + j * ALTO_WAVE < rem;
       const uint32_t dig = valid ? pass_digit(packed, c.ps, sh, rg, key[j]) : 0u;
       const uint64_t peers = match_digit(dig, valid);
@@ -541,7 +549,7 @@ __global__ __launch_bounds__(NT, PACKED ? 6 : 4) void k_onesweep(SortBufs b, int
     }
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < IT; ++j) {
+    for (int j = 0; j < OS_IT; ++j) {
       if (lbase + j * ALTO_WAVE < rem) {
         const uint32_t dg = dof[j] & 0xFFu;
         const uint32_t r = s_base[dg] + (uint32_t)s_cnt[w][dg] + (dof[j] >> 8);
@@ -868,7 +876,7 @@ template int scan_exclusive<uint32_t>(const uint32_t*, uint32_t*, int64_t, const
 template int scan_exclusive<int32_t>(const int32_t*, int32_t*, int64_t, const int64_t*, int32_t*, int32_t*, hipStream_t);
 template int scan_exclusive<int64_t>(const int64_t*, int64_t*, int64_t, const int64_t*, int64_t*, int64_t*, hipStream_t);
 
-int sort_tiles(int64_t n_max) { return (int)(n_max < 1 ? 1 : cdiv(n_max, SORT_TILE)); }
+int sort_tiles(int64_t n_max) { return (int)(n_max < 1 ? 1 : cdiv(n_max, SORT_OS_TILE)); }
 
 int sort_max_key_windows(int key_bits) { return (int)cdiv(key_bits, SORT_RADIX); }
 
@@ -898,8 +906,9 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     ALTO_LAUNCH_CHECK();
     return ALTO_OK;
   }
-  const int nblocks = sort_tiles(n_max);
-  if (!b.os_status || !b.os_ctr || !b.os_hist || b.os_ntiles < nblocks) return ALTO_E_ARG;
+  const int ostiles = sort_tiles(n_max);                   // tiles of the look-back passes
+  const int htiles = (int)cdiv(n_max, SORT_TILE);          // tiles of the counting sweep
+  if (!b.os_status || !b.os_ctr || !b.os_hist || b.os_ntiles < ostiles) return ALTO_E_ARG;
   const int grid_r = (int)(cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048);
   if (n_dev) {
     // the count is known on the device only: small counts go to one workgroup
@@ -944,25 +953,22 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
   k_sort_plan<<<1, 1, 0, st>>>(b.ctl, n_max, n_dev, mk, md);
   ALTO_LAUNCH_CHECK();
   // passes at most: general windows, or packed windows over 64 - index bits
-  int passes = maxp;
-  if (packable) {
-    const int mp = (int)cdiv(64 - b.fl.ib, SORT_RADIX);
-    if (mp > passes) passes = mp;
-  }
-  if (passes > SORT_MAX_PASSES) passes = SORT_MAX_PASSES;
+  int mp = packable ? (int)cdiv(64 - b.fl.ib, SORT_RADIX) : 0;
+  if (mp > SORT_MAX_PASSES) mp = SORT_MAX_PASSES;
+  const int passes = mp > maxp ? mp : maxp;
   const int copies = os_copies(passes);
-  const int64_t g0 = cdiv(nblocks, os_hist_max_tiles(copies));
-  const int grid_h = (int)(g0 > 1024 ? g0 : (nblocks < 1024 ? nblocks : 1024));
+  const int64_t g0 = cdiv(htiles, os_hist_max_tiles(copies));
+  const int grid_h = (int)(g0 > 1024 ? g0 : (htiles < 1024 ? htiles : 1024));
   const size_t lds = (size_t)passes * 128 * copies * sizeof(uint32_t) +
                      (packable ? ((size_t)1 << FLOW_DIRECT_BITS) * sizeof(uint16_t) : 0);
-  const int64_t pb = cdiv((int64_t)nblocks * SORT_BUCKETS, 256);
+  const int64_t pb = cdiv((int64_t)ostiles * SORT_BUCKETS, 256);
   k_os_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(b, n_max, n_dev);
   k_sort_hist<<<grid_h, NT, lds, st>>>(b, n_max, n_dev, rg, passes, copies);
   k_os_bases<<<1, SORT_MAX_PASSES * ALTO_WAVE, 0, st>>>(b);
-  const int grid_o = nblocks < OS_GRID ? nblocks : OS_GRID;
+  const int grid_o = ostiles < OS_GRID ? ostiles : OS_GRID;
   const int64_t region = (int64_t)b.os_ntiles * SORT_BUCKETS;
   for (int slot = 0; slot < passes; ++slot) {
-    if (packable) k_onesweep<true><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
+    if (slot < mp) k_onesweep<true><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
     if (slot < maxp) k_onesweep<false><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
   }
   k_sort_identity<<<grid_r, 256, 0, st>>>(b, n_max, n_dev);
