@@ -109,7 +109,6 @@ struct AggBufs {
   uint32_t* perm_used;  // perm buffer the sort wrote (caller's or ours)
   int32_t* scan_i32;
   int64_t* scan_i64;
-  int32_t* blkcnt;
   LevelNodes lv[ALTO_MAX_LEVELS + 1];
   int32_t* carry_fan;
   uint64_t* rkey;

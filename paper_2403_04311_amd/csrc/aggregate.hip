@@ -560,7 +560,6 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   int Lt, Lseg;
   agg_levels(g, agg->level, agg->mask_level, Lr, &Lt, &Lseg);
   const int d = g.depth;
-  b.blkcnt = c.take<int32_t>((int64_t)(d - Lt) * seg_blocks(n) + 1);
   for (int m = Lt; m < d; ++m) {
     LevelNodes& L = b.lv[m];
     L.start = c.take<int32_t>(n + 1);
@@ -670,8 +669,9 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   fj.carry_ld = n < 1 ? 1 : n;
   for (int m = 0; m <= ALTO_MAX_LEVELS; ++m) fj.lv[m] = b.lv[m];
   fj.nnodes = b.nnodes;
-  fj.blkcnt = b.blkcnt;
-  fj.scan_part = b.scan_i32;
+  fj.lb_status = b.os_status;
+  fj.lb_ctr = b.os_ctr;
+  fj.lb_tiles = b.os_ntiles * 2 * SORT_BUCKETS / SEG_LB_STRIDE;   // the sort's status words, free by now
   fj.fp_nodes = b.fp_nodes;
   fj.status = status;
   rc = seg_run(g, fj, st);
@@ -715,8 +715,9 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     rj.chain_check = 1;
     for (int m = 0; m <= ALTO_MAX_LEVELS; ++m) rj.lv[m] = b.lv[m];
     rj.nnodes = b.nnodes;
-    rj.blkcnt = b.blkcnt;
-    rj.scan_part = b.scan_i32;
+    rj.lb_status = b.os_status;
+    rj.lb_ctr = b.os_ctr;
+    rj.lb_tiles = b.os_ntiles * 2 * SORT_BUCKETS / SEG_LB_STRIDE;   // the sort's status words, free by now
     rj.status = status;
     rc = seg_run(g, rj, st);
     if (rc) return rc;

@@ -126,6 +126,48 @@ __device__ inline T block_excl_scan(T v, T* sh, T* total) {
 }
 
 // ---------------------------------------------------------------------------
+// decoupled look-back over tiles processed in ticket order
+// ---------------------------------------------------------------------------
+// A tile publishes its count, then finds the exclusive prefix of all earlier tiles
+// by walking back over their words, one per round trip: a count is added and
+// passed, an inclusive prefix ends the walk (tile 0 publishes one at once). A tile
+// only waits on tiles whose tickets were taken before its own, by blocks that are
+// running, so the walk ends; the wait for an unpublished word is still bounded,
+// and on giving up the status word gets ALTO_E_INTERNAL and the kernel goes on.
+// Word: 0 = not yet published, bit 31 = inclusive prefix in bits 0-30, bit 30 =
+// the tile's own count in bits 0-29 (counts < 2^30, prefixes < 2^31).
+#define LB_INC (1u << 31)
+#define LB_AGG (1u << 30)
+#define LB_SPIN_LIMIT (1 << 22)
+
+__device__ inline void lb_publish(uint32_t* st, int64_t tile, int64_t stride, uint32_t count) {
+  __hip_atomic_store(&st[tile * stride], (tile == 0 ? LB_INC : LB_AGG) | count, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint32_t lb_resolve(uint32_t* st, int64_t tile, int64_t stride, uint32_t count, int32_t* status) {
+  if (tile == 0) return 0;
+  uint32_t excl = 0;
+  for (int64_t t = tile - 1;; --t) {
+    uint32_t u = __hip_atomic_load(&st[t * stride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int spin = 0;
+    while (u == 0) {
+      if (++spin > LB_SPIN_LIMIT) {
+        if (status) raise_status(status, ALTO_E_INTERNAL);
+        u = LB_INC;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      u = __hip_atomic_load(&st[t * stride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    excl += (u & LB_INC) ? (u & ~LB_INC) : (u & (LB_AGG - 1u));
+    if (u & LB_INC) break;
+  }
+  __hip_atomic_store(&st[tile * stride], LB_INC | (excl + count), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return excl;
+}
+
+// ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
 #define ALTO_LAUNCH_CHECK()                                  \

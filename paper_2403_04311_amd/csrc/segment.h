@@ -3,9 +3,10 @@
 #pragma once
 #include "alto_internal.h"
 
-#define SEG_NT 256
-#define SEG_IT 8
+#define SEG_NT 512
+#define SEG_IT 16                      // consecutive elements per thread
 #define SEG_TILE (SEG_NT * SEG_IT)
+#define SEG_LB_STRIDE ALTO_MAX_LEVELS  // look-back words per tile (one per level)
 #define NODE_GRID 512
 
 // Arrays describing the nodes of one level, in element order.
@@ -47,13 +48,14 @@ struct SegJob {
   int64_t carry_ld;
   LevelNodes lv[ALTO_MAX_LEVELS + 1];   // indexed by level
   int64_t* nnodes;          // device [ALTO_MAX_LEVELS + 1]: node count per level
-  int32_t* blkcnt;          // [(elem_level - lo) * nblk + 1]
-  int32_t* scan_part;       // [SCAN_MAX_BLOCKS + 1]
+  uint32_t* lb_status;      // [lb_tiles * SEG_LB_STRIDE] look-back words (cleared by seg_run)
+  uint32_t* lb_ctr;         // [1] tile tickets
+  int64_t lb_tiles;         // >= seg_tiles(n_max)
   uint64_t* fp_nodes;       // device [ALTO_MAX_LEVELS + 1]: fingerprint sums over nodes (fragments)
   int32_t* status;
   int64_t* dest_offsets;    // fragments sorted by (dest, key): start of each destination (nullable)
   RouteGeom rg;
 };
 
-int seg_blocks(int64_t n_max);
+int seg_tiles(int64_t n_max);   // tiles of SEG_TILE elements
 int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st);

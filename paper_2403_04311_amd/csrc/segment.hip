@@ -4,9 +4,10 @@
 // Ancestry levels (Section 4.2 of the paper) nest: when elements are ordered by
 // key, every node is a contiguous run, and a boundary of a level-m node is also a
 // boundary at every deeper level. One pass counts the boundaries of each level per
-// tile, a scan turns them into node ids, and a second pass writes each node's
-// first element, first child and parent. Completion (Section 3.1: the extent of a
-// stream is known only at its end, so each node declares its child count) is then
+// tile; a look-back over earlier tiles turns them into node ids in the same pass,
+// which writes each node's first element, first child and parent. Completion
+// (Section 3.1: the extent of a stream is known only at its end, so each node
+// declares its child count) is then
 // evaluated bottom-up, one level per launch: a node is complete when it has as many
 // children as it declares and none of them is incomplete.
 #include "segment.h"
@@ -31,162 +32,176 @@ __device__ inline int32_t fan_at(const SegJob& j, int m, int64_t e) {
   return j.fan[(int64_t)(m - j.fan_base) * j.fan_ld + j.idx[e]];
 }
 
-// Loads the tile's keys plus the key before the tile into LDS.
-__device__ inline void load_tile(const SegJob& j, int64_t tile0, int64_t n, uint64_t* s_key) {
-  for (int t = threadIdx.x; t <= TILE; t += NT) {
-    int64_t e = tile0 - 1 + t;
-    s_key[t] = (e >= 0 && e < n) ? j.keys[e] : 0ull;
-  }
-  __syncthreads();
-}
-
-__global__ __launch_bounds__(NT) void k_seg_count(KeyGeom g, SegJob j, int nblk) {
-  __shared__ uint64_t s_key[TILE + 1];
-  __shared__ int32_t s_w[NT / ALTO_WAVE];
+// Clears the look-back words and the ticket; with no elements, writes the empty
+// node counts and sentinels.
+__global__ void k_seg_prep(SegJob j) {
   const int64_t n = nelem(j);
-  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-  const int K = j.elem_level - j.lo;
-  if (blockIdx.x == 0 && threadIdx.x == 0) j.blkcnt[(int64_t)K * nblk] = 0;
-  if (tile0 >= n) {
-    if (threadIdx.x < K) j.blkcnt[(int64_t)threadIdx.x * nblk + blockIdx.x] = 0;
-    return;
-  }
-  load_tile(j, tile0, n, s_key);
-  if (j.dest_offsets) {
-    // destination offsets from the sorted keys: each change of destination fills
-    // the starts of the destinations it passes
-    const uint32_t D = j.rg.num_dest;
-    int64_t* offs = j.dest_offsets;
-#pragma unroll
-    for (int i = 0; i < IT; ++i) {
-      const int t = threadIdx.x * IT + i;
-      const int64_t e = tile0 + t;
-      if (e >= n) break;
-      const uint32_t d = dest_of_key(j.rg, s_key[t + 1]);
-      if (e == 0) {
-        for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
-      } else {
-        const uint32_t dp = dest_of_key(j.rg, s_key[t]);
-        if (d != dp)
-          for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = e;
+  const int64_t len = cdiv(n, TILE) * SEG_LB_STRIDE;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
+    j.lb_status[i] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *j.lb_ctr = 0;
+    if (n == 0) {
+      for (int m = j.lo; m < j.elem_level; ++m) {
+        j.nnodes[m] = 0;
+        j.lv[m].start[0] = 0;
+        if (m + 1 < j.elem_level) j.lv[m].fc[0] = 0;
       }
-      if (e == n - 1)
-        for (uint32_t x = d + 1; x <= D; ++x) offs[x] = n;
     }
-  }
-  for (int m = j.lo; m < j.elem_level; ++m) {
-    const int es = es_of(g, j, m);
-    int32_t c = 0;
-#pragma unroll
-    for (int i = 0; i < IT; ++i) {
-      int t = threadIdx.x * IT + i;
-      int64_t e = tile0 + t;
-      if (e < n) c += (e == 0) || (key_prefix(s_key[t + 1], es) != key_prefix(s_key[t], es));
-    }
-    c = wave_sum(c);
-    if (lane_id() == 0) s_w[threadIdx.x / ALTO_WAVE] = c;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int32_t t = 0;
-      for (int w = 0; w < NT / ALTO_WAVE; ++w) t += s_w[w];
-      j.blkcnt[(int64_t)(m - j.lo) * nblk + blockIdx.x] = t;
-    }
-    __syncthreads();
   }
 }
 
-// Node counts per level from the scanned block counts; sentinels.
-__global__ void k_seg_totals(SegJob j, int nblk, int64_t total_len) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const int K = j.elem_level - j.lo;
-  // blkcnt has been scanned in place; the sum sits in the scan partials (part[nb])
-  for (int m = j.lo; m < j.elem_level; ++m) {
-    int64_t base = j.blkcnt[(int64_t)(m - j.lo) * nblk];
-    int64_t next = (m + 1 < j.elem_level) ? (int64_t)j.blkcnt[(int64_t)(m + 1 - j.lo) * nblk] : (int64_t)j.blkcnt[(int64_t)K * nblk];
-    j.nnodes[m] = next - base;
-  }
-}
-
+// One pass over the sorted elements: per tile, the boundary flags of every level
+// (a boundary of a level is also one of every deeper level), node counts by block
+// scan, node ids by look-back over earlier tiles, then the node records (first
+// element, first child, parent, declared fan). Also: duplicate keys (fragments),
+// the exact fan chain check (records), destination offsets at route-prefix changes.
+// Persistent; tiles by ticket. Up to four levels share one 64-bit scan (16-bit
+// counts; a tile has at most SEG_TILE < 2^16 elements).
 template <int KM>
-__global__ __launch_bounds__(NT) void k_seg_write(KeyGeom g, SegJob j, int nblk) {
-  __shared__ uint64_t s_key[TILE + 1];
-  __shared__ int32_t s_w[NT / ALTO_WAVE];
+__global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
+  constexpr int NP = (KM + 3) / 4;
   const int64_t n = nelem(j);
-  const int64_t tile0 = (int64_t)blockIdx.x * TILE;
-  if (tile0 >= n) return;
-  load_tile(j, tile0, n, s_key);
+  const int64_t ntiles = cdiv(n, TILE);
   const int lo = j.lo, E = j.elem_level, K = E - lo;
-  // slot q holds level lo + q; every loop below is fully unrolled so that the
-  // per-level arrays stay in registers
-  int32_t cur[KM];
+  __shared__ uint64_t s_w[NT / ALTO_WAVE];
+  __shared__ uint32_t s_excl[KM], s_tot[KM];
+  __shared__ uint32_t s_tile;
   int es[KM];
 #pragma unroll
-  for (int q = 0; q < KM; ++q) {
-    cur[q] = 0;
-    es[q] = q < K ? es_of(g, j, lo + q) : 64;
-  }
-  // per level: node id of the element before this thread's first element
+  for (int q = 0; q < KM; ++q) es[q] = q < K ? es_of(g, j, lo + q) : 64;
+  const int lane = lane_id();
+  const bool vec_ok = (reinterpret_cast<uintptr_t>(j.keys) & 15) == 0;
+  while (true) {
+    if (threadIdx.x == 0) s_tile = atomicAdd(j.lb_ctr, 1u);
+    __syncthreads();
+    const int64_t tile = (int64_t)__builtin_amdgcn_readfirstlane(s_tile);
+    if (tile >= ntiles) break;   // uniform across the block
+    const int64_t e0 = tile * TILE + (int64_t)threadIdx.x * IT;
+    uint64_t k[IT];
+    if (vec_ok && e0 + IT <= n) {
+      const ulonglong2* p = reinterpret_cast<const ulonglong2*>(j.keys + e0);
 #pragma unroll
-  for (int q = 0; q < KM; ++q) {
-    if (q < K) {
-      int32_t c = 0;
-#pragma unroll
-      for (int i = 0; i < IT; ++i) {
-        const int t = threadIdx.x * IT + i;
-        const int64_t e = tile0 + t;
-        if (e < n) c += (e == 0) || (key_prefix(s_key[t + 1], es[q]) != key_prefix(s_key[t], es[q]));
+      for (int i = 0; i < IT / 2; ++i) {
+        const ulonglong2 v = p[i];
+        k[2 * i] = v.x;
+        k[2 * i + 1] = v.y;
       }
-      int32_t tot;
-      const int32_t ex = block_excl_scan<int32_t, NT>(c, s_w, &tot);
-      const int32_t lvl_base = j.blkcnt[(int64_t)q * nblk];
-      const int32_t blk_off = j.blkcnt[(int64_t)q * nblk + blockIdx.x] - lvl_base;
-      cur[q] = blk_off + ex - 1;
-    }
-  }
-  for (int i = 0; i < IT; ++i) {
-    const int t = threadIdx.x * IT + i;
-    const int64_t e = tile0 + t;
-    if (e >= n) break;
-    const uint64_t k = s_key[t + 1], kp = s_key[t];
-    uint32_t flags = 0;
+    } else {
 #pragma unroll
-    for (int q = 0; q < KM; ++q) {
-      if (q < K && ((e == 0) || (key_prefix(k, es[q]) != key_prefix(kp, es[q])))) {
-        flags |= 1u << q;
-        ++cur[q];
+      for (int i = 0; i < IT; ++i) k[i] = e0 + i < n ? j.keys[e0 + i] : 0ull;
+    }
+    uint64_t prev = __shfl_up(k[IT - 1], 1);
+    if (lane == 0) prev = (e0 > 0 && e0 - 1 < n) ? j.keys[e0 - 1] : 0ull;
+    // boundary bits of this thread's elements per level (bit i = element e0 + i),
+    // route-prefix changes, duplicate keys
+    uint32_t fl[KM];
+#pragma unroll
+    for (int q = 0; q < KM; ++q) fl[q] = 0;
+    uint32_t rbits = 0;
+    bool dup = false;
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      const int64_t e = e0 + i;
+      if (e >= n) continue;
+      const uint64_t kp = i == 0 ? prev : k[i - 1];
+#pragma unroll
+      for (int q = 0; q < KM; ++q)
+        if (q < K && (e == 0 || key_prefix(k[i], es[q]) != key_prefix(kp, es[q]))) fl[q] |= 1u << i;
+      if (e == 0 || (j.rg.shift < 64 && (k[i] >> j.rg.shift) != (kp >> j.rg.shift)) || e == n - 1) rbits |= 1u << i;
+      dup |= e > 0 && k[i] == kp;
+    }
+    if (j.check_dup && dup) raise_status(j.status, ALTO_E_DUPLICATE);
+    // node counts: four levels per 64-bit word, 16-bit fields
+    uint64_t pw[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) pw[p] = 0;
+#pragma unroll
+    for (int q = 0; q < KM; ++q) pw[q / 4] += (uint64_t)__popc(fl[q]) << (16 * (q % 4));
+    uint64_t ex[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      uint64_t tot;
+      ex[p] = block_excl_scan<uint64_t, NT>(pw[p], s_w, &tot);
+      if (threadIdx.x < KM && threadIdx.x / 4 == p) s_tot[threadIdx.x] = (uint32_t)((tot >> (16 * (threadIdx.x % 4))) & 0xFFFFu);
+    }
+    __syncthreads();
+    if (threadIdx.x < K) {
+      const int q = threadIdx.x;
+      lb_publish(j.lb_status + q, tile, SEG_LB_STRIDE, s_tot[q]);
+      const uint32_t excl = lb_resolve(j.lb_status + q, tile, SEG_LB_STRIDE, s_tot[q], j.status);
+      s_excl[q] = excl;
+      if (tile == ntiles - 1) {
+        s_tot[q] = excl + s_tot[q];   // node count of the level
+        j.nnodes[lo + q] = (int64_t)s_tot[q];
       }
     }
-    if (j.check_dup && e > 0 && k == kp) raise_status(j.status, ALTO_E_DUPLICATE);
+    __syncthreads();
+    // ids: base[q] = level-q boundaries before this thread's first element
+    int32_t base[KM];
+#pragma unroll
+    for (int q = 0; q < KM; ++q)
+      base[q] = q < K ? (int32_t)(s_excl[q] + (uint32_t)((ex[q / 4] >> (16 * (q % 4))) & 0xFFFFu)) : 0;
+    // destination offsets, where the route prefix changes (keys reloaded: rare)
+    if (j.dest_offsets) {
+      int64_t* offs = j.dest_offsets;
+      for (uint32_t r = rbits; r; r &= r - 1) {
+        const int i = __builtin_ctz(r);
+        const int64_t e = e0 + i;
+        const uint64_t kk = j.keys[e];
+        const uint32_t d = dest_of_key(j.rg, kk);
+        const bool change = e == 0 || (j.rg.shift < 64 && (kk >> j.rg.shift) != (j.keys[e - 1] >> j.rg.shift));
+        if (e == 0) {
+          for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
+        } else if (change) {
+          const uint32_t dp = dest_of_key(j.rg, j.keys[e - 1]);
+          for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = e;
+        }
+        if (e == n - 1)
+          for (uint32_t x = d + 1; x <= j.rg.num_dest; ++x) offs[x] = n;
+      }
+    }
+    // node records at the boundaries
 #pragma unroll
     for (int q = 0; q < KM; ++q) {
       if (q >= K) continue;
       const int m = lo + q;
-      if (flags & (1u << q)) {
-        const int32_t id = cur[q];
-        const LevelNodes& L = j.lv[m];
+      const LevelNodes& L = j.lv[m];
+      for (uint32_t r = fl[q]; r; r &= r - 1) {
+        const int i = __builtin_ctz(r);
+        const int64_t e = e0 + i;
+        const uint32_t below = (1u << i) - 1u;
+        const int32_t id = base[q] + __popc(fl[q] & below);
         L.start[id] = (int32_t)e;
-        if (q + 1 < K) L.fc[id] = cur[q + 1 < KM ? q + 1 : q];
-        if (q > 0) L.par[id] = cur[q > 0 ? q - 1 : 0];
+        // a boundary of this level is one of the next: the first child starts here
+        if (q + 1 < K) L.fc[id] = base[q + 1 < KM ? q + 1 : q] + __popc(fl[q + 1 < KM ? q + 1 : q] & below);
+        if (q > 0) L.par[id] = base[q > 0 ? q - 1 : 0] + __popc(fl[q > 0 ? q - 1 : 0] & (below | (1u << i))) - 1;
         L.nfan[id] = fan_at(j, m, e);
         L.bad[id] = 0;
         if (q == 0 && j.carry_fan) {
           for (int mm = j.carry_lo; mm < lo; ++mm)
             j.carry_fan[(int64_t)(mm - j.carry_lo) * j.carry_ld + id] = fan_at(j, mm, e);
         }
-      } else if (j.chain_check) {
-        if (fan_at(j, m, e) != fan_at(j, m, e - 1)) raise_status(j.status, ALTO_E_FANOUT);
+      }
+      if (j.chain_check) {
+        // records: carriers of one node must declare the same fan
+        for (int i = 0; i < IT; ++i) {
+          const int64_t e = e0 + i;
+          if (e >= n) break;
+          if (!((fl[q] >> i) & 1u) && fan_at(j, m, e) != fan_at(j, m, e - 1)) raise_status(j.status, ALTO_E_FANOUT);
+        }
       }
     }
+    if (tile == ntiles - 1 && threadIdx.x == 0) {
+      // sentinels: start[N] = element count, fc[N] = node count of the next level
+      for (int q = 0; q < K; ++q) {
+        const LevelNodes& L = j.lv[lo + q];
+        L.start[s_tot[q]] = (int32_t)n;
+        if (q + 1 < K) L.fc[s_tot[q]] = (int32_t)s_tot[q + 1];
+      }
+    }
+    __syncthreads();   // shared words and the ticket are reused by the next tile
   }
-}
-
-__global__ void k_seg_sentinels(SegJob j) {
-  const int64_t n = nelem(j);
-  const int m = j.lo + (int)threadIdx.x;
-  if (blockIdx.x != 0 || m >= j.elem_level) return;
-  const int64_t N = j.nnodes[m];
-  j.lv[m].start[N] = (int32_t)n;
-  if (m + 1 < j.elem_level) j.lv[m].fc[N] = (int32_t)j.nnodes[m + 1];
 }
 
 // Completion of the level-m nodes (children are level m+1 nodes, or elements when
@@ -275,22 +290,19 @@ __global__ __launch_bounds__(256) void k_elem_bad(SegJob j) {
 
 }  // namespace
 
-int seg_blocks(int64_t n_max) { return (int)(n_max < 1 ? 1 : cdiv(n_max, SEG_TILE)); }
+int seg_tiles(int64_t n_max) { return (int)(n_max < 1 ? 1 : cdiv(n_max, SEG_TILE)); }
 
 int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st) {
-  const int nblk = seg_blocks(job.n_max);
   const int K = job.elem_level - job.lo;
   if (K <= 0) return ALTO_OK;
-  k_seg_count<<<nblk, NT, 0, st>>>(g, job, nblk);
-  // one scan over all levels' block counts; level m's ids are relative to its first entry
-  const int64_t len = (int64_t)K * nblk;
-  int rc = scan_exclusive<int32_t>(job.blkcnt, job.blkcnt, len + 1, nullptr, job.scan_part, nullptr, st);
-  if (rc) return rc;
-  k_seg_totals<<<1, 1, 0, st>>>(job, nblk, len);
-  if (K <= 2) k_seg_write<2><<<nblk, NT, 0, st>>>(g, job, nblk);
-  else if (K <= 4) k_seg_write<4><<<nblk, NT, 0, st>>>(g, job, nblk);
-  else k_seg_write<ALTO_MAX_LEVELS><<<nblk, NT, 0, st>>>(g, job, nblk);
-  k_seg_sentinels<<<1, 64, 0, st>>>(job);
+  const int tiles = seg_tiles(job.n_max);
+  if (!job.lb_status || !job.lb_ctr || job.lb_tiles < tiles) return ALTO_E_ARG;
+  const int64_t pb = cdiv((int64_t)tiles * SEG_LB_STRIDE, 256);
+  k_seg_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(job);
+  const int grid = tiles < 1024 ? tiles : 1024;
+  if (K <= 2) k_seg_pass<2><<<grid, NT, 0, st>>>(g, job);
+  else if (K <= 4) k_seg_pass<4><<<grid, NT, 0, st>>>(g, job);
+  else k_seg_pass<ALTO_MAX_LEVELS><<<grid, NT, 0, st>>>(g, job);
   if (job.elem_ok) k_elem_bad<<<NODE_GRID, 256, 0, st>>>(job);
   for (int m = job.elem_level - 1; m >= job.lo; --m) k_seg_nodes<<<NODE_GRID, 256, 0, st>>>(g, job, m);
   ALTO_LAUNCH_CHECK();

@@ -327,21 +327,11 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
 // ---- single-pass passes (decoupled look-back) -----------------------------------
 // Each pass is one persistent kernel. A block takes tile tickets in order; for a
 // tile it ranks the digits locally, publishes the tile's per-digit counts, and looks
-// back over earlier tiles (whose tickets were taken before, so they are running or
-// done) for the exclusive prefix of every digit; global digit bases come from
-// counts taken for all passes in one earlier sweep over the input. Status words:
-// 0 = not yet published, bit 31 = inclusive prefix in bits 0-30, bit 30 = tile
-// count in bits 0-29. Two status regions alternate between passes; a pass clears
-// the other region at its own tiles for the next pass.
-#define OS_INC (1u << 31)
-#define OS_AGG (1u << 30)
-#define OS_SPIN_LIMIT (1 << 22)
-#ifndef OS_LOOKBACK
-#define OS_LOOKBACK 1   // earlier tiles read per look-back round trip
-#endif
+// back over earlier tiles (lb_publish / lb_resolve) for the exclusive prefix of
+// every digit; global digit bases come from counts taken for all passes in one
+// earlier sweep over the input. Two status regions alternate between passes; a
+// pass clears the other region at its own tiles for the next pass.
 #define OS_GRID 1024
-
-__device__ inline uint32_t os_value(uint32_t w) { return (w & OS_INC) ? (w & ~OS_INC) : (w & (OS_AGG - 1u)); }
 
 // Counter copies of the digit counting sweep: 16-bit counters, two digits to a word,
 // `copies` copies picked by lane so that a row whose lanes share one digit (common
@@ -539,8 +529,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
         s_cnt[ww][d] = (uint16_t)run;
         run += cc;
       }
-      __hip_atomic_store(&st[tile * SORT_BUCKETS + d], (tile == 0 ? OS_INC : OS_AGG) | run, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+      lb_publish(st + d, tile, SORT_BUCKETS, run);
     }
     uint32_t tot;
     {
@@ -558,43 +547,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
       }
     }
     if (d < SORT_BUCKETS) {
-      uint32_t excl = 0;
-      if (tile > 0) {
-        // OS_LOOKBACK earlier tiles per round trip: an unpublished tile is waited
-        // for (bounded), a tile count is added and passed, an inclusive prefix
-        // ends the walk (tile 0 always publishes one)
-        int64_t t = tile - 1;
-        bool done = false;
-        while (!done) {
-          uint32_t v[OS_LOOKBACK];
-#pragma unroll
-          for (int k = 0; k < OS_LOOKBACK; ++k)
-            v[k] = t - k >= 0 ? __hip_atomic_load(&st[(t - k) * SORT_BUCKETS + d], __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT)
-                              : OS_INC;
-#pragma unroll
-          for (int k = 0; k < OS_LOOKBACK; ++k) {
-            if (done) break;
-            uint32_t u = v[k];
-            int spin = 0;
-            while (u == 0) {
-              if (++spin > OS_SPIN_LIMIT) {
-                // give up so that the kernel ends; the outputs are then invalid
-                if (b.status) raise_status(b.status, ALTO_E_INTERNAL);
-                u = OS_INC;
-                break;
-              }
-              __builtin_amdgcn_s_sleep(1);
-              u = __hip_atomic_load(&st[(t - k) * SORT_BUCKETS + d], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            excl += os_value(u);
-            if (u & OS_INC) done = true;
-          }
-          t -= OS_LOOKBACK;
-        }
-        __hip_atomic_store(&st[tile * SORT_BUCKETS + d], OS_INC | (excl + run), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-      }
+      const uint32_t excl = lb_resolve(st + d, tile, SORT_BUCKETS, run, b.status);
       s_gbase[d] = b.os_hist[slot * SORT_BUCKETS + d] + excl;
       st_next[tile * SORT_BUCKETS + d] = 0;   // the next pass's status of this tile
     }

@@ -532,8 +532,9 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
   j.check_dup = 1;
   for (int m = 0; m <= ALTO_MAX_LEVELS; ++m) j.lv[m] = b.lv[m];
   j.nnodes = b.nnodes;
-  j.blkcnt = b.blkcnt;
-  j.scan_part = b.scan_i32;
+  j.lb_status = b.os_status;
+  j.lb_ctr = b.os_ctr;
+  j.lb_tiles = b.os_ntiles * 2 * SORT_BUCKETS / SEG_LB_STRIDE;   // the sort's status words, free by now
   j.fp_nodes = b.fp_nodes;
   j.status = status;
   rc = seg_run(g, j, st);
