@@ -19,6 +19,28 @@ __device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : 
 // in flight; each block leaves one record of partial results (no contended atomics).
 constexpr int PU = 4;
 constexpr int PREP_GRID = 2048;
+constexpr int PREP_FLOW_SLOTS = 2048;   // per-block LDS set of route prefixes already inserted
+
+// Inserts a route prefix into the flow set through a block-local LDS set: a prefix
+// the block has seen goes to the global set once per block (the global set sees
+// about blocks x flows inserts instead of one per element).
+__device__ inline void prep_flow_insert(uint64_t* s_fl, const FlowBufs& fl, uint64_t p, bool* full) {
+  uint32_t h = (uint32_t)((p * 0x9E3779B97F4A7C15ull) >> 53);   // 11 bits: PREP_FLOW_SLOTS
+  for (int probe = 0; probe < 8; ++probe) {
+    const uint64_t v = s_fl[h];
+    if (v == p) return;
+    if (v == ~0ull) {
+      const uint64_t old = atomicCAS((unsigned long long*)&s_fl[h], ~0ull, (unsigned long long)p);
+      if (old == ~0ull) {
+        flow_insert(fl, p, full);
+        return;
+      }
+      if (old == p) return;
+    }
+    h = (h + 1) & (PREP_FLOW_SLOTS - 1);
+  }
+  flow_insert(fl, p, full);   // local set crowded: straight to the global set
+}
 
 template <int NL>
 __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
@@ -37,6 +59,11 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
     tm[q] = g.tagmask[flo + q + 1];
   }
   bool bad_layout = false, bad_fan = false, flow_full = false;
+  __shared__ uint64_t s_fl[PREP_FLOW_SLOTS];
+  if (fl.hcap) {
+    for (int i = threadIdx.x; i < PREP_FLOW_SLOTS; i += PREP_NT) s_fl[i] = ~0ull;
+    __syncthreads();
+  }
   const int total = g.total;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += stride * PU) {
@@ -54,13 +81,20 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
       const int64_t i = i0 + u * stride;
       if (i >= n) continue;
       bad_layout |= (k[u] >> total) != 0;
-      const uint32_t d = dest_of_key(rg, k[u]);
-      if (dest) dest[i] = (int32_t)d;
+      if (!fl.hcap) {
+        // without flows the destinations are computed here; with flows the
+        // sort's counting sweep takes them from the ranked flows
+        const uint32_t d = dest_of_key(rg, k[u]);
+        if (dest) dest[i] = (int32_t)d;
+        dor |= d;
+        dand &= d;
+      } else {
+        dor = ~0u;   // unknown here: a fallback plan covers every destination bit
+        dand = 0u;
+      }
       kor |= k[u];
       kand &= k[u];
-      dor |= d;
-      dand &= d;
-      if (fl.hcap) flow_insert(fl, k[u] >> fl.shift, &flow_full);
+      if (fl.hcap) prep_flow_insert(s_fl, fl, k[u] >> fl.shift, &flow_full);
 #pragma unroll
       for (int q = 0; q < NL; ++q) {
         const uint32_t child = (uint32_t)((k[u] >> shc[q]) & (uint64_t)tm[q]);
@@ -548,6 +582,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
     f.ct_key = c.take<uint64_t>(h);
     f.ct_rank = c.take<uint32_t>(h);
     f.drank = c.take<uint16_t>((int64_t)1 << FLOW_DIRECT_BITS);
+    f.fdest = c.take<uint32_t>(f.fcap);
     f.flow_key = c.take<uint64_t>(f.fcap);
     f.flow_slot = c.take<uint32_t>(f.fcap);
     f.flow_sorted = c.take<uint64_t>(f.fcap);
@@ -589,17 +624,21 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
               int32_t* status, hipStream_t st, bool offsets_later) {
+  // flows (packed sort) only when the sort runs its multi-block passes
+  FlowBufs fl;
+  if (n > SORT_SMALL_MAX) fl = b.fl;
+  else memset(&fl, 0, sizeof(fl));
   {
     ProfScope ps(PH_PREP, st);
     k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
-    flow_clear_launch(b.fl, b.ctl, st);
+    flow_clear_launch(fl, b.ctl, st);
     k_zero_u64<<<1, 64, 0, st>>>(b.fp_in, ALTO_MAX_LEVELS + 1);
     k_zero_u64<<<1, 64, 0, st>>>(b.fp_nodes, ALTO_MAX_LEVELS + 1);
     const int nl = fhi >= flo ? fhi - flo + 1 : 0;
     const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
 #define ALTO_PREP_CASE(NLV)                                                                                   \
   case NLV:                                                                                                   \
-    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, b.fl, b.prep_part); \
+    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part); \
     break;
     switch (nl) {
       ALTO_PREP_CASE(0) ALTO_PREP_CASE(1) ALTO_PREP_CASE(2) ALTO_PREP_CASE(3) ALTO_PREP_CASE(4)
@@ -620,12 +659,13 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   sb.out_keys = b.sk;
   sb.out_vals = perm_out ? reinterpret_cast<uint32_t*>(perm_out) : b.perm;
   sb.ctl = b.ctl;
-  sb.fl = b.fl;
+  sb.fl = fl;
   sb.os_status = b.os_status;
   sb.os_ctr = b.os_ctr;
   sb.os_hist = b.os_hist;
   sb.os_ntiles = b.os_ntiles;
   sb.status = status;
+  sb.dest_out = fl.hcap ? dest : nullptr;   // with flows the counting sweep writes them
   b.perm_used = sb.out_vals;
   int rc = sort_pairs(sb, n, nullptr, rg, g.total, true, st);
   if (rc) return rc;

@@ -55,6 +55,7 @@ struct FlowBufs {
   uint64_t* ct_key;      // [hcap] compact rank table (power of two >= 2 x flows), ~0 = empty
   uint32_t* ct_rank;     // [hcap]
   uint16_t* drank;       // [1 << FLOW_DIRECT_BITS] rank by the varying bits of the prefix
+  uint32_t* fdest;       // [fcap] destination of each ranked flow
   int64_t hcap;          // power of two, 0 = flows not used
   int32_t shift;         // bits below the route level
   int32_t ib;            // bits of the largest input index
@@ -82,6 +83,8 @@ struct SortBufs {
   uint32_t* os_hist;         // [SORT_MAX_PASSES][256] global digit counts, then bases
   int64_t os_ntiles;         // >= sort_tiles(n_max)
   int32_t* status;           // raised to ALTO_E_INTERNAL if a look-back wait gives up (may be null)
+  int32_t* dest_out;         // with flows: destination of every input element, written by the
+                             // counting sweep (input order); null: not wanted
 };
 
 int sort_tiles(int64_t n_max);   // tiles of SORT_OS_TILE elements (look-back passes)
@@ -106,27 +109,6 @@ void flow_clear_launch(const FlowBufs& fl, SortCtl* ctl, hipStream_t st);
 // non-null) receive the sum.
 template <typename T>
 int scan_exclusive(const T* in, T* out, int64_t len_max, const int64_t* len_dev, T* part, T* total, hipStream_t st);
-
-__device__ inline uint64_t flow_slot0(const FlowBufs& fl, uint64_t p) {
-  return mix64(p ^ 0xD6E8FEB86659FD93ull) & ((uint64_t)fl.hcap - 1);
-}
-
-// Insert of a route-level prefix into the flow set (called from the input pass),
-// starting at slot h whose content v the caller has already read.
-__device__ inline void flow_insert_from(const FlowBufs& fl, uint64_t p, uint64_t h, uint64_t v, bool* overflow) {
-  if (v == p) return;
-  const uint64_t mask = (uint64_t)fl.hcap - 1;
-  for (int probe = 0; probe < 256; ++probe) {
-    if (probe > 0) v = fl.ht_key[h];
-    if (v == p) return;
-    if (v == ~0ull) {
-      const uint64_t old = atomicCAS((unsigned long long*)&fl.ht_key[h], ~0ull, (unsigned long long)p);
-      if (old == ~0ull || old == p) return;
-    }
-    h = (h + 1) & mask;
-  }
-  *overflow = true;
-}
 
 // Insert of a route-level prefix into the flow set (called from the input pass).
 __device__ inline void flow_insert(const FlowBufs& fl, uint64_t p, bool* overflow) {

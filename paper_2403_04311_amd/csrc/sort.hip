@@ -134,12 +134,13 @@ __global__ void k_flow_clear(FlowBufs fl) {
 
 // Compact rank table: the ranked flows in a table of about twice their number, so
 // that the lookups of the first pass stay in the caches.
-__global__ void k_ct_insert(FlowBufs fl, const SortCtl* ctl) {
+__global__ void k_ct_insert(FlowBufs fl, const SortCtl* ctl, uint32_t num_dest) {
   const int64_t F = ctl->nflows_c;
   const uint64_t mask = (uint64_t)ctl->ct_mask;
   const int dlo = ctl->dlo, dbits = ctl->dbits;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < F; r += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t p = fl.flow_sorted[r];
+    fl.fdest[r] = dest_of_prefix(p, num_dest);
     if (dbits >= 0) {
       fl.drank[(p >> dlo) & ((1ull << dbits) - 1ull)] = (uint16_t)r;
       continue;
@@ -279,7 +280,7 @@ __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
 // before any is resolved (independent loads), collisions are resolved afterwards.
 template <int NI>
 __device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n, uint64_t* out,
-                                  const uint16_t* s_drank) {
+                                  const uint16_t* s_drank, uint32_t* rank_out) {
   const int S = c.sbits;
   const int hi = S + c.ib;
   uint64_t key[NI];
@@ -291,6 +292,7 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
       const uint32_t rank = gi[j] < n ? s_drank[((key[j] >> S) >> c.dlo) & dm] : 0u;
+      rank_out[j] = rank;
       const uint64_t suffix = S == 0 ? 0ull : (key[j] & ((1ull << S) - 1ull));
       const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
       out[j] = gi[j] < n ? (r | (suffix << c.ib) | (uint64_t)gi[j]) : 0ull;
@@ -310,6 +312,7 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
   for (int j = 0; j < NI; ++j) {
     if (gi[j] >= n) {
       out[j] = 0;
+      rank_out[j] = 0;
       continue;
     }
     uint64_t hh = h[j], vv = v[j];
@@ -318,6 +321,7 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
       vv = b.fl.ct_key[hh];
     }
     const uint32_t rank = vv == p[j] ? b.fl.ct_rank[hh] : 0u;
+    rank_out[j] = rank;
     const uint64_t suffix = S == 0 ? 0ull : (key[j] & ((1ull << S) - 1ull));
     const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
     out[j] = r | (suffix << c.ib) | (uint64_t)gi[j];
@@ -356,10 +360,11 @@ __global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev) {
 __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
                                                   int max_passes, int copies) {
   const PassView c = read_pass(b.ctl, 0);
-  if (c.npass == 0) return;   // nothing varies, or sorted in one workgroup
+  int32_t* const dest_out = b.dest_out ? opaque(b.dest_out) : nullptr;
+  if (c.npass == 0 && (!dest_out || b.ctl->plan.idle)) return;   // nothing varies, or sorted in one workgroup
   const int64_t n = load_n(n_host, n_dev);
   const int64_t ntiles = cdiv(n, TILE);
-  const bool packed = c.mode == SORT_PACKED;
+  const bool packed = c.mode == SORT_PACKED && c.npass > 0;
   extern __shared__ uint32_t s_hw[];
   __shared__ int s_sh[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
   const int np = c.npass < max_passes ? c.npass : max_passes;   // npass <= max_passes by the plan
@@ -367,10 +372,18 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
   for (int i = threadIdx.x; i < np * wpp; i += NT) s_hw[i] = 0;
   // packed mode with a direct rank table: the table follows the counters
   uint16_t* const s_drank = (packed && c.dbits >= 0) ? reinterpret_cast<uint16_t*>(s_hw + max_passes * wpp) : nullptr;
+  // and the flows' destinations (ranks < 2^dbits), after the rank table
+  uint32_t* const s_fdest = s_drank ? s_hw + max_passes * wpp + (1 << FLOW_DIRECT_BITS) / 2 : nullptr;
   if (s_drank) {
     const uint16_t* dr = opaque(b.fl.drank);
     for (int i = threadIdx.x; i < (1 << c.dbits); i += NT) s_drank[i] = dr[i];
+    if (dest_out) {
+      const uint32_t* fd = opaque(b.fl.fdest);
+      const int F = (int)b.ctl->nflows_c;
+      for (int i = threadIdx.x; i < F; i += NT) s_fdest[i] = fd[i];
+    }
   }
+  const uint32_t* const g_fdest = packed ? opaque(b.fl.fdest) : nullptr;
   if (threadIdx.x < SORT_MAX_PASSES) {
     const SortPass ps = b.ctl->plan.pass[threadIdx.x];
     s_sh[threadIdx.x] = (packed ? c.ib : 0) + ps.lo;
@@ -388,18 +401,30 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
     uint64_t key[IT];
 #pragma unroll
     for (int j = 0; j < IT; ++j) gi[j] = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    uint32_t dv[IT];
     if (packed) {
-      pack_items<IT>(b, c, gi, n, key, s_drank);
+      uint32_t rank[IT];
+      pack_items<IT>(b, c, gi, n, key, s_drank, rank);
 #pragma unroll
       for (int j = 0; j < IT; ++j)
         if (gi[j] < n) stage[gi[j]] = key[j];
+      if (dest_out) {
+        // the element's destination is its flow's (ranks follow (destination, prefix))
+#pragma unroll
+        for (int j = 0; j < IT; ++j)
+          if (gi[j] < n) dest_out[gi[j]] = (int32_t)(s_fdest ? s_fdest[rank[j]] : g_fdest[rank[j]]);
+      }
     } else {
 #pragma unroll
       for (int j = 0; j < IT; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
-    }
-    uint32_t dv[IT];
 #pragma unroll
-    for (int j = 0; j < IT; ++j) dv[j] = any_dest ? dest_of_key(rg, key[j]) : 0u;
+      for (int j = 0; j < IT; ++j) dv[j] = (any_dest || dest_out) ? dest_of_key(rg, key[j]) : 0u;
+      if (dest_out) {
+#pragma unroll
+        for (int j = 0; j < IT; ++j)
+          if (gi[j] < n) dest_out[gi[j]] = (int32_t)dv[j];
+      }
+    }
     for (int q = 0; q < np; ++q) {
       const int sh = s_sh[q];
       const bool fd = s_fd[q] != 0;
@@ -898,7 +923,7 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     if (rc) return rc;
     const int64_t rb = cdiv(fl.fcap, 256);
     k_flow_rank<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, n_max, packable ? 1 : 0);
-    k_ct_insert<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl);
+    k_ct_insert<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, rg.num_dest);
   }
   const int mk = sort_max_key_windows(key_bits), md = sort_max_dest_windows(rg);
   int maxp = mk + md;   // general passes
@@ -913,7 +938,7 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
   const int64_t g0 = cdiv(htiles, os_hist_max_tiles(copies));
   const int grid_h = (int)(g0 > 1024 ? g0 : (htiles < 1024 ? htiles : 1024));
   const size_t lds = (size_t)passes * 128 * copies * sizeof(uint32_t) +
-                     (packable ? ((size_t)1 << FLOW_DIRECT_BITS) * sizeof(uint16_t) : 0);
+                     (packable ? ((size_t)1 << FLOW_DIRECT_BITS) * (sizeof(uint16_t) + sizeof(uint32_t)) : 0);
   const int64_t pb = cdiv((int64_t)ostiles * SORT_BUCKETS, 256);
   k_os_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(b, n_max, n_dev);
   k_sort_hist<<<grid_h, NT, lds, st>>>(b, n_max, n_dev, rg, passes, copies);
