@@ -86,6 +86,21 @@ def test_route_parity(D, Lr):
     assert np.array_equal(dest.cpu().numpy(), rt.dest)
 
 
+@pytest.mark.parametrize("op", ["concat", "mean"])
+def test_general_mode_sort(op):
+    """More distinct route prefixes than the flow set holds: the sort falls back to
+    (key, index) pairs with destination windows (no packed words)."""
+    bits = (17, 2, 2, 3)
+    path, fan, p32, pf = _case(321, 4, bits, (2, 2, 3), 40000, 0.01, 8)
+    keys = O.pack_keys(path, bits)
+    assert len(np.unique(O.prefix(keys, bits, 1))) > 32768
+    code, rt, g = U.oracle_aggregate(keys, fan, bits, 2, op, 8, 0, 1, 1000, p32, pf if op == "mean" else None)
+    assert code == O.OK
+    res = U.run_aggregate(keys, fan, bits, 2, op, 8, 0, 1, 1000, p32, pf if op == "mean" else None)
+    assert res["status"] == O.OK
+    U.compare(res, rt, g, op, 0, 2)
+
+
 def test_route_duplicate_and_layout():
     import torch
     from paper_2403_04311_amd import alto
