@@ -21,6 +21,78 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 PHASES = ["prep", "sort", "segment", "groups", "gather", "mean_kernel", "total"]
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_mean_zipf64M_traffic.json")
+MEAN_SRC = os.path.join(ROOT, "paper_2403_04311_amd", "csrc", "aggregate.hip")
+MEAN_KERNEL = "k_mean<4, 1, BatchSrc>"
+
+
+def mean_kernel_source_sha():
+    """sha256 of the mean-gather kernel's source text (its template through the
+    closing brace): the traffic measured by hardware counters is reported only
+    while this text is unchanged."""
+    import hashlib
+    src = open(MEAN_SRC).read()
+    a = src.index("template <int VEC, int CPL, typename Src>\n__global__ __launch_bounds__(256) void k_mean(")
+    b = src.index("\n}\n", a)
+    return hashlib.sha256(src[a:b].encode()).hexdigest()
+
+
+def derive_traffic(fetch_csv, write_csv, command):
+    """HBM bytes per launch of every kernel from two rocprofv3 --pmc runs of
+    `bench.py --steps 1 --warmup 1 --copy-calibration-mib M` (FETCH_SIZE, then
+    WRITE_SIZE, KiB per dispatch), each scaled by what the same counter reads for
+    the calibration copy of known size. Writes the summary next to the profiles."""
+    import csv
+    import collections
+    per = {}
+    calib = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == name]
+        cal = [r for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        big = max(cal, key=lambda r: int(r["Grid_Size"]))
+        calib[name] = float(big["Counter_Value"]) * 1024.0
+        acc = collections.defaultdict(list)
+        for r in rows:
+            k = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(")[0]
+            k = k[5:] if k.startswith("void ") else k
+            acc[k].append(float(r["Counter_Value"]) * 1024.0)
+        per[name] = acc
+    return calib, per
+
+
+def write_traffic_summary(fetch_csv, write_csv, copy_mib, command):
+    calib, per = derive_traffic(fetch_csv, write_csv, command)
+    known = copy_mib * 1024.0 * 1024.0
+    fs, ws = known / calib["FETCH_SIZE"], known / calib["WRITE_SIZE"]
+    kernels = {}
+    for k in sorted(set(per["FETCH_SIZE"]) | set(per["WRITE_SIZE"])):
+        f = per["FETCH_SIZE"].get(k, [])
+        w = per["WRITE_SIZE"].get(k, [])
+        if not f or not w:
+            continue
+        fb, wb = max(f) * fs, max(w) * ws   # the largest dispatch of each kernel (the full-size launch)
+        kernels[k] = {"fetch_bytes": fb, "write_bytes": wb, "dispatches": len(f)}
+    mk = kernels[MEAN_KERNEL]
+    out = {"kernel": MEAN_KERNEL, "source_sha256": mean_kernel_source_sha(),
+           "traffic_bytes_per_launch": mk["fetch_bytes"] + mk["write_bytes"],
+           "fetch_bytes_per_launch": mk["fetch_bytes"], "write_bytes_per_launch": mk["write_bytes"],
+           "calibration": {"copy_bytes": known, "FETCH_SIZE_scale": fs, "WRITE_SIZE_scale": ws},
+           "command": command, "kernels": kernels}
+    with open(TRAFFIC_SUMMARY, "w") as fh:
+        json.dump(out, fh, indent=1)
+    return out
+
+
+def measured_traffic():
+    """Traffic of the mean kernel per launch from the committed counter summary,
+    or None when there is none or the kernel's source changed since."""
+    try:
+        t = json.load(open(TRAFFIC_SUMMARY))
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != mean_kernel_source_sha():
+        return None
+    return t["traffic_bytes_per_launch"]
 
 
 def log(msg):
@@ -50,12 +122,21 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--leaves-log2", type=int, default=26)
-    ap.add_argument("--cpu-sample-log2", type=int, default=20)
+    ap.add_argument("--cpu-sample-log2", type=int, default=24)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before the workload (untimed), the "
                          "reference for scaling hardware byte counters")
+    ap.add_argument("--derive-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the mean kernel's HBM traffic summary from two rocprofv3 --pmc "
+                         "counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) and exit")
+    ap.add_argument("--pmc-command", default="", help="the rocprofv3 commands, recorded in the summary")
     args = ap.parse_args()
+    if args.derive_traffic:
+        out = write_traffic_summary(args.derive_traffic[0], args.derive_traffic[1],
+                                    args.copy_calibration_mib or 1024, args.pmc_command)
+        print(json.dumps({k: out[k] for k in ("kernel", "traffic_bytes_per_launch", "calibration")}))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
@@ -155,7 +236,7 @@ def main():
                    "fragments": n, "groups": E, "mask_nodes": M, "dim": dim, "num_dest": D},
         "roofline": {"bound": "hbm", "kernel": "k_mean (fp64-accumulating row gather)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(),
                      "algorithmic_bytes_per_launch": kern_bytes, "avg_launch_ms": kern_ms},
         "path_roofline": {"algorithmic_bytes_per_step": path_bytes, "bytes_per_fragment": per_frag,
                           "achieved": path_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
