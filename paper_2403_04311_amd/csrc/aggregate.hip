@@ -9,6 +9,7 @@ namespace {
 
 constexpr int PREP_NT = 256;
 constexpr int GRID_CAP = 4096;
+constexpr int MEAN_GRID = 2048;   // 8 blocks of 256 threads per CU
 
 __device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : h; }
 
@@ -364,7 +365,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 template <int VEC, int CPL, typename Src>
 __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src srcp,
-                                              int dim, int lpr, double* part, float* mean, int64_t cap_groups) {
+                                              int dim, int lpr, double* part, float* mean, int64_t cap_groups,
+                                              unsigned long long* ticket) {
   constexpr int NW = 4;
   constexpr int U = 2;   // row loads in flight per lane (more lowers occupancy)
   __shared__ double red[NW][64 * CPL * VEC];
@@ -372,8 +374,19 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
   const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
   const int rpw = ALTO_WAVE / lpr, sub = lane / lpr, cl = lane % lpr;
   const int64_t NC = *nchunks;
-  for (int64_t c = blockIdx.x; c < NC; c += gridDim.x) {
+  __shared__ int64_t s_c;
+  // chunks are taken by ticket: groups have very different sizes, and a block that
+  // finishes early takes the next chunk (the sum of a chunk does not depend on
+  // which block computes it)
+  while (true) {
+    if (threadIdx.x == 0) s_c = (int64_t)atomicAdd(ticket, 1ull);
+    __syncthreads();
+    const int64_t c = s_c;
+    if (c >= NC) break;   // uniform
     const Chunk ch = chunks[c];
+    // a row of the chunk that exists: lanes past the end load it and discard it, so
+    // that no load sits behind a branch (which would wait for each load in turn)
+    const int32_t row_safe = (int32_t)srcp.row(ch.begin);
     for (int col0 = 0; col0 < C; col0 += lpr * CPL) {
       double acc[CPL][VEC];
 #pragma unroll
@@ -391,27 +404,25 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
 #pragma unroll
           for (int u = 0; u < U; ++u) {
             const int r = (it0 + u) * rpw + sub;
-            const int32_t row = __shfl(myrow, r & (ALTO_WAVE - 1));
+            const int32_t rr = __shfl(myrow, r & (ALTO_WAVE - 1));
             const bool ok = (it0 + u < lpr) && r < nr;
-            const float* src = srcp.pay_of(row);
+            const float* src = srcp.pay_of(ok ? rr : row_safe);
 #pragma unroll
             for (int q = 0; q < CPL; ++q) {
               const int col = col0 + cl + q * lpr;
-              if (ok && col < C) {
-                // payload rows are read once: non-temporal loads keep them from
-                // displacing reusable lines in the caches
-                if constexpr (VEC == 4) {
-                  const f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + (int64_t)col * 4));
-                  x[u][q][0] = t[0];
-                  x[u][q][1] = t[1];
-                  x[u][q][2] = t[2];
-                  x[u][q][3] = t[3];
-                } else {
-                  x[u][q][0] = __builtin_nontemporal_load(src + col);
-                }
+              const bool okc = ok && col < C;
+              const int colc = col < C ? col : C - 1;
+              // payload rows are read once: non-temporal loads keep them from
+              // displacing reusable lines in the caches
+              if constexpr (VEC == 4) {
+                const f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + (int64_t)colc * 4));
+                x[u][q][0] = okc ? t[0] : 0.f;
+                x[u][q][1] = okc ? t[1] : 0.f;
+                x[u][q][2] = okc ? t[2] : 0.f;
+                x[u][q][3] = okc ? t[3] : 0.f;
               } else {
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) x[u][q][v] = 0.f;
+                const float t = __builtin_nontemporal_load(src + colc);
+                x[u][q][0] = okc ? t : 0.f;
               }
             }
           }
@@ -452,6 +463,7 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
       }
       __syncthreads();
     }
+    __syncthreads();   // s_c is rewritten by the next ticket
   }
 }
 
@@ -513,6 +525,7 @@ __global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* to
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   const int64_t G = *Gp;
   scal[1] = nch[G];
+  scal[2] = 0;   // chunk tickets of the mean gather
   const int64_t E = em[G];
   const int64_t T = tokc ? tokc[G] : 0;
   const int64_t M = Mp ? *Mp : 0;
@@ -812,11 +825,12 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
     while (lpr < C && lpr < 64) lpr <<= 1;
     const int cpl_need = (int)cdiv(C, lpr);
     const int cpl = cpl_need >= 4 ? 4 : cpl_need;
-    const int grid = GRID_CAP * 4;
+    const int grid = MEAN_GRID;   // persistent: chunks by ticket
 #define ALTO_MEAN_CASE(V, P)                                                                                 \
   do {                                                                                                       \
     ProfScope ps_mean(PH_MEAN, st);                                                                          \
-    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NCp, src, dim, lpr, b.part, out.mean, out.cap_groups); \
+    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NCp, src, dim, lpr, b.part, out.mean, out.cap_groups,  \
+                                            reinterpret_cast<unsigned long long*>(b.scal + 2));                 \
   } while (0)
     if (v4) {
       if (cpl == 1) ALTO_MEAN_CASE(4, 1);
