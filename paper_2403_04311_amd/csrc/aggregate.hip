@@ -25,7 +25,7 @@ constexpr int PREP_FLOW_SLOTS = 2048;   // per-block LDS set of route prefixes a
 // Inserts a route prefix into the flow set through a block-local LDS set: a prefix
 // the block has seen goes to the global set once per block (the global set sees
 // about blocks x flows inserts instead of one per element).
-__device__ inline void prep_flow_insert(uint64_t* s_fl, const FlowBufs& fl, uint64_t p, bool* full) {
+__device__ inline void prep_flow_insert(uint64_t* s_fl, const FlowBufs& fl, uint64_t p, uint32_t fan, bool* full) {
   uint32_t h = (uint32_t)((p * 0x9E3779B97F4A7C15ull) >> 53);   // 11 bits: PREP_FLOW_SLOTS
   for (int probe = 0; probe < 8; ++probe) {
     const uint64_t v = s_fl[h];
@@ -33,20 +33,23 @@ __device__ inline void prep_flow_insert(uint64_t* s_fl, const FlowBufs& fl, uint
     if (v == ~0ull) {
       const uint64_t old = atomicCAS((unsigned long long*)&s_fl[h], ~0ull, (unsigned long long)p);
       if (old == ~0ull) {
-        flow_insert(fl, p, full);
+        const int64_t slot = flow_insert(fl, p, full);
+        if (slot >= 0 && fl.child_ok) fl.ht_fan[slot] = fan;   // carriers agree unless a FANOUT error
         return;
       }
       if (old == p) return;
     }
     h = (h + 1) & (PREP_FLOW_SLOTS - 1);
   }
-  flow_insert(fl, p, full);   // local set crowded: straight to the global set
+  const int64_t slot = flow_insert(fl, p, full);   // local set crowded: straight to the global set
+  if (slot >= 0 && fl.child_ok) fl.ht_fan[slot] = fan;
 }
 
 template <int NL>
 __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
                                                   RouteGeom rg, int32_t* dest, const int32_t* __restrict__ fan,
-                                                  int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part) {
+                                                  int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part,
+                                                  int fq) {
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
   uint64_t fp[NL > 0 ? NL : 1];
@@ -95,7 +98,14 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
       }
       kor |= k[u];
       kand &= k[u];
-      if (fl.hcap) prep_flow_insert(s_fl, fl, k[u] >> fl.shift, &flow_full);
+      if (fl.hcap) {
+        // the route-level node's declared child count (column fq of those read)
+        uint32_t fr = 0;
+#pragma unroll
+        for (int q = 0; q < NL; ++q)
+          if (q == fq) fr = (uint32_t)f[u][q];
+        prep_flow_insert(s_fl, fl, k[u] >> fl.shift, fr, &flow_full);
+      }
 #pragma unroll
       for (int q = 0; q < NL; ++q) {
         const uint32_t child = (uint32_t)((k[u] >> shc[q]) & (uint64_t)tm[q]);
@@ -221,6 +231,8 @@ __global__ void k_init_ctl(SortCtl* ctl) {
     ctl->flow_overflow = 0;
     ctl->nflows = 0;
     ctl->nflows_c = 0;
+    ctl->cmode = 0;
+    ctl->dbits = -1;
   }
 }
 
@@ -596,6 +608,14 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
     f.ct_rank = c.take<uint32_t>(h);
     f.drank = c.take<uint16_t>((int64_t)1 << FLOW_DIRECT_BITS);
     f.fdest = c.take<uint32_t>(f.fcap);
+    f.ht_fan = c.take<uint32_t>(h);
+    f.fbase = c.take<uint32_t>(f.fcap + 1);
+    f.ctab_cap = n < ((int64_t)1 << 22) ? n : ((int64_t)1 << 22);
+    f.ctab = c.take<uint64_t>(f.ctab_cap);
+    // the child level (route level + 1); none when routing by the full key
+    f.cshift = Lr < g.depth ? g.shift[Lr + 1] : 0;
+    f.cmask = Lr < g.depth ? g.tagmask[Lr + 1] : 0u;
+    f.child_ok = 0;                 // set per call
     f.flow_key = c.take<uint64_t>(f.fcap);
     f.flow_slot = c.take<uint32_t>(f.fcap);
     f.flow_sorted = c.take<uint64_t>(f.fcap);
@@ -641,6 +661,12 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   FlowBufs fl;
   if (n > SORT_SMALL_MAX) fl = b.fl;
   else memset(&fl, 0, sizeof(fl));
+  // child ranks need the route level's declared child counts, read here when the
+  // route level is among the levels whose counts are checked
+  int fq = -1;
+  for (int m = flo; fan && m <= fhi; ++m)
+    if (rg.shift < 64 && g.shift[m] == rg.shift) fq = m - flo;
+  fl.child_ok = (fl.hcap && fq >= 0 && fl.cmask != 0u) ? 1 : 0;
   {
     ProfScope ps(PH_PREP, st);
     k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
@@ -651,7 +677,7 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
     const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
 #define ALTO_PREP_CASE(NLV)                                                                                   \
   case NLV:                                                                                                   \
-    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part); \
+    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part, fq); \
     break;
     switch (nl) {
       ALTO_PREP_CASE(0) ALTO_PREP_CASE(1) ALTO_PREP_CASE(2) ALTO_PREP_CASE(3) ALTO_PREP_CASE(4)

@@ -26,6 +26,7 @@ struct SortPass {
 
 struct SortPlan {
   int32_t npass;
+  int32_t first;         // slot of the first pass (packed passes end at the host's last packed slot)
   int32_t idle;          // the multi-block path does nothing (sorted in one workgroup)
   SortPass pass[SORT_MAX_PASSES];
 };
@@ -40,6 +41,9 @@ struct SortCtl {
   int32_t rbits;         // packed: bits of the flow rank (high bits)
   int32_t flow_overflow; // the flow set filled up
   int32_t dlo, dbits;    // packed: rank = drank[(prefix >> dlo) & (2^dbits - 1)]; dbits < 0: hashed table
+  int32_t cmode;         // packed by child rank: fbase[rank] + child tag replaces (rank, child tag)
+  int32_t pad2;
+  int64_t ctotal;        // child ranks in use (sum of the flows' declared child counts)
   int64_t nflows;        // distinct flows inserted
   int64_t nflows_c;      // the same, clamped to the flow capacity
   int64_t hist_len;      // histogram entries the scan covers (0 when idle)
@@ -56,6 +60,15 @@ struct FlowBufs {
   uint32_t* ct_rank;     // [hcap]
   uint16_t* drank;       // [1 << FLOW_DIRECT_BITS] rank by the varying bits of the prefix
   uint32_t* fdest;       // [fcap] destination of each ranked flow
+  // child ranks: a flow's children (the nodes one level below the route level) are
+  // numbered consecutively from fbase[rank], using the flow's declared child count
+  uint32_t* ht_fan;      // [hcap] declared child count of the flow in the slot (a carrier's)
+  uint32_t* fbase;       // [fcap + 1] first child rank of each ranked flow
+  uint64_t* ctab;        // [ctab_cap] child rank -> key bits above the child level's suffix
+  int64_t ctab_cap;
+  int32_t cshift;        // key bits below the child level
+  uint32_t cmask;        // tag mask of the child level
+  int32_t child_ok;      // the route level's declared child counts are read by the input pass
   int64_t hcap;          // power of two, 0 = flows not used
   int32_t shift;         // bits below the route level
   int32_t ib;            // bits of the largest input index
@@ -110,20 +123,22 @@ void flow_clear_launch(const FlowBufs& fl, SortCtl* ctl, hipStream_t st);
 template <typename T>
 int scan_exclusive(const T* in, T* out, int64_t len_max, const int64_t* len_dev, T* part, T* total, hipStream_t st);
 
-// Insert of a route-level prefix into the flow set (called from the input pass).
-__device__ inline void flow_insert(const FlowBufs& fl, uint64_t p, bool* overflow) {
+// Insert of a route-level prefix into the flow set (called from the input pass);
+// returns the prefix's slot, or -1 when the set overflowed.
+__device__ inline int64_t flow_insert(const FlowBufs& fl, uint64_t p, bool* overflow) {
   const uint64_t mask = (uint64_t)fl.hcap - 1;
   uint64_t h = mix64(p ^ 0xD6E8FEB86659FD93ull) & mask;
   for (int probe = 0; probe < 256; ++probe) {
     // a plain (cached) read is enough: a slot changes once, from empty to a key,
     // and the compare-and-swap settles a stale empty
     const uint64_t v = fl.ht_key[h];
-    if (v == p) return;
+    if (v == p) return (int64_t)h;
     if (v == ~0ull) {
       const uint64_t old = atomicCAS((unsigned long long*)&fl.ht_key[h], ~0ull, (unsigned long long)p);
-      if (old == ~0ull || old == p) return;
+      if (old == ~0ull || old == p) return (int64_t)h;
     }
     h = (h + 1) & mask;
   }
   *overflow = true;
+  return -1;
 }

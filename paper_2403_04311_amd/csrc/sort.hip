@@ -35,6 +35,8 @@ __global__ void k_sort_init(SortCtl* ctl) {
     ctl->flow_overflow = 0;
     ctl->nflows = 0;
     ctl->nflows_c = 0;
+    ctl->cmode = 0;
+    ctl->dbits = -1;
   }
 }
 
@@ -88,34 +90,42 @@ __device__ inline int greedy_windows(uint64_t v, int limit, int from_dest, SortP
 // ping-pong so that the last pass lands in the final buffers. With a device-side
 // count of at most SORT_SMALL_MAX the one-workgroup sort has done the work.
 __global__ void k_sort_plan(SortCtl* ctl, int64_t n_host, const int64_t* n_dev, int max_key_windows,
-                            int max_dest_windows) {
+                            int max_dest_windows, int packed_slots) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   const int64_t n = load_n(n_host, n_dev);
   SortPlan p;
+  SortPass win[SORT_MAX_PASSES];
   int np = 0;
   p.idle = (n_dev && n <= SORT_SMALL_MAX) ? 1 : 0;
+  const bool packed = ctl->mode == SORT_PACKED;
   if (!p.idle) {
-    if (ctl->mode == SORT_PACKED) {
+    if (packed) {
       const int S = ctl->sbits, R = ctl->rbits;
       uint64_t vs = (ctl->key_or ^ ctl->key_and) & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
       uint64_t vr = R > 0 ? (((1ull << R) - 1ull) << S) : 0ull;
-      np = greedy_windows(vs | vr, SORT_MAX_PASSES, 0, p.pass, np);
+      np = greedy_windows(vs | vr, SORT_MAX_PASSES, 0, win, np);
     } else {
-      np = greedy_windows(ctl->key_or ^ ctl->key_and, max_key_windows, 0, p.pass, np);
-      np = greedy_windows((uint64_t)(ctl->dest_or ^ ctl->dest_and), max_dest_windows, 1, p.pass, np);
+      np = greedy_windows(ctl->key_or ^ ctl->key_and, max_key_windows, 0, win, np);
+      np = greedy_windows((uint64_t)(ctl->dest_or ^ ctl->dest_and), max_dest_windows, 1, win, np);
     }
   }
-  for (int k = 0; k < np; ++k) {
-    p.pass[k].active = 1;
-    p.pass[k].dst = ((np - 1 - k) % 2 == 0) ? SORT_BUF_FINAL : SORT_BUF_TMP;
-    p.pass[k].src = (k == 0) ? SORT_BUF_INPUT : p.pass[k - 1].dst;
-  }
-  for (int k = np; k < SORT_MAX_PASSES; ++k) {
+  // packed passes end at the host's last packed slot, whose kernel also unpacks
+  const int first = (packed && packed_slots >= np) ? packed_slots - np : 0;
+  for (int k = 0; k < SORT_MAX_PASSES; ++k) {
     p.pass[k].active = 0;
     p.pass[k].src = p.pass[k].dst = 0;
     p.pass[k].from_dest = p.pass[k].lo = 0;
   }
+  for (int k = 0; k < np; ++k) {
+    SortPass& q = p.pass[first + k];
+    q.active = 1;
+    q.from_dest = win[k].from_dest;
+    q.lo = win[k].lo;
+    q.dst = ((np - 1 - k) % 2 == 0) ? SORT_BUF_FINAL : SORT_BUF_TMP;
+    q.src = (k == 0) ? SORT_BUF_INPUT : p.pass[first + k - 1].dst;
+  }
   p.npass = np;
+  p.first = first;
   ctl->plan = p;
 }
 
@@ -212,12 +222,80 @@ __global__ void k_flow_rank(FlowBufs fl, SortCtl* ctl, int64_t n, int allow_pack
   }
 }
 
+// Child ranks (packed mode with a direct rank table): the children of flow r (the
+// nodes one level below the route level) take the ranks fbase[r] .. fbase[r] +
+// count - 1 in tag order, with count the flow's declared child count. A packed word
+// then holds (child rank | key bits below the child level | index): the ranks of
+// all children together need fewer bits than (flow rank, child tag), since a tag
+// field must hold the largest child count. Used when every count is >= 1, the
+// ranks fit the lookup table and the word fits 64 bits; a child tag >= its declared
+// count is a FANOUT error, reported by the input pass (the order is then undefined).
+// One workgroup; flows <= 2^FLOW_DIRECT_BITS here.
+__global__ __launch_bounds__(1024) void k_flow_base(FlowBufs fl, SortCtl* ctl) {
+  __shared__ uint32_t s_w[1024 / ALTO_WAVE];
+  __shared__ int s_bad;
+  if (threadIdx.x == 0) {
+    ctl->cmode = 0;
+    s_bad = 0;
+  }
+  __syncthreads();
+  if (ctl->mode != SORT_PACKED || ctl->dbits < 0 || !fl.child_ok) return;   // uniform
+  const int F = (int)ctl->nflows_c;   // <= 2^FLOW_DIRECT_BITS = 4 per thread
+  uint32_t c[4], sum = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = threadIdx.x * 4 + k;
+    c[k] = r < F ? fl.ht_fan[fl.flow_slot[fl.flow_order[r]]] : 0u;
+    if (r < F && (c[k] < 1u || c[k] > (1u << 24))) s_bad = 1;
+    sum += c[k];
+  }
+  uint32_t tot;
+  uint32_t run = block_excl_scan<uint32_t, 1024>(sum, s_w, &tot);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int r = threadIdx.x * 4 + k;
+    if (r < F) fl.fbase[r] = run;
+    run += c[k];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    fl.fbase[F] = tot;
+    int R = 0;
+    while (R < 63 && ((int64_t)1 << R) < (int64_t)tot) ++R;
+    if (!s_bad && (int64_t)tot <= fl.ctab_cap && R + fl.cshift + fl.ib <= 64) {
+      ctl->cmode = 1;
+      ctl->ctotal = tot;
+      ctl->rbits = R;
+      ctl->sbits = fl.cshift;
+    }
+  }
+}
+
+// Child rank -> the key's bits above the child level's suffix (child-rank packing):
+// the flow r is the last whose first child rank is <= t (binary search over fbase),
+// the child tag is t - fbase[r]; the last pass then rebuilds a key with one lookup.
+__global__ void k_ctab_fill(FlowBufs fl, const SortCtl* ctl) {
+  if (!ctl->cmode) return;
+  const int64_t C = ctl->ctotal;
+  const int F = (int)ctl->nflows_c;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < C; t += (int64_t)gridDim.x * blockDim.x) {
+    int lo = 0, hi = F - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if ((int64_t)fl.fbase[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    fl.ctab[t] = (fl.flow_sorted[lo] << fl.shift) | ((uint64_t)(t - fl.fbase[lo]) << fl.cshift);
+  }
+}
+
 // What a pass kernel needs from the control block (kept in scalars, not a copy of
 // the whole block).
 struct PassView {
   SortPass ps;
   int32_t mode, ib, sbits, npass;
   int32_t dlo, dbits;
+  int32_t cmode;
+  int32_t first;
   uint64_t ct_mask;
 };
 
@@ -231,14 +309,18 @@ __device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
   v.ct_mask = (uint64_t)ctl->ct_mask;
   v.dlo = ctl->dlo;
   v.dbits = ctl->dbits;
+  v.cmode = ctl->cmode;
+  v.first = ctl->plan.first;
   return v;
 }
 
-__device__ inline uint64_t unpack_key(const uint64_t* flow_sorted, const PassView& c, uint64_t e) {
+__device__ inline uint64_t unpack_key(const FlowBufs& fl, const uint64_t* flow_sorted, const PassView& c,
+                                      uint64_t e) {
   const int S = c.sbits, hi = S + c.ib;
-  const uint64_t rank = hi >= 64 ? 0ull : (e >> hi);
+  const uint64_t top = hi >= 64 ? 0ull : (e >> hi);
   const uint64_t suffix = S == 0 ? 0ull : ((e >> c.ib) & ((1ull << S) - 1ull));
-  return (flow_sorted[rank] << S) | suffix;
+  if (c.cmode) return fl.ctab[top] | suffix;   // child rank -> (prefix, child tag)
+  return (flow_sorted[top] << S) | suffix;
 }
 
 // A pointer value hidden from the optimiser: selecting between buffers of the
@@ -280,19 +362,22 @@ __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
 // before any is resolved (independent loads), collisions are resolved afterwards.
 template <int NI>
 __device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n, uint64_t* out,
-                                  const uint16_t* s_drank, uint32_t* rank_out) {
+                                  const uint16_t* s_drank, const uint32_t* s_fbase, uint32_t* rank_out) {
   const int S = c.sbits;
   const int hi = S + c.ib;
   uint64_t key[NI];
 #pragma unroll
   for (int j = 0; j < NI; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
   if (s_drank) {
-    // direct table in LDS
+    // direct table in LDS; with child ranks, S is the bits below the child level and
+    // the route prefix sits above the child tag
     const uint64_t dm = (1ull << c.dbits) - 1ull;
+    const int SR = c.cmode ? b.fl.shift : S;   // bits below the route level
 #pragma unroll
     for (int j = 0; j < NI; ++j) {
-      const uint32_t rank = gi[j] < n ? s_drank[((key[j] >> S) >> c.dlo) & dm] : 0u;
-      rank_out[j] = rank;
+      const uint32_t rank0 = gi[j] < n ? s_drank[((key[j] >> SR) >> c.dlo) & dm] : 0u;
+      rank_out[j] = rank0;
+      const uint32_t rank = c.cmode ? s_fbase[rank0] + (uint32_t)((key[j] >> S) & b.fl.cmask) : rank0;
       const uint64_t suffix = S == 0 ? 0ull : (key[j] & ((1ull << S) - 1ull));
       const uint64_t r = hi >= 64 ? 0ull : ((uint64_t)rank << hi);
       out[j] = gi[j] < n ? (r | (suffix << c.ib) | (uint64_t)gi[j]) : 0ull;
@@ -344,11 +429,12 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
 __host__ __device__ inline int os_copies(int passes) { return passes <= 6 ? 16 : 8; }
 __host__ __device__ inline int os_hist_max_tiles(int copies) { return 65535 / (SORT_TILE / copies); }
 
-__global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev) {
+__global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev, int64_t region) {
   const int64_t n = load_n(n_host, n_dev);
-  const int64_t len = cdiv(n, OS_TILE) * SORT_BUCKETS;   // status region 0
+  const int64_t len = cdiv(n, OS_TILE) * SORT_BUCKETS;   // status words of the first pass
+  uint32_t* st = b.os_status + (b.ctl->plan.first & 1) * region;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
-    b.os_status[i] = 0;
+    st[i] = 0;
   if (blockIdx.x == 0) {
     for (int i = threadIdx.x; i < SORT_MAX_PASSES * SORT_BUCKETS; i += blockDim.x) b.os_hist[i] = 0;
     if (threadIdx.x < SORT_MAX_PASSES) b.os_ctr[threadIdx.x] = 0;
@@ -359,7 +445,8 @@ __global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev) {
 // composes the words and stages them for the first pass. Persistent.
 __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
                                                   int max_passes, int copies) {
-  const PassView c = read_pass(b.ctl, 0);
+  const int first = b.ctl->plan.first;
+  const PassView c = read_pass(b.ctl, first);
   int32_t* const dest_out = b.dest_out ? opaque(b.dest_out) : nullptr;
   if (c.npass == 0 && (!dest_out || b.ctl->plan.idle)) return;   // nothing varies, or sorted in one workgroup
   const int64_t n = load_n(n_host, n_dev);
@@ -374,18 +461,24 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
   uint16_t* const s_drank = (packed && c.dbits >= 0) ? reinterpret_cast<uint16_t*>(s_hw + max_passes * wpp) : nullptr;
   // and the flows' destinations (ranks < 2^dbits), after the rank table
   uint32_t* const s_fdest = s_drank ? s_hw + max_passes * wpp + (1 << FLOW_DIRECT_BITS) / 2 : nullptr;
+  // and the child-rank bases (child-rank packing)
+  uint32_t* const s_fbase = s_drank ? s_fdest + (1 << FLOW_DIRECT_BITS) : nullptr;
   if (s_drank) {
     const uint16_t* dr = opaque(b.fl.drank);
     for (int i = threadIdx.x; i < (1 << c.dbits); i += NT) s_drank[i] = dr[i];
+    const int F = (int)b.ctl->nflows_c;
     if (dest_out) {
       const uint32_t* fd = opaque(b.fl.fdest);
-      const int F = (int)b.ctl->nflows_c;
       for (int i = threadIdx.x; i < F; i += NT) s_fdest[i] = fd[i];
+    }
+    if (c.cmode) {
+      const uint32_t* fb = opaque(b.fl.fbase);
+      for (int i = threadIdx.x; i < F; i += NT) s_fbase[i] = fb[i];
     }
   }
   const uint32_t* const g_fdest = packed ? opaque(b.fl.fdest) : nullptr;
   if (threadIdx.x < SORT_MAX_PASSES) {
-    const SortPass ps = b.ctl->plan.pass[threadIdx.x];
+    const SortPass ps = b.ctl->plan.pass[first + threadIdx.x < SORT_MAX_PASSES ? first + threadIdx.x : 0];
     s_sh[threadIdx.x] = (packed ? c.ib : 0) + ps.lo;
     s_fd[threadIdx.x] = packed ? 0 : ps.from_dest;
   }
@@ -404,7 +497,7 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
     uint32_t dv[IT];
     if (packed) {
       uint32_t rank[IT];
-      pack_items<IT>(b, c, gi, n, key, s_drank, rank);
+      pack_items<IT>(b, c, gi, n, key, s_drank, s_fbase, rank);
 #pragma unroll
       for (int j = 0; j < IT; ++j)
         if (gi[j] < n) stage[gi[j]] = key[j];
@@ -444,7 +537,7 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
     const uint32_t* hq = s_hw + q * wpp + (d >> 1) * copies;
     uint32_t v = 0;
     for (int k = 0; k < copies; ++k) v += (hq[k] >> ((d & 1) * 16)) & 0xFFFFu;
-    if (v) atomicAdd(&b.os_hist[i], v);
+    if (v) atomicAdd(&b.os_hist[(first + q) * SORT_BUCKETS + d], v);
   }
 }
 
@@ -476,7 +569,10 @@ __device__ inline uint32_t pass_digit(bool packed, const SortPass& ps, int sh, c
 // unpacks it into key and input index); general mode moves a key and a value. One
 // instantiation per mode (each exits when the device chose the other), so that the
 // packed one keeps the registers of its simpler digits.
-template <bool PACKED>
+// Packed passes: LAST is the instantiation launched for the host's last packed slot,
+// where the plan puts the final pass; only it unpacks (keeping the unpacking code
+// and its registers out of the other passes).
+template <bool PACKED, bool LAST = false>
 __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesweep(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
                                                  int slot, int64_t region) {
   const PassView c = read_pass(b.ctl, slot);
@@ -484,7 +580,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
   const int64_t n = load_n(n_host, n_dev);
   const int64_t ntiles = cdiv(n, OS_TILE);
   constexpr bool packed = PACKED;
-  const bool last = (slot + 1 == c.npass);
+  const bool last = PACKED ? LAST : (slot + 1 == c.first + c.npass);
   const int sh = c.ib + c.ps.lo;
   __shared__ uint16_t s_cnt[NW][SORT_BUCKETS];
   __shared__ uint32_t s_base[SORT_BUCKETS];
@@ -577,19 +673,19 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
       st_next[tile * SORT_BUCKETS + d] = 0;   // the next pass's status of this tile
     }
     __syncthreads();
-    if (packed && !last) {
+    if (packed && !LAST) {
       for (uint32_t e = threadIdx.x; e < tot; e += NT) {
         const uint64_t el = s_key[e];
         const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
         dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = el;
       }
-    } else if (packed) {
+    } else if (packed && LAST) {
       const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
       for (uint32_t e = threadIdx.x; e < tot; e += NT) {
         const uint64_t el = s_key[e];
         const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
         const uint64_t g = (uint64_t)s_gbase[dg] + (e - s_base[dg]);
-        ok[g] = unpack_key(fsorted, c, el);
+        ok[g] = unpack_key(b.fl, fsorted, c, el);
         ov[g] = (uint32_t)(el & imask);
       }
     } else {
@@ -923,30 +1019,34 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     if (rc) return rc;
     const int64_t rb = cdiv(fl.fcap, 256);
     k_flow_rank<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, n_max, packable ? 1 : 0);
+    k_flow_base<<<1, 1024, 0, st>>>(fl, b.ctl);
     k_ct_insert<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, rg.num_dest);
+    const int64_t cb2 = cdiv(fl.ctab_cap, 256);
+    k_ctab_fill<<<(int)(cb2 < 1024 ? cb2 : 1024), 256, 0, st>>>(fl, b.ctl);
   }
   const int mk = sort_max_key_windows(key_bits), md = sort_max_dest_windows(rg);
   int maxp = mk + md;   // general passes
   if (maxp > SORT_MAX_PASSES) maxp = SORT_MAX_PASSES;
-  k_sort_plan<<<1, 1, 0, st>>>(b.ctl, n_max, n_dev, mk, md);
+  const int mp_slots = packable ? (int)cdiv(64 - b.fl.ib, SORT_RADIX) : 0;
+  k_sort_plan<<<1, 1, 0, st>>>(b.ctl, n_max, n_dev, mk, md, mp_slots < SORT_MAX_PASSES ? mp_slots : SORT_MAX_PASSES);
   ALTO_LAUNCH_CHECK();
   // passes at most: general windows, or packed windows over 64 - index bits
-  int mp = packable ? (int)cdiv(64 - b.fl.ib, SORT_RADIX) : 0;
-  if (mp > SORT_MAX_PASSES) mp = SORT_MAX_PASSES;
+  const int mp = mp_slots < SORT_MAX_PASSES ? mp_slots : SORT_MAX_PASSES;
   const int passes = mp > maxp ? mp : maxp;
   const int copies = os_copies(passes);
   const int64_t g0 = cdiv(htiles, os_hist_max_tiles(copies));
   const int grid_h = (int)(g0 > 1024 ? g0 : (htiles < 1024 ? htiles : 1024));
   const size_t lds = (size_t)passes * 128 * copies * sizeof(uint32_t) +
-                     (packable ? ((size_t)1 << FLOW_DIRECT_BITS) * (sizeof(uint16_t) + sizeof(uint32_t)) : 0);
+                     (packable ? ((size_t)1 << FLOW_DIRECT_BITS) * (sizeof(uint16_t) + 2 * sizeof(uint32_t)) : 0);
   const int64_t pb = cdiv((int64_t)ostiles * SORT_BUCKETS, 256);
-  k_os_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(b, n_max, n_dev);
+  const int64_t region = (int64_t)b.os_ntiles * SORT_BUCKETS;
+  k_os_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(b, n_max, n_dev, region);
   k_sort_hist<<<grid_h, NT, lds, st>>>(b, n_max, n_dev, rg, passes, copies);
   k_os_bases<<<1, SORT_MAX_PASSES * ALTO_WAVE, 0, st>>>(b);
   const int grid_o = ostiles < OS_GRID ? ostiles : OS_GRID;
-  const int64_t region = (int64_t)b.os_ntiles * SORT_BUCKETS;
   for (int slot = 0; slot < passes; ++slot) {
-    if (slot < mp) k_onesweep<true><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
+    if (slot + 1 == mp) k_onesweep<true, true><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
+    else if (slot < mp) k_onesweep<true, false><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
     if (slot < maxp) k_onesweep<false><<<grid_o, NT, 0, st>>>(b, n_max, n_dev, rg, slot, region);
   }
   k_sort_identity<<<grid_r, 256, 0, st>>>(b, n_max, n_dev);
