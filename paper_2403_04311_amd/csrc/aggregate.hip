@@ -217,22 +217,29 @@ __global__ __launch_bounds__(256) void k_prep_fold(const PrepPartial* part, int 
   }
 }
 
-__global__ void k_zero_u64(uint64_t* p, int count) {
-  for (int i = threadIdx.x; i < count; i += blockDim.x) p[i] = 0;
-}
-
-__global__ void k_init_ctl(SortCtl* ctl) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    ctl->key_or = 0;
-    ctl->key_and = ~0ull;
-    ctl->dest_or = 0;
-    ctl->dest_and = ~0u;
-    ctl->mode = SORT_GENERAL;
-    ctl->flow_overflow = 0;
-    ctl->nflows = 0;
-    ctl->nflows_c = 0;
-    ctl->cmode = 0;
-    ctl->dbits = -1;
+// Start of a routing call: control block, fingerprint sums and the flow set.
+__global__ void k_route_init(SortCtl* ctl, uint64_t* fp_in, uint64_t* fp_nodes, FlowBufs fl) {
+  if (blockIdx.x == 0) {
+    if (threadIdx.x == 0) {
+      ctl->key_or = 0;
+      ctl->key_and = ~0ull;
+      ctl->dest_or = 0;
+      ctl->dest_and = ~0u;
+      ctl->mode = SORT_GENERAL;
+      ctl->flow_overflow = 0;
+      ctl->nflows = 0;
+      ctl->nflows_c = 0;
+      ctl->cmode = 0;
+      ctl->dbits = -1;
+    }
+    for (int i = threadIdx.x; i <= ALTO_MAX_LEVELS; i += blockDim.x) {
+      fp_in[i] = 0;
+      fp_nodes[i] = 0;
+    }
+  }
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < fl.hcap; i += (int64_t)gridDim.x * blockDim.x) {
+    fl.ht_key[i] = ~0ull;
+    fl.ct_key[i] = ~0ull;
   }
 }
 
@@ -274,23 +281,76 @@ __global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, in
 }
 
 // Per-group scan inputs.
-__global__ __launch_bounds__(256) void k_group_flags(LevelNodes L, const int64_t* Gp, int32_t* em, int64_t* tokc,
-                                                     int64_t* nch, int64_t* pch, int chunk_rows) {
+// Group prefix sums in one pass: over groups u = 0..G (entry G holds the totals),
+// the exclusive sums of emitted (complete) flags, emitted tokens, mean chunks and
+// chunk partials (groups of more than one chunk). Tiles by ticket, sums across
+// tiles by look-back (64-bit words: token sums may exceed 2^30).
+constexpr int GS_NT = 256;
+constexpr int GS_IT = 16;
+constexpr int GS_TILE = GS_NT * GS_IT;
+
+__global__ void k_group_scan_prep(const int64_t* Gp, uint64_t* st, uint32_t* ctr) {
+  const int64_t len = cdiv(*Gp + 1, GS_TILE) * 4;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
+    st[i] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *ctr = 0;
+}
+
+__global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_t* Gp, int32_t* em, int64_t* tokc,
+                                                     int64_t* nch, int64_t* pch, int chunk_rows, uint64_t* st,
+                                                     uint32_t* ctr, int32_t* status) {
   const int64_t G = *Gp;
-  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
-    const bool ok = L.ok[u];
-    const int64_t cnt = (int64_t)L.start[u + 1] - L.start[u];
-    em[u] = ok ? 1 : 0;
-    tokc[u] = ok ? cnt : 0;
-    const int64_t c = ok ? cdiv(cnt, chunk_rows) : 0;
-    nch[u] = c;
-    pch[u] = c > 1 ? c : 0;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    em[G] = 0;
-    tokc[G] = 0;
-    nch[G] = 0;
-    pch[G] = 0;
+  const int64_t ntiles = cdiv(G + 1, GS_TILE);
+  __shared__ int64_t s_w[GS_NT / ALTO_WAVE];
+  __shared__ int64_t s_ex[4];
+  __shared__ uint32_t s_tile;
+  while (true) {
+    if (threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
+    __syncthreads();
+    const int64_t tile = (int64_t)s_tile;
+    if (tile >= ntiles) break;   // uniform
+    const int64_t u0 = tile * GS_TILE + (int64_t)threadIdx.x * GS_IT;
+    int64_t v[GS_IT][4];
+    int64_t sum[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < GS_IT; ++i) {
+      const int64_t u = u0 + i;
+      const bool ok = u < G && L.ok[u];
+      const int64_t cnt = ok ? (int64_t)L.start[u + 1] - L.start[u] : 0;
+      const int64_t c = ok ? cdiv(cnt, chunk_rows) : 0;
+      v[i][0] = ok ? 1 : 0;
+      v[i][1] = cnt;
+      v[i][2] = c;
+      v[i][3] = c > 1 ? c : 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sum[q] += v[i][q];
+    }
+    int64_t ex[4], tot[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) ex[q] = block_excl_scan<int64_t, GS_NT>(sum[q], s_w, &tot[q]);
+    if (threadIdx.x < 4) {
+      const int q = threadIdx.x;
+      const int64_t t = q == 0 ? tot[0] : q == 1 ? tot[1] : q == 2 ? tot[2] : tot[3];
+      lb64_publish(st + q, tile, 4, (uint64_t)t);
+      s_ex[q] = (int64_t)lb64_resolve(st + q, tile, 4, (uint64_t)t, status);
+    }
+    __syncthreads();
+    int64_t run[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) run[q] = s_ex[q] + ex[q];
+#pragma unroll
+    for (int i = 0; i < GS_IT; ++i) {
+      const int64_t u = u0 + i;
+      if (u <= G) {
+        em[u] = (int32_t)run[0];
+        tokc[u] = run[1];
+        nch[u] = run[2];
+        pch[u] = run[3];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) run[q] += v[i][q];
+    }
+    __syncthreads();   // s_ex and the ticket are reused by the next tile
   }
 }
 
@@ -528,10 +588,6 @@ __global__ void k_record_keys(LevelNodes L, const int64_t* Np, const uint64_t* _
     rkey[u] = key_prefix(sk[L.start[u]], shift);
 }
 
-__global__ void k_gplus1(const int64_t* Gp, int64_t* scal) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) scal[0] = *Gp + 1;
-}
-
 __global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* tokc, const int64_t* nch, const int64_t* Mp,
                          int64_t* counts, int64_t* tok_off, GroupOut out, int64_t* scal, int32_t* status) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
@@ -669,10 +725,8 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   fl.child_ok = (fl.hcap && fq >= 0 && fl.cmask != 0u) ? 1 : 0;
   {
     ProfScope ps(PH_PREP, st);
-    k_init_ctl<<<1, 1, 0, st>>>(b.ctl);
-    flow_clear_launch(fl, b.ctl, st);
-    k_zero_u64<<<1, 64, 0, st>>>(b.fp_in, ALTO_MAX_LEVELS + 1);
-    k_zero_u64<<<1, 64, 0, st>>>(b.fp_nodes, ALTO_MAX_LEVELS + 1);
+    const int64_t cb = fl.hcap > 0 ? cdiv(fl.hcap, 256) : 1;
+    k_route_init<<<(int)(cb < 2048 ? cb : 2048), 256, 0, st>>>(b.ctl, b.fp_in, b.fp_nodes, fl);
     const int nl = fhi >= flo ? fhi - flo + 1 : 0;
     const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
 #define ALTO_PREP_CASE(NLV)                                                                                   \
@@ -823,15 +877,17 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
   prof_begin(PH_GROUPS, st);
   const int64_t* Gp = b.nnodes + La;
   const LevelNodes& GL = b.lv[La];
-  k_group_flags<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, MEAN_CHUNK_ROWS);
-  k_gplus1<<<1, 1, 0, st>>>(Gp, b.scal);
-  // exclusive scans over G+1 entries (entry G is zero): entry G receives the total
-  const int64_t* G1 = b.scal;
-  int rc = scan_exclusive<int32_t>(b.em, b.em, n + 1, G1, b.scan_i32, nullptr, st);
-  if (!rc) rc = scan_exclusive<int64_t>(b.tokc, b.tokc, n + 1, G1, b.scan_i64, nullptr, st);
-  if (!rc) rc = scan_exclusive<int64_t>(b.nch, b.nch, n + 1, G1, b.scan_i64, nullptr, st);
-  if (!rc && agg.op == ALTO_MEAN_F32) rc = scan_exclusive<int64_t>(b.pch, b.pch, n + 1, G1, b.scan_i64, nullptr, st);
-  if (rc) return rc;
+  {
+    // the sort's status words and a ticket word are free by now
+    uint64_t* gst = reinterpret_cast<uint64_t*>(b.os_status);
+    uint32_t* gctr = b.os_ctr;
+    const int64_t tiles = cdiv(n + 1, GS_TILE);
+    if (tiles * 4 * 2 > (int64_t)b.os_ntiles * 2 * SORT_BUCKETS) return ALTO_E_ARG;   // never: words to spare
+    const int64_t pb = cdiv(tiles * 4, 256);
+    k_group_scan_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(Gp, gst, gctr);
+    k_group_scan<<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch,
+                                                                  MEAN_CHUNK_ROWS, gst, gctr, status);
+  }
   k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, out);
   k_chunks<<<grid_for(n / MEAN_CHUNK_ROWS + 1, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.chunks,
                                                                  MEAN_CHUNK_ROWS);

@@ -167,6 +167,38 @@ __device__ inline uint32_t lb_resolve(uint32_t* st, int64_t tile, int64_t stride
   return excl;
 }
 
+// The same with 64-bit words (bit 63 = inclusive prefix, bit 62 = count, 62-bit
+// values), for sums that may exceed 2^30 per tile.
+#define LB64_INC (1ull << 63)
+#define LB64_AGG (1ull << 62)
+
+__device__ inline void lb64_publish(uint64_t* st, int64_t tile, int64_t stride, uint64_t count) {
+  __hip_atomic_store(&st[tile * stride], (tile == 0 ? LB64_INC : LB64_AGG) | count, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint64_t lb64_resolve(uint64_t* st, int64_t tile, int64_t stride, uint64_t count, int32_t* status) {
+  if (tile == 0) return 0;
+  uint64_t excl = 0;
+  for (int64_t t = tile - 1;; --t) {
+    uint64_t u = __hip_atomic_load(&st[t * stride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int spin = 0;
+    while (u == 0) {
+      if (++spin > LB_SPIN_LIMIT) {
+        if (status) raise_status(status, ALTO_E_INTERNAL);
+        u = LB64_INC;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      u = __hip_atomic_load(&st[t * stride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    excl += u & (LB64_AGG - 1ull);
+    if (u & LB64_INC) break;
+  }
+  __hip_atomic_store(&st[tile * stride], LB64_INC | (excl + count), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return excl;
+}
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------

@@ -13,8 +13,8 @@
 #define SORT_BUCKETS 256
 #define SORT_MAX_PASSES 12
 #define SCAN_MAX_BLOCKS 1023
-#define SORT_SMALL_MAX 4096
-#define FLOW_CAP (1 << 15)
+#define SORT_SMALL_MAX 8192
+#define FLOW_CAP 8192          // flows sort in one workgroup (<= SORT_SMALL_MAX)
 #define FLOW_DIRECT_BITS 12   // flow prefixes varying within this many bits: direct rank table
 
 enum { SORT_BUF_INPUT = 0, SORT_BUF_TMP = 1, SORT_BUF_FINAL = 2 };
@@ -115,7 +115,6 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
                bool ctl_has_reduction, hipStream_t st);
 void sort_reduce_launch(const uint64_t* keys, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, SortCtl* ctl,
                         hipStream_t st);
-void flow_clear_launch(const FlowBufs& fl, SortCtl* ctl, hipStream_t st);
 
 // Exclusive scan of len (= *len_dev if len_dev, else len_max) elements; in may
 // equal out. part needs SCAN_MAX_BLOCKS + 1 entries; part[nb] and *total (if

@@ -135,13 +135,6 @@ __device__ inline uint32_t digit_of(const SortPass& ps, const RouteGeom& rg, uin
 }
 
 // ---- flows (packed mode) ----------------------------------------------------
-__global__ void k_flow_clear(FlowBufs fl) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < fl.hcap; i += (int64_t)gridDim.x * blockDim.x) {
-    fl.ht_key[i] = ~0ull;
-    fl.ct_key[i] = ~0ull;
-  }
-}
-
 // Compact rank table: the ranked flows in a table of about twice their number, so
 // that the lookups of the first pass stay in the caches.
 __global__ void k_ct_insert(FlowBufs fl, const SortCtl* ctl, uint32_t num_dest) {
@@ -965,12 +958,6 @@ int bits_for(int64_t v) {
   int b = 0;
   while (b < 63 && ((int64_t)1 << b) <= v) ++b;
   return b;
-}
-
-void flow_clear_launch(const FlowBufs& fl, SortCtl* ctl, hipStream_t st) {
-  if (fl.hcap <= 0) return;
-  const int64_t blocks = cdiv(fl.hcap, 256);
-  k_flow_clear<<<(int)(blocks < 2048 ? blocks : 2048), 256, 0, st>>>(fl);
 }
 
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
