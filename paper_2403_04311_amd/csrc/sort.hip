@@ -347,6 +347,21 @@ __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
   return __ballot(valid) & ~(((uint64_t)hi << 32) | lo);
 }
 
+// Stable in-wave rank of one row of 64 digits against the wave's running digit
+// counters `cnt` (LDS): the number of earlier elements with the same digit (rows
+// before this one, then lower lanes of this row); the counters advance past the
+// row. Every lane reads its digit's counter before the lowest lane of each digit
+// writes it back (one instruction after the other, in the wave's order), so no
+// broadcast is needed. Invalid lanes (digit 0) read but neither count nor write.
+__device__ inline uint32_t wave_rank(uint16_t* cnt, uint32_t dig, bool valid) {
+  const uint64_t peers = match_digit(dig, valid);
+  const uint32_t below =
+      __builtin_amdgcn_mbcnt_hi((uint32_t)(peers >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)peers, 0u));
+  const uint32_t old = cnt[dig];
+  if (valid && below == 0) cnt[dig] = (uint16_t)(old + (uint32_t)__popcll(peers));
+  return old + below;
+}
+
 // ---- packed passes: one 64-bit word per element, (rank | suffix | index) --------
 // The digit is a plain bit field of the word, so LDS holds only the staged words and
 // 16-bit per-wave counters. The words are composed once from the input keys and
@@ -354,13 +369,11 @@ __device__ inline uint64_t match_digit(uint32_t dig, bool valid) {
 // Packs IT input keys with their ranks: the first probe of every item is issued
 // before any is resolved (independent loads), collisions are resolved afterwards.
 template <int NI>
-__device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n, uint64_t* out,
-                                  const uint16_t* s_drank, const uint32_t* s_fbase, uint32_t* rank_out) {
+__device__ inline void pack_items(const SortBufs& b, const PassView& c, const int64_t* gi, int64_t n,
+                                  const uint64_t* key, uint64_t* out, const uint16_t* s_drank, const uint32_t* s_fbase,
+                                  uint32_t* rank_out) {
   const int S = c.sbits;
   const int hi = S + c.ib;
-  uint64_t key[NI];
-#pragma unroll
-  for (int j = 0; j < NI; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
   if (s_drank) {
     // direct table in LDS; with child ranks, S is the bits below the child level and
     // the route prefix sits above the child tag
@@ -419,7 +432,7 @@ __device__ inline void pack_items(const SortBufs& b, const PassView& c, const in
 // `copies` copies picked by lane so that a row whose lanes share one digit (common
 // for flow-rank digits) makes at most 64 / copies same-address LDS atomics; copies
 // sit in consecutive words (banks).
-__host__ __device__ inline int os_copies(int passes) { return passes <= 6 ? 16 : 8; }
+__host__ __device__ inline int os_copies(int passes) { return passes <= 6 ? 16 : 4; }
 __host__ __device__ inline int os_hist_max_tiles(int copies) { return 65535 / (SORT_TILE / copies); }
 
 __global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev, int64_t region) {
@@ -437,7 +450,7 @@ __global__ void k_os_prep(SortBufs b, int64_t n_host, const int64_t* n_dev, int6
 // Digit counts of every pass, in one sweep over the input. Packed mode also
 // composes the words and stages them for the first pass. Persistent.
 __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
-                                                  int max_passes, int copies) {
+                                                  int max_passes, int copies_h) {
   const int first = b.ctl->plan.first;
   const PassView c = read_pass(b.ctl, first);
   int32_t* const dest_out = b.dest_out ? opaque(b.dest_out) : nullptr;
@@ -448,12 +461,17 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
   extern __shared__ uint32_t s_hw[];
   __shared__ int s_sh[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
   const int np = c.npass < max_passes ? c.npass : max_passes;   // npass <= max_passes by the plan
+  // the counters were sized for max_passes passes of copies_h copies; fewer passes
+  // take more copies (up to 16) in the same words
+  int copies = copies_h;
+  while (copies < 16 && 2 * copies * np <= copies_h * max_passes) copies *= 2;
   const int wpp = 128 * copies;   // words per pass
   for (int i = threadIdx.x; i < np * wpp; i += NT) s_hw[i] = 0;
   // packed mode with a direct rank table: the table follows the counters
-  uint16_t* const s_drank = (packed && c.dbits >= 0) ? reinterpret_cast<uint16_t*>(s_hw + max_passes * wpp) : nullptr;
+  const int cwords = max_passes * 128 * copies_h;
+  uint16_t* const s_drank = (packed && c.dbits >= 0) ? reinterpret_cast<uint16_t*>(s_hw + cwords) : nullptr;
   // and the flows' destinations (ranks < 2^dbits), after the rank table
-  uint32_t* const s_fdest = s_drank ? s_hw + max_passes * wpp + (1 << FLOW_DIRECT_BITS) / 2 : nullptr;
+  uint32_t* const s_fdest = s_drank ? s_hw + cwords + (1 << FLOW_DIRECT_BITS) / 2 : nullptr;
   // and the child-rank bases (child-rank packing)
   uint32_t* const s_fbase = s_drank ? s_fdest + (1 << FLOW_DIRECT_BITS) : nullptr;
   if (s_drank) {
@@ -481,16 +499,36 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
   uint64_t* const stage = packed ? (c.ps.dst == SORT_BUF_TMP ? opaque(b.out_keys) : opaque(b.tmp_keys)) : nullptr;
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   const int copy = lane & (copies - 1);
+  const int lofs = w * (IT * ALTO_WAVE) + lane;   // tile-local index of item 0
+  // the input keys of the block's next tile are loaded while it works on the current
+  // one (the loads stay in flight across the counting)
+  const uint64_t* const ik = opaque(b.in_keys);
+  uint64_t nkey[IT];
+  auto load_keys = [&](int64_t t) {
+    const int64_t t0 = t * TILE;
+    if (t0 + TILE <= n) {
+#pragma unroll
+      for (int j = 0; j < IT; ++j) nkey[j] = ik[t0 + lofs + j * ALTO_WAVE];
+    } else {
+#pragma unroll
+      for (int j = 0; j < IT; ++j) nkey[j] = t0 + lofs + j * ALTO_WAVE < n ? ik[t0 + lofs + j * ALTO_WAVE] : 0ull;
+    }
+  };
+  if ((int64_t)blockIdx.x < ntiles) load_keys(blockIdx.x);
   for (int64_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
     const int64_t tile0 = t * TILE;
     int64_t gi[IT];
     uint64_t key[IT];
 #pragma unroll
-    for (int j = 0; j < IT; ++j) gi[j] = tile0 + (int64_t)w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    for (int j = 0; j < IT; ++j) {
+      gi[j] = tile0 + lofs + j * ALTO_WAVE;
+      key[j] = nkey[j];
+    }
+    if (t + gridDim.x < ntiles) load_keys(t + gridDim.x);
     uint32_t dv[IT];
     if (packed) {
       uint32_t rank[IT];
-      pack_items<IT>(b, c, gi, n, key, s_drank, s_fbase, rank);
+      pack_items<IT>(b, c, gi, n, key, key, s_drank, s_fbase, rank);
 #pragma unroll
       for (int j = 0; j < IT; ++j)
         if (gi[j] < n) stage[gi[j]] = key[j];
@@ -501,8 +539,6 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
           if (gi[j] < n) dest_out[gi[j]] = (int32_t)(s_fdest ? s_fdest[rank[j]] : g_fdest[rank[j]]);
       }
     } else {
-#pragma unroll
-      for (int j = 0; j < IT; ++j) key[j] = gi[j] < n ? b.in_keys[gi[j]] : 0ull;
 #pragma unroll
       for (int j = 0; j < IT; ++j) dv[j] = (any_dest || dest_out) ? dest_of_key(rg, key[j]) : 0u;
       if (dest_out) {
@@ -620,15 +656,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
     for (int j = 0; j < OS_IT; ++j) {
       const bool valid = lbase + j * ALTO_WAVE < rem;
       const uint32_t dig = valid ? pass_digit(packed, c.ps, sh, rg, key[j]) : 0u;
-      const uint64_t peers = match_digit(dig, valid);
-      const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
-      uint32_t old = 0;
-      if (valid && lane == leader) {
-        old = s_cnt[w][dig];
-        s_cnt[w][dig] = (uint16_t)(old + (uint32_t)__popcll(peers));
-      }
-      old = __shfl(old, leader);
-      dof[j] = dig | ((old + (uint32_t)__popcll(peers & lanemask_lt())) << 8);
+      dof[j] = dig | (wave_rank(s_cnt[w], dig, valid) << 8);
     }
     __syncthreads();
     // per-wave offsets of every digit, the tile's count published at once (so that
@@ -875,15 +903,7 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     for (int j = 0; j < SM_IT; ++j) {
       const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       const bool valid = e < n;
-      const uint64_t peers = match_digit(dig[j], valid);
-      const int leader = valid ? (__ffsll((unsigned long long)peers) - 1) : lane;
-      uint32_t old = 0;
-      if (valid && lane == leader) {
-        old = s_cnt[w][dig[j]];
-        s_cnt[w][dig[j]] = (uint16_t)(old + (uint32_t)__popcll(peers));
-      }
-      old = __shfl(old, leader);
-      off[j] = old + (uint32_t)__popcll(peers & lanemask_lt());
+      off[j] = wave_rank(s_cnt[w], dig[j], valid);
     }
     __syncthreads();
     if (threadIdx.x < SORT_BUCKETS) {
