@@ -290,6 +290,7 @@ struct PassView {
   int32_t cmode;
   int32_t first;
   uint64_t ct_mask;
+  uint64_t ctotal;
 };
 
 __device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
@@ -304,6 +305,7 @@ __device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
   v.dbits = ctl->dbits;
   v.cmode = ctl->cmode;
   v.first = ctl->plan.first;
+  v.ctotal = (uint64_t)ctl->ctotal;
   return v;
 }
 
@@ -312,7 +314,9 @@ __device__ inline uint64_t unpack_key(const FlowBufs& fl, const uint64_t* flow_s
   const int S = c.sbits, hi = S + c.ib;
   const uint64_t top = hi >= 64 ? 0ull : (e >> hi);
   const uint64_t suffix = S == 0 ? 0ull : ((e >> c.ib) & ((1ull << S) - 1ull));
-  if (c.cmode) return fl.ctab[top] | suffix;   // child rank -> (prefix, child tag)
+  // child rank -> (prefix, child tag); a rank past the table comes only from a child
+  // tag beyond its declared count (a FANOUT error, order undefined): kept in bounds
+  if (c.cmode) return fl.ctab[top < c.ctotal ? top : 0] | suffix;
   return (flow_sorted[top] << S) | suffix;
 }
 

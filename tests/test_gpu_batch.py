@@ -101,6 +101,25 @@ def test_general_mode_sort(op):
     U.compare(res, rt, g, op, 0, 2)
 
 
+def test_child_index_error_with_child_ranks():
+    """A child tag equal to its node's declared count in a batch that the sort packs
+    by child ranks over several workgroups: the FANOUT error is reported (the order is
+    undefined then, and the rank table is still read within bounds)."""
+    bits = (5, 5, 8, 8)
+    path, fan, p32, _ = _case(91, 4, bits, (6, 40, 60), 20)
+    keys = O.pack_keys(path, bits)
+    assert len(keys) > 8192
+    fan = fan.copy()
+    i = int(np.argmax(O.tag(keys, bits, 3)))
+    sel = O.prefix(keys, bits, 2) == O.prefix(keys[i:i + 1], bits, 2)[0]
+    fan[1, sel] = int(O.tag(keys[i:i + 1], bits, 3)[0])     # child index == declared count
+    La, Lm, Lr, D = 2, 0, 2, 16
+    code, _, _ = U.oracle_aggregate(keys, fan, bits, La, "concat", 1, Lm, Lr, D, p32)
+    assert code == O.E_FANOUT
+    res = U.run_aggregate(keys, fan, bits, La, "concat", 1, Lm, Lr, D, p32)
+    assert res["status"] == code
+
+
 def test_route_duplicate_and_layout():
     import torch
     from paper_2403_04311_amd import alto
