@@ -91,6 +91,7 @@ struct PrepPartial {
 
 struct AggBufs {
   PrepPartial* prep_part;   // per-block records of the input-order pass
+  int32_t fx_lo, fx_hi;     // count levels checked exactly per flow instead of by fingerprint (fx_lo > fx_hi: none)
   FlowBufs fl;          // flows of the route level (packed sort); hcap == 0 when unused
   uint32_t* os_status;  // sort passes: [2][tiles][256] tile status words
   uint32_t* os_ctr;     // [SORT_MAX_PASSES] tile tickets
@@ -127,7 +128,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
                   AggBufs& b);
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st, bool offsets_later = false);
+              int32_t* status, hipStream_t st, bool offsets_later = false, bool exact_flow_levels = false);
 // Groups, chunk lists, counts and payload gathers over an element array already
 // segmented at level La (nodes in b.lv[La]); elements sorted by (dest, key).
 template <typename Src>

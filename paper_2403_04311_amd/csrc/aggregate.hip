@@ -7,49 +7,50 @@
 
 namespace {
 
-constexpr int PREP_NT = 256;
+constexpr int PREP_NT = 1024;
 constexpr int GRID_CAP = 4096;
 constexpr int MEAN_GRID = 2048;   // 8 blocks of 256 threads per CU
 
 __device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : h; }
 
 // Input order, one pass: layout check, destination, OR/AND of keys and
-// destinations for the sort, flow-set inserts, per-fragment fan-out checks, and the
-// fragment side of the fan fingerprint. NL = number of count levels read (flo ..
-// flo + NL - 1); the per-level sums stay in registers. Each thread keeps PU elements
-// in flight; each block leaves one record of partial results (no contended atomics).
+// destinations for the sort, flow-set inserts, per-fragment fan-out checks, and
+// the carrier-agreement checks of the declared child counts. NL = number of count
+// levels read (flo .. flo + NL - 1). Levels xlo..xhi (the route level and up to
+// two levels above it: functions of the flow) are checked exactly: the block's LDS
+// flow set keeps, per flow and level, the first count seen, every later carrier
+// compares against it, and the block's flows are merged into the global set (and
+// their counts compared there) when the block ends. The other levels add their
+// terms to the fan fingerprint (sums stay in registers). Each thread keeps PU
+// elements in flight; each block leaves one record of partial results.
 constexpr int PU = 4;
-constexpr int PREP_GRID = 2048;
-constexpr int PREP_FLOW_SLOTS = 2048;   // per-block LDS set of route prefixes already inserted
+constexpr int PREP_GRID = 512;          // two blocks of PREP_NT threads per CU
+constexpr int PREP_SLOTS = 3072;        // LDS flow set of a block (open addressing)
+constexpr int PREP_PROBES = 16;         // then the global set directly
+constexpr int PREP_NX = FLOW_EXACT_LEVELS;
 
-// Inserts a route prefix into the flow set through a block-local LDS set: a prefix
-// the block has seen goes to the global set once per block (the global set sees
-// about blocks x flows inserts instead of one per element).
-__device__ inline void prep_flow_insert(uint64_t* s_fl, const FlowBufs& fl, uint64_t p, uint32_t fan, bool* full) {
-  uint32_t h = (uint32_t)((p * 0x9E3779B97F4A7C15ull) >> 53);   // 11 bits: PREP_FLOW_SLOTS
-  for (int probe = 0; probe < 8; ++probe) {
-    const uint64_t v = s_fl[h];
-    if (v == p) return;
-    if (v == ~0ull) {
-      const uint64_t old = atomicCAS((unsigned long long*)&s_fl[h], ~0ull, (unsigned long long)p);
-      if (old == ~0ull) {
-        const int64_t slot = flow_insert(fl, p, full);
-        if (slot >= 0 && fl.child_ok) fl.ht_fan[slot] = fan;   // carriers agree unless a FANOUT error
-        return;
-      }
-      if (old == p) return;
-    }
-    h = (h + 1) & (PREP_FLOW_SLOTS - 1);
-  }
-  const int64_t slot = flow_insert(fl, p, full);   // local set crowded: straight to the global set
-  if (slot >= 0 && fl.child_ok) fl.ht_fan[slot] = fan;
+__device__ inline uint32_t prep_slot(uint64_t p) {
+  uint32_t x = ((uint32_t)p ^ ((uint32_t)(p >> 32) * 0x9E3779B1u)) * 0x85EBCA6Bu;
+  x ^= x >> 15;
+  return (uint32_t)(((uint64_t)(x * 0xC2B2AE35u) * PREP_SLOTS) >> 32);
+}
+
+// The count of level x of the flow in global slot s: set by the first carrier
+// (0 = unset), compared by every later one. Returns false on a disagreement.
+__device__ inline bool flow_fan_check(const FlowBufs& fl, int x, int nx, int64_t s, uint32_t f) {
+  uint32_t* w = (x == nx - 1 && fl.x_route) ? &fl.ht_fan[s] : &fl.ht_anc[(int64_t)x * fl.hcap + s];
+  const uint32_t cur = *w;   // a count changes once, from 0; the CAS settles a stale 0
+  if (cur == f) return true;
+  if (cur != 0u) return false;
+  const uint32_t old = atomicCAS(w, 0u, f);
+  return old == 0u || old == f;
 }
 
 template <int NL>
 __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
                                                   RouteGeom rg, int32_t* dest, const int32_t* __restrict__ fan,
-                                                  int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part,
-                                                  int fq) {
+                                                  int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part, int qx0,
+                                                  int nx, int skip_fp) {
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
   uint64_t fp[NL > 0 ? NL : 1];
@@ -63,9 +64,14 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
     tm[q] = g.tagmask[flo + q + 1];
   }
   bool bad_layout = false, bad_fan = false, flow_full = false;
-  __shared__ uint64_t s_fl[PREP_FLOW_SLOTS];
+  __shared__ uint64_t s_fl[PREP_SLOTS];
+  __shared__ uint32_t s_ff[PREP_NX][PREP_SLOTS];
   if (fl.hcap) {
-    for (int i = threadIdx.x; i < PREP_FLOW_SLOTS; i += PREP_NT) s_fl[i] = ~0ull;
+    for (int i = threadIdx.x; i < PREP_SLOTS; i += PREP_NT) {
+      s_fl[i] = ~0ull;
+#pragma unroll
+      for (int x = 0; x < PREP_NX; ++x) s_ff[x][i] = 0u;
+    }
     __syncthreads();
   }
   const int total = g.total;
@@ -99,19 +105,60 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
       kor |= k[u];
       kand &= k[u];
       if (fl.hcap) {
-        // the route-level node's declared child count (column fq of those read)
-        uint32_t fr = 0;
+        const uint64_t p = k[u] >> fl.shift;
+        uint32_t h = prep_slot(p);
+        uint64_t v = s_fl[h];
+        int probes = 0;
+        while (v != p) {
+          if (v == ~0ull) {
+            const uint64_t old = atomicCAS((unsigned long long*)&s_fl[h], ~0ull, (unsigned long long)p);
+            if (old == ~0ull || old == p) break;
+          }
+          if (++probes >= PREP_PROBES) {
+            h = PREP_SLOTS;   // crowded: this element goes to the global set itself
+            break;
+          }
+          h = h + 1 == PREP_SLOTS ? 0 : h + 1;
+          v = s_fl[h];
+        }
+        if (h < PREP_SLOTS) {
 #pragma unroll
-        for (int q = 0; q < NL; ++q)
-          if (q == fq) fr = (uint32_t)f[u][q];
-        prep_flow_insert(s_fl, fl, k[u] >> fl.shift, fr, &flow_full);
+          for (int q = 0; q < NL; ++q) {
+            if (q < qx0 || q >= qx0 + nx) continue;   // uniform
+            const uint32_t fx = (uint32_t)f[u][q];
+            uint32_t* w = &s_ff[q - qx0][h];
+            const uint32_t cur = *w;
+            if (cur != fx) {
+              const uint32_t old = cur == 0u ? atomicCAS(w, 0u, fx) : cur;
+              bad_fan |= old != 0u && old != fx;
+            }
+          }
+        } else {
+          const int64_t s = flow_insert(fl, p, &flow_full);
+          if (s >= 0) {
+#pragma unroll
+            for (int q = 0; q < NL; ++q)
+              if (q >= qx0 && q < qx0 + nx) bad_fan |= !flow_fan_check(fl, q - qx0, nx, s, (uint32_t)f[u][q]);
+          }
+        }
       }
 #pragma unroll
       for (int q = 0; q < NL; ++q) {
         const uint32_t child = (uint32_t)((k[u] >> shc[q]) & (uint64_t)tm[q]);
         bad_fan |= (f[u][q] < 1) || ((int64_t)child >= (int64_t)f[u][q]);
-        fp[q] += fan_term(flo + q, key_prefix(k[u], sh[q]), (uint32_t)f[u][q]);
+        if (!skip_fp || q < qx0 || q >= qx0 + nx) fp[q] += fan_term(flo + q, key_prefix(k[u], sh[q]), (uint32_t)f[u][q]);
       }
+    }
+  }
+  if (fl.hcap) {
+    // the block's flows into the global set, with their counts
+    __syncthreads();
+    for (int h = threadIdx.x; h < PREP_SLOTS; h += PREP_NT) {
+      const uint64_t p = s_fl[h];
+      if (p == ~0ull) continue;
+      const int64_t s = flow_insert(fl, p, &flow_full);
+      if (s < 0) continue;
+      for (int x = 0; x < nx; ++x) bad_fan |= !flow_fan_check(fl, x, nx, s, s_ff[x][h]);
     }
   }
 #pragma unroll
@@ -150,6 +197,30 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
       for (int q = 0; q < NL; ++q) r.fp[q] += s_w[ww].fp[q];
     }
     part[blockIdx.x] = r;
+  }
+}
+
+// When the flow set overflowed, some fragments had no exact check: the exactly
+// checked levels then join the fingerprint (their terms over every fragment).
+__global__ __launch_bounds__(256) void k_prep_fp(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
+                                                 const int32_t* __restrict__ fan, int64_t fan_ld, int xlo, int xhi,
+                                                 const SortCtl* ctl, uint64_t* fp_in) {
+  if (!ctl->flow_overflow) return;
+  uint64_t fp[FLOW_EXACT_LEVELS];
+#pragma unroll
+  for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) fp[x] = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = keys[i];
+#pragma unroll
+    for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) {
+      const int m = xlo + x;
+      if (m <= xhi) fp[x] += fan_term(m, key_prefix(k, g.shift[m]), (uint32_t)fan[(int64_t)(m - 1) * fan_ld + i]);
+    }
+  }
+#pragma unroll
+  for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) {
+    const uint64_t v = wave_sum(fp[x]);
+    if (lane_id() == 0 && v && xlo + x <= xhi) atomicAdd((unsigned long long*)&fp_in[xlo + x], (unsigned long long)v);
   }
 }
 
@@ -240,6 +311,9 @@ __global__ void k_route_init(SortCtl* ctl, uint64_t* fp_in, uint64_t* fp_nodes, 
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < fl.hcap; i += (int64_t)gridDim.x * blockDim.x) {
     fl.ht_key[i] = ~0ull;
     fl.ct_key[i] = ~0ull;
+    fl.ht_fan[i] = 0u;
+#pragma unroll
+    for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) fl.ht_anc[(int64_t)x * fl.hcap + i] = 0u;
   }
 }
 
@@ -274,10 +348,14 @@ __global__ void k_fill_i64(int64_t* p, int64_t count, int64_t v) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
 }
 
-__global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status) {
+// Levels xlo..xhi were checked exactly per flow and have no fragment-side
+// fingerprint, unless the flow set overflowed (then k_prep_fp added it).
+__global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int xlo, int xhi,
+                             const SortCtl* ctl, int32_t* status) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  const bool all = ctl == nullptr || ctl->flow_overflow;
   for (int m = flo; m <= fhi; ++m)
-    if (fp_in[m] != fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
+    if ((all || m < xlo || m > xhi) && fp_in[m] != fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
 }
 
 // Per-group scan inputs.
@@ -665,6 +743,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
     f.drank = c.take<uint16_t>((int64_t)1 << FLOW_DIRECT_BITS);
     f.fdest = c.take<uint32_t>(f.fcap);
     f.ht_fan = c.take<uint32_t>(h);
+    f.ht_anc = c.take<uint32_t>((int64_t)FLOW_EXACT_LEVELS * h);
     f.fbase = c.take<uint32_t>(f.fcap + 1);
     f.ctab_cap = n < ((int64_t)1 << 22) ? n : ((int64_t)1 << 22);
     f.ctab = c.take<uint64_t>(f.ctab_cap);
@@ -712,7 +791,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 // ---------------------------------------------------------------------------
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st, bool offsets_later) {
+              int32_t* status, hipStream_t st, bool offsets_later, bool exact_flow_levels) {
   // flows (packed sort) only when the sort runs its multi-block passes
   FlowBufs fl;
   if (n > SORT_SMALL_MAX) fl = b.fl;
@@ -723,6 +802,22 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   for (int m = flo; fan && m <= fhi; ++m)
     if (rg.shift < 64 && g.shift[m] == rg.shift) fq = m - flo;
   fl.child_ok = (fl.hcap && fq >= 0 && fl.cmask != 0u) ? 1 : 0;
+  // count levels that are functions of the flow (the route level and the ones
+  // above it, at most FLOW_EXACT_LEVELS of them) are checked exactly per flow;
+  // with exact_flow_levels they also leave the fingerprint
+  int xhi = 0, xlo = 1;
+  if (fl.hcap && fan && fhi >= flo && rg.shift < 64) {
+    int lr = 0;   // the route level
+    for (int m = 1; m <= g.depth; ++m)
+      if (g.shift[m] == rg.shift) lr = m;
+    xhi = lr < fhi ? lr : fhi;
+    xlo = xhi - FLOW_EXACT_LEVELS + 1 > flo ? xhi - FLOW_EXACT_LEVELS + 1 : flo;
+    if (xhi < flo) { xhi = 0; xlo = 1; }
+    fl.x_route = (xhi == lr) ? 1 : 0;
+  }
+  const int nx = xhi >= xlo ? xhi - xlo + 1 : 0;
+  b.fx_lo = exact_flow_levels ? xlo : 1;
+  b.fx_hi = exact_flow_levels ? xhi : 0;
   {
     ProfScope ps(PH_PREP, st);
     const int64_t cb = fl.hcap > 0 ? cdiv(fl.hcap, 256) : 1;
@@ -731,7 +826,8 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
     const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
 #define ALTO_PREP_CASE(NLV)                                                                                   \
   case NLV:                                                                                                   \
-    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part, fq); \
+    k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part, xlo - flo, nx, \
+                                          exact_flow_levels ? 1 : 0);                                          \
     break;
     switch (nl) {
       ALTO_PREP_CASE(0) ALTO_PREP_CASE(1) ALTO_PREP_CASE(2) ALTO_PREP_CASE(3) ALTO_PREP_CASE(4)
@@ -741,6 +837,8 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
     }
 #undef ALTO_PREP_CASE
     k_prep_fold<<<1, 256, 0, st>>>(b.prep_part, grid, flo, nl, b.ctl, b.fp_in, status);
+    if (exact_flow_levels && nx > 0)
+      k_prep_fp<<<grid_for(n, 256 * 8, 2048), 256, 0, st>>>(keys, n, g, fan, fan_ld, xlo, xhi, b.ctl, b.fp_in);
     ALTO_LAUNCH_CHECK();
   }
   ProfScope ps_sort(PH_SORT, st);
@@ -777,7 +875,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   int Lt, Lseg;
   agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
   ProfScope ps_total(PH_TOTAL, st);
-  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st, true);
+  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st, true, true);
   if (rc) return rc;
   const uint32_t* perm = b.perm_used;
   prof_begin(PH_SEGMENT, st);
@@ -861,7 +959,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     Mp = b.nnodes + Lm;
     k_mask_out<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lm], Mp, b.sk, g.shift[Lm], out.mask_key, out.mask, out.cap_mask);
   }
-  k_fp_compare<<<1, 1, 0, st>>>(b.fp_in, b.fp_nodes, Lt, d - 1, status);
+  k_fp_compare<<<1, 1, 0, st>>>(b.fp_in, b.fp_nodes, Lt, d - 1, b.fx_lo, b.fx_hi, b.ctl, status);
   prof_end(PH_SEGMENT, st);
 
   // groups
@@ -965,5 +1063,5 @@ void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st) {
 
 void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,
                        hipStream_t st) {
-  k_fp_compare<<<1, 1, 0, st>>>(fp_in, fp_nodes, flo, fhi, status);
+  k_fp_compare<<<1, 1, 0, st>>>(fp_in, fp_nodes, flo, fhi, 1, 0, nullptr, status);
 }

@@ -4,7 +4,7 @@
 #include "alto_internal.h"
 
 #define SEG_NT 512
-#define SEG_IT 16                      // consecutive elements per thread
+#define SEG_IT 32                      // consecutive elements per thread (fewer, larger tiles: fewer look-back rounds)
 #define SEG_TILE (SEG_NT * SEG_IT)
 #define SEG_LB_STRIDE ALTO_MAX_LEVELS  // look-back words per tile (one per level)
 #define NODE_GRID 512

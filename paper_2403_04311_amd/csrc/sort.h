@@ -16,6 +16,7 @@
 #define SORT_SMALL_MAX 8192
 #define FLOW_CAP 8192          // flows sort in one workgroup (<= SORT_SMALL_MAX)
 #define FLOW_DIRECT_BITS 12   // flow prefixes varying within this many bits: direct rank table
+#define FLOW_EXACT_LEVELS 3   // count levels up to the route level checked exactly per flow
 
 enum { SORT_BUF_INPUT = 0, SORT_BUF_TMP = 1, SORT_BUF_FINAL = 2 };
 enum { SORT_GENERAL = 0, SORT_PACKED = 1 };
@@ -62,7 +63,9 @@ struct FlowBufs {
   uint32_t* fdest;       // [fcap] destination of each ranked flow
   // child ranks: a flow's children (the nodes one level below the route level) are
   // numbered consecutively from fbase[rank], using the flow's declared child count
-  uint32_t* ht_fan;      // [hcap] declared child count of the flow in the slot (a carrier's)
+  uint32_t* ht_fan;      // [hcap] declared child count of the flow in the slot (the first carrier's; 0 = unset)
+  uint32_t* ht_anc;      // [FLOW_EXACT_LEVELS][hcap] counts of the other exactly checked levels (0 = unset)
+  int32_t x_route;       // the last exactly checked level is the route level (its counts are in ht_fan)
   uint32_t* fbase;       // [fcap + 1] first child rank of each ranked flow
   uint64_t* ctab;        // [ctab_cap] child rank -> key bits above the child level's suffix
   int64_t ctab_cap;

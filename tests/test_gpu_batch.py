@@ -235,3 +235,69 @@ def test_determinism_and_permutation_invariance_of_means():
     c = U.run_aggregate(keys2, fan2, bits, 3, "mean", 64, 0, 2, 9, p322, np.ascontiguousarray(pft2.T))
     assert np.array_equal(a["mean"], c["mean"])          # sums follow key order, not arrival
     assert np.array_equal(a["key"], c["key"])
+
+
+def _flow_case():
+    bits = (6, 3, 2, 3, 8)
+    path, fan, p32, _ = _case(61, 5, bits, (4, 3, 5, 60), 40)
+    keys = O.pack_keys(path, bits)
+    assert len(keys) > 8192           # multi-workgroup sort: the input pass keeps a flow set
+    return bits, keys, fan, p32
+
+
+def _carriers(keys, bits, level, min_count=2):
+    """Fragments of the first level-`level` node that has at least min_count of them."""
+    pre = O.prefix(keys, bits, level)
+    vals, counts = np.unique(pre, return_counts=True)
+    v = vals[np.argmax(counts >= min_count)]
+    return np.nonzero(pre == v)[0]
+
+
+@pytest.mark.parametrize("kind", ["valid", "route_level", "above_same_flow", "above_across_flows"])
+def test_flow_level_count_checks(kind):
+    """Declared counts of the route level and the levels above it are compared per
+    flow in the input pass; disagreements between flows are caught on the node
+    records. Route level 3, mean at level 4, mask at level 2 (levels 2..4 read)."""
+    bits, keys, fan, p32 = _flow_case()
+    La, Lm, Lr, D = 4, 2, 3, 64
+    fan = fan.copy()
+    if kind == "route_level":
+        c = _carriers(keys, bits, 3)
+        fan[2, c[-1]] += 1                       # one carrier of a level-3 node
+    elif kind == "above_same_flow":
+        c = _carriers(keys, bits, 3)
+        fan[1, c[0]] += 1                        # its level-2 count, one carrier
+    elif kind == "above_across_flows":
+        pre2 = O.prefix(keys, bits, 2)
+        pre3 = O.prefix(keys, bits, 3)
+        # a level-2 node with several level-3 children: change all carriers of one child
+        v2 = next(v for v in np.unique(pre2) if len(np.unique(pre3[pre2 == v])) > 1)
+        child = np.unique(pre3[pre2 == v2])[1]
+        fan[1, pre3 == child] += 1
+    code, rt, g = U.oracle_aggregate(keys, fan, bits, La, "concat", 1, Lm, Lr, D, p32)
+    assert code == (O.OK if kind == "valid" else O.E_FANOUT)
+    res = U.run_aggregate(keys, fan, bits, La, "concat", 1, Lm, Lr, D, p32)
+    assert res["status"] == code, (kind, res["status"], code)
+    if kind == "valid":
+        U.compare(res, rt, g, "concat", Lm, La)
+
+
+@pytest.mark.parametrize("bad", [False, True])
+def test_flow_set_overflow_count_check(bad):
+    """More route prefixes than the flow set holds, with the route level's counts
+    read: the per-flow check is incomplete, so those counts join the fingerprint."""
+    bits = (17, 2, 2, 3)
+    path, fan, p32, _ = _case(322, 4, bits, (2, 2, 3), 40000)
+    keys = O.pack_keys(path, bits)
+    assert len(np.unique(O.prefix(keys, bits, 1))) > 32768
+    La, Lm, Lr, D = 1, 0, 1, 1000
+    if bad:
+        fan = fan.copy()
+        c = _carriers(keys, bits, 1)
+        fan[0, c[-1]] += 1
+    code, rt, g = U.oracle_aggregate(keys, fan, bits, La, "concat", 1, Lm, Lr, D, p32)
+    assert code == (O.E_FANOUT if bad else O.OK)
+    res = U.run_aggregate(keys, fan, bits, La, "concat", 1, Lm, Lr, D, p32)
+    assert res["status"] == code
+    if not bad:
+        U.compare(res, rt, g, "concat", Lm, La)
