@@ -382,6 +382,7 @@ __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_
   __shared__ int64_t s_w[GS_NT / ALTO_WAVE];
   __shared__ int64_t s_ex[4];
   __shared__ uint32_t s_tile;
+  if ((int64_t)blockIdx.x >= ntiles) return;   // no tile would be left for this block
   while (true) {
     if (threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
     __syncthreads();
@@ -525,6 +526,7 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
   const int rpw = ALTO_WAVE / lpr, sub = lane / lpr, cl = lane % lpr;
   const int64_t NC = *nchunks;
   __shared__ int64_t s_c;
+  if ((int64_t)blockIdx.x >= NC) return;   // fewer chunks than blocks: no ticket contention
   // chunks are taken by ticket: groups have very different sizes, and a block that
   // finishes early takes the next chunk (the sum of a chunk does not depend on
   // which block computes it)

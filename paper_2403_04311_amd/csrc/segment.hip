@@ -72,6 +72,9 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
   for (int q = 0; q < KM; ++q) es[q] = q < K ? es_of(g, j, lo + q) : 64;
   const int lane = lane_id();
   const bool vec_ok = (reinterpret_cast<uintptr_t>(j.keys) & 15) == 0;
+  // blocks past the tile count would only contend for tickets (the grid is sized
+  // for the largest count, the count may be known on the device only)
+  if ((int64_t)blockIdx.x >= ntiles) return;
   while (true) {
     if (threadIdx.x == 0) s_tile = atomicAdd(j.lb_ctr, 1u);
     __syncthreads();

@@ -612,6 +612,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
   if (!c.ps.active || (c.mode == SORT_PACKED) != PACKED) return;
   const int64_t n = load_n(n_host, n_dev);
   const int64_t ntiles = cdiv(n, OS_TILE);
+  if ((int64_t)blockIdx.x >= ntiles) return;   // the grid covers the largest count; no tile for this block
   constexpr bool packed = PACKED;
   const bool last = PACKED ? LAST : (slot + 1 == c.first + c.npass);
   const int sh = c.ib + c.ps.lo;

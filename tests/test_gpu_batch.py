@@ -37,6 +37,9 @@ CASES = [
     # mask above the route level with more than one workgroup's worth of fragments
     (5, (6, 3, 2, 3, 8), (4, 3, 5, 60), 20, 4, 2, 3, 64, 0.02, 8),
     (6, (3, 12, 12, 12, 12, 12), (3, 4, 30, 60, 40), 2, 4, 2, 4, 256, 0.0, 128),
+    # groups are the flows (mean gathered beside segmentation), incomplete groups and
+    # a mask above them
+    (5, (6, 3, 2, 3, 8), (4, 3, 5, 60), 40, 3, 1, 3, 64, 0.03, 16),
 ]
 
 
