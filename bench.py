@@ -9,6 +9,12 @@ one alto_aggregate call over the whole batch (routing outputs perm, dest_offsets
 dest, plus groups, means and mask). Inputs are resident in HBM before timing.
 
 Prints one JSON line. --gpus N > 1 is refused: this build runs on one GPU.
+
+--workload picks another of the synthetic workloads (one JSON line each, "all" for
+every one): tiny (64-query depth-4 tree, token concat), factool (1,024-query
+FacTool-shaped batch, 768-d mean per document then document-id concat per claim),
+tokens (256-generator token stream in 4,096-fragment steps), factool_stream
+(10,000 steps of 4,096 fragments, both stages per step, per-step latency).
 """
 import argparse
 import json
@@ -116,6 +122,246 @@ def cpu_baseline(leaves_log2: int):
                       f"workload): pack + route + aggregate, {dt:.1f} s single-threaded numpy"}
 
 
+
+def _timed(fn, steps, warmup):
+    """Runs fn warmup + steps times; returns ms per call of the timed calls
+    (HIP events on the current stream around all of them)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def _line(workload, n, ms, steps, warmup, path_bytes, extra=None):
+    res = {
+        "metric": "fragments/sec routed+aggregated at 1 MI355X; achieved HBM GB/s vs peak",
+        "value": n / (ms * 1e-3), "unit": "fragments/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
+        "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic", "config": {"workload": workload, "fragments": n},
+        "path_roofline": {"algorithmic_bytes_per_step": path_bytes, "achieved": path_bytes / (ms * 1e-3) / 1e9,
+                          "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                          "frac": path_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS},
+    }
+    if extra:
+        res.update(extra)
+    return res
+
+
+def bench_tiny(args):
+    """64-query depth-4 tree: one alto_aggregate (route by query to 8 destinations,
+    token concat per sentence); launch-latency bound."""
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+    w = W.config1("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n = w.n
+    ws = alto.new_workspace(alto.workspace_bytes(w.bits, n, w.num_dest, w.agg_level, "concat"))
+    perm = torch.empty(n, dtype=torch.int32, device="cuda")
+    offs = torch.empty(w.num_dest + 1, dtype=torch.int64, device="cuda")
+    dest = torch.empty(n, dtype=torch.int32, device="cuda")
+    out = alto.new_groups(n, w.agg_level, "concat", cap_tokens=n)
+    status = alto.new_status()
+
+    def step():
+        alto.aggregate(keys, w.fan, w.bits, w.agg_level, "concat", 1, 0, w.route_level, w.num_dest,
+                       w.payload_i32, None, ws=ws, perm=perm, dest_offsets=offs, dest=dest, out=out,
+                       status=status, n=n)
+    ms = _timed(step, args.steps * 20, args.warmup)
+    assert int(status.item()) == 0
+    E = int(out.counts[0])
+    nl = w.depth - 1 - w.agg_level + 1
+    path_bytes = n * (8 + 4 * nl + 4 + 4 + 4 + 4) + E * (8 + 4 + 8 + 4 * (w.agg_level - 1) + 8)
+    return _line("64-query depth-4 tree (query/doc/sentence/token), token concat per sentence, 8 destinations "
+                 "by query, one batch", n, ms, args.steps * 20, args.warmup, path_bytes,
+                 {"groups": E, "us_per_call": ms * 1e3})
+
+
+def bench_factool(args):
+    """FacTool-shaped batch, both stages per step: 768-d mean per document (route by
+    claim to 32 destinations), then concat of the documents' corpus ids per claim
+    over the first stage's records."""
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+    w = W.config2("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n, dim = w.n, w.dim
+    sb = W.CONFIG2_STAGE_B
+    ws = alto.new_workspace(alto.workspace_bytes(w.bits, n, 32, 4, "mean", dim))
+    perm = torch.empty(n, dtype=torch.int32, device="cuda")
+    offs = torch.empty(33, dtype=torch.int64, device="cuda")
+    dest = torch.empty(n, dtype=torch.int32, device="cuda")
+    gA = alto.new_groups(n // 4 + 1024, 4, "mean", dim)
+    stA, stB = alto.new_status(), alto.new_status()
+    alto.aggregate(keys, w.fan, w.bits, 4, "mean", dim, 0, 2, 32, w.payload_i32, w.payload_f32, ws=ws,
+                   perm=perm, dest_offsets=offs, dest=dest, out=gA, status=stA, n=n)
+    torch.cuda.synchronize()
+    E = int(gA.counts[0])
+    assert int(stA.item()) == 0 and E > 0
+    wsB = alto.new_workspace(alto.workspace_bytes(sb["bits"], E, 32, 2, "concat"))
+    permB = torch.empty(E, dtype=torch.int32, device="cuda")
+    destB = torch.empty(E, dtype=torch.int32, device="cuda")
+    gB = alto.new_groups(E, 2, "concat", cap_tokens=E)
+    fanB = gA.fan_up.view(3, -1)[:, :E]
+    prof = {}
+
+    def step():
+        alto.aggregate(keys, w.fan, w.bits, 4, "mean", dim, 0, 2, 32, w.payload_i32, w.payload_f32, ws=ws,
+                       perm=perm, dest_offsets=offs, dest=dest, out=gA, status=stA, n=n)
+        alto.aggregate(gA.key, fanB, sb["bits"], 2, "concat", 1, 0, 2, 32, gA.first_i32, None, ws=wsB,
+                       perm=permB, dest_offsets=offs, dest=destB, out=gB, status=stB, n=E)
+    lib = alto.load()
+    import ctypes as C
+    lib.alto_profile_begin.argtypes = [C.c_int32]
+    lib.alto_profile_end.argtypes = [C.POINTER(C.c_float), C.POINTER(C.c_int32), C.c_int32]
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert lib.alto_profile_begin(32 * args.steps + 32) == 0
+    ms = _timed(step, args.steps, 0)
+    msp = (C.c_float * len(PHASES))()
+    calls = (C.c_int32 * len(PHASES))()
+    assert lib.alto_profile_end(msp, calls, len(PHASES)) == 0
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    C2 = int(gB.counts[0])
+    # mean gather of stage A: one launch per step (stage B has no mean)
+    mean_ms = msp[PHASES.index("mean_kernel")] / max(calls[PHASES.index("mean_kernel")], 1)
+    kern_bytes = (n + E) * dim * 4
+    path_bytes = (n * (8 + 4 + 4 + 4 * dim + 4 + 4) + E * (8 + 4 + 8 + 4 + 12 + 4 * dim)
+                  + E * (8 + 8 + 4 + 4 + 4 + 4) + C2 * (8 + 4 + 8 + 4 + 8))
+    return _line("FacTool-shaped batch: 1,024 queries, depth 5, 768-d mean per document (route by claim to 32 "
+                 "destinations), then document-id concat per claim", n, ms, args.steps, args.warmup, path_bytes,
+                 {"documents": E, "claims": C2,
+                  "roofline": {"bound": "hbm", "kernel": "k_mean (first stage)", "achieved":
+                               kern_bytes / (mean_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                               "frac": kern_bytes / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                               "algorithmic_bytes_per_launch": kern_bytes, "avg_launch_ms": mean_ms}})
+
+
+def _stream_run(steps, step_of):
+    """Runs every step of a stream (stage callables per step); returns total ms
+    (events around all steps) and per-step device ms (events per step)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for s in range(steps):
+        step_of(s)
+        ev[s + 1].record()
+    torch.cuda.synchronize()
+    per = [ev[s].elapsed_time(ev[s + 1]) for s in range(steps)]
+    return ev[0].elapsed_time(ev[steps]), per
+
+
+def _pct(xs, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(xs), q))
+
+
+def bench_tokens(args):
+    """Token stream: 256 generators, round-robin arrival, 4,096-fragment steps,
+    sentences carried across steps and emitted when their last token arrives."""
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+    w = W.config3("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n, step = w.n, w.step
+    nsteps = (n + step - 1) // step
+    out = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
+    status = alto.new_status()
+
+    def run():
+        s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step)
+
+        def one(i):
+            a, b = i * step, min(n, (i + 1) * step)
+            s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status)
+        tot, per = _stream_run(nsteps, one)
+        s.close()
+        return tot, per
+    for _ in range(max(args.warmup, 1)):
+        run()
+    tot, per = run()
+    assert int(status.item()) == 0
+    ms = tot / nsteps
+    path_bytes = (n * (8 + 4 + 4 + 4 + 4 + 4) + 16384 * (8 + 4 + 8 + 4 + 8)) / nsteps
+    return _line(f"token stream: 256 generators x 64 sentences, geometric(1/24) tokens, round-robin, "
+                 f"{step}-fragment steps, concat per sentence, 64 destinations", n / nsteps, ms, nsteps, 1,
+                 path_bytes, {"stream_fragments": n, "stream_ms": tot,
+                              "step_ms_p50": _pct(per, 50), "step_ms_p99": _pct(per, 99),
+                              "step_ms_max": max(per)})
+
+
+def bench_factool_stream(args):
+    """FacTool-shaped windowed stream, 10,000 steps of 4,096 fragments; per step the
+    document stage (768-d mean) and the claim stage over its emitted records (the
+    emitted count is read back each step: the second stage's size)."""
+    import time as T
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+    w = W.config4("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    step, steps = w.step, w.info["steps"]
+    ring, ring_rows = w.payload_f32, w.payload_f32.shape[0]
+    sbB = W.CONFIG2_STAGE_B
+    gA = alto.new_groups(step, 4, "mean", 768)
+    gB = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
+    stA, stB = alto.new_status(), alto.new_status()
+
+    def run(nsteps):
+        sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22,
+                         step_max=step)
+        sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
+                         step_max=step)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(nsteps)]
+        wall = []
+        emitted = [0, 0]
+        torch.cuda.synchronize()
+        t_all = T.perf_counter()
+        for s in range(nsteps):
+            t0 = T.perf_counter()
+            a, b = s * step, (s + 1) * step
+            r0 = (s * step) % ring_rows
+            evs[s][0].record()
+            sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gA, status=stA)
+            E = int(gA.counts[0])          # synchronizes: the second stage's size
+            sB.step(gA.key[:E], gA.fan_up.view(3, -1)[:, :E], gA.first_i32[:E], None, out=gB, status=stB, n=E)
+            evs[s][1].record()
+            emitted[0] += E
+            wall.append((T.perf_counter() - t0) * 1e3)
+        torch.cuda.synchronize()
+        total = (T.perf_counter() - t_all) * 1e3
+        dev = [a.elapsed_time(b) for a, b in evs]
+        sA.close()
+        sB.close()
+        return total, wall, dev, emitted[0]
+    run(max(args.warmup, 1) * 50)
+    total, wall, dev, E = run(steps)
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    n = steps * step
+    # inputs read once (key, 3 count columns, doc id, 768-d row), perm/dest, emitted document
+    # records and their means; the carried partial state is not counted
+    path_bytes = (n * (8 + 12 + 4 + 3072 + 8) + E * (8 + 4 + 8 + 4 + 12 + 3072)) / steps
+    ms = total / steps
+    return _line(f"FacTool-shaped windowed stream: {steps} steps x {step} fragments, 768-d mean per document "
+                 "then document-id concat per claim (both stages each step, emitted count read back per step)",
+                 step, ms, steps, 50, path_bytes,
+                 {"stream_fragments": n, "documents_emitted": E, "window_fragments": w.info["window"],
+                  "long_lived_fraction": w.info["calibrated_frac"],
+                  "step_ms_p50": _pct(wall, 50), "step_ms_p99": _pct(wall, 99), "step_ms_max": max(wall),
+                  "device_step_ms_p50": _pct(dev, 50), "device_step_ms_p99": _pct(dev, 99)})
+
+
+WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_tokens,
+             "factool_stream": bench_factool_stream}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -131,6 +377,8 @@ def main():
                     help="write the mean kernel's HBM traffic summary from two rocprofv3 --pmc "
                          "counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--pmc-command", default="", help="the rocprofv3 commands, recorded in the summary")
+    ap.add_argument("--workload", default="zipf64M", choices=["zipf64M", "all"] + sorted(WORKLOADS),
+                    help="zipf64M (default): the 2^26-fragment Zipf batch")
     args = ap.parse_args()
     if args.derive_traffic:
         out = write_traffic_summary(args.derive_traffic[0], args.derive_traffic[1],
@@ -140,6 +388,14 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
+
+    if args.workload != "zipf64M":
+        names = sorted(WORKLOADS) if args.workload == "all" else [args.workload]
+        for name in names:
+            log(f"workload {name}")
+            print(json.dumps(WORKLOADS[name](args)), flush=True)
+        if args.workload != "all":
+            return
 
     import ctypes as C
     import numpy as np
