@@ -545,19 +545,24 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
       for (int q = 0; q < CPL; ++q)
 #pragma unroll
         for (int v = 0; v < VEC; ++v) acc[q][v] = 0.0;
-      // each wave takes batches of 64 consecutive rows: the 64 row indices are read
-      // with one coalesced load and passed to the lanes that load the rows, so the
-      // payload loads do not wait on per-row index loads
-      for (int b0 = w * ALTO_WAVE; b0 < ch.len; b0 += NW * ALTO_WAVE) {
-        const int nr = ch.len - b0 < ALTO_WAVE ? ch.len - b0 : ALTO_WAVE;
-        const int32_t myrow = lane < nr ? (int32_t)srcp.row(ch.begin + b0 + lane) : 0;
-        for (int it0 = 0; it0 < lpr; it0 += U) {   // lpr steps of rpw rows cover the batch
+      // the block takes batches of NW x 64 rows; in a batch, step `it` loads rows
+      // b0 + (it x NW + w) x rpw + sub (rpw rows per wave and step, the waves
+      // interleaved, so that a short chunk still spreads over every wave). Each wave
+      // first reads the row indices of its 64 rows with one load and passes them to
+      // the lanes that load the rows, so the payload loads do not wait on index loads.
+      for (int b0 = 0; b0 < ch.len; b0 += NW * ALTO_WAVE) {
+        const int mine = b0 + ((lane / rpw) * NW + w) * rpw + lane % rpw;   // row of index slot `lane`
+        const int32_t myrow = mine < ch.len ? (int32_t)srcp.row(ch.begin + mine) : 0;
+        // steps holding a row of this wave: b0 + (it x NW + w) x rpw < len
+        const int left = ch.len - b0 - w * rpw;
+        const int steps = left <= 0 ? 0 : (int)cdiv(left, NW * rpw) < lpr ? (int)cdiv(left, NW * rpw) : lpr;
+        for (int it0 = 0; it0 < steps; it0 += U) {
           float x[U][CPL][VEC];
 #pragma unroll
           for (int u = 0; u < U; ++u) {
-            const int r = (it0 + u) * rpw + sub;
+            const int r = (it0 + u) * rpw + sub;   // index slot
             const int32_t rr = __shfl(myrow, r & (ALTO_WAVE - 1));
-            const bool ok = (it0 + u < lpr) && r < nr;
+            const bool ok = (it0 + u < steps) && b0 + ((it0 + u) * NW + w) * rpw + sub < ch.len;
             const float* src = srcp.pay_of(ok ? rr : row_safe);
 #pragma unroll
             for (int q = 0; q < CPL; ++q) {
