@@ -465,33 +465,29 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
   }
 }
 
-// One chunk descriptor per thread: the group is found by binary search over the
-// scanned chunk counts.
+// Chunk descriptors: one thread per group writes the group's chunks (their first
+// index comes from the scanned chunk counts).
 __global__ __launch_bounds__(256) void k_chunks(LevelNodes L, const int64_t* Gp, const int32_t* em, const int64_t* tokb,
                                                 const int64_t* chb, const int64_t* pb, Chunk* chunks, int chunk_rows) {
   const int64_t G = *Gp;
-  const int64_t C = chb[G];
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < C; c += (int64_t)gridDim.x * blockDim.x) {
-    int64_t lo = 0, hi = G - 1;   // last u with chb[u] <= c
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (chb[mid] <= c) lo = mid; else hi = mid - 1;
-    }
-    const int64_t u = lo;
-    const int64_t k = c - chb[u];
-    const int64_t nc = chb[u + 1] - chb[u];
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t c0 = chb[u], nc = chb[u + 1] - c0;
+    if (nc <= 0) continue;   // an incomplete group has no chunk
     const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
-    Chunk ch;
-    ch.e = em[u];
-    ch.begin = s + (int32_t)(k * chunk_rows);
-    ch.len = (int32_t)((cnt - k * chunk_rows) < chunk_rows ? (cnt - k * chunk_rows) : chunk_rows);
-    ch.k = (int32_t)k;
-    ch.nch = (int32_t)nc;
-    ch.count = cnt;
-    ch.part = nc > 1 ? pb[u] : -1;
-    ch.out = tokb[u] + k * chunk_rows;
-    ch.pad = 0;
-    chunks[c] = ch;
+    const int64_t e = em[u], part = nc > 1 ? pb[u] : -1, out = tokb[u];
+    for (int64_t k = 0; k < nc; ++k) {
+      Chunk ch;
+      ch.e = e;
+      ch.begin = s + (int32_t)(k * chunk_rows);
+      ch.len = (int32_t)((cnt - k * chunk_rows) < chunk_rows ? (cnt - k * chunk_rows) : chunk_rows);
+      ch.k = (int32_t)k;
+      ch.nch = (int32_t)nc;
+      ch.count = cnt;
+      ch.part = part;
+      ch.out = out + k * chunk_rows;
+      ch.pad = 0;
+      chunks[c0 + k] = ch;
+    }
   }
 }
 
@@ -994,8 +990,7 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
                                                                   MEAN_CHUNK_ROWS, gst, gctr, status);
   }
   k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, out);
-  k_chunks<<<grid_for(n / MEAN_CHUNK_ROWS + 1, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.chunks,
-                                                                 MEAN_CHUNK_ROWS);
+  k_chunks<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.chunks, MEAN_CHUNK_ROWS);
   k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, Mp, out.counts, out.tok_off,
                             out, b.scal, status);
   ALTO_LAUNCH_CHECK();
