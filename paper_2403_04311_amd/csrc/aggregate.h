@@ -5,6 +5,7 @@
 #include "sort.h"
 
 #define MEAN_CHUNK_ROWS 4096
+#define MEAN_SMALL_ROWS 256    // groups of at most this many rows: one chunk, gathered by one wave
 
 // One unit of gather work: rows [begin, begin+len) of the sorted fragments, the
 // k-th of nch chunks of emitted group e.
@@ -102,7 +103,7 @@ struct AggBufs {
   uint64_t* fp_in;
   uint64_t* fp_nodes;
   int64_t* nnodes;
-  int64_t* scal;        // [8] device scalars: 0 = G+1, 1 = chunk count
+  int64_t* scal;        // [8] device scalars: 1 = chunk count, 2 = block ticket, 3 = chunks of long groups
   uint64_t* tmp_keys;
   uint32_t* tmp_vals;
   uint64_t* sk;
@@ -119,6 +120,7 @@ struct AggBufs {
   int64_t* tokc;
   int64_t* nch;
   int64_t* pch;
+  int64_t* nsm;         // scanned count of small groups (one wave-gathered chunk each)
   Chunk* chunks;
   double* part;
 };

@@ -367,20 +367,22 @@ constexpr int GS_NT = 256;
 constexpr int GS_IT = 16;
 constexpr int GS_TILE = GS_NT * GS_IT;
 
+constexpr int GS_NV = 5;   // scanned values per group
+
 __global__ void k_group_scan_prep(const int64_t* Gp, uint64_t* st, uint32_t* ctr) {
-  const int64_t len = cdiv(*Gp + 1, GS_TILE) * 4;
+  const int64_t len = cdiv(*Gp + 1, GS_TILE) * GS_NV;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
     st[i] = 0;
   if (blockIdx.x == 0 && threadIdx.x == 0) *ctr = 0;
 }
 
 __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_t* Gp, int32_t* em, int64_t* tokc,
-                                                     int64_t* nch, int64_t* pch, int chunk_rows, uint64_t* st,
-                                                     uint32_t* ctr, int32_t* status) {
+                                                     int64_t* nch, int64_t* pch, int64_t* nsm, int chunk_rows,
+                                                     uint64_t* st, uint32_t* ctr, int32_t* status) {
   const int64_t G = *Gp;
   const int64_t ntiles = cdiv(G + 1, GS_TILE);
   __shared__ int64_t s_w[GS_NT / ALTO_WAVE];
-  __shared__ int64_t s_ex[4];
+  __shared__ int64_t s_ex[GS_NV];
   __shared__ uint32_t s_tile;
   if ((int64_t)blockIdx.x >= ntiles) return;   // no tile would be left for this block
   while (true) {
@@ -389,34 +391,39 @@ __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_
     const int64_t tile = (int64_t)s_tile;
     if (tile >= ntiles) break;   // uniform
     const int64_t u0 = tile * GS_TILE + (int64_t)threadIdx.x * GS_IT;
-    int64_t v[GS_IT][4];
-    int64_t sum[4] = {0, 0, 0, 0};
+    int64_t v[GS_IT][GS_NV];
+    int64_t sum[GS_NV] = {0, 0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < GS_IT; ++i) {
       const int64_t u = u0 + i;
       const bool ok = u < G && L.ok[u];
       const int64_t cnt = ok ? (int64_t)L.start[u + 1] - L.start[u] : 0;
-      const int64_t c = ok ? cdiv(cnt, chunk_rows) : 0;
+      const bool small = ok && cnt <= MEAN_SMALL_ROWS;
+      const int64_t c = ok && !small ? cdiv(cnt, chunk_rows) : 0;
       v[i][0] = ok ? 1 : 0;
       v[i][1] = cnt;
       v[i][2] = c;
       v[i][3] = c > 1 ? c : 0;
+      v[i][4] = small ? 1 : 0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) sum[q] += v[i][q];
+      for (int q = 0; q < GS_NV; ++q) sum[q] += v[i][q];
     }
-    int64_t ex[4], tot[4];
+    int64_t ex[GS_NV], tot[GS_NV];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) ex[q] = block_excl_scan<int64_t, GS_NT>(sum[q], s_w, &tot[q]);
-    if (threadIdx.x < 4) {
+    for (int q = 0; q < GS_NV; ++q) ex[q] = block_excl_scan<int64_t, GS_NT>(sum[q], s_w, &tot[q]);
+    if (threadIdx.x < GS_NV) {
       const int q = threadIdx.x;
-      const int64_t t = q == 0 ? tot[0] : q == 1 ? tot[1] : q == 2 ? tot[2] : tot[3];
-      lb64_publish(st + q, tile, 4, (uint64_t)t);
-      s_ex[q] = (int64_t)lb64_resolve(st + q, tile, 4, (uint64_t)t, status);
+      int64_t t = tot[0];
+#pragma unroll
+      for (int qq = 1; qq < GS_NV; ++qq)
+        if (q == qq) t = tot[qq];
+      lb64_publish(st + q, tile, GS_NV, (uint64_t)t);
+      s_ex[q] = (int64_t)lb64_resolve(st + q, tile, GS_NV, (uint64_t)t, status);
     }
     __syncthreads();
-    int64_t run[4];
+    int64_t run[GS_NV];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) run[q] = s_ex[q] + ex[q];
+    for (int q = 0; q < GS_NV; ++q) run[q] = s_ex[q] + ex[q];
 #pragma unroll
     for (int i = 0; i < GS_IT; ++i) {
       const int64_t u = u0 + i;
@@ -425,9 +432,10 @@ __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_
         tokc[u] = run[1];
         nch[u] = run[2];
         pch[u] = run[3];
+        nsm[u] = run[4];
       }
 #pragma unroll
-      for (int q = 0; q < 4; ++q) run[q] += v[i][q];
+      for (int q = 0; q < GS_NV; ++q) run[q] += v[i][q];
     }
     __syncthreads();   // s_ex and the ticket are reused by the next tile
   }
@@ -465,13 +473,17 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
   }
 }
 
-// Chunk descriptors: one thread per group writes the group's chunks (their first
-// index comes from the scanned chunk counts).
+// Chunk descriptors: one thread per group writes the group's chunks. Groups of more
+// than MEAN_SMALL_ROWS rows are cut into chunks of chunk_rows (their first index
+// from the scanned chunk counts); each shorter group is one chunk after those.
 __global__ __launch_bounds__(256) void k_chunks(LevelNodes L, const int64_t* Gp, const int32_t* em, const int64_t* tokb,
-                                                const int64_t* chb, const int64_t* pb, Chunk* chunks, int chunk_rows) {
+                                                const int64_t* chb, const int64_t* pb, const int64_t* smb, Chunk* chunks,
+                                                int chunk_rows) {
   const int64_t G = *Gp;
+  const int64_t NB = chb[G];   // chunks of the long groups come first, then one per short group
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t c0 = chb[u], nc = chb[u + 1] - c0;
+    const bool small = smb[u + 1] > smb[u];
+    const int64_t c0 = small ? NB + smb[u] : chb[u], nc = small ? 1 : chb[u + 1] - chb[u];
     if (nc <= 0) continue;   // an incomplete group has no chunk
     const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
     const int64_t e = em[u], part = nc > 1 ? pb[u] : -1, out = tokb[u];
@@ -510,27 +522,100 @@ __global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks
 // one chunk are finished here; the others leave a partial sum per chunk.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// One short group (a single chunk of at most MEAN_SMALL_ROWS rows) gathered by one
+// wave: rows in batches of 64 (one coalesced index load each), UW rows per lane in
+// flight, lanes holding the same columns combined in lane order; the mean is
+// written directly.
 template <int VEC, int CPL, typename Src>
-__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src srcp,
-                                              int dim, int lpr, double* part, float* mean, int64_t cap_groups,
-                                              unsigned long long* ticket) {
+__device__ inline void mean_short_chunk(const Chunk& ch, const Src& srcp, int dim, int C, int lpr, float* mean,
+                                        int64_t cap_groups) {
+  constexpr int UW = 4;
+  const int lane = lane_id();
+  const int rpw = ALTO_WAVE / lpr, sub = lane / lpr, cl = lane % lpr;
+  const int32_t row_safe = (int32_t)srcp.row(ch.begin);
+  for (int col0 = 0; col0 < C; col0 += lpr * CPL) {
+    double acc[CPL][VEC];
+#pragma unroll
+    for (int q = 0; q < CPL; ++q)
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) acc[q][v] = 0.0;
+    for (int b0 = 0; b0 < ch.len; b0 += ALTO_WAVE) {
+      const int nr = ch.len - b0 < ALTO_WAVE ? ch.len - b0 : ALTO_WAVE;
+      const int32_t myrow = lane < nr ? (int32_t)srcp.row(ch.begin + b0 + lane) : 0;
+      const int steps = (int)cdiv(nr, rpw);
+      for (int it0 = 0; it0 < steps; it0 += UW) {
+        float x[UW][CPL][VEC];
+#pragma unroll
+        for (int u = 0; u < UW; ++u) {
+          const int r = (it0 + u) * rpw + sub;
+          const int32_t rr = __shfl(myrow, r & (ALTO_WAVE - 1));
+          const bool ok = (it0 + u < steps) && r < nr;
+          const float* src = srcp.pay_of(ok ? rr : row_safe);
+#pragma unroll
+          for (int q = 0; q < CPL; ++q) {
+            const int col = col0 + cl + q * lpr;
+            const bool okc = ok && col < C;
+            const int colc = col < C ? col : C - 1;
+            if constexpr (VEC == 4) {
+              const f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(src + (int64_t)colc * 4));
+              x[u][q][0] = okc ? t[0] : 0.f;
+              x[u][q][1] = okc ? t[1] : 0.f;
+              x[u][q][2] = okc ? t[2] : 0.f;
+              x[u][q][3] = okc ? t[3] : 0.f;
+            } else {
+              const float t = __builtin_nontemporal_load(src + colc);
+              x[u][q][0] = okc ? t : 0.f;
+            }
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UW; ++u)
+#pragma unroll
+          for (int q = 0; q < CPL; ++q)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[q][v] += (double)x[u][q][v];
+      }
+    }
+    for (int o = lpr; o < ALTO_WAVE; o <<= 1)
+#pragma unroll
+      for (int q = 0; q < CPL; ++q)
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) acc[q][v] += __shfl_xor(acc[q][v], o);
+    if (sub == 0 && ch.e < cap_groups) {
+#pragma unroll
+      for (int q = 0; q < CPL; ++q) {
+        const int col = col0 + cl + q * lpr;
+        if (col >= C) continue;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+          mean[ch.e * (int64_t)dim + (int64_t)col * VEC + v] = (float)(acc[q][v] / (double)ch.count);
+      }
+    }
+  }
+}
+
+// Chunks [0, NB) belong to long groups and are gathered a block each (first phase);
+// chunks [NB, NC) are short groups, gathered a wave each (second phase).
+template <int VEC, int CPL, typename Src>
+__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks,
+                                              const int64_t* nblock, Src srcp, int dim, int lpr, double* part,
+                                              float* mean, int64_t cap_groups, unsigned long long* ticket) {
   constexpr int NW = 4;
   constexpr int U = 2;   // row loads in flight per lane (more lowers occupancy)
   __shared__ double red[NW][64 * CPL * VEC];
   const int C = dim / VEC;
   const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
   const int rpw = ALTO_WAVE / lpr, sub = lane / lpr, cl = lane % lpr;
-  const int64_t NC = *nchunks;
+  const int64_t NC = *nchunks, NB = *nblock;
   __shared__ int64_t s_c;
-  if ((int64_t)blockIdx.x >= NC) return;   // fewer chunks than blocks: no ticket contention
   // chunks are taken by ticket: groups have very different sizes, and a block that
   // finishes early takes the next chunk (the sum of a chunk does not depend on
-  // which block computes it)
-  while (true) {
+  // which block computes it). Blocks past the chunk count take none (no contention).
+  while ((int64_t)blockIdx.x < NB) {
     if (threadIdx.x == 0) s_c = (int64_t)atomicAdd(ticket, 1ull);
     __syncthreads();
     const int64_t c = s_c;
-    if (c >= NC) break;   // uniform
+    if (c >= NB) break;   // uniform
     const Chunk ch = chunks[c];
     // a row of the chunk that exists: lanes past the end load it and discard it, so
     // that no load sits behind a branch (which would wait for each load in turn)
@@ -618,6 +703,12 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
     }
     __syncthreads();   // s_c is rewritten by the next ticket
   }
+  // short groups: one wave each, assigned round robin (they have similar sizes, and
+  // tickets would serialise on one counter: one atomic per short group)
+  for (int64_t c = NB + (int64_t)blockIdx.x * NW + w; c < NC; c += (int64_t)gridDim.x * NW) {
+    const Chunk ch = chunks[c];
+    mean_short_chunk<VEC, CPL, Src>(ch, srcp, dim, C, lpr, mean, cap_groups);
+  }
 }
 
 // Sum of a group's chunk partials in chunk order. 256 threads = SUBS chunk subsets
@@ -669,12 +760,14 @@ __global__ void k_record_keys(LevelNodes L, const int64_t* Np, const uint64_t* _
     rkey[u] = key_prefix(sk[L.start[u]], shift);
 }
 
-__global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* tokc, const int64_t* nch, const int64_t* Mp,
+__global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* tokc, const int64_t* nch, const int64_t* nsm,
+                         const int64_t* Mp,
                          int64_t* counts, int64_t* tok_off, GroupOut out, int64_t* scal, int32_t* status) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   const int64_t G = *Gp;
-  scal[1] = nch[G];
-  scal[2] = 0;   // chunk tickets of the mean gather
+  scal[1] = nch[G] + nsm[G];   // chunks: those of long groups, then one per short group
+  scal[2] = 0;                 // block tickets of the mean gather (long groups)
+  scal[3] = nch[G];            // short groups: chunks scal[3] .. scal[1] - 1
   const int64_t E = em[G];
   const int64_t T = tokc ? tokc[G] : 0;
   const int64_t M = Mp ? *Mp : 0;
@@ -785,6 +878,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   b.tokc = c.take<int64_t>(n + 1);
   b.nch = c.take<int64_t>(n + 1);
   b.pch = c.take<int64_t>(n + 1);
+  b.nsm = c.take<int64_t>(n + 1);
   b.chunks = c.take<Chunk>(n / MEAN_CHUNK_ROWS + n + 1);
   if (agg->op == ALTO_MEAN_F32) b.part = c.take<double>((2 * cdiv(n, MEAN_CHUNK_ROWS) + 2) * (int64_t)agg->dim);
 }
@@ -983,15 +1077,15 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
     uint64_t* gst = reinterpret_cast<uint64_t*>(b.os_status);
     uint32_t* gctr = b.os_ctr;
     const int64_t tiles = cdiv(n + 1, GS_TILE);
-    if (tiles * 4 * 2 > (int64_t)b.os_ntiles * 2 * SORT_BUCKETS) return ALTO_E_ARG;   // never: words to spare
-    const int64_t pb = cdiv(tiles * 4, 256);
+    if (tiles * GS_NV * 2 > (int64_t)b.os_ntiles * 2 * SORT_BUCKETS) return ALTO_E_ARG;   // never: words to spare
+    const int64_t pb = cdiv(tiles * GS_NV, 256);
     k_group_scan_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(Gp, gst, gctr);
-    k_group_scan<<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch,
+    k_group_scan<<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.nsm,
                                                                   MEAN_CHUNK_ROWS, gst, gctr, status);
   }
   k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, out);
-  k_chunks<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.chunks, MEAN_CHUNK_ROWS);
-  k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, Mp, out.counts, out.tok_off,
+  k_chunks<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.nsm, b.chunks, MEAN_CHUNK_ROWS);
+  k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, b.nsm, Mp, out.counts, out.tok_off,
                             out, b.scal, status);
   ALTO_LAUNCH_CHECK();
   prof_end(PH_GROUPS, st);
@@ -1011,8 +1105,8 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
 #define ALTO_MEAN_CASE(V, P)                                                                                 \
   do {                                                                                                       \
     ProfScope ps_mean(PH_MEAN, st);                                                                          \
-    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NCp, src, dim, lpr, b.part, out.mean, out.cap_groups,  \
-                                            reinterpret_cast<unsigned long long*>(b.scal + 2));                 \
+    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NCp, b.scal + 3, src, dim, lpr, b.part, out.mean,       \
+                                            out.cap_groups, reinterpret_cast<unsigned long long*>(b.scal + 2)); \
   } while (0)
     if (v4) {
       if (cpl == 1) ALTO_MEAN_CASE(4, 1);
