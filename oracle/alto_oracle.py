@@ -34,6 +34,11 @@ Readings where the paper is silent (each is listed in the design notes):
   order. FIRST is the payload of the group's first leaf in key order.
 * Error priority in a batch: layout, then fan-out, then duplicate, then capacity.
   In a stream: layout, late, fan-out, duplicate, capacity.
+* Release order of a stream (Section 3.2, pmap: as items finish, the stream is put
+  back in its original order and sent on): by default a group leaves in the step
+  that completes it; in order, the groups under one parent (the level above the
+  aggregation level) leave in child-index order, a complete group waiting for all
+  of its earlier siblings. Groups of different parents do not wait for each other.
 
 Parity is pinned against brute force, closed forms and textbook routines in
 ``tests/test_oracle_*.py``.
@@ -338,17 +343,30 @@ class StepResult:
     groups: Groups       # emitted this step (mask and pending unused)
 
 
+RELEASE_COMPLETE, RELEASE_IN_ORDER = "complete", "in_order"
+
+
 class Stream:
     """Feed a stream in steps. Each step is routed on its own; leaves of groups that
-    are not yet complete are carried; a group is emitted once, in the step that
-    completes it, with its payload computed over all of its leaves in key order."""
+    are not released are carried; a group is emitted once, in the step that releases
+    it, with its payload computed over all of its leaves in key order.
+
+    release="complete": a group is released in the step that completes it.
+    release="in_order": the children of one parent (level agg_level - 1) are released
+    in child-index order: child c leaves once children 0..c are all complete (the
+    pmap exit of Section 3.2 puts the parallelised stream back in its original
+    order). With agg_level 1 there is no parent and the two coincide."""
 
     def __init__(self, bits, route_level: int, num_dest: int, agg_level: int, op: str,
-                 dim: int = 1):
+                 dim: int = 1, release: str = RELEASE_COMPLETE):
         check_layout(bits)
         d = len(bits)
         if not (1 <= agg_level <= d - 1) or not (1 <= route_level <= agg_level) or num_dest < 1:
             raise OracleError(E_ARG, "levels")
+        if release not in (RELEASE_COMPLETE, RELEASE_IN_ORDER):
+            raise OracleError(E_ARG, "release order")
+        self.release = release
+        self.cursor = {}                                       # parent prefix -> next child to release
         self.bits, self.Lr, self.D, self.La, self.op, self.dim = tuple(bits), route_level, num_dest, agg_level, op, dim
         self.d = d
         self.keys = np.zeros(0, U64)                           # arrived leaves of live groups
@@ -389,13 +407,29 @@ class Stream:
         all_pf = None
         if self.op == MEAN:
             all_pf = np.concatenate([self.pf, np.asarray(payload_f32, np.float32).reshape(n, self.dim)])
-        # completion of the groups this step touched, over all their arrived leaves
-        touched = np.unique(gk)
         live_gk = prefix(all_keys, bits, La)
-        sel = np.isin(live_gk, touched)
-        comp = completion(all_keys[sel], all_fan[:, sel], bits, La)
-        gnodes, gcomplete = comp[La]
-        done = gnodes[gcomplete]
+        if self.release == RELEASE_IN_ORDER and La >= 2:
+            # completion of every live group (a complete group may wait for earlier
+            # siblings across steps), then each parent's children in child order
+            comp = completion(all_keys, all_fan, bits, La)
+            gnodes, gcomplete = comp[La]
+            complete = set(int(x) for x in gnodes[gcomplete])
+            cb = bits[La - 1]
+            released = []
+            for parent in sorted(set(int(x) >> cb for x in gnodes)):
+                c = self.cursor.get(parent, 0)
+                while ((parent << cb) | c) in complete:
+                    released.append((parent << cb) | c)
+                    c += 1
+                self.cursor[parent] = c
+            done = np.array(sorted(released), dtype=U64)
+        else:
+            # completion of the groups this step touched, over all their arrived leaves
+            touched = np.unique(gk)
+            sel = np.isin(live_gk, touched)
+            comp = completion(all_keys[sel], all_fan[:, sel], bits, La)
+            gnodes, gcomplete = comp[La]
+            done = gnodes[gcomplete]
         in_done = np.isin(live_gk, done)
         if len(done):
             _, g = aggregate(all_keys[in_done], all_fan[:, in_done], bits, La, self.op, self.dim, 0,

@@ -91,3 +91,18 @@ def stream_emission_steps(true_leaves, arrival, step_of_arrival, agg_level):
         if all(t in arrived_set for t in true_leaves if t[:agg_level] == g):
             out[g] = s
     return out
+
+
+def stream_release_steps_in_order(true_leaves, arrival, step_of_arrival, agg_level):
+    """Group tuple -> step in which it leaves when each parent's children leave in
+    child-index order: the latest completion step among children 0..c of its parent,
+    if all of them complete; absent otherwise. With no parent level, completion."""
+    comp = stream_emission_steps(true_leaves, arrival, step_of_arrival, agg_level)
+    if agg_level < 2:
+        return comp
+    out = {}
+    for g in {t[:agg_level] for t in true_leaves}:
+        sibs = [g[:-1] + (k,) for k in range(g[-1] + 1)]
+        if all(s in comp for s in sibs):
+            out[g] = max(comp[s] for s in sibs)
+    return out

@@ -438,3 +438,78 @@ def test_config3_emission_step_closed_form():
         want[int(k)] = i // w.step
     assert got == want
     assert len(s.pending()[0]) == 0
+
+
+def test_stream_in_order_release_brute_force():
+    # Children of one parent leave in child-index order: a group leaves in the step
+    # where it and all of its earlier siblings are complete (brute force on tag
+    # tuples and the arrival schedule), exactly once, with the same content whatever
+    # the arrival order; with a leaf missing, that group and its later siblings never
+    # leave and are pending, complete or not.
+    bits = (4, 2, 2, 3)
+    Lr, D = 1, 3
+    checked = 0
+    for seed in range(60):
+        La = 2 + seed % 2
+        path, fan = W.random_tree(500 + seed, 4, 1 + seed % 2, (2, 3, 2), bits)
+        n = path.shape[1]
+        if n > 9 or n < 3:
+            continue
+        true_leaves = brute.leaves_of(path)
+        drop = seed % 3 == 0
+        keep_idx = np.arange(n)
+        if drop:
+            keep_idx = np.delete(keep_idx, seed % n)
+        p32 = np.arange(n, dtype=np.int32) + 100
+        batch = brute.batch_expect(true_leaves, true_leaves, p32, None, La, 0, _dest_fn(bits, D), Lr)
+        tok_of = {r["key"]: r["tok"] for r in batch["emitted"]}
+        rng = np.random.default_rng(seed)
+        m = len(keep_idx)
+        for oi in range(60):
+            order = keep_idx[rng.permutation(m)]
+            ncut = 1 + oi % min(m, 4)
+            cuts = [0] + sorted(rng.choice(np.arange(1, m), size=ncut - 1, replace=False).tolist()) + [m]
+            sp, sf, st = path[:, order], fan[:, order], p32[order]
+            s = O.Stream(bits, Lr, D, La, "concat", 1, release="in_order")
+            keys = O.pack_keys(sp, bits)
+            seen = {}
+            for si, (a, b) in enumerate(zip(cuts[:-1], cuts[1:])):
+                r = s.step(keys[a:b], sf[:, a:b], st[a:b], None)
+                for j, k in enumerate(r.groups.key):
+                    gt = _tuple_of(int(k), bits, La)
+                    assert gt not in seen
+                    seen[gt] = si
+                    assert list(r.groups.tok[r.groups.tok_off[j]:r.groups.tok_off[j + 1]]) == tok_of[gt]
+            arrival = brute.leaves_of(sp)
+            step_of = np.searchsorted(cuts, np.arange(m), side="right") - 1
+            want = brute.stream_release_steps_in_order(true_leaves, arrival, step_of, La)
+            assert seen == want
+            pend = {_tuple_of(int(k), bits, La) for k in s.pending()[0]}
+            assert pend == {t[:La] for t in arrival} - set(want)
+            if drop:
+                assert true_leaves[seed % n][:La] not in seen   # its group never completes
+            checked += 1
+    assert checked > 1500
+
+
+def test_in_order_release_token_stream_matches_completion():
+    # Tokens of a generator arrive in order, so its sentences also complete in order:
+    # in-order release changes nothing (floor(last token's arrival index / step)).
+    w = W.config3(generators=16, sentences=8, step=256)
+    path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
+    keys = O.pack_keys(path, w.bits)
+    s = O.Stream(w.bits, w.route_level, w.num_dest, w.agg_level, "concat", release="in_order")
+    got = {}
+    for si, a in enumerate(range(0, w.n, w.step)):
+        b = min(a + w.step, w.n)
+        r = s.step(keys[a:b], fan[:, a:b], tok[a:b])
+        for k in r.groups.key:
+            got[int(k)] = si
+    gk = O.prefix(keys, w.bits, 2)
+    assert got == {int(k): i // w.step for i, k in enumerate(gk)}
+
+
+def test_in_order_release_argument():
+    with pytest.raises(O.OracleError) as e:
+        O.Stream((4, 3, 3), 1, 4, 2, "concat", release="sorted")
+    assert e.value.code == O.E_ARG
