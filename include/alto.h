@@ -72,17 +72,25 @@ typedef struct {
 } alto_layout;
 
 enum { ALTO_CONCAT_I32 = 0, ALTO_MEAN_F32 = 1 };
+enum { ALTO_RELEASE_COMPLETE = 0, ALTO_RELEASE_IN_ORDER = 1 };
 
 /* Aggregation at a pmap exit: level = La in [1, d-1] (groups are the level-La
  * nodes); op = ALTO_CONCAT_I32 (list the int32 payloads of a group's leaves in key
  * order) or ALTO_MEAN_F32 (flat mean of the float32 rows of all leaves, float64
  * accumulation, one rounding to float32); dim = row width for MEAN (1 for
- * CONCAT); mask_level = Lm in [1, d-1], or 0 for no completion mask. */
+ * CONCAT); mask_level = Lm in [1, d-1], or 0 for no completion mask.
+ * release (streams): ALTO_RELEASE_COMPLETE emits a group in the step that completes
+ * it; ALTO_RELEASE_IN_ORDER puts the pmap's output stream back in its original
+ * order (Section 3.2): the children of one parent (the level-(La-1) node) leave in
+ * child-index order, a complete group waiting in the carried state until all of its
+ * earlier siblings have left (with La = 1 the two coincide). Batches take
+ * ALTO_RELEASE_COMPLETE only. */
 typedef struct {
   int32_t level;
   int32_t op;
   int32_t dim;
   int32_t mask_level;
+  int32_t release;
 } alto_agg;
 
 /* Outputs of an aggregation. Any array pointer may be NULL to skip that output;
@@ -161,7 +169,8 @@ typedef struct alto_stream alto_stream; /* opaque host handle; state memory is t
 /* Device state bytes for a stream that holds at most max_live_leaves arrived
  * leaves of not-yet-emitted groups and sees at most max_groups distinct level-La
  * groups over its lifetime (emitted groups are remembered to detect late
- * fragments). Returns 0 for invalid arguments. */
+ * fragments; with in-order release, so are the parents' release positions).
+ * Returns 0 for invalid arguments. */
 size_t alto_stream_state_bytes(const alto_layout *layout, const alto_agg *agg,
                                int64_t max_live_leaves, int64_t max_groups);
 
@@ -174,8 +183,9 @@ int alto_stream_create(const alto_layout *layout, int32_t route_level, int32_t n
 
 /* One step: routes the step's n fragments on their own (perm, dest_offsets, dest as
  * in alto_route, all nullable), merges them into the carried state, and emits the
- * groups this step completes, each once, with its payload computed over all of its
- * leaves in key order (count, key, dest, first_i32, fan_up, tok_off/tok or mean).
+ * groups this step releases (see alto_agg.release), each once, with its payload
+ * computed over all of its leaves in key order (count, key, dest, first_i32,
+ * fan_up, tok_off/tok or mean); groups not released are listed in pend_key/pend_count.
  * Emitted groups per step are at most n; emitted tokens at most max_live_leaves + n.
  * Workspace: alto_workspace_bytes(layout, max_live_leaves + n_max, num_dest, agg)
  * with n_max >= n (the step is merged with the carried leaves).
@@ -186,7 +196,8 @@ int alto_stream_step(alto_stream *s, const uint64_t *keys, const int32_t *fan, i
                      int32_t *perm, int64_t *dest_offsets, int32_t *dest, alto_groups *emitted,
                      int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Lists the groups that have arrived leaves but never completed, by (dest, key):
+/* Lists the groups that have arrived leaves but were never released (incomplete,
+ * or complete and waiting for an earlier sibling), by (dest, key):
  * pend_key, pend_count and counts[3] of `out`; other members are ignored. */
 int alto_stream_pending(alto_stream *s, alto_groups *out, int32_t *status, hipStream_t stream);
 

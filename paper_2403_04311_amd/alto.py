@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(HERE, "libalto.so")
 
 OK, E_ARG, E_LAYOUT, E_DUPLICATE, E_FANOUT, E_LATE, E_CAPACITY, E_HIP = range(8)
 CONCAT_I32, MEAN_F32 = 0, 1
+RELEASE = {"complete": 0, "in_order": 1}
 STATUS_NAMES = {0: "OK", 1: "ARG", 2: "LAYOUT", 3: "DUPLICATE", 4: "FANOUT", 5: "LATE",
                 6: "CAPACITY", 7: "HIP"}
 
@@ -33,7 +34,7 @@ class Layout(C.Structure):
 
 class Agg(C.Structure):
     _fields_ = [("level", C.c_int32), ("op", C.c_int32), ("dim", C.c_int32),
-                ("mask_level", C.c_int32)]
+                ("mask_level", C.c_int32), ("release", C.c_int32)]
 
 
 class Groups(C.Structure):
@@ -96,9 +97,10 @@ def layout(bits: Sequence[int]) -> Layout:
     return l
 
 
-def agg_struct(level: int, op: str, dim: int = 1, mask_level: int = 0) -> Agg:
+def agg_struct(level: int, op: str, dim: int = 1, mask_level: int = 0, release: str = "complete") -> Agg:
     a = Agg()
     a.level, a.op, a.dim, a.mask_level = level, (MEAN_F32 if op == "mean" else CONCAT_I32), dim, mask_level
+    a.release = RELEASE[release]
     return a
 
 
@@ -249,12 +251,12 @@ class Stream:
     """Carried-state stream over caller-owned device memory."""
 
     def __init__(self, bits, route_level, num_dest, agg_level, op, dim=1, max_live_leaves=1 << 16,
-                 max_groups=1 << 20, step_max=4096, device="cuda", stream=None):
+                 max_groups=1 << 20, step_max=4096, device="cuda", stream=None, release="complete"):
         lib = load()
         self.lib = lib
         self.bits, self.Lr, self.D, self.La, self.op, self.dim = tuple(bits), route_level, num_dest, agg_level, op, dim
         self.L = layout(bits)
-        self.A = agg_struct(agg_level, op, dim, 0)
+        self.A = agg_struct(agg_level, op, dim, 0, release)
         nbytes = lib.alto_stream_state_bytes(C.byref(self.L), C.byref(self.A), max_live_leaves, max_groups)
         if nbytes == 0:
             raise AltoError(E_ARG, "alto_stream_state_bytes")

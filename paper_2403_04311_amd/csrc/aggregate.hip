@@ -868,8 +868,9 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
     L.ok = c.take<uint8_t>(n);
     L.bad = c.take<uint8_t>(n);
   }
-  if (Lt < Lseg) {
-    b.carry_fan = c.take<int32_t>((int64_t)(Lseg - Lt) * n);
+  if (Lt < Lseg) b.carry_fan = c.take<int32_t>((int64_t)(Lseg - Lt) * n);
+  if (Lt < Lseg || agg->release == ALTO_RELEASE_IN_ORDER) {
+    // node records re-sorted by key (a mask above the route level; release order)
     b.rkey = c.take<uint64_t>(n);
     b.rsk = c.take<uint64_t>(n);
     b.ridx = c.take<uint32_t>(n);

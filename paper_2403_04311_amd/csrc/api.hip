@@ -62,6 +62,7 @@ bool agg_ok(const alto_layout* l, const alto_agg* a, int route_level, int num_de
   if (a->mask_level < 0 || a->mask_level > d - 1) return false;
   if (a->op != ALTO_CONCAT_I32 && a->op != ALTO_MEAN_F32) return false;
   if (a->op == ALTO_MEAN_F32 && (a->dim < 1 || a->dim > (1 << 20))) return false;
+  if (a->release != ALTO_RELEASE_COMPLETE && a->release != ALTO_RELEASE_IN_ORDER) return false;
   if (route_level < 0 || route_level > a->level) return false;
   if (route_level == 0 && num_dest != 1) return false;
   return true;
@@ -153,6 +154,7 @@ int alto_aggregate(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, con
       !out->counts || !agg_ok(layout, agg, route_level, num_dest) || out->cap_groups < 0 || out->cap_tokens < 0 ||
       out->cap_mask < 0)
     return ALTO_E_ARG;
+  if (agg->release != ALTO_RELEASE_COMPLETE) return ALTO_E_ARG;   // an order of release needs a stream
   if (agg->op == ALTO_CONCAT_I32 && !payload_i32 && n > 0) return ALTO_E_ARG;
   if (agg->op == ALTO_MEAN_F32 && !payload_f32 && n > 0) return ALTO_E_ARG;
   GroupOut o = to_dev_out(out);

@@ -8,7 +8,9 @@
 //              written alternately;
 //   arena      MEAN: one float32 row per live leaf, with a stack of free slots;
 //   emitted    an insert-only open-addressing set of emitted group keys, to
-//              report fragments that arrive after their group was released.
+//              report fragments that arrive after their group was released;
+//   parents    with in-order release: each parent's next child to release, in an
+//              insert-only open-addressing table keyed by the parent's prefix.
 // A step sorts its own fragments, merges them with the live set by binary search
 // (merge path), segments the merged run into nodes, evaluates completion, emits the
 // complete groups with the batch kernels, and writes the survivors as the new live
@@ -50,11 +52,17 @@ __device__ inline bool dk_less(const RouteGeom& rg, uint64_t a, uint64_t b) {
   return da < db || (da == db && a < b);
 }
 
-__global__ void k_stream_init(StreamCtl* ctl, int32_t* stack, int64_t cap, uint64_t* ht, int64_t htcap) {
+__global__ void k_stream_init(StreamCtl* ctl, int32_t* stack, int64_t cap, uint64_t* ht, int64_t htcap, uint64_t* pht,
+                              int32_t* pcur) {
   const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (int64_t)gridDim.x * blockDim.x;
   if (stack)
     for (int64_t i = t0; i < cap; i += stride) stack[i] = (int32_t)i;
   for (int64_t i = t0; i < htcap; i += stride) ht[i] = HT_EMPTY;
+  if (pht)
+    for (int64_t i = t0; i < htcap; i += stride) {
+      pht[i] = HT_EMPTY;
+      pcur[i] = 0;
+    }
   if (t0 == 0) {
     ctl->error = 0;
     ctl->live = 0;
@@ -304,6 +312,61 @@ __global__ void k_emit_insert(KeyGeom g, int La, LevelNodes L, const int64_t* Gp
   if (full) raise_status(status, ALTO_E_CAPACITY);
 }
 
+// Group records for in-order release: the level-La prefix of every group of the
+// merged run.
+__global__ void k_rel_keys(LevelNodes L, const int64_t* Gp, const uint64_t* __restrict__ mkey, int shiftLa,
+                           uint64_t* rkey) {
+  const int64_t G = *Gp;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x)
+    rkey[u] = key_prefix(mkey[L.start[u]], shiftLa);
+}
+
+// In-order release (Section 3.2: the parallelised stream is put back in its
+// original order). Over the group records sorted by key, the first record of each
+// parent's run walks the run in child order from the parent's release position and
+// releases complete children until the first missing or incomplete one; the
+// completion flags of the run's groups become their release flags. One thread per
+// parent, so a parent's position has one writer per step.
+__global__ void k_release(LevelNodes L, const int64_t* Gp, const uint64_t* __restrict__ rsk,
+                          const uint32_t* __restrict__ ridx, int cbits, uint64_t cmask, uint64_t* pht, int32_t* pcur,
+                          int64_t htcap, int32_t* status) {
+  const int64_t R = *Gp;
+  bool full = false;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < R; i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t P = rsk[i] >> cbits;
+    if (i > 0 && (rsk[i - 1] >> cbits) == P) continue;   // not the first record of its parent
+    int64_t h = (int64_t)(mix64(P ^ 0x5851F42D4C957F2Dull) & (uint64_t)(htcap - 1));
+    int64_t slot = -1;
+    for (int64_t probe = 0; probe < htcap; ++probe) {
+      const uint64_t v = pht[h];   // a slot changes once, from empty; the CAS settles a stale empty
+      if (v == P) {
+        slot = h;
+        break;
+      }
+      if (v == HT_EMPTY) {
+        const uint64_t old = atomicCAS((unsigned long long*)&pht[h], (unsigned long long)HT_EMPTY, (unsigned long long)P);
+        if (old == HT_EMPTY || old == P) {
+          slot = h;
+          break;
+        }
+      }
+      h = (h + 1) & (htcap - 1);
+    }
+    if (slot < 0) full = true;
+    int64_t cur = slot >= 0 ? pcur[slot] : -1;   // table full: nothing is released
+    bool open = slot >= 0;
+    for (int64_t j = i; j < R && (rsk[j] >> cbits) == P; ++j) {
+      const uint32_t u = ridx[j];
+      const bool rel = open && L.ok[u] && (int64_t)(rsk[j] & cmask) == cur;
+      if (rel) ++cur;
+      else open = false;
+      L.ok[u] = rel ? 1 : 0;
+    }
+    if (slot >= 0) pcur[slot] = (int32_t)cur;
+  }
+  if (full) raise_status(status, ALTO_E_CAPACITY);
+}
+
 // pending groups of the live set
 __global__ void k_pend_flags(KeyGeom g, int La, const StreamCtl* ctl, int64_t cap, const uint64_t* __restrict__ key,
                              int32_t* flag, int64_t* len1) {
@@ -353,6 +416,8 @@ struct alto_stream {
   float* arena;
   int32_t* stack;
   uint64_t* ht;
+  uint64_t* pht;   // in-order release: parent prefixes
+  int32_t* pcur;   // in-order release: next child to release per parent
   int32_t* pflag;
   int32_t* ppart;
   int64_t* plen;
@@ -384,6 +449,13 @@ void carve_state(const KeyGeom& g, const alto_agg& agg, int64_t cap, int64_t max
   }
   s->htcap = ht_capacity(max_groups);
   s->ht = c.take<uint64_t>(s->htcap);
+  if (agg.release == ALTO_RELEASE_IN_ORDER && agg.level >= 2) {   // parents <= groups
+    s->pht = c.take<uint64_t>(s->htcap);
+    s->pcur = c.take<int32_t>(s->htcap);
+  } else {
+    s->pht = nullptr;
+    s->pcur = nullptr;
+  }
   s->pflag = c.take<int32_t>(cap + 1);
   s->ppart = c.take<int32_t>(SCAN_MAX_BLOCKS + 1);
   s->plen = c.take<int64_t>(4);
@@ -404,6 +476,7 @@ bool stream_args_ok(const alto_layout* l, const alto_agg* a, int64_t cap, int64_
   if (a->level < 1 || a->level > l->depth - 1 || a->mask_level != 0) return false;
   if (a->op != ALTO_CONCAT_I32 && a->op != ALTO_MEAN_F32) return false;
   if (a->op == ALTO_MEAN_F32 && (a->dim < 1 || a->dim > (1 << 20))) return false;
+  if (a->release != ALTO_RELEASE_COMPLETE && a->release != ALTO_RELEASE_IN_ORDER) return false;
   if (cap < 1 || cap > (int64_t)(1 << 30) || max_groups < 1 || max_groups > ((int64_t)1 << 40)) return false;
   return true;
 }
@@ -464,7 +537,8 @@ int alto_stream_create(const alto_layout* layout, int32_t route_level, int32_t n
     return ALTO_E_ARG;
   }
   k_stream_init<<<grid_for(s->htcap > s->cap ? s->htcap : s->cap, 256), 256, 0, stream>>>(s->ctl, s->stack, s->cap,
-                                                                                         s->ht, s->htcap);
+                                                                                         s->ht, s->htcap, s->pht,
+                                                                                         s->pcur);
   if (hipGetLastError() != hipSuccess) {
     delete s;
     return ALTO_E_HIP;
@@ -540,6 +614,33 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
   rc = seg_run(g, j, st);
   if (rc) return rc;
   fp_compare_launch(b.fp_in, b.fp_nodes, La, d - 1, status, st);
+  if (s->pht) {
+    // in-order release: group records by key (the step's sort buffers are free
+    // after the merge), then each parent's run from its release position
+    const int64_t* Gp = b.nnodes + La;
+    k_rel_keys<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, mkey, g.shift[La], b.rkey);
+    SortBufs rb;
+    memset(&rb, 0, sizeof(rb));
+    rb.in_keys = b.rkey;
+    rb.tmp_keys = b.sk;
+    rb.tmp_vals = b.perm;
+    rb.out_keys = b.rsk;
+    rb.out_vals = b.ridx;
+    rb.ctl = b.rctl;
+    rb.os_status = b.os_status;
+    rb.os_ctr = b.os_ctr;
+    rb.os_hist = b.os_hist;
+    rb.os_ntiles = b.os_ntiles;
+    rb.status = status;
+    RouteGeom none;
+    none.shift = 64;
+    none.num_dest = 1;
+    rc = sort_pairs(rb, ntot, Gp, none, g.total - g.shift[La], false, st);
+    if (rc) return rc;
+    k_release<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, b.rsk, b.ridx, g.shift[La - 1] - g.shift[La],
+                                                   (uint64_t)g.tagmask[La], s->pht, s->pcur, s->htcap, status);
+    ALTO_LAUNCH_CHECK();
+  }
   prof_end(PH_SEGMENT, st);
   // 4. emitted groups (payload over all of each group's leaves, in key order)
   MergedSrc src{msrc, payload_i32, fan, fan_ld, payload_f32, old.p32, old.fan, s->cap, old.slot, s->arena, s->cap,

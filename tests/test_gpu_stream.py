@@ -12,11 +12,11 @@ pytestmark = pytest.mark.gpu
 
 
 def gpu_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pf, cuts, max_live=4096, max_groups=1 << 16,
-              step_max=None):
+              step_max=None, release="complete"):
     """Runs a stream on the GPU; returns per-step dicts of numpy outputs and statuses."""
     step_max = step_max or max(int(np.diff(cuts).max()), 1)
     s = alto.Stream(bits, Lr, D, La, op, dim, max_live_leaves=max_live, max_groups=max_groups,
-                    step_max=step_max)
+                    step_max=step_max, release=release)
     dk = U.to_dev(keys.astype(np.uint64).view(np.int64))
     dfan = U.to_dev(fan.astype(np.int32))
     d32 = U.to_dev(p32.astype(np.int32)) if p32 is not None else None
@@ -63,8 +63,8 @@ def gpu_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pf, cuts, max_live=4096,
     return out, pres
 
 
-def oracle_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pf, cuts):
-    s = O.Stream(bits, Lr, D, La, op, dim)
+def oracle_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pf, cuts, release="complete"):
+    s = O.Stream(bits, Lr, D, La, op, dim, release=release)
     res = []
     for a, b in zip(cuts[:-1], cuts[1:]):
         try:
@@ -260,3 +260,65 @@ def test_stream_errors_and_poison(kind):
     else:
         assert codes_g == codes_o, (codes_g, codes_o)
         assert codes_o[-1] != O.OK                                    # poisoned after the error
+
+
+# ---------------------------------------------------------------- in-order release
+
+@pytest.mark.parametrize("case", range(len(STREAM_CASES)))
+@pytest.mark.parametrize("op", ["concat", "mean"])
+def test_stream_in_order_release_parity(case, op):
+    """Children of a parent leave in child-index order (the pmap exit puts its output
+    stream back in order); complete groups wait in the carried state."""
+    depth, bits, mf, roots, La, Lr, D, drop, dim, nsteps = STREAM_CASES[case]
+    keys, fan, p32, pf = _tiny(600 + case, depth, bits, mf, roots, drop, dim)
+    n = len(keys)
+    rng = np.random.default_rng(100 + case)
+    cuts = [0] + sorted(rng.choice(np.arange(1, n), size=nsteps - 1, replace=False).tolist()) + [n]
+    pfa = pf if op == "mean" else None
+    gpu = gpu_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pfa, cuts, release="in_order")
+    ora = oracle_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pfa, cuts, release="in_order")
+    compare_steps(gpu, ora, op, La)
+    # something was held back at least once (the order differs from completion)
+    ora_c = oracle_steps(bits, Lr, D, La, op, dim, keys, fan, p32, pfa, cuts)
+    step_of = lambda res: {int(k): i for i, (c, r) in enumerate(res[0]) if c == O.OK for k in r.groups.key}
+    assert step_of(ora) != step_of(ora_c)
+
+
+def test_stream_in_order_release_many_groups():
+    """More groups in one step than one workgroup sorts (the group records take the
+    multi-block sort), with dropped leaves holding later siblings back."""
+    bits = (10, 8, 4)
+    keys, fan, p32, pf = _tiny(71, 3, bits, (60, 3), 400, 0.01, 1)
+    n = len(keys)
+    cuts = [0, n // 3, n]
+    gpu = gpu_steps(bits, 1, 16, 2, "concat", 1, keys, fan, p32, None, cuts, max_live=1 << 15,
+                    max_groups=1 << 15, step_max=n, release="in_order")
+    ora = oracle_steps(bits, 1, 16, 2, "concat", 1, keys, fan, p32, None, cuts, release="in_order")
+    assert sum(len(r.groups.key) for c, r in ora[0] if c == O.OK) > 8192
+    compare_steps(gpu, ora, "concat", 2)
+
+
+def test_factool_stream_in_order_two_stages():
+    """Documents leave in order within their search query; claims in order within
+    their query."""
+    path, fan, docid, pf = _windowed_factool(8, 24, 3000, 256)
+    bits = (31, 3, 2, 3, 8)
+    keys = O.pack_keys(path, bits)
+    n = len(keys)
+    cuts = sorted(set(list(range(0, n, 256)) + [n]))
+    gA = gpu_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, max_live=8192,
+                   max_groups=1 << 14, step_max=256, release="in_order")
+    oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, release="in_order")
+    compare_steps(gA, oA, "mean", 4)
+    bB = W.CONFIG2_STAGE_B["bits"]
+    kB, fB, pB, cB = [], [], [], [0]
+    for r in gA[0]:
+        kB.append(r["key"])
+        fB.append(r["fan_up"])
+        pB.append(r["first"])
+        cB.append(cB[-1] + len(r["key"]))
+    kB, fB, pB = np.concatenate(kB), np.concatenate(fB, axis=1), np.concatenate(pB)
+    gB = gpu_steps(bB, 2, 32, 2, "concat", 1, kB, fB, pB, None, cB, max_live=8192, max_groups=1 << 14,
+                   step_max=max(int(np.diff(cB).max()), 1), release="in_order")
+    oB = oracle_steps(bB, 2, 32, 2, "concat", 1, kB, fB, pB, None, cB, release="in_order")
+    compare_steps(gB, oB, "concat", 2)
