@@ -276,7 +276,8 @@ def bench_tokens(args):
     status = alto.new_status()
 
     def run():
-        s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step)
+        s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step,
+                        release=args.release)
 
         def one(i):
             a, b = i * step, min(n, (i + 1) * step)
@@ -291,7 +292,8 @@ def bench_tokens(args):
     ms = tot / nsteps
     path_bytes = (n * (8 + 4 + 4 + 4 + 4 + 4) + 16384 * (8 + 4 + 8 + 4 + 8)) / nsteps
     return _line(f"token stream: 256 generators x 64 sentences, geometric(1/24) tokens, round-robin, "
-                 f"{step}-fragment steps, concat per sentence, 64 destinations", n / nsteps, ms, nsteps, 1,
+                 f"{step}-fragment steps, concat per sentence, 64 destinations, release {args.release}",
+                 n / nsteps, ms, nsteps, 1,
                  path_bytes, {"stream_fragments": n, "stream_ms": tot,
                               "step_ms_p50": _pct(per, 50), "step_ms_p99": _pct(per, 99),
                               "step_ms_max": max(per)})
@@ -315,9 +317,9 @@ def bench_factool_stream(args):
 
     def run(nsteps):
         sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22,
-                         step_max=step)
+                         step_max=step, release=args.release)
         sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
-                         step_max=step)
+                         step_max=step, release=args.release)
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(nsteps)]
         wall = []
@@ -350,7 +352,8 @@ def bench_factool_stream(args):
     path_bytes = (n * (8 + 12 + 4 + 3072 + 8) + E * (8 + 4 + 8 + 4 + 12 + 3072)) / steps
     ms = total / steps
     return _line(f"FacTool-shaped windowed stream: {steps} steps x {step} fragments, 768-d mean per document "
-                 "then document-id concat per claim (both stages each step, emitted count read back per step)",
+                 f"then document-id concat per claim (both stages each step, emitted count read back per step), "
+                 f"release {args.release}",
                  step, ms, steps, 50, path_bytes,
                  {"stream_fragments": n, "documents_emitted": E, "window_fragments": w.info["window"],
                   "long_lived_fraction": w.info["calibrated_frac"],
@@ -377,6 +380,8 @@ def main():
                     help="write the mean kernel's HBM traffic summary from two rocprofv3 --pmc "
                          "counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--pmc-command", default="", help="the rocprofv3 commands, recorded in the summary")
+    ap.add_argument("--release", default="complete", choices=["complete", "in_order"],
+                    help="streams: a group leaves when complete, or in child order within its parent")
     ap.add_argument("--workload", default="zipf64M", choices=["zipf64M", "all"] + sorted(WORKLOADS),
                     help="zipf64M (default): the 2^26-fragment Zipf batch")
     args = ap.parse_args()

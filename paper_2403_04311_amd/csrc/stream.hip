@@ -327,6 +327,8 @@ __global__ void k_rel_keys(LevelNodes L, const int64_t* Gp, const uint64_t* __re
 // releases complete children until the first missing or incomplete one; the
 // completion flags of the run's groups become their release flags. One thread per
 // parent, so a parent's position has one writer per step.
+// ridx null: the records are already in key order within each parent (the merged
+// run's own order, when the route level is above the aggregation level).
 __global__ void k_release(LevelNodes L, const int64_t* Gp, const uint64_t* __restrict__ rsk,
                           const uint32_t* __restrict__ ridx, int cbits, uint64_t cmask, uint64_t* pht, int32_t* pcur,
                           int64_t htcap, int32_t* status) {
@@ -356,7 +358,7 @@ __global__ void k_release(LevelNodes L, const int64_t* Gp, const uint64_t* __res
     int64_t cur = slot >= 0 ? pcur[slot] : -1;   // table full: nothing is released
     bool open = slot >= 0;
     for (int64_t j = i; j < R && (rsk[j] >> cbits) == P; ++j) {
-      const uint32_t u = ridx[j];
+      const int64_t u = ridx ? (int64_t)ridx[j] : j;
       const bool rel = open && L.ok[u] && (int64_t)(rsk[j] & cmask) == cur;
       if (rel) ++cur;
       else open = false;
@@ -614,9 +616,18 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
   rc = seg_run(g, j, st);
   if (rc) return rc;
   fp_compare_launch(b.fp_in, b.fp_nodes, La, d - 1, status, st);
-  if (s->pht) {
-    // in-order release: group records by key (the step's sort buffers are free
-    // after the merge), then each parent's run from its release position
+  if (s->pht && s->Lr < La) {
+    // in-order release, a parent's children in one destination: the merged run
+    // already lists them in key order
+    const int64_t* Gp = b.nnodes + La;
+    k_rel_keys<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, mkey, g.shift[La], b.rkey);
+    k_release<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, b.rkey, nullptr, g.shift[La - 1] - g.shift[La],
+                                                   (uint64_t)g.tagmask[La], s->pht, s->pcur, s->htcap, status);
+    ALTO_LAUNCH_CHECK();
+  } else if (s->pht) {
+    // in-order release, siblings in several destinations: group records by key (the
+    // step's sort buffers are free after the merge), then each parent's run from
+    // its release position
     const int64_t* Gp = b.nnodes + La;
     k_rel_keys<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, mkey, g.shift[La], b.rkey);
     SortBufs rb;

@@ -284,16 +284,19 @@ def test_stream_in_order_release_parity(case, op):
     assert step_of(ora) != step_of(ora_c)
 
 
-def test_stream_in_order_release_many_groups():
-    """More groups in one step than one workgroup sorts (the group records take the
-    multi-block sort), with dropped leaves holding later siblings back."""
+@pytest.mark.parametrize("Lr", [1, 2])
+def test_stream_in_order_release_many_groups(Lr):
+    """More groups in one step than one workgroup sorts, with dropped leaves holding
+    later siblings back. Route level 2 = aggregation level: siblings sit in several
+    destinations and the group records take the multi-block sort; route level 1:
+    they are contiguous in the merged run."""
     bits = (10, 8, 4)
     keys, fan, p32, pf = _tiny(71, 3, bits, (60, 3), 400, 0.01, 1)
     n = len(keys)
     cuts = [0, n // 3, n]
-    gpu = gpu_steps(bits, 1, 16, 2, "concat", 1, keys, fan, p32, None, cuts, max_live=1 << 15,
+    gpu = gpu_steps(bits, Lr, 16, 2, "concat", 1, keys, fan, p32, None, cuts, max_live=1 << 15,
                     max_groups=1 << 15, step_max=n, release="in_order")
-    ora = oracle_steps(bits, 1, 16, 2, "concat", 1, keys, fan, p32, None, cuts, release="in_order")
+    ora = oracle_steps(bits, Lr, 16, 2, "concat", 1, keys, fan, p32, None, cuts, release="in_order")
     assert sum(len(r.groups.key) for c, r in ora[0] if c == O.OK) > 8192
     compare_steps(gpu, ora, "concat", 2)
 
