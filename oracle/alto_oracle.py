@@ -462,3 +462,47 @@ def _empty_groups(La, op, dim):
                   np.zeros(0, np.int32) if op == CONCAT else None,
                   np.zeros((0, dim), np.float32) if op == MEAN else None,
                   None, None, z64, np.zeros(0, np.int64))
+
+
+# ---------------------------------------------------------------------------
+# pcombine: join of two branches by ancestry
+# ---------------------------------------------------------------------------
+
+@dataclass
+class Join:
+    match: np.ndarray      # int32 [n_right]: left index with the same level-Lj prefix, or -1
+    hits: np.ndarray       # int32 [n_left]: right elements matched to each left object
+    counts: np.ndarray     # int64 [2]: matched right elements, left objects with a match
+
+
+def join(left_prefixes, right_keys, bits, level: int) -> Join:
+    """Section 3.2 (pcombine) and Section 4.2: objects produced by two parallel branches
+    under the same ancestry are combined. Left: one object per level-``level`` node,
+    given by its prefix (``key >> bits below level``, as the group keys of
+    ``aggregate``); right: fragments with full keys of layout ``bits``. Each right
+    element is paired with the left object whose prefix is its own level-``level``
+    prefix, or none (-1). A prefix held by two left objects is a DUPLICATE error;
+    a right key or left prefix wider than the layout is a LAYOUT error."""
+    check_layout(bits)
+    d = len(bits)
+    if not (1 <= level <= d):
+        raise OracleError(E_ARG, "join level")
+    left = np.asarray(left_prefixes, dtype=U64)
+    right = np.asarray(right_keys, dtype=U64)
+    _check_keys_fit(right, bits)
+    lbits = sum(bits[:level])
+    if len(left) and int(left.max()) >> lbits:
+        raise OracleError(E_LAYOUT, "left prefix wider than its levels")
+    index = {}
+    for i, p in enumerate(left.tolist()):
+        if p in index:
+            raise OracleError(E_DUPLICATE, "two left objects for one node")
+        index[p] = i
+    rp = prefix(right, bits, level)
+    match = np.array([index.get(int(p), -1) for p in rp.tolist()], dtype=np.int32)
+    hits = np.zeros(len(left), np.int32)
+    for m in match.tolist():
+        if m >= 0:
+            hits[m] += 1
+    counts = np.array([int((match >= 0).sum()), int((hits > 0).sum())], np.int64)
+    return Join(match, hits, counts)

@@ -513,3 +513,52 @@ def test_in_order_release_argument():
     with pytest.raises(O.OracleError) as e:
         O.Stream((4, 3, 3), 1, 4, 2, "concat", release="sorted")
     assert e.value.code == O.E_ARG
+
+
+# ---------------------------------------------------------------- pcombine join
+
+def test_join_matches_tuple_brute_force():
+    # Each right fragment is paired with the left object of its level-Lj ancestor
+    # (tuple comparison on the tag paths, no packed keys), or with none.
+    bits = (5, 3, 3, 4)
+    for seed in range(30):
+        path, fan = W.random_tree(700 + seed, 4, 6, (4, 5, 9), bits)
+        rng = np.random.default_rng(seed)
+        Lj = 1 + seed % 3
+        leaves = brute.leaves_of(path)
+        nodes = sorted({t[:Lj] for t in leaves})
+        chosen = [nodes[i] for i in rng.permutation(len(nodes))[: max(1, int(0.7 * len(nodes)))]]
+        chosen.append(tuple(list(nodes[0][:-1]) + [(1 << bits[Lj - 1]) - 1]))   # a node without fragments
+        chosen = list(dict.fromkeys(chosen))
+        left = np.array([_key_of(t + (0,) * (len(bits) - Lj), bits) >> O.shift_below(bits, Lj)
+                         for t in chosen], dtype=np.uint64)
+        sel = rng.random(len(leaves)) < 0.8
+        right = O.pack_keys(path[:, sel], bits)
+        rleaves = [t for t, s in zip(leaves, sel) if s]
+        j = O.join(left, right, bits, Lj)
+        pos = {t: i for i, t in enumerate(chosen)}
+        want = [pos.get(t[:Lj], -1) for t in rleaves]
+        assert j.match.tolist() == want
+        assert j.hits.tolist() == [sum(1 for w in want if w == i) for i in range(len(chosen))]
+        assert j.counts.tolist() == [sum(1 for w in want if w >= 0), sum(1 for i in range(len(chosen)) if i in want)]
+        assert j.hits[-1] == 0 or chosen[-1] in {t[:Lj] for t in rleaves}
+
+
+def test_join_errors_and_empty():
+    bits = (5, 3, 3, 4)
+    path, fan = W.random_tree(9, 4, 3, (3, 3, 3), bits)
+    keys = O.pack_keys(path, bits)
+    left = np.unique(O.prefix(keys, bits, 2))
+    with pytest.raises(O.OracleError) as e:
+        O.join(np.concatenate([left, left[:1]]), keys, bits, 2)
+    assert e.value.code == O.E_DUPLICATE
+    with pytest.raises(O.OracleError) as e:
+        O.join(np.array([1 << 8], np.uint64), keys, bits, 2)          # 9 bits for 8 bits of levels 1-2
+    assert e.value.code == O.E_LAYOUT
+    with pytest.raises(O.OracleError) as e:
+        O.join(left, np.array([1 << 15], np.uint64), bits, 2)
+    assert e.value.code == O.E_LAYOUT
+    j = O.join(left, keys[:0], bits, 2)
+    assert len(j.match) == 0 and j.hits.tolist() == [0] * len(left) and j.counts.tolist() == [0, 0]
+    j = O.join(left[:0], keys, bits, 2)
+    assert (j.match == -1).all() and j.counts.tolist() == [0, 0]
