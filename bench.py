@@ -361,8 +361,52 @@ def bench_factool_stream(args):
                   "device_step_ms_p50": _pct(dev, 50), "device_step_ms_p99": _pct(dev, 99)})
 
 
+def bench_join(args):
+    """pcombine by ancestry: left objects of one level joined with every fragment below
+    them. Timed: the 2^26-fragment Zipf tree (1,452 level-4 group objects); also
+    reported: the FacTool-shaped tree (search-query objects with their sentences)."""
+    import ctypes
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+
+    def one(keys, bits, level, steps, warmup):
+        shift = sum(bits[level:])
+        left = torch.unique(keys >> shift)
+        g = torch.Generator(device="cuda")
+        g.manual_seed(11)
+        left = left[torch.randperm(left.numel(), generator=g, device="cuda")].contiguous()
+        nl, nr = left.numel(), keys.numel()
+        L = alto.layout(bits)
+        ws = alto.new_workspace(alto.load().alto_join_workspace_bytes(ctypes.byref(L), nl))
+        match = torch.empty(nr, dtype=torch.int32, device="cuda")
+        hits = torch.empty(nl, dtype=torch.int32, device="cuda")
+        counts = torch.zeros(2, dtype=torch.int64, device="cuda")
+        st = alto.new_status()
+        ms = _timed(lambda: alto.join(left, keys, bits, level, match=match, hits=hits, counts=counts, status=st,
+                                      ws=ws), steps, warmup)
+        assert int(st.item()) == 0 and int(counts[0]) == nr
+        return nl, nr, ms
+
+    w2 = W.config2("cuda")
+    k2, _ = alto.pack_keys(w2.path, w2.bits)
+    nl2, nr2, ms2 = one(k2, w2.bits, 3, args.steps * 10, args.warmup)
+    del w2, k2
+    w5 = W.config5("cuda", leaves=1 << args.leaves_log2)
+    k5, _ = alto.pack_keys(w5.path, w5.bits)
+    del w5
+    torch.cuda.empty_cache()
+    nl5, nr5, ms5 = one(k5, (3, 12, 12, 12, 12, 12), 4, args.steps, args.warmup)
+    path_bytes = nr5 * (8 + 4) + nl5 * (8 + 4)
+    return _line(f"pcombine join: {nl5} level-4 group objects with all 2^{args.leaves_log2} fragments of the Zipf "
+                 f"depth-6 tree", nr5, ms5, args.steps, args.warmup, path_bytes,
+                 {"left_objects": nl5,
+                  "factool": {"left_objects": nl2, "right_fragments": nr2, "ms": ms2,
+                              "fragments_per_s": nr2 / (ms2 * 1e-3),
+                              "hbm_frac": (nr2 * 12 + nl2 * 12) / (ms2 * 1e-3) / 1e9 / HBM_PEAK_GBPS}})
+
+
 WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_tokens,
-             "factool_stream": bench_factool_stream}
+             "factool_stream": bench_factool_stream, "join": bench_join}
 
 
 def main():

@@ -204,6 +204,27 @@ int alto_stream_pending(alto_stream *s, alto_groups *out, int32_t *status, hipSt
 /* Frees the host handle (the caller frees the state memory). */
 int alto_stream_destroy(alto_stream *s);
 
+/* ---- pcombine: combining the outputs of two parallel branches by ancestry
+ * (Section 3.2, the pcombine operator; Section 4.2: the runtime associates objects
+ * that share ancestry) ---- */
+
+/* Workspace bytes for alto_join with up to n_left_max left objects. */
+size_t alto_join_workspace_bytes(const alto_layout *layout, int64_t n_left_max);
+
+/* Pairs every right fragment with the left object of its level-`level` ancestor.
+ * left[n_left] (uint64): one object per level-`level` node, given by the node's
+ * prefix (key >> bits below `level`, the format of alto_groups.key); right_keys
+ * [n_right] (uint64): full keys of `layout`. level in [1, depth].
+ * match[n_right] (int32): index into left of the fragment's object, -1 if none.
+ * hits[n_left] (int32, nullable): right fragments paired with each left object.
+ * counts: device int64[2]: paired right fragments, left objects with a pair.
+ * All arrays are caller-owned device memory; enqueues on `stream`, no sync.
+ * Errors: LAYOUT (a right key or left prefix wider than its levels), DUPLICATE
+ * (two left objects for one node; match is then undefined). */
+int alto_join(const uint64_t *left, int64_t n_left, const uint64_t *right_keys, int64_t n_right,
+              const alto_layout *layout, int32_t level, int32_t *match, int32_t *hits, int64_t *counts,
+              int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---- diagnostics: per-phase timing with HIP events on the caller's stream ----
  * Phases: 0 input-order pass (layout check, routing hash, fan checks), 1 radix sort
  * and destination offsets, 2 node segmentation and completion, 3 group records and

@@ -25,7 +25,7 @@ STATUS_NAMES = {0: "OK", 1: "ARG", 2: "LAYOUT", 3: "DUPLICATE", 4: "FANOUT", 5: 
 
 EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggregate",
            "alto_stream_state_bytes", "alto_stream_create", "alto_stream_step",
-           "alto_stream_pending", "alto_stream_destroy")
+           "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join")
 
 
 class Layout(C.Structure):
@@ -85,6 +85,10 @@ def load():
     lib.alto_stream_pending.argtypes = [vp, C.POINTER(Groups), vp, vp]
     lib.alto_stream_destroy.restype = C.c_int
     lib.alto_stream_destroy.argtypes = [vp]
+    lib.alto_join_workspace_bytes.restype = C.c_size_t
+    lib.alto_join_workspace_bytes.argtypes = [C.POINTER(Layout), i64]
+    lib.alto_join.restype = C.c_int
+    lib.alto_join.argtypes = [vp, i64, vp, i64, C.POINTER(Layout), i32, vp, vp, vp, vp, vp, C.c_size_t, vp]
     _lib = lib
     return lib
 
@@ -313,3 +317,29 @@ class Stream:
             self.close()
         except Exception:
             pass
+
+
+def join(left: torch.Tensor, right_keys: torch.Tensor, bits, level: int, match=None, hits=None, counts=None,
+         status=None, ws=None, stream=None, n_left=None, n_right=None):
+    """pcombine by ancestry: for every right fragment, the index of the left object
+    whose prefix is the fragment's level-``level`` prefix (-1 if none); returns
+    (match, hits, counts, status)."""
+    lib = load()
+    nl = left.shape[0] if n_left is None else n_left
+    nr = right_keys.shape[0] if n_right is None else n_right
+    dev = right_keys.device
+    L = layout(bits)
+    if ws is None:
+        ws = new_workspace(lib.alto_join_workspace_bytes(C.byref(L), nl), dev)
+    if match is None:
+        match = torch.empty(max(nr, 1), dtype=torch.int32, device=dev)
+    if hits is None:
+        hits = torch.empty(max(nl, 1), dtype=torch.int32, device=dev)
+    if counts is None:
+        counts = torch.zeros(2, dtype=torch.int64, device=dev)
+    if status is None:
+        status = new_status(dev)
+    rc = lib.alto_join(_p(left), nl, _p(right_keys), nr, C.byref(L), level, _p(match), _p(hits), _p(counts),
+                       _p(status), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "alto_join")
+    return match, hits, counts, status
