@@ -506,3 +506,91 @@ def join(left_prefixes, right_keys, bits, level: int) -> Join:
             hits[m] += 1
     counts = np.array([int((match >= 0).sum()), int((hits > 0).sum())], np.int64)
     return Join(match, hits, counts)
+
+
+# ---------------------------------------------------------------------------
+# split_text: pmap entry, one more level of ancestry
+# ---------------------------------------------------------------------------
+
+SPLIT_NONE = np.uint64(0xFFFFFFFFFFFFFFFF)
+
+
+@dataclass
+class Split:
+    keys: np.ndarray     # uint64 [n]: keys of layout bits_in[:-1] + (seg_bits, tok_bits), or SPLIT_NONE
+    fan: np.ndarray      # int32 [d][n]: declared child counts of levels 1..d of the new layout
+    counts: np.ndarray   # int64 [4]: tokens placed, delimiters, tokens of incomplete parents, segments
+
+
+def split_text(keys, fan, tokens, bits_in, delim: int, seg_bits: int, tok_bits: int) -> Split:
+    """Section 3.2 (split_text) and Section 4.2 (pmap entry pushes a level). The
+    fragments are tokens: leaves of layout ``bits_in`` whose parent (level d-1) is one
+    stream element, e.g. one language-model output, and whose leaf tag is the token's
+    index in that stream. Each parent's tokens are split at ``delim`` tokens into
+    segments (maximal runs of other tokens; the delimiters are separators and are not
+    placed, empty segments do not exist). A placed token gets the key (parent, segment
+    index, index in segment) in the layout ``bits_in[:-1] + (seg_bits, tok_bits)`` and
+    the declared child counts of the new levels: segments of its parent, tokens of its
+    segment (the counts of the levels above are copied). A parent is split only when
+    all of its declared tokens are present (the segment boundaries depend on every
+    token); its tokens are otherwise left unplaced (SPLIT_NONE), like delimiters.
+    Errors, by priority: LAYOUT (a key wider than bits_in), FANOUT (a declared count
+    < 1, a token index >= it, carriers of one parent disagreeing), DUPLICATE (a token
+    key twice), CAPACITY (a segment index or an index in a segment that does not fit
+    its bits)."""
+    bits_in = tuple(bits_in)
+    check_layout(bits_in)
+    d = len(bits_in)
+    if d < 2 or seg_bits < 1 or tok_bits < 1 or seg_bits > 32 or tok_bits > 32:
+        raise OracleError(E_ARG, "split layout")
+    bits_out = bits_in[:-1] + (seg_bits, tok_bits)
+    check_layout(bits_out)
+    keys = np.asarray(keys, dtype=U64)
+    fan = np.asarray(fan).astype(np.int64).reshape(d - 1, len(keys))
+    tokens = np.asarray(tokens).astype(np.int64)
+    n = len(keys)
+    _check_keys_fit(keys, bits_in)
+    par = prefix(keys, bits_in, d - 1)
+    idx = tag(keys, bits_in, d)
+    pfan = fan[d - 2]
+    if n and (pfan.min() < 1 or (idx >= pfan).any()):
+        raise OracleError(E_FANOUT, "token index outside its parent's declared count")
+    declared = {}
+    for p, f in zip(par.tolist(), pfan.tolist()):
+        if declared.setdefault(p, f) != f:
+            raise OracleError(E_FANOUT, "carriers of one parent disagree")
+    if len(np.unique(keys)) != n:
+        raise OracleError(E_DUPLICATE, "same token twice")
+    out_keys = np.full(n, SPLIT_NONE, dtype=U64)
+    out_fan = np.zeros((d, n), np.int32)
+    placed = delims = incomplete = segments = 0
+    rows = {}
+    for i, p in enumerate(par.tolist()):
+        rows.setdefault(p, []).append(i)
+    for p, members in rows.items():
+        if len(members) != declared[p]:
+            incomplete += len(members)
+            continue
+        members.sort(key=lambda i: int(idx[i]))
+        segs, cur = [], []
+        for i in members:
+            if tokens[i] == delim:
+                delims += 1
+                if cur:
+                    segs.append(cur)
+                cur = []
+            else:
+                cur.append(i)
+        if cur:
+            segs.append(cur)
+        segments += len(segs)
+        for c, seg in enumerate(segs):
+            for t, i in enumerate(seg):
+                if c >= (1 << seg_bits) or t >= (1 << tok_bits):
+                    raise OracleError(E_CAPACITY, "segment or index does not fit its bits")
+                out_keys[i] = (U64(p) << U64(seg_bits + tok_bits)) | (U64(c) << U64(tok_bits)) | U64(t)
+                out_fan[: d - 2, i] = fan[: d - 2, i]
+                out_fan[d - 2, i] = len(segs)
+                out_fan[d - 1, i] = len(seg)
+                placed += 1
+    return Split(out_keys, out_fan, np.array([placed, delims, incomplete, segments], np.int64))

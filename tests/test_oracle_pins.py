@@ -562,3 +562,125 @@ def test_join_errors_and_empty():
     assert len(j.match) == 0 and j.hits.tolist() == [0] * len(left) and j.counts.tolist() == [0, 0]
     j = O.join(left[:0], keys, bits, 2)
     assert (j.match == -1).all() and j.counts.tolist() == [0, 0]
+
+
+# ---------------------------------------------------------------- split_text (pmap entry)
+
+def _text_case(seed, parents, max_len, delim, p_delim, drop=0.0):
+    """Parents (level 2 of a (bits 6, 8, 10) layout) each holding a token stream;
+    returns keys, fan, tokens (shuffled) and the streams as Python lists."""
+    rng = np.random.default_rng(seed)
+    streams = {}
+    for q in range(parents):
+        L = int(rng.integers(1, max_len + 1))
+        toks = [int(delim) if rng.random() < p_delim else int(rng.integers(0, 1000)) for _ in range(L)]
+        streams[(int(rng.integers(0, 64)), q)] = toks
+    rows = [(r, q, i, t, len(toks)) for (r, q), toks in streams.items() for i, t in enumerate(toks)]
+    if drop:
+        rows = [x for x in rows if rng.random() >= drop]
+    rows = [rows[i] for i in rng.permutation(len(rows))]
+    path = np.array([[x[0] for x in rows], [x[1] for x in rows], [x[2] for x in rows]], np.int32)
+    fan = np.array([[1] * len(rows), [x[4] for x in rows]], np.int32)
+    # level-1 declared counts must agree per node: the number of parents under each root
+    roots = {}
+    for (r, q) in streams:
+        roots[r] = roots.get(r, 0) + 1
+    fan[0] = [roots[x[0]] for x in rows]
+    return path, fan, np.array([x[3] for x in rows], np.int32), streams
+
+
+def test_split_text_matches_list_splitting():
+    # Segments are the maximal runs of non-delimiter tokens of each complete parent,
+    # in token order (plain list splitting); keys decode to (parent, segment, index)
+    # and carry the new declared counts.
+    bits = (6, 8, 10)
+    for seed in range(40):
+        delim = 7
+        path, fan, tok, streams = _text_case(900 + seed, 12, 40, delim, 0.2, drop=0.05 if seed % 4 == 0 else 0.0)
+        keys = O.pack_keys(path, bits)
+        sp = O.split_text(keys, fan, tok, bits, delim, 6, 8)
+        present = {}
+        for i in range(len(keys)):
+            present.setdefault((int(path[0, i]), int(path[1, i])), set()).add(int(path[2, i]))
+        want_segments = 0
+        for i in range(len(keys)):
+            par = (int(path[0, i]), int(path[1, i]))
+            toks = streams[par]
+            complete = len(present[par]) == len(toks)
+            segs, cur = [], []
+            for j, t in enumerate(toks):
+                if t == delim:
+                    if cur:
+                        segs.append(cur)
+                    cur = []
+                else:
+                    cur.append(j)
+            if cur:
+                segs.append(cur)
+            where = {j: (c, k) for c, sg in enumerate(segs) for k, j in enumerate(sg)}
+            j = int(path[2, i])
+            if not complete or j not in where:
+                assert sp.keys[i] == O.SPLIT_NONE
+                assert (sp.fan[:, i] == 0).all()
+                continue
+            c, k = where[j]
+            assert _tuple_of(int(sp.keys[i]), (6, 8, 6, 8), 4) == par + (c, k)
+            assert sp.fan[:, i].tolist() == [int(fan[0, i]), len(segs), len(segs[c])]
+        for par, toks in streams.items():
+            if par in present and len(present[par]) == len(toks):
+                want_segments += sum(1 for x in "".join("d" if t == delim else "x" for t in toks).split("d") if x)
+        n_inc = sum(len(v) for p, v in present.items() if len(v) != len(streams[p]))
+        n_del = sum(1 for i in range(len(keys)) if tok[i] == delim
+                    and len(present[(int(path[0, i]), int(path[1, i]))]) == len(streams[(int(path[0, i]), int(path[1, i]))]))
+        assert sp.counts.tolist() == [int((sp.keys != O.SPLIT_NONE).sum()), n_del, n_inc, want_segments]
+
+
+def test_split_text_round_trip_through_concat():
+    # Concatenating the split tokens per segment (level 3 of the new layout) gives the
+    # segments of each parent's stream, in order.
+    bits = (6, 8, 10)
+    path, fan, tok, streams = _text_case(77, 20, 60, 3, 0.15)
+    keys = O.pack_keys(path, bits)
+    sp = O.split_text(keys, fan, tok, bits, 3, 6, 8)
+    keep = sp.keys != O.SPLIT_NONE
+    rt, g = O.aggregate(sp.keys[keep], sp.fan[:, keep], (6, 8, 6, 8), 3, "concat", 1, 0, 0, 1, tok[keep])
+    assert len(g.pend_key) == 0
+    got = {}
+    for j, k in enumerate(g.key):
+        par = _tuple_of(int(k), (6, 8, 6, 8), 3)[:2]
+        got.setdefault(par, []).append(list(g.tok[g.tok_off[j]:g.tok_off[j + 1]]))
+    for par, toks in streams.items():
+        segs, cur = [], []
+        for t in toks:
+            if t == 3:
+                if cur:
+                    segs.append(cur)
+                cur = []
+            else:
+                cur.append(t)
+        if cur:
+            segs.append(cur)
+        assert got.get(par, []) == segs
+
+
+def test_split_text_errors():
+    bits = (6, 8, 10)
+    path, fan, tok, _ = _text_case(5, 6, 30, 9, 0.1)
+    keys = O.pack_keys(path, bits)
+    for kind, code in [("dup", O.E_DUPLICATE), ("fan", O.E_FANOUT), ("idx", O.E_FANOUT), ("layout", O.E_LAYOUT),
+                       ("capacity", O.E_CAPACITY)]:
+        k, f, t = keys.copy(), fan.copy(), tok.copy()
+        sb, tb = 6, 8
+        if kind == "dup":
+            k, f, t = np.concatenate([k, k[:1]]), np.concatenate([f, f[:, :1]], axis=1), np.concatenate([t, t[:1]])
+        elif kind == "fan":
+            f[1, 0] += 1
+        elif kind == "idx":
+            f[1] = np.where(O.prefix(k, bits, 2) == O.prefix(k[:1], bits, 2)[0], 1, f[1])
+        elif kind == "layout":
+            k[0] = np.uint64(1 << 24)
+        else:
+            tb = 1                                            # segments longer than 2 tokens
+        with pytest.raises(O.OracleError) as e:
+            O.split_text(k, f, t, bits, 9, sb, tb)
+        assert e.value.code == code, kind
