@@ -39,6 +39,11 @@ Readings where the paper is silent (each is listed in the design notes):
   that completes it; in order, the groups under one parent (the level above the
   aggregation level) leave in child-index order, a complete group waiting for all
   of its earlier siblings. Groups of different parents do not wait for each other.
+* split_text at a pmap entry (Section 3.2; Section 4.2 pushes a level): a parent's
+  tokens are cut at a delimiter token into maximal runs of other tokens; only a
+  parent whose declared tokens have all arrived is cut (a missing token could be a
+  delimiter). The new fragments leave as a batch in new-key order; the tokens of
+  incomplete parents are listed in key order for a later attempt.
 
 Parity is pinned against brute force, closed forms and textbook routines in
 ``tests/test_oracle_*.py``.
@@ -520,6 +525,8 @@ class Split:
     keys: np.ndarray     # uint64 [n]: keys of layout bits_in[:-1] + (seg_bits, tok_bits), or SPLIT_NONE
     fan: np.ndarray      # int32 [d][n]: declared child counts of levels 1..d of the new layout
     counts: np.ndarray   # int64 [4]: tokens placed, delimiters, tokens of incomplete parents, segments
+    order: np.ndarray    # int64 [placed]: input indices of the placed tokens, by new key
+    rest: np.ndarray     # int64 [incomplete]: input indices of the tokens of incomplete parents, by key
 
 
 def split_text(keys, fan, tokens, bits_in, delim: int, seg_bits: int, tok_bits: int) -> Split:
@@ -534,6 +541,9 @@ def split_text(keys, fan, tokens, bits_in, delim: int, seg_bits: int, tok_bits: 
     segment (the counts of the levels above are copied). A parent is split only when
     all of its declared tokens are present (the segment boundaries depend on every
     token); its tokens are otherwise left unplaced (SPLIT_NONE), like delimiters.
+    The new fragments leave the entry as a batch in new-key order (``order``); the
+    tokens of incomplete parents are listed in key order (``rest``), to be offered
+    again with the rest of their stream.
     Errors, by priority: LAYOUT (a key wider than bits_in), FANOUT (a declared count
     < 1, a token index >= it, carriers of one parent disagreeing), DUPLICATE (a token
     key twice), CAPACITY (a segment index or an index in a segment that does not fit
@@ -564,12 +574,14 @@ def split_text(keys, fan, tokens, bits_in, delim: int, seg_bits: int, tok_bits: 
     out_keys = np.full(n, SPLIT_NONE, dtype=U64)
     out_fan = np.zeros((d, n), np.int32)
     placed = delims = incomplete = segments = 0
+    rest = []
     rows = {}
     for i, p in enumerate(par.tolist()):
         rows.setdefault(p, []).append(i)
     for p, members in rows.items():
         if len(members) != declared[p]:
             incomplete += len(members)
+            rest.extend(members)
             continue
         members.sort(key=lambda i: int(idx[i]))
         segs, cur = [], []
@@ -593,4 +605,8 @@ def split_text(keys, fan, tokens, bits_in, delim: int, seg_bits: int, tok_bits: 
                 out_fan[d - 2, i] = len(segs)
                 out_fan[d - 1, i] = len(seg)
                 placed += 1
-    return Split(out_keys, out_fan, np.array([placed, delims, incomplete, segments], np.int64))
+    placed_idx = np.nonzero(out_keys != SPLIT_NONE)[0]
+    order = placed_idx[np.argsort(out_keys[placed_idx], kind="stable")]
+    rest = np.array(sorted(rest, key=lambda i: int(keys[i])), dtype=np.int64)
+    return Split(out_keys, out_fan, np.array([placed, delims, incomplete, segments], np.int64),
+                 order.astype(np.int64), rest)

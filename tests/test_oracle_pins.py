@@ -633,6 +633,16 @@ def test_split_text_matches_list_splitting():
         n_del = sum(1 for i in range(len(keys)) if tok[i] == delim
                     and len(present[(int(path[0, i]), int(path[1, i]))]) == len(streams[(int(path[0, i]), int(path[1, i]))]))
         assert sp.counts.tolist() == [int((sp.keys != O.SPLIT_NONE).sum()), n_del, n_inc, want_segments]
+        # the batch leaves in (parent, segment, index) order; the rest in (parent, position) order
+        tup = {}
+        for i in range(len(keys)):
+            par = (int(path[0, i]), int(path[1, i]))
+            if sp.keys[i] != O.SPLIT_NONE:
+                tup[i] = _tuple_of(int(sp.keys[i]), (6, 8, 6, 8), 4)
+        assert sp.order.tolist() == sorted(tup, key=lambda i: tup[i])
+        inc = [i for i in range(len(keys)) if len(present[(int(path[0, i]), int(path[1, i]))])
+               != len(streams[(int(path[0, i]), int(path[1, i]))])]
+        assert sp.rest.tolist() == sorted(inc, key=lambda i: (int(path[0, i]), int(path[1, i]), int(path[2, i])))
 
 
 def test_split_text_round_trip_through_concat():
