@@ -14,7 +14,9 @@ Prints one JSON line. --gpus N > 1 is refused: this build runs on one GPU.
 every one): tiny (64-query depth-4 tree, token concat), factool (1,024-query
 FacTool-shaped batch, 768-d mean per document then document-id concat per claim),
 tokens (256-generator token stream in 4,096-fragment steps), factool_stream
-(10,000 steps of 4,096 fragments, both stages per step, per-step latency).
+(10,000 steps of 4,096 fragments, both stages per step, per-step latency), join
+(pcombine of level-4 group objects with the Zipf tree's fragments), split
+(split_text of 16,384 generator token streams into sentences at a pmap entry).
 """
 import argparse
 import json
@@ -405,8 +407,48 @@ def bench_join(args):
                               "hbm_frac": (nr2 * 12 + nl2 * 12) / (ms2 * 1e-3) / 1e9 / HBM_PEAK_GBPS}})
 
 
+def bench_split(args):
+    """split_text at a pmap entry: generator token streams cut at sentence delimiters
+    into (request, sentence, token) keys with their declared counts. Timed: 16,384
+    generator streams (64x the token-stream workload, 26.2M positions); also
+    reported: the 256 streams of the token-stream workload itself (408,190)."""
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+
+    def one(t, steps, warmup):
+        keys, st = alto.pack_keys(t.path, t.bits)
+        n = t.n
+        L = alto.layout(t.bits)
+        import ctypes
+        ws = alto.new_workspace(alto.load().alto_split_workspace_bytes(ctypes.byref(L), n))
+        ok = torch.empty(n, dtype=torch.int64, device="cuda")
+        of = torch.empty((len(t.bits), n), dtype=torch.int32, device="cuda")
+        otok = torch.empty(n, dtype=torch.int32, device="cuda")
+        oidx = torch.empty(n, dtype=torch.int32, device="cuda")
+        rest = torch.empty(n, dtype=torch.int32, device="cuda")
+        counts = torch.zeros(4, dtype=torch.int64, device="cuda")
+        ms = _timed(lambda: alto.split(keys, t.fan, t.tokens, t.bits, t.delim, t.seg_bits, t.tok_bits, out_keys=ok,
+                                       out_fan=of, out_tokens=otok, out_idx=oidx, rest_idx=rest, counts=counts,
+                                       status=st, ws=ws), steps, warmup)
+        assert int(st.item()) == 0 and int(counts[2]) == 0
+        return n, ms
+
+    t3 = W.config3_text("cuda")
+    n3, ms3 = one(t3, args.steps * 10, args.warmup)
+    del t3
+    t = W.config3_text("cuda", generators=16384)
+    n, ms = one(t, args.steps, args.warmup)
+    # in: key, stream length, token; out per placed token: key, two counts, token, input index
+    per = 8 + 4 + 4 + 8 + 4 + 4 + 4 + 4
+    return _line("split_text: 16,384 generator streams x 64 sentences, geometric(1/24) tokens + delimiter "
+                 "per sentence, round-robin arrival, cut into (request, sentence, token)", n, ms, args.steps,
+                 args.warmup, n * per,
+                 {"token_stream_256": {"positions": n3, "ms": ms3, "fragments_per_s": n3 / (ms3 * 1e-3),
+                                       "hbm_frac": n3 * per / (ms3 * 1e-3) / 1e9 / HBM_PEAK_GBPS}})
+
+
 WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_tokens,
-             "factool_stream": bench_factool_stream, "join": bench_join}
+             "factool_stream": bench_factool_stream, "join": bench_join, "split": bench_split}
 
 
 def main():

@@ -225,6 +225,43 @@ int alto_join(const uint64_t *left, int64_t n_left, const uint64_t *right_keys, 
               const alto_layout *layout, int32_t level, int32_t *match, int32_t *hits, int64_t *counts,
               int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- split_text at a pmap entry (Section 3.2, the split_text operator; Section
+ * 4.2: entering a pmap pushes a level onto the tag stack) ---- */
+
+/* Workspace bytes for alto_split with up to n_max tokens. */
+size_t alto_split_workspace_bytes(const alto_layout *layout, int64_t n_max);
+
+/* Splits token streams at a delimiter. keys[n] (uint64, `layout` of depth d in
+ * [2, 15]): tokens, leaves whose level-(d-1) node (the parent) is one stream
+ * element and whose leaf tag is the token's index in it. fan: int32 [(d-1)][fan_ld]
+ * as in alto_aggregate; row d-2 holds the parent's declared token count.
+ * tokens[n] (int32): token ids; tokens equal to `delim` separate segments. A
+ * parent whose declared tokens are all present is cut into segments, the maximal
+ * runs of non-delimiter tokens in index order (no empty segments); a parent with a
+ * token missing is not cut (the missing token could be a delimiter).
+ * The new fragments leave as a batch in ascending new-key order, rows
+ * 0..counts[0]-1 of: out_keys (uint64): (parent prefix << (seg_bits + tok_bits)) |
+ * (segment index << tok_bits) | index in segment, a key of the layout
+ * bits[0..d-2] + (seg_bits, tok_bits), seg_bits and tok_bits in [1, 32];
+ * out_fan: int32 [d][out_fan_ld], rows 0..d-3 copied from fan, row d-2 the
+ * parent's segment count, row d-1 the segment's token count; out_tokens (int32,
+ * nullable): the token; out_idx (int32, nullable): its input index (to move other
+ * payload columns). rest_idx (int32, nullable): input indices of the tokens of
+ * incomplete parents, in key order, counts[2] of them (to be offered again with
+ * the rest of their stream). Delimiters are dropped. Every output array holds n
+ * entries (out_fan_ld >= n). counts: device int64[4]: placed tokens, delimiters of
+ * complete parents, tokens of incomplete parents, segments. Arrays are
+ * caller-owned device memory; enqueues on `stream`, no sync. Errors: LAYOUT (a key
+ * wider than the layout), FANOUT (a declared count < 1, an index >= it, carriers
+ * of one parent disagreeing), DUPLICATE (a token key twice), CAPACITY (a segment
+ * index or an index in a segment that does not fit its bits); outputs are
+ * undefined on any error. */
+int alto_split(const uint64_t *keys, const int32_t *fan, int64_t fan_ld, const int32_t *tokens, int64_t n,
+               const alto_layout *layout, int32_t delim, int32_t seg_bits, int32_t tok_bits,
+               uint64_t *out_keys, int32_t *out_fan, int64_t out_fan_ld, int32_t *out_tokens,
+               int32_t *out_idx, int32_t *rest_idx, int64_t *counts, int32_t *status, void *ws,
+               size_t ws_bytes, hipStream_t stream);
+
 /* ---- diagnostics: per-phase timing with HIP events on the caller's stream ----
  * Phases: 0 input-order pass (layout check, routing hash, fan checks), 1 radix sort
  * and destination offsets, 2 node segmentation and completion, 3 group records and

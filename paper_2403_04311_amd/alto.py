@@ -25,7 +25,8 @@ STATUS_NAMES = {0: "OK", 1: "ARG", 2: "LAYOUT", 3: "DUPLICATE", 4: "FANOUT", 5: 
 
 EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggregate",
            "alto_stream_state_bytes", "alto_stream_create", "alto_stream_step",
-           "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join")
+           "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join",
+           "alto_split_workspace_bytes", "alto_split")
 
 
 class Layout(C.Structure):
@@ -89,6 +90,11 @@ def load():
     lib.alto_join_workspace_bytes.argtypes = [C.POINTER(Layout), i64]
     lib.alto_join.restype = C.c_int
     lib.alto_join.argtypes = [vp, i64, vp, i64, C.POINTER(Layout), i32, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.alto_split_workspace_bytes.restype = C.c_size_t
+    lib.alto_split_workspace_bytes.argtypes = [C.POINTER(Layout), i64]
+    lib.alto_split.restype = C.c_int
+    lib.alto_split.argtypes = [vp, vp, i64, vp, i64, C.POINTER(Layout), i32, i32, i32, vp, vp, i64, vp, vp, vp,
+                               vp, vp, vp, C.c_size_t, vp]
     _lib = lib
     return lib
 
@@ -343,3 +349,41 @@ def join(left: torch.Tensor, right_keys: torch.Tensor, bits, level: int, match=N
                        _p(status), _p(ws), ws.numel(), _stream(stream))
     _check(rc, "alto_join")
     return match, hits, counts, status
+
+
+def split(keys: torch.Tensor, fan: torch.Tensor, tokens: torch.Tensor, bits, delim: int, seg_bits: int,
+          tok_bits: int, out_keys=None, out_fan=None, out_tokens=None, out_idx=None, rest_idx=None, counts=None,
+          status=None, ws=None, stream=None, n=None, want_rest=True):
+    """split_text at a pmap entry: each complete parent's tokens cut at ``delim``
+    into segments. Returns (out_keys, out_fan, out_tokens, out_idx, rest_idx,
+    counts, status): rows 0..counts[0]-1 of the first four are the new fragments in
+    new-key order (layout ``bits[:-1] + (seg_bits, tok_bits)``); rest_idx[:counts[2]]
+    lists the input indices of the tokens of incomplete parents."""
+    lib = load()
+    n = keys.shape[0] if n is None else n
+    dev = keys.device
+    L = layout(bits)
+    d = len(bits)
+    m = max(n, 1)
+    if ws is None:
+        ws = new_workspace(lib.alto_split_workspace_bytes(C.byref(L), n), dev)
+    if out_keys is None:
+        out_keys = torch.empty(m, dtype=torch.int64, device=dev)
+    if out_fan is None:
+        out_fan = torch.empty((d, m), dtype=torch.int32, device=dev)
+    if out_tokens is None:
+        out_tokens = torch.empty(m, dtype=torch.int32, device=dev)
+    if out_idx is None:
+        out_idx = torch.empty(m, dtype=torch.int32, device=dev)
+    if rest_idx is None and want_rest:
+        rest_idx = torch.empty(m, dtype=torch.int32, device=dev)
+    if counts is None:
+        counts = torch.zeros(4, dtype=torch.int64, device=dev)
+    if status is None:
+        status = new_status(dev)
+    rc = lib.alto_split(_p(keys), _p(fan), fan.stride(0) if fan.dim() == 2 else m, _p(tokens), n,
+                        C.byref(L), delim, seg_bits, tok_bits, _p(out_keys), _p(out_fan), out_fan.stride(0),
+                        _p(out_tokens), _p(out_idx), _p(rest_idx) if rest_idx is not None else None,
+                        _p(counts), _p(status), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "alto_split")
+    return out_keys, out_fan, out_tokens, out_idx, rest_idx, counts, status

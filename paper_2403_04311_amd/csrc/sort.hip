@@ -40,15 +40,18 @@ __global__ void k_sort_init(SortCtl* ctl) {
   }
 }
 
-// OR / AND of keys and destinations (which bits vary).
+// OR / AND of the keys and destinations (which bits vary). Waves reduce with shuffles, blocks in
+// LDS, and each block adds one atomic per value: the four words are shared by the
+// whole grid, and same-address atomics serialise.
 __global__ __launch_bounds__(256) void k_sort_reduce(const uint64_t* __restrict__ keys, int64_t n_host,
                                                      const int64_t* n_dev, RouteGeom rg, SortCtl* ctl) {
+  __shared__ uint64_t s_or[256 / ALTO_WAVE], s_and[256 / ALTO_WAVE];
+  __shared__ uint32_t s_dor[256 / ALTO_WAVE], s_dand[256 / ALTO_WAVE];
   const int64_t n = load_n(n_host, n_dev);
+  if ((int64_t)blockIdx.x * blockDim.x >= n) return;   // block-uniform
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
-  // waves with no element skip the atomics (they would only add contention)
-  const int64_t wave0 = (int64_t)blockIdx.x * blockDim.x + (threadIdx.x & ~(ALTO_WAVE - 1));
-  if (wave0 >= n) return;
+#pragma unroll 4
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     uint64_t k = keys[i];
     kor |= k;
@@ -64,7 +67,21 @@ __global__ __launch_bounds__(256) void k_sort_reduce(const uint64_t* __restrict_
     dor |= __shfl_xor(dor, o);
     dand &= __shfl_xor(dand, o);
   }
+  const int w = threadIdx.x / ALTO_WAVE;
   if (lane_id() == 0) {
+    s_or[w] = kor;
+    s_and[w] = kand;
+    s_dor[w] = dor;
+    s_dand[w] = dand;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int v = 1; v < 256 / ALTO_WAVE; ++v) {
+      kor |= s_or[v];
+      kand &= s_and[v];
+      dor |= s_dor[v];
+      dand &= s_dand[v];
+    }
     atomicOr((unsigned long long*)&ctl->key_or, (unsigned long long)kor);
     atomicAnd((unsigned long long*)&ctl->key_and, (unsigned long long)kand);
     atomicOr(&ctl->dest_or, dor);
@@ -1002,7 +1019,7 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
   }
   if (!ctl_has_reduction) {
     k_sort_init<<<1, 1, 0, st>>>(b.ctl);
-    k_sort_reduce<<<grid_r, 256, 0, st>>>(b.in_keys, n_max, n_dev, rg, b.ctl);
+    k_sort_reduce<<<grid_r < 512 ? grid_r : 512, 256, 0, st>>>(b.in_keys, n_max, n_dev, rg, b.ctl);
   }
   // packed words need a host-known count (the index bits are fixed on the host)
   const bool packable = b.fl.hcap > 0 && n_dev == nullptr;
@@ -1070,5 +1087,5 @@ void sort_reduce_launch(const uint64_t* keys, int64_t n_max, const int64_t* n_de
                         hipStream_t st) {
   const int grid_r = (int)(n_max < 1 ? 1 : (cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048));
   k_sort_init<<<1, 1, 0, st>>>(ctl);
-  k_sort_reduce<<<grid_r, 256, 0, st>>>(keys, n_max, n_dev, rg, ctl);
+  k_sort_reduce<<<grid_r < 512 ? grid_r : 512, 256, 0, st>>>(keys, n_max, n_dev, rg, ctl);
 }

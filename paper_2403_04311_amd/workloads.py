@@ -288,6 +288,93 @@ def config3(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
     return w
 
 
+DELIM_TOKEN = 50000   # a token id outside the range tokens() draws: a sentence end
+
+
+def text_tokens(seed: int, n: int, p_delim: float, delim: int = DELIM_TOKEN) -> np.ndarray:
+    """Token ids of n stream positions, each the delimiter with probability p_delim."""
+    rng = np.random.default_rng(seed)
+    t = tokens(rng, n)
+    t[rng.random(n) < p_delim] = delim
+    return t
+
+
+@dataclass
+class TextStreams:
+    """Token streams at a pmap entry: one stream per level-(d-1) node (the parent),
+    a token's leaf tag being its position in the stream."""
+
+    bits: tuple                 # input layout (..., parent, position)
+    seg_bits: int               # bits of the segment level the split pushes
+    tok_bits: int               # bits of the token index within a segment
+    delim: int
+    path: torch.Tensor          # int32 [d][n], arrival order
+    fan: torch.Tensor           # int32 [d-1][n]; row d-2 is the stream length
+    tokens: torch.Tensor        # int32 [n]
+    tree_path: torch.Tensor     # int32 [d+1][n]: tags the position was written from (-1 for delimiters)
+    tree_fan: torch.Tensor      # int32 [d][n]: counts of those nodes (0 for delimiters)
+
+    @property
+    def n(self) -> int:
+        return int(self.path.shape[1])
+
+
+def config3_text(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
+                 sentences: int = 64) -> TextStreams:
+    """The token streams config 3's sentences come from: every generator writes its
+    sentences as one stream, each sentence followed by a delimiter token, and a pmap
+    entry cuts the streams back into sentences. Same draws as config 3 (same seed,
+    same generators: the same requests, sentence lengths and token ids).
+    Layout (request 31 bits, position 18 bits) -> (request, sentence 6, token 12);
+    arrival round-robin over generators, in order within each. The streams are laid
+    out with torch on ``device`` (the draws stay numpy)."""
+    rng = np.random.default_rng(seed)
+    roots = distinct_ids(rng, generators)
+    fans = draw_topdown(rng, roots, [const_int(sentences), geometric(1.0 / 24.0, 4095)])
+    L_np = fans[1].astype(np.int64)                    # sentence lengths, request-major
+    tok = _to_dev(tokens(rng, int(L_np.sum())), device)
+    L = _to_dev(L_np, device)
+    rt = _to_dev(roots, device)
+    width = L + 1                                      # each sentence and its delimiter
+    rlen = width.view(generators, sentences).sum(1)
+    n = int(rlen.sum())
+    # request-major concatenation of the streams
+    g = torch.arange(n, device=device)
+    req = torch.repeat_interleave(torch.arange(generators, device=device), rlen)
+    pos = g - torch.repeat_interleave(torch.cumsum(rlen, 0) - rlen, rlen)
+    assert int(pos.max()) < (1 << 18)
+    sent = torch.repeat_interleave(torch.arange(len(L_np), device=device), width)   # global sentence index
+    idx = g - torch.repeat_interleave(torch.cumsum(width, 0) - width, width)        # index within the sentence
+    del g
+    is_delim = idx == L[sent]
+    tk = torch.full((n,), DELIM_TOKEN, dtype=torch.int32, device=device)
+    tk[~is_delim] = tok
+    order = torch.argsort(pos, stable=True)            # tick-major, generators in index order
+    req, pos, sent, idx, is_delim, tk = req[order], pos[order], sent[order], idx[order], is_delim[order], tk[order]
+    p2 = torch.stack([rt[req], pos.to(torch.int32)])
+    f1 = rlen[req].to(torch.int32)[None, :]
+    tp = torch.stack([rt[req], (sent % sentences).to(torch.int32), idx.to(torch.int32)])
+    tp[:, is_delim] = -1
+    tf = torch.stack([torch.full((n,), sentences, dtype=torch.int32, device=device), L[sent].to(torch.int32)])
+    tf[:, is_delim] = 0
+    return TextStreams((31, 18), 6, 12, DELIM_TOKEN, p2.contiguous(), f1.contiguous(), tk, tp, tf)
+
+
+def random_text(seed: int, depth: int, roots: int, max_fan: Sequence[int], bits: Sequence[int], p_delim: float,
+                drop: float = 0.0, seg_bits: int = 8, tok_bits: int = 10, delim: int = DELIM_TOKEN):
+    """Random token streams: a depth-``depth`` tree whose leaf tags are stream
+    positions (U{1..max_fan[-1]} tokens per stream), shuffled, optionally with a
+    fraction of tokens dropped (incomplete streams). Returns (path, fan, tokens)
+    as numpy arrays in arrival order."""
+    path, fan = random_tree(seed, depth, roots, max_fan, bits)
+    tok = text_tokens(seed + 1, path.shape[1], p_delim, delim)
+    if drop:
+        path, fan, keep = drop_leaves(path, fan, drop, seed + 2)
+        tok = tok[keep]
+    (path, fan, tok), _ = permute([path, fan, tok], seed + 3)
+    return path, fan, tok
+
+
 def config4(device="cpu", seed: int = SEED_BASE + 4, steps: int = 10000, step: int = 4096,
             target_frac: float = 0.30, ring_steps: int = 256) -> Workload:
     """FacTool-shaped trees as a continuous windowed stream of ``steps`` x ``step``.
