@@ -44,6 +44,11 @@ Readings where the paper is silent (each is listed in the design notes):
   parent whose declared tokens have all arrived is cut (a missing token could be a
   delimiter). The new fragments leave as a batch in new-key order; the tokens of
   incomplete parents are listed in key order for a later attempt.
+* Load-aware routing (Section 4.3: a new flow of tags may be sent by load rather
+  than by hash; Section 5: replicas chosen by queue length): a flow is a distinct
+  route-level prefix and keeps its first destination. Per batch the fragments of
+  known flows join their queues first, then new flows in ascending prefix order take
+  the shortest queue (lowest index among ties), which grows by the flow's fragments.
 
 Parity is pinned against brute force, closed forms and textbook routines in
 ``tests/test_oracle_*.py``.
@@ -610,3 +615,68 @@ def split_text(keys, fan, tokens, bits_in, delim: int, seg_bits: int, tok_bits: 
     rest = np.array(sorted(rest, key=lambda i: int(keys[i])), dtype=np.int64)
     return Split(out_keys, out_fan, np.array([placed, delims, incomplete, segments], np.int64),
                  order.astype(np.int64), rest)
+
+
+# ---------------------------------------------------------------------------
+# load-aware routing (Section 4.3: a new flow of tags may go where the load is
+# lowest instead of where a hash sends it; Section 5: replicas chosen by queue length)
+# ---------------------------------------------------------------------------
+
+@dataclass
+class LoadRoute:
+    perm: np.ndarray          # int32 [n], input indices in (dest, key) order
+    dest_offsets: np.ndarray  # int64 [D+1]
+    dest: np.ndarray          # int32 [n], input order
+    load: np.ndarray          # int64 [D], queue lengths after the batch
+    counts: np.ndarray        # int64 [2]: new flows assigned, flows seen before
+
+
+class LoadRouter:
+    """Sticky least-loaded routing of flows (distinct level-``route_level`` prefixes).
+
+    A flow keeps the destination it was first given, so all fragments with the same
+    tags reach the same instance (Section 4.3). Per batch: the fragments of flows
+    seen before join their destination's queue first; then the new flows, in
+    ascending prefix order, each go to the destination with the shortest queue
+    (ties: the lowest index), whose queue then grows by the flow's fragments in the
+    batch. Queue lengths are the caller's (``load``): routing adds every fragment it
+    sends, the caller subtracts what a destination has consumed. At most
+    ``max_flows`` flows are remembered; a batch whose new flows do not fit raises
+    CAPACITY and changes nothing."""
+
+    def __init__(self, bits, route_level: int, num_dest: int, max_flows: int):
+        check_layout(bits)
+        if not (1 <= route_level <= len(bits)) or num_dest < 1 or max_flows < 1:
+            raise OracleError(E_ARG, "load router")
+        self.bits, self.Lr, self.D, self.max_flows = tuple(bits), route_level, num_dest, max_flows
+        self.table: Dict[int, int] = {}
+
+    def route(self, keys, load) -> LoadRoute:
+        keys = np.asarray(keys, dtype=U64)
+        load = np.array(load, dtype=np.int64).copy()
+        if load.shape != (self.D,) or (load < 0).any():
+            raise OracleError(E_ARG, "load")
+        n = len(keys)
+        _check_keys_fit(keys, self.bits)
+        if len(np.unique(keys)) != n:
+            raise OracleError(E_DUPLICATE, "same key twice")
+        flows = prefix(keys, self.bits, self.Lr)
+        size: Dict[int, int] = {}
+        for f in flows.tolist():
+            size[f] = size.get(f, 0) + 1
+        new = sorted(f for f in size if f not in self.table)
+        if len(self.table) + len(new) > self.max_flows:
+            raise OracleError(E_CAPACITY, "flow table full")
+        known = 0
+        for f, c in size.items():
+            if f in self.table:
+                load[self.table[f]] += c
+                known += 1
+        for f in new:
+            d = int(np.argmin(load))          # first minimum: the lowest index among ties
+            self.table[f] = d
+            load[d] += size[f]
+        dest = np.array([self.table[f] for f in flows.tolist()], dtype=np.int32)
+        perm = np.lexsort((keys, dest)).astype(np.int32)
+        offs = np.concatenate([[0], np.cumsum(np.bincount(dest, minlength=self.D))]).astype(np.int64)
+        return LoadRoute(perm, offs, dest, load, np.array([len(new), known], np.int64))

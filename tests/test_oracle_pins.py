@@ -694,3 +694,93 @@ def test_split_text_errors():
         with pytest.raises(O.OracleError) as e:
             O.split_text(k, f, t, bits, 9, sb, tb)
         assert e.value.code == code, kind
+
+
+# ---------------------------------------------------------------- load-aware routing
+
+def _keys2(pairs):
+    """Keys of layout (4, 4) from (flow, leaf) pairs."""
+    return np.array([(f << 4) | c for f, c in pairs], dtype=np.uint64)
+
+
+def test_load_router_worked_example():
+    # Two destinations, flows at level 1. Batch 1 from empty queues: flow 1 (two
+    # fragments) takes destination 0, flow 3 the then shorter queue 1. Batch 2, the
+    # caller reports queues [5, 0]: flow 3 is known, its 7 fragments join queue 1
+    # (-> [5, 7]); new flow 2 (3 fragments) takes queue 0 (-> [8, 7]); new flow 4 takes
+    # queue 1 (-> [8, 8]).
+    r = O.LoadRouter((4, 4), 1, 2, 16)
+    a = r.route(_keys2([(3, 0), (1, 0), (1, 1)]), [0, 0])
+    assert a.dest.tolist() == [1, 0, 0] and a.load.tolist() == [2, 1] and a.counts.tolist() == [2, 0]
+    assert a.perm.tolist() == [1, 2, 0] and a.dest_offsets.tolist() == [0, 2, 3]
+    b = r.route(_keys2([(4, 0)] + [(3, c) for c in range(1, 8)] + [(2, 0), (2, 1), (2, 2)]), [5, 0])
+    assert b.dest.tolist() == [1] + [1] * 7 + [0, 0, 0]
+    assert b.load.tolist() == [8, 8] and b.counts.tolist() == [2, 1]
+    assert b.perm.tolist() == [8, 9, 10] + list(range(1, 8)) + [0]
+
+
+def test_load_router_equal_flows_go_round_robin():
+    # F new flows of m fragments each on D empty queues: flow k (prefix order) lands
+    # on queue k mod D; queues end at m * ceil or floor of F / D.
+    for D, F, m in [(4, 10, 3), (7, 7, 1), (3, 20, 5), (16, 5, 2)]:
+        r = O.LoadRouter((8, 4), 1, D, 64)
+        rng = np.random.default_rng(D * 100 + F)
+        flows = np.sort(rng.choice(256, F, replace=False))
+        keys = _keys_fl(flows, m)
+        out = r.route(keys[rng.permutation(len(keys))], np.zeros(D, np.int64))
+        for k, f in enumerate(flows):
+            assert r.table[int(f)] == k % D
+        assert out.load.tolist() == [m * (F // D + (1 if d < F % D else 0)) for d in range(D)]
+
+
+def _keys_fl(flows, m):
+    return np.array([(int(f) << 4) | c for f in flows for c in range(m)], dtype=np.uint64)
+
+
+def test_load_router_sticky_balanced_and_ordered():
+    # Over random batches: a flow's destination never changes; after the first batch
+    # from empty queues the longest queue is within one flow of the mean (the bound
+    # of greedy list scheduling); queue growth equals the batch size; perm is the
+    # (destination, key) order.
+    bits = (6, 5, 4)
+    for seed in range(12):
+        rng = np.random.default_rng(4000 + seed)
+        D = int(rng.integers(1, 9))
+        r = O.LoadRouter(bits, 2, D, 4096)
+        load = np.zeros(D, np.int64)
+        seen = {}
+        for step in range(4):
+            path, fan = W.random_tree(4100 + seed * 10 + step, 3, int(rng.integers(1, 30)), (12, 9), bits)
+            keys = O.pack_keys(path, bits)
+            keys = keys[rng.permutation(len(keys))]
+            out = r.route(keys, load)
+            flows = O.prefix(keys, bits, 2)
+            sizes = {}
+            for f, d in zip(flows.tolist(), out.dest.tolist()):
+                assert seen.setdefault(f, d) == d
+                sizes[f] = sizes.get(f, 0) + 1
+            assert int(out.load.sum() - load.sum()) == len(keys)
+            if step == 0:
+                assert out.load.max() <= len(keys) / D + max(sizes.values())
+            want = sorted(range(len(keys)), key=lambda i: (int(out.dest[i]), int(keys[i])))
+            assert out.perm.tolist() == want
+            assert out.dest_offsets.tolist() == [0] + np.cumsum(np.bincount(out.dest, minlength=D)).tolist()
+            # a replica drains part of its queue between batches
+            load = out.load - rng.integers(0, out.load + 1)
+
+
+def test_load_router_errors():
+    r = O.LoadRouter((4, 4), 1, 2, 2)
+    with pytest.raises(O.OracleError) as e:
+        r.route(_keys2([(1, 0), (1, 0)]), [0, 0])
+    assert e.value.code == O.E_DUPLICATE
+    with pytest.raises(O.OracleError) as e:
+        r.route(np.array([1 << 9], np.uint64), [0, 0])
+    assert e.value.code == O.E_LAYOUT
+    r.route(_keys2([(1, 0)]), [0, 0])
+    with pytest.raises(O.OracleError) as e:
+        r.route(_keys2([(2, 0), (3, 0)]), [0, 0])       # two new flows, one slot left
+    assert e.value.code == O.E_CAPACITY
+    assert r.table == {1: 0}                             # nothing changed
+    out = r.route(_keys2([(2, 0), (1, 1)]), [0, 0])
+    assert out.counts.tolist() == [1, 1] and r.table == {1: 0, 2: 1}
