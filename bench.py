@@ -16,7 +16,8 @@ FacTool-shaped batch, 768-d mean per document then document-id concat per claim)
 tokens (256-generator token stream in 4,096-fragment steps), factool_stream
 (10,000 steps of 4,096 fragments, both stages per step, per-step latency), join
 (pcombine of level-4 group objects with the Zipf tree's fragments), split
-(split_text of 16,384 generator token streams into sentences at a pmap entry).
+(split_text of 16,384 generator token streams into sentences at a pmap entry),
+route_load (sticky least-loaded routing of flows, against hash routing).
 """
 import argparse
 import json
@@ -447,8 +448,110 @@ def bench_split(args):
                                        "hbm_frac": n3 * per / (ms3 * 1e-3) / 1e9 / HBM_PEAK_GBPS}})
 
 
+def bench_route_load(args):
+    """Load-aware routing (flows keep their first destination; new flows take the
+    shortest queue). Timed: the 2^26-fragment Zipf tree routed by its level-4 prefix
+    (1,452 flows) to 256 destinations with every flow known (steady state; the
+    queues are emptied between calls). Also: the first call (every flow new, the
+    greedy assignment included), hash routing (alto_route) of the same keys, the
+    queue balance of both, and the FacTool-shaped stream routed by claim to 32
+    destinations step by step, each destination draining 128 fragments per step."""
+    import time as T
+    import torch
+    from paper_2403_04311_amd import alto, workloads as W
+    w5 = W.config5("cuda", leaves=1 << args.leaves_log2)
+    keys, _ = alto.pack_keys(w5.path, w5.bits)
+    bits = w5.bits
+    del w5
+    torch.cuda.empty_cache()
+    n, D = keys.numel(), 256
+    rt = alto.LoadRouter(bits, 4, D, 1 << 16, n)
+    load = torch.zeros(D, dtype=torch.int64, device="cuda")
+    perm = torch.empty(n, dtype=torch.int32, device="cuda")
+    offs = torch.empty(D + 1, dtype=torch.int64, device="cuda")
+    dest = torch.empty(n, dtype=torch.int32, device="cuda")
+    counts = torch.zeros(2, dtype=torch.int64, device="cuda")
+    st = alto.new_status()
+    first = []
+    for _ in range(3):
+        rt.reset()
+        load.zero_()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rt.route(keys, load, perm=perm, dest_offsets=offs, dest=dest, counts=counts, status=st)
+        e1.record()
+        torch.cuda.synchronize()
+        first.append(e0.elapsed_time(e1))
+    assert int(st.item()) == 0 and int(counts[0]) > 0
+    flows = int(counts[0])
+    bal_load = float(load.max()) / float(load.double().mean())
+
+    def steady():
+        load.zero_()
+        rt.route(keys, load, perm=perm, dest_offsets=offs, dest=dest, counts=counts, status=st)
+    ms = _timed(steady, args.steps, args.warmup)
+    assert int(st.item()) == 0 and int(counts[0]) == 0 and int(counts[1]) == flows
+    hws = alto.new_workspace(alto.workspace_bytes(bits, n, D))
+    hoffs = torch.empty(D + 1, dtype=torch.int64, device="cuda")
+    hst = alto.new_status()
+    ms_hash = _timed(lambda: alto.route(keys, bits, 4, D, ws=hws, perm=perm, dest_offsets=hoffs, dest=dest,
+                                        status=hst), args.steps, args.warmup)
+    hc = (hoffs[1:] - hoffs[:-1]).double()
+    bal_hash = float(hc.max()) / float(hc.mean())
+    del hws, perm, dest, keys, rt
+    torch.cuda.empty_cache()
+
+    # the FacTool-shaped stream: claims as flows, 32 destinations, 128 fragments drained per step
+    w = W.config4("cuda")
+    skeys, _ = alto.pack_keys(w.path, w.bits)
+    step, steps = w.step, min(w.info["steps"], args.stream_steps)
+    Ds, service = 32, 128
+    srt = alto.LoadRouter(w.bits, 2, Ds, 1 << 20, step)
+    sload = torch.zeros(Ds, dtype=torch.int64, device="cuda")
+    hload = torch.zeros(Ds, dtype=torch.int64, device="cuda")
+    sp = torch.empty(step, dtype=torch.int32, device="cuda")
+    so = torch.empty(Ds + 1, dtype=torch.int64, device="cuda")
+    sd = torch.empty(step, dtype=torch.int32, device="cuda")
+    sc = torch.zeros(2, dtype=torch.int64, device="cuda")
+    sst = alto.new_status()
+    hws = alto.new_workspace(alto.workspace_bytes(w.bits, step, Ds))
+    hso = torch.empty(Ds + 1, dtype=torch.int64, device="cuda")
+    maxq = torch.zeros(steps, dtype=torch.int64, device="cuda")
+    hmaxq = torch.zeros(steps, dtype=torch.int64, device="cuda")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = T.perf_counter()
+    for s in range(steps):
+        k = skeys[s * step:(s + 1) * step]
+        evs[s][0].record()
+        srt.route(k, sload, perm=sp, dest_offsets=so, dest=sd, counts=sc, status=sst)
+        evs[s][1].record()
+        maxq[s] = sload.max()
+        sload.sub_(service).clamp_(min=0)
+        alto.route(k, w.bits, 2, Ds, ws=hws, perm=sp, dest_offsets=hso, dest=sd, status=hst)
+        hload.add_(hso[1:] - hso[:-1])
+        hmaxq[s] = hload.max()
+        hload.sub_(service).clamp_(min=0)
+    torch.cuda.synchronize()
+    wall = (T.perf_counter() - t0) * 1e3
+    assert int(sst.item()) == 0 and int(hst.item()) == 0
+    dev = [a.elapsed_time(b) for a, b in evs]
+    stream = {"steps": steps, "step_fragments": step, "destinations": Ds, "drain_per_step": service,
+              "route_load_ms_p50": _pct(dev, 50), "route_load_ms_p99": _pct(dev, 99),
+              "loop_ms_per_step_both_routers": wall / steps,
+              "mean_longest_queue_load_aware": float(maxq.double().mean()),
+              "mean_longest_queue_hash": float(hmaxq.double().mean())}
+    return _line(f"load-aware routing: 2^{args.leaves_log2}-fragment Zipf depth-6 tree, {flows} level-4 flows known, "
+                 f"256 destinations", n, ms, args.steps, args.warmup, n * (8 + 4 + 4),
+                 {"first_call_ms": min(first), "hash_route_ms": ms_hash,
+                  "longest_over_mean_queue": {"load_aware": bal_load, "hash": bal_hash},
+                  "factool_stream": stream})
+
+
 WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_tokens,
-             "factool_stream": bench_factool_stream, "join": bench_join, "split": bench_split}
+             "factool_stream": bench_factool_stream, "join": bench_join, "split": bench_split,
+             "route_load": bench_route_load}
 
 
 def main():
@@ -459,6 +562,8 @@ def main():
     ap.add_argument("--leaves-log2", type=int, default=26)
     ap.add_argument("--cpu-sample-log2", type=int, default=24)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--stream-steps", type=int, default=10000,
+                    help="route_load: steps of the FacTool-shaped stream part (at most 10,000)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB before the workload (untimed), the "
                          "reference for scaling hardware byte counters")

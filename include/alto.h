@@ -225,6 +225,43 @@ int alto_join(const uint64_t *left, int64_t n_left, const uint64_t *right_keys, 
               const alto_layout *layout, int32_t level, int32_t *match, int32_t *hits, int64_t *counts,
               int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- load-aware routing (Section 4.3: the destination of a new flow of tags may
+ * be chosen by load instead of by hashing; Section 5: replicas chosen by queue
+ * length) ---- */
+
+typedef struct alto_router alto_router; /* opaque host handle; flow table in caller memory */
+
+/* Device state bytes for a router that remembers up to max_flows flows. */
+size_t alto_router_state_bytes(int64_t max_flows);
+
+/* Creates a router over caller-owned device memory `state` and clears it on
+ * `stream`. A flow is a distinct level-`route_level` prefix (route_level in [1,
+ * depth]); num_dest in [1, 4096]. */
+int alto_router_create(const alto_layout *layout, int32_t route_level, int32_t num_dest, int64_t max_flows,
+                       void *state, size_t state_bytes, hipStream_t stream, alto_router **out);
+
+/* Frees the host handle (the caller frees the state memory). */
+int alto_router_destroy(alto_router *r);
+
+/* Workspace bytes for alto_route_load with up to n_max fragments. */
+size_t alto_route_load_workspace_bytes(int64_t n_max, int32_t num_dest);
+
+/* Routes one batch. load: device int64[num_dest], the destinations' queue lengths,
+ * updated in place (the caller subtracts what a destination has consumed between
+ * calls). A flow seen in an earlier call keeps its destination, and its fragments
+ * are added to that queue first; then the batch's new flows, in ascending prefix
+ * order, each go to the shortest queue (the lowest index among equal ones), which
+ * grows by the flow's fragments in the batch. perm (int32 [n], nullable): input
+ * indices in (destination, key) order; dest_offsets (int64 [num_dest + 1],
+ * nullable); dest (int32 [n], nullable): per input fragment. counts: device
+ * int64[2]: new flows assigned, flows seen before. Errors: LAYOUT, DUPLICATE,
+ * CAPACITY (the new flows do not fit in max_flows). On any error, including one
+ * already in *status on entry, neither load nor the flow table changes and the
+ * outputs are undefined. Calls on one router must not overlap. */
+int alto_route_load(alto_router *r, const uint64_t *keys, int64_t n, int64_t *load, int32_t *perm,
+                    int64_t *dest_offsets, int32_t *dest, int64_t *counts, int32_t *status, void *ws,
+                    size_t ws_bytes, hipStream_t stream);
+
 /* ---- split_text at a pmap entry (Section 3.2, the split_text operator; Section
  * 4.2: entering a pmap pushes a level onto the tag stack) ---- */
 

@@ -651,7 +651,8 @@ class LoadRouter:
         self.bits, self.Lr, self.D, self.max_flows = tuple(bits), route_level, num_dest, max_flows
         self.table: Dict[int, int] = {}
 
-    def route(self, keys, load) -> LoadRoute:
+    def route(self, keys, load, with_perm: bool = True) -> LoadRoute:
+        """``with_perm=False`` leaves perm empty (large batches in tests)."""
         keys = np.asarray(keys, dtype=U64)
         load = np.array(load, dtype=np.int64).copy()
         if load.shape != (self.D,) or (load < 0).any():
@@ -660,23 +661,22 @@ class LoadRouter:
         _check_keys_fit(keys, self.bits)
         if len(np.unique(keys)) != n:
             raise OracleError(E_DUPLICATE, "same key twice")
-        flows = prefix(keys, self.bits, self.Lr)
-        size: Dict[int, int] = {}
-        for f in flows.tolist():
-            size[f] = size.get(f, 0) + 1
-        new = sorted(f for f in size if f not in self.table)
+        flows, inverse, sizes = np.unique(prefix(keys, self.bits, self.Lr), return_inverse=True,
+                                          return_counts=True)
+        flows, sizes = flows.tolist(), sizes.tolist()           # ascending prefix order
+        new = [k for k, f in enumerate(flows) if f not in self.table]
         if len(self.table) + len(new) > self.max_flows:
             raise OracleError(E_CAPACITY, "flow table full")
         known = 0
-        for f, c in size.items():
+        for f, c in zip(flows, sizes):
             if f in self.table:
                 load[self.table[f]] += c
                 known += 1
-        for f in new:
+        for k in new:
             d = int(np.argmin(load))          # first minimum: the lowest index among ties
-            self.table[f] = d
-            load[d] += size[f]
-        dest = np.array([self.table[f] for f in flows.tolist()], dtype=np.int32)
-        perm = np.lexsort((keys, dest)).astype(np.int32)
+            self.table[flows[k]] = d
+            load[d] += sizes[k]
+        dest = np.array([self.table[f] for f in flows], dtype=np.int32)[inverse].astype(np.int32)
+        perm = np.lexsort((keys, dest)).astype(np.int32) if with_perm else np.zeros(0, np.int32)
         offs = np.concatenate([[0], np.cumsum(np.bincount(dest, minlength=self.D))]).astype(np.int64)
         return LoadRoute(perm, offs, dest, load, np.array([len(new), known], np.int64))

@@ -26,7 +26,8 @@ STATUS_NAMES = {0: "OK", 1: "ARG", 2: "LAYOUT", 3: "DUPLICATE", 4: "FANOUT", 5: 
 EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggregate",
            "alto_stream_state_bytes", "alto_stream_create", "alto_stream_step",
            "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join",
-           "alto_split_workspace_bytes", "alto_split")
+           "alto_split_workspace_bytes", "alto_split", "alto_router_state_bytes", "alto_router_create",
+           "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load")
 
 
 class Layout(C.Structure):
@@ -90,6 +91,16 @@ def load():
     lib.alto_join_workspace_bytes.argtypes = [C.POINTER(Layout), i64]
     lib.alto_join.restype = C.c_int
     lib.alto_join.argtypes = [vp, i64, vp, i64, C.POINTER(Layout), i32, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.alto_router_state_bytes.restype = C.c_size_t
+    lib.alto_router_state_bytes.argtypes = [i64]
+    lib.alto_router_create.restype = C.c_int
+    lib.alto_router_create.argtypes = [C.POINTER(Layout), i32, i32, i64, vp, C.c_size_t, vp, C.POINTER(C.c_void_p)]
+    lib.alto_router_destroy.restype = C.c_int
+    lib.alto_router_destroy.argtypes = [vp]
+    lib.alto_route_load_workspace_bytes.restype = C.c_size_t
+    lib.alto_route_load_workspace_bytes.argtypes = [i64, i32]
+    lib.alto_route_load.restype = C.c_int
+    lib.alto_route_load.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
     lib.alto_split_workspace_bytes.restype = C.c_size_t
     lib.alto_split_workspace_bytes.argtypes = [C.POINTER(Layout), i64]
     lib.alto_split.restype = C.c_int
@@ -316,6 +327,72 @@ class Stream:
     def close(self):
         if self.handle:
             self.lib.alto_stream_destroy(self.handle)
+            self.handle = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class LoadRouter:
+    """Sticky least-loaded routing of flows (route-level prefixes) over
+    caller-owned device memory; ``load`` (int64 [num_dest], device) holds the queue
+    lengths: route() adds the fragments it sends, the caller subtracts what each
+    destination has consumed."""
+
+    def __init__(self, bits, route_level, num_dest, max_flows, n_max, device="cuda", stream=None):
+        lib = load()
+        self.lib = lib
+        self.bits, self.Lr, self.D = tuple(bits), route_level, num_dest
+        self.L = layout(bits)
+        nbytes = lib.alto_router_state_bytes(max_flows)
+        if nbytes == 0:
+            raise AltoError(E_ARG, "alto_router_state_bytes")
+        self.state = torch.empty(int(nbytes), dtype=torch.uint8, device=device)
+        wsb = lib.alto_route_load_workspace_bytes(n_max, num_dest)
+        if wsb == 0:
+            raise AltoError(E_ARG, "alto_route_load_workspace_bytes")
+        self.ws = new_workspace(wsb, device)
+        self.n_max = n_max
+        self.max_flows = max_flows
+        self.handle = C.c_void_p()
+        self.reset(stream)
+
+    def reset(self, stream=None):
+        """(Re)creates the router on its state memory: every flow is forgotten."""
+        self.close()
+        rc = self.lib.alto_router_create(C.byref(self.L), self.Lr, self.D, self.max_flows, _p(self.state),
+                                         self.state.numel(), _stream(stream), C.byref(self.handle))
+        _check(rc, "alto_router_create")
+
+    def route(self, keys, load, perm=None, dest_offsets=None, dest=None, counts=None, status=None, stream=None,
+              n=None):
+        """Returns (perm, dest_offsets, dest, counts, status); ``load`` is updated in place."""
+        n = keys.shape[0] if n is None else n
+        if n > self.n_max:
+            raise AltoError(E_ARG, "batch larger than n_max")
+        dev = keys.device
+        m = max(n, 1)
+        if perm is None:
+            perm = torch.empty(m, dtype=torch.int32, device=dev)
+        if dest_offsets is None:
+            dest_offsets = torch.empty(self.D + 1, dtype=torch.int64, device=dev)
+        if dest is None:
+            dest = torch.empty(m, dtype=torch.int32, device=dev)
+        if counts is None:
+            counts = torch.zeros(2, dtype=torch.int64, device=dev)
+        if status is None:
+            status = new_status(dev)
+        rc = self.lib.alto_route_load(self.handle, _p(keys), n, _p(load), _p(perm), _p(dest_offsets), _p(dest),
+                                      _p(counts), _p(status), _p(self.ws), self.ws.numel(), _stream(stream))
+        _check(rc, "alto_route_load")
+        return perm, dest_offsets, dest, counts, status
+
+    def close(self):
+        if self.handle:
+            self.lib.alto_router_destroy(self.handle)
             self.handle = C.c_void_p()
 
     def __del__(self):

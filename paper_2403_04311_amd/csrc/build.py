@@ -6,7 +6,7 @@ from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
-SOURCES = ["sort.hip", "segment.hip", "aggregate.hip", "profile.hip", "stream.hip", "api.hip", "join.hip", "split.hip"]
+SOURCES = ["sort.hip", "segment.hip", "aggregate.hip", "profile.hip", "stream.hip", "api.hip", "join.hip", "split.hip", "loadroute.hip"]
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-Wall", "-Wno-unused-function",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

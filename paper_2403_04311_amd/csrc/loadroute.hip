@@ -1,0 +1,462 @@
+// Load-aware routing (Section 4.3: because elements are produced slowly, the
+// destination of a new flow of tags can be chosen by load instead of by a hash;
+// Section 5: the controller picks replicas by queue length). A flow is a distinct
+// route-level prefix. It keeps the destination it is first given (all fragments
+// with the same tags reach the same instance), held in a device flow table that
+// lives across calls. Per batch, the fragments of known flows join their queues
+// first; the new flows then go, in ascending prefix order, each to the shortest
+// queue (lowest index among ties), which grows by the flow's fragments.
+//
+// Steps: the keys are radix sorted; flow runs are found with a head-flag scan; run
+// heads look their prefix up in the table; known runs add their lengths to a
+// per-destination delta; the new runs are compacted in prefix order. One wave then
+// assigns the new flows in order: the queue lengths sit in LDS, each lane keeps the
+// minimum over the queues it owns (d = lane mod 64), and a wave reduction picks the
+// shortest queue per flow, so only the owner lane rescans after an update. The new
+// flows enter the table; destinations are written per sorted position, and a
+// stable sort by destination gives the (destination, key) order of perm.
+#include "sort.h"
+
+#include <limits.h>
+#include <string.h>
+
+#include <new>
+
+#define LR_MAX_DEST 4096
+#define LR_CHUNK 2048   // new flows staged in LDS per round of the assignment wave
+
+struct alto_router {
+  KeyGeom g;
+  int32_t route_level, num_dest;
+  int64_t max_flows, hcap;
+  uint64_t* tkey;    // [hcap] flow prefixes, ~0 = empty
+  int32_t* tdest;    // [hcap] their destinations
+  int64_t* nflows;   // flows stored
+};
+
+namespace {
+
+struct LrBufs {
+  uint64_t* skey;
+  uint32_t* sidx;
+  uint64_t* tmp_keys;
+  uint32_t* tmp_vals;
+  SortCtl* ctl;
+  uint32_t* os_status;
+  uint32_t* os_ctr;
+  uint32_t* os_hist;
+  int64_t os_ntiles;
+  uint32_t* hs;         // [n + 1] run heads before each sorted position
+  uint32_t* part;       // [SCAN_MAX_BLOCKS + 1]
+  uint32_t* run_start;  // [n] first sorted position of each run
+  int32_t* run_dest;    // [n] destination of each run (-1: new, until assigned)
+  uint32_t* nf;         // [n + 1] new-flow flag of each run, then their exclusive scan
+  uint32_t* new_run;    // [n] runs of the new flows, in prefix order
+  int64_t* delta;       // [D] fragments of known flows per destination
+  uint64_t* dkey;       // [n] destination of each sorted position
+  uint64_t* dsk;        // [n] the same, sorted
+  uint32_t* dval;       // [n] sorted position of each
+};
+
+void plan_lr(int64_t n_max, int D, WsCarver& c, LrBufs& b) {
+  const int64_t n = n_max < 1 ? 1 : n_max;
+  b.skey = c.take<uint64_t>(n);
+  b.sidx = c.take<uint32_t>(n);
+  b.tmp_keys = c.take<uint64_t>(n);
+  b.tmp_vals = c.take<uint32_t>(n);
+  b.ctl = c.take<SortCtl>(1);
+  b.os_ntiles = sort_tiles(n);
+  b.os_status = c.take<uint32_t>(2 * b.os_ntiles * SORT_BUCKETS);
+  b.os_ctr = c.take<uint32_t>(SORT_MAX_PASSES);
+  b.os_hist = c.take<uint32_t>((int64_t)SORT_MAX_PASSES * SORT_BUCKETS);
+  b.hs = c.take<uint32_t>(n + 1);
+  b.part = c.take<uint32_t>(SCAN_MAX_BLOCKS + 1);
+  b.run_start = c.take<uint32_t>(n);
+  b.run_dest = c.take<int32_t>(n);
+  b.nf = c.take<uint32_t>(n + 1);
+  b.new_run = c.take<uint32_t>(n);
+  b.delta = c.take<int64_t>(D);
+  b.dkey = c.take<uint64_t>(n);
+  b.dsk = c.take<uint64_t>(n);
+  b.dval = c.take<uint32_t>(n);
+}
+
+inline int grid_of(int64_t n, int nt = 256, int cap = 4096) {
+  int64_t b = cdiv(n < 1 ? 1 : n, nt);
+  return (int)(b < cap ? b : cap);
+}
+
+__device__ inline int read_status(const int32_t* st) {
+  return __hip_atomic_load(st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ inline uint64_t lr_hash(uint64_t p, int64_t hcap) {
+  return mix64(p ^ 0x5851F42D4C957F2Dull) & (uint64_t)(hcap - 1);
+}
+
+__global__ void k_lr_clear(uint64_t* tkey, int64_t hcap, int64_t* nflows) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < hcap; i += (int64_t)gridDim.x * blockDim.x)
+    tkey[i] = ~0ull;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *nflows = 0;
+}
+
+__global__ void k_lr_init(int64_t* counts, int64_t* delta, int D, uint32_t* hs_end, uint32_t* nf_end) {
+  for (int d = threadIdx.x; d < D; d += blockDim.x) delta[d] = 0;
+  if (threadIdx.x == 0) {
+    counts[0] = counts[1] = 0;
+    *hs_end = 0;
+    *nf_end = 0;
+  }
+}
+
+// Run heads (a new route prefix in sorted order); layout and duplicate checks.
+__global__ __launch_bounds__(256) void k_lr_heads(const uint64_t* __restrict__ skey, int64_t n, int total, int sh,
+                                                  uint32_t* __restrict__ hs, uint32_t* __restrict__ nf,
+                                                  int32_t* status) {
+  bool bad = false, dup = false;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t k = skey[j];
+    bad |= (k >> total) != 0;
+    bool head = true;
+    if (j > 0) {
+      const uint64_t kp = skey[j - 1];
+      dup |= kp == k;
+      head = key_prefix(k, sh) != key_prefix(kp, sh);
+    }
+    hs[j] = head ? 1u : 0u;
+    nf[j] = 0u;
+  }
+  if (bad) raise_status(status, ALTO_E_LAYOUT);
+  if (dup) raise_status(status, ALTO_E_DUPLICATE);
+}
+
+// Each run head looks its flow up in the table.
+__global__ __launch_bounds__(256) void k_lr_runs(const uint64_t* __restrict__ skey, int64_t n, int sh,
+                                                 const uint32_t* __restrict__ hs, const uint64_t* __restrict__ tkey,
+                                                 const int32_t* __restrict__ tdest, int64_t hcap,
+                                                 uint32_t* __restrict__ run_start, int32_t* __restrict__ run_dest,
+                                                 uint32_t* __restrict__ nf, int64_t* counts) {
+  __shared__ uint64_t s_n[256 / ALTO_WAVE];
+  uint64_t known = 0;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t r = hs[j];
+    if (hs[j + 1] == r) continue;   // not a head
+    run_start[r] = (uint32_t)j;
+    const uint64_t p = key_prefix(skey[j], sh);
+    uint64_t h = lr_hash(p, hcap);
+    int32_t d = -1;
+    for (int64_t probe = 0; probe < hcap; ++probe) {
+      const uint64_t v = tkey[h];
+      if (v == p) {
+        d = tdest[h];
+        break;
+      }
+      if (v == ~0ull) break;
+      h = (h + 1) & (uint64_t)(hcap - 1);
+    }
+    run_dest[r] = d;
+    nf[r] = d < 0 ? 1u : 0u;
+    known += d >= 0 ? 1 : 0;
+  }
+  const uint64_t v = wave_sum(known);
+  if (lane_id() == 0) s_n[threadIdx.x / ALTO_WAVE] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t t = 0;
+    for (int w = 0; w < 256 / ALTO_WAVE; ++w) t += s_n[w];
+    if (t) atomicAdd((unsigned long long*)&counts[1], (unsigned long long)t);
+  }
+}
+
+__device__ inline int64_t run_len(const uint32_t* run_start, uint32_t r, uint32_t R, int64_t n) {
+  return (r + 1 < R ? (int64_t)run_start[r + 1] : n) - (int64_t)run_start[r];
+}
+
+// Known runs add their fragments to their destination (through an LDS histogram);
+// new runs are listed in prefix order.
+__global__ __launch_bounds__(256) void k_lr_known(int64_t n, const uint32_t* __restrict__ hs,
+                                                  const uint32_t* __restrict__ run_start,
+                                                  const int32_t* __restrict__ run_dest, const uint32_t* __restrict__ nf,
+                                                  uint32_t* __restrict__ new_run, int64_t* delta, int D) {
+  __shared__ unsigned long long s_d[LR_MAX_DEST];
+  for (int d = threadIdx.x; d < D; d += blockDim.x) s_d[d] = 0ull;
+  __syncthreads();
+  const uint32_t R = hs[n];
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < R; r += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t d = run_dest[r];
+    if (d >= 0) {
+      if (d < D) atomicAdd(&s_d[d], (unsigned long long)run_len(run_start, (uint32_t)r, R, n));
+    } else {
+      new_run[nf[r]] = (uint32_t)r;
+    }
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < D; d += blockDim.x)
+    if (s_d[d]) atomicAdd((unsigned long long*)&delta[d], s_d[d]);
+}
+
+__device__ inline void lr_better(int64_t& v, int32_t& i, int64_t ov, int32_t oi) {
+  if (ov < v || (ov == v && oi < i)) {
+    v = ov;
+    i = oi;
+  }
+}
+
+// One wave: the new flows in prefix order, each to the shortest queue. Nothing
+// changes if this call has raised an error or the flows do not fit the table.
+__global__ __launch_bounds__(ALTO_WAVE) void k_lr_assign(int64_t n, const uint32_t* __restrict__ hs,
+                                                         const uint32_t* __restrict__ run_start,
+                                                         int32_t* __restrict__ run_dest,
+                                                         const uint32_t* __restrict__ nf,
+                                                         const uint32_t* __restrict__ new_run,
+                                                         const int64_t* __restrict__ delta, int64_t* load, int D,
+                                                         int64_t* nflows, int64_t max_flows, int64_t* counts,
+                                                         int32_t* status) {
+  __shared__ int64_t s_load[LR_MAX_DEST];
+  __shared__ int32_t s_len[LR_CHUNK];
+  __shared__ int32_t s_dst[LR_CHUNK];
+  const int lane = threadIdx.x;
+  if (read_status(status) != ALTO_OK) return;
+  const uint32_t R = hs[n];
+  const int64_t F = nf[n];
+  const int64_t stored = *nflows;
+  if (stored + F > max_flows) {
+    if (lane == 0) raise_status(status, ALTO_E_CAPACITY);
+    return;
+  }
+  for (int d = lane; d < D; d += ALTO_WAVE) s_load[d] = load[d] + delta[d];
+  // the lane's shortest queue among d = lane, lane + 64, ...
+  int64_t lv = INT64_MAX;
+  int32_t li = INT32_MAX;
+  for (int d = lane; d < D; d += ALTO_WAVE) lr_better(lv, li, s_load[d], d);
+  for (int64_t base = 0; base < F; base += LR_CHUNK) {
+    const int cnt = (int)(F - base < LR_CHUNK ? F - base : LR_CHUNK);
+    for (int k = lane; k < cnt; k += ALTO_WAVE) s_len[k] = (int32_t)run_len(run_start, new_run[base + k], R, n);
+    __syncthreads();
+    for (int k = 0; k < cnt; ++k) {
+      int64_t gv = lv;
+      int32_t gi = li;
+#pragma unroll
+      for (int o = ALTO_WAVE / 2; o > 0; o >>= 1) {
+        const int64_t ov = __shfl_xor(gv, o);
+        const int32_t oi = __shfl_xor(gi, o);
+        lr_better(gv, gi, ov, oi);
+      }
+      if (lane == 0) s_dst[k] = gi;
+      if (lane == (gi & (ALTO_WAVE - 1))) {
+        s_load[gi] += s_len[k];
+        lv = INT64_MAX;
+        li = INT32_MAX;
+        for (int d = lane; d < D; d += ALTO_WAVE) lr_better(lv, li, s_load[d], d);
+      }
+      __syncthreads();
+    }
+    for (int k = lane; k < cnt; k += ALTO_WAVE) run_dest[new_run[base + k]] = s_dst[k];
+    __syncthreads();
+  }
+  for (int d = lane; d < D; d += ALTO_WAVE) load[d] = s_load[d];
+  if (lane == 0) {
+    *nflows = stored + F;
+    counts[0] = F;
+  }
+}
+
+// The new flows enter the table (distinct prefixes: one run each).
+__global__ __launch_bounds__(256) void k_lr_insert(int64_t n, const uint32_t* __restrict__ nf,
+                                                   const uint32_t* __restrict__ new_run,
+                                                   const uint32_t* __restrict__ run_start,
+                                                   const int32_t* __restrict__ run_dest,
+                                                   const uint64_t* __restrict__ skey, int sh, uint64_t* tkey,
+                                                   int32_t* tdest, int64_t hcap, const int32_t* status) {
+  if (read_status(status) != ALTO_OK) return;
+  const int64_t F = nf[n];
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < F; k += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t r = new_run[k];
+    const uint64_t p = key_prefix(skey[run_start[r]], sh);
+    uint64_t h = lr_hash(p, hcap);
+    for (int64_t probe = 0; probe < hcap; ++probe) {
+      const uint64_t old = atomicCAS((unsigned long long*)&tkey[h], ~0ull, (unsigned long long)p);
+      if (old == ~0ull || old == p) {
+        tdest[h] = run_dest[r];
+        break;
+      }
+      h = (h + 1) & (uint64_t)(hcap - 1);
+    }
+  }
+}
+
+// Destination of every sorted position (and of every input fragment).
+__global__ __launch_bounds__(256) void k_lr_dest(int64_t n, const uint32_t* __restrict__ hs,
+                                                 const int32_t* __restrict__ run_dest,
+                                                 const uint32_t* __restrict__ sidx, int D, uint64_t* __restrict__ dkey,
+                                                 int32_t* __restrict__ dest) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+    int32_t d = run_dest[hs[j + 1] - 1];
+    d = (d < 0 || d >= D) ? 0 : d;   // only after an error (outputs undefined, accesses in bounds)
+    dkey[j] = (uint64_t)d;
+    if (dest) dest[sidx[j]] = d;
+  }
+}
+
+// perm in (destination, key) order and the destination offsets.
+__global__ __launch_bounds__(256) void k_lr_perm(int64_t n, const uint64_t* __restrict__ dsk,
+                                                 const uint32_t* __restrict__ dval, const uint32_t* __restrict__ sidx,
+                                                 int D, int32_t* __restrict__ perm, int64_t* __restrict__ offs) {
+  for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < n; m += (int64_t)gridDim.x * blockDim.x) {
+    if (perm) perm[m] = (int32_t)sidx[dval[m]];
+    if (!offs) continue;
+    const uint32_t d = (uint32_t)dsk[m];
+    if (m == 0) {
+      for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
+    } else {
+      const uint32_t dp = (uint32_t)dsk[m - 1];
+      for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = m;
+    }
+    if (m == n - 1)
+      for (uint32_t x = d + 1; x <= (uint32_t)D; ++x) offs[x] = n;
+  }
+}
+
+__global__ void k_lr_zero_offsets(int64_t* offs, int D) {
+  for (int d = threadIdx.x; d <= D; d += blockDim.x) offs[d] = 0;
+}
+
+bool lr_layout_ok(const alto_layout* l) {
+  if (!l || l->depth < 1 || l->depth > ALTO_MAX_LEVELS) return false;
+  int total = 0;
+  for (int i = 0; i < l->depth; ++i) {
+    if (l->bits[i] < 1 || l->bits[i] > 32) return false;
+    total += l->bits[i];
+  }
+  return total <= 63;
+}
+
+int64_t lr_hcap(int64_t max_flows) {
+  int64_t h = 64;
+  while (h < 2 * max_flows) h <<= 1;
+  return h;
+}
+
+const int64_t LR_N_LIMIT = (int64_t)INT_MAX - 1;
+const int64_t LR_FLOWS_LIMIT = (int64_t)1 << 30;
+
+}  // namespace
+
+extern "C" {
+
+size_t alto_router_state_bytes(int64_t max_flows) {
+  if (max_flows < 1 || max_flows > LR_FLOWS_LIMIT) return 0;
+  WsCarver c{nullptr, (size_t)-1, 0, true};
+  const int64_t h = lr_hcap(max_flows);
+  c.take<uint64_t>(h);
+  c.take<int32_t>(h);
+  c.take<int64_t>(1);
+  return c.off;
+}
+
+int alto_router_create(const alto_layout* layout, int32_t route_level, int32_t num_dest, int64_t max_flows,
+                       void* state, size_t state_bytes, hipStream_t stream, alto_router** out) {
+  if (!out || !lr_layout_ok(layout) || route_level < 1 || route_level > layout->depth || num_dest < 1 ||
+      num_dest > LR_MAX_DEST || max_flows < 1 || max_flows > LR_FLOWS_LIMIT || !state)
+    return ALTO_E_ARG;
+  const int64_t h = lr_hcap(max_flows);
+  WsCarver c{(char*)state, state_bytes, 0, true};
+  uint64_t* tkey = c.take<uint64_t>(h);
+  int32_t* tdest = c.take<int32_t>(h);
+  int64_t* nflows = c.take<int64_t>(1);
+  if (!c.ok) return ALTO_E_ARG;
+  alto_router* r = new (std::nothrow) alto_router;
+  if (!r) return ALTO_E_ARG;
+  r->g = make_geom(layout);
+  r->route_level = route_level;
+  r->num_dest = num_dest;
+  r->max_flows = max_flows;
+  r->hcap = h;
+  r->tkey = tkey;
+  r->tdest = tdest;
+  r->nflows = nflows;
+  k_lr_clear<<<grid_of(h), 256, 0, stream>>>(tkey, h, nflows);
+  if (hipGetLastError() != hipSuccess) {
+    delete r;
+    return ALTO_E_HIP;
+  }
+  *out = r;
+  return ALTO_OK;
+}
+
+int alto_router_destroy(alto_router* r) {
+  delete r;
+  return ALTO_OK;
+}
+
+size_t alto_route_load_workspace_bytes(int64_t n_max, int32_t num_dest) {
+  if (n_max < 0 || n_max > LR_N_LIMIT || num_dest < 1 || num_dest > LR_MAX_DEST) return 0;
+  WsCarver c{nullptr, (size_t)-1, 0, true};
+  LrBufs b;
+  plan_lr(n_max, num_dest, c, b);
+  return c.off;
+}
+
+int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* load, int32_t* perm,
+                    int64_t* dest_offsets, int32_t* dest, int64_t* counts, int32_t* status, void* ws,
+                    size_t ws_bytes, hipStream_t stream) {
+  if (!r || n < 0 || n > LR_N_LIMIT || !load || !counts || !status || !ws || (n > 0 && !keys)) return ALTO_E_ARG;
+  const int D = r->num_dest;
+  WsCarver c{(char*)ws, ws_bytes, 0, true};
+  LrBufs b;
+  plan_lr(n, D, c, b);
+  if (!c.ok) return ALTO_E_ARG;
+  k_lr_init<<<1, 256, 0, stream>>>(counts, b.delta, D, b.hs + n, b.nf + n);
+  if (n == 0) {
+    if (dest_offsets) k_lr_zero_offsets<<<1, 256, 0, stream>>>(dest_offsets, D);
+    ALTO_LAUNCH_CHECK();
+    return ALTO_OK;
+  }
+  const int total = r->g.total;
+  const int sh = r->g.shift[r->route_level];
+  SortBufs sb;
+  memset(&sb, 0, sizeof(sb));
+  sb.in_keys = keys;
+  sb.tmp_keys = b.tmp_keys;
+  sb.tmp_vals = b.tmp_vals;
+  sb.out_keys = b.skey;
+  sb.out_vals = b.sidx;
+  sb.ctl = b.ctl;
+  sb.os_status = b.os_status;
+  sb.os_ctr = b.os_ctr;
+  sb.os_hist = b.os_hist;
+  sb.os_ntiles = b.os_ntiles;
+  sb.status = status;
+  RouteGeom none;
+  none.shift = 64;
+  none.num_dest = 1;
+  int rc = sort_pairs(sb, n, nullptr, none, total, false, stream);
+  if (rc) return rc;
+  k_lr_heads<<<grid_of(n), 256, 0, stream>>>(b.skey, n, total, sh, b.hs, b.nf, status);
+  rc = scan_exclusive<uint32_t>(b.hs, b.hs, n + 1, nullptr, b.part, nullptr, stream);
+  if (rc) return rc;
+  k_lr_runs<<<grid_of(n), 256, 0, stream>>>(b.skey, n, sh, b.hs, r->tkey, r->tdest, r->hcap, b.run_start,
+                                            b.run_dest, b.nf, counts);
+  rc = scan_exclusive<uint32_t>(b.nf, b.nf, n + 1, nullptr, b.part, nullptr, stream);
+  if (rc) return rc;
+  k_lr_known<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta,
+                                                        D);
+  k_lr_assign<<<1, ALTO_WAVE, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta, load, D,
+                                           r->nflows, r->max_flows, counts, status);
+  k_lr_insert<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.nf, b.new_run, b.run_start, b.run_dest, b.skey, sh,
+                                                         r->tkey, r->tdest, r->hcap, status);
+  k_lr_dest<<<grid_of(n), 256, 0, stream>>>(n, b.hs, b.run_dest, b.sidx, D, b.dkey, dest);
+  if (perm || dest_offsets) {
+    SortBufs db = sb;
+    db.in_keys = b.dkey;
+    db.out_keys = b.dsk;
+    db.out_vals = b.dval;
+    rc = sort_pairs(db, n, nullptr, none, bits_for(D - 1), false, stream);
+    if (rc) return rc;
+    k_lr_perm<<<grid_of(n), 256, 0, stream>>>(n, b.dsk, b.dval, b.sidx, D, perm, dest_offsets);
+  }
+  ALTO_LAUNCH_CHECK();
+  return ALTO_OK;
+}
+
+}  // extern "C"
