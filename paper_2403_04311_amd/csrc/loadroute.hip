@@ -52,6 +52,7 @@ struct LrBufs {
   int32_t* run_dest;    // [n] destination of each run (-1: new, until assigned)
   uint32_t* nf;         // [n + 1] new-flow flag of each run, then their exclusive scan
   uint32_t* new_run;    // [n] runs of the new flows, in prefix order
+  int64_t* nrun1;       // runs + 1 (the length of the new-flow scan)
   int64_t* delta;       // [D] fragments of known flows per destination
   uint64_t* dkey;       // [n] destination of each sorted position
   uint64_t* dsk;        // [n] the same, sorted
@@ -75,6 +76,7 @@ void plan_lr(int64_t n_max, int D, WsCarver& c, LrBufs& b) {
   b.run_dest = c.take<int32_t>(n);
   b.nf = c.take<uint32_t>(n + 1);
   b.new_run = c.take<uint32_t>(n);
+  b.nrun1 = c.take<int64_t>(1);
   b.delta = c.take<int64_t>(D);
   b.dkey = c.take<uint64_t>(n);
   b.dsk = c.take<uint64_t>(n);
@@ -100,19 +102,17 @@ __global__ void k_lr_clear(uint64_t* tkey, int64_t hcap, int64_t* nflows) {
   if (blockIdx.x == 0 && threadIdx.x == 0) *nflows = 0;
 }
 
-__global__ void k_lr_init(int64_t* counts, int64_t* delta, int D, uint32_t* hs_end, uint32_t* nf_end) {
+__global__ void k_lr_init(int64_t* counts, int64_t* delta, int D, uint32_t* hs_end) {
   for (int d = threadIdx.x; d < D; d += blockDim.x) delta[d] = 0;
   if (threadIdx.x == 0) {
     counts[0] = counts[1] = 0;
     *hs_end = 0;
-    *nf_end = 0;
   }
 }
 
 // Run heads (a new route prefix in sorted order); layout and duplicate checks.
 __global__ __launch_bounds__(256) void k_lr_heads(const uint64_t* __restrict__ skey, int64_t n, int total, int sh,
-                                                  uint32_t* __restrict__ hs, uint32_t* __restrict__ nf,
-                                                  int32_t* status) {
+                                                  uint32_t* __restrict__ hs, int32_t* status) {
   bool bad = false, dup = false;
   for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t k = skey[j];
@@ -124,20 +124,25 @@ __global__ __launch_bounds__(256) void k_lr_heads(const uint64_t* __restrict__ s
       head = key_prefix(k, sh) != key_prefix(kp, sh);
     }
     hs[j] = head ? 1u : 0u;
-    nf[j] = 0u;
   }
   if (bad) raise_status(status, ALTO_E_LAYOUT);
   if (dup) raise_status(status, ALTO_E_DUPLICATE);
 }
 
-// Each run head looks its flow up in the table.
+// Each run head looks its flow up in the table; the new-flow flags of the R runs
+// (and a zero at R) are written for a scan of R + 1 entries.
 __global__ __launch_bounds__(256) void k_lr_runs(const uint64_t* __restrict__ skey, int64_t n, int sh,
                                                  const uint32_t* __restrict__ hs, const uint64_t* __restrict__ tkey,
                                                  const int32_t* __restrict__ tdest, int64_t hcap,
                                                  uint32_t* __restrict__ run_start, int32_t* __restrict__ run_dest,
-                                                 uint32_t* __restrict__ nf, int64_t* counts) {
+                                                 uint32_t* __restrict__ nf, int64_t* nrun1, int64_t* counts) {
   __shared__ uint64_t s_n[256 / ALTO_WAVE];
   uint64_t known = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    const uint32_t R = hs[n];
+    nf[R] = 0u;
+    *nrun1 = (int64_t)R + 1;
+  }
   for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t r = hs[j];
     if (hs[j + 1] == r) continue;   // not a head
@@ -218,7 +223,7 @@ __global__ __launch_bounds__(ALTO_WAVE) void k_lr_assign(int64_t n, const uint32
   const int lane = threadIdx.x;
   if (read_status(status) != ALTO_OK) return;
   const uint32_t R = hs[n];
-  const int64_t F = nf[n];
+  const int64_t F = nf[R];
   const int64_t stored = *nflows;
   if (stored + F > max_flows) {
     if (lane == 0) raise_status(status, ALTO_E_CAPACITY);
@@ -262,14 +267,15 @@ __global__ __launch_bounds__(ALTO_WAVE) void k_lr_assign(int64_t n, const uint32
 }
 
 // The new flows enter the table (distinct prefixes: one run each).
-__global__ __launch_bounds__(256) void k_lr_insert(int64_t n, const uint32_t* __restrict__ nf,
+__global__ __launch_bounds__(256) void k_lr_insert(int64_t n, const uint32_t* __restrict__ hs,
+                                                   const uint32_t* __restrict__ nf,
                                                    const uint32_t* __restrict__ new_run,
                                                    const uint32_t* __restrict__ run_start,
                                                    const int32_t* __restrict__ run_dest,
                                                    const uint64_t* __restrict__ skey, int sh, uint64_t* tkey,
                                                    int32_t* tdest, int64_t hcap, const int32_t* status) {
   if (read_status(status) != ALTO_OK) return;
-  const int64_t F = nf[n];
+  const int64_t F = nf[hs[n]];
   for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < F; k += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t r = new_run[k];
     const uint64_t p = key_prefix(skey[run_start[r]], sh);
@@ -285,16 +291,63 @@ __global__ __launch_bounds__(256) void k_lr_insert(int64_t n, const uint32_t* __
   }
 }
 
-// Destination of every sorted position (and of every input fragment).
+// Destination of every sorted position (the key of the destination sort).
 __global__ __launch_bounds__(256) void k_lr_dest(int64_t n, const uint32_t* __restrict__ hs,
-                                                 const int32_t* __restrict__ run_dest,
-                                                 const uint32_t* __restrict__ sidx, int D, uint64_t* __restrict__ dkey,
-                                                 int32_t* __restrict__ dest) {
+                                                 const int32_t* __restrict__ run_dest, int D,
+                                                 uint64_t* __restrict__ dkey) {
   for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
     int32_t d = run_dest[hs[j + 1] - 1];
     d = (d < 0 || d >= D) ? 0 : d;   // only after an error (outputs undefined, accesses in bounds)
     dkey[j] = (uint64_t)d;
-    if (dest) dest[sidx[j]] = d;
+  }
+}
+
+// Destination of every input fragment, looked up in input order (coalesced reads
+// and writes; the table of a batch's flows stays in the caches). LU lookups per
+// thread are in flight together: a probe is a dependent load.
+constexpr int LU = 4;
+
+__global__ __launch_bounds__(256) void k_lr_dest_in(const uint64_t* __restrict__ keys, int64_t n, int sh,
+                                                    const uint64_t* __restrict__ tkey,
+                                                    const int32_t* __restrict__ tdest, int64_t hcap,
+                                                    int32_t* __restrict__ dest) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const uint64_t mask = (uint64_t)(hcap - 1);
+  for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += stride * LU) {
+    uint64_t p[LU], h[LU];
+    int64_t slot[LU];
+    bool done[LU];
+#pragma unroll
+    for (int u = 0; u < LU; ++u) {
+      const int64_t i = i0 + u * stride;
+      p[u] = i < n ? key_prefix(keys[i], sh) : 0ull;
+      h[u] = lr_hash(p[u], hcap);
+      slot[u] = -1;   // a flow missing from the table only after an error
+      done[u] = i >= n;
+    }
+    for (int64_t probe = 0; probe < hcap; ++probe) {
+      bool all = true;
+#pragma unroll
+      for (int u = 0; u < LU; ++u) {
+        if (done[u]) continue;
+        const uint64_t v = tkey[h[u]];
+        if (v == p[u]) {
+          slot[u] = (int64_t)h[u];
+          done[u] = true;
+        } else if (v == ~0ull) {
+          done[u] = true;
+        } else {
+          h[u] = (h[u] + 1) & mask;
+        }
+        all = all && done[u];
+      }
+      if (all) break;
+    }
+#pragma unroll
+    for (int u = 0; u < LU; ++u) {
+      const int64_t i = i0 + u * stride;
+      if (i < n) dest[i] = slot[u] >= 0 ? tdest[slot[u]] : 0;
+    }
   }
 }
 
@@ -406,7 +459,7 @@ int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* lo
   LrBufs b;
   plan_lr(n, D, c, b);
   if (!c.ok) return ALTO_E_ARG;
-  k_lr_init<<<1, 256, 0, stream>>>(counts, b.delta, D, b.hs + n, b.nf + n);
+  k_lr_init<<<1, 256, 0, stream>>>(counts, b.delta, D, b.hs + n);
   if (n == 0) {
     if (dest_offsets) k_lr_zero_offsets<<<1, 256, 0, stream>>>(dest_offsets, D);
     ALTO_LAUNCH_CHECK();
@@ -432,21 +485,23 @@ int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* lo
   none.num_dest = 1;
   int rc = sort_pairs(sb, n, nullptr, none, total, false, stream);
   if (rc) return rc;
-  k_lr_heads<<<grid_of(n), 256, 0, stream>>>(b.skey, n, total, sh, b.hs, b.nf, status);
+  k_lr_heads<<<grid_of(n), 256, 0, stream>>>(b.skey, n, total, sh, b.hs, status);
   rc = scan_exclusive<uint32_t>(b.hs, b.hs, n + 1, nullptr, b.part, nullptr, stream);
   if (rc) return rc;
   k_lr_runs<<<grid_of(n), 256, 0, stream>>>(b.skey, n, sh, b.hs, r->tkey, r->tdest, r->hcap, b.run_start,
-                                            b.run_dest, b.nf, counts);
-  rc = scan_exclusive<uint32_t>(b.nf, b.nf, n + 1, nullptr, b.part, nullptr, stream);
+                                            b.run_dest, b.nf, b.nrun1, counts);
+  rc = scan_exclusive<uint32_t>(b.nf, b.nf, n + 1, b.nrun1, b.part, nullptr, stream);
   if (rc) return rc;
   k_lr_known<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta,
                                                         D);
   k_lr_assign<<<1, ALTO_WAVE, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta, load, D,
                                            r->nflows, r->max_flows, counts, status);
-  k_lr_insert<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.nf, b.new_run, b.run_start, b.run_dest, b.skey, sh,
+  k_lr_insert<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.nf, b.new_run, b.run_start, b.run_dest, b.skey, sh,
                                                          r->tkey, r->tdest, r->hcap, status);
-  k_lr_dest<<<grid_of(n), 256, 0, stream>>>(n, b.hs, b.run_dest, b.sidx, D, b.dkey, dest);
+  if (dest)
+    k_lr_dest_in<<<grid_of(n, 256 * LU), 256, 0, stream>>>(keys, n, sh, r->tkey, r->tdest, r->hcap, dest);
   if (perm || dest_offsets) {
+    k_lr_dest<<<grid_of(n), 256, 0, stream>>>(n, b.hs, b.run_dest, D, b.dkey);
     SortBufs db = sb;
     db.in_keys = b.dkey;
     db.out_keys = b.dsk;
