@@ -309,6 +309,11 @@ int alto_split(const uint64_t *keys, const int32_t *fan, int64_t fan_ld, const i
  * milliseconds and the number of records per phase (arrays of nphase entries),
  * and destroys the pool. Host-side only; not thread-safe. */
 int alto_profile_begin(int32_t max_records);
+
+/* Selects the phases recorded by the next alto_profile_begin (bit p = phase p;
+ * default: all). Fewer event pairs per call disturb the timed calls less. Not
+ * while a pool is active (ALTO_E_ARG). */
+int alto_profile_phases(uint32_t mask);
 int alto_profile_end(float *ms, int32_t *calls, int32_t nphase);
 
 #ifdef __cplusplus

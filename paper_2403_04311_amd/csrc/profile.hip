@@ -9,13 +9,14 @@ struct Rec {
   hipEvent_t a, b;
 };
 bool g_on = false;
+uint32_t g_mask = ~0u;   // phases recorded
 std::vector<Rec> g_recs;
 size_t g_used = 0;
 int g_open[PH_COUNT];
 }  // namespace
 
 void prof_begin(int phase, hipStream_t st) {
-  if (!g_on || g_used >= g_recs.size()) {
+  if (!g_on || g_used >= g_recs.size() || !((g_mask >> phase) & 1u)) {
     g_open[phase] = -1;
     return;
   }
@@ -32,6 +33,12 @@ void prof_end(int phase, hipStream_t st) {
 }
 
 extern "C" {
+
+int alto_profile_phases(uint32_t mask) {
+  if (g_on) return ALTO_E_ARG;
+  g_mask = mask;
+  return ALTO_OK;
+}
 
 int alto_profile_begin(int32_t max_records) {
   if (g_on || max_records < 1) return ALTO_E_ARG;
