@@ -126,8 +126,10 @@ struct AggBufs {
 };
 
 void agg_levels(const KeyGeom& g, int La, int Lm, int Lr, int* Lt, int* Lseg);
+// flow_cap: flows of the route level ranked for the packed sort (more flows fall back
+// to the general sort)
 void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const alto_agg* agg, int Lr, WsCarver& c,
-                  AggBufs& b);
+                  AggBufs& b, int64_t flow_cap = FLOW_CAP);
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
               int32_t* status, hipStream_t st, bool offsets_later = false, bool exact_flow_levels = false);

@@ -802,7 +802,7 @@ void agg_levels(const KeyGeom& g, int La, int Lm, int Lr, int* Lt, int* Lseg) {
 }
 
 void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const alto_agg* agg, int Lr, WsCarver& c,
-                  AggBufs& b) {
+                  AggBufs& b, int64_t flow_cap) {
   memset(&b, 0, sizeof(b));
   const int64_t n = n_max < 1 ? 1 : n_max;
   b.ctl = c.take<SortCtl>(1);
@@ -826,7 +826,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   if (n_max > SORT_SMALL_MAX && Lr >= 1) {
     // flows of the route level, ranked in (dest, prefix) order (packed sort)
     FlowBufs& f = b.fl;
-    f.fcap = n < FLOW_CAP ? n : FLOW_CAP;
+    f.fcap = n < flow_cap ? n : flow_cap;
     int64_t h = 1024;
     while (h < 2 * f.fcap) h <<= 1;
     f.hcap = h;

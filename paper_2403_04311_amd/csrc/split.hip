@@ -7,8 +7,10 @@
 // of the two new levels. A parent is split only when all of its declared tokens
 // are present, since a missing token could be a delimiter.
 //
-// Steps: the keys are radix sorted, which puts each parent's tokens next to each
-// other in index order. A marking pass over LDS tiles of the sorted order checks
+// Steps: the keys are sorted the way alto_route sorts them, with the parents as the
+// flows of the route level and one destination (the parents are ranked in prefix
+// order and (rank, position, index) words sort in a few passes over the bits that
+// vary); this puts each parent's tokens next to each other in index order. A marking pass over LDS tiles of the sorted order checks
 // the keys and decides per token, with two reads, whether its parent is complete:
 // a run of distinct indices below P that holds index 0 at its start and index P-1
 // P-1 places later holds every index. It flags segment starts and ends; one
@@ -18,6 +20,7 @@
 // (which is new-key order), every access coalesced. The sorted order is never
 // scattered back to the input order: the caller gets the input index of each new
 // fragment instead, as alto_route's perm.
+#include "aggregate.h"
 #include "sort.h"
 
 #include <limits.h>
@@ -26,6 +29,7 @@
 namespace {
 
 #define SPLIT_NT 256
+#define SPLIT_FLOW_CAP (1 << 16)   // parents ranked for the packed sort (more: general sort)
 #define SPLIT_IT 4
 #define SPLIT_TILE (SPLIT_NT * SPLIT_IT)
 
@@ -38,15 +42,7 @@ enum : uint8_t {
 };
 
 struct SplitBufs {
-  uint64_t* skey;      // [n] sorted keys
-  uint32_t* sidx;      // [n] input index of each
-  uint64_t* tmp_keys;  // [n] sort scratch
-  uint32_t* tmp_vals;
-  SortCtl* ctl;
-  uint32_t* os_status;
-  uint32_t* os_ctr;
-  uint32_t* os_hist;
-  int64_t os_ntiles;
+  AggBufs ab;          // the routing sort: ab.sk sorted keys, ab.perm input index of each
   uint8_t* sflag;      // [n] SF_* of each sorted position
   int32_t* stok;       // [n] token of each sorted position
   int32_t* sfan;       // [n] declared token count of its parent
@@ -59,17 +55,10 @@ struct SplitBufs {
   uint32_t* send;      // [n] ... and of its last
 };
 
-void plan_split(int64_t n_max, WsCarver& c, SplitBufs& b) {
+void plan_split(const KeyGeom& g, int64_t n_max, WsCarver& c, SplitBufs& b) {
   const int64_t n = n_max < 1 ? 1 : n_max;
-  b.skey = c.take<uint64_t>(n);
-  b.sidx = c.take<uint32_t>(n);
-  b.tmp_keys = c.take<uint64_t>(n);
-  b.tmp_vals = c.take<uint32_t>(n);
-  b.ctl = c.take<SortCtl>(1);
-  b.os_ntiles = sort_tiles(n);
-  b.os_status = c.take<uint32_t>(2 * b.os_ntiles * SORT_BUCKETS);
-  b.os_ctr = c.take<uint32_t>(SORT_MAX_PASSES);
-  b.os_hist = c.take<uint32_t>((int64_t)SORT_MAX_PASSES * SORT_BUCKETS);
+  const RouteGeom rg = make_route(g, g.depth - 1, 1);
+  plan_buffers(g, n, rg, nullptr, g.depth - 1, c, b.ab, SPLIT_FLOW_CAP);
   b.sflag = c.take<uint8_t>(n);
   b.stok = c.take<int32_t>(n);
   b.sfan = c.take<int32_t>(n);
@@ -305,7 +294,7 @@ size_t alto_split_workspace_bytes(const alto_layout* layout, int64_t n_max) {
   if (!split_layout_ok(layout, 1, 1) || n_max < 0 || n_max > SPLIT_N_LIMIT) return 0;
   WsCarver c{nullptr, (size_t)-1, 0, true};
   SplitBufs b;
-  plan_split(n_max, c, b);
+  plan_split(make_geom(layout), n_max, c, b);
   return c.off;
 }
 
@@ -321,42 +310,29 @@ int alto_split(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const i
   const int d = layout->depth;
   WsCarver c{(char*)ws, ws_bytes, 0, true};
   SplitBufs b;
-  plan_split(n, c, b);
+  plan_split(g, n, c, b);
   if (!c.ok) return ALTO_E_ARG;
   k_split_init<<<1, 64, 0, stream>>>(counts, b.cpl + n, b.cinc + n);
   if (n == 0) {
     ALTO_LAUNCH_CHECK();
     return ALTO_OK;
   }
-  SortBufs sb;
-  memset(&sb, 0, sizeof(sb));
-  sb.in_keys = keys;
-  sb.tmp_keys = b.tmp_keys;
-  sb.tmp_vals = b.tmp_vals;
-  sb.out_keys = b.skey;
-  sb.out_vals = b.sidx;
-  sb.ctl = b.ctl;
-  sb.os_status = b.os_status;
-  sb.os_ctr = b.os_ctr;
-  sb.os_hist = b.os_hist;
-  sb.os_ntiles = b.os_ntiles;
-  sb.status = status;
-  RouteGeom none;
-  none.shift = 64;
-  none.num_dest = 1;
-  int rc = sort_pairs(sb, n, nullptr, none, g.total, false, stream);
+  const RouteGeom rg = make_route(g, d - 1, 1);
+  int rc = route_run(g, rg, keys, n, b.ab, nullptr, nullptr, nullptr, nullptr, 0, 1, 0, status, stream);
   if (rc) return rc;
+  const uint64_t* skey = b.ab.sk;
+  const uint32_t* sidx = b.ab.perm;
   const int tbits = layout->bits[d - 1];
   const int mgrid = (int)(cdiv(n, SPLIT_TILE) < 2048 ? cdiv(n, SPLIT_TILE) : 2048);
   k_split_pair<<<grid_of(n), 256, 0, stream>>>(tokens, fan + (int64_t)(d - 2) * fan_ld, n, b.tf);
-  k_split_mark<<<mgrid, SPLIT_NT, 0, stream>>>(b.skey, b.sidx, b.tf, n, g.total,
+  k_split_mark<<<mgrid, SPLIT_NT, 0, stream>>>(skey, sidx, b.tf, n, g.total,
                                                tbits, delim, b.sflag, b.stok, b.sfan, b.cpl, rest_idx ? b.cinc : nullptr,
                                                counts, status);
   rc = scan_exclusive<int64_t>(b.cpl, b.cpl, n + 1, nullptr, b.part, nullptr, stream);
   if (!rc && rest_idx) rc = scan_exclusive<uint32_t>(b.cinc, b.cinc, n + 1, nullptr, b.part32, nullptr, stream);
   if (rc) return rc;
   k_split_bounds<<<grid_of(n), 256, 0, stream>>>(b.sflag, b.cpl, n, b.sbeg, b.send);
-  k_split_emit<<<grid_of(n), 256, 0, stream>>>(b.skey, b.sidx, b.sflag, b.stok, b.sfan, b.cpl, b.cinc, b.sbeg, b.send, fan,
+  k_split_emit<<<grid_of(n), 256, 0, stream>>>(skey, sidx, b.sflag, b.stok, b.sfan, b.cpl, b.cinc, b.sbeg, b.send, fan,
                                                fan_ld, d - 1, n, tbits, seg_bits, tok_bits, out_keys, out_fan,
                                                out_fan_ld, out_tokens, out_idx, rest_idx, status);
   ALTO_LAUNCH_CHECK();
