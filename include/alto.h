@@ -243,8 +243,10 @@ int alto_router_create(const alto_layout *layout, int32_t route_level, int32_t n
 /* Frees the host handle (the caller frees the state memory). */
 int alto_router_destroy(alto_router *r);
 
-/* Workspace bytes for alto_route_load with up to n_max fragments. */
-size_t alto_route_load_workspace_bytes(int64_t n_max, int32_t num_dest);
+/* Workspace bytes for alto_route_load with up to n_max fragments (layout and
+ * route_level as given to alto_router_create). */
+size_t alto_route_load_workspace_bytes(const alto_layout *layout, int32_t route_level, int64_t n_max,
+                                       int32_t num_dest);
 
 /* Routes one batch. load: device int64[num_dest], the destinations' queue lengths,
  * updated in place (the caller subtracts what a destination has consumed between

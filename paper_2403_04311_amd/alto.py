@@ -98,7 +98,7 @@ def load():
     lib.alto_router_destroy.restype = C.c_int
     lib.alto_router_destroy.argtypes = [vp]
     lib.alto_route_load_workspace_bytes.restype = C.c_size_t
-    lib.alto_route_load_workspace_bytes.argtypes = [i64, i32]
+    lib.alto_route_load_workspace_bytes.argtypes = [C.POINTER(Layout), i32, i64, i32]
     lib.alto_route_load.restype = C.c_int
     lib.alto_route_load.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
     lib.alto_split_workspace_bytes.restype = C.c_size_t
@@ -351,7 +351,7 @@ class LoadRouter:
         if nbytes == 0:
             raise AltoError(E_ARG, "alto_router_state_bytes")
         self.state = torch.empty(int(nbytes), dtype=torch.uint8, device=device)
-        wsb = lib.alto_route_load_workspace_bytes(n_max, num_dest)
+        wsb = lib.alto_route_load_workspace_bytes(C.byref(self.L), route_level, n_max, num_dest)
         if wsb == 0:
             raise AltoError(E_ARG, "alto_route_load_workspace_bytes")
         self.ws = new_workspace(wsb, device)

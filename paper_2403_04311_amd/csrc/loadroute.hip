@@ -7,14 +7,20 @@
 // first; the new flows then go, in ascending prefix order, each to the shortest
 // queue (lowest index among ties), which grows by the flow's fragments.
 //
-// Steps: the keys are radix sorted; flow runs are found with a head-flag scan; run
+// Steps: the keys are sorted by the routing sort of alto_route with one destination
+// (the flows ranked in prefix order, packed words); flow runs are found with a
+// head-flag scan; run
 // heads look their prefix up in the table; known runs add their lengths to a
 // per-destination delta; the new runs are compacted in prefix order. One wave then
 // assigns the new flows in order: the queue lengths sit in LDS, each lane keeps the
 // minimum over the queues it owns (d = lane mod 64), and a wave reduction picks the
 // shortest queue per flow, so only the owner lane rescans after an update. The new
-// flows enter the table; destinations are written per sorted position, and a
-// stable sort by destination gives the (destination, key) order of perm.
+// flows enter the table. A flow's fragments share its destination and form one run
+// of the key order, so the (destination, key) order of perm only needs the runs
+// sorted by (destination, prefix) (a small sort) and a segmented copy of each run
+// to its offset; the input-order destinations are looked up in a table of the
+// batch's flows built in LDS.
+#include "aggregate.h"
 #include "sort.h"
 
 #include <limits.h>
@@ -37,50 +43,47 @@ struct alto_router {
 namespace {
 
 struct LrBufs {
-  uint64_t* skey;
-  uint32_t* sidx;
-  uint64_t* tmp_keys;
-  uint32_t* tmp_vals;
-  SortCtl* ctl;
-  uint32_t* os_status;
-  uint32_t* os_ctr;
-  uint32_t* os_hist;
-  int64_t os_ntiles;
+  AggBufs ab;           // the key sort: ab.sk sorted keys, ab.perm input index of each;
+                        // its scratch serves the destination sort afterwards
   uint32_t* hs;         // [n + 1] run heads before each sorted position
   uint32_t* part;       // [SCAN_MAX_BLOCKS + 1]
   uint32_t* run_start;  // [n] first sorted position of each run
+  uint64_t* run_pfx;    // [n] flow prefix of each run
+  int32_t* rank;        // [n] flow rank of every input element (packed routing sort)
   int32_t* run_dest;    // [n] destination of each run (-1: new, until assigned)
   uint32_t* nf;         // [n + 1] new-flow flag of each run, then their exclusive scan
   uint32_t* new_run;    // [n] runs of the new flows, in prefix order
   int64_t* nrun1;       // runs + 1 (the length of the new-flow scan)
+  int64_t* nrun;        // runs (device count of the run sort)
   int64_t* delta;       // [D] fragments of known flows per destination
-  uint64_t* dkey;       // [n] destination of each sorted position
-  uint64_t* dsk;        // [n] the same, sorted
-  uint32_t* dval;       // [n] sorted position of each
+  uint64_t* rkey;       // [n] (destination << 32 | run) of each run
+  uint64_t* rsk;        // [n] the same, sorted
+  uint32_t* rval;       // [n] run of each sorted entry
+  int64_t* roff;        // [n + 1] output offset of each run (scan in sorted-run order)
+  int64_t* rpart;       // [SCAN_MAX_BLOCKS + 1]
+  int64_t* rbase;       // [n] output offset by run index
 };
 
-void plan_lr(int64_t n_max, int D, WsCarver& c, LrBufs& b) {
+void plan_lr(const KeyGeom& g, int Lr, int64_t n_max, int D, WsCarver& c, LrBufs& b) {
   const int64_t n = n_max < 1 ? 1 : n_max;
-  b.skey = c.take<uint64_t>(n);
-  b.sidx = c.take<uint32_t>(n);
-  b.tmp_keys = c.take<uint64_t>(n);
-  b.tmp_vals = c.take<uint32_t>(n);
-  b.ctl = c.take<SortCtl>(1);
-  b.os_ntiles = sort_tiles(n);
-  b.os_status = c.take<uint32_t>(2 * b.os_ntiles * SORT_BUCKETS);
-  b.os_ctr = c.take<uint32_t>(SORT_MAX_PASSES);
-  b.os_hist = c.take<uint32_t>((int64_t)SORT_MAX_PASSES * SORT_BUCKETS);
+  plan_buffers(g, n, make_route(g, Lr, 1), nullptr, Lr, c, b.ab);
   b.hs = c.take<uint32_t>(n + 1);
   b.part = c.take<uint32_t>(SCAN_MAX_BLOCKS + 1);
   b.run_start = c.take<uint32_t>(n);
+  b.run_pfx = c.take<uint64_t>(n);
+  b.rank = c.take<int32_t>(n);
   b.run_dest = c.take<int32_t>(n);
   b.nf = c.take<uint32_t>(n + 1);
   b.new_run = c.take<uint32_t>(n);
   b.nrun1 = c.take<int64_t>(1);
+  b.nrun = c.take<int64_t>(1);
   b.delta = c.take<int64_t>(D);
-  b.dkey = c.take<uint64_t>(n);
-  b.dsk = c.take<uint64_t>(n);
-  b.dval = c.take<uint32_t>(n);
+  b.rkey = c.take<uint64_t>(n);
+  b.rsk = c.take<uint64_t>(n);
+  b.rval = c.take<uint32_t>(n);
+  b.roff = c.take<int64_t>(n + 1);
+  b.rpart = c.take<int64_t>(SCAN_MAX_BLOCKS + 1);
+  b.rbase = c.take<int64_t>(n);
 }
 
 inline int grid_of(int64_t n, int nt = 256, int cap = 4096) {
@@ -134,20 +137,23 @@ __global__ __launch_bounds__(256) void k_lr_heads(const uint64_t* __restrict__ s
 __global__ __launch_bounds__(256) void k_lr_runs(const uint64_t* __restrict__ skey, int64_t n, int sh,
                                                  const uint32_t* __restrict__ hs, const uint64_t* __restrict__ tkey,
                                                  const int32_t* __restrict__ tdest, int64_t hcap,
-                                                 uint32_t* __restrict__ run_start, int32_t* __restrict__ run_dest,
-                                                 uint32_t* __restrict__ nf, int64_t* nrun1, int64_t* counts) {
+                                                 uint32_t* __restrict__ run_start, uint64_t* __restrict__ run_pfx,
+                                                 int32_t* __restrict__ run_dest, uint32_t* __restrict__ nf,
+                                                 int64_t* nrun1, int64_t* nrun, int64_t* counts) {
   __shared__ uint64_t s_n[256 / ALTO_WAVE];
   uint64_t known = 0;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     const uint32_t R = hs[n];
     nf[R] = 0u;
     *nrun1 = (int64_t)R + 1;
+    *nrun = (int64_t)R;
   }
   for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t r = hs[j];
     if (hs[j + 1] == r) continue;   // not a head
     run_start[r] = (uint32_t)j;
     const uint64_t p = key_prefix(skey[j], sh);
+    run_pfx[r] = p;
     uint64_t h = lr_hash(p, hcap);
     int32_t d = -1;
     for (int64_t probe = 0; probe < hcap; ++probe) {
@@ -291,48 +297,103 @@ __global__ __launch_bounds__(256) void k_lr_insert(int64_t n, const uint32_t* __
   }
 }
 
-// Destination of every sorted position (the key of the destination sort).
-__global__ __launch_bounds__(256) void k_lr_dest(int64_t n, const uint32_t* __restrict__ hs,
-                                                 const int32_t* __restrict__ run_dest, int D,
-                                                 uint64_t* __restrict__ dkey) {
-  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
-    int32_t d = run_dest[hs[j + 1] - 1];
+// Sort key of every run: (destination, run), the run index being prefix order.
+__global__ __launch_bounds__(256) void k_lr_runkeys(const int64_t* __restrict__ nrun,
+                                                    const int32_t* __restrict__ run_dest, int D,
+                                                    uint64_t* __restrict__ rkey) {
+  const int64_t R = *nrun;
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < R; r += (int64_t)gridDim.x * blockDim.x) {
+    int32_t d = run_dest[r];
     d = (d < 0 || d >= D) ? 0 : d;   // only after an error (outputs undefined, accesses in bounds)
-    dkey[j] = (uint64_t)d;
+    rkey[r] = ((uint64_t)d << 32) | (uint64_t)r;
   }
 }
 
-// Destination of every input fragment, looked up in input order (coalesced reads
-// and writes; the table of a batch's flows stays in the caches). LU lookups per
-// thread are in flight together: a probe is a dependent load.
-constexpr int LU = 4;
+// Fragments of each run in sorted-run order (the input of the offset scan).
+__global__ __launch_bounds__(256) void k_lr_runlen(int64_t n, const int64_t* __restrict__ nrun,
+                                                   const uint32_t* __restrict__ rval,
+                                                   const uint32_t* __restrict__ run_start,
+                                                   int64_t* __restrict__ roff) {
+  const int64_t R = *nrun;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q <= R; q += (int64_t)gridDim.x * blockDim.x)
+    roff[q] = q < R ? run_len(run_start, rval[q], (uint32_t)R, n) : 0;
+}
 
-__global__ __launch_bounds__(256) void k_lr_dest_in(const uint64_t* __restrict__ keys, int64_t n, int sh,
-                                                    const uint64_t* __restrict__ tkey,
-                                                    const int32_t* __restrict__ tdest, int64_t hcap,
-                                                    int32_t* __restrict__ dest) {
+// Output offset by run index, and the destination offsets (from the first run of
+// every destination in sorted-run order).
+__global__ __launch_bounds__(256) void k_lr_runoff(int64_t n, const int64_t* __restrict__ nrun,
+                                                   const uint64_t* __restrict__ rsk,
+                                                   const uint32_t* __restrict__ rval,
+                                                   const int64_t* __restrict__ roff, int D,
+                                                   int64_t* __restrict__ rbase, int64_t* __restrict__ offs) {
+  const int64_t R = *nrun;
+  for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < R; q += (int64_t)gridDim.x * blockDim.x) {
+    rbase[rval[q]] = roff[q];
+    if (!offs) continue;
+    const uint32_t d = (uint32_t)(rsk[q] >> 32);
+    if (q == 0) {
+      for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
+    } else {
+      const uint32_t dp = (uint32_t)(rsk[q - 1] >> 32);
+      for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = roff[q];
+    }
+    if (q == R - 1)
+      for (uint32_t x = d + 1; x <= (uint32_t)D; ++x) offs[x] = n;
+  }
+}
+
+// perm: every run copied to its offset (reads and writes contiguous within runs).
+__global__ __launch_bounds__(256) void k_lr_copy(int64_t n, const uint32_t* __restrict__ hs,
+                                                 const uint32_t* __restrict__ run_start,
+                                                 const int64_t* __restrict__ rbase,
+                                                 const uint32_t* __restrict__ sidx, int32_t* __restrict__ perm) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t r = hs[j + 1] - 1;
+    int64_t o = rbase[r] + (j - (int64_t)run_start[r]);
+    o = o < 0 ? 0 : (o >= n ? n - 1 : o);   // in bounds whatever an error left behind
+    perm[o] = (int32_t)sidx[j];
+  }
+}
+
+// Destination of every input fragment, in input order (coalesced reads and
+// writes), when the key sort did not run packed (then k_lr_dest_rank below has it
+// from the flow ranks). With at most LR_LDS_FLOWS runs, every block first builds an
+// open-addressing table of the batch's flows in LDS from the runs (prefix, run
+// destination); otherwise the lookups go to the flow table (L2). LU lookups per
+// thread are in flight together.
+constexpr int LU = 8;
+constexpr int LR_LDS_FLOWS = 2048;
+constexpr int LR_LDS_SLOTS = 4096;
+
+template <typename KT, typename DT>
+__device__ inline void lr_lookup(const uint64_t* __restrict__ keys, int64_t n, int sh, KT tk, DT td, int64_t cap,
+                                 int32_t* __restrict__ dest) {
+  const uint64_t mask = (uint64_t)(cap - 1);
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const uint64_t mask = (uint64_t)(hcap - 1);
   for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += stride * LU) {
     uint64_t p[LU], h[LU];
-    int64_t slot[LU];
+    int32_t d[LU];
     bool done[LU];
 #pragma unroll
     for (int u = 0; u < LU; ++u) {
       const int64_t i = i0 + u * stride;
-      p[u] = i < n ? key_prefix(keys[i], sh) : 0ull;
-      h[u] = lr_hash(p[u], hcap);
-      slot[u] = -1;   // a flow missing from the table only after an error
-      done[u] = i >= n;
+      p[u] = i < n ? keys[i] : 0ull;
     }
-    for (int64_t probe = 0; probe < hcap; ++probe) {
+#pragma unroll
+    for (int u = 0; u < LU; ++u) {
+      p[u] = key_prefix(p[u], sh);
+      h[u] = lr_hash(p[u], cap);
+      d[u] = 0;   // a flow missing from the table only after an error
+      done[u] = i0 + u * stride >= n;
+    }
+    for (uint64_t probe = 0; probe <= mask; ++probe) {
       bool all = true;
 #pragma unroll
       for (int u = 0; u < LU; ++u) {
         if (done[u]) continue;
-        const uint64_t v = tkey[h[u]];
+        const uint64_t v = tk[h[u]];
         if (v == p[u]) {
-          slot[u] = (int64_t)h[u];
+          d[u] = td[h[u]];
           done[u] = true;
         } else if (v == ~0ull) {
           done[u] = true;
@@ -346,27 +407,67 @@ __global__ __launch_bounds__(256) void k_lr_dest_in(const uint64_t* __restrict__
 #pragma unroll
     for (int u = 0; u < LU; ++u) {
       const int64_t i = i0 + u * stride;
-      if (i < n) dest[i] = slot[u] >= 0 ? tdest[slot[u]] : 0;
+      if (i < n) dest[i] = d[u];
     }
   }
 }
 
-// perm in (destination, key) order and the destination offsets.
-__global__ __launch_bounds__(256) void k_lr_perm(int64_t n, const uint64_t* __restrict__ dsk,
-                                                 const uint32_t* __restrict__ dval, const uint32_t* __restrict__ sidx,
-                                                 int D, int32_t* __restrict__ perm, int64_t* __restrict__ offs) {
-  for (int64_t m = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; m < n; m += (int64_t)gridDim.x * blockDim.x) {
-    if (perm) perm[m] = (int32_t)sidx[dval[m]];
-    if (!offs) continue;
-    const uint32_t d = (uint32_t)dsk[m];
-    if (m == 0) {
-      for (uint32_t x = 0; x <= d; ++x) offs[x] = 0;
-    } else {
-      const uint32_t dp = (uint32_t)dsk[m - 1];
-      for (uint32_t x = dp + 1; x <= d; ++x) offs[x] = m;
+__global__ __launch_bounds__(256) void k_lr_dest_in(const uint64_t* __restrict__ keys, int64_t n, int sh,
+                                                    const uint64_t* __restrict__ run_pfx,
+                                                    const int32_t* __restrict__ run_dest,
+                                                    const int64_t* __restrict__ nrun,
+                                                    const uint64_t* __restrict__ tkey,
+                                                    const int32_t* __restrict__ tdest, int64_t hcap,
+                                                    const SortCtl* ctl, const int32_t* __restrict__ rank,
+                                                    int32_t* __restrict__ dest) {
+  __shared__ uint64_t s_k[LR_LDS_SLOTS];
+  __shared__ int32_t s_d[LR_LDS_SLOTS];
+  const int64_t R = *nrun;
+  if (rank && ctl->mode == SORT_PACKED) return;   // k_lr_dest_rank does it
+  if (R > LR_LDS_FLOWS) {   // uniform
+    lr_lookup(keys, n, sh, tkey, tdest, hcap, dest);
+    return;
+  }
+  for (int i = threadIdx.x; i < LR_LDS_SLOTS; i += blockDim.x) s_k[i] = ~0ull;
+  __syncthreads();
+  for (int64_t r = threadIdx.x; r < R; r += blockDim.x) {
+    const uint64_t p = run_pfx[r];
+    uint64_t h = lr_hash(p, LR_LDS_SLOTS);
+    for (int probe = 0; probe < LR_LDS_SLOTS; ++probe) {
+      const unsigned long long old =
+          atomicCAS(reinterpret_cast<unsigned long long*>(&s_k[h]), ~0ull, (unsigned long long)p);
+      if (old == ~0ull || old == p) {
+        s_d[h] = run_dest[r];
+        break;
+      }
+      h = (h + 1) & (uint64_t)(LR_LDS_SLOTS - 1);
     }
-    if (m == n - 1)
-      for (uint32_t x = d + 1; x <= (uint32_t)D; ++x) offs[x] = n;
+  }
+  __syncthreads();
+  lr_lookup(keys, n, sh, s_k, s_d, LR_LDS_SLOTS, dest);
+}
+
+// The same from the flow ranks of the packed key sort: dest = run_dest[rank], LU
+// elements per thread in flight (no LDS, full occupancy).
+__global__ __launch_bounds__(256) void k_lr_dest_rank(int64_t n, const int64_t* __restrict__ nrun,
+                                                      const int32_t* __restrict__ run_dest, const SortCtl* ctl,
+                                                      const int32_t* __restrict__ rank, int32_t* __restrict__ dest) {
+  if (ctl->mode != SORT_PACKED) return;   // k_lr_dest_in does it
+  const int64_t R = *nrun;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < n; i0 += stride * LU) {
+    int64_t q[LU];
+#pragma unroll
+    for (int u = 0; u < LU; ++u) {
+      const int64_t i = i0 + u * stride;
+      q[u] = i < n ? rank[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < LU; ++u) {
+      const int64_t i = i0 + u * stride;
+      const int64_t r = q[u] < 0 ? 0 : (q[u] >= R ? R - 1 : q[u]);   // in bounds whatever an error left behind
+      if (i < n) dest[i] = run_dest[r];
+    }
   }
 }
 
@@ -375,7 +476,7 @@ __global__ void k_lr_zero_offsets(int64_t* offs, int D) {
 }
 
 bool lr_layout_ok(const alto_layout* l) {
-  if (!l || l->depth < 1 || l->depth > ALTO_MAX_LEVELS) return false;
+  if (!l || l->depth < 2 || l->depth > ALTO_MAX_LEVELS) return false;
   int total = 0;
   for (int i = 0; i < l->depth; ++i) {
     if (l->bits[i] < 1 || l->bits[i] > 32) return false;
@@ -442,11 +543,14 @@ int alto_router_destroy(alto_router* r) {
   return ALTO_OK;
 }
 
-size_t alto_route_load_workspace_bytes(int64_t n_max, int32_t num_dest) {
-  if (n_max < 0 || n_max > LR_N_LIMIT || num_dest < 1 || num_dest > LR_MAX_DEST) return 0;
+size_t alto_route_load_workspace_bytes(const alto_layout* layout, int32_t route_level, int64_t n_max,
+                                       int32_t num_dest) {
+  if (!lr_layout_ok(layout) || route_level < 1 || route_level > layout->depth || n_max < 0 || n_max > LR_N_LIMIT ||
+      num_dest < 1 || num_dest > LR_MAX_DEST)
+    return 0;
   WsCarver c{nullptr, (size_t)-1, 0, true};
   LrBufs b;
-  plan_lr(n_max, num_dest, c, b);
+  plan_lr(make_geom(layout), route_level, n_max, num_dest, c, b);
   return c.off;
 }
 
@@ -457,7 +561,7 @@ int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* lo
   const int D = r->num_dest;
   WsCarver c{(char*)ws, ws_bytes, 0, true};
   LrBufs b;
-  plan_lr(n, D, c, b);
+  plan_lr(r->g, r->route_level, n, D, c, b);
   if (!c.ok) return ALTO_E_ARG;
   k_lr_init<<<1, 256, 0, stream>>>(counts, b.delta, D, b.hs + n);
   if (n == 0) {
@@ -467,48 +571,62 @@ int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* lo
   }
   const int total = r->g.total;
   const int sh = r->g.shift[r->route_level];
-  SortBufs sb;
-  memset(&sb, 0, sizeof(sb));
-  sb.in_keys = keys;
-  sb.tmp_keys = b.tmp_keys;
-  sb.tmp_vals = b.tmp_vals;
-  sb.out_keys = b.skey;
-  sb.out_vals = b.sidx;
-  sb.ctl = b.ctl;
-  sb.os_status = b.os_status;
-  sb.os_ctr = b.os_ctr;
-  sb.os_hist = b.os_hist;
-  sb.os_ntiles = b.os_ntiles;
-  sb.status = status;
-  RouteGeom none;
-  none.shift = 64;
-  none.num_dest = 1;
-  int rc = sort_pairs(sb, n, nullptr, none, total, false, stream);
+  // duplicates are reported by k_lr_heads (the routing sort's own offset pass is skipped)
+  // with flows, the counting sweep writes every element's flow rank into b.rank
+  const bool flows = b.ab.fl.hcap > 0 && n > SORT_SMALL_MAX;
+  b.ab.fl.rank_dest = 1;
+  int rc = route_run(r->g, make_route(r->g, r->route_level, 1), keys, n, b.ab, nullptr, nullptr,
+                     flows ? b.rank : nullptr, nullptr, 0, 1, 0, status, stream, true);
   if (rc) return rc;
-  k_lr_heads<<<grid_of(n), 256, 0, stream>>>(b.skey, n, total, sh, b.hs, status);
+  const uint64_t* skey = b.ab.sk;
+  const uint32_t* sidx = b.ab.perm;
+  k_lr_heads<<<grid_of(n), 256, 0, stream>>>(skey, n, total, sh, b.hs, status);
   rc = scan_exclusive<uint32_t>(b.hs, b.hs, n + 1, nullptr, b.part, nullptr, stream);
   if (rc) return rc;
-  k_lr_runs<<<grid_of(n), 256, 0, stream>>>(b.skey, n, sh, b.hs, r->tkey, r->tdest, r->hcap, b.run_start,
-                                            b.run_dest, b.nf, b.nrun1, counts);
+  k_lr_runs<<<grid_of(n), 256, 0, stream>>>(skey, n, sh, b.hs, r->tkey, r->tdest, r->hcap, b.run_start, b.run_pfx,
+                                            b.run_dest, b.nf, b.nrun1, b.nrun, counts);
   rc = scan_exclusive<uint32_t>(b.nf, b.nf, n + 1, b.nrun1, b.part, nullptr, stream);
   if (rc) return rc;
   k_lr_known<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta,
                                                         D);
   k_lr_assign<<<1, ALTO_WAVE, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta, load, D,
                                            r->nflows, r->max_flows, counts, status);
-  k_lr_insert<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.nf, b.new_run, b.run_start, b.run_dest, b.skey, sh,
+  k_lr_insert<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.nf, b.new_run, b.run_start, b.run_dest, skey, sh,
                                                          r->tkey, r->tdest, r->hcap, status);
-  if (dest)
-    k_lr_dest_in<<<grid_of(n, 256 * LU), 256, 0, stream>>>(keys, n, sh, r->tkey, r->tdest, r->hcap, dest);
+  if (dest) {
+    // one of the two does the work, as the key sort ran packed or not
+    if (flows) k_lr_dest_rank<<<grid_of(n, 256 * LU), 256, 0, stream>>>(n, b.nrun, b.run_dest, b.ab.ctl, b.rank, dest);
+    k_lr_dest_in<<<grid_of(n, 256 * LU, 1024), 256, 0, stream>>>(keys, n, sh, b.run_pfx, b.run_dest, b.nrun, r->tkey,
+                                                                  r->tdest, r->hcap, b.ab.ctl, flows ? b.rank : nullptr,
+                                                                  dest);
+  }
   if (perm || dest_offsets) {
-    k_lr_dest<<<grid_of(n), 256, 0, stream>>>(n, b.hs, b.run_dest, D, b.dkey);
-    SortBufs db = sb;
-    db.in_keys = b.dkey;
-    db.out_keys = b.dsk;
-    db.out_vals = b.dval;
-    rc = sort_pairs(db, n, nullptr, none, bits_for(D - 1), false, stream);
+    // the runs in (destination, prefix) order, their offsets, then the runs copied
+    k_lr_runkeys<<<grid_of(n, 256, 1024), 256, 0, stream>>>(b.nrun, b.run_dest, D, b.rkey);
+    SortBufs db;
+    memset(&db, 0, sizeof(db));
+    db.in_keys = b.rkey;
+    db.tmp_keys = b.ab.tmp_keys;
+    db.tmp_vals = b.ab.tmp_vals;
+    db.out_keys = b.rsk;
+    db.out_vals = b.rval;
+    db.ctl = b.ab.rctl;
+    db.os_status = b.ab.os_status;
+    db.os_ctr = b.ab.os_ctr;
+    db.os_hist = b.ab.os_hist;
+    db.os_ntiles = b.ab.os_ntiles;
+    db.status = status;
+    RouteGeom none;
+    none.shift = 64;
+    none.num_dest = 1;
+    rc = sort_pairs(db, n, b.nrun, none, 32 + bits_for(D - 1), false, stream);
     if (rc) return rc;
-    k_lr_perm<<<grid_of(n), 256, 0, stream>>>(n, b.dsk, b.dval, b.sidx, D, perm, dest_offsets);
+    k_lr_runlen<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.nrun, b.rval, b.run_start, b.roff);
+    rc = scan_exclusive<int64_t>(b.roff, b.roff, n + 1, b.nrun1, b.rpart, nullptr, stream);
+    if (rc) return rc;
+    k_lr_runoff<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.nrun, b.rsk, b.rval, b.roff, D, b.rbase,
+                                                           dest_offsets);
+    if (perm) k_lr_copy<<<grid_of(n), 256, 0, stream>>>(n, b.hs, b.run_start, b.rbase, sidx, perm);
   }
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;

@@ -61,6 +61,8 @@ struct FlowBufs {
   uint32_t* ct_rank;     // [hcap]
   uint16_t* drank;       // [1 << FLOW_DIRECT_BITS] rank by the varying bits of the prefix
   uint32_t* fdest;       // [fcap] destination of each ranked flow
+  int32_t rank_dest;     // fdest holds each flow's rank instead (the counting sweep then
+                         // writes every element's flow rank where it writes destinations)
   // child ranks: a flow's children (the nodes one level below the route level) are
   // numbered consecutively from fbase[rank], using the flow's declared child count
   uint32_t* ht_fan;      // [hcap] declared child count of the flow in the slot (the first carrier's; 0 = unset)

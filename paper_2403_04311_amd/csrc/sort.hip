@@ -160,7 +160,7 @@ __global__ void k_ct_insert(FlowBufs fl, const SortCtl* ctl, uint32_t num_dest) 
   const int dlo = ctl->dlo, dbits = ctl->dbits;
   for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < F; r += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t p = fl.flow_sorted[r];
-    fl.fdest[r] = dest_of_prefix(p, num_dest);
+    fl.fdest[r] = fl.rank_dest ? (uint32_t)r : dest_of_prefix(p, num_dest);
     if (dbits >= 0) {
       fl.drank[(p >> dlo) & ((1ull << dbits) - 1ull)] = (uint16_t)r;
       continue;

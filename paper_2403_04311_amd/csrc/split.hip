@@ -318,7 +318,8 @@ int alto_split(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const i
     return ALTO_OK;
   }
   const RouteGeom rg = make_route(g, d - 1, 1);
-  int rc = route_run(g, rg, keys, n, b.ab, nullptr, nullptr, nullptr, nullptr, 0, 1, 0, status, stream);
+  // duplicates are reported by k_split_mark (the routing sort's own offset pass is skipped)
+  int rc = route_run(g, rg, keys, n, b.ab, nullptr, nullptr, nullptr, nullptr, 0, 1, 0, status, stream, true);
   if (rc) return rc;
   const uint64_t* skey = b.ab.sk;
   const uint32_t* sidx = b.ab.perm;

@@ -107,7 +107,9 @@ def test_load_route_rejects_bad_arguments():
     for Lr, D, mf in [(0, 2, 8), (4, 2, 8), (1, 0, 8), (1, 4097, 8), (1, 2, 0)]:
         assert lib.alto_router_create(C.byref(L), Lr, D, mf, st.data_ptr(), st.numel(), None, C.byref(h)) == 1
     assert lib.alto_router_create(C.byref(L), 1, 2, 1 << 20, st.data_ptr(), st.numel(), None, C.byref(h)) == 1
-    assert lib.alto_route_load_workspace_bytes(16, 0) == 0
+    assert lib.alto_route_load_workspace_bytes(C.byref(L), 1, 16, 0) == 0
+    assert lib.alto_route_load_workspace_bytes(C.byref(L), 4, 16, 2) == 0
+    assert lib.alto_route_load_workspace_bytes(C.byref(L), 1, 16, 2) > 0
     assert lib.alto_router_state_bytes(0) == 0
 
 
