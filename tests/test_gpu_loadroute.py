@@ -46,9 +46,10 @@ CASES = [
     (1, (6, 5, 4), 2, 5, (12, 9), 20, 4),
     (2, (31, 3, 2, 3, 8), 2, 32, (6, 3, 5, 40), 60, 3),        # multi-block sorts
     (3, (20, 12, 8), 2, 1, (300, 30), 40, 3),                   # one destination
-    (4, (20, 12, 8), 2, 4096, (300, 30), 40, 3),                # most destinations, > 2,048 new flows
+    (4, (20, 12, 8), 2, 4096, (300, 30), 50, 3),                # most destinations, > 2,048 new flows
     (5, (16, 10, 6), 1, 7, (50, 20), 3000, 2),                  # 3,000 level-1 flows per batch
     (6, (8, 8, 8), 3, 64, (8, 8), 100, 3),                      # flows are the leaves
+    (7, (20, 12, 8), 2, 48, (400, 30), 60, 2),                  # > 8,192 flows: general sort, table lookups
 ]
 
 
