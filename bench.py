@@ -122,8 +122,52 @@ def cpu_baseline(leaves_log2: int):
     dt = time.perf_counter() - t0
     return {"value": (1 << leaves_log2) / dt, "unit": "fragments/s", "cores": 1, "kind": "oracle",
             "sample": f"same generator at 2^{leaves_log2} leaves (1/{1 << (26 - leaves_log2)} of the "
-                      f"workload): pack + route + aggregate, {dt:.1f} s single-threaded numpy"}
+                      f"workload): pack + route + aggregate, {dt:.1f} s single-threaded numpy",
+            "host": host_info()}
 
+
+def host_info():
+    """CPU model, hardware threads and RAM of the machine the oracle ran on."""
+    info = {"cpu_model": None, "threads": os.cpu_count(), "ram_gib": None}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    info["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+        with open("/proc/meminfo") as f:
+            for line in f:
+                if line.startswith("MemTotal"):
+                    info["ram_gib"] = round(int(line.split()[1]) / (1 << 20), 1)
+                    break
+    except OSError:
+        pass
+    return info
+
+
+def read_ceiling_gbps(dev, gib: int = 16, reps: int = 5):
+    """Attainable streaming read on this GPU: alto_read_probe (16-byte non-temporal
+    loads, XOR-reduced) over a resident array, bytes read per rep over the time."""
+    import ctypes as C
+    import torch
+    from paper_2403_04311_amd import alto
+    lib = alto.load()
+    lib.alto_read_probe.argtypes = [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p]
+    x = torch.ones(gib << 30, dtype=torch.uint8, device=dev)
+    out = torch.zeros(16384, dtype=torch.int64, device=dev)
+    st = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    assert lib.alto_read_probe(C.c_void_p(x.data_ptr()), x.numel(), C.c_void_p(out.data_ptr()), st) == 0
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        lib.alto_read_probe(C.c_void_p(x.data_ptr()), x.numel(), C.c_void_p(out.data_ptr()), st)
+    e1.record()
+    torch.cuda.synchronize()
+    gbps = x.numel() * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del x
+    torch.cuda.empty_cache()
+    return gbps
 
 
 def _timed(fn, steps, warmup):
@@ -654,14 +698,15 @@ def main():
     assert lib.alto_profile_phases(1 << PHASES.index("mean_kernel")) == 0
     rc = lib.alto_profile_begin(4 * args.steps + 4)
     assert rc == 0
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for k in range(args.steps):
         step()
-    e1.record()
+        evs[k + 1].record()
     torch.cuda.synchronize()
-    ms_total = e0.elapsed_time(e1)
+    ms_total = evs[0].elapsed_time(evs[-1])
+    per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
     ms = (C.c_float * len(PHASES))()
     calls = (C.c_int32 * len(PHASES))()
     rc = lib.alto_profile_end(ms, calls, len(PHASES))
@@ -693,6 +738,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_median": per_step[len(per_step) // 2],
+        "ms_per_step_min": per_step[0],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -709,6 +756,7 @@ def main():
                           "achieved": path_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                           "frac": path_gbps / HBM_PEAK_GBPS},
         "phase_ms_one_call": phase_ms,
+        "read_ceiling_gbps": read_ceiling_gbps(dev),
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")

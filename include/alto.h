@@ -316,6 +316,14 @@ int alto_profile_begin(int32_t max_records);
  * default: all). Fewer event pairs per call disturb the timed calls less. Not
  * while a pool is active (ALTO_E_ARG). */
 int alto_profile_phases(uint32_t mask);
+
+/* Diagnostics: reads `bytes` (a multiple of 16, 16-byte aligned) of device memory
+ * once with a plain streaming kernel; the attainable read bandwidth that the kernels
+ * above are compared with. out: device uint64[ALTO_READ_PROBE_WORDS]; entry b gets
+ * the XOR of the 32-bit words read by block b (unused entries 0), so the XOR of all
+ * entries is the XOR of all words read. */
+enum { ALTO_READ_PROBE_WORDS = 16384 };
+int alto_read_probe(const void *p, int64_t bytes, uint64_t *out, hipStream_t stream);
 int alto_profile_end(float *ms, int32_t *calls, int32_t nphase);
 
 #ifdef __cplusplus

@@ -27,7 +27,8 @@ EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggrega
            "alto_stream_state_bytes", "alto_stream_create", "alto_stream_step",
            "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join",
            "alto_split_workspace_bytes", "alto_split", "alto_router_state_bytes", "alto_router_create",
-           "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load", "alto_profile_phases")
+           "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load", "alto_profile_phases",
+           "alto_read_probe")
 
 
 class Layout(C.Structure):
