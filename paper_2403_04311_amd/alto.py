@@ -102,6 +102,10 @@ def load():
     lib.alto_route_load_workspace_bytes.argtypes = [C.POINTER(Layout), i32, i64, i32]
     lib.alto_route_load.restype = C.c_int
     lib.alto_route_load.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp, vp, vp, C.c_size_t, vp]
+    lib.alto_profile_phases.restype = C.c_int
+    lib.alto_profile_phases.argtypes = [C.c_uint32]
+    lib.alto_read_probe.restype = C.c_int
+    lib.alto_read_probe.argtypes = [vp, i64, vp, vp]
     lib.alto_split_workspace_bytes.restype = C.c_size_t
     lib.alto_split_workspace_bytes.argtypes = [C.POINTER(Layout), i64]
     lib.alto_split.restype = C.c_int

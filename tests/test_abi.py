@@ -50,3 +50,28 @@ def test_workspace_sizing_host_checks():
     assert lib.alto_stream_state_bytes(C.byref(L), C.byref(A), 1 << 12, 1 << 14) == 0
     # growing with the sizes it is given
     assert alto.workspace_bytes((31, 2, 3, 4), 1 << 20, 8, 3, "concat") > ok
+
+
+def test_join_split_router_sizing_host_checks():
+    lib = alto.load()
+    L = alto.layout((31, 6, 12))
+    assert lib.alto_join_workspace_bytes(C.byref(L), 1000) > 0
+    assert lib.alto_join_workspace_bytes(C.byref(L), -1) == 0
+    assert lib.alto_join_workspace_bytes(C.byref(L), 1 << 20) > lib.alto_join_workspace_bytes(C.byref(L), 1000)
+    # split: the input layout gains a level, so at most 15 input levels
+    assert lib.alto_split_workspace_bytes(C.byref(alto.layout((31, 18))), 1000) > 0
+    assert lib.alto_split_workspace_bytes(C.byref(alto.layout((31, 18))), -1) == 0
+    assert lib.alto_split_workspace_bytes(C.byref(alto.layout((2,) * 15)), 10) > 0
+    assert lib.alto_split_workspace_bytes(C.byref(alto.layout((2,) * 16)), 10) == 0
+    assert lib.alto_split_workspace_bytes(C.byref(alto.layout((40, 30))), 10) == 0   # wider than 63 bits
+    # load-aware routing
+    assert lib.alto_router_state_bytes(0) == 0
+    assert 0 < lib.alto_router_state_bytes(1) < lib.alto_router_state_bytes(1 << 20)
+    assert lib.alto_route_load_workspace_bytes(C.byref(L), 2, 1 << 16, 64) > 0
+    for Lr, n, D in [(0, 100, 4), (4, 100, 4), (2, -1, 4), (2, 100, 0), (2, 100, 4097)]:
+        assert lib.alto_route_load_workspace_bytes(C.byref(L), Lr, n, D) == 0, (Lr, n, D)
+    h = C.c_void_p()
+    # bad arguments are refused on the host, before anything is enqueued
+    assert lib.alto_router_create(C.byref(L), 2, 4, 16, None, 0, None, C.byref(h)) == 1
+    assert lib.alto_route_load(None, None, 0, None, None, None, None, None, None, None, 0, None) == 1
+    assert lib.alto_read_probe(None, 16, None, None) == 1
