@@ -142,3 +142,26 @@ def test_load_route_zipf_tree_full_size():
     same_d = dest[p][1:] == dest[p][:-1]
     assert bool((dest[p][1:] >= dest[p][:-1]).all())
     assert bool((ks[1:] > ks[:-1])[same_d].all())
+
+
+def test_load_route_factool_stream_steps():
+    """A FacTool-shaped tree (1,024 queries, ~0.9M fragments, shuffled arrival) streamed
+    in 4,096-fragment steps, routed by claim (level 2) to 32 destinations, each
+    destination draining 128 fragments per step: destinations, queues, perm and counts
+    of every step against the oracle."""
+    rng = np.random.default_rng(W.SEED_BASE + 2)
+    roots = W.distinct_ids(rng, 1024)
+    path, _ = W.expand_tree(W.factool_fans(rng, roots), roots)   # the FacTool-shaped tree, no payload
+    (path,), _ = W.permute([path], 77)
+    bits = (31, 3, 2, 3, 8)
+    keys = O.pack_keys(path, bits)
+    step, D = 4096, 32
+    rt = alto.LoadRouter(bits, 2, D, 1 << 16, step)
+    orc = O.LoadRouter(bits, 2, D, 1 << 16)
+    load = np.zeros(D, np.int64)
+    for s in range(0, len(keys), step):
+        part = keys[s:s + step]
+        o = orc.route(part, load)
+        same(gpu_route(rt, part, load), o)
+        load = np.maximum(o.load - 128, 0)
+    assert len(orc.table) > 1000
