@@ -828,13 +828,15 @@ __global__ __launch_bounds__(SCAN_NT) void k_scan_apply(const T* in, T* out, int
 // passes; the digit windows are planned in the block from its own OR/AND.
 // ---------------------------------------------------------------------------
 constexpr int SM_NT = 1024;
-constexpr int SM_IT = SORT_SMALL_MAX / SM_NT;
 constexpr int SM_NW = SM_NT / ALTO_WAVE;
 
+// IT items per thread (IT * SM_NT elements at most): launched with the smallest IT
+// that holds the host's bound on the count, so small sorts rank fewer items per pass.
+template <int IT>
 __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
                                                       int max_key_windows, int max_dest_windows) {
-  __shared__ uint64_t s_key[SORT_SMALL_MAX];
-  __shared__ uint32_t s_val[SORT_SMALL_MAX];
+  __shared__ uint64_t s_key[IT * SM_NT];
+  __shared__ uint32_t s_val[IT * SM_NT];
   __shared__ uint16_t s_cnt[SM_NW][SORT_BUCKETS];
   __shared__ uint32_t s_base[SORT_BUCKETS];
   __shared__ uint32_t s_wsum[SM_NW];
@@ -843,12 +845,12 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
   __shared__ int s_np;
   __shared__ int s_lo[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
   const int64_t n = load_n(n_host, n_dev);
-  if (n > SORT_SMALL_MAX) return;   // the multi-block path sorts it
+  if (n > IT * SM_NT) return;   // the multi-block path sorts it
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
-  for (int j = 0; j < SM_IT; ++j) {
-    const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+  for (int j = 0; j < IT; ++j) {
+    const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
     if (e < n) {
       const uint64_t k = b.in_keys[e];
       s_key[e] = k;
@@ -910,11 +912,11 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     ps.from_dest = s_fd[p];
     ps.lo = s_lo[p];
     for (int i = threadIdx.x; i < SM_NW * SORT_BUCKETS; i += SM_NT) (&s_cnt[0][0])[i] = 0;
-    uint64_t key[SM_IT];
-    uint32_t val[SM_IT], dig[SM_IT], off[SM_IT];
+    uint64_t key[IT];
+    uint32_t val[IT], dig[IT], off[IT];
 #pragma unroll
-    for (int j = 0; j < SM_IT; ++j) {
-      const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    for (int j = 0; j < IT; ++j) {
+      const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       const bool valid = e < n;
       key[j] = valid ? s_key[e] : 0ull;
       val[j] = valid ? s_val[e] : 0u;
@@ -922,8 +924,8 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     }
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < SM_IT; ++j) {
-      const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    for (int j = 0; j < IT; ++j) {
+      const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       const bool valid = e < n;
       off[j] = wave_rank(s_cnt[w], dig[j], valid);
     }
@@ -948,8 +950,8 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     }
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < SM_IT; ++j) {
-      const int e = w * (SM_IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
+    for (int j = 0; j < IT; ++j) {
+      const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       if (e < n) {
         const uint32_t pos = s_base[dig[j]] + (uint32_t)s_cnt[w][dig[j]] + off[j];
         s_key[pos] = key[j];
@@ -1002,10 +1004,20 @@ int bits_for(int64_t v) {
   return b;
 }
 
+// The one-workgroup sort with the fewest items per thread that holds n_max elements.
+static void launch_sort_small(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg,
+                              int key_bits, hipStream_t st) {
+  const int kw = sort_max_key_windows(key_bits), dw = sort_max_dest_windows(rg);
+  if (n_max <= SM_NT) k_sort_small<1><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
+  else if (n_max <= 2 * SM_NT) k_sort_small<2><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
+  else if (n_max <= 4 * SM_NT) k_sort_small<4><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
+  else k_sort_small<SORT_SMALL_MAX / SM_NT><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
+}
+
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
                bool ctl_has_reduction, hipStream_t st) {
   if (n_max <= SORT_SMALL_MAX) {
-    k_sort_small<<<1, 1024, 0, st>>>(b, n_max, n_dev, rg, sort_max_key_windows(key_bits), sort_max_dest_windows(rg));
+    launch_sort_small(b, n_max, n_dev, rg, key_bits, st);
     ALTO_LAUNCH_CHECK();
     return ALTO_OK;
   }
@@ -1015,7 +1027,7 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
   const int grid_r = (int)(cdiv(n_max, 256 * 8) < 2048 ? cdiv(n_max, 256 * 8) : 2048);
   if (n_dev) {
     // the count is known on the device only: small counts go to one workgroup
-    k_sort_small<<<1, 1024, 0, st>>>(b, n_max, n_dev, rg, sort_max_key_windows(key_bits), sort_max_dest_windows(rg));
+    launch_sort_small(b, n_max, n_dev, rg, key_bits, st);
   }
   if (!ctl_has_reduction) {
     k_sort_init<<<1, 1, 0, st>>>(b.ctl);
