@@ -162,20 +162,28 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
 
 // Per merged element: survives (its group is not emitted), frees its arena slot
 // (emitted live leaf), or needs a slot (surviving step leaf).
+// Per merged element: kept (its group is not released), arena slot freed (MEAN: a
+// released group's carried element), slot needed (MEAN: a kept group's new element).
+// One thread per element; its group is the last node starting at or before it (the
+// nodes of level La cover the merged elements in order), found by binary search.
 __global__ void k_keep(LevelNodes L, const int64_t* Gp, const int32_t* __restrict__ msrc, const StreamCtl* ctl,
                        int32_t* keep, int64_t* freef, int64_t* allocf, int mean) {
   const int64_t G = *Gp;
-  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
-    const bool ok = L.ok[u];
-    for (int32_t e = L.start[u]; e < L.start[u + 1]; ++e) {
-      const bool live_elem = msrc[e] < 0;
-      keep[e] = ok ? 0 : 1;
-      freef[e] = (mean && ok && live_elem) ? 1 : 0;
-      allocf[e] = (mean && !ok && !live_elem) ? 1 : 0;
+  const int64_t M = ctl->merged;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < M; e += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo = 0, hi = G - 1;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (L.start[mid] <= e) lo = mid;
+      else hi = mid - 1;
     }
+    const bool ok = G > 0 && L.ok[lo];
+    const bool live_elem = msrc[e] < 0;
+    keep[e] = ok ? 0 : 1;
+    freef[e] = (mean && ok && live_elem) ? 1 : 0;
+    allocf[e] = (mean && !ok && !live_elem) ? 1 : 0;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
-    const int64_t M = ctl->merged;
     keep[M] = 0;
     freef[M] = 0;
     allocf[M] = 0;
