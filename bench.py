@@ -604,7 +604,7 @@ WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_token
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=30,
                     help="untimed steps first (the GPU settles at its steady clock after ~20 steps "
                          "of the 2^26-fragment call)")
