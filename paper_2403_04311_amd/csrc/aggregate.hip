@@ -786,10 +786,6 @@ inline bool src_rows_aligned16(const MergedSrc& s) {
   return ((reinterpret_cast<uintptr_t>(s.spf) | reinterpret_cast<uintptr_t>(s.arena)) & 15) == 0;
 }
 
-inline int grid_for(int64_t n, int nt, int cap = GRID_CAP) {
-  int64_t b = cdiv(n < 1 ? 1 : n, nt);
-  return (int)(b < cap ? b : cap);
-}
 
 }  // namespace
 

@@ -209,6 +209,12 @@ __device__ inline uint64_t lb64_resolve(uint64_t* st, int64_t tile, int64_t stri
 
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Blocks for a grid-stride loop over n items with nt threads per block, at most cap.
+inline int grid_for(int64_t n, int nt, int cap = 4096) {
+  const int64_t b = cdiv(n < 1 ? 1 : n, nt);
+  return (int)(b < cap ? b : cap);
+}
+
 // Bump allocator over a caller workspace; every buffer is 256-byte aligned.
 struct WsCarver {
   char* base;

@@ -38,10 +38,6 @@ void plan_join(int64_t n_max, WsCarver& c, JoinBufs& b) {
   b.hits = c.take<int32_t>(n);
 }
 
-inline int grid_of(int64_t n, int nt = 256, int cap = 4096) {
-  int64_t b = cdiv(n < 1 ? 1 : n, nt);
-  return (int)(b < cap ? b : cap);
-}
 
 // Counts and hits cleared; left prefixes wider than their levels are LAYOUT.
 __global__ void k_join_init(const uint64_t* __restrict__ left, int64_t nl, int lbits, int32_t* hits, int64_t* counts,
@@ -203,7 +199,7 @@ int alto_join(const uint64_t* left, int64_t n_left, const uint64_t* right_keys, 
   if (!c.ok) return ALTO_E_ARG;
   int32_t* h = hits ? hits : b.hits;
   const int lbits = g.total - g.shift[level];
-  k_join_init<<<grid_of(n_left), 256, 0, stream>>>(left, n_left, lbits, h, counts, status);
+  k_join_init<<<grid_for(n_left, 256), 256, 0, stream>>>(left, n_left, lbits, h, counts, status);
   if (n_left > 0) {
     SortBufs sb;
     memset(&sb, 0, sizeof(sb));
@@ -223,10 +219,10 @@ int alto_join(const uint64_t* left, int64_t n_left, const uint64_t* right_keys, 
     none.num_dest = 1;
     int rc = sort_pairs(sb, n_left, nullptr, none, lbits, false, stream);
     if (rc) return rc;
-    k_join_dups<<<grid_of(n_left), 256, 0, stream>>>(b.skey, n_left, status);
+    k_join_dups<<<grid_for(n_left, 256), 256, 0, stream>>>(b.skey, n_left, status);
   }
   if (n_right > 0) {
-    const int grid = grid_of(n_right, 256 * JU, 1024);
+    const int grid = grid_for(n_right, 256 * JU, 1024);
     if (n_left <= JOIN_LDS_KEYS)
       k_join_probe<2><<<grid, 256, (size_t)n_left * 16, stream>>>(right_keys, n_right, g.total, g.shift[level], b.skey,
                                                                   b.sidx, n_left, match, h, counts, status);
@@ -237,7 +233,7 @@ int alto_join(const uint64_t* left, int64_t n_left, const uint64_t* right_keys, 
       k_join_probe<0><<<grid, 256, 0, stream>>>(right_keys, n_right, g.total, g.shift[level], b.skey, b.sidx, n_left,
                                                 match, h, counts, status);
   }
-  if (n_left > 0) k_join_count<<<grid_of(n_left), 256, 0, stream>>>(h, n_left, counts);
+  if (n_left > 0) k_join_count<<<grid_for(n_left, 256), 256, 0, stream>>>(h, n_left, counts);
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;
 }

@@ -86,10 +86,6 @@ void plan_lr(const KeyGeom& g, int Lr, int64_t n_max, int D, WsCarver& c, LrBufs
   b.rbase = c.take<int64_t>(n);
 }
 
-inline int grid_of(int64_t n, int nt = 256, int cap = 4096) {
-  int64_t b = cdiv(n < 1 ? 1 : n, nt);
-  return (int)(b < cap ? b : cap);
-}
 
 __device__ inline int read_status(const int32_t* st) {
   return __hip_atomic_load(st, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -529,7 +525,7 @@ int alto_router_create(const alto_layout* layout, int32_t route_level, int32_t n
   r->tkey = tkey;
   r->tdest = tdest;
   r->nflows = nflows;
-  k_lr_clear<<<grid_of(h), 256, 0, stream>>>(tkey, h, nflows);
+  k_lr_clear<<<grid_for(h, 256), 256, 0, stream>>>(tkey, h, nflows);
   if (hipGetLastError() != hipSuccess) {
     delete r;
     return ALTO_E_HIP;
@@ -580,29 +576,29 @@ int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* lo
   if (rc) return rc;
   const uint64_t* skey = b.ab.sk;
   const uint32_t* sidx = b.ab.perm;
-  k_lr_heads<<<grid_of(n), 256, 0, stream>>>(skey, n, total, sh, b.hs, status);
+  k_lr_heads<<<grid_for(n, 256), 256, 0, stream>>>(skey, n, total, sh, b.hs, status);
   rc = scan_exclusive<uint32_t>(b.hs, b.hs, n + 1, nullptr, b.part, nullptr, stream);
   if (rc) return rc;
-  k_lr_runs<<<grid_of(n), 256, 0, stream>>>(skey, n, sh, b.hs, r->tkey, r->tdest, r->hcap, b.run_start, b.run_pfx,
+  k_lr_runs<<<grid_for(n, 256), 256, 0, stream>>>(skey, n, sh, b.hs, r->tkey, r->tdest, r->hcap, b.run_start, b.run_pfx,
                                             b.run_dest, b.nf, b.nrun1, b.nrun, counts);
   rc = scan_exclusive<uint32_t>(b.nf, b.nf, n + 1, b.nrun1, b.part, nullptr, stream);
   if (rc) return rc;
-  k_lr_known<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta,
+  k_lr_known<<<grid_for(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta,
                                                         D);
   k_lr_assign<<<1, ALTO_WAVE, 0, stream>>>(n, b.hs, b.run_start, b.run_dest, b.nf, b.new_run, b.delta, load, D,
                                            r->nflows, r->max_flows, counts, status);
-  k_lr_insert<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.nf, b.new_run, b.run_start, b.run_dest, skey, sh,
+  k_lr_insert<<<grid_for(n, 256, 1024), 256, 0, stream>>>(n, b.hs, b.nf, b.new_run, b.run_start, b.run_dest, skey, sh,
                                                          r->tkey, r->tdest, r->hcap, status);
   if (dest) {
     // one of the two does the work, as the key sort ran packed or not
-    if (flows) k_lr_dest_rank<<<grid_of(n, 256 * LU), 256, 0, stream>>>(n, b.nrun, b.run_dest, b.ab.ctl, b.rank, dest);
-    k_lr_dest_in<<<grid_of(n, 256 * LU, 1024), 256, 0, stream>>>(keys, n, sh, b.run_pfx, b.run_dest, b.nrun, r->tkey,
+    if (flows) k_lr_dest_rank<<<grid_for(n, 256 * LU), 256, 0, stream>>>(n, b.nrun, b.run_dest, b.ab.ctl, b.rank, dest);
+    k_lr_dest_in<<<grid_for(n, 256 * LU, 1024), 256, 0, stream>>>(keys, n, sh, b.run_pfx, b.run_dest, b.nrun, r->tkey,
                                                                   r->tdest, r->hcap, b.ab.ctl, flows ? b.rank : nullptr,
                                                                   dest);
   }
   if (perm || dest_offsets) {
     // the runs in (destination, prefix) order, their offsets, then the runs copied
-    k_lr_runkeys<<<grid_of(n, 256, 1024), 256, 0, stream>>>(b.nrun, b.run_dest, D, b.rkey);
+    k_lr_runkeys<<<grid_for(n, 256, 1024), 256, 0, stream>>>(b.nrun, b.run_dest, D, b.rkey);
     SortBufs db;
     memset(&db, 0, sizeof(db));
     db.in_keys = b.rkey;
@@ -621,12 +617,12 @@ int alto_route_load(alto_router* r, const uint64_t* keys, int64_t n, int64_t* lo
     none.num_dest = 1;
     rc = sort_pairs(db, n, b.nrun, none, 32 + bits_for(D - 1), false, stream);
     if (rc) return rc;
-    k_lr_runlen<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.nrun, b.rval, b.run_start, b.roff);
+    k_lr_runlen<<<grid_for(n, 256, 1024), 256, 0, stream>>>(n, b.nrun, b.rval, b.run_start, b.roff);
     rc = scan_exclusive<int64_t>(b.roff, b.roff, n + 1, b.nrun1, b.rpart, nullptr, stream);
     if (rc) return rc;
-    k_lr_runoff<<<grid_of(n, 256, 1024), 256, 0, stream>>>(n, b.nrun, b.rsk, b.rval, b.roff, D, b.rbase,
+    k_lr_runoff<<<grid_for(n, 256, 1024), 256, 0, stream>>>(n, b.nrun, b.rsk, b.rval, b.roff, D, b.rbase,
                                                            dest_offsets);
-    if (perm) k_lr_copy<<<grid_of(n), 256, 0, stream>>>(n, b.hs, b.run_start, b.rbase, sidx, perm);
+    if (perm) k_lr_copy<<<grid_for(n, 256), 256, 0, stream>>>(n, b.hs, b.run_start, b.rbase, sidx, perm);
   }
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;

@@ -71,10 +71,6 @@ void plan_split(const KeyGeom& g, int64_t n_max, WsCarver& c, SplitBufs& b) {
   b.send = c.take<uint32_t>(n);
 }
 
-inline int grid_of(int64_t n, int nt = 256, int cap = 4096) {
-  int64_t b = cdiv(n < 1 ? 1 : n, nt);
-  return (int)(b < cap ? b : cap);
-}
 
 __global__ void k_split_init(int64_t* counts, int64_t* cpl_end, uint32_t* cinc_end) {
   if (threadIdx.x < 4) counts[threadIdx.x] = 0;
@@ -325,15 +321,15 @@ int alto_split(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const i
   const uint32_t* sidx = b.ab.perm;
   const int tbits = layout->bits[d - 1];
   const int mgrid = (int)(cdiv(n, SPLIT_TILE) < 2048 ? cdiv(n, SPLIT_TILE) : 2048);
-  k_split_pair<<<grid_of(n), 256, 0, stream>>>(tokens, fan + (int64_t)(d - 2) * fan_ld, n, b.tf);
+  k_split_pair<<<grid_for(n, 256), 256, 0, stream>>>(tokens, fan + (int64_t)(d - 2) * fan_ld, n, b.tf);
   k_split_mark<<<mgrid, SPLIT_NT, 0, stream>>>(skey, sidx, b.tf, n, g.total,
                                                tbits, delim, b.sflag, b.stok, b.sfan, b.cpl, rest_idx ? b.cinc : nullptr,
                                                counts, status);
   rc = scan_exclusive<int64_t>(b.cpl, b.cpl, n + 1, nullptr, b.part, nullptr, stream);
   if (!rc && rest_idx) rc = scan_exclusive<uint32_t>(b.cinc, b.cinc, n + 1, nullptr, b.part32, nullptr, stream);
   if (rc) return rc;
-  k_split_bounds<<<grid_of(n), 256, 0, stream>>>(b.sflag, b.cpl, n, b.sbeg, b.send);
-  k_split_emit<<<grid_of(n), 256, 0, stream>>>(skey, sidx, b.sflag, b.stok, b.sfan, b.cpl, b.cinc, b.sbeg, b.send, fan,
+  k_split_bounds<<<grid_for(n, 256), 256, 0, stream>>>(b.sflag, b.cpl, n, b.sbeg, b.send);
+  k_split_emit<<<grid_for(n, 256), 256, 0, stream>>>(skey, sidx, b.sflag, b.stok, b.sfan, b.cpl, b.cinc, b.sbeg, b.send, fan,
                                                fan_ld, d - 1, n, tbits, seg_bits, tok_bits, out_keys, out_fan,
                                                out_fan_ld, out_tokens, out_idx, rest_idx, status);
   ALTO_LAUNCH_CHECK();

@@ -42,10 +42,6 @@ struct LiveSet {
   int32_t* slot;   // MEAN
 };
 
-inline int grid_for(int64_t n, int nt, int cap = 4096) {
-  int64_t b = cdiv(n < 1 ? 1 : n, nt);
-  return (int)(b < cap ? b : cap);
-}
 
 __device__ inline bool dk_less(const RouteGeom& rg, uint64_t a, uint64_t b) {
   const uint32_t da = dest_of_key(rg, a), db = dest_of_key(rg, b);
