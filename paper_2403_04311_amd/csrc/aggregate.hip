@@ -26,7 +26,9 @@ __device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : 
 constexpr int PU = 4;
 constexpr int PREP_GRID = 512;          // two blocks of PREP_NT threads per CU
 constexpr int PREP_SLOTS = 3072;        // LDS flow set of a block (open addressing)
-constexpr int PREP_PROBES = 16;         // then the global set directly
+constexpr int PREP_PROBES = 4;          // then the global set directly: when the flows outnumber the
+                                        // slots the block's set fills up, and a long walk over it
+                                        // costs more than the cached global lookup
 constexpr int PREP_NX = FLOW_EXACT_LEVELS;
 
 __device__ inline uint32_t prep_slot(uint64_t p) {
