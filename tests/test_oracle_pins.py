@@ -240,6 +240,41 @@ def test_mean_is_textbook_group_mean():
         assert np.allclose(g.mean[i], rows.mean(axis=0).astype(np.float32), rtol=0, atol=1e-7)
 
 
+def test_mean_float64_batches_match_exact_rational_means():
+    # The oracle sums a group's rows in float64 batches of at most 2^24 / dim rows
+    # (a group larger than that takes a batch of its own). At dim 2^20 a batch holds
+    # 16 rows, so these group sizes put groups exactly at, just over and far over the
+    # budget, runs of small groups that fill a batch exactly, and single rows. Rows
+    # are multiples of 1/16 in [-4, 4): every float64 sum is exact, so each mean must
+    # equal the exact rational mean (integer sum over 16 x count) rounded once to
+    # float64 and then to float32 (the aggregate operator of Section 3.3, flat mean).
+    dim = 1 << 20
+    assert (1 << 24) // dim == 16
+    sizes = [3, 13, 16, 17, 1, 1, 14, 35, 2, 9, 16, 15, 1]
+    bits = (2, 5, 7)
+    rows = []
+    for g, s in enumerate(sizes):
+        rows += [(0, g, c) for c in range(s)]
+    path = np.array(rows, dtype=np.int64).T
+    fan = np.stack([np.ones(len(rows), np.int32) * len(sizes),
+                    np.array([sizes[g] for _, g, _ in rows], np.int32)])
+    rng = np.random.default_rng(11)
+    ints = (np.frombuffer(rng.bytes(len(rows) * dim), np.int8) >> 1).reshape(len(rows), dim)   # [-64, 64)
+    (sp, sf, order), _ = W.permute([path, fan, np.arange(len(rows))], 12)
+    x = ints[order].astype(np.float32)
+    x *= np.float32(1.0 / 16.0)
+    keys = O.pack_keys(sp, bits)
+    _, g = O.aggregate(keys, sf, bits, 2, "mean", dim, payload_f32=x)
+    assert [int(k) for k in g.key] == list(range(len(sizes)))
+    assert list(g.count) == sizes
+    start = 0
+    for gi, s in enumerate(sizes):
+        isum = ints[start:start + s].sum(axis=0, dtype=np.int64)       # rows in generation order
+        want = (isum.astype(np.float64) / np.float64(16 * s)).astype(np.float32)
+        assert np.array_equal(g.mean[gi], want), gi
+        start += s
+
+
 def test_arrival_permutation_invariance():
     bits = (6, 3, 2, 3, 5)
     path, fan = W.random_tree(9, 5, 4, (3, 3, 3, 6), bits)
@@ -393,6 +428,56 @@ def test_stream_brute_force_all_orders_and_cuts():
             assert len(s.pending()[0]) == 0
             checked += 1
     assert checked > 3000
+
+
+def test_stream_mean_brute_force_all_orders_and_cuts():
+    # The MEAN variant of the test above: carried rows must follow their leaves from
+    # step to step (Section 3.1: outputs stream before the input is complete). Every
+    # arrival order of tiny trees (sampled above 6 leaves), cut into steps at random
+    # points: each group is emitted once, in the step of its last leaf, and its mean
+    # is exactly the mean of all of its leaves' rows (dyadic rows: exact sums),
+    # whatever the order and the cuts.
+    bits = (4, 2, 2, 3)
+    La, Lr, D, dim = 2, 1, 3, 2
+    checked = 0
+    for seed in range(40):
+        roots = 1 + seed % 2
+        path, fan = W.random_tree(300 + seed, 4, roots, (2, 2, 2), bits)
+        n = path.shape[1]
+        if n > 8 or n < 3:
+            continue
+        true_leaves = brute.leaves_of(path)
+        rng = np.random.default_rng(seed + 7)
+        pf = (rng.integers(-64, 64, size=(n, dim)) / 16.0).astype(np.float32)
+        batch = brute.batch_expect(true_leaves, true_leaves, None, pf, La, 0, _dest_fn(bits, D), Lr)
+        mean_of = {r["key"]: np.array([float(v) for v in r["mean"]], np.float64).astype(np.float32)
+                   for r in batch["emitted"]}
+        if n <= 6:
+            orders = [list(o) for o in itertools.permutations(range(n))]
+        else:
+            orders = [list(rng.permutation(n)) for _ in range(150)]
+        for oi, order in enumerate(orders):
+            ncut = 1 + oi % min(n, 4)
+            cuts = [0] + sorted(rng.choice(np.arange(1, n), size=ncut - 1, replace=False).tolist()) + [n]
+            sp, sf, spf = path[:, order], fan[:, order], pf[order]
+            s = O.Stream(bits, Lr, D, La, "mean", dim)
+            keys = O.pack_keys(sp, bits)
+            arrival = brute.leaves_of(sp)
+            step_of = np.searchsorted(cuts, np.arange(n), side="right") - 1
+            want = brute.stream_emission_steps(true_leaves, arrival, step_of, La)
+            seen = {}
+            for si, (a, b) in enumerate(zip(cuts[:-1], cuts[1:])):
+                r = s.step(keys[a:b], sf[:, a:b], None, spf[a:b])
+                assert r.groups.mean.shape == (len(r.groups.key), dim)
+                for j, k in enumerate(r.groups.key):
+                    gt = _tuple_of(int(k), bits, La)
+                    assert gt not in seen
+                    seen[gt] = si
+                    assert np.array_equal(r.groups.mean[j], mean_of[gt]), (seed, order, cuts, gt)
+            assert seen == want
+            assert len(s.pending()[0]) == 0 and len(s.keys) == 0 and s.pf.shape == (0, dim)
+            checked += 1
+    assert checked > 2000
 
 
 def test_stream_late_and_duplicate():
