@@ -271,6 +271,18 @@ def _group_payloads(members: List[np.ndarray], op: str, dim: int, payload_i32, p
     return tok_off, tok, mean
 
 
+def group_mean(rows) -> np.ndarray:
+    """The pooled vector of one group from all of its leaves' rows: their float64
+    sum divided by their count, rounded once to float32 (the aggregate operator of
+    Section 3.3 read as a flat mean over the group's leaves). ``aggregate`` computes
+    the same for every group of a batch; this form takes one group's rows at a time,
+    so a check of a very large batch never holds more than one group in float64."""
+    x = np.asarray(rows, dtype=np.float32)
+    if x.ndim != 2 or len(x) == 0:
+        raise OracleError(E_ARG, "rows of one non-empty group")
+    return (x.sum(axis=0, dtype=np.float64) / np.float64(len(x))).astype(np.float32)
+
+
 def aggregate(keys, fan, bits, agg_level: int, op: str, dim: int = 1, mask_level: int = 0,
               route_level: int = 0, num_dest: int = 1, payload_i32=None, payload_f32=None,
               cap_groups: Optional[int] = None, cap_tokens: Optional[int] = None,

@@ -134,6 +134,91 @@ def _p(t: Optional[torch.Tensor]):
     return None if t is None else C.c_void_p(t.data_ptr())
 
 
+_KEY_DTYPES = (torch.int64, torch.uint64) if hasattr(torch, "uint64") else (torch.int64,)
+
+
+class _Args:
+    """Host-side checks of the tensors handed to the C ABI: the kernels index them
+    by the sizes given, so a tensor of the wrong type, device, layout or size is
+    refused here (AltoError E_ARG) instead of being read or written out of bounds.
+    Type, layout and size are checked before the device, so the checks also run on
+    a host without a GPU."""
+
+    def __init__(self, what: str):
+        self.what = what
+        self.dev = None
+        self.tensors = []
+
+    def fail(self, msg):
+        raise AltoError(E_ARG, f"{self.what}: {msg}")
+
+    def t(self, x, name, dtypes, numel=0, optional=False):
+        """A flat buffer: one of ``dtypes``, contiguous, at least ``numel`` elements."""
+        if x is None:
+            if not optional:
+                self.fail(f"{name} is required")
+            return None
+        if not isinstance(x, torch.Tensor):
+            self.fail(f"{name} must be a torch tensor")
+        dts = dtypes if isinstance(dtypes, tuple) else (dtypes,)
+        if x.dtype not in dts:
+            self.fail(f"{name} has dtype {x.dtype}, expected {' or '.join(str(d) for d in dts)}")
+        if not x.is_contiguous():
+            self.fail(f"{name} must be contiguous")
+        if x.numel() < numel:
+            self.fail(f"{name} holds {x.numel()} elements, needs {numel}")
+        self.tensors.append((name, x))
+        return x
+
+    def rows(self, x, name, dtypes, nrows, ncols, optional=False):
+        """A level-major [rows][ld] array (ld = stride(0) >= ncols, unit stride) with
+        at least ``nrows`` rows; returns its leading dimension."""
+        if x is None:
+            if not optional:
+                self.fail(f"{name} is required")
+            return 0
+        if not isinstance(x, torch.Tensor) or x.dim() != 2:
+            self.fail(f"{name} must be a 2-D tensor [levels][n]")
+        dts = dtypes if isinstance(dtypes, tuple) else (dtypes,)
+        if x.dtype not in dts:
+            self.fail(f"{name} has dtype {x.dtype}, expected {dts[0]}")
+        if x.shape[1] > 1 and x.stride(1) != 1:
+            self.fail(f"{name} must have unit stride along fragments")
+        if x.shape[0] < nrows or x.shape[1] < ncols:
+            self.fail(f"{name} is {tuple(x.shape)}, needs at least ({nrows}, {ncols})")
+        ld = x.stride(0) if x.shape[0] > 1 else max(x.shape[1], 1)
+        if ld < ncols:
+            self.fail(f"{name} rows overlap (stride {ld} < {ncols})")
+        self.tensors.append((name, x))
+        return ld
+
+    def payload(self, x, name, n, dim, optional=False):
+        """float32 rows of ``dim`` values, row-major and contiguous, at least n rows."""
+        if x is None:
+            if not optional:
+                self.fail(f"{name} is required")
+            return None
+        self.t(x, name, torch.float32, n * dim)
+        if x.dim() >= 2 and x.shape[-1] != dim:
+            self.fail(f"{name} rows hold {x.shape[-1]} values, dim is {dim}")
+        return x
+
+    def device(self):
+        """Every tensor on one GPU; returns it."""
+        for name, x in self.tensors:
+            if x.device.type != "cuda":
+                self.fail(f"{name} is on {x.device}, not on a GPU")
+            if self.dev is None:
+                self.dev = x.device
+            elif x.device != self.dev:
+                self.fail(f"{name} is on {x.device}, other arguments on {self.dev}")
+        return self.dev
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
 def _stream(stream=None):
     s = stream if stream is not None else torch.cuda.current_stream()
     return C.c_void_p(s.cuda_stream)
@@ -162,13 +247,18 @@ def new_status(device="cuda") -> torch.Tensor:
 def pack_keys(path: torch.Tensor, bits, keys: Optional[torch.Tensor] = None, status=None, stream=None):
     """path: int32 [d][ld] (level-major, first n columns used)."""
     lib = load()
-    n = path.shape[1]
+    a = _Args("alto_pack_keys")
+    n = path.shape[1] if isinstance(path, torch.Tensor) and path.dim() == 2 else 0
+    ld = a.rows(path, "path", torch.int32, len(bits), n)
     if keys is None:
         keys = torch.empty(n, dtype=torch.int64, device=path.device)
     if status is None:
         status = new_status(path.device)
+    a.t(keys, "keys", _KEY_DTYPES, n)
+    a.t(status, "status", torch.int32, 1)
+    a.device()
     L = layout(bits)
-    rc = lib.alto_pack_keys(_p(path), path.stride(0), n, C.byref(L), _p(keys), _p(status), _stream(stream))
+    rc = lib.alto_pack_keys(_p(path), ld, n, C.byref(L), _p(keys), _p(status), _stream(stream))
     _check(rc, "alto_pack_keys")
     return keys, status
 
@@ -176,7 +266,9 @@ def pack_keys(path: torch.Tensor, bits, keys: Optional[torch.Tensor] = None, sta
 def route(keys, bits, route_level, num_dest, ws=None, perm=None, dest_offsets=None, dest=None,
           status=None, stream=None, with_dest=True):
     lib = load()
+    a = _Args("alto_route")
     n = keys.shape[0]
+    a.t(keys, "keys", _KEY_DTYPES, n)
     dev = keys.device
     if ws is None:
         ws = new_workspace(workspace_bytes(bits, n, num_dest), dev)
@@ -188,9 +280,15 @@ def route(keys, bits, route_level, num_dest, ws=None, perm=None, dest_offsets=No
         dest = torch.empty(n, dtype=torch.int32, device=dev)
     if status is None:
         status = new_status(dev)
+    a.t(ws, "ws", torch.uint8)
+    a.t(perm, "perm", torch.int32, n)
+    a.t(dest_offsets, "dest_offsets", torch.int64, num_dest + 1)
+    a.t(dest, "dest", torch.int32, n, optional=True)
+    a.t(status, "status", torch.int32, 1)
+    a.device()
     L = layout(bits)
     rc = lib.alto_route(_p(keys), n, C.byref(L), route_level, num_dest, _p(perm), _p(dest_offsets),
-                        _p(dest), _p(status), _p(ws), ws.numel(), _stream(stream))
+                        _p(dest), _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_route")
     return perm, dest_offsets, dest, status
 
@@ -213,6 +311,26 @@ class GroupTensors:
     cap_groups: int
     cap_tokens: int
     cap_mask: int
+
+    def check(self, a: "_Args", op: str, agg_level: int, dim: int):
+        """Every member large enough for the capacities it declares."""
+        cg, ct, cm = self.cap_groups, self.cap_tokens, self.cap_mask
+        if min(cg, ct, cm) < 0:
+            a.fail("negative capacity")
+        a.t(self.key, "out.key", _KEY_DTYPES, cg, optional=True)
+        a.t(self.dest, "out.dest", torch.int32, cg, optional=True)
+        a.t(self.count, "out.count", torch.int64, cg, optional=True)
+        a.t(self.first_i32, "out.first_i32", torch.int32, cg, optional=True)
+        a.t(self.fan_up, "out.fan_up", torch.int32, (agg_level - 1) * cg, optional=True)
+        a.t(self.tok_off, "out.tok_off", torch.int64, cg + 1, optional=True)
+        a.t(self.tok, "out.tok", torch.int32, ct, optional=True)
+        if self.mean is not None:
+            a.payload(self.mean, "out.mean", cg, dim)
+        a.t(self.mask_key, "out.mask_key", _KEY_DTYPES, cm, optional=True)
+        a.t(self.mask, "out.mask", torch.uint8, cm, optional=True)
+        a.t(self.pend_key, "out.pend_key", _KEY_DTYPES, cg, optional=True)
+        a.t(self.pend_count, "out.pend_count", torch.int64, cg, optional=True)
+        a.t(self.counts, "out.counts", torch.int64, 4)
 
     def struct(self) -> Groups:
         g = Groups()
@@ -247,7 +365,12 @@ def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0
               out: Optional[GroupTensors] = None, status=None, stream=None, n=None):
     """Routes and aggregates one batch; returns (perm, dest_offsets, dest, groups, status)."""
     lib = load()
+    a = _Args("alto_aggregate")
     n = keys.shape[0] if n is None else n
+    a.t(keys, "keys", _KEY_DTYPES, n)
+    fan_ld = a.rows(fan, "fan", torch.int32, len(bits) - 1, n)
+    a.t(payload_i32, "payload_i32", torch.int32, n, optional=op != "concat")
+    a.payload(payload_f32, "payload_f32", n, dim, optional=op != "mean")
     dev = keys.device
     if ws is None:
         ws = new_workspace(workspace_bytes(bits, n, num_dest, agg_level, op, dim, mask_level), dev)
@@ -263,12 +386,19 @@ def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0
                          with_first=payload_i32 is not None)
     if status is None:
         status = new_status(dev)
+    a.t(ws, "ws", torch.uint8)
+    a.t(perm, "perm", torch.int32, n, optional=True)
+    a.t(dest_offsets, "dest_offsets", torch.int64, num_dest + 1, optional=True)
+    a.t(dest, "dest", torch.int32, n, optional=True)
+    out.check(a, op, agg_level, dim)
+    a.t(status, "status", torch.int32, 1)
+    a.device()
     L = layout(bits)
     A = agg_struct(agg_level, op, dim, mask_level)
     G = out.struct()
-    rc = lib.alto_aggregate(_p(keys), _p(fan), fan.stride(0), _p(payload_i32), _p(payload_f32), n,
+    rc = lib.alto_aggregate(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n,
                             C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
-                            _p(dest), C.byref(G), _p(status), _p(ws), ws.numel(), _stream(stream))
+                            _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_aggregate")
     return perm, dest_offsets, dest, out, status
 
@@ -303,6 +433,11 @@ class Stream:
         n = keys.shape[0] if n is None else n
         if n > self.step_max:
             raise AltoError(E_ARG, "step larger than step_max")
+        a = _Args("alto_stream_step")
+        a.t(keys, "keys", _KEY_DTYPES, n)
+        fan_ld = a.rows(fan, "fan", torch.int32, len(self.bits) - 1, n)
+        a.t(payload_i32, "payload_i32", torch.int32, n, optional=self.op != "concat")
+        a.payload(payload_f32, "payload_f32", n, self.dim, optional=self.op != "mean")
         dev = keys.device
         if out is None:
             out = new_groups(n, self.La, self.op, self.dim,
@@ -310,10 +445,18 @@ class Stream:
                              device=dev, with_first=payload_i32 is not None)
         if status is None:
             status = new_status(dev)
+        a.t(perm, "perm", torch.int32, n, optional=True)
+        a.t(dest_offsets, "dest_offsets", torch.int64, self.D + 1, optional=True)
+        a.t(dest, "dest", torch.int32, n, optional=True)
+        out.check(a, self.op, self.La, self.dim)
+        a.t(status, "status", torch.int32, 1)
+        a.t(self.ws, "workspace", torch.uint8)
+        if a.device() != self.state.device:
+            a.fail(f"arguments on {a.dev}, stream state on {self.state.device}")
         G = out.struct()
-        rc = self.lib.alto_stream_step(self.handle, _p(keys), _p(fan), fan.stride(0), _p(payload_i32),
+        rc = self.lib.alto_stream_step(self.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32),
                                        _p(payload_f32), n, _p(perm), _p(dest_offsets), _p(dest),
-                                       C.byref(G), _p(status), _p(self.ws), self.ws.numel(),
+                                       C.byref(G), _p(status), _p(self.ws), _nbytes(self.ws),
                                        _stream(stream))
         _check(rc, "alto_stream_step")
         return out, status
@@ -324,6 +467,13 @@ class Stream:
             out = new_groups(cap or self.max_live_leaves, self.La, self.op, self.dim, device=dev)
         if status is None:
             status = new_status(dev)
+        a = _Args("alto_stream_pending")
+        a.t(out.pend_key, "out.pend_key", _KEY_DTYPES, out.cap_groups, optional=True)
+        a.t(out.pend_count, "out.pend_count", torch.int64, out.cap_groups, optional=True)
+        a.t(out.counts, "out.counts", torch.int64, 4)
+        a.t(status, "status", torch.int32, 1)
+        if a.device() != self.state.device:
+            a.fail(f"arguments on {a.dev}, stream state on {self.state.device}")
         G = out.struct()
         rc = self.lib.alto_stream_pending(self.handle, C.byref(G), _p(status), _stream(stream))
         _check(rc, "alto_stream_pending")
@@ -390,8 +540,18 @@ class LoadRouter:
             counts = torch.zeros(2, dtype=torch.int64, device=dev)
         if status is None:
             status = new_status(dev)
+        a = _Args("alto_route_load")
+        a.t(keys, "keys", _KEY_DTYPES, n)
+        a.t(load, "load", torch.int64, self.D)
+        a.t(perm, "perm", torch.int32, n, optional=True)
+        a.t(dest_offsets, "dest_offsets", torch.int64, self.D + 1, optional=True)
+        a.t(dest, "dest", torch.int32, n, optional=True)
+        a.t(counts, "counts", torch.int64, 2)
+        a.t(status, "status", torch.int32, 1)
+        if a.device() != self.state.device:
+            a.fail(f"arguments on {a.dev}, router state on {self.state.device}")
         rc = self.lib.alto_route_load(self.handle, _p(keys), n, _p(load), _p(perm), _p(dest_offsets), _p(dest),
-                                      _p(counts), _p(status), _p(self.ws), self.ws.numel(), _stream(stream))
+                                      _p(counts), _p(status), _p(self.ws), _nbytes(self.ws), _stream(stream))
         _check(rc, "alto_route_load")
         return perm, dest_offsets, dest, counts, status
 
@@ -427,8 +587,17 @@ def join(left: torch.Tensor, right_keys: torch.Tensor, bits, level: int, match=N
         counts = torch.zeros(2, dtype=torch.int64, device=dev)
     if status is None:
         status = new_status(dev)
+    a = _Args("alto_join")
+    a.t(left, "left", _KEY_DTYPES, nl)
+    a.t(right_keys, "right_keys", _KEY_DTYPES, nr)
+    a.t(match, "match", torch.int32, nr)
+    a.t(hits, "hits", torch.int32, nl, optional=True)
+    a.t(counts, "counts", torch.int64, 2)
+    a.t(status, "status", torch.int32, 1)
+    a.t(ws, "ws", torch.uint8)
+    a.device()
     rc = lib.alto_join(_p(left), nl, _p(right_keys), nr, C.byref(L), level, _p(match), _p(hits), _p(counts),
-                       _p(status), _p(ws), ws.numel(), _stream(stream))
+                       _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_join")
     return match, hits, counts, status
 
@@ -463,9 +632,26 @@ def split(keys: torch.Tensor, fan: torch.Tensor, tokens: torch.Tensor, bits, del
         counts = torch.zeros(4, dtype=torch.int64, device=dev)
     if status is None:
         status = new_status(dev)
-    rc = lib.alto_split(_p(keys), _p(fan), fan.stride(0) if fan.dim() == 2 else m, _p(tokens), n,
-                        C.byref(L), delim, seg_bits, tok_bits, _p(out_keys), _p(out_fan), out_fan.stride(0),
+    a = _Args("alto_split")
+    a.t(keys, "keys", _KEY_DTYPES, n)
+    if isinstance(fan, torch.Tensor) and fan.dim() == 1 and d - 1 == 1:
+        a.t(fan, "fan", torch.int32, n)
+        fan_ld = m
+    else:
+        fan_ld = a.rows(fan, "fan", torch.int32, d - 1, n)
+    a.t(tokens, "tokens", torch.int32, n)
+    a.t(out_keys, "out_keys", _KEY_DTYPES, n)
+    out_fan_ld = a.rows(out_fan, "out_fan", torch.int32, d, n)
+    a.t(out_tokens, "out_tokens", torch.int32, n, optional=True)
+    a.t(out_idx, "out_idx", torch.int32, n, optional=True)
+    a.t(rest_idx, "rest_idx", torch.int32, n, optional=True)
+    a.t(counts, "counts", torch.int64, 4)
+    a.t(status, "status", torch.int32, 1)
+    a.t(ws, "ws", torch.uint8)
+    a.device()
+    rc = lib.alto_split(_p(keys), _p(fan), fan_ld, _p(tokens), n,
+                        C.byref(L), delim, seg_bits, tok_bits, _p(out_keys), _p(out_fan), out_fan_ld,
                         _p(out_tokens), _p(out_idx), _p(rest_idx) if rest_idx is not None else None,
-                        _p(counts), _p(status), _p(ws), ws.numel(), _stream(stream))
+                        _p(counts), _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_split")
     return out_keys, out_fan, out_tokens, out_idx, rest_idx, counts, status

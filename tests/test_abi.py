@@ -75,3 +75,66 @@ def test_join_split_router_sizing_host_checks():
     assert lib.alto_router_create(C.byref(L), 2, 4, 16, None, 0, None, C.byref(h)) == 1
     assert lib.alto_route_load(None, None, 0, None, None, None, None, None, None, None, 0, None) == 1
     assert lib.alto_read_probe(None, 16, None, None) == 1
+
+
+# ---- host-side checks of the Python binding: tensors that would make a kernel read
+# or write out of bounds are refused before anything reaches the library
+
+def _err(fn, *a, **k):
+    with pytest.raises(alto.AltoError) as e:
+        fn(*a, **k)
+    assert e.value.code == alto.E_ARG
+    return str(e.value)
+
+
+def test_binding_refuses_bad_tensors_for_aggregate():
+    import torch
+    bits = (6, 3, 2, 3, 5)
+    n = 10
+    keys = torch.zeros(n, dtype=torch.int64)
+    fan = torch.ones((4, n), dtype=torch.int32)
+    pf = torch.zeros((n, 8), dtype=torch.float32)
+    p32 = torch.zeros(n, dtype=torch.int32)
+    kw = dict(bits=bits, agg_level=4, op="mean", dim=8)
+    assert "keys has dtype" in _err(alto.aggregate, keys.to(torch.int32), fan, payload_f32=pf, **kw)
+    assert "fan is" in _err(alto.aggregate, keys, fan[:3], payload_f32=pf, **kw)            # too few levels
+    assert "fan is" in _err(alto.aggregate, keys, fan[:, :5], payload_f32=pf, **kw)         # too few fragments
+    assert "unit stride" in _err(alto.aggregate, keys, fan.t().contiguous().t(), payload_f32=pf, **kw)
+    assert "payload_f32 holds" in _err(alto.aggregate, keys, fan, payload_f32=pf[:5], **kw)
+    assert "rows hold" in _err(alto.aggregate, keys, fan, payload_f32=pf.reshape(n * 2, 4), **kw)
+    assert "contiguous" in _err(alto.aggregate, keys, fan, payload_f32=pf.t(), **kw)
+    assert "payload_f32 is required" in _err(alto.aggregate, keys, fan, **kw)
+    assert "payload_i32 is required" in _err(alto.aggregate, keys, fan, bits=bits, agg_level=4, op="concat")
+    out = alto.new_groups(n, 4, "mean", 8, device="cpu")
+    out.mean = out.mean[:3]
+    assert "out.mean holds" in _err(alto.aggregate, keys, fan, payload_f32=pf, out=out, **kw)
+    out = alto.new_groups(n, 4, "concat", 1, cap_tokens=n, device="cpu")
+    out.tok = out.tok[: n - 1]
+    assert "out.tok holds" in _err(alto.aggregate, keys, fan, bits=bits, agg_level=4, op="concat",
+                                   payload_i32=p32, out=out)
+    assert "perm holds" in _err(alto.aggregate, keys, fan, payload_f32=pf, perm=torch.zeros(3, dtype=torch.int32),
+                                **kw)
+    assert "dest_offsets holds" in _err(alto.aggregate, keys, fan, payload_f32=pf, route_level=2, num_dest=8,
+                                        dest_offsets=torch.zeros(8, dtype=torch.int64), **kw)
+    # well-formed host tensors get as far as the device check
+    assert "not on a GPU" in _err(alto.aggregate, keys, fan, payload_f32=pf, **kw)
+
+
+def test_binding_refuses_bad_tensors_for_route_join_split_pack():
+    import torch
+    n = 16
+    keys = torch.zeros(n, dtype=torch.int64)
+    assert "keys has dtype" in _err(alto.route, keys.float(), (31, 6, 12), 2, 4)
+    assert "perm holds" in _err(alto.route, keys, (31, 6, 12), 2, 4, perm=torch.zeros(2, dtype=torch.int32))
+    assert "not on a GPU" in _err(alto.route, keys, (31, 6, 12), 2, 4)
+    assert "match holds" in _err(alto.join, keys[:4], keys, (31, 6, 12), 2, match=torch.zeros(3, dtype=torch.int32))
+    assert "not on a GPU" in _err(alto.join, keys[:4], keys, (31, 6, 12), 2)
+    fan = torch.ones((2, n), dtype=torch.int32)
+    tok = torch.zeros(n, dtype=torch.int32)
+    assert "tokens holds" in _err(alto.split, keys, fan, tok[:3], (31, 6, 12), 0, 4, 4)
+    assert "out_fan is" in _err(alto.split, keys, fan, tok, (31, 6, 12), 0, 4, 4,
+                                out_fan=torch.zeros((2, n), dtype=torch.int32))
+    assert "not on a GPU" in _err(alto.split, keys, fan, tok, (31, 6, 12), 0, 4, 4)
+    path = torch.zeros((2, n), dtype=torch.int32)
+    assert "path is" in _err(alto.pack_keys, path, (31, 6, 12))
+    assert "not on a GPU" in _err(alto.pack_keys, torch.zeros((3, n), dtype=torch.int32), (31, 6, 12))

@@ -57,6 +57,26 @@ def test_aggregate_parity(case, op):
     U.compare(res, rt, g, op, Lm, La)
 
 
+@pytest.mark.parametrize("drop,Lr,seed", [(0.0, 4, 113), (0.01, 4, 113), (0.01, 3, 117)])
+def test_mean_dim128_groups_of_several_chunks(drop, Lr, seed):
+    # The 2^26-fragment workload's layout and launch (128-d rows, mean at level 4,
+    # mask at level 2, 256 destinations) at a size the oracle finishes quickly, with
+    # level-4 groups longer than one 4,096-row gather chunk (partial sums per chunk,
+    # combined in chunk order) and, with drop > 0, incomplete groups and masks.
+    bits = (3, 12, 12, 12, 12, 12)
+    path, fan, p32, pf = _case(seed, 6, bits, (2, 2, 3, 200, 60), 2, drop, 128)
+    keys = O.pack_keys(path, bits)
+    _, cnt = np.unique(O.prefix(keys, bits, 4), return_counts=True)
+    assert (cnt > 4096).sum() >= 2 and (cnt <= 256).sum() + ((cnt > 256) & (cnt <= 4096)).sum() >= 1
+    code, rt, g = U.oracle_aggregate(keys, fan, bits, 4, "mean", 128, 2, Lr, 256, p32, pf)
+    assert code == O.OK
+    if drop:
+        assert len(g.pend_key) > 0 and (g.mask == 0).any()
+    res = U.run_aggregate(keys, fan, bits, 4, "mean", 128, 2, Lr, 256, p32, pf)
+    assert res["status"] == O.OK
+    U.compare(res, rt, g, "mean", 2, 4)
+
+
 def test_pack_parity_and_layout_error():
     bits = (31, 2, 3, 4)
     path, fan, _, _ = _case(5, 4, bits, (4, 8, 16), 64)

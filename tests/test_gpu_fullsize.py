@@ -18,6 +18,37 @@ def log(msg):
     print(f"[fullsize] {msg}", flush=True)
 
 
+def _group_rows(gk):
+    """Input rows of every group (ascending group key): (groups, order, starts, counts)
+    with the rows of group i at order[starts[i]:starts[i] + counts[i]]."""
+    order = np.argsort(gk, kind="stable")
+    groups, starts, counts = np.unique(gk[order], return_index=True, return_counts=True)
+    return groups, order, starts, counts
+
+
+def _oracle_means(payload, rows_of, idx):
+    """The oracle's pooled vector of each listed group, one group at a time (rows
+    gathered from the device-resident payload with torch indexing)."""
+    out = []
+    for i in idx:
+        r = torch.from_numpy(rows_of(i)).cuda()
+        out.append(O.group_mean(payload.index_select(0, r).cpu().numpy()))
+    return np.stack(out) if out else np.zeros((0, payload.shape[1]), np.float32)
+
+
+def _zipf_call(w, keys, n):
+    perm = torch.empty(n, dtype=torch.int32, device="cuda")
+    offs = torch.empty(w.num_dest + 1, dtype=torch.int64, device="cuda")
+    dest = torch.empty(n, dtype=torch.int32, device="cuda")
+    out = alto.new_groups(1 << 16, w.agg_level, "mean", w.dim, cap_mask=1 << 16, with_first=False)
+    _, _, _, out, st = alto.aggregate(keys, w.fan, w.bits, w.agg_level, "mean", w.dim, w.mask_level,
+                                      w.route_level, w.num_dest, None, w.payload_f32, perm=perm,
+                                      dest_offsets=offs, dest=dest, out=out, n=n)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    return perm, offs, dest, out
+
+
 def test_zipf_64M_mean_mask():
     log("config: zipf depth-6, 2^26 fragments, 128-d mean at level 4, mask at level 2")
     w = W.config5("cuda")
@@ -28,15 +59,7 @@ def test_zipf_64M_mean_mask():
     hkeys = O.pack_keys(w.path.cpu().numpy(), w.bits)
     assert np.array_equal(keys.cpu().numpy().view(np.uint64), hkeys)
     w.path = None
-    perm = torch.empty(n, dtype=torch.int32, device="cuda")
-    offs = torch.empty(w.num_dest + 1, dtype=torch.int64, device="cuda")
-    dest = torch.empty(n, dtype=torch.int32, device="cuda")
-    out = alto.new_groups(1 << 16, w.agg_level, "mean", w.dim, cap_mask=1 << 16, with_first=False)
-    _, _, _, out, st = alto.aggregate(keys, w.fan, w.bits, w.agg_level, "mean", w.dim, w.mask_level,
-                                      w.route_level, w.num_dest, None, w.payload_f32, perm=perm,
-                                      dest_offsets=offs, dest=dest, out=out, n=n)
-    torch.cuda.synchronize()
-    assert int(st.item()) == 0
+    perm, offs, dest, out = _zipf_call(w, keys, n)
     log("gpu done; checking routing")
     odest = O.route_dest(hkeys, w.bits, w.route_level, w.num_dest)
     assert np.array_equal(dest.cpu().numpy(), odest)
@@ -46,10 +69,11 @@ def test_zipf_64M_mean_mask():
     assert (np.bincount(p, minlength=n) == 1).all()                      # a permutation
     d, k = odest[p], hkeys[p]
     assert ((d[1:] > d[:-1]) | ((d[1:] == d[:-1]) & (k[1:] > k[:-1]))).all()   # strictly by (dest, key)
+    del p, d, k
     log("checking groups")
     E, T, M, P = [int(x) for x in out.counts.cpu()]
     gk = O.prefix(hkeys, w.bits, w.agg_level)
-    nodes, cnt = np.unique(gk, return_counts=True)
+    nodes, order, starts, cnt = _group_rows(gk)
     gd = O.route_dest(nodes << np.uint64(O.shift_below(w.bits, w.agg_level)), w.bits, w.route_level,
                       w.num_dest)
     o = np.lexsort((nodes, gd))
@@ -61,17 +85,35 @@ def test_zipf_64M_mean_mask():
     assert M == len(m2)
     assert np.array_equal(out.mask_key[:M].cpu().numpy().view(np.uint64), m2)
     assert (out.mask[:M].cpu().numpy() == 1).all()
-    log("checking sampled means")
+    log(f"checking all {E} means against the oracle")
+    rows_of = lambda i: order[starts[o[i]]:starts[o[i]] + cnt[o[i]]]
+    U.assert_mean_close(out.mean[:E].cpu().numpy(), _oracle_means(w.payload_f32, rows_of, range(E)))
+    # the same batch without its last arrival: one leaf missing leaves its
+    # level-5 node, its group and every ancestor incomplete
+    log("again without the last fragment in arrival order")
+    perm, offs, dest, out = _zipf_call(w, keys, n - 1)
+    miss = int(gk[n - 1])
+    gi = int(np.searchsorted(nodes, np.uint64(miss)))
+    E2, _, M2, P2 = [int(x) for x in out.counts.cpu()]
+    keep = o[nodes[o] != np.uint64(miss)]
+    assert (E2, P2, M2) == (E - 1, 1, M)
+    assert np.array_equal(out.key[:E2].cpu().numpy().view(np.uint64), nodes[keep])
+    assert np.array_equal(out.count[:E2].cpu().numpy(), cnt[keep])
+    assert out.pend_key[:1].cpu().numpy().view(np.uint64)[0] == miss
+    assert int(out.pend_count[0]) == int(cnt[gi]) - 1
+    mk = O.prefix(hkeys[n - 1:n], w.bits, w.mask_level)[0]
+    mask = out.mask[:M2].cpu().numpy()
+    assert np.array_equal(out.mask_key[:M2].cpu().numpy().view(np.uint64), m2)
+    assert list(mask) == [0 if k == mk else 1 for k in m2]
+    pos = {int(x): j for j, x in enumerate(nodes[o])}
     rng = np.random.default_rng(5)
-    order_groups = nodes[o]
-    picks = sorted(set([int(np.argmax(cnt[o])), int(np.argmin(cnt[o]))] +
-                       rng.choice(E, size=10, replace=False).tolist()))
-    gmean = out.mean[:E].cpu().numpy()
-    for i in picks:
-        rows = np.nonzero(gk == order_groups[i])[0]
-        x = w.payload_f32[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
-        ref = (x.sum(axis=0) / len(rows)).astype(np.float32)
-        U.assert_mean_close(gmean[i:i + 1], ref[None])
+    picks = rng.choice(E2, size=min(E2, 24), replace=False)
+    got = out.mean[:E2].cpu().numpy()[picks]
+    U.assert_mean_close(got, _oracle_means(w.payload_f32, rows_of, [pos[int(nodes[keep][j])] for j in picks]))
+    p = perm[:n - 1].cpu().numpy()
+    assert np.array_equal(np.sort(p), np.arange(n - 1))
+    d, k = odest[p], hkeys[p]
+    assert ((d[1:] > d[:-1]) | ((d[1:] == d[:-1]) & (k[1:] > k[:-1]))).all()
 
 
 def test_factool_batch_two_stages():
@@ -103,10 +145,10 @@ def test_factool_stream_10000_steps():
     ring_rows = ring.shape[0]
     keys_d, st = alto.pack_keys(w.path, w.bits)
     torch.cuda.synchronize()
-    hkeys = keys_d.cpu().numpy().view(np.uint64)
+    hkeys = O.pack_keys(w.path.cpu().numpy(), w.bits)
     hfan = w.fan.cpu().numpy()
     hdoc = w.payload_i32.cpu().numpy()
-    assert np.array_equal(hkeys, O.pack_keys(w.path.cpu().numpy(), w.bits))
+    assert np.array_equal(keys_d.cpu().numpy().view(np.uint64), hkeys)
     sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22, step_max=step)
     sbB = W.CONFIG2_STAGE_B
     sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
@@ -120,31 +162,42 @@ def test_factool_stream_10000_steps():
     declared = hfan[3][o][first_idx]
     complete = cnt == declared
     want_step = dict(zip(docs[complete].tolist(), last_step[complete].tolist()))
-    rng = np.random.default_rng(9)
-    sample = set(rng.choice(docs[complete], size=12, replace=False).tolist())
-    got_step, got_first, got_count, got_mean = {}, {}, {}, {}
+    full_steps = set(range(0, steps, max(steps // 100, 1)))     # every document and the routing checked
+    got_step, got_first, got_count = {}, {}, {}
+    step_means = {}
     recB_keys, recB_step = [], []
     claims_got = {}
     gA = alto.new_groups(step, 4, "mean", 768, device="cuda")
     gB = alto.new_groups(step, 2, "concat", 1, cap_tokens=(1 << 16) + step, device="cuda")
     stA, stB = alto.new_status(), alto.new_status()
+    perm = torch.empty(step, dtype=torch.int32, device="cuda")
+    offs = torch.empty(33, dtype=torch.int64, device="cuda")
+    dest = torch.empty(step, dtype=torch.int32, device="cuda")
+    checked_route = 0
     for s in range(steps):
         a, b = s * step, (s + 1) * step
         r0 = (s * step) % ring_rows
         stA.zero_()
-        sA.step(keys_d[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gA, status=stA)
+        full = s in full_steps
+        sA.step(keys_d[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gA, status=stA,
+                perm=perm if full else None, dest_offsets=offs if full else None, dest=dest if full else None)
         torch.cuda.synchronize()
         assert int(stA.item()) == 0, s
         E = int(gA.counts[0])
+        if full:
+            rt = O.route(hkeys[a:b], w.bits, 2, 32)
+            assert np.array_equal(perm.cpu().numpy(), rt.perm), s
+            assert np.array_equal(dest.cpu().numpy(), rt.dest), s
+            assert np.array_equal(offs.cpu().numpy(), rt.dest_offsets), s
+            step_means[s] = (gA.key[:E].cpu().numpy().view(np.uint64).copy(), gA.mean[:E].cpu().numpy())
+            checked_route += 1
         stB.zero_()
         sB.step(gA.key[:E], gA.fan_up.view(3, -1)[:, :E], gA.first_i32[:E], None, out=gB, status=stB, n=E)
         torch.cuda.synchronize()
         assert int(stB.item()) == 0, s
         ks = gA.key[:E].cpu().numpy().view(np.uint64)
-        for i, kk in enumerate(ks.tolist()):
+        for kk in ks.tolist():
             got_step[kk] = s
-            if kk in sample:
-                got_mean[kk] = gA.mean[i].cpu().numpy()
         got_first.update(zip(ks.tolist(), gA.first_i32[:E].cpu().numpy().tolist()))
         got_count.update(zip(ks.tolist(), gA.count[:E].cpu().numpy().tolist()))
         EB, TB = int(gB.counts[0]), int(gB.counts[1])
@@ -160,10 +213,19 @@ def test_factool_stream_10000_steps():
     doc_first = dict(zip(docs.tolist(), hdoc[o][first_idx].tolist()))
     assert all(got_first[k] == doc_first[k] for k in got_step)
     assert all(got_count[k] == int(c) for k, c in zip(docs[complete].tolist(), cnt[complete].tolist()))
-    for kk in sample:
-        rows = np.nonzero(gk == np.uint64(kk))[0]
-        x = ring[torch.from_numpy(rows % ring_rows).cuda()].cpu().numpy().astype(np.float64)
-        U.assert_mean_close(got_mean[kk][None], (x.sum(axis=0) / len(rows)).astype(np.float32)[None])
+    log(f"checking every document mean of {len(step_means)} steps (routing of those steps: {checked_route})")
+    assert len(step_means) >= 100
+    ndocs = 0
+    for s, (ks, means) in sorted(step_means.items()):
+        di = np.searchsorted(docs, ks)
+        ref = []
+        for j in di:
+            rows = o[first_idx[j]:first_idx[j] + cnt[j]]
+            ref.append(O.group_mean(ring.index_select(0, torch.from_numpy(rows % ring_rows).cuda()).cpu().numpy()))
+        if len(ref):
+            U.assert_mean_close(means, np.stack(ref))
+        ndocs += len(ks)
+    log(f"{ndocs} document means checked")
     log("checking claims")
     # a claim is emitted once all its documents were emitted, in the step of the last one
     ck = O.prefix(docs, (31, 3, 2, 3), 2)

@@ -869,3 +869,27 @@ def test_load_router_errors():
     assert r.table == {1: 0}                             # nothing changed
     out = r.route(_keys2([(2, 0), (1, 1)]), [0, 0])
     assert out.counts.tolist() == [1, 1] and r.table == {1: 0, 2: 1}
+
+
+def test_group_mean_of_one_group_matches_aggregate_and_exact_means():
+    # group_mean (one group's rows at a time) against aggregate's means of the same
+    # groups (pinned above against the brute-force model) and, for dyadic rows,
+    # against the exact rational mean rounded once.
+    bits = (31, 3, 2, 3, 8)
+    path, fan = W.random_tree(15, 5, 5, (6, 3, 5, 30), bits)
+    rng = np.random.default_rng(16)
+    x = rng.standard_normal((path.shape[1], 24)).astype(np.float32)
+    (sp, sf, xt), _ = W.permute([path, fan, x.T], 17)
+    x = np.ascontiguousarray(xt.T)
+    keys = O.pack_keys(sp, bits)
+    _, g = O.aggregate(keys, sf, bits, 3, "mean", 24, 0, 2, 32, None, x)
+    gk = O.prefix(keys, bits, 3)
+    for i, k in enumerate(g.key):
+        rows = x[gk == k]
+        assert np.array_equal(O.group_mean(rows[::-1]), g.mean[i]) or \
+            np.abs(O.group_mean(rows[::-1]) - g.mean[i]).max() <= 1e-6 * np.abs(g.mean[i]).max()
+    ints = rng.integers(-64, 64, size=(37, 5))
+    want = np.array([float(Fraction(int(c), 16 * 37)) for c in ints.sum(axis=0)]).astype(np.float32)
+    assert np.array_equal(O.group_mean((ints / 16.0).astype(np.float32)), want)
+    with pytest.raises(O.OracleError):
+        O.group_mean(np.zeros((0, 3), np.float32))
