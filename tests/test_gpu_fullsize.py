@@ -218,12 +218,14 @@ def test_factool_stream_10000_steps():
     ndocs = 0
     for s, (ks, means) in sorted(step_means.items()):
         di = np.searchsorted(docs, ks)
-        ref = []
-        for j in di:
-            rows = o[first_idx[j]:first_idx[j] + cnt[j]]
-            ref.append(O.group_mean(ring.index_select(0, torch.from_numpy(rows % ring_rows).cuda()).cpu().numpy()))
-        if len(ref):
-            U.assert_mean_close(means, np.stack(ref))
+        if len(di) == 0:
+            continue
+        rows = [o[first_idx[j]:first_idx[j] + cnt[j]] for j in di]
+        allrows = np.concatenate(rows)
+        x = ring.index_select(0, torch.from_numpy(allrows % ring_rows).cuda()).cpu().numpy()   # one copy per step
+        ends = np.cumsum([len(r) for r in rows])
+        ref = [O.group_mean(x[e - len(r):e]) for r, e in zip(rows, ends)]
+        U.assert_mean_close(means, np.stack(ref))
         ndocs += len(ks)
     log(f"{ndocs} document means checked")
     log("checking claims")
