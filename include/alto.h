@@ -16,7 +16,8 @@
  * Conventions for every entry point:
  *  - Array arguments are DEVICE pointers owned by the caller. The library never
  *    allocates device memory; temporary memory comes from a caller workspace sized
- *    by alto_workspace_bytes(). Struct arguments (alto_layout, alto_agg,
+ *    by alto_workspace_bytes() (alto_aggregate_noalloc instead uses a fixed array
+ *    of the library's own, see there). Struct arguments (alto_layout, alto_agg,
  *    alto_groups) are HOST pointers to structs whose array members are device
  *    pointers.
  *  - Calls only enqueue work on the given stream and return without synchronising.
@@ -160,6 +161,27 @@ int alto_aggregate(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
                    int32_t num_dest, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
                    alto_groups *out, int32_t *status, void *ws, size_t ws_bytes,
                    hipStream_t stream);
+
+/* ---- alto_aggregate without a workspace argument ----
+ * For callers that cannot allocate device memory at the time of the call (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, outputs, orders and errors as alto_aggregate, without ws and
+ * ws_bytes: the workspace is a fixed array of ALTO_NOALLOC_SCRATCH_BYTES in the
+ * library's own device memory, one per GPU, held from the first call on that GPU
+ * until the process ends. Calls with alto_workspace_bytes(layout, n, num_dest,
+ * agg) > ALTO_NOALLOC_SCRATCH_BYTES return ALTO_E_ARG (nothing is enqueued); for
+ * the layouts of this library that is about 600k fragments with a 128-float mean,
+ * 900k with a 768-float one. The call allocates nothing. Every call on one GPU
+ * shares that GPU's array, and it keeps what the last call left there: calls on
+ * one GPU that overlap in time (different streams, or different host threads)
+ * race on it and give undefined outputs; serialise them. ALTO_E_HIP if the
+ * array's device address cannot be obtained. */
+#define ALTO_NOALLOC_SCRATCH_BYTES (128ull << 20)
+int alto_aggregate_noalloc(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                           const int32_t *payload_i32, const float *payload_f32, int64_t n,
+                           const alto_layout *layout, const alto_agg *agg, int32_t route_level,
+                           int32_t num_dest, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
+                           alto_groups *out, int32_t *status, hipStream_t stream);
 
 /* ---- streams: partial groups carried across steps (Section 3.1: outputs stream
  * before their inputs are complete; Section 4.2: aggregation at pmap exit) ---- */

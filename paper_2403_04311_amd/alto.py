@@ -28,7 +28,8 @@ EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggrega
            "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join",
            "alto_split_workspace_bytes", "alto_split", "alto_router_state_bytes", "alto_router_create",
            "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load", "alto_profile_phases",
-           "alto_read_probe")
+           "alto_read_probe", "alto_aggregate_noalloc")
+NOALLOC_SCRATCH_BYTES = 128 << 20   # ALTO_NOALLOC_SCRATCH_BYTES of include/alto.h
 
 
 class Layout(C.Structure):
@@ -76,6 +77,9 @@ def load():
     lib.alto_aggregate.restype = C.c_int
     lib.alto_aggregate.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
                                    vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp]
+    lib.alto_aggregate_noalloc.restype = C.c_int
+    lib.alto_aggregate_noalloc.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
+                                           vp, vp, vp, C.POINTER(Groups), vp, vp]
     lib.alto_stream_state_bytes.restype = C.c_size_t
     lib.alto_stream_state_bytes.argtypes = [C.POINTER(Layout), C.POINTER(Agg), i64, i64]
     lib.alto_stream_create.restype = C.c_int
@@ -401,6 +405,41 @@ def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0
                             _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_aggregate")
     return perm, dest_offsets, dest, out, status
+
+
+def aggregate_noalloc(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0, num_dest=1,
+                      payload_i32=None, payload_f32=None, perm=None, dest_offsets=None, dest=None,
+                      out: Optional[GroupTensors] = None, status=None, stream=None, n=None):
+    """alto_aggregate_noalloc: as ``aggregate`` with every output given by the caller
+    and no workspace (the library's own fixed device array serves as one; calls on
+    one GPU must not overlap). Nothing is allocated here either: perm, dest_offsets,
+    dest, out and status are required. Returns status."""
+    lib = load()
+    a = _Args("alto_aggregate_noalloc")
+    n = keys.shape[0] if n is None else n
+    a.t(keys, "keys", _KEY_DTYPES, n)
+    fan_ld = a.rows(fan, "fan", torch.int32, len(bits) - 1, n)
+    a.t(payload_i32, "payload_i32", torch.int32, n, optional=op != "concat")
+    a.payload(payload_f32, "payload_f32", n, dim, optional=op != "mean")
+    a.t(perm, "perm", torch.int32, n)
+    a.t(dest_offsets, "dest_offsets", torch.int64, num_dest + 1)
+    a.t(dest, "dest", torch.int32, n)
+    if out is None:
+        a.fail("out is required")
+    out.check(a, op, agg_level, dim)
+    a.t(status, "status", torch.int32, 1)
+    need = workspace_bytes(bits, n, num_dest, agg_level, op, dim, mask_level)
+    if need == 0 or need > NOALLOC_SCRATCH_BYTES:
+        a.fail(f"needs {need} bytes of workspace, more than the fixed {NOALLOC_SCRATCH_BYTES}")
+    a.device()
+    L = layout(bits)
+    A = agg_struct(agg_level, op, dim, mask_level)
+    G = out.struct()
+    rc = lib.alto_aggregate_noalloc(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n, C.byref(L),
+                                    C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets), _p(dest),
+                                    C.byref(G), _p(status), _stream(stream))
+    _check(rc, "alto_aggregate_noalloc")
+    return status
 
 
 class Stream:

@@ -1,8 +1,14 @@
 // Host entry points of the C ABI declared in include/alto.h.
 #include <limits.h>
+#include <mutex>
 #include <string.h>
 
 #include "aggregate.h"
+
+// Workspace of alto_aggregate_noalloc: one array per GPU, held until the process
+// ends. Host code never uses this name as an address (on the host it only stands
+// for the symbol); each device's address comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[ALTO_NOALLOC_SCRATCH_BYTES];
 
 KeyGeom make_geom(const alto_layout* l) {
   KeyGeom g;
@@ -93,6 +99,29 @@ GroupOut to_dev_out(const alto_groups* o) {
 
 }  // namespace
 
+namespace {
+constexpr int NOALLOC_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[NOALLOC_MAX_DEVICES];
+
+// Device address of the scratch array on the current device, looked up once per
+// device (with that device current); null if the lookup fails.
+void* scratch_on_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= NOALLOC_MAX_DEVICES) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
 extern "C" {
 
 size_t alto_workspace_bytes(const alto_layout* layout, int64_t n_max, int32_t num_dest, const alto_agg* agg) {
@@ -172,6 +201,22 @@ int alto_aggregate(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, con
   if (!c.ok) return ALTO_E_ARG;
   return aggregate_run(g, rg, route_level, *agg, keys, fan, fan_ld, payload_i32, payload_f32, n, b, perm,
                        dest_offsets, dest, o, status, stream);
+}
+
+
+int alto_aggregate_noalloc(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
+                           const float* payload_f32, int64_t n, const alto_layout* layout, const alto_agg* agg,
+                           int32_t route_level, int32_t num_dest, int32_t* perm, int64_t* dest_offsets,
+                           int32_t* dest, alto_groups* out, int32_t* status, hipStream_t stream) {
+  if (!layout_ok(layout) || n < 0 || n > N_LIMIT || num_dest < 1 || num_dest > (1 << 24) ||
+      !agg_ok(layout, agg, route_level, num_dest))
+    return ALTO_E_ARG;
+  const size_t need = alto_workspace_bytes(layout, n, num_dest, agg);
+  if (need == 0 || need > (size_t)ALTO_NOALLOC_SCRATCH_BYTES) return ALTO_E_ARG;   // too large for the scratch
+  void* ws = scratch_on_current_device();
+  if (!ws) return ALTO_E_HIP;
+  return alto_aggregate(keys, fan, fan_ld, payload_i32, payload_f32, n, layout, agg, route_level, num_dest, perm,
+                        dest_offsets, dest, out, status, ws, (size_t)ALTO_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"

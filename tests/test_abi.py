@@ -138,3 +138,26 @@ def test_binding_refuses_bad_tensors_for_route_join_split_pack():
     path = torch.zeros((2, n), dtype=torch.int32)
     assert "path is" in _err(alto.pack_keys, path, (31, 6, 12))
     assert "not on a GPU" in _err(alto.pack_keys, torch.zeros((3, n), dtype=torch.int32), (31, 6, 12))
+
+
+def test_noalloc_entry_point_refuses_inputs_larger_than_its_array():
+    # refused on the host, before anything is enqueued or any device is touched
+    bits = (3, 12, 12, 12, 12, 12)
+    n = 1 << 21
+    assert alto.workspace_bytes(bits, n, 256, 4, "mean", 128, 2) > alto.NOALLOC_SCRATCH_BYTES
+    lib = alto.load()
+    L, A = alto.layout(bits), alto.agg_struct(4, "mean", 128, 2)
+    G = alto.Groups()
+    rc = lib.alto_aggregate_noalloc(None, None, n, None, None, n, C.byref(L), C.byref(A), 4, 256,
+                                    None, None, None, C.byref(G), None, None)
+    assert rc == alto.E_ARG
+    import torch
+    small = 1000
+    assert "more than the fixed" in _err(alto.aggregate_noalloc, torch.zeros(n, dtype=torch.int64),
+                                         torch.ones((5, n), dtype=torch.int32), bits, 4, "mean", 128, 2, 4, 256,
+                                         payload_f32=torch.zeros((n, 128)),
+                                         perm=torch.zeros(n, dtype=torch.int32),
+                                         dest_offsets=torch.zeros(257, dtype=torch.int64),
+                                         dest=torch.zeros(n, dtype=torch.int32),
+                                         out=alto.new_groups(small, 4, "mean", 128, cap_mask=small, device="cpu"),
+                                         status=torch.zeros(1, dtype=torch.int32))
