@@ -49,7 +49,18 @@ struct BatchSrc {
   int64_t fan_ld;
   const float* pf;
   int dim;
-  __device__ int64_t row(int64_t e) const { return perm[e]; }
+  int64_t n;
+  int32_t* status;
+  // perm is a permutation of 0..n-1 unless the input had duplicate keys: with direct
+  // placement a position is then left at DP_UNPLACED, reported here as DUPLICATE
+  // (the gathers read every position of the complete groups, i.e. all of them); the
+  // row is kept in bounds either way
+  __device__ int64_t row(int64_t e) const {
+    const uint32_t r = perm[e];
+    if (r < (uint64_t)n) return (int64_t)r;
+    raise_status(status, ALTO_E_DUPLICATE);
+    return 0;
+  }
   __device__ int32_t p32_of(int64_t r) const { return p32 ? p32[r] : 0; }
   __device__ int32_t fan_of(int m, int64_t r) const { return fan[(int64_t)(m - 1) * fan_ld + r]; }
   __device__ const float* pay_of(int64_t r) const { return pf + r * (int64_t)dim; }
@@ -130,9 +141,11 @@ void agg_levels(const KeyGeom& g, int La, int Lm, int Lr, int* Lt, int* Lseg);
 // to the general sort)
 void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const alto_agg* agg, int Lr, WsCarver& c,
                   AggBufs& b, int64_t flow_cap = FLOW_CAP);
+// allow_dp: a batch aggregation may use direct placement (FlowBufs.dp)
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st, bool offsets_later = false, bool exact_flow_levels = false);
+              int32_t* status, hipStream_t st, bool offsets_later = false, bool exact_flow_levels = false,
+              bool allow_dp = false);
 // Groups, chunk lists, counts and payload gathers over an element array already
 // segmented at level La (nodes in b.lv[La]); elements sorted by (dest, key).
 template <typename Src>

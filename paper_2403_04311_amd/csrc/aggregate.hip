@@ -23,8 +23,8 @@ __device__ inline int64_t dev_or(const int64_t* p, int64_t h) { return p ? *p : 
 // their counts compared there) when the block ends. The other levels add their
 // terms to the fan fingerprint (sums stay in registers). Each thread keeps PU
 // elements in flight; each block leaves one record of partial results.
-constexpr int PU = 4;
-constexpr int PREP_GRID = 512;          // two blocks of PREP_NT threads per CU
+constexpr int PU = 2;
+constexpr int PREP_GRID = PREP_BLOCKS_MAX;   // two blocks of PREP_NT threads per CU
 constexpr int PREP_SLOTS = 3072;        // LDS flow set of a block (open addressing)
 constexpr int PREP_PROBES = 4;          // then the global set directly: when the flows outnumber the
                                         // slots the block's set fills up, and a long walk over it
@@ -49,7 +49,7 @@ __device__ inline bool flow_fan_check(const FlowBufs& fl, int x, int nx, int64_t
 }
 
 template <int NL>
-__global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
+__global__ __launch_bounds__(PREP_NT, 8) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
                                                   RouteGeom rg, int32_t* dest, const int32_t* __restrict__ fan,
                                                   int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part, int qx0,
                                                   int nx, int skip_fp) {
@@ -68,6 +68,8 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
   bool bad_layout = false, bad_fan = false, flow_full = false;
   __shared__ uint64_t s_fl[PREP_SLOTS];
   __shared__ uint32_t s_ff[PREP_NX][PREP_SLOTS];
+  __shared__ uint32_t s_mk;
+  if (threadIdx.x == 0) s_mk = 0u;
   if (fl.hcap) {
     for (int i = threadIdx.x; i < PREP_SLOTS; i += PREP_NT) {
       s_fl[i] = ~0ull;
@@ -150,7 +152,25 @@ __global__ __launch_bounds__(PREP_NT) void k_prep(const uint64_t* __restrict__ k
         bad_fan |= (f[u][q] < 1) || ((int64_t)child >= (int64_t)f[u][q]);
         if (!skip_fp || q < qx0 || q >= qx0 + nx) fp[q] += fan_term(flo + q, key_prefix(k[u], sh[q]), (uint32_t)f[u][q]);
       }
+      if (NL > 0 && fl.dp) {
+        // markers (direct placement): leaves whose tag is their parent's count - 1,
+        // listed in the block's own region (an LDS counter: few markers per block)
+        const int32_t fl_ = f[u][NL > 0 ? NL - 1 : 0];
+        const uint32_t leaf = (uint32_t)((k[u] >> shc[NL > 0 ? NL - 1 : 0]) & (uint64_t)tm[NL > 0 ? NL - 1 : 0]);
+        if (fl_ >= 1 && leaf == (uint32_t)(fl_ - 1)) {
+          const uint32_t j = atomicAdd(&s_mk, 1u);
+          if (j < (uint32_t)fl.mk_per) {
+            const int64_t at = (int64_t)blockIdx.x * fl.mk_per + j;
+            fl.mk_key[at] = k[u];
+            fl.mk_fan[at] = (uint32_t)fl_;
+          }
+        }
+      }
     }
+  }
+  if (fl.dp) {
+    __syncthreads();
+    if (threadIdx.x == 0) fl.mk_cnt[blockIdx.x] = s_mk;
   }
   if (fl.hcap) {
     // the block's flows into the global set, with their counts
@@ -303,6 +323,7 @@ __global__ void k_route_init(SortCtl* ctl, uint64_t* fp_in, uint64_t* fp_nodes, 
       ctl->nflows = 0;
       ctl->nflows_c = 0;
       ctl->cmode = 0;
+      ctl->dp = 0;
       ctl->dbits = -1;
     }
     for (int i = threadIdx.x; i <= ALTO_MAX_LEVELS; i += blockDim.x) {
@@ -316,6 +337,91 @@ __global__ void k_route_init(SortCtl* ctl, uint64_t* fp_in, uint64_t* fp_nodes, 
     fl.ht_fan[i] = 0u;
 #pragma unroll
     for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) fl.ht_anc[(int64_t)x * fl.hcap + i] = 0u;
+  }
+}
+
+// Direct placement (see FlowBufs.dp), after the sort: the groups are the flows,
+// their bounds the child-rank bases of their first children (with check_all, also
+// the search for positions left unplaced, when no gather reads them all). Writes what the segmentation pass writes for the group level:
+// node starts, complete flags, declared and carried counts, the node side of the
+// fingerprints of those levels, destination offsets, and the sorted key at each
+// group start (its prefix bits: the group's key and destination come from it).
+__global__ __launch_bounds__(256) void k_dp_groups(KeyGeom g, FlowBufs fl, const SortCtl* ctl, int64_t n, int La,
+                                                   LevelNodes L, int64_t* nnodes, int64_t* dest_offsets,
+                                                   uint32_t num_dest, uint64_t* sk, const uint32_t* perm,
+                                                   const int32_t* fan, int64_t fan_ld, int carry_lo,
+                                                   int32_t* carry_fan, int64_t carry_ld, uint64_t* fp_nodes,
+                                                   int32_t* status, int check_all) {
+  if (!ctl->dp) return;
+  const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  if (check_all) {
+    // no gather reads the whole permutation in this call: look for unplaced
+    // positions here
+    bool hole = false;
+    for (int64_t i = gtid; i < n; i += stride) hole |= perm[i] == DP_UNPLACED;
+    if (__ballot(hole) && lane_id() == 0) raise_status(status, ALTO_E_DUPLICATE);
+  }
+  const int64_t F = ctl->nflows_c;
+  const int nc = La - carry_lo;   // carried levels carry_lo .. La-1
+  uint64_t fpm = 0;
+  uint64_t fpc[ALTO_MAX_LEVELS];
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q) fpc[q] = 0;
+  for (int64_t r = gtid; r < F; r += stride) {
+    // with direct placement chosen, cbase rises strictly (every count >= 1) from 0 to
+    // n; the clamps only keep every later index in bounds
+    int64_t s = fl.cbase[fl.fbase[r]], e = fl.cbase[fl.fbase[r + 1]];
+    s = s < n ? s : n;
+    e = e < n ? e : n;
+    const int64_t cnt = e > s ? e - s : 0;
+    L.start[r] = (int32_t)s;
+    L.ok[r] = 1;
+    L.bad[r] = 0;
+    if (cnt == 0) {
+      L.nfan[r] = 0;
+      continue;
+    }
+    // the first leaf's row (a position left unwritten holds no row: duplicate keys,
+    // reported by whoever reads the permutation; any row in bounds serves then)
+    const uint32_t row0 = perm[s];
+    const uint32_t row = (int64_t)row0 < n ? row0 : 0u;
+    const uint64_t pk = fl.flow_sorted[r] << fl.shift;
+    const int32_t nf = fan[(int64_t)(La - 1) * fan_ld + row];
+    L.nfan[r] = nf;
+    sk[s] = pk;
+    fpm += (uint64_t)cnt * fan_term(La, key_prefix(pk, g.shift[La]), (uint32_t)nf);
+#pragma unroll
+    for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
+      if (q >= nc) break;
+      const int m = carry_lo + q;
+      const int32_t cf = fan[(int64_t)(m - 1) * fan_ld + row];
+      if (carry_fan) carry_fan[(int64_t)q * carry_ld + r] = cf;
+      fpc[q] += (uint64_t)cnt * fan_term(m, key_prefix(pk, g.shift[m]), (uint32_t)cf);
+    }
+    if (dest_offsets) {
+      const uint32_t d = fl.fdest[r];
+      if (r == 0) {
+        for (uint32_t x = 0; x <= d; ++x) dest_offsets[x] = 0;
+      } else {
+        const uint32_t dp = fl.fdest[r - 1];
+        for (uint32_t x = dp + 1; x <= d; ++x) dest_offsets[x] = s;
+      }
+      if (r == F - 1)
+        for (uint32_t x = d + 1; x <= num_dest; ++x) dest_offsets[x] = n;
+    }
+  }
+  if (gtid == 0) {
+    nnodes[La] = F;
+    L.start[F] = (int32_t)n;
+  }
+  fpm = wave_sum(fpm);
+  if (lane_id() == 0 && fpm) atomicAdd((unsigned long long*)&fp_nodes[La], (unsigned long long)fpm);
+#pragma unroll
+  for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
+    if (q >= nc) break;
+    const uint64_t v = wave_sum(fpc[q]);
+    if (lane_id() == 0 && v) atomicAdd((unsigned long long*)&fp_nodes[carry_lo + q], (unsigned long long)v);
   }
 }
 
@@ -857,6 +963,18 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   int Lt, Lseg;
   agg_levels(g, agg->level, agg->mask_level, Lr, &Lt, &Lseg);
   const int d = g.depth;
+  if (b.fl.hcap && agg->level == Lr && d == Lr + 2 && (agg->mask_level == 0 || agg->mask_level <= agg->level)) {
+    // direct placement: groups are the flows, leaves one level below their children
+    FlowBufs& f = b.fl;
+    f.mk_cap = n < ((int64_t)1 << 22) ? n : ((int64_t)1 << 22);
+    f.mk_key = c.take<uint64_t>(f.mk_cap);
+    f.mk_fan = c.take<uint32_t>(f.mk_cap);
+    f.mk_cnt = c.take<uint32_t>(PREP_GRID);
+    f.cfan = c.take<uint32_t>(f.ctab_cap);
+    f.cmk = c.take<uint32_t>(f.ctab_cap);
+    f.cbase = c.take<uint32_t>(f.ctab_cap + 1);
+    f.dp_part = c.take<uint64_t>(3 * (DP_MAX_BLOCKS + 1));
+  }
   for (int m = Lt; m < d; ++m) {
     LevelNodes& L = b.lv[m];
     L.start = c.take<int32_t>(n + 1);
@@ -887,11 +1005,16 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 // ---------------------------------------------------------------------------
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st, bool offsets_later, bool exact_flow_levels) {
+              int32_t* status, hipStream_t st, bool offsets_later, bool exact_flow_levels, bool allow_dp) {
   // flows (packed sort) only when the sort runs its multi-block passes
   FlowBufs fl;
   if (n > SORT_SMALL_MAX) fl = b.fl;
   else memset(&fl, 0, sizeof(fl));
+  // direct placement: the child level's counts (level depth - 1) are among those read
+  fl.dp = (allow_dp && fl.hcap && fl.mk_key && fan && fhi == g.depth - 1 && flo <= fhi) ? 1 : 0;
+  fl.dp_level = g.depth - 1;
+  fl.fp_child = b.fp_nodes + (g.depth - 1);
+  b.fl.dp = fl.dp;
   // child ranks need the route level's declared child counts, read here when the
   // route level is among the levels whose counts are checked
   int fq = -1;
@@ -920,6 +1043,8 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
     k_route_init<<<(int)(cb < 2048 ? cb : 2048), 256, 0, st>>>(b.ctl, b.fp_in, b.fp_nodes, fl);
     const int nl = fhi >= flo ? fhi - flo + 1 : 0;
     const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
+    fl.mk_blocks = grid;
+    fl.mk_per = fl.dp ? (int32_t)(fl.mk_cap / grid) : 0;
 #define ALTO_PREP_CASE(NLV)                                                                                   \
   case NLV:                                                                                                   \
     k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part, xlo - flo, nx, \
@@ -971,10 +1096,19 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   int Lt, Lseg;
   agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
   ProfScope ps_total(PH_TOTAL, st);
-  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st, true, true);
+  int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st, true, true,
+                     true);
   if (rc) return rc;
   const uint32_t* perm = b.perm_used;
   prof_begin(PH_SEGMENT, st);
+  if (b.fl.dp) {
+    // direct placement chosen on the device: the group level from the child ranks
+    // (the segmentation kernels below then return at once)
+    k_dp_groups<<<grid_for(n, 256 * 16, 1024), 256, 0, st>>>(
+        g, b.fl, b.ctl, n, La, b.lv[La], b.nnodes, dest_offsets, rg.num_dest, b.sk, perm, fan, fan_ld, Lt,
+        (Lt < Lseg) ? b.carry_fan : nullptr, n < 1 ? 1 : n, b.fp_nodes, status,
+        (agg.op == ALTO_MEAN_F32 ? out.mean == nullptr : out.tok == nullptr) ? 1 : 0);
+  }
 
   // fragments: levels Lseg..d-1 are contiguous in (dest, key) order
   SegJob fj;
@@ -1001,6 +1135,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   fj.lb_tiles = b.os_ntiles * 2 * SORT_BUCKETS / SEG_LB_STRIDE;   // the sort's status words, free by now
   fj.fp_nodes = b.fp_nodes;
   fj.status = status;
+  fj.skip_ctl = b.fl.dp ? b.ctl : nullptr;
   rc = seg_run(g, fj, st);
   if (rc) return rc;
 
@@ -1059,7 +1194,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   prof_end(PH_SEGMENT, st);
 
   // groups
-  BatchSrc src{perm, p32, fan, fan_ld, pf, agg.dim};
+  BatchSrc src{perm, p32, fan, fan_ld, pf, agg.dim, n, status};
   return groups_run<BatchSrc>(g, rg, agg, src, b.sk, n, b, Mp, out, status, st);
 }
 

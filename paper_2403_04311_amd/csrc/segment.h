@@ -2,6 +2,7 @@
 // (internal).
 #pragma once
 #include "alto_internal.h"
+#include "sort.h"
 
 #define SEG_NT 512
 #define SEG_IT 32                      // consecutive elements per thread (fewer, larger tiles: fewer look-back rounds)
@@ -55,6 +56,8 @@ struct SegJob {
   int32_t* status;
   int64_t* dest_offsets;    // fragments sorted by (dest, key): start of each destination (nullable)
   RouteGeom rg;
+  const SortCtl* skip_ctl;  // nullable: every kernel returns at once when skip_ctl->dp (the sort
+                            // placed the elements directly and set the group level itself)
 };
 
 int seg_tiles(int64_t n_max);   // tiles of SEG_TILE elements

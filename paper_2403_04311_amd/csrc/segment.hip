@@ -21,6 +21,8 @@ constexpr int TILE = SEG_TILE;
 
 __device__ inline int64_t nelem(const SegJob& j) { return j.n_dev ? *j.n_dev : j.n_host; }
 
+__device__ inline bool skipped(const SegJob& j) { return j.skip_ctl && j.skip_ctl->dp; }
+
 __device__ inline int es_of(const KeyGeom& g, const SegJob& j, int m) { return g.shift[m] - g.shift[j.elem_level]; }
 
 __device__ inline int32_t fan_at(const SegJob& j, int m, int64_t e) {
@@ -35,6 +37,7 @@ __device__ inline int32_t fan_at(const SegJob& j, int m, int64_t e) {
 // Clears the look-back words and the ticket; with no elements, writes the empty
 // node counts and sentinels.
 __global__ void k_seg_prep(SegJob j) {
+  if (skipped(j)) return;
   const int64_t n = nelem(j);
   const int64_t len = cdiv(n, TILE) * SEG_LB_STRIDE;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
@@ -60,6 +63,7 @@ __global__ void k_seg_prep(SegJob j) {
 // counts; a tile has at most SEG_TILE < 2^16 elements).
 template <int KM>
 __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
+  if (skipped(j)) return;
   constexpr int NP = (KM + 3) / 4;
   const int64_t n = nelem(j);
   const int64_t ntiles = cdiv(n, TILE);
@@ -210,6 +214,7 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
 // Completion of the level-m nodes (children are level m+1 nodes, or elements when
 // m = elem_level - 1), and the node side of the fan fingerprint.
 __global__ __launch_bounds__(256) void k_seg_nodes(KeyGeom g, SegJob j, int m) {
+  if (skipped(j)) return;
   const int64_t N = j.nnodes[m];
   const LevelNodes L = j.lv[m];
   const bool leafy = (m + 1 == j.elem_level);
@@ -276,6 +281,7 @@ __global__ __launch_bounds__(256) void k_seg_nodes(KeyGeom g, SegJob j, int m) {
 // Records that are themselves incomplete make their parent incomplete: one thread
 // per record finds its parent node by binary search over the node starts.
 __global__ __launch_bounds__(256) void k_elem_bad(SegJob j) {
+  if (skipped(j)) return;
   const int64_t n = nelem(j);
   const int m = j.elem_level - 1;
   const int64_t N = j.nnodes[m];

@@ -29,6 +29,8 @@ struct SortPlan {
   int32_t npass;
   int32_t first;         // slot of the first pass (packed passes end at the host's last packed slot)
   int32_t idle;          // the multi-block path does nothing (sorted in one workgroup)
+  int32_t direct;        // packed by child rank, passes over the child-rank bits only; the last
+                         // pass puts each element at its final position (see FlowBufs.dp)
   SortPass pass[SORT_MAX_PASSES];
 };
 
@@ -43,7 +45,7 @@ struct SortCtl {
   int32_t flow_overflow; // the flow set filled up
   int32_t dlo, dbits;    // packed: rank = drank[(prefix >> dlo) & (2^dbits - 1)]; dbits < 0: hashed table
   int32_t cmode;         // packed by child rank: fbase[rank] + child tag replaces (rank, child tag)
-  int32_t pad2;
+  int32_t dp;            // direct placement chosen for this call (FlowBufs.dp)
   int64_t ctotal;        // child ranks in use (sum of the flows' declared child counts)
   int64_t nflows;        // distinct flows inserted
   int64_t nflows_c;      // the same, clamped to the flow capacity
@@ -85,7 +87,37 @@ struct FlowBufs {
   uint32_t* ftmp_vals;
   SortCtl* fctl;
   int64_t fcap;
+  // Direct placement (a batch whose groups are the flows and whose leaves lie one
+  // level below the flows' children). A leaf whose tag is its parent's declared
+  // count - 1 is a "marker"; the input pass lists them. When every child rank has
+  // exactly one marker and the children's declared counts add up to the number of
+  // elements, every child and flow is complete (given no duplicate keys) and the
+  // sorted position of a leaf is cbase[child rank] + leaf tag: the sort then orders
+  // the child-rank bits only and its last pass writes each element's input index
+  // there. The permutation is first filled with DP_UNPLACED, so a key given twice
+  // (two elements at one position) leaves another position holding it; whoever
+  // reads the permutation reports that as DUPLICATE.
+  int32_t dp;            // host: the call may use it (markers are collected)
+  int32_t dp_level;      // the child level (depth - 1): level of the fingerprint of child counts
+  uint64_t* mk_key;      // [mk_cap] keys of the markers: block b of the input pass lists its
+  uint32_t* mk_fan;      //   markers at [b * mk_per, (b + 1) * mk_per); and their declared counts
+  uint32_t* mk_cnt;      // [mk_blocks] markers seen by each block (may exceed mk_per: then no
+                         //   direct placement)
+  int64_t mk_cap;
+  int32_t mk_per;        // per block (set with the input pass's grid)
+  int32_t mk_blocks;     // blocks of the input pass
+  uint32_t* cfan;        // [ctab_cap] declared leaf count of each child rank (from its marker)
+  uint32_t* cmk;         // [ctab_cap] markers of each child rank
+  uint32_t* cbase;       // [ctab_cap + 1] first sorted position of each child rank
+  uint64_t* dp_part;     // [3 * (DP_MAX_BLOCKS + 1)] per-block sums, flags and fingerprints
+  uint64_t* fp_child;    // fingerprint sum of the child level over nodes (set when direct)
 };
+
+#define DP_UNPLACED 0xFFFFFFFFu   // a position of the permutation no element was placed at
+
+#define DP_CHUNK 4096          // child ranks per block of the direct-placement scan
+#define PREP_BLOCKS_MAX 512    // blocks of the input pass at most (marker regions)
+#define DP_MAX_BLOCKS 1024     // ctab_cap <= DP_CHUNK * DP_MAX_BLOCKS
 
 struct SortBufs {
   const uint64_t* in_keys;   // input keys; values are the input indices

@@ -36,6 +36,7 @@ __global__ void k_sort_init(SortCtl* ctl) {
     ctl->nflows = 0;
     ctl->nflows_c = 0;
     ctl->cmode = 0;
+    ctl->dp = 0;
     ctl->dbits = -1;
   }
 }
@@ -115,12 +116,16 @@ __global__ void k_sort_plan(SortCtl* ctl, int64_t n_host, const int64_t* n_dev, 
   int np = 0;
   p.idle = (n_dev && n <= SORT_SMALL_MAX) ? 1 : 0;
   const bool packed = ctl->mode == SORT_PACKED;
+  p.direct = (packed && ctl->cmode && ctl->dp && !p.idle) ? 1 : 0;
   if (!p.idle) {
     if (packed) {
       const int S = ctl->sbits, R = ctl->rbits;
-      uint64_t vs = (ctl->key_or ^ ctl->key_and) & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
+      // with direct placement the leaf tags (the suffix bits) are not sorted: the
+      // last pass puts each element at its child's start + its tag
+      uint64_t vs = p.direct ? 0ull : (ctl->key_or ^ ctl->key_and) & (S >= 64 ? ~0ull : ((1ull << S) - 1ull));
       uint64_t vr = R > 0 ? (((1ull << R) - 1ull) << S) : 0ull;
       np = greedy_windows(vs | vr, SORT_MAX_PASSES, 0, win, np);
+      if (np == 0) p.direct = 0;
     } else {
       np = greedy_windows(ctl->key_or ^ ctl->key_and, max_key_windows, 0, win, np);
       np = greedy_windows((uint64_t)(ctl->dest_or ^ ctl->dest_and), max_dest_windows, 1, win, np);
@@ -295,6 +300,158 @@ __global__ void k_ctab_fill(FlowBufs fl, const SortCtl* ctl) {
       if ((int64_t)fl.fbase[mid] <= t) lo = mid; else hi = mid - 1;
     }
     fl.ctab[t] = (fl.flow_sorted[lo] << fl.shift) | ((uint64_t)(t - fl.fbase[lo]) << fl.cshift);
+    if (fl.dp) {
+      fl.cfan[t] = 0u;
+      fl.cmk[t] = 0u;
+    }
+  }
+}
+
+// ---- direct placement (see FlowBufs.dp) --------------------------------------
+// The markers into the child-rank table: declared count (one marker's) and the
+// number of markers per child rank.
+__global__ __launch_bounds__(256) void k_dp_table(FlowBufs fl, const SortCtl* ctl) {
+  if (!ctl->cmode || ctl->mode != SORT_PACKED || ctl->dbits < 0 || fl.mk_per <= 0) return;
+  const int64_t C = ctl->ctotal, F = ctl->nflows_c;
+  const uint64_t dm = (1ull << ctl->dbits) - 1ull;
+  const int dlo = ctl->dlo;
+  // one block per region of the input pass, over its markers only
+  for (int blk = blockIdx.x; blk < fl.mk_blocks; blk += gridDim.x) {
+    const uint32_t mc = fl.mk_cnt[blk] < (uint32_t)fl.mk_per ? fl.mk_cnt[blk] : (uint32_t)fl.mk_per;
+    for (uint32_t i = threadIdx.x; i < mc; i += blockDim.x) {
+      const int64_t j = (int64_t)blk * fl.mk_per + i;
+      const uint64_t k = fl.mk_key[j];
+      const uint64_t pfx = k >> fl.shift;
+      const uint32_t r = fl.drank[(pfx >> dlo) & dm];
+      if ((int64_t)r >= F || fl.flow_sorted[r] != pfx) continue;   // a key of no flow: the input had errors
+      const uint32_t tag = (uint32_t)((k >> fl.cshift) & fl.cmask);
+      const uint64_t cr = (uint64_t)fl.fbase[r] + tag;
+      if (tag >= fl.fbase[r + 1] - fl.fbase[r] || (int64_t)cr >= C) continue;   // a FANOUT error (input pass)
+      fl.cfan[cr] = fl.mk_fan[j];
+      atomicAdd(&fl.cmk[cr], 1u);
+    }
+  }
+}
+
+// Per block of DP_CHUNK child ranks: the sum of declared counts, whether some rank
+// has no or several markers, and the node side of the child level's fingerprint
+// (each complete child contributes its count x its term). dp_part holds three
+// arrays of DP_MAX_BLOCKS + 1 words.
+__global__ __launch_bounds__(256) void k_dp_sums(FlowBufs fl, const SortCtl* ctl) {
+  if (!ctl->cmode || ctl->mode != SORT_PACKED || ctl->dbits < 0) return;
+  const int64_t C = ctl->ctotal;
+  const int64_t nb = cdiv(C, DP_CHUNK);
+  __shared__ uint64_t s_s[256 / ALTO_WAVE], s_f[256 / ALTO_WAVE];
+  __shared__ uint32_t s_b[256 / ALTO_WAVE];
+  for (int64_t blk = blockIdx.x; blk < nb; blk += gridDim.x) {
+    uint64_t sum = 0, fp = 0;
+    uint32_t bad = 0;
+    const int64_t c1 = (blk + 1) * DP_CHUNK < C ? (blk + 1) * DP_CHUNK : C;
+    for (int64_t c = blk * DP_CHUNK + threadIdx.x; c < c1; c += blockDim.x) {
+      const uint32_t f = fl.cfan[c];
+      sum += f;
+      bad |= fl.cmk[c] != 1u;
+      fp += (uint64_t)f * fan_term(fl.dp_level, fl.ctab[c] >> fl.cshift, f);
+    }
+    sum = wave_sum(sum);
+    fp = wave_sum(fp);
+    const uint64_t ball = __ballot(bad != 0);
+    const int w = threadIdx.x / ALTO_WAVE;
+    if (lane_id() == 0) {
+      s_s[w] = sum;
+      s_f[w] = fp;
+      s_b[w] = ball ? 1u : 0u;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t ts = 0, tf = 0;
+      uint32_t tb = 0;
+      for (int i = 0; i < 256 / ALTO_WAVE; ++i) {
+        ts += s_s[i];
+        tf += s_f[i];
+        tb |= s_b[i];
+      }
+      fl.dp_part[blk] = ts;
+      fl.dp_part[(DP_MAX_BLOCKS + 1) + blk] = tb;
+      fl.dp_part[2 * (DP_MAX_BLOCKS + 1) + blk] = tf;
+    }
+    __syncthreads();
+  }
+}
+
+// One block: the block sums become exclusive block prefixes, and the choice. Direct
+// placement needs child ranks, at most mk_cap markers, exactly one marker per child
+// rank (ctotal of them) and declared counts adding up to n.
+__global__ __launch_bounds__(1024) void k_dp_decide(FlowBufs fl, SortCtl* ctl, int64_t n) {
+  __shared__ uint64_t s_w[1024 / ALTO_WAVE];
+  __shared__ uint32_t s_bad;
+  const bool can = ctl->cmode && ctl->mode == SORT_PACKED && ctl->dbits >= 0;
+  if (threadIdx.x == 0) s_bad = 0;
+  __syncthreads();
+  if (!can) {
+    if (threadIdx.x == 0) ctl->dp = 0;
+    return;
+  }
+  const int64_t C = ctl->ctotal;
+  const int nb = (int)cdiv(C, DP_CHUNK);   // <= DP_MAX_BLOCKS = the block size
+  const int b = threadIdx.x;
+  const uint64_t v = b < nb ? fl.dp_part[b] : 0ull;
+  const uint64_t f = b < nb ? fl.dp_part[2 * (DP_MAX_BLOCKS + 1) + b] : 0ull;
+  if (b < nb && fl.dp_part[(DP_MAX_BLOCKS + 1) + b]) s_bad = 1u;
+  uint64_t tot;
+  const uint64_t ex = block_excl_scan<uint64_t, 1024>(v, s_w, &tot);
+  __syncthreads();
+  uint64_t ftot;
+  (void)block_excl_scan<uint64_t, 1024>(f, s_w, &ftot);
+  if (b < nb) fl.dp_part[b] = ex;
+  // markers: every block within its region, C of them in all
+  __shared__ uint64_t s_m;
+  __shared__ uint32_t s_over;
+  if (threadIdx.x == 0) {
+    s_m = 0;
+    s_over = 0;
+  }
+  __syncthreads();
+  if (threadIdx.x < fl.mk_blocks) {
+    const uint32_t mc = fl.mk_cnt[threadIdx.x];
+    atomicAdd((unsigned long long*)&s_m, (unsigned long long)mc);
+    if (mc > (uint32_t)fl.mk_per) s_over = 1u;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint64_t m = s_m;
+    const bool ok = C >= 1 && !s_bad && !s_over && m == (uint64_t)C && tot == (uint64_t)n;
+    ctl->dp = ok ? 1 : 0;
+    if (ok) {
+      fl.cbase[C] = (uint32_t)n;
+      *fl.fp_child = ftot;
+    }
+  }
+}
+
+// cbase: exclusive scan of the declared counts over child ranks (direct placement).
+__global__ __launch_bounds__(256) void k_dp_base(FlowBufs fl, const SortCtl* ctl) {
+  if (!ctl->dp) return;
+  constexpr int PER = DP_CHUNK / 256;
+  const int64_t C = ctl->ctotal;
+  const int64_t nb = cdiv(C, DP_CHUNK);
+  __shared__ uint32_t s_w[256 / ALTO_WAVE];
+  for (int64_t blk = blockIdx.x; blk < nb; blk += gridDim.x) {
+    const int64_t c0 = blk * DP_CHUNK + (int64_t)threadIdx.x * PER;
+    uint32_t v[PER], sum = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      v[k] = c0 + k < C ? fl.cfan[c0 + k] : 0u;
+      sum += v[k];
+    }
+    uint32_t tot;
+    uint32_t run = (uint32_t)fl.dp_part[blk] + block_excl_scan<uint32_t, 256>(sum, s_w, &tot);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (c0 + k < C) fl.cbase[c0 + k] = run;
+      run += v[k];
+    }
+    __syncthreads();
   }
 }
 
@@ -306,6 +463,7 @@ struct PassView {
   int32_t dlo, dbits;
   int32_t cmode;
   int32_t first;
+  int32_t direct;
   uint64_t ct_mask;
   uint64_t ctotal;
 };
@@ -322,6 +480,7 @@ __device__ inline PassView read_pass(const SortCtl* ctl, int slot) {
   v.dbits = ctl->dbits;
   v.cmode = ctl->cmode;
   v.first = ctl->plan.first;
+  v.direct = ctl->plan.direct;
   v.ctotal = (uint64_t)ctl->ctotal;
   return v;
 }
@@ -553,6 +712,14 @@ __global__ __launch_bounds__(NT) void k_sort_hist(SortBufs b, int64_t n_host, co
 #pragma unroll
       for (int j = 0; j < IT; ++j)
         if (gi[j] < n) stage[gi[j]] = key[j];
+      if (c.direct) {
+        // the last pass writes every position of the permutation once (unless a key
+        // is given twice): positions it misses keep this value
+        uint32_t* const pv = opaque(b.out_vals);
+#pragma unroll
+        for (int j = 0; j < IT; ++j)
+          if (gi[j] < n) pv[gi[j]] = DP_UNPLACED;
+      }
       if (dest_out) {
         // the element's destination is its flow's (ranks follow (destination, prefix))
 #pragma unroll
@@ -686,6 +853,8 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
     // after it, when the elements no longer occupy registers
     const int d = threadIdx.x;
     uint32_t run = 0;
+    // direct placement (last pass): positions come from the child ranks, no look-back
+    const bool direct = PACKED && LAST && c.direct;
     if (d < SORT_BUCKETS) {
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) {
@@ -693,7 +862,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
         s_cnt[ww][d] = (uint16_t)run;
         run += cc;
       }
-      lb_publish(st + d, tile, SORT_BUCKETS, run);
+      if (!direct) lb_publish(st + d, tile, SORT_BUCKETS, run);
     }
     uint32_t tot;
     {
@@ -710,7 +879,7 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
         if (!packed) s_slot[r] = (uint16_t)(lbase + j * ALTO_WAVE);
       }
     }
-    if (d < SORT_BUCKETS) {
+    if (d < SORT_BUCKETS && !direct) {
       const uint32_t excl = lb_resolve(st + d, tile, SORT_BUCKETS, run, b.status);
       s_gbase[d] = b.os_hist[slot * SORT_BUCKETS + d] + excl;
       st_next[tile * SORT_BUCKETS + d] = 0;   // the next pass's status of this tile
@@ -721,6 +890,42 @@ __global__ __launch_bounds__(NT, PACKED ? (OS_IT <= 8 ? 6 : 4) : 2) void k_onesw
         const uint64_t el = s_key[e];
         const uint32_t dg = (uint32_t)((el >> sh) & (SORT_BUCKETS - 1));
         dk[(uint64_t)s_gbase[dg] + (e - s_base[dg])] = el;
+      }
+    } else if (direct) {
+      // element (child rank cr, leaf tag t) goes to cbase[cr] + t; only the
+      // permutation is written (the sorted keys are not needed: group bounds come
+      // from cbase). A rank past the table comes only from an input error and is not
+      // written.
+      const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
+      const int S = c.sbits;
+      const uint64_t tmask = S >= 64 ? ~0ull : ((1ull << S) - 1ull);
+      const uint32_t* const cbase = opaque(b.fl.cbase);
+      // the base lookups of all of a thread's elements are issued before any is used
+      // (their latency is not hidden by other waves). A tag past its child's count (an
+      // input error) lands in a neighbour's range: a position is then written twice
+      // and another left at DP_UNPLACED.
+      constexpr int DH = OS_IT / 2;   // two halves: fewer registers live
+#pragma unroll 1
+      for (int h = 0; h < 2; ++h) {
+        uint64_t el[DH];
+        uint32_t gb[DH];
+#pragma unroll
+        for (int u = 0; u < DH; ++u) {
+          const uint32_t e = threadIdx.x + (uint32_t)(h * DH + u) * NT;
+          el[u] = e < tot ? s_key[e] : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < DH; ++u) {
+          const uint32_t e = threadIdx.x + (uint32_t)(h * DH + u) * NT;
+          const uint64_t cr = (S + c.ib >= 64) ? 0ull : (el[u] >> (S + c.ib));
+          gb[u] = (e < tot && cr < c.ctotal) ? cbase[cr] : 0xFFFFFFFFu;
+        }
+#pragma unroll
+        for (int u = 0; u < DH; ++u) {
+          const uint64_t g = (uint64_t)gb[u] + ((el[u] >> c.ib) & tmask);
+          if (gb[u] == 0xFFFFFFFFu || g >= (uint64_t)n) continue;
+          ov[g] = (uint32_t)(el[u] & imask);
+        }
       }
     } else if (packed && LAST) {
       const uint64_t imask = c.ib >= 64 ? ~0ull : ((1ull << c.ib) - 1ull);
@@ -1064,6 +1269,13 @@ int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const Rou
     k_ct_insert<<<(int)(rb < 1024 ? rb : 1024), 256, 0, st>>>(fl, b.ctl, rg.num_dest);
     const int64_t cb2 = cdiv(fl.ctab_cap, 256);
     k_ctab_fill<<<(int)(cb2 < 1024 ? cb2 : 1024), 256, 0, st>>>(fl, b.ctl);
+    if (fl.dp && packable) {
+      k_dp_table<<<PREP_BLOCKS_MAX, 256, 0, st>>>(fl, b.ctl);
+      const int64_t db = cdiv(fl.ctab_cap, DP_CHUNK);
+      k_dp_sums<<<(int)(db < 1024 ? db : 1024), 256, 0, st>>>(fl, b.ctl);
+      k_dp_decide<<<1, 1024, 0, st>>>(fl, b.ctl, n_max);
+      k_dp_base<<<(int)(db < 1024 ? db : 1024), 256, 0, st>>>(fl, b.ctl);
+    }
   }
   const int mk = sort_max_key_windows(key_bits), md = sort_max_dest_windows(rg);
   int maxp = mk + md;   // general passes

@@ -1,0 +1,97 @@
+"""GPU parity of batches that the sort can place directly: groups are the route
+level's flows and leaves lie one level below their children (the 2^26-fragment
+workload's shape: one root, one level-2 and one level-3 node, so the flows'
+prefixes differ in the level-4 tag only). Complete batches, and the data errors
+whose detection direct placement changes: a key given twice (a position of the
+sorted order left empty) and a leaf declaring another count than its siblings
+(the child level's fingerprint), alone and together (FANOUT wins), against the
+oracle's status."""
+import numpy as np
+import pytest
+
+from oracle import alto_oracle as O
+from paper_2403_04311_amd import workloads as W
+from tests import gpu_util as U
+
+pytestmark = pytest.mark.gpu
+
+BITS = (3, 12, 12, 12, 12, 12)
+
+
+def _tree(seed, f4=150, f5=30, f6=40, dim=8):
+    path, fan = W.random_tree(seed, 6, 1, (1, 1, f4, f5, f6), BITS, dense_roots=True)
+    rng = np.random.default_rng(seed + 1)
+    n = path.shape[1]
+    pf = rng.standard_normal((n, dim)).astype(np.float32)
+    p32 = rng.integers(0, 1 << 30, size=n).astype(np.int32)
+    (path, fan, p32, pft), _ = W.permute([path, fan, p32, pf.T], seed + 2)
+    return path, fan, p32, np.ascontiguousarray(pft.T)
+
+
+def _eligible(keys, fan):
+    # complete batch, more than one workgroup's sort, flows varying in the level-4 tag
+    n = len(keys)
+    assert n > 8192
+    assert len(np.unique(O.prefix(keys, BITS, 3))) == 1
+    comp = O.completion(keys, fan, BITS, 4)
+    assert comp[4][1].all() and comp[5][1].all()
+
+
+@pytest.mark.parametrize("seed,op,Lm", [(500, "mean", 2), (501, "concat", 0), (502, "mean", 4), (503, "concat", 3)])
+def test_direct_placement_complete_batches(seed, op, Lm):
+    path, fan, p32, pf = _tree(seed)
+    keys = O.pack_keys(path, BITS)
+    _eligible(keys, fan)
+    dim = pf.shape[1] if op == "mean" else 1
+    code, rt, g = U.oracle_aggregate(keys, fan, BITS, 4, op, dim, Lm, 4, 256, p32, pf if op == "mean" else None)
+    assert code == O.OK
+    res = U.run_aggregate(keys, fan, BITS, 4, op, dim, Lm, 4, 256, p32, pf if op == "mean" else None)
+    assert res["status"] == O.OK
+    U.compare(res, rt, g, op, Lm, 4)
+
+
+def _leaf_cols(keys, fan):
+    """Per fragment: level-5 prefix, leaf tag, declared leaf count."""
+    return O.prefix(keys, BITS, 5), O.tag(keys, BITS, 6).astype(np.int64), fan[4].astype(np.int64)
+
+
+@pytest.mark.parametrize("case", ["duplicate", "fanout", "both"])
+def test_direct_placement_errors_match_oracle(case):
+    path, fan, p32, pf = _tree(510)
+    keys = O.pack_keys(path, BITS)
+    _eligible(keys, fan)
+    node, tag, cnt = _leaf_cols(keys, fan)
+    # two non-marker leaves of one level-5 node with at least 3 leaves
+    nodes, nc = np.unique(node, return_counts=True)
+    big = nodes[np.argmax(nc)]
+    idx = np.nonzero((node == big) & (tag != cnt - 1))[0]
+    assert len(idx) >= 2
+    keys, fan = keys.copy(), fan.copy()
+    if case in ("duplicate", "both"):
+        keys[idx[0]] = keys[idx[1]]                  # a key twice, another tag missing
+    if case in ("fanout", "both"):
+        other = np.nonzero((node != big) & (tag != cnt - 1))[0][0]
+        fan[4, other] += 1                           # one carrier disagrees (still > its tag)
+    want = {"duplicate": O.E_DUPLICATE, "fanout": O.E_FANOUT, "both": O.E_FANOUT}[case]
+    code, _, _ = U.oracle_aggregate(keys, fan, BITS, 4, "mean", 8, 2, 4, 256, p32, pf)
+    assert code == want
+    for rep in range(2):   # the second call finds the first one's workspace contents
+        res = U.run_aggregate(keys, fan, BITS, 4, "mean", 8, 2, 4, 256, p32, pf)
+        assert res["status"] == want, rep
+
+
+def test_direct_placement_not_taken_when_a_marker_is_missing():
+    # the marker of one node replaced by a duplicate of a sibling: that node has no
+    # marker, so the sort takes the ordinary path, which finds the duplicate
+    path, fan, p32, pf = _tree(520)
+    keys = O.pack_keys(path, BITS)
+    _eligible(keys, fan)
+    node, tag, cnt = _leaf_cols(keys, fan)
+    m = np.nonzero((tag == cnt - 1) & (cnt >= 2))[0][0]
+    sib = np.nonzero((node == node[m]) & (tag != cnt - 1))[0][0]
+    keys = keys.copy()
+    keys[m] = keys[sib]
+    code, _, _ = U.oracle_aggregate(keys, fan, BITS, 4, "mean", 8, 2, 4, 256, p32, pf)
+    assert code == O.E_DUPLICATE
+    res = U.run_aggregate(keys, fan, BITS, 4, "mean", 8, 2, 4, 256, p32, pf)
+    assert res["status"] == O.E_DUPLICATE
