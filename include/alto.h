@@ -162,6 +162,24 @@ int alto_aggregate(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
                    alto_groups *out, int32_t *status, void *ws, size_t ws_bytes,
                    hipStream_t stream);
 
+/* alto_aggregate with a count held in device memory (Section 4.2: a pmap exit
+ * pops a level, so one stage's records are the next stage's fragments; reading the
+ * count on the device lets a caller chain stages without a host synchronisation).
+ * n_dev: device int64, read by the call's kernels in stream order (so it may be
+ * written by earlier work on the same stream, e.g. counts[0] of a previous call);
+ * n_max: a host bound on it that sizes every array argument (fan_ld >= n_max,
+ * perm/dest/payloads of n_max entries) and the workspace (alto_workspace_bytes
+ * with n_max). A count outside [0, n_max] is clamped and reported as CAPACITY.
+ * With n_dev NULL this is alto_aggregate with n = n_max. Otherwise as
+ * alto_aggregate (the radix sort then does not use its packed-word mode, whose
+ * index width the host fixes). */
+int alto_aggregate_dev(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                       const int32_t *payload_i32, const float *payload_f32, int64_t n_max,
+                       const int64_t *n_dev, const alto_layout *layout, const alto_agg *agg,
+                       int32_t route_level, int32_t num_dest, int32_t *perm, int64_t *dest_offsets,
+                       int32_t *dest, alto_groups *out, int32_t *status, void *ws, size_t ws_bytes,
+                       hipStream_t stream);
+
 /* ---- alto_aggregate without a workspace argument ----
  * For callers that cannot allocate device memory at the time of the call (code
  * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
@@ -217,6 +235,19 @@ int alto_stream_step(alto_stream *s, const uint64_t *keys, const int32_t *fan, i
                      const int32_t *payload_i32, const float *payload_f32, int64_t n,
                      int32_t *perm, int64_t *dest_offsets, int32_t *dest, alto_groups *emitted,
                      int32_t *status, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* alto_stream_step with the step's count in device memory (n_dev, read in stream
+ * order; n_max bounds it and sizes the arrays, the workspace and the emitted
+ * capacities as n does for alto_stream_step). Chaining two streams: stage B's
+ * keys, fan, payload_i32 and n_dev are stage A's emitted key, fan_up, first_i32
+ * and counts[0] (emitted groups per step are at most the step's count, so stage A's
+ * bound serves as stage B's n_max). A count outside [0, n_max] is clamped and
+ * reported as CAPACITY. */
+int alto_stream_step_dev(alto_stream *s, const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                         const int32_t *payload_i32, const float *payload_f32, int64_t n_max,
+                         const int64_t *n_dev, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
+                         alto_groups *emitted, int32_t *status, void *ws, size_t ws_bytes,
+                         hipStream_t stream);
 
 /* Lists the groups that have arrived leaves but were never released (incomplete,
  * or complete and waiting for an earlier sibling), by (dest, key):

@@ -28,7 +28,7 @@ EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggrega
            "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join",
            "alto_split_workspace_bytes", "alto_split", "alto_router_state_bytes", "alto_router_create",
            "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load", "alto_profile_phases",
-           "alto_read_probe", "alto_aggregate_noalloc")
+           "alto_read_probe", "alto_aggregate_noalloc", "alto_aggregate_dev", "alto_stream_step_dev")
 NOALLOC_SCRATCH_BYTES = 128 << 20   # ALTO_NOALLOC_SCRATCH_BYTES of include/alto.h
 
 
@@ -77,6 +77,12 @@ def load():
     lib.alto_aggregate.restype = C.c_int
     lib.alto_aggregate.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
                                    vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp]
+    lib.alto_aggregate_dev.restype = C.c_int
+    lib.alto_aggregate_dev.argtypes = [vp, vp, i64, vp, vp, i64, vp, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
+                                       vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp]
+    lib.alto_stream_step_dev.restype = C.c_int
+    lib.alto_stream_step_dev.argtypes = [vp, vp, vp, i64, vp, vp, i64, vp, vp, vp, vp, C.POINTER(Groups), vp,
+                                         vp, C.c_size_t, vp]
     lib.alto_aggregate_noalloc.restype = C.c_int
     lib.alto_aggregate_noalloc.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
                                            vp, vp, vp, C.POINTER(Groups), vp, vp]
@@ -366,8 +372,10 @@ def new_groups(cap_groups, agg_level, op, dim=1, cap_tokens=0, cap_mask=0, devic
 
 def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0, num_dest=1,
               payload_i32=None, payload_f32=None, ws=None, perm=None, dest_offsets=None, dest=None,
-              out: Optional[GroupTensors] = None, status=None, stream=None, n=None):
-    """Routes and aggregates one batch; returns (perm, dest_offsets, dest, groups, status)."""
+              out: Optional[GroupTensors] = None, status=None, stream=None, n=None, n_dev=None):
+    """Routes and aggregates one batch; returns (perm, dest_offsets, dest, groups, status).
+    n_dev (int64 device tensor, optional): the count is read there on the device (n,
+    or keys.shape[0], is then its bound: alto_aggregate_dev)."""
     lib = load()
     a = _Args("alto_aggregate")
     n = keys.shape[0] if n is None else n
@@ -396,13 +404,19 @@ def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0
     a.t(dest, "dest", torch.int32, n, optional=True)
     out.check(a, op, agg_level, dim)
     a.t(status, "status", torch.int32, 1)
+    a.t(n_dev, "n_dev", torch.int64, 1, optional=True)
     a.device()
     L = layout(bits)
     A = agg_struct(agg_level, op, dim, mask_level)
     G = out.struct()
-    rc = lib.alto_aggregate(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n,
-                            C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
-                            _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream))
+    if n_dev is None:
+        rc = lib.alto_aggregate(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n,
+                                C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
+                                _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream))
+    else:
+        rc = lib.alto_aggregate_dev(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n, _p(n_dev),
+                                    C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
+                                    _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_aggregate")
     return perm, dest_offsets, dest, out, status
 
@@ -468,7 +482,10 @@ class Stream:
         _check(rc, "alto_stream_create")
 
     def step(self, keys, fan, payload_i32=None, payload_f32=None, out: Optional[GroupTensors] = None,
-             perm=None, dest_offsets=None, dest=None, status=None, stream=None, n=None):
+             perm=None, dest_offsets=None, dest=None, status=None, stream=None, n=None, n_dev=None):
+        """One step. n_dev (int64 device tensor, optional): the step's count is read
+        there on the device, n (or keys.shape[0]) being its bound
+        (alto_stream_step_dev): e.g. the previous stage's out.counts[0:1]."""
         n = keys.shape[0] if n is None else n
         if n > self.step_max:
             raise AltoError(E_ARG, "step larger than step_max")
@@ -490,13 +507,14 @@ class Stream:
         out.check(a, self.op, self.La, self.dim)
         a.t(status, "status", torch.int32, 1)
         a.t(self.ws, "workspace", torch.uint8)
+        a.t(n_dev, "n_dev", torch.int64, 1, optional=True)
         if a.device() != self.state.device:
             a.fail(f"arguments on {a.dev}, stream state on {self.state.device}")
         G = out.struct()
-        rc = self.lib.alto_stream_step(self.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32),
-                                       _p(payload_f32), n, _p(perm), _p(dest_offsets), _p(dest),
-                                       C.byref(G), _p(status), _p(self.ws), _nbytes(self.ws),
-                                       _stream(stream))
+        rc = self.lib.alto_stream_step_dev(self.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32),
+                                           _p(payload_f32), n, _p(n_dev), _p(perm), _p(dest_offsets), _p(dest),
+                                           C.byref(G), _p(status), _p(self.ws), _nbytes(self.ws),
+                                           _stream(stream))
         _check(rc, "alto_stream_step")
         return out, status
 

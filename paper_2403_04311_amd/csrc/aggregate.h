@@ -4,6 +4,8 @@
 #include "segment.h"
 #include "sort.h"
 
+#define GROUP_SCAN_TILE 4096   // groups per tile of the group scan (k_group_scan)
+#define GROUP_SCAN_WORDS 5     // its look-back words per tile
 #define MEAN_CHUNK_ROWS 4096
 #define MEAN_SMALL_ROWS 256    // groups of at most this many rows: one chunk, gathered by one wave
 
@@ -134,6 +136,7 @@ struct AggBufs {
   int64_t* nsm;         // scanned count of small groups (one wave-gathered chunk each)
   Chunk* chunks;
   double* part;
+  uint2* gw;            // [cdiv(n_max, SEG_IT)] group-level boundary words of the segmentation pass (streams)
 };
 
 void agg_levels(const KeyGeom& g, int La, int Lm, int Lr, int* Lt, int* Lseg);
@@ -145,16 +148,78 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
               int32_t* status, hipStream_t st, bool offsets_later = false, bool exact_flow_levels = false,
-              bool allow_dp = false);
+              bool allow_dp = false, const int64_t* n_dev = nullptr);
+// Work folded into the kernels of groups_run (fewer launches per call):
+//  - the comparison of the fan fingerprints, in the record kernel (fp_in null:
+//    none; levels flo..fhi, those in xlo..xhi only when ctl reports a flow-set
+//    overflow, as in k_fp_compare);
+//  - the group scan's look-back words at gst and its ticket at *gctr (null: the
+//    sort's status words and first ticket); cleared = the caller's earlier kernel
+//    cleared them (cdiv(n_max + 1, GROUP_SCAN_TILE) * GROUP_SCAN_WORDS words),
+//    else the scan's first kernel does, and also clears another look-back region
+//    (xst null: none) of cdiv(*xlen, xtile) * xper words and its ticket *xctr, for
+//    a scan that runs after the groups;
+//  - the emitted set (ht null: none): the record kernel inserts the key of every
+//    emitted group into an insert-only open-addressing set of htcap (a power of
+//    two) slots, counting new keys in *emit_count; more than max_emit keys, or a
+//    full table, raise ALTO_E_CAPACITY.
+struct GroupsExtra {
+  const uint64_t* fp_in;
+  const uint64_t* fp_nodes;
+  int32_t flo, fhi, xlo, xhi;
+  const SortCtl* ctl;
+  uint64_t* gst;
+  uint32_t* gctr;
+  int32_t cleared;
+  uint64_t* xst;
+  uint32_t* xctr;
+  const int64_t* xlen;
+  int64_t xtile, xper;
+  uint64_t* ht;
+  int64_t htcap, max_emit;
+  int64_t* emit_count;
+};
+
+#define EMIT_EMPTY (~0ull)
+
+// Inserts a group key into the emitted set: 1 = new, 0 = present, -1 = table full.
+__device__ inline int emitted_insert(uint64_t gk, uint64_t* ht, int64_t htcap) {
+  int64_t h = (int64_t)(mix64(gk) & (uint64_t)(htcap - 1));
+  for (int64_t p = 0; p < htcap; ++p) {
+    const uint64_t v = ht[h];
+    if (v == gk) return 0;
+    if (v == EMIT_EMPTY) {
+      const uint64_t old = atomicCAS((unsigned long long*)&ht[h], (unsigned long long)EMIT_EMPTY, (unsigned long long)gk);
+      if (old == EMIT_EMPTY) return 1;
+      if (old == gk) return 0;
+    }
+    h = (h + 1) & (htcap - 1);
+  }
+  return -1;
+}
+
+// Whether a group key is in the emitted set.
+__device__ inline bool emitted_has(uint64_t gk, const uint64_t* ht, int64_t htcap) {
+  int64_t h = (int64_t)(mix64(gk) & (uint64_t)(htcap - 1));
+  for (int64_t p = 0; p < htcap; ++p) {
+    const uint64_t v = ht[h];
+    if (v == gk) return true;
+    if (v == EMIT_EMPTY) return false;
+    h = (h + 1) & (htcap - 1);
+  }
+  return false;
+}
+
 // Groups, chunk lists, counts and payload gathers over an element array already
 // segmented at level La (nodes in b.lv[La]); elements sorted by (dest, key).
 template <typename Src>
 int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const Src& src, const uint64_t* sk,
-               int64_t n_max, AggBufs& b, const int64_t* Mp, const GroupOut& out, int32_t* status, hipStream_t st);
+               int64_t n_max, AggBufs& b, const int64_t* Mp, const GroupOut& out, int32_t* status, hipStream_t st,
+               const GroupsExtra* ex = nullptr);
 int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
                   const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
                   int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
-                  hipStream_t st);
+                  hipStream_t st, const int64_t* n_dev = nullptr);
 void empty_outputs(const GroupOut& out, int64_t* dest_offsets, int num_dest, hipStream_t st);
 void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st);
 void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,

@@ -52,7 +52,8 @@ template <int NL>
 __global__ __launch_bounds__(PREP_NT, 8) void k_prep(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
                                                   RouteGeom rg, int32_t* dest, const int32_t* __restrict__ fan,
                                                   int64_t fan_ld, int flo, FlowBufs fl, PrepPartial* part, int qx0,
-                                                  int nx, int skip_fp) {
+                                                  int nx, int skip_fp, const int64_t* n_dev) {
+  n = dev_n(n_dev, n);
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
   uint64_t fp[NL > 0 ? NL : 1];
@@ -226,8 +227,9 @@ __global__ __launch_bounds__(PREP_NT, 8) void k_prep(const uint64_t* __restrict_
 // checked levels then join the fingerprint (their terms over every fragment).
 __global__ __launch_bounds__(256) void k_prep_fp(const uint64_t* __restrict__ keys, int64_t n, KeyGeom g,
                                                  const int32_t* __restrict__ fan, int64_t fan_ld, int xlo, int xhi,
-                                                 const SortCtl* ctl, uint64_t* fp_in) {
+                                                 const SortCtl* ctl, uint64_t* fp_in, const int64_t* n_dev) {
   if (!ctl->flow_overflow) return;
+  n = dev_n(n_dev, n);
   uint64_t fp[FLOW_EXACT_LEVELS];
 #pragma unroll
   for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) fp[x] = 0;
@@ -311,9 +313,11 @@ __global__ __launch_bounds__(256) void k_prep_fold(const PrepPartial* part, int 
 }
 
 // Start of a routing call: control block, fingerprint sums and the flow set.
-__global__ void k_route_init(SortCtl* ctl, uint64_t* fp_in, uint64_t* fp_nodes, FlowBufs fl) {
+__global__ void k_route_init(SortCtl* ctl, uint64_t* fp_in, uint64_t* fp_nodes, FlowBufs fl, const int64_t* n_dev,
+                             int64_t n_max, int32_t* status) {
   if (blockIdx.x == 0) {
     if (threadIdx.x == 0) {
+      if (n_dev && (*n_dev < 0 || *n_dev > n_max)) raise_status(status, ALTO_E_CAPACITY);
       ctl->key_or = 0;
       ctl->key_and = ~0ull;
       ctl->dest_or = 0;
@@ -427,8 +431,14 @@ __global__ __launch_bounds__(256) void k_dp_groups(KeyGeom g, FlowBufs fl, const
 
 // dest_offsets from the sorted keys; duplicate keys are adjacent after the sort.
 __global__ __launch_bounds__(256) void k_dest_offsets(const uint64_t* __restrict__ sk, int64_t n, RouteGeom rg,
-                                                      int64_t* offs, int32_t* status) {
+                                                      int64_t* offs, int32_t* status, const int64_t* n_dev) {
   const uint32_t D = rg.num_dest;
+  n = dev_n(n_dev, n);
+  if (n == 0) {
+    if (offs && blockIdx.x == 0)
+      for (uint32_t x = threadIdx.x; x <= D; x += blockDim.x) offs[x] = 0;
+    return;
+  }
   bool dup = false;
   for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n; j += (int64_t)gridDim.x * blockDim.x) {
     const uint64_t k = sk[j];
@@ -474,14 +484,22 @@ __global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, in
 constexpr int GS_NT = 256;
 constexpr int GS_IT = 16;
 constexpr int GS_TILE = GS_NT * GS_IT;
+static_assert(GS_TILE == GROUP_SCAN_TILE, "group scan tile");
 
-constexpr int GS_NV = 5;   // scanned values per group
+constexpr int GS_NV = GROUP_SCAN_WORDS;   // scanned values per group
 
-__global__ void k_group_scan_prep(const int64_t* Gp, uint64_t* st, uint32_t* ctr) {
+__global__ void k_group_scan_prep(const int64_t* Gp, uint64_t* st, uint32_t* ctr, GroupsExtra ex) {
   const int64_t len = cdiv(*Gp + 1, GS_TILE) * GS_NV;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
-    st[i] = 0;
-  if (blockIdx.x == 0 && threadIdx.x == 0) *ctr = 0;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = t0; i < len; i += stride) st[i] = 0;
+  if (ex.xst) {
+    const int64_t xl = cdiv(*ex.xlen, ex.xtile) * ex.xper;
+    for (int64_t i = t0; i < xl; i += stride) ex.xst[i] = 0;
+  }
+  if (t0 == 0) {
+    *ctr = 0;
+    if (ex.xst) *ex.xctr = 0;
+  }
 }
 
 __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_t* Gp, int32_t* em, int64_t* tokc,
@@ -549,12 +567,44 @@ __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_
   }
 }
 
+// Group records and chunk descriptors, one thread per group; block 0 also writes
+// the call's counts and the chunk totals the gathers read (emitted groups, tokens,
+// mask nodes, pending groups; capacity) and compares the fan fingerprints.
+// Chunks: groups of more than MEAN_SMALL_ROWS rows are cut into chunks of
+// chunk_rows (their first index from the scanned chunk counts); each shorter
+// group is one chunk after those. Emitted groups enter the emitted set (ex.ht).
 template <typename Src>
 __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int La, LevelNodes L, const int64_t* Gp,
                                                    const uint64_t* __restrict__ sk, Src src, const int32_t* em,
                                                    const int64_t* tokb, const int64_t* chb, const int64_t* pb,
-                                                   GroupOut out) {
+                                                   const int64_t* smb, Chunk* chunks, int chunk_rows, GroupOut out,
+                                                   const int64_t* tokc_or_null, const int64_t* Mp, int64_t* scal,
+                                                   GroupsExtra ex, int32_t* status) {
   const int64_t G = *Gp;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    scal[1] = chb[G] + smb[G];   // chunks: those of long groups, then one per short group
+    scal[2] = 0;                 // block tickets of the mean gather (long groups)
+    scal[3] = chb[G];            // short groups: chunks scal[3] .. scal[1] - 1
+    const int64_t E = em[G];
+    const int64_t T = tokc_or_null ? tokc_or_null[G] : 0;
+    const int64_t M = Mp ? *Mp : 0;
+    const int64_t P = G - E;
+    out.counts[0] = E;
+    out.counts[1] = T;
+    out.counts[2] = M;
+    out.counts[3] = P;
+    if (out.tok_off && E <= out.cap_groups) out.tok_off[E] = T;
+    if (E > out.cap_groups || P > out.cap_groups || T > out.cap_tokens || M > out.cap_mask)
+      raise_status(status, ALTO_E_CAPACITY);
+    if (ex.fp_in) {
+      const bool all = ex.ctl == nullptr || ex.ctl->flow_overflow;
+      for (int m = ex.flo; m <= ex.fhi; ++m)
+        if ((all || m < ex.xlo || m > ex.xhi) && ex.fp_in[m] != ex.fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
+    }
+  }
+  const int64_t NB = chb[G];   // chunks of the long groups come first, then one per short group
+  int64_t fresh = 0;           // keys new to the emitted set
+  bool full = false;
   for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
     const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
     const uint64_t k = sk[s];
@@ -571,6 +621,11 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
           for (int l = 1; l < La; ++l) out.fan_up[(int64_t)(l - 1) * out.cap_groups + e] = src.fan_of(l, first);
         if (out.tok_off) out.tok_off[e] = tokb[u];
       }
+      if (ex.ht) {
+        const int r = emitted_insert(gk, ex.ht, ex.htcap);
+        if (r < 0) full = true;
+        else fresh += r;
+      }
     } else {
       const int64_t p = u - em[u];
       if (p < out.cap_groups) {
@@ -578,36 +633,32 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
         if (out.pend_count) out.pend_count[p] = cnt;
       }
     }
-  }
-}
-
-// Chunk descriptors: one thread per group writes the group's chunks. Groups of more
-// than MEAN_SMALL_ROWS rows are cut into chunks of chunk_rows (their first index
-// from the scanned chunk counts); each shorter group is one chunk after those.
-__global__ __launch_bounds__(256) void k_chunks(LevelNodes L, const int64_t* Gp, const int32_t* em, const int64_t* tokb,
-                                                const int64_t* chb, const int64_t* pb, const int64_t* smb, Chunk* chunks,
-                                                int chunk_rows) {
-  const int64_t G = *Gp;
-  const int64_t NB = chb[G];   // chunks of the long groups come first, then one per short group
-  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
     const bool small = smb[u + 1] > smb[u];
     const int64_t c0 = small ? NB + smb[u] : chb[u], nc = small ? 1 : chb[u + 1] - chb[u];
     if (nc <= 0) continue;   // an incomplete group has no chunk
-    const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
-    const int64_t e = em[u], part = nc > 1 ? pb[u] : -1, out = tokb[u];
-    for (int64_t k = 0; k < nc; ++k) {
+    const int64_t e = em[u], part = nc > 1 ? pb[u] : -1, o = tokb[u];
+    for (int64_t c = 0; c < nc; ++c) {
       Chunk ch;
       ch.e = e;
-      ch.begin = s + (int32_t)(k * chunk_rows);
-      ch.len = (int32_t)((cnt - k * chunk_rows) < chunk_rows ? (cnt - k * chunk_rows) : chunk_rows);
-      ch.k = (int32_t)k;
+      ch.begin = s + (int32_t)(c * chunk_rows);
+      ch.len = (int32_t)((cnt - c * chunk_rows) < chunk_rows ? (cnt - c * chunk_rows) : chunk_rows);
+      ch.k = (int32_t)c;
       ch.nch = (int32_t)nc;
       ch.count = cnt;
       ch.part = part;
-      ch.out = out + k * chunk_rows;
+      ch.out = o + c * chunk_rows;
       ch.pad = 0;
-      chunks[c0 + k] = ch;
+      chunks[c0 + c] = ch;
     }
+  }
+  if (ex.ht) {
+    // one count update per wave
+    const int64_t w = wave_sum(fresh);
+    if (lane_id() == 0 && w) {
+      const int64_t before = (int64_t)atomicAdd((unsigned long long*)ex.emit_count, (unsigned long long)w);
+      if (before + w > ex.max_emit) full = true;
+    }
+    if (full) raise_status(status, ALTO_E_CAPACITY);
   }
 }
 
@@ -868,27 +919,6 @@ __global__ void k_record_keys(LevelNodes L, const int64_t* Np, const uint64_t* _
     rkey[u] = key_prefix(sk[L.start[u]], shift);
 }
 
-__global__ void k_counts(const int64_t* Gp, const int32_t* em, const int64_t* tokc, const int64_t* nch, const int64_t* nsm,
-                         const int64_t* Mp,
-                         int64_t* counts, int64_t* tok_off, GroupOut out, int64_t* scal, int32_t* status) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const int64_t G = *Gp;
-  scal[1] = nch[G] + nsm[G];   // chunks: those of long groups, then one per short group
-  scal[2] = 0;                 // block tickets of the mean gather (long groups)
-  scal[3] = nch[G];            // short groups: chunks scal[3] .. scal[1] - 1
-  const int64_t E = em[G];
-  const int64_t T = tokc ? tokc[G] : 0;
-  const int64_t M = Mp ? *Mp : 0;
-  const int64_t P = G - E;
-  counts[0] = E;
-  counts[1] = T;
-  counts[2] = M;
-  counts[3] = P;
-  if (tok_off && E <= out.cap_groups) tok_off[E] = T;
-  if (E > out.cap_groups || P > out.cap_groups || T > out.cap_tokens || M > out.cap_mask)
-    raise_status(status, ALTO_E_CAPACITY);
-}
-
 inline bool src_rows_aligned16(const BatchSrc& s) { return (reinterpret_cast<uintptr_t>(s.pf) & 15) == 0; }
 inline bool src_rows_aligned16(const MergedSrc& s) {
   return ((reinterpret_cast<uintptr_t>(s.spf) | reinterpret_cast<uintptr_t>(s.arena)) & 15) == 0;
@@ -926,6 +956,7 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   b.os_hist = c.take<uint32_t>((int64_t)SORT_MAX_PASSES * SORT_BUCKETS);
   b.scan_i32 = c.take<int32_t>(SCAN_MAX_BLOCKS + 1);
   b.scan_i64 = c.take<int64_t>(SCAN_MAX_BLOCKS + 1);
+  b.gw = c.take<uint2>(cdiv(n, SEG_IT));
   memset(&b.fl, 0, sizeof(b.fl));
   if (n_max > SORT_SMALL_MAX && Lr >= 1) {
     // flows of the route level, ranked in (dest, prefix) order (packed sort)
@@ -1005,13 +1036,14 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
 // ---------------------------------------------------------------------------
 int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64_t n, AggBufs& b, int32_t* perm_out,
               int64_t* dest_offsets, int32_t* dest, const int32_t* fan, int64_t fan_ld, int flo, int fhi,
-              int32_t* status, hipStream_t st, bool offsets_later, bool exact_flow_levels, bool allow_dp) {
+              int32_t* status, hipStream_t st, bool offsets_later, bool exact_flow_levels, bool allow_dp,
+              const int64_t* n_dev) {
   // flows (packed sort) only when the sort runs its multi-block passes
   FlowBufs fl;
   if (n > SORT_SMALL_MAX) fl = b.fl;
   else memset(&fl, 0, sizeof(fl));
   // direct placement: the child level's counts (level depth - 1) are among those read
-  fl.dp = (allow_dp && fl.hcap && fl.mk_key && fan && fhi == g.depth - 1 && flo <= fhi) ? 1 : 0;
+  fl.dp = (allow_dp && !n_dev && fl.hcap && fl.mk_key && fan && fhi == g.depth - 1 && flo <= fhi) ? 1 : 0;
   fl.dp_level = g.depth - 1;
   fl.fp_child = b.fp_nodes + (g.depth - 1);
   b.fl.dp = fl.dp;
@@ -1037,10 +1069,12 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   const int nx = xhi >= xlo ? xhi - xlo + 1 : 0;
   b.fx_lo = exact_flow_levels ? xlo : 1;
   b.fx_hi = exact_flow_levels ? xhi : 0;
-  {
+  // a call that fits one workgroup: the sort does the preparation too
+  const bool small = n <= SORT_SMALL_MAX && !fl.hcap;
+  if (!small) {
     ProfScope ps(PH_PREP, st);
     const int64_t cb = fl.hcap > 0 ? cdiv(fl.hcap, 256) : 1;
-    k_route_init<<<(int)(cb < 2048 ? cb : 2048), 256, 0, st>>>(b.ctl, b.fp_in, b.fp_nodes, fl);
+    k_route_init<<<(int)(cb < 2048 ? cb : 2048), 256, 0, st>>>(b.ctl, b.fp_in, b.fp_nodes, fl, n_dev, n, status);
     const int nl = fhi >= flo ? fhi - flo + 1 : 0;
     const int grid = grid_for(n, PREP_NT * PU, PREP_GRID);
     fl.mk_blocks = grid;
@@ -1048,7 +1082,7 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
 #define ALTO_PREP_CASE(NLV)                                                                                   \
   case NLV:                                                                                                   \
     k_prep<NLV><<<grid, PREP_NT, 0, st>>>(keys, n, g, rg, dest, fan, fan_ld, flo, fl, b.prep_part, xlo - flo, nx, \
-                                          exact_flow_levels ? 1 : 0);                                          \
+                                          exact_flow_levels ? 1 : 0, n_dev);                                   \
     break;
     switch (nl) {
       ALTO_PREP_CASE(0) ALTO_PREP_CASE(1) ALTO_PREP_CASE(2) ALTO_PREP_CASE(3) ALTO_PREP_CASE(4)
@@ -1059,7 +1093,7 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
 #undef ALTO_PREP_CASE
     k_prep_fold<<<1, 256, 0, st>>>(b.prep_part, grid, flo, nl, b.ctl, b.fp_in, status);
     if (exact_flow_levels && nx > 0)
-      k_prep_fp<<<grid_for(n, 256 * 8, 2048), 256, 0, st>>>(keys, n, g, fan, fan_ld, xlo, xhi, b.ctl, b.fp_in);
+      k_prep_fp<<<grid_for(n, 256 * 8, 2048), 256, 0, st>>>(keys, n, g, fan, fan_ld, xlo, xhi, b.ctl, b.fp_in, n_dev);
     ALTO_LAUNCH_CHECK();
   }
   ProfScope ps_sort(PH_SORT, st);
@@ -1078,12 +1112,24 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   sb.os_ntiles = b.os_ntiles;
   sb.status = status;
   sb.dest_out = fl.hcap ? dest : nullptr;   // with flows the counting sweep writes them
+  if (small) {
+    sb.prep.ctl = b.ctl;
+    sb.prep.fp_in = b.fp_in;
+    sb.prep.fp_nodes = b.fp_nodes;
+    sb.prep.fan = fan;
+    sb.prep.fan_ld = fan_ld;
+    sb.prep.flo = flo;
+    sb.prep.fhi = fhi;
+    sb.prep.dest = dest;
+    sb.prep.status = status;
+    sb.prep.g = g;
+  }
   b.perm_used = sb.out_vals;
-  int rc = sort_pairs(sb, n, nullptr, rg, g.total, true, st);
+  int rc = sort_pairs(sb, n, n_dev, rg, g.total, true, st);
   if (rc) return rc;
   // destination offsets and duplicate keys; aggregation does both in its
   // segmentation pass over the same sorted keys
-  if (!offsets_later) k_dest_offsets<<<grid_for(n, 256), 256, 0, st>>>(b.sk, n, rg, dest_offsets, status);
+  if (!offsets_later) k_dest_offsets<<<grid_for(n, 256), 256, 0, st>>>(b.sk, n, rg, dest_offsets, status, n_dev);
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;
 }
@@ -1091,13 +1137,13 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
 int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
                   const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
                   int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
-                  hipStream_t st) {
+                  hipStream_t st, const int64_t* n_dev) {
   const int d = g.depth, La = agg.level, Lm = agg.mask_level;
   int Lt, Lseg;
   agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
   ProfScope ps_total(PH_TOTAL, st);
   int rc = route_run(g, rg, keys, n, b, perm_out, dest_offsets, dest, fan, fan_ld, Lt, d - 1, status, st, true, true,
-                     true);
+                     true, n_dev);
   if (rc) return rc;
   const uint32_t* perm = b.perm_used;
   prof_begin(PH_SEGMENT, st);
@@ -1116,6 +1162,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   fj.keys = b.sk;
   fj.idx = perm;
   fj.n_host = n;
+  fj.n_dev = n_dev;
   fj.n_max = n;
   fj.elem_level = d;
   fj.lo = Lseg;
@@ -1190,37 +1237,51 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
     Mp = b.nnodes + Lm;
     k_mask_out<<<grid_for(n, 256), 256, 0, st>>>(b.lv[Lm], Mp, b.sk, g.shift[Lm], out.mask_key, out.mask, out.cap_mask);
   }
-  k_fp_compare<<<1, 1, 0, st>>>(b.fp_in, b.fp_nodes, Lt, d - 1, b.fx_lo, b.fx_hi, b.ctl, status);
   prof_end(PH_SEGMENT, st);
 
-  // groups
+  // groups (their record kernel also compares the fan fingerprints)
+  GroupsExtra ex;
+  memset(&ex, 0, sizeof(ex));
+  ex.fp_in = b.fp_in;
+  ex.fp_nodes = b.fp_nodes;
+  ex.flo = Lt;
+  ex.fhi = d - 1;
+  ex.xlo = b.fx_lo;
+  ex.xhi = b.fx_hi;
+  ex.ctl = b.ctl;
   BatchSrc src{perm, p32, fan, fan_ld, pf, agg.dim, n, status};
-  return groups_run<BatchSrc>(g, rg, agg, src, b.sk, n, b, Mp, out, status, st);
+  return groups_run<BatchSrc>(g, rg, agg, src, b.sk, n, b, Mp, out, status, st, &ex);
 }
 
 template <typename Src>
 int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const Src& src, const uint64_t* sk,
-               int64_t n_max, AggBufs& b, const int64_t* Mp, const GroupOut& out, int32_t* status, hipStream_t st) {
+               int64_t n_max, AggBufs& b, const int64_t* Mp, const GroupOut& out, int32_t* status, hipStream_t st,
+               const GroupsExtra* ex) {
   const int La = agg.level;
   const int64_t n = n_max;
   prof_begin(PH_GROUPS, st);
   const int64_t* Gp = b.nnodes + La;
   const LevelNodes& GL = b.lv[La];
+  GroupsExtra none;
+  memset(&none, 0, sizeof(none));
+  const GroupsExtra& x = ex ? *ex : none;
+  // the sort's status words and a ticket word are free by now (or the caller's)
+  uint64_t* gst = x.gst ? x.gst : reinterpret_cast<uint64_t*>(b.os_status);
+  uint32_t* gctr = x.gctr ? x.gctr : b.os_ctr;
   {
-    // the sort's status words and a ticket word are free by now
-    uint64_t* gst = reinterpret_cast<uint64_t*>(b.os_status);
-    uint32_t* gctr = b.os_ctr;
     const int64_t tiles = cdiv(n + 1, GS_TILE);
-    if (tiles * GS_NV * 2 > (int64_t)b.os_ntiles * 2 * SORT_BUCKETS) return ALTO_E_ARG;   // never: words to spare
+    const int64_t xwords = x.xst ? cdiv(n + 1, x.xtile) * x.xper : 0;   // the caller's, after ours
+    if (!x.gst && (tiles * GS_NV + xwords) * 2 > (int64_t)b.os_ntiles * 2 * SORT_BUCKETS)
+      return ALTO_E_ARG;   // never: words to spare
     const int64_t pb = cdiv(tiles * GS_NV, 256);
-    k_group_scan_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(Gp, gst, gctr);
+    if (!x.cleared) k_group_scan_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(Gp, gst, gctr, x);
     k_group_scan<<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.nsm,
                                                                   MEAN_CHUNK_ROWS, gst, gctr, status);
   }
-  k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, out);
-  k_chunks<<<grid_for(n, 256), 256, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.nsm, b.chunks, MEAN_CHUNK_ROWS);
-  k_counts<<<1, 1, 0, st>>>(Gp, b.em, agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, b.nch, b.nsm, Mp, out.counts, out.tok_off,
-                            out, b.scal, status);
+  k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, b.nsm,
+                                                     b.chunks, MEAN_CHUNK_ROWS, out,
+                                                     agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, Mp, b.scal, x,
+                                                     status);
   ALTO_LAUNCH_CHECK();
   prof_end(PH_GROUPS, st);
   ProfScope ps_gather(PH_GATHER, st);
@@ -1261,10 +1322,11 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
 }
 
 template int groups_run<BatchSrc>(const KeyGeom&, const RouteGeom&, const alto_agg&, const BatchSrc&, const uint64_t*,
-                                  int64_t, AggBufs&, const int64_t*, const GroupOut&, int32_t*, hipStream_t);
+                                  int64_t, AggBufs&, const int64_t*, const GroupOut&, int32_t*, hipStream_t,
+                                  const GroupsExtra*);
 template int groups_run<MergedSrc>(const KeyGeom&, const RouteGeom&, const alto_agg&, const MergedSrc&,
                                    const uint64_t*, int64_t, AggBufs&, const int64_t*, const GroupOut&, int32_t*,
-                                   hipStream_t);
+                                   hipStream_t, const GroupsExtra*);
 
 namespace {
 __global__ void k_empty(GroupOut out, int64_t* offs, int num_dest) {

@@ -79,6 +79,16 @@ __device__ inline void raise_status(int32_t* st, int code) {
   }
 }
 
+// Element count of a call whose count may be on the device (n_dev, written by
+// earlier work on the stream, e.g. a previous stage's emitted count): n_max bounds
+// every buffer; a device count outside [0, n_max] is clamped (and reported as
+// CAPACITY by the call's first kernel).
+__device__ inline int64_t dev_n(const int64_t* n_dev, int64_t n_max) {
+  if (!n_dev) return n_max;
+  const int64_t v = *n_dev;
+  return v < 0 ? 0 : (v > n_max ? n_max : v);
+}
+
 // ---------------------------------------------------------------------------
 // wave / block primitives
 // ---------------------------------------------------------------------------
@@ -196,6 +206,40 @@ __device__ inline uint64_t lb64_resolve(uint64_t* st, int64_t tile, int64_t stri
     if (u & LB64_INC) break;
   }
   __hip_atomic_store(&st[tile * stride], LB64_INC | (excl + count), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return excl;
+}
+
+// The same look-back by a whole wave: its lanes read the words of up to 64
+// earlier tiles at once, so a tile far from the last inclusive prefix waits for
+// one round trip per 64 tiles instead of one per tile. All 64 lanes call it;
+// the count was published before (lb64_publish).
+__device__ inline uint64_t lb64_resolve_wave(uint64_t* st, int64_t tile, int64_t stride, uint64_t count,
+                                             int32_t* status) {
+  const int lane = lane_id();
+  uint64_t excl = 0;
+  for (int64_t t = tile - 1; t >= 0; t -= ALTO_WAVE) {
+    const int64_t tt = t - lane;
+    uint64_t u = LB64_INC;   // before tile 0: nothing to add
+    if (tt >= 0) {
+      u = __hip_atomic_load(&st[tt * stride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      int spin = 0;
+      while (u == 0) {
+        if (++spin > LB_SPIN_LIMIT) {
+          if (status) raise_status(status, ALTO_E_INTERNAL);
+          u = LB64_INC;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        u = __hip_atomic_load(&st[tt * stride], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    const uint64_t inc = __ballot((u & LB64_INC) != 0ull);
+    const int first = inc ? __builtin_ctzll(inc) : ALTO_WAVE - 1;   // the nearest inclusive prefix
+    excl += wave_sum(lane <= first ? (u & (LB64_AGG - 1ull)) : 0ull);
+    if (inc) break;   // uniform
+  }
+  if (lane == 0) __hip_atomic_store(&st[tile * stride], LB64_INC | (excl + count), __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
   return excl;
 }
 

@@ -175,10 +175,12 @@ int alto_route(const uint64_t* keys, int64_t n, const alto_layout* layout, int32
   return route_run(g, rg, keys, n, b, perm, dest_offsets, dest, nullptr, 0, 1, 0, status, stream);
 }
 
-int alto_aggregate(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
-                   const float* payload_f32, int64_t n, const alto_layout* layout, const alto_agg* agg,
-                   int32_t route_level, int32_t num_dest, int32_t* perm, int64_t* dest_offsets, int32_t* dest,
-                   alto_groups* out, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream) {
+int alto_aggregate_dev(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
+                       const float* payload_f32, int64_t n, const int64_t* n_dev, const alto_layout* layout,
+                       const alto_agg* agg, int32_t route_level, int32_t num_dest, int32_t* perm,
+                       int64_t* dest_offsets, int32_t* dest, alto_groups* out, int32_t* status, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
+  // n: the batch's count (n_dev null) or its bound (the count is *n_dev on the device)
   if (!layout_ok(layout) || n < 0 || n > N_LIMIT || num_dest < 1 || num_dest > (1 << 24) || !status || !out ||
       !out->counts || !agg_ok(layout, agg, route_level, num_dest) || out->cap_groups < 0 || out->cap_tokens < 0 ||
       out->cap_mask < 0)
@@ -200,7 +202,15 @@ int alto_aggregate(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, con
   plan_buffers(g, n, rg, agg, route_level, c, b);
   if (!c.ok) return ALTO_E_ARG;
   return aggregate_run(g, rg, route_level, *agg, keys, fan, fan_ld, payload_i32, payload_f32, n, b, perm,
-                       dest_offsets, dest, o, status, stream);
+                       dest_offsets, dest, o, status, stream, n_dev);
+}
+
+int alto_aggregate(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
+                   const float* payload_f32, int64_t n, const alto_layout* layout, const alto_agg* agg,
+                   int32_t route_level, int32_t num_dest, int32_t* perm, int64_t* dest_offsets, int32_t* dest,
+                   alto_groups* out, int32_t* status, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return alto_aggregate_dev(keys, fan, fan_ld, payload_i32, payload_f32, n, nullptr, layout, agg, route_level,
+                            num_dest, perm, dest_offsets, dest, out, status, ws, ws_bytes, stream);
 }
 
 

@@ -58,7 +58,34 @@ struct SegJob {
   RouteGeom rg;
   const SortCtl* skip_ctl;  // nullable: every kernel returns at once when skip_ctl->dp (the sort
                             // placed the elements directly and set the group level itself)
+  int32_t no_prep;          // the caller's previous kernel did seg_prep_device (one launch less)
+  uint2* gw;                // nullable, [cdiv(n_max, SEG_IT)]: for each run of SEG_IT elements from
+                            // element r * SEG_IT, x = level-lo boundaries before the run, y = its
+                            // boundary bits (bit i: element r * SEG_IT + i starts a level-lo node),
+                            // so the level-lo node of element r * SEG_IT + i is
+                            // x + popcount(y & (2^(i+1) - 1)) - 1
 };
+
+// What k_seg_prep does, for a kernel that runs before the segmentation pass and
+// knows the element count (n elements): clears the look-back words and the ticket,
+// and with no element writes the empty node counts. t0/stride: the calling
+// thread's grid-stride position.
+__device__ inline void seg_prep_device(const SegJob& j, int64_t n, int64_t t0, int64_t stride) {
+  const int64_t len = cdiv(n, SEG_TILE) * SEG_LB_STRIDE;
+  for (int64_t i = t0; i < len; i += stride) j.lb_status[i] = 0;
+  if (t0 == 0) {
+    *j.lb_ctr = 0;
+    if (n == 0) {
+      for (int m = j.lo; m < j.elem_level; ++m) {
+        j.nnodes[m] = 0;
+        j.lv[m].start[0] = 0;
+        if (m + 1 < j.elem_level) j.lv[m].fc[0] = 0;
+      }
+      if (j.dest_offsets)
+        for (uint32_t x = 0; x <= j.rg.num_dest; ++x) j.dest_offsets[x] = 0;
+    }
+  }
+}
 
 int seg_tiles(int64_t n_max);   // tiles of SEG_TILE elements
 int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st);

@@ -38,20 +38,8 @@ __device__ inline int32_t fan_at(const SegJob& j, int m, int64_t e) {
 // node counts and sentinels.
 __global__ void k_seg_prep(SegJob j) {
   if (skipped(j)) return;
-  const int64_t n = nelem(j);
-  const int64_t len = cdiv(n, TILE) * SEG_LB_STRIDE;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < len; i += (int64_t)gridDim.x * blockDim.x)
-    j.lb_status[i] = 0;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    *j.lb_ctr = 0;
-    if (n == 0) {
-      for (int m = j.lo; m < j.elem_level; ++m) {
-        j.nnodes[m] = 0;
-        j.lv[m].start[0] = 0;
-        if (m + 1 < j.elem_level) j.lv[m].fc[0] = 0;
-      }
-    }
-  }
+  // with no element (a count known on the device only) every destination is empty
+  seg_prep_device(j, nelem(j), (int64_t)blockIdx.x * blockDim.x + threadIdx.x, (int64_t)gridDim.x * blockDim.x);
 }
 
 // One pass over the sorted elements: per tile, the boundary flags of every level
@@ -149,6 +137,7 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
 #pragma unroll
     for (int q = 0; q < KM; ++q)
       base[q] = q < K ? (int32_t)(s_excl[q] + (uint32_t)((ex[q / 4] >> (16 * (q % 4))) & 0xFFFFu)) : 0;
+    if (j.gw && e0 < n) j.gw[e0 / IT] = make_uint2((uint32_t)base[0], fl[0]);
     // destination offsets, where the route prefix changes (keys reloaded: rare)
     if (j.dest_offsets) {
       int64_t* offs = j.dest_offsets;
@@ -307,7 +296,7 @@ int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st) {
   const int tiles = seg_tiles(job.n_max);
   if (!job.lb_status || !job.lb_ctr || job.lb_tiles < tiles) return ALTO_E_ARG;
   const int64_t pb = cdiv((int64_t)tiles * SEG_LB_STRIDE, 256);
-  k_seg_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(job);
+  if (!job.no_prep) k_seg_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(job);
   const int grid = tiles < 1024 ? tiles : 1024;
   if (K <= 2) k_seg_pass<2><<<grid, NT, 0, st>>>(g, job);
   else if (K <= 4) k_seg_pass<4><<<grid, NT, 0, st>>>(g, job);

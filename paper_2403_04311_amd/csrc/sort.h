@@ -119,6 +119,23 @@ struct FlowBufs {
 #define PREP_BLOCKS_MAX 512    // blocks of the input pass at most (marker regions)
 #define DP_MAX_BLOCKS 1024     // ctab_cap <= DP_CHUNK * DP_MAX_BLOCKS
 
+// A routing call's preparation, done by the one-workgroup sort before it sorts
+// (ctl null: none), so that a small call launches one kernel instead of four:
+// reset of the control block and the fingerprint sums, the count check of a
+// device-side count, each element's destination, the layout and declared-count
+// checks, and the fragment side of the fan fingerprint of levels flo..fhi.
+struct SmallPrep {
+  SortCtl* ctl;
+  uint64_t* fp_in;            // [ALTO_MAX_LEVELS + 1]
+  uint64_t* fp_nodes;         // [ALTO_MAX_LEVELS + 1] cleared
+  const int32_t* fan;         // level-major declared counts (null: no level checked)
+  int64_t fan_ld;
+  int32_t flo, fhi;
+  int32_t* dest;              // nullable
+  int32_t* status;
+  KeyGeom g;
+};
+
 struct SortBufs {
   const uint64_t* in_keys;   // input keys; values are the input indices
   uint64_t* tmp_keys;
@@ -135,6 +152,7 @@ struct SortBufs {
   int32_t* status;           // raised to ALTO_E_INTERNAL if a look-back wait gives up (may be null)
   int32_t* dest_out;         // with flows: destination of every input element, written by the
                              // counting sweep (input order); null: not wanted
+  SmallPrep prep;            // n_max <= SORT_SMALL_MAX only
 };
 
 int sort_tiles(int64_t n_max);   // tiles of SORT_OS_TILE elements (look-back passes)

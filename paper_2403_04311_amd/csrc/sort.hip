@@ -1035,6 +1035,65 @@ __global__ __launch_bounds__(SCAN_NT) void k_scan_apply(const T* in, T* out, int
 constexpr int SM_NT = 1024;
 constexpr int SM_NW = SM_NT / ALTO_WAVE;
 
+// The routing call's preparation (SmallPrep), by the whole workgroup.
+__device__ void small_prep(const SortBufs& b, const RouteGeom& rg, int64_t n, int64_t n_host, const int64_t* n_dev) {
+  const SmallPrep& pp = b.prep;
+  __shared__ unsigned long long s_fp[ALTO_MAX_LEVELS + 1];
+  __shared__ uint32_t s_flags;
+  if (threadIdx.x == 0) {
+    s_flags = 0u;
+    if (n_dev && (*n_dev < 0 || *n_dev > n_host)) raise_status(pp.status, ALTO_E_CAPACITY);
+    SortCtl* c = pp.ctl;
+    c->key_or = 0;
+    c->key_and = ~0ull;
+    c->dest_or = 0;
+    c->dest_and = ~0u;
+    c->mode = SORT_GENERAL;
+    c->flow_overflow = 0;
+    c->nflows = 0;
+    c->nflows_c = 0;
+    c->cmode = 0;
+    c->dp = 0;
+    c->dbits = -1;
+  }
+  const int flo = pp.flo, fhi = pp.fan ? pp.fhi : pp.flo - 1;
+  for (int i = threadIdx.x; i <= ALTO_MAX_LEVELS; i += SM_NT) {
+    s_fp[i] = 0ull;
+    pp.fp_nodes[i] = 0;
+    if (i < flo || i > fhi) pp.fp_in[i] = 0;
+  }
+  __syncthreads();
+  const KeyGeom& g = pp.g;
+  bool bad_layout = false, bad_fan = false;
+  for (int64_t e = threadIdx.x; e < n; e += SM_NT) {
+    const uint64_t k = b.in_keys[e];
+    bad_layout |= (k >> g.total) != 0;
+    if (pp.dest) pp.dest[e] = (int32_t)dest_of_key(rg, k);
+  }
+  // one level at a time: a scalar sum per level, a wave sum, one LDS add per wave
+  for (int m = flo; m <= fhi; ++m) {
+    const int sh = g.shift[m], shc = g.shift[m + 1];
+    const uint64_t tm = (uint64_t)g.tagmask[m + 1];
+    uint64_t acc = 0;
+    for (int64_t e = threadIdx.x; e < n; e += SM_NT) {
+      const uint64_t k = b.in_keys[e];
+      const int32_t f = pp.fan[(int64_t)(m - 1) * pp.fan_ld + e];
+      bad_fan |= (f < 1) || ((int64_t)((k >> shc) & tm) >= (int64_t)f);
+      acc += fan_term(m, key_prefix(k, sh), (uint32_t)f);
+    }
+    acc = wave_sum(acc);
+    if (lane_id() == 0 && acc) atomicAdd(&s_fp[m], (unsigned long long)acc);
+  }
+  if (bad_layout) atomicOr(&s_flags, 1u);
+  if (bad_fan) atomicOr(&s_flags, 2u);
+  __syncthreads();
+  for (int m = flo + (int)threadIdx.x; m <= fhi; m += SM_NT) pp.fp_in[m] = (uint64_t)s_fp[m];
+  if (threadIdx.x == 0) {
+    if (s_flags & 1u) raise_status(pp.status, ALTO_E_LAYOUT);
+    if (s_flags & 2u) raise_status(pp.status, ALTO_E_FANOUT);
+  }
+}
+
 // IT items per thread (IT * SM_NT elements at most): launched with the smallest IT
 // that holds the host's bound on the count, so small sorts rank fewer items per pass.
 template <int IT>
@@ -1049,8 +1108,13 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
   __shared__ uint32_t s_dor[SM_NW], s_dand[SM_NW];
   __shared__ int s_np;
   __shared__ int s_lo[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
-  const int64_t n = load_n(n_host, n_dev);
-  if (n > IT * SM_NT) return;   // the multi-block path sorts it
+  int64_t n = load_n(n_host, n_dev);
+  // the call's only sort (its bound fits here): a device count outside [0, bound]
+  // is clamped (and reported by the preparation); otherwise larger counts are the
+  // multi-block path's
+  if (n_host <= IT * SM_NT) n = n < 0 ? 0 : (n > n_host ? n_host : n);
+  if (b.prep.ctl) small_prep(b, rg, n, n_host, n_dev);
+  if (n > IT * SM_NT) return;
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;

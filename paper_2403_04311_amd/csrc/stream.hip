@@ -22,7 +22,7 @@
 
 namespace {
 
-constexpr uint64_t HT_EMPTY = ~0ull;
+constexpr uint64_t HT_EMPTY = EMIT_EMPTY;
 
 struct StreamCtl {
   int32_t error;     // data error of an earlier step (the handle is poisoned)
@@ -31,9 +31,17 @@ struct StreamCtl {
   int64_t top;       // free slots on the stack (MEAN)
   int64_t emitted;   // keys in the emitted set
   int64_t merged;    // live + step, this step
-  int64_t merged1;   // merged + 1 (scan length)
-  int64_t pad2[2];
+  int64_t merged1;   // merged + 1
+  // this step's totals, from the last tile of the live-set update: kept leaves,
+  // freed arena slots, slots needed (MEAN)
+  int64_t knext, ftot, atot;
+  uint32_t done[2];  // blocks finished, per kernel that may end the step
 };
+
+// live-set update: tiles of LU_TILE merged elements, LU_IT consecutive ones per thread
+constexpr int LU_NT = 256;
+constexpr int LU_IT = 8;
+constexpr int LU_TILE = LU_NT * LU_IT;
 
 struct LiveSet {
   uint64_t* key;
@@ -73,46 +81,47 @@ __global__ void k_stream_begin(const StreamCtl* ctl, int32_t* status) {
   if (threadIdx.x == 0 && blockIdx.x == 0 && ctl->error) raise_status(status, ctl->error);
 }
 
-__global__ void k_stream_end(StreamCtl* ctl, const int32_t* status) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    const int32_t s = *status;
-    if (s != 0 && ctl->error == 0) ctl->error = s;
-  }
-}
-
-// Fragments of groups that were already emitted are late.
-__global__ void k_late(const uint64_t* __restrict__ keys, int64_t n, int shiftLa, const uint64_t* __restrict__ ht,
-                       int64_t htcap, int32_t* status) {
-  bool late = false;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-    const uint64_t gk = key_prefix(keys[i], shiftLa);
-    int64_t h = (int64_t)(mix64(gk) & (uint64_t)(htcap - 1));
-    for (int64_t p = 0; p < htcap; ++p) {
-      const uint64_t v = ht[h];
-      if (v == gk) {
-        late = true;
-        break;
-      }
-      if (v == HT_EMPTY) break;
-      h = (h + 1) & (htcap - 1);
-    }
-  }
-  if (late) raise_status(status, ALTO_E_LATE);
-}
-
 // Merge path: every element finds its place by binary search in the other run.
 // Live elements go before equal step keys (which are duplicates, reported later).
 // Also adds the live leaves' terms of the fan fingerprint.
+// Also, so that the step launches fewer kernels: reports a poisoned handle, finds
+// late fragments (their group is in the emitted set), writes the step's destination
+// offsets (from its sorted keys) and does the segmentation pass's preparation for
+// the merged run (seg_prep_device), and clears the look-back words and tickets of
+// the group scan (gst, ctr[0]) and the live-set update (lst, ctr[1]).
 __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCtl* ctl, int64_t cap, LiveSet live,
                                                const uint64_t* __restrict__ sk, const uint32_t* __restrict__ sperm,
                                                int64_t n, int flo, int fhi, uint64_t* mkey, int32_t* msrc,
-                                               uint64_t* fp_in) {
+                                               uint64_t* fp_in, const int64_t* n_dev, int shiftLa,
+                                               const uint64_t* __restrict__ ht, int64_t htcap, int64_t* dest_offsets,
+                                               SegJob sj, uint64_t* gst, uint64_t* lst, uint32_t* ctr,
+                                               int32_t* status) {
+  n = dev_n(n_dev, n);
   int64_t Lc = ctl->live;
   Lc = Lc < 0 ? 0 : (Lc > cap ? cap : Lc);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = (int64_t)gridDim.x * blockDim.x;
+  if (gtid == 0) {
     ctl->merged = Lc + n;
     ctl->merged1 = Lc + n + 1;
+    ctl->knext = 0;
+    ctl->ftot = 0;
+    ctl->atot = 0;
+    ctl->done[0] = 0;
+    ctl->done[1] = 0;
+    ctr[0] = 0;
+    ctr[1] = 0;
+    if (ctl->error) raise_status(status, ctl->error);
   }
+  seg_prep_device(sj, Lc + n, gtid, gstride);
+  if (gst) {
+    const int64_t gl = cdiv(Lc + n + 1, GROUP_SCAN_TILE) * GROUP_SCAN_WORDS;
+    for (int64_t i = gtid; i < gl; i += gstride) gst[i] = 0;
+    const int64_t ll = cdiv(Lc + n, LU_TILE) * 3;
+    for (int64_t i = gtid; i < ll; i += gstride) lst[i] = 0;
+  }
+  if (dest_offsets && n == 0 && gtid == 0)
+    for (uint32_t x = 0; x <= rg.num_dest; ++x) dest_offsets[x] = 0;
+  bool late = false;
   const int nl = fhi - flo + 1;
   uint64_t fp[ALTO_MAX_LEVELS];
   int sh[ALTO_MAX_LEVELS];
@@ -145,8 +154,22 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
       }
       mkey[j + lo] = k;
       msrc[j + lo] = (int32_t)sperm[j];
+      late |= emitted_has(key_prefix(k, shiftLa), ht, htcap);
+      if (dest_offsets) {
+        // the step's destination offsets, where the destination changes in its sorted keys
+        const uint32_t d = dest_of_key(rg, k);
+        if (j == 0) {
+          for (uint32_t x = 0; x <= d; ++x) dest_offsets[x] = 0;
+        } else {
+          const uint32_t dp = dest_of_key(rg, sk[j - 1]);
+          for (uint32_t x = dp + 1; x <= d; ++x) dest_offsets[x] = j;
+        }
+        if (j == n - 1)
+          for (uint32_t x = d + 1; x <= rg.num_dest; ++x) dest_offsets[x] = n;
+      }
     }
   }
+  if (late) raise_status(status, ALTO_E_LATE);
 #pragma unroll
   for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
     if (q < nl) {
@@ -156,164 +179,205 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   }
 }
 
-// Per merged element: survives (its group is not emitted), frees its arena slot
-// (emitted live leaf), or needs a slot (surviving step leaf).
-// Per merged element: kept (its group is not released), arena slot freed (MEAN: a
-// released group's carried element), slot needed (MEAN: a kept group's new element).
-// One thread per element; its group is the last node starting at or before it (the
-// nodes of level La cover the merged elements in order), found by binary search.
-__global__ void k_keep(LevelNodes L, const int64_t* Gp, const int32_t* __restrict__ msrc, const StreamCtl* ctl,
-                       int32_t* keep, int64_t* freef, int64_t* allocf, int mean) {
-  const int64_t G = *Gp;
-  const int64_t M = ctl->merged;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < M; e += (int64_t)gridDim.x * blockDim.x) {
-    int64_t lo = 0, hi = G - 1;
-    while (lo < hi) {
-      const int64_t mid = (lo + hi + 1) >> 1;
-      if (L.start[mid] <= e) lo = mid;
-      else hi = mid - 1;
-    }
-    const bool ok = G > 0 && L.ok[lo];
-    const bool live_elem = msrc[e] < 0;
-    keep[e] = ok ? 0 : 1;
-    freef[e] = (mean && ok && live_elem) ? 1 : 0;
-    allocf[e] = (mean && !ok && !live_elem) ? 1 : 0;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    keep[M] = 0;
-    freef[M] = 0;
-    allocf[M] = 0;
-  }
-}
-
-__global__ void k_free_slots(const StreamCtl* ctl, int64_t cap, const int32_t* __restrict__ msrc,
-                             const int64_t* __restrict__ freef_scan, LiveSet old, int32_t* stack, int32_t* status) {
-  const int64_t M = ctl->merged, top = ctl->top;
-  bool bad = false;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < M; e += (int64_t)gridDim.x * blockDim.x) {
-    if (freef_scan[e + 1] != freef_scan[e]) {
-      const int64_t pos = top + freef_scan[e];
-      const int32_t i = -1 - msrc[e];
-      if (pos >= 0 && pos < cap && i >= 0 && i < cap) stack[pos] = old.slot[i];
-      else bad = true;
-    }
-  }
-  if (bad) raise_status(status, ALTO_E_CAPACITY);
-}
-
-__device__ inline int64_t alloc_pos(const StreamCtl* ctl, const int64_t* freef_scan, const int64_t* allocf_scan,
-                                    int64_t e) {
-  const int64_t M = ctl->merged;
-  return ctl->top + freef_scan[M] - allocf_scan[M] + allocf_scan[e];
-}
-
-__global__ void k_live_write(KeyGeom g, const StreamCtl* ctl, int64_t cap, const uint64_t* __restrict__ mkey,
-                             const int32_t* __restrict__ msrc, const int32_t* __restrict__ keep_scan,
-                             const int64_t* __restrict__ freef_scan, const int64_t* __restrict__ allocf_scan,
-                             LiveSet old, LiveSet nw, const int32_t* __restrict__ sp32, const int32_t* __restrict__ sfan,
-                             int64_t sfan_ld, const int32_t* stack, int mean, int32_t* status) {
-  const int64_t M = ctl->merged;
-  const int nf = g.depth - 1;
-  bool bad = false;
-  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < M; e += (int64_t)gridDim.x * blockDim.x) {
-    if (keep_scan[e + 1] == keep_scan[e]) continue;
-    const int64_t ki = keep_scan[e];
-    if (ki >= cap) {
-      bad = true;
-      continue;
-    }
-    const int32_t s = msrc[e];
-    nw.key[ki] = mkey[e];
-    if (s < 0) {
-      const int64_t i = -1 - (int64_t)s;
-      nw.p32[ki] = old.p32[i];
-      for (int l = 0; l < nf; ++l) nw.fan[(int64_t)l * cap + ki] = old.fan[(int64_t)l * cap + i];
-      if (mean) nw.slot[ki] = old.slot[i];
-    } else {
-      nw.p32[ki] = sp32 ? sp32[s] : 0;
-      for (int l = 0; l < nf; ++l) nw.fan[(int64_t)l * cap + ki] = sfan[(int64_t)l * sfan_ld + s];
-      if (mean) {
-        const int64_t pos = alloc_pos(ctl, freef_scan, allocf_scan, e);
-        if (pos >= 0 && pos < cap) nw.slot[ki] = stack[pos];
-        else {
-          nw.slot[ki] = 0;
-          bad = true;
-        }
-      }
-    }
-  }
-  if (bad) raise_status(status, ALTO_E_CAPACITY);
-}
-
-// Rows of surviving step leaves go to their arena slots (one wave per row).
-__global__ void k_arena_copy(const StreamCtl* ctl, int64_t cap, const int32_t* __restrict__ msrc,
-                             const int64_t* __restrict__ freef_scan, const int64_t* __restrict__ allocf_scan,
-                             const int32_t* stack, const float* __restrict__ spf, int dim, float* arena) {
-  const int64_t M = ctl->merged;
-  const int lane = lane_id();
-  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / ALTO_WAVE;
-  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / ALTO_WAVE;
-  for (int64_t e = wave; e < M; e += nwaves) {
-    if (allocf_scan[e + 1] == allocf_scan[e]) continue;
-    const int64_t pos = alloc_pos(ctl, freef_scan, allocf_scan, e);
-    if (pos < 0 || pos >= cap) continue;
-    const int64_t slot = stack[pos];
-    if (slot < 0 || slot >= cap) continue;
-    const float* src = spf + (int64_t)msrc[e] * dim;
-    float* dst = arena + slot * (int64_t)dim;
-    for (int c = lane; c < dim; c += ALTO_WAVE) dst[c] = src[c];
-  }
-}
-
-__global__ void k_stream_finish(StreamCtl* ctl, int64_t cap, const int32_t* keep_scan, const int64_t* freef_scan,
-                                const int64_t* allocf_scan, int mean, int32_t* status) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const int64_t M = ctl->merged;
-  const int64_t K = keep_scan[M];
+// The step's end, by the last block to finish the last kernel: the new live
+// count (and MEAN: the free-slot stack top); the handle is poisoned if the step
+// reported an error.
+__device__ void stream_finish(StreamCtl* ctl, int64_t cap, int mean, int32_t* status) {
+  const int64_t K = __hip_atomic_load(&ctl->knext, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (K > cap) raise_status(status, ALTO_E_CAPACITY);
   ctl->live = K > cap ? cap : K;
   if (mean) {
-    int64_t t = ctl->top + freef_scan[M] - allocf_scan[M];
+    const int64_t A = __hip_atomic_load(&ctl->atot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t F = __hip_atomic_load(&ctl->ftot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int64_t t = ctl->top - A + F;
     if (t < 0 || t > cap) {
       raise_status(status, ALTO_E_CAPACITY);
       t = t < 0 ? 0 : cap;
     }
     ctl->top = t;
   }
+  const int32_t sv = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (sv != 0 && ctl->error == 0) ctl->error = sv;
 }
 
-// Remember the emitted groups.
-__global__ void k_emit_insert(KeyGeom g, int La, LevelNodes L, const int64_t* Gp, const uint64_t* __restrict__ mkey,
-                              uint64_t* ht, int64_t htcap, int64_t max_groups, StreamCtl* ctl, int32_t* status) {
-  const int64_t G = *Gp;
-  bool full = false;
-  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
-    if (!L.ok[u]) continue;
-    const uint64_t gk = key_prefix(mkey[L.start[u]], g.shift[La]);
-    int64_t h = (int64_t)(mix64(gk) & (uint64_t)(htcap - 1));
-    bool done = false;
-    for (int64_t p = 0; p < htcap && !done; ++p) {
-      const uint64_t v = ht[h];
-      if (v == gk) {
-        done = true;
-      } else if (v == HT_EMPTY) {
-        const uint64_t old = atomicCAS((unsigned long long*)&ht[h], (unsigned long long)HT_EMPTY, (unsigned long long)gk);
-        if (old == HT_EMPTY || old == gk) {
-          done = true;
-          if (old == HT_EMPTY) {
-            const int64_t c = atomicAdd((unsigned long long*)&ctl->emitted, 1ull);
-            if (c + 1 > max_groups) full = true;
+// Whether this block is the last of the grid to get here (counter *done, cleared
+// by the merge). Every block calls it once, all its threads.
+__device__ inline bool last_block(uint32_t* done) {
+  __shared__ int s_last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    s_last = atomicAdd(done, 1u) == gridDim.x - 1 ? 1 : 0;
+    if (s_last) __threadfence();
+  }
+  __syncthreads();
+  return s_last != 0;
+}
+
+// The live-set update. Per merged element: kept (its group is not released) or
+// not. A kept element goes to the new live set at its rank among the kept ones
+// (exclusive scan over the merged run in one pass: tiles by ticket, a block scan,
+// a look-back over earlier tiles by one wave per scanned value). MEAN: a released
+// carried element frees its arena slot (listed in fslot, in scan order) and a kept
+// step element needs one (listed in alist with its live position and step row,
+// for k_arena_slots). The group of each element comes from the segmentation
+// pass's boundary words (gw). The last tile writes the totals; with CONCAT the
+// last block ends the step.
+static_assert(SEG_IT % LU_IT == 0, "a thread's elements lie in one boundary word");
+
+__global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, const uint2* __restrict__ gw,
+                                                       const uint64_t* __restrict__ mkey,
+                                                       const int32_t* __restrict__ msrc, StreamCtl* ctl,
+                                                       int64_t cap, LiveSet old, LiveSet nw,
+                                                       const int32_t* __restrict__ sp32,
+                                                       const int32_t* __restrict__ sfan, int64_t sfan_ld, int mean,
+                                                       int32_t* fslot, int64_t* alist, uint64_t* st, uint32_t* ctr,
+                                                       int32_t* status) {
+  constexpr uint64_t F21 = (1ull << 21) - 1ull;   // a tile's counts fit 21 bits (LU_TILE < 2^21)
+  const int64_t M = ctl->merged;
+  const int64_t ntiles = cdiv(M, LU_TILE);
+  const int nf = g.depth - 1;
+  __shared__ uint64_t s_w[LU_NT / ALTO_WAVE];
+  __shared__ int64_t s_ex[3];
+  __shared__ uint32_t s_tile;
+  bool bad = false;
+  if ((int64_t)blockIdx.x < ntiles) {
+    while (true) {
+      if (threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
+      __syncthreads();
+      const int64_t tile = (int64_t)s_tile;
+      if (tile >= ntiles) break;   // uniform
+      const int64_t e0 = tile * LU_TILE + (int64_t)threadIdx.x * LU_IT;
+      int32_t ms[LU_IT];
+      uint32_t km = 0, fm = 0, am = 0;   // bit i: element e0 + i is kept / frees a slot / needs one
+      if (e0 < M) {
+        if (e0 + LU_IT <= M) {
+          const int4* p = reinterpret_cast<const int4*>(msrc + e0);
+#pragma unroll
+          for (int v = 0; v < LU_IT / 4; ++v) {
+            const int4 q = p[v];
+            ms[4 * v] = q.x;
+            ms[4 * v + 1] = q.y;
+            ms[4 * v + 2] = q.z;
+            ms[4 * v + 3] = q.w;
           }
         } else {
-          h = (h + 1) & (htcap - 1);
+#pragma unroll
+          for (int i = 0; i < LU_IT; ++i) ms[i] = e0 + i < M ? msrc[e0 + i] : 0;
         }
-      } else {
-        h = (h + 1) & (htcap - 1);
+        const uint2 w = gw[e0 / SEG_IT];
+        const int off = (int)(e0 % SEG_IT);
+        const uint32_t fs = w.y >> off;                                          // bit i: e0 + i starts a group
+        const int32_t u0 = (int32_t)w.x + __popc(w.y & ((1u << off) - 1u));      // groups started before e0
+#pragma unroll
+        for (int i = 0; i < LU_IT; ++i) {
+          if (e0 + i >= M) break;
+          const int32_t u = u0 + __popc(fs & ((2u << i) - 1u)) - 1;
+          const bool ok = u >= 0 && L.ok[u];
+          const bool carried = ms[i] < 0;
+          km |= (ok ? 0u : 1u) << i;
+          fm |= ((mean && ok && carried) ? 1u : 0u) << i;
+          am |= ((mean && !ok && !carried) ? 1u : 0u) << i;
+        }
       }
+      const uint64_t c = (uint64_t)__popc(km) | ((uint64_t)__popc(fm) << 21) | ((uint64_t)__popc(am) << 42);
+      uint64_t tot;
+      const uint64_t x = block_excl_scan<uint64_t, LU_NT>(c, s_w, &tot);
+      const int wv = threadIdx.x / ALTO_WAVE;
+      if (wv < 3) {
+        const uint64_t tq = (tot >> (21 * wv)) & F21;
+        if (lane_id() == 0) lb64_publish(st + wv, tile, 3, tq);
+        const uint64_t exq = lb64_resolve_wave(st + wv, tile, 3, tq, status);
+        if (lane_id() == 0) {
+          s_ex[wv] = (int64_t)exq;
+          if (tile == ntiles - 1) {
+            int64_t* totp = wv == 0 ? &ctl->knext : (wv == 1 ? &ctl->ftot : &ctl->atot);
+            __hip_atomic_store(totp, (int64_t)(exq + tq), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+      }
+      __syncthreads();
+      int64_t r0 = s_ex[0] + (int64_t)(x & F21), r1 = s_ex[1] + (int64_t)((x >> 21) & F21),
+              r2 = s_ex[2] + (int64_t)((x >> 42) & F21);
+      for (int i = 0; i < LU_IT; ++i) {
+        const int64_t e = e0 + i;
+        if (e >= M) break;
+        const int32_t s = ms[i];
+        if ((km >> i) & 1u) {
+          const int64_t ki = r0++;
+          if (ki >= cap) {
+            bad = true;
+            if (mean && s >= 0) alist[r2++] = -1;
+            continue;
+          }
+          nw.key[ki] = mkey[e];
+          if (s < 0) {
+            const int64_t li = -1 - (int64_t)s;
+            nw.p32[ki] = old.p32[li];
+            for (int l = 0; l < nf; ++l) nw.fan[(int64_t)l * cap + ki] = old.fan[(int64_t)l * cap + li];
+            if (mean) nw.slot[ki] = old.slot[li];
+          } else {
+            nw.p32[ki] = sp32 ? sp32[s] : 0;
+            for (int l = 0; l < nf; ++l) nw.fan[(int64_t)l * cap + ki] = sfan[(int64_t)l * sfan_ld + s];
+            if (mean) alist[r2++] = (ki << 32) | (int64_t)(uint32_t)s;
+          }
+        } else if (mean && s < 0) {
+          fslot[r1++] = old.slot[-1 - (int64_t)s];
+        }
+      }
+      __syncthreads();   // s_ex and the ticket are reused by the next tile
     }
-    if (!done) full = true;
   }
-  if (full) raise_status(status, ALTO_E_CAPACITY);
+  if (bad) raise_status(status, ALTO_E_CAPACITY);
+  if (last_block(&ctl->done[0]) && threadIdx.x == 0 && !mean) stream_finish(ctl, cap, 0, status);
+}
+
+// MEAN, after the live-set update: the arena slots of the kept step elements
+// (the slots freed this step first, in scan order, then the top of the free-slot
+// stack), their rows copied in (one wave per row), the freed slots not reused
+// pushed onto the stack; the last block ends the step.
+__global__ __launch_bounds__(256) void k_arena_slots(StreamCtl* ctl, int64_t cap, const int64_t* __restrict__ alist,
+                                                     const int32_t* __restrict__ fslot, int32_t* stack, LiveSet nw,
+                                                     const float* __restrict__ spf, int dim, int v4, float* arena,
+                                                     int32_t* status) {
+  const int64_t A = ctl->atot, F = ctl->ftot, top = ctl->top;
+  const int lane = lane_id();
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / ALTO_WAVE;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / ALTO_WAVE;
+  bool bad = false;
+  for (int64_t a = wave; a < A; a += nwaves) {   // wave-uniform
+    const int64_t v = alist[a];
+    if (v < 0) continue;   // its element did not fit the live set (reported)
+    int64_t slot = -1;
+    if (a < F) {
+      slot = fslot[a];
+    } else {
+      const int64_t p = top - 1 - (a - F);
+      if (p >= 0 && p < cap) slot = stack[p];
+    }
+    if (slot < 0 || slot >= cap) {
+      bad = true;
+      continue;
+    }
+    const int64_t ki = v >> 32, row = v & 0xFFFFFFFFll;
+    if (lane == 0) nw.slot[ki] = (int32_t)slot;
+    if (v4) {
+      const float4* src = reinterpret_cast<const float4*>(spf + row * dim);
+      float4* dst = reinterpret_cast<float4*>(arena + slot * (int64_t)dim);
+      for (int c = lane; c < dim / 4; c += ALTO_WAVE) dst[c] = src[c];
+    } else {
+      const float* src = spf + row * dim;
+      float* dst = arena + slot * (int64_t)dim;
+      for (int c = lane; c < dim; c += ALTO_WAVE) dst[c] = src[c];
+    }
+  }
+  for (int64_t f = A + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; f < F; f += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t p = top + (f - A);
+    if (p >= 0 && p < cap) stack[p] = fslot[f];
+    else bad = true;
+  }
+  if (bad) raise_status(status, ALTO_E_CAPACITY);
+  if (last_block(&ctl->done[1]) && threadIdx.x == 0) stream_finish(ctl, cap, 1, status);
 }
 
 // Group records for in-order release: the level-La prefix of every group of the
@@ -553,10 +617,11 @@ int alto_stream_create(const alto_layout* layout, int32_t route_level, int32_t n
   return ALTO_OK;
 }
 
-int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
-                     const int32_t* payload_i32, const float* payload_f32, int64_t n, int32_t* perm,
-                     int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status, void* ws,
-                     size_t ws_bytes, hipStream_t st) {
+int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
+                         const int32_t* payload_i32, const float* payload_f32, int64_t n, const int64_t* n_dev,
+                         int32_t* perm, int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status,
+                         void* ws, size_t ws_bytes, hipStream_t st) {
+  // n: the step's count (n_dev null) or its bound (the count is *n_dev on the device)
   if (!s || !status || !emitted || !emitted->counts || n < 0 || n > (int64_t)INT32_MAX / 2 ||
       emitted->cap_groups < 0 || emitted->cap_tokens < 0)
     return ALTO_E_ARG;
@@ -567,8 +632,8 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
   const KeyGeom& g = s->g;
   const int d = g.depth, La = agg.level;
   GroupOut o = dev_out(emitted);
-  k_stream_begin<<<1, 1, 0, st>>>(s->ctl, status);
   if (n == 0) {
+    k_stream_begin<<<1, 1, 0, st>>>(s->ctl, status);   // otherwise the merge reports a poisoned handle
     empty_outputs(o, dest_offsets, s->D, st);
     ALTO_LAUNCH_CHECK();
     return ALTO_OK;
@@ -581,20 +646,25 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
   plan_buffers(g, ntot, s->rg, &plan_agg, s->Lr, c, b);
   if (!c.ok) return ALTO_E_ARG;
   // 1. route the step on its own
-  int rc = route_run(g, s->rg, keys, n, b, perm, dest_offsets, dest, fan, fan_ld, La, d - 1, status, st);
+  // (destination offsets: written by the merge, from the step's sorted keys)
+  int rc = route_run(g, s->rg, keys, n, b, perm, dest_offsets, dest, fan, fan_ld, La, d - 1, status, st, true, false,
+                     false, n_dev);
   if (rc) return rc;
   prof_begin(PH_SEGMENT, st);
   const uint32_t* sperm = b.perm_used;
-  k_late<<<grid_for(n, 256), 256, 0, st>>>(keys, n, g.shift[La], s->ht, s->htcap, status);
-  // 2. merge with the live set
   LiveSet& old = s->live[s->cur];
   LiveSet& nw = s->live[s->cur ^ 1];
   uint64_t* mkey = b.tmp_keys;
   int32_t* msrc = reinterpret_cast<int32_t*>(b.tmp_vals);
   const int64_t* Mp = &s->ctl->merged;
-  k_merge<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc,
-                                               b.fp_in);
-  // 3. nodes and completion over the merged run
+  // look-back words, after the segmentation pass's in the sort's status words:
+  // the group scan's, then the live-set update's; tickets after the pass's
+  const int64_t seg_words = (cdiv(ntot, SEG_TILE) * SEG_LB_STRIDE + 1) & ~(int64_t)1;
+  const int64_t g_words = cdiv(ntot + 1, GROUP_SCAN_TILE) * GROUP_SCAN_WORDS;
+  const int64_t l_words = cdiv(ntot, LU_TILE) * 3;
+  if (seg_words + 2 * (g_words + l_words) > (int64_t)b.os_ntiles * 2 * SORT_BUCKETS) return ALTO_E_ARG;   // never
+  uint64_t* gst = reinterpret_cast<uint64_t*>(b.os_status + seg_words);
+  uint64_t* lst = gst + g_words;
   SegJob j;
   memset(&j, 0, sizeof(j));
   j.keys = mkey;
@@ -617,9 +687,17 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
   j.lb_tiles = b.os_ntiles * 2 * SORT_BUCKETS / SEG_LB_STRIDE;   // the sort's status words, free by now
   j.fp_nodes = b.fp_nodes;
   j.status = status;
+  j.no_prep = 1;   // done by the merge
+  j.gw = b.gw;
+  // 2. merge with the live set (also: late fragments, a poisoned handle, the step's
+  // destination offsets, the clearing of the step's look-back words)
+  k_merge<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc,
+                                               b.fp_in, n_dev, g.shift[La], s->ht, s->htcap, dest_offsets, j, gst,
+                                               lst, b.os_ctr + 1, status);
+  // 3. nodes and completion over the merged run
   rc = seg_run(g, j, st);
   if (rc) return rc;
-  fp_compare_launch(b.fp_in, b.fp_nodes, La, d - 1, status, st);
+  bool words_clear = true;
   if (s->pht && s->Lr < La) {
     // in-order release, a parent's children in one destination: the merged run
     // already lists them in key order
@@ -652,40 +730,62 @@ int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, i
     none.num_dest = 1;
     rc = sort_pairs(rb, ntot, Gp, none, g.total - g.shift[La], false, st);
     if (rc) return rc;
+    words_clear = false;   // the sort used them
     k_release<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, b.rsk, b.ridx, g.shift[La - 1] - g.shift[La],
                                                    (uint64_t)g.tagmask[La], s->pht, s->pcur, s->htcap, status);
     ALTO_LAUNCH_CHECK();
   }
   prof_end(PH_SEGMENT, st);
-  // 4. emitted groups (payload over all of each group's leaves, in key order)
+  // 4. emitted groups (payload over all of each group's leaves, in key order); their
+  // record kernel also compares the fan fingerprints and fills the emitted set
   MergedSrc src{msrc, payload_i32, fan, fan_ld, payload_f32, old.p32, old.fan, s->cap, old.slot, s->arena, s->cap,
                 agg.dim};
-  rc = groups_run<MergedSrc>(g, s->rg, agg, src, mkey, ntot, b, nullptr, o, status, st);
+  GroupsExtra ex;
+  memset(&ex, 0, sizeof(ex));
+  ex.fp_in = b.fp_in;
+  ex.fp_nodes = b.fp_nodes;
+  ex.flo = La;
+  ex.fhi = d - 1;
+  ex.xlo = 1;
+  ex.xhi = 0;
+  ex.gst = gst;
+  ex.gctr = b.os_ctr + 1;
+  ex.cleared = words_clear ? 1 : 0;
+  if (!words_clear) {
+    ex.xst = lst;
+    ex.xctr = b.os_ctr + 2;
+    ex.xlen = Mp;
+    ex.xtile = LU_TILE;
+    ex.xper = 3;
+  }
+  ex.ht = s->ht;
+  ex.htcap = s->htcap;
+  ex.max_emit = s->max_groups;
+  ex.emit_count = &s->ctl->emitted;
+  rc = groups_run<MergedSrc>(g, s->rg, agg, src, mkey, ntot, b, nullptr, o, status, st, &ex);
   if (rc) return rc;
   // 5. survivors become the new live set
-  const int64_t* Gp = b.nnodes + La;
-  int32_t* keep = b.em;
-  int64_t* freef = b.tokc;
-  int64_t* allocf = b.nch;
-  const int64_t* M1 = &s->ctl->merged1;
-  k_keep<<<grid_for(ntot, 256), 256, 0, st>>>(b.lv[La], Gp, msrc, s->ctl, keep, freef, allocf, mean ? 1 : 0);
-  rc = scan_exclusive<int32_t>(keep, keep, ntot + 1, M1, b.scan_i32, nullptr, st);
-  if (!rc && mean) rc = scan_exclusive<int64_t>(freef, freef, ntot + 1, M1, b.scan_i64, nullptr, st);
-  if (!rc && mean) rc = scan_exclusive<int64_t>(allocf, allocf, ntot + 1, M1, b.scan_i64, nullptr, st);
-  if (rc) return rc;
-  if (mean) k_free_slots<<<grid_for(ntot, 256), 256, 0, st>>>(s->ctl, s->cap, msrc, freef, old, s->stack, status);
-  k_live_write<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->ctl, s->cap, mkey, msrc, keep, freef, allocf, old, nw,
-                                                    payload_i32, fan, fan_ld, s->stack, mean ? 1 : 0, status);
-  if (mean)
-    k_arena_copy<<<grid_for(ntot * ALTO_WAVE, 256), 256, 0, st>>>(s->ctl, s->cap, msrc, freef, allocf, s->stack,
-                                                                  payload_f32, agg.dim, s->arena);
-  k_emit_insert<<<grid_for(ntot, 256), 256, 0, st>>>(g, La, b.lv[La], Gp, mkey, s->ht, s->htcap, s->max_groups, s->ctl,
-                                                     status);
-  k_stream_finish<<<1, 1, 0, st>>>(s->ctl, s->cap, keep, freef, allocf, mean ? 1 : 0, status);
-  k_stream_end<<<1, 1, 0, st>>>(s->ctl, status);
+  int32_t* fslot = b.em;
+  int64_t* alist = b.tokc;
+  k_live_update<<<grid_for(ntot, LU_TILE, 1024), LU_NT, 0, st>>>(g, b.lv[La], b.gw, mkey, msrc, s->ctl, s->cap, old, nw,
+                                                                payload_i32, fan, fan_ld, mean ? 1 : 0, fslot, alist,
+                                                                lst, b.os_ctr + 2, status);
+  if (mean) {
+    const bool v4 = agg.dim % 4 == 0 && ((reinterpret_cast<uintptr_t>(payload_f32) | reinterpret_cast<uintptr_t>(s->arena)) & 15) == 0;
+    k_arena_slots<<<grid_for(n * ALTO_WAVE, 256), 256, 0, st>>>(s->ctl, s->cap, alist, fslot, s->stack, nw,
+                                                                 payload_f32, agg.dim, v4 ? 1 : 0, s->arena, status);
+  }
   ALTO_LAUNCH_CHECK();
   s->cur ^= 1;
   return ALTO_OK;
+}
+
+int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
+                     const int32_t* payload_i32, const float* payload_f32, int64_t n, int32_t* perm,
+                     int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status, void* ws,
+                     size_t ws_bytes, hipStream_t st) {
+  return alto_stream_step_dev(s, keys, fan, fan_ld, payload_i32, payload_f32, n, nullptr, perm, dest_offsets, dest,
+                              emitted, status, ws, ws_bytes, st);
 }
 
 int alto_stream_pending(alto_stream* s, alto_groups* out, int32_t* status, hipStream_t st) {

@@ -137,7 +137,7 @@ def test_factool_batch_two_stages():
 
 
 def test_factool_stream_10000_steps():
-    log("config: FacTool windowed stream, 10,000 steps x 4,096 fragments, two chained stages")
+    log("config: FacTool windowed stream, 10,000 steps x 4,096 fragments, two stages chained on the device")
     w = W.config4("cuda")
     log(f"generated: window {w.info['window']:.0f}, long-lived fraction {w.info['calibrated_frac']:.3f}")
     step, steps = w.step, w.info["steps"]
@@ -181,8 +181,13 @@ def test_factool_stream_10000_steps():
         full = s in full_steps
         sA.step(keys_d[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gA, status=stA,
                 perm=perm if full else None, dest_offsets=offs if full else None, dest=dest if full else None)
+        # stage B takes stage A's records and count on the device (no host read between)
+        stB.zero_()
+        sB.step(gA.key, gA.fan_up.view(3, -1), gA.first_i32, None, out=gB, status=stB, n=step,
+                n_dev=gA.counts[0:1])
         torch.cuda.synchronize()
         assert int(stA.item()) == 0, s
+        assert int(stB.item()) == 0, s
         E = int(gA.counts[0])
         if full:
             rt = O.route(hkeys[a:b], w.bits, 2, 32)
@@ -191,10 +196,6 @@ def test_factool_stream_10000_steps():
             assert np.array_equal(offs.cpu().numpy(), rt.dest_offsets), s
             step_means[s] = (gA.key[:E].cpu().numpy().view(np.uint64).copy(), gA.mean[:E].cpu().numpy())
             checked_route += 1
-        stB.zero_()
-        sB.step(gA.key[:E], gA.fan_up.view(3, -1)[:, :E], gA.first_i32[:E], None, out=gB, status=stB, n=E)
-        torch.cuda.synchronize()
-        assert int(stB.item()) == 0, s
         ks = gA.key[:E].cpu().numpy().view(np.uint64)
         for kk in ks.tolist():
             got_step[kk] = s

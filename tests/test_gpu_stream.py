@@ -180,6 +180,61 @@ def _windowed_factool(seed, queries, W_frag, step):
     return path[:, order], fan[:, order], docid[order], pf[order]
 
 
+def gpu_chain(bits, keys, fan, p32, pf, cuts, step_max, max_live, max_groups, release="complete"):
+    """The two FacTool stages on the device, step by step, stage B reading stage A's
+    emitted count on the device (alto_stream_step_dev): no host read between the
+    stages. Returns per-step (stage A dict, stage B dict)."""
+    bB = W.CONFIG2_STAGE_B["bits"]
+    sA = alto.Stream(bits, 2, 32, 4, "mean", 768, max_live_leaves=max_live, max_groups=max_groups,
+                     step_max=step_max, release=release)
+    sB = alto.Stream(bB, 2, 32, 2, "concat", 1, max_live_leaves=max_live, max_groups=max_groups,
+                     step_max=step_max, release=release)
+    dk = U.to_dev(keys.astype(np.uint64).view(np.int64))
+    dfan = U.to_dev(fan.astype(np.int32))
+    d32 = U.to_dev(p32.astype(np.int32))
+    dpf = U.to_dev(pf.astype(np.float32))
+    gA = alto.new_groups(step_max, 4, "mean", 768, device="cuda")
+    gB = alto.new_groups(step_max, 2, "concat", 1, cap_tokens=max_live + step_max, device="cuda")
+    stA, stB = alto.new_status(), alto.new_status()
+    out = []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        stA.zero_()
+        stB.zero_()
+        sA.step(dk[a:b], dfan[:, a:b], d32[a:b], dpf[a:b], out=gA, status=stA, n=b - a)
+        sB.step(gA.key, gA.fan_up.view(3, -1), gA.first_i32, None, out=gB, status=stB, n=step_max,
+                n_dev=gA.counts[0:1])
+        torch.cuda.synchronize()
+        E, EB, TB = int(gA.counts[0]), int(gB.counts[0]), int(gB.counts[1])
+        out.append(({"status": int(stA.item()), "key": gA.key[:E].cpu().numpy().view(np.uint64),
+                     "count": gA.count[:E].cpu().numpy(), "first": gA.first_i32[:E].cpu().numpy(),
+                     "mean": gA.mean[:E].cpu().numpy()},
+                    {"status": int(stB.item()), "key": gB.key[:EB].cpu().numpy().view(np.uint64),
+                     "count": gB.count[:EB].cpu().numpy(), "gdest": gB.dest[:EB].cpu().numpy(),
+                     "tok_off": gB.tok_off[:EB + 1].cpu().numpy(), "tok": gB.tok[:TB].cpu().numpy()}))
+    sA.close()
+    sB.close()
+    return out
+
+
+def compare_chain(got, oA, bB, release):
+    """Stage A against the oracle's stream, stage B against the oracle's stream fed
+    with stage A's oracle emissions."""
+    sB = O.Stream(bB, 2, 32, 2, "concat", 1, release=release)
+    assert len(got) == len(oA[0])
+    for (ga, gb), (ca, ra) in zip(got, oA[0]):
+        assert ca == O.OK and ga["status"] == O.OK and gb["status"] == O.OK
+        assert np.array_equal(ga["key"], ra.groups.key)
+        assert np.array_equal(ga["count"], ra.groups.count)
+        assert np.array_equal(ga["first"], ra.groups.first_i32)
+        U.assert_mean_close(ga["mean"], ra.groups.mean)
+        rb = sB.step(ra.groups.key, ra.groups.fan_up, ra.groups.first_i32, None)
+        assert np.array_equal(gb["key"], rb.groups.key)
+        assert np.array_equal(gb["count"], rb.groups.count)
+        assert np.array_equal(gb["gdest"], rb.groups.dest)
+        assert np.array_equal(gb["tok_off"], rb.groups.tok_off)
+        assert np.array_equal(gb["tok"], rb.groups.tok)
+
+
 def test_factool_stream_two_stages():
     path, fan, docid, pf = _windowed_factool(7, 24, 3000, 256)
     bits = (31, 3, 2, 3, 8)
@@ -187,11 +242,14 @@ def test_factool_stream_two_stages():
     n = len(keys)
     cuts = list(range(0, n, 256)) + [n]
     cuts = sorted(set(cuts))
+    # stage B consumes stage A's emitted records step by step, on the device
+    got = gpu_chain(bits, keys, fan, docid, pf, cuts, 256, 8192, 1 << 14)
+    oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts)
+    compare_chain(got, oA, W.CONFIG2_STAGE_B["bits"], "complete")
+    # and through host-side copies of stage A's records, with per-step routing outputs
     gA = gpu_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, max_live=8192,
                    max_groups=1 << 14, step_max=256)
-    oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts)
     compare_steps(gA, oA, "mean", 4)
-    # stage B consumes stage A's emitted records step by step
     bB = W.CONFIG2_STAGE_B["bits"]
     kB, fB, pB, cB = [], [], [], [0]
     for r in gA[0]:
@@ -309,9 +367,11 @@ def test_factool_stream_in_order_two_stages():
     keys = O.pack_keys(path, bits)
     n = len(keys)
     cuts = sorted(set(list(range(0, n, 256)) + [n]))
+    oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, release="in_order")
+    got = gpu_chain(bits, keys, fan, docid, pf, cuts, 256, 8192, 1 << 14, release="in_order")
+    compare_chain(got, oA, W.CONFIG2_STAGE_B["bits"], "in_order")
     gA = gpu_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, max_live=8192,
                    max_groups=1 << 14, step_max=256, release="in_order")
-    oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, release="in_order")
     compare_steps(gA, oA, "mean", 4)
     bB = W.CONFIG2_STAGE_B["bits"]
     kB, fB, pB, cB = [], [], [], [0]
