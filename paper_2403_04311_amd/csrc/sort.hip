@@ -1034,6 +1034,7 @@ __global__ __launch_bounds__(SCAN_NT) void k_scan_apply(const T* in, T* out, int
 // ---------------------------------------------------------------------------
 constexpr int SM_NT = 1024;
 constexpr int SM_NW = SM_NT / ALTO_WAVE;
+static_assert(SM_NT == 4 * SORT_BUCKETS && SM_NW == 16, "the count scan gives each thread 4 waves of one digit");
 
 // The routing call's preparation (SmallPrep), by the whole workgroup.
 __device__ void small_prep(const SortBufs& b, const RouteGeom& rg, int64_t n, int64_t n_host, const int64_t* n_dev) {
@@ -1102,7 +1103,6 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
   __shared__ uint64_t s_key[IT * SM_NT];
   __shared__ uint32_t s_val[IT * SM_NT];
   __shared__ uint16_t s_cnt[SM_NW][SORT_BUCKETS];
-  __shared__ uint32_t s_base[SORT_BUCKETS];
   __shared__ uint32_t s_wsum[SM_NW];
   __shared__ uint64_t s_or[SM_NW], s_and[SM_NW];
   __shared__ uint32_t s_dor[SM_NW], s_dand[SM_NW];
@@ -1199,30 +1199,31 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
       off[j] = wave_rank(s_cnt[w], dig[j], valid);
     }
     __syncthreads();
-    if (threadIdx.x < SORT_BUCKETS) {
-      const int d = threadIdx.x;
-      uint32_t run = 0;
-      for (int ww = 0; ww < SM_NW; ++ww) {
-        const uint32_t c = s_cnt[ww][d];
-        s_cnt[ww][d] = (uint16_t)run;
-        run += c;
-      }
-      s_base[d] = run;
-    }
-    __syncthreads();
     {
-      // every thread of the block takes part (the scan holds barriers)
+      // the per-wave digit counts in (digit, wave) order, scanned by the whole block:
+      // thread t holds digit t / 4, waves 4 (t % 4) .. 4 (t % 4) + 3; the counters
+      // become the wave's first position for the digit
+      const int d = threadIdx.x >> 2, q0 = (threadIdx.x & 3) * 4;
+      uint32_t c[4], sum = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        c[k] = s_cnt[q0 + k][d];
+        sum += c[k];
+      }
       uint32_t tot;
-      const uint32_t v = threadIdx.x < SORT_BUCKETS ? s_base[threadIdx.x] : 0u;
-      const uint32_t ex = block_excl_scan<uint32_t, SM_NT>(v, s_wsum, &tot);
-      if (threadIdx.x < SORT_BUCKETS) s_base[threadIdx.x] = ex;
+      uint32_t ex = block_excl_scan<uint32_t, SM_NT>(sum, s_wsum, &tot);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        s_cnt[q0 + k][d] = (uint16_t)ex;
+        ex += c[k];
+      }
     }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
       const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       if (e < n) {
-        const uint32_t pos = s_base[dig[j]] + (uint32_t)s_cnt[w][dig[j]] + off[j];
+        const uint32_t pos = (uint32_t)s_cnt[w][dig[j]] + off[j];
         s_key[pos] = key[j];
         s_val[pos] = val[j];
       }

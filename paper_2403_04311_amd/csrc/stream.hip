@@ -28,14 +28,13 @@ struct StreamCtl {
   int32_t error;     // data error of an earlier step (the handle is poisoned)
   int32_t pad;
   int64_t live;      // carried leaves
-  int64_t top;       // free slots on the stack (MEAN)
+  int64_t top[2];    // free slots on the stack (MEAN), by step parity: read [p], written [p ^ 1]
   int64_t emitted;   // keys in the emitted set
   int64_t merged;    // live + step, this step
   int64_t merged1;   // merged + 1
   // this step's totals, from the last tile of the live-set update: kept leaves,
   // freed arena slots, slots needed (MEAN)
   int64_t knext, ftot, atot;
-  uint32_t done[2];  // blocks finished, per kernel that may end the step
 };
 
 // live-set update: tiles of LU_TILE merged elements, LU_IT consecutive ones per thread
@@ -70,7 +69,7 @@ __global__ void k_stream_init(StreamCtl* ctl, int32_t* stack, int64_t cap, uint6
   if (t0 == 0) {
     ctl->error = 0;
     ctl->live = 0;
-    ctl->top = stack ? cap : 0;
+    ctl->top[0] = ctl->top[1] = stack ? cap : 0;
     ctl->emitted = 0;
     ctl->merged = 0;
     ctl->merged1 = 1;
@@ -106,8 +105,6 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
     ctl->knext = 0;
     ctl->ftot = 0;
     ctl->atot = 0;
-    ctl->done[0] = 0;
-    ctl->done[1] = 0;
     ctr[0] = 0;
     ctr[1] = 0;
     if (ctl->error) raise_status(status, ctl->error);
@@ -179,39 +176,11 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   }
 }
 
-// The step's end, by the last block to finish the last kernel: the new live
-// count (and MEAN: the free-slot stack top); the handle is poisoned if the step
-// reported an error.
-__device__ void stream_finish(StreamCtl* ctl, int64_t cap, int mean, int32_t* status) {
-  const int64_t K = __hip_atomic_load(&ctl->knext, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (K > cap) raise_status(status, ALTO_E_CAPACITY);
-  ctl->live = K > cap ? cap : K;
-  if (mean) {
-    const int64_t A = __hip_atomic_load(&ctl->atot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int64_t F = __hip_atomic_load(&ctl->ftot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    int64_t t = ctl->top - A + F;
-    if (t < 0 || t > cap) {
-      raise_status(status, ALTO_E_CAPACITY);
-      t = t < 0 ? 0 : cap;
-    }
-    ctl->top = t;
-  }
+// The step's end, by one thread once every error of the step that can still be
+// raised is known: the handle is poisoned if the step reported an error.
+__device__ inline void stream_poison(StreamCtl* ctl, int32_t* status) {
   const int32_t sv = __hip_atomic_load(status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (sv != 0 && ctl->error == 0) ctl->error = sv;
-}
-
-// Whether this block is the last of the grid to get here (counter *done, cleared
-// by the merge). Every block calls it once, all its threads.
-__device__ inline bool last_block(uint32_t* done) {
-  __shared__ int s_last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    s_last = atomicAdd(done, 1u) == gridDim.x - 1 ? 1 : 0;
-    if (s_last) __threadfence();
-  }
-  __syncthreads();
-  return s_last != 0;
 }
 
 // The live-set update. Per merged element: kept (its group is not released) or
@@ -221,10 +190,15 @@ __device__ inline bool last_block(uint32_t* done) {
 // carried element frees its arena slot (listed in fslot, in scan order) and a kept
 // step element needs one (listed in alist with its live position and step row,
 // for k_arena_slots). The group of each element comes from the segmentation
-// pass's boundary words (gw). The last tile writes the totals; with CONCAT the
-// last block ends the step.
+// pass's boundary words (gw). The last tile writes the totals and the new live
+// count; a live set over capacity is found from the total (the elements past it
+// are not written), so with CONCAT the last tile also ends the step.
+// The kept elements' fields are loaded before the scan (they do not depend on the
+// ranks), all of a thread's elements at once; fans of the first NFP levels too, the
+// others level by level after it.
 static_assert(SEG_IT % LU_IT == 0, "a thread's elements lie in one boundary word");
 
+template <int NFP>
 __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, const uint2* __restrict__ gw,
                                                        const uint64_t* __restrict__ mkey,
                                                        const int32_t* __restrict__ msrc, StreamCtl* ctl,
@@ -240,7 +214,14 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   __shared__ uint64_t s_w[LU_NT / ALTO_WAVE];
   __shared__ int64_t s_ex[3];
   __shared__ uint32_t s_tile;
-  bool bad = false;
+  if (ntiles == 0) {
+    // nothing carried and nothing arrived
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      ctl->live = 0;
+      if (!mean) stream_poison(ctl, status);
+    }
+    return;
+  }
   if ((int64_t)blockIdx.x < ntiles) {
     while (true) {
       if (threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
@@ -280,6 +261,21 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
           am |= ((mean && !ok && !carried) ? 1u : 0u) << i;
         }
       }
+      uint64_t kk[LU_IT];
+      int32_t pv[LU_IT], sv[LU_IT], fv[NFP > 0 ? NFP : 1][LU_IT];
+#pragma unroll
+      for (int i = 0; i < LU_IT; ++i) {
+        const bool kept = (km >> i) & 1u;
+        const int32_t s = ms[i];
+        const bool car = s < 0;
+        const int64_t li = -1 - (int64_t)s;
+        kk[i] = kept ? mkey[e0 + i] : 0ull;
+        pv[i] = kept ? (car ? old.p32[li] : (sp32 ? sp32[s] : 0)) : 0;
+        sv[i] = (car && (kept || ((fm >> i) & 1u)) && mean) ? old.slot[li] : 0;
+#pragma unroll
+        for (int l = 0; l < NFP; ++l)
+          fv[l][i] = kept ? (car ? old.fan[(int64_t)l * cap + li] : sfan[(int64_t)l * sfan_ld + s]) : 0;
+      }
       const uint64_t c = (uint64_t)__popc(km) | ((uint64_t)__popc(fm) << 21) | ((uint64_t)__popc(am) << 42);
       uint64_t tot;
       const uint64_t x = block_excl_scan<uint64_t, LU_NT>(c, s_w, &tot);
@@ -291,60 +287,86 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
         if (lane_id() == 0) {
           s_ex[wv] = (int64_t)exq;
           if (tile == ntiles - 1) {
-            int64_t* totp = wv == 0 ? &ctl->knext : (wv == 1 ? &ctl->ftot : &ctl->atot);
-            __hip_atomic_store(totp, (int64_t)(exq + tq), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const int64_t T = (int64_t)(exq + tq);
+            if (wv == 0) {
+              if (T > cap) raise_status(status, ALTO_E_CAPACITY);
+              ctl->live = T > cap ? cap : T;   // read by the next step only
+              if (!mean) stream_poison(ctl, status);
+            } else {
+              __hip_atomic_store(wv == 1 ? &ctl->ftot : &ctl->atot, T, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
           }
         }
       }
       __syncthreads();
-      int64_t r0 = s_ex[0] + (int64_t)(x & F21), r1 = s_ex[1] + (int64_t)((x >> 21) & F21),
-              r2 = s_ex[2] + (int64_t)((x >> 42) & F21);
+      const int64_t k0 = s_ex[0] + (int64_t)(x & F21);
+      int64_t r0 = k0, r1 = s_ex[1] + (int64_t)((x >> 21) & F21), r2 = s_ex[2] + (int64_t)((x >> 42) & F21);
+#pragma unroll
       for (int i = 0; i < LU_IT; ++i) {
-        const int64_t e = e0 + i;
-        if (e >= M) break;
         const int32_t s = ms[i];
         if ((km >> i) & 1u) {
           const int64_t ki = r0++;
-          if (ki >= cap) {
-            bad = true;
-            if (mean && s >= 0) alist[r2++] = -1;
-            continue;
+          const bool fits = ki < cap;
+          if (fits) {
+            nw.key[ki] = kk[i];
+            nw.p32[ki] = pv[i];
+#pragma unroll
+            for (int l = 0; l < NFP; ++l) nw.fan[(int64_t)l * cap + ki] = fv[l][i];
+            if (mean) nw.slot[ki] = s < 0 ? sv[i] : 0;   // a step element's slot: k_arena_slots
           }
-          nw.key[ki] = mkey[e];
-          if (s < 0) {
-            const int64_t li = -1 - (int64_t)s;
-            nw.p32[ki] = old.p32[li];
-            for (int l = 0; l < nf; ++l) nw.fan[(int64_t)l * cap + ki] = old.fan[(int64_t)l * cap + li];
-            if (mean) nw.slot[ki] = old.slot[li];
-          } else {
-            nw.p32[ki] = sp32 ? sp32[s] : 0;
-            for (int l = 0; l < nf; ++l) nw.fan[(int64_t)l * cap + ki] = sfan[(int64_t)l * sfan_ld + s];
-            if (mean) alist[r2++] = (ki << 32) | (int64_t)(uint32_t)s;
-          }
-        } else if (mean && s < 0) {
-          fslot[r1++] = old.slot[-1 - (int64_t)s];
+          if (mean && s >= 0) alist[r2++] = fits ? ((ki << 32) | (int64_t)(uint32_t)s) : -1;
+        } else if ((fm >> i) & 1u) {
+          fslot[r1++] = sv[i];
+        }
+      }
+      // fans of the other levels, one level at a time
+      for (int l = NFP; l < nf; ++l) {
+        int32_t f[LU_IT];
+#pragma unroll
+        for (int i = 0; i < LU_IT; ++i) {
+          const int32_t s = ms[i];
+          f[i] = ((km >> i) & 1u) ? (s < 0 ? old.fan[(int64_t)l * cap + (-1 - (int64_t)s)]
+                                           : sfan[(int64_t)l * sfan_ld + s])
+                                  : 0;
+        }
+        int64_t ki = k0;
+#pragma unroll
+        for (int i = 0; i < LU_IT; ++i) {
+          if (!((km >> i) & 1u)) continue;
+          if (ki < cap) nw.fan[(int64_t)l * cap + ki] = f[i];
+          ++ki;
         }
       }
       __syncthreads();   // s_ex and the ticket are reused by the next tile
     }
   }
-  if (bad) raise_status(status, ALTO_E_CAPACITY);
-  if (last_block(&ctl->done[0]) && threadIdx.x == 0 && !mean) stream_finish(ctl, cap, 0, status);
 }
 
 // MEAN, after the live-set update: the arena slots of the kept step elements
 // (the slots freed this step first, in scan order, then the top of the free-slot
 // stack), their rows copied in (one wave per row), the freed slots not reused
-// pushed onto the stack; the last block ends the step.
+// pushed onto the stack. The stack top is read from top[par] and written to
+// top[par ^ 1] (blocks read it while the first one writes); that thread also
+// ends the step (every error of the step is known from the totals by then).
 __global__ __launch_bounds__(256) void k_arena_slots(StreamCtl* ctl, int64_t cap, const int64_t* __restrict__ alist,
                                                      const int32_t* __restrict__ fslot, int32_t* stack, LiveSet nw,
                                                      const float* __restrict__ spf, int dim, int v4, float* arena,
-                                                     int32_t* status) {
-  const int64_t A = ctl->atot, F = ctl->ftot, top = ctl->top;
+                                                     int par, int32_t* status) {
+  const int64_t A = ctl->atot, F = ctl->ftot, top = ctl->top[par];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    // the stack after the step; too few free slots, or more than the capacity
+    // (the slots past either end are neither taken nor written)
+    int64_t t = top - A + F;
+    if (t < 0 || t > cap) {
+      raise_status(status, ALTO_E_CAPACITY);
+      t = t < 0 ? 0 : cap;
+    }
+    ctl->top[par ^ 1] = t;
+    stream_poison(ctl, status);
+  }
   const int lane = lane_id();
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / ALTO_WAVE;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) / ALTO_WAVE;
-  bool bad = false;
   for (int64_t a = wave; a < A; a += nwaves) {   // wave-uniform
     const int64_t v = alist[a];
     if (v < 0) continue;   // its element did not fit the live set (reported)
@@ -355,10 +377,7 @@ __global__ __launch_bounds__(256) void k_arena_slots(StreamCtl* ctl, int64_t cap
       const int64_t p = top - 1 - (a - F);
       if (p >= 0 && p < cap) slot = stack[p];
     }
-    if (slot < 0 || slot >= cap) {
-      bad = true;
-      continue;
-    }
+    if (slot < 0 || slot >= cap) continue;   // past the stack (reported above)
     const int64_t ki = v >> 32, row = v & 0xFFFFFFFFll;
     if (lane == 0) nw.slot[ki] = (int32_t)slot;
     if (v4) {
@@ -374,10 +393,7 @@ __global__ __launch_bounds__(256) void k_arena_slots(StreamCtl* ctl, int64_t cap
   for (int64_t f = A + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; f < F; f += (int64_t)gridDim.x * blockDim.x) {
     const int64_t p = top + (f - A);
     if (p >= 0 && p < cap) stack[p] = fslot[f];
-    else bad = true;
   }
-  if (bad) raise_status(status, ALTO_E_CAPACITY);
-  if (last_block(&ctl->done[1]) && threadIdx.x == 0) stream_finish(ctl, cap, 1, status);
 }
 
 // Group records for in-order release: the level-La prefix of every group of the
@@ -767,13 +783,22 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   // 5. survivors become the new live set
   int32_t* fslot = b.em;
   int64_t* alist = b.tokc;
-  k_live_update<<<grid_for(ntot, LU_TILE, 1024), LU_NT, 0, st>>>(g, b.lv[La], b.gw, mkey, msrc, s->ctl, s->cap, old, nw,
-                                                                payload_i32, fan, fan_ld, mean ? 1 : 0, fslot, alist,
-                                                                lst, b.os_ctr + 2, status);
+  {
+    const int nf = d - 1;
+#define ALTO_LU_CASE(P)                                                                                          \
+  k_live_update<P><<<grid_for(ntot, LU_TILE, 1024), LU_NT, 0, st>>>(g, b.lv[La], b.gw, mkey, msrc, s->ctl, s->cap, \
+                                                                   old, nw, payload_i32, fan, fan_ld, mean ? 1 : 0, \
+                                                                   fslot, alist, lst, b.os_ctr + 2, status)
+    if (nf <= 1) ALTO_LU_CASE(1);
+    else if (nf == 2) ALTO_LU_CASE(2);
+    else ALTO_LU_CASE(3);
+#undef ALTO_LU_CASE
+  }
   if (mean) {
     const bool v4 = agg.dim % 4 == 0 && ((reinterpret_cast<uintptr_t>(payload_f32) | reinterpret_cast<uintptr_t>(s->arena)) & 15) == 0;
     k_arena_slots<<<grid_for(n * ALTO_WAVE, 256), 256, 0, st>>>(s->ctl, s->cap, alist, fslot, s->stack, nw,
-                                                                 payload_f32, agg.dim, v4 ? 1 : 0, s->arena, status);
+                                                                 payload_f32, agg.dim, v4 ? 1 : 0, s->arena, s->cur,
+                                                                 status);
   }
   ALTO_LAUNCH_CHECK();
   s->cur ^= 1;
