@@ -592,7 +592,59 @@ def bench_route_load(args):
                   "factool_stream": stream})
 
 
-WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_tokens,
+def bench_live_scaling(args):
+    """Per-step cost of a stream step against the size of the carried state. A token
+    stream in config 3's layout (31, 6, 12) whose 256 sentences stay open (each
+    declares 4,095 tokens): every 4,096-fragment step adds 16 tokens to each, so the
+    live set grows by 4,096 leaves a step, to 1,044,480 after 255 steps. Reports the
+    device time per step at several live-set sizes and the least-squares slope."""
+    import numpy as np
+    import torch
+    from paper_2403_04311_amd import alto
+    bits, G, per, steps = (31, 6, 12), 256, 16, 255
+    step = G * per
+    rng = np.random.default_rng(20240307)
+    roots = rng.choice(1 << 31, size=G, replace=False).astype(np.int64)
+    # step s: tokens s*16 .. s*16+15 of every generator's sentence 0, generator-major
+    # within a tick (round robin), as config 3 arrives
+    t = np.arange(steps * per, dtype=np.int64)
+    tick, gen = np.meshgrid(t, np.arange(G), indexing="ij")
+    path = np.stack([roots[gen.ravel()], np.zeros(gen.size, np.int64), tick.ravel()]).astype(np.int32)
+    keys, st = alto.pack_keys(torch.from_numpy(path).cuda(), bits)
+    n = keys.numel()
+    fan = torch.empty((2, n), dtype=torch.int32, device="cuda")
+    fan[0].fill_(64)
+    fan[1].fill_(4095)
+    p32 = torch.arange(n, dtype=torch.int32, device="cuda")
+    out = alto.new_groups(step, 2, "concat", cap_tokens=step)
+    status = alto.new_status()
+
+    def run():
+        s = alto.Stream(bits, 2, 64, 2, "concat", 1, max_live_leaves=steps * step, max_groups=1 << 12,
+                        step_max=step)
+
+        def one(i):
+            s.step(keys[i * step:(i + 1) * step], fan[:, i * step:(i + 1) * step], p32[i * step:(i + 1) * step],
+                   None, out=out, status=status)
+        tot, per_ms = _stream_run(steps, one)
+        s.close()
+        return tot, per_ms
+    run()   # one untimed pass (255 steps)
+    tot, per_ms = run()
+    assert int(status.item()) == 0 and int(out.counts[0]) == 0
+    live = np.arange(steps) * step           # carried leaves before each step
+    slope, icpt = np.polyfit(live, np.asarray(per_ms) * 1e3, 1)
+    at = {}
+    for lo in (0, 1 << 16, 1 << 18, 1 << 19, 1 << 20):
+        sel = (live >= lo) & (live < lo + (1 << 16))
+        if sel.any():
+            at[str(lo)] = float(np.median(np.asarray(per_ms)[sel]) * 1e3)
+    return _line("open token stream (live set growing 4,096 leaves a step to 1,044,480), config 3 layout, "
+                 "concat per sentence, 64 destinations", step, tot / steps, steps, 1, 0,
+                 {"step_us_p50_at_live": at, "step_us_per_1k_live": float(slope * 1e3), "step_us_at_live_0": float(icpt)})
+
+
+WORKLOADS = {"tiny": bench_tiny, "factool": bench_factool, "tokens": bench_tokens, "live_scaling": bench_live_scaling,
              "factool_stream": bench_factool_stream, "join": bench_join, "split": bench_split,
              "route_load": bench_route_load}
 

@@ -151,7 +151,7 @@ __global__ __launch_bounds__(PREP_NT, 8) void k_prep(const uint64_t* __restrict_
       for (int q = 0; q < NL; ++q) {
         const uint32_t child = (uint32_t)((k[u] >> shc[q]) & (uint64_t)tm[q]);
         bad_fan |= (f[u][q] < 1) || ((int64_t)child >= (int64_t)f[u][q]);
-        if (!skip_fp || q < qx0 || q >= qx0 + nx) fp[q] += fan_term(flo + q, key_prefix(k[u], sh[q]), (uint32_t)f[u][q]);
+        if (!skip_fp || q < qx0 || q >= qx0 + nx) fp[q] += fan_term(g.fkey, flo + q, key_prefix(k[u], sh[q]), (uint32_t)f[u][q]);
       }
       if (NL > 0 && fl.dp) {
         // markers (direct placement): leaves whose tag is their parent's count - 1,
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(256) void k_prep_fp(const uint64_t* __restrict__ ke
 #pragma unroll
     for (int x = 0; x < FLOW_EXACT_LEVELS; ++x) {
       const int m = xlo + x;
-      if (m <= xhi) fp[x] += fan_term(m, key_prefix(k, g.shift[m]), (uint32_t)fan[(int64_t)(m - 1) * fan_ld + i]);
+      if (m <= xhi) fp[x] += fan_term(g.fkey, m, key_prefix(k, g.shift[m]), (uint32_t)fan[(int64_t)(m - 1) * fan_ld + i]);
     }
   }
 #pragma unroll
@@ -394,14 +394,14 @@ __global__ __launch_bounds__(256) void k_dp_groups(KeyGeom g, FlowBufs fl, const
     const int32_t nf = fan[(int64_t)(La - 1) * fan_ld + row];
     L.nfan[r] = nf;
     sk[s] = pk;
-    fpm += (uint64_t)cnt * fan_term(La, key_prefix(pk, g.shift[La]), (uint32_t)nf);
+    fpm += (uint64_t)cnt * fan_term(g.fkey, La, key_prefix(pk, g.shift[La]), (uint32_t)nf);
 #pragma unroll
     for (int q = 0; q < ALTO_MAX_LEVELS; ++q) {
       if (q >= nc) break;
       const int m = carry_lo + q;
       const int32_t cf = fan[(int64_t)(m - 1) * fan_ld + row];
       if (carry_fan) carry_fan[(int64_t)q * carry_ld + r] = cf;
-      fpc[q] += (uint64_t)cnt * fan_term(m, key_prefix(pk, g.shift[m]), (uint32_t)cf);
+      fpc[q] += (uint64_t)cnt * fan_term(g.fkey, m, key_prefix(pk, g.shift[m]), (uint32_t)cf);
     }
     if (dest_offsets) {
       const uint32_t d = fl.fdest[r];
@@ -1046,6 +1046,7 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
   fl.dp = (allow_dp && !n_dev && fl.hcap && fl.mk_key && fan && fhi == g.depth - 1 && flo <= fhi) ? 1 : 0;
   fl.dp_level = g.depth - 1;
   fl.fp_child = b.fp_nodes + (g.depth - 1);
+  fl.fkey = g.fkey;
   b.fl.dp = fl.dp;
   // child ranks need the route level's declared child counts, read here when the
   // route level is among the levels whose counts are checked

@@ -19,6 +19,7 @@ struct KeyGeom {
   int32_t total;                      // sum of bits
   int32_t shift[ALTO_MAX_LEVELS + 1]; // shift[l] = bits below level l (l = 1..depth), shift[0] = total
   uint32_t tagmask[ALTO_MAX_LEVELS + 1];  // tagmask[l] = 2^bits[l-1] - 1
+  uint64_t fkey;                      // key of the fan fingerprint, drawn afresh for every call
 };
 
 __host__ __device__ inline uint64_t key_prefix(uint64_t k, int sh) { return sh >= 64 ? 0ull : (k >> sh); }
@@ -51,8 +52,11 @@ __host__ __device__ inline uint32_t dest_of_key(const RouteGeom& r, uint64_t k) 
 // Term of the additive multiset fingerprint used to check that all carriers of a
 // node declare the same child count (sums of a random-looking function over a
 // multiset, Clarke et al., "Incremental multiset hash functions", ASIACRYPT 2003).
-__host__ __device__ inline uint64_t fan_term(int level, uint64_t node, uint32_t fan) {
-  return mix64(node * 0x9E3779B97F4A7C15ull + ((uint64_t)fan << 8) + (uint64_t)level + 0x632BE59BD9B4E019ull);
+// Keyed: the node is hashed with the call's key first, so which (node, count)
+// pairs collide depends on a key the input cannot know; the count and level are
+// then mixed into that hash.
+__host__ __device__ inline uint64_t fan_term(uint64_t key, int level, uint64_t node, uint32_t fan) {
+  return mix64(mix64(node ^ key) ^ (((uint64_t)fan << 8) | (uint64_t)level));
 }
 
 // ---------------------------------------------------------------------------
@@ -275,6 +279,7 @@ struct WsCarver {
   }
 };
 
-// Geometry helpers (host).
+// Geometry helpers (host). make_geom draws a fresh fingerprint key (fresh_fp_key).
 KeyGeom make_geom(const alto_layout* l);
+uint64_t fresh_fp_key();
 RouteGeom make_route(const KeyGeom& g, int route_level, int num_dest);

@@ -3,6 +3,9 @@
 #include <mutex>
 #include <string.h>
 
+#include <atomic>
+#include <random>
+
 #include "aggregate.h"
 
 // Workspace of alto_aggregate_noalloc: one array per GPU, held until the process
@@ -10,9 +13,21 @@
 // for the symbol); each device's address comes from hipGetSymbolAddress.
 static __device__ __align__(256) unsigned char scratch[ALTO_NOALLOC_SCRATCH_BYTES];
 
+// Fingerprint keys: SplitMix64 outputs of a counter that starts at a value drawn
+// from the operating system's entropy source when the library first needs one.
+uint64_t fresh_fp_key() {
+  static std::atomic<uint64_t> next{0};
+  static const uint64_t base = [] {
+    std::random_device rd;
+    return ((uint64_t)rd() << 32) ^ (uint64_t)rd();
+  }();
+  return mix64(base + 0x9E3779B97F4A7C15ull * next.fetch_add(1, std::memory_order_relaxed));
+}
+
 KeyGeom make_geom(const alto_layout* l) {
   KeyGeom g;
   memset(&g, 0, sizeof(g));
+  g.fkey = fresh_fp_key();
   g.depth = l->depth;
   int total = 0;
   for (int i = 0; i < l->depth; ++i) total += l->bits[i];

@@ -232,11 +232,11 @@ __global__ __launch_bounds__(256) void k_seg_nodes(KeyGeom g, SegJob j, int m) {
     if (!ok && m > j.lo) j.lv[m - 1].bad[L.par[u]] = 1;
     if (j.fp_nodes) {
       const uint64_t k = j.keys[s];
-      fpm += (uint64_t)cnt * fan_term(m, key_prefix(k, es), (uint32_t)L.nfan[u]);
+      fpm += (uint64_t)cnt * fan_term(g.fkey, m, key_prefix(k, es), (uint32_t)L.nfan[u]);
 #pragma unroll
       for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
         if (q < nc)
-          fpc[q] += (uint64_t)cnt * fan_term(clo + q, key_prefix(k, esc[q]),
+          fpc[q] += (uint64_t)cnt * fan_term(g.fkey, clo + q, key_prefix(k, esc[q]),
                                              (uint32_t)j.carry_fan[(int64_t)q * j.carry_ld + u]);
     }
   }

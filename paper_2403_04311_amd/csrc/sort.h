@@ -57,6 +57,7 @@ struct SortCtl {
 // Distinct route-level prefixes ("flows") of one batch and their rank in
 // (destination, prefix) order; used by the packed mode.
 struct FlowBufs {
+  uint64_t fkey;         // the call's fan fingerprint key (KeyGeom.fkey)
   uint64_t* ht_key;      // [hcap] open-addressing set of prefixes, ~0 = empty
   uint32_t* ht_rank;     // [hcap] rank of the prefix held in the slot
   uint64_t* ct_key;      // [hcap] compact rank table (power of two >= 2 x flows), ~0 = empty

@@ -351,7 +351,7 @@ __global__ __launch_bounds__(256) void k_dp_sums(FlowBufs fl, const SortCtl* ctl
       const uint32_t f = fl.cfan[c];
       sum += f;
       bad |= fl.cmk[c] != 1u;
-      fp += (uint64_t)f * fan_term(fl.dp_level, fl.ctab[c] >> fl.cshift, f);
+      fp += (uint64_t)f * fan_term(fl.fkey, fl.dp_level, fl.ctab[c] >> fl.cshift, f);
     }
     sum = wave_sum(sum);
     fp = wave_sum(fp);
@@ -1080,7 +1080,7 @@ __device__ void small_prep(const SortBufs& b, const RouteGeom& rg, int64_t n, in
       const uint64_t k = b.in_keys[e];
       const int32_t f = pp.fan[(int64_t)(m - 1) * pp.fan_ld + e];
       bad_fan |= (f < 1) || ((int64_t)((k >> shc) & tm) >= (int64_t)f);
-      acc += fan_term(m, key_prefix(k, sh), (uint32_t)f);
+      acc += fan_term(g.fkey, m, key_prefix(k, sh), (uint32_t)f);
     }
     acc = wave_sum(acc);
     if (lane_id() == 0 && acc) atomicAdd(&s_fp[m], (unsigned long long)acc);

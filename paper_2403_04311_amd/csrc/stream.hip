@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
 #pragma unroll
       for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
         if (q < nl)
-          fp[q] += fan_term(flo + q, key_prefix(k, sh[q]), (uint32_t)live.fan[(int64_t)(flo + q - 1) * cap + t]);
+          fp[q] += fan_term(g.fkey, flo + q, key_prefix(k, sh[q]), (uint32_t)live.fan[(int64_t)(flo + q - 1) * cap + t]);
     } else {
       const int64_t j = t - Lc;
       const uint64_t k = sk[j];
@@ -648,6 +648,7 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   const KeyGeom& g = s->g;
   const int d = g.depth, La = agg.level;
   GroupOut o = dev_out(emitted);
+  s->g.fkey = fresh_fp_key();   // a fresh fingerprint key for every step
   if (n == 0) {
     k_stream_begin<<<1, 1, 0, st>>>(s->ctl, status);   // otherwise the merge reports a poisoned handle
     empty_outputs(o, dest_offsets, s->D, st);
