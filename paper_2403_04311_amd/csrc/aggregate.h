@@ -162,7 +162,8 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
 //  - the emitted set (ht null: none): the record kernel inserts the key of every
 //    emitted group into an insert-only open-addressing set of htcap (a power of
 //    two) slots, counting new keys in *emit_count; more than max_emit keys, or a
-//    full table, raise ALTO_E_CAPACITY.
+//    full table, raise ALTO_E_CAPACITY;
+//  - concat / multi-chunk means left to the caller (defer_concat, defer_combine).
 struct GroupsExtra {
   const uint64_t* fp_in;
   const uint64_t* fp_nodes;
@@ -178,9 +179,72 @@ struct GroupsExtra {
   uint64_t* ht;
   int64_t htcap, max_emit;
   int64_t* emit_count;
+  // the gathers the caller runs itself later (concat_chunks / mean_combine_chunks)
+  int32_t defer_concat, defer_combine;
 };
 
 #define EMIT_EMPTY (~0ull)
+
+// Concatenation of the chunks [c0, NC) step cstride (a block each): every row of a
+// chunk copies its int32 payload to the chunk's token range.
+template <typename Src>
+__device__ inline void concat_chunks(const Chunk* __restrict__ chunks, int64_t NC, const Src& src, int32_t* tok,
+                                     int64_t cap_tokens, int64_t c0, int64_t cstride) {
+  for (int64_t c = c0; c < NC; c += cstride) {
+    const Chunk ch = chunks[c];
+    for (int r = threadIdx.x; r < ch.len; r += blockDim.x) {
+      const int64_t o = ch.out + r;
+      if (o < cap_tokens) tok[o] = src.p32_of(src.row(ch.begin + r));
+    }
+  }
+}
+
+// The same with one wave per chunk (wave wid of nw), for chunks of a few rows.
+template <typename Src>
+__device__ inline void concat_chunks_wave(const Chunk* __restrict__ chunks, int64_t NC, const Src& src, int32_t* tok,
+                                          int64_t cap_tokens, int64_t wid, int64_t nw) {
+  const int lane = lane_id();
+  for (int64_t c = wid; c < NC; c += nw) {
+    const Chunk ch = chunks[c];
+    for (int r = lane; r < ch.len; r += ALTO_WAVE) {
+      const int64_t o = ch.out + r;
+      if (o < cap_tokens) tok[o] = src.p32_of(src.row(ch.begin + r));
+    }
+  }
+}
+
+// The mean of every group of several chunks from its chunks' partial sums (chunk
+// order), chunks [c0, NC) step cstride, a block of 256 threads each: SUBS chunk
+// subsets x COLS columns; each thread sums every SUBS-th chunk, then the subsets are
+// added in subset order. Every thread of the block calls it (it holds barriers).
+__device__ inline void mean_combine_chunks(const Chunk* __restrict__ chunks, int64_t NC,
+                                           const double* __restrict__ part, int dim, float* mean,
+                                           int64_t cap_groups, int64_t c0, int64_t cstride) {
+  constexpr int COLS = 64, SUBS = 256 / COLS;
+  __shared__ double red[SUBS][COLS];
+  const int col_l = threadIdx.x % COLS, sidx = threadIdx.x / COLS;
+  for (int64_t c = c0; c < NC; c += cstride) {
+    const Chunk ch = chunks[c];
+    if (ch.k != 0 || ch.nch <= 1 || ch.e >= cap_groups) continue;   // uniform per block
+    for (int col0 = 0; col0 < dim; col0 += COLS) {
+      const int x = col0 + col_l;
+      double sum = 0.0;
+      if (x < dim) {
+#pragma unroll 4
+        for (int t = sidx; t < ch.nch; t += SUBS) sum += part[(ch.part + t) * (int64_t)dim + x];
+      }
+      red[sidx][col_l] = sum;
+      __syncthreads();
+      if (sidx == 0 && x < dim) {
+        double tot = 0.0;
+#pragma unroll
+        for (int q = 0; q < SUBS; ++q) tot += red[q][col_l];
+        mean[ch.e * (int64_t)dim + x] = (float)(tot / (double)ch.count);
+      }
+      __syncthreads();
+    }
+  }
+}
 
 // Inserts a group key into the emitted set: 1 = new, 0 = present, -1 = table full.
 __device__ inline int emitted_insert(uint64_t gk, uint64_t* ht, int64_t htcap) {

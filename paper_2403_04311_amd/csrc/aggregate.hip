@@ -665,14 +665,7 @@ __global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int 
 template <typename Src>
 __global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src src,
                                                 int32_t* tok, int64_t cap_tokens) {
-  const int64_t C = *nchunks;
-  for (int64_t c = blockIdx.x; c < C; c += gridDim.x) {
-    const Chunk ch = chunks[c];
-    for (int r = threadIdx.x; r < ch.len; r += blockDim.x) {
-      const int64_t o = ch.out + r;
-      if (o < cap_tokens) tok[o] = src.p32_of(src.row(ch.begin + r));
-    }
-  }
+  concat_chunks<Src>(chunks, *nchunks, src, tok, cap_tokens, blockIdx.x, gridDim.x);
 }
 
 // fp64 sum of the rows of one chunk of a group, in a fixed order: each lane sums
@@ -870,37 +863,11 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
   }
 }
 
-// Sum of a group's chunk partials in chunk order. 256 threads = SUBS chunk subsets
-// x COLS columns; each thread sums every SUBS-th chunk, then the subsets are added in
-// subset order.
+// The means of the groups of several chunks (mean_combine_chunks).
 __global__ __launch_bounds__(256) void k_mean_combine(const Chunk* __restrict__ chunks, const int64_t* nchunks,
                                                       const double* __restrict__ part, int dim, float* mean,
                                                       int64_t cap_groups) {
-  constexpr int COLS = 64, SUBS = 256 / COLS;
-  __shared__ double red[SUBS][COLS];
-  const int64_t NC = *nchunks;
-  const int col_l = threadIdx.x % COLS, sidx = threadIdx.x / COLS;
-  for (int64_t c = blockIdx.x; c < NC; c += gridDim.x) {
-    const Chunk ch = chunks[c];
-    if (ch.k != 0 || ch.nch <= 1 || ch.e >= cap_groups) continue;   // uniform per block
-    for (int col0 = 0; col0 < dim; col0 += COLS) {
-      const int x = col0 + col_l;
-      double s = 0.0;
-      if (x < dim) {
-#pragma unroll 4
-        for (int t = sidx; t < ch.nch; t += SUBS) s += part[(ch.part + t) * (int64_t)dim + x];
-      }
-      red[sidx][col_l] = s;
-      __syncthreads();
-      if (sidx == 0 && x < dim) {
-        double tot = 0.0;
-#pragma unroll
-        for (int q = 0; q < SUBS; ++q) tot += red[q][col_l];
-        mean[ch.e * (int64_t)dim + x] = (float)(tot / (double)ch.count);
-      }
-      __syncthreads();
-    }
-  }
+  mean_combine_chunks(chunks, *nchunks, part, dim, mean, cap_groups, blockIdx.x, gridDim.x);
 }
 
 __global__ void k_mask_out(LevelNodes L, const int64_t* Np, const uint64_t* __restrict__ keys, int shift,
@@ -1288,7 +1255,7 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
   ProfScope ps_gather(PH_GATHER, st);
   const int64_t* NCp = b.scal + 1;   // chunk count
   if (agg.op == ALTO_CONCAT_I32) {
-    if (out.tok) k_concat<Src><<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, src, out.tok, out.cap_tokens);
+    if (out.tok && !x.defer_concat) k_concat<Src><<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, src, out.tok, out.cap_tokens);
   } else if (out.mean) {
     const int dim = agg.dim;
     const bool v4 = (dim % 4 == 0) && src_rows_aligned16(src);
@@ -1316,7 +1283,8 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
       else ALTO_MEAN_CASE(1, 4);
     }
 #undef ALTO_MEAN_CASE
-    k_mean_combine<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, b.part, dim, out.mean, out.cap_groups);
+    if (!x.defer_combine)
+      k_mean_combine<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, b.part, dim, out.mean, out.cap_groups);
   }
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;

@@ -198,6 +198,17 @@ __device__ inline void stream_poison(StreamCtl* ctl, int32_t* status) {
 // others level by level after it.
 static_assert(SEG_IT % LU_IT == 0, "a thread's elements lie in one boundary word");
 
+// CONCAT: the same kernel also copies the emitted groups' tokens (the chunks that
+// k_group_out listed), one wave per chunk, in the blocks that have no tile (beside
+// the tiles, not after them); only when every block has a tile, after the tiles.
+struct ConcatJob {
+  const Chunk* chunks;
+  const int64_t* nchunks;
+  MergedSrc src;
+  int32_t* tok;           // null: no concatenation here
+  int64_t cap_tokens;
+};
+
 template <int NFP>
 __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, const uint2* __restrict__ gw,
                                                        const uint64_t* __restrict__ mkey,
@@ -206,7 +217,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
                                                        const int32_t* __restrict__ sp32,
                                                        const int32_t* __restrict__ sfan, int64_t sfan_ld, int mean,
                                                        int32_t* fslot, int64_t* alist, uint64_t* st, uint32_t* ctr,
-                                                       int32_t* status) {
+                                                       ConcatJob cj, int32_t* status) {
   constexpr uint64_t F21 = (1ull << 21) - 1ull;   // a tile's counts fit 21 bits (LU_TILE < 2^21)
   const int64_t M = ctl->merged;
   const int64_t ntiles = cdiv(M, LU_TILE);
@@ -214,6 +225,11 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   __shared__ uint64_t s_w[LU_NT / ALTO_WAVE];
   __shared__ int64_t s_ex[3];
   __shared__ uint32_t s_tile;
+  const int64_t idle = (int64_t)gridDim.x - ntiles;   // blocks without a tile
+  if (cj.tok && idle > 0 && (int64_t)blockIdx.x >= ntiles)
+    concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nchunks, cj.src, cj.tok, cj.cap_tokens,
+                                  ((int64_t)blockIdx.x - ntiles) * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE,
+                                  idle * (LU_NT / ALTO_WAVE));
   if (ntiles == 0) {
     // nothing carried and nothing arrived
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -339,10 +355,15 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
       }
       __syncthreads();   // s_ex and the ticket are reused by the next tile
     }
+    if (cj.tok && idle <= 0)
+      concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nchunks, cj.src, cj.tok, cj.cap_tokens,
+                                    (int64_t)blockIdx.x * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE,
+                                    (int64_t)gridDim.x * (LU_NT / ALTO_WAVE));
   }
 }
 
-// MEAN, after the live-set update: the arena slots of the kept step elements
+// MEAN, after the live-set update (and the mean gather): the means of the emitted
+// groups of several chunks (mean_combine_chunks); the arena slots of the kept step elements
 // (the slots freed this step first, in scan order, then the top of the free-slot
 // stack), their rows copied in (one wave per row), the freed slots not reused
 // pushed onto the stack. The stack top is read from top[par] and written to
@@ -351,7 +372,11 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
 __global__ __launch_bounds__(256) void k_arena_slots(StreamCtl* ctl, int64_t cap, const int64_t* __restrict__ alist,
                                                      const int32_t* __restrict__ fslot, int32_t* stack, LiveSet nw,
                                                      const float* __restrict__ spf, int dim, int v4, float* arena,
-                                                     int par, int32_t* status) {
+                                                     int par, const Chunk* __restrict__ chunks, const int64_t* nchunks,
+                                                     const double* __restrict__ part, float* mean, int64_t cap_groups,
+                                                     int32_t* status) {
+  // the emitted groups of several chunks first (their chunks' partial sums)
+  if (mean) mean_combine_chunks(chunks, *nchunks, part, dim, mean, cap_groups, blockIdx.x, gridDim.x);
   const int64_t A = ctl->atot, F = ctl->ftot, top = ctl->top[par];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     // the stack after the step; too few free slots, or more than the capacity
@@ -779,6 +804,8 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   ex.htcap = s->htcap;
   ex.max_emit = s->max_groups;
   ex.emit_count = &s->ctl->emitted;
+  ex.defer_concat = mean ? 0 : 1;   // the live-set update copies the tokens
+  ex.defer_combine = mean ? 1 : 0;  // the arena-slot kernel combines the chunks
   rc = groups_run<MergedSrc>(g, s->rg, agg, src, mkey, ntot, b, nullptr, o, status, st, &ex);
   if (rc) return rc;
   // 5. survivors become the new live set
@@ -786,10 +813,19 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   int64_t* alist = b.tokc;
   {
     const int nf = d - 1;
+    ConcatJob cj;
+    memset(&cj, 0, sizeof(cj));
+    if (!mean && o.tok) {
+      cj.chunks = b.chunks;
+      cj.nchunks = b.scal + 1;
+      cj.src = src;
+      cj.tok = o.tok;
+      cj.cap_tokens = o.cap_tokens;
+    }
 #define ALTO_LU_CASE(P)                                                                                          \
   k_live_update<P><<<grid_for(ntot, LU_TILE, 1024), LU_NT, 0, st>>>(g, b.lv[La], b.gw, mkey, msrc, s->ctl, s->cap, \
                                                                    old, nw, payload_i32, fan, fan_ld, mean ? 1 : 0, \
-                                                                   fslot, alist, lst, b.os_ctr + 2, status)
+                                                                   fslot, alist, lst, b.os_ctr + 2, cj, status)
     if (nf <= 1) ALTO_LU_CASE(1);
     else if (nf == 2) ALTO_LU_CASE(2);
     else ALTO_LU_CASE(3);
@@ -799,6 +835,7 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
     const bool v4 = agg.dim % 4 == 0 && ((reinterpret_cast<uintptr_t>(payload_f32) | reinterpret_cast<uintptr_t>(s->arena)) & 15) == 0;
     k_arena_slots<<<grid_for(n * ALTO_WAVE, 256), 256, 0, st>>>(s->ctl, s->cap, alist, fslot, s->stack, nw,
                                                                  payload_f32, agg.dim, v4 ? 1 : 0, s->arena, s->cur,
+                                                                 b.chunks, b.scal + 1, b.part, o.mean, o.cap_groups,
                                                                  status);
   }
   ALTO_LAUNCH_CHECK();
