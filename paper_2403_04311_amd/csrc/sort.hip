@@ -1036,13 +1036,13 @@ constexpr int SM_NT = 1024;
 constexpr int SM_NW = SM_NT / ALTO_WAVE;
 static_assert(SM_NT == 4 * SORT_BUCKETS && SM_NW == 16, "the count scan gives each thread 4 waves of one digit");
 
-// The routing call's preparation (SmallPrep), by the whole workgroup.
-__device__ void small_prep(const SortBufs& b, const RouteGeom& rg, int64_t n, int64_t n_host, const int64_t* n_dev) {
-  const SmallPrep& pp = b.prep;
-  __shared__ unsigned long long s_fp[ALTO_MAX_LEVELS + 1];
-  __shared__ uint32_t s_flags;
+// The routing call's preparation (SmallPrep), by the whole workgroup, in two parts
+// around the sort's own read of the keys (which also writes the destinations and
+// checks the layout): the control block and the fingerprint sums are reset first.
+__device__ inline void small_prep_begin(const SmallPrep& pp, int64_t n_host, const int64_t* n_dev,
+                                        unsigned long long* s_fp, uint32_t* s_flags) {
   if (threadIdx.x == 0) {
-    s_flags = 0u;
+    *s_flags = 0u;
     if (n_dev && (*n_dev < 0 || *n_dev > n_host)) raise_status(pp.status, ALTO_E_CAPACITY);
     SortCtl* c = pp.ctl;
     c->key_or = 0;
@@ -1063,21 +1063,22 @@ __device__ void small_prep(const SortBufs& b, const RouteGeom& rg, int64_t n, in
     pp.fp_nodes[i] = 0;
     if (i < flo || i > fhi) pp.fp_in[i] = 0;
   }
-  __syncthreads();
+}
+
+// Second part, with the keys in LDS (s_key[e] & kmask is element e's key): the
+// declared-count checks and the fragment side of the fan fingerprint, one level at
+// a time (a scalar sum per level, a wave sum, one LDS add per wave).
+__device__ inline void small_prep_levels(const SmallPrep& pp, const uint64_t* s_key, uint64_t kmask, int64_t n,
+                                         bool bad_layout, unsigned long long* s_fp, uint32_t* s_flags) {
   const KeyGeom& g = pp.g;
-  bool bad_layout = false, bad_fan = false;
-  for (int64_t e = threadIdx.x; e < n; e += SM_NT) {
-    const uint64_t k = b.in_keys[e];
-    bad_layout |= (k >> g.total) != 0;
-    if (pp.dest) pp.dest[e] = (int32_t)dest_of_key(rg, k);
-  }
-  // one level at a time: a scalar sum per level, a wave sum, one LDS add per wave
+  const int flo = pp.flo, fhi = pp.fan ? pp.fhi : pp.flo - 1;
+  bool bad_fan = false;
   for (int m = flo; m <= fhi; ++m) {
     const int sh = g.shift[m], shc = g.shift[m + 1];
     const uint64_t tm = (uint64_t)g.tagmask[m + 1];
     uint64_t acc = 0;
     for (int64_t e = threadIdx.x; e < n; e += SM_NT) {
-      const uint64_t k = b.in_keys[e];
+      const uint64_t k = s_key[e] & kmask;
       const int32_t f = pp.fan[(int64_t)(m - 1) * pp.fan_ld + e];
       bad_fan |= (f < 1) || ((int64_t)((k >> shc) & tm) >= (int64_t)f);
       acc += fan_term(g.fkey, m, key_prefix(k, sh), (uint32_t)f);
@@ -1085,21 +1086,24 @@ __device__ void small_prep(const SortBufs& b, const RouteGeom& rg, int64_t n, in
     acc = wave_sum(acc);
     if (lane_id() == 0 && acc) atomicAdd(&s_fp[m], (unsigned long long)acc);
   }
-  if (bad_layout) atomicOr(&s_flags, 1u);
-  if (bad_fan) atomicOr(&s_flags, 2u);
+  if (bad_layout) atomicOr(s_flags, 1u);
+  if (bad_fan) atomicOr(s_flags, 2u);
   __syncthreads();
   for (int m = flo + (int)threadIdx.x; m <= fhi; m += SM_NT) pp.fp_in[m] = (uint64_t)s_fp[m];
   if (threadIdx.x == 0) {
-    if (s_flags & 1u) raise_status(pp.status, ALTO_E_LAYOUT);
-    if (s_flags & 2u) raise_status(pp.status, ALTO_E_FANOUT);
+    if (*s_flags & 1u) raise_status(pp.status, ALTO_E_LAYOUT);
+    if (*s_flags & 2u) raise_status(pp.status, ALTO_E_FANOUT);
   }
 }
 
 // IT items per thread (IT * SM_NT elements at most): launched with the smallest IT
 // that holds the host's bound on the count, so small sorts rank fewer items per pass.
+// dshift >= 0: the destination is placed above the key bits (dshift = key bits; the
+// host checked that both fit 64 bits), so the destination takes no pass of its own
+// and is hashed once per element; the key is unpacked when written out.
 template <int IT>
 __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host, const int64_t* n_dev, RouteGeom rg,
-                                                      int max_key_windows, int max_dest_windows) {
+                                                      int max_key_windows, int max_dest_windows, int dshift) {
   __shared__ uint64_t s_key[IT * SM_NT];
   __shared__ uint32_t s_val[IT * SM_NT];
   __shared__ uint16_t s_cnt[SM_NW][SORT_BUCKETS];
@@ -1108,27 +1112,38 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
   __shared__ uint32_t s_dor[SM_NW], s_dand[SM_NW];
   __shared__ int s_np;
   __shared__ int s_lo[SORT_MAX_PASSES], s_fd[SORT_MAX_PASSES];
+  __shared__ unsigned long long s_fp[ALTO_MAX_LEVELS + 1];
+  __shared__ uint32_t s_flags;
   int64_t n = load_n(n_host, n_dev);
   // the call's only sort (its bound fits here): a device count outside [0, bound]
   // is clamped (and reported by the preparation); otherwise larger counts are the
   // multi-block path's
   if (n_host <= IT * SM_NT) n = n < 0 ? 0 : (n > n_host ? n_host : n);
-  if (b.prep.ctl) small_prep(b, rg, n, n_host, n_dev);
-  if (n > IT * SM_NT) return;
+  const bool prep = b.prep.ctl != nullptr;
+  if (prep) small_prep_begin(b.prep, n_host, n_dev, s_fp, &s_flags);
+  if (n > IT * SM_NT) return;   // block-uniform
+  const bool packed = dshift >= 0;
+  const uint64_t kmask = packed ? ((1ull << dshift) - 1ull) : ~0ull;
   const int w = threadIdx.x / ALTO_WAVE, lane = lane_id();
   uint64_t kor = 0, kand = ~0ull;
   uint32_t dor = 0, dand = ~0u;
+  bool bad_layout = false;
   for (int j = 0; j < IT; ++j) {
     const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
     if (e < n) {
       const uint64_t k = b.in_keys[e];
-      s_key[e] = k;
-      s_val[e] = (uint32_t)e;
-      kor |= k;
-      kand &= k;
       const uint32_t d = dest_of_key(rg, k);
+      const uint64_t word = packed ? (k | ((uint64_t)d << dshift)) : k;
+      s_key[e] = word;
+      s_val[e] = (uint32_t)e;
+      kor |= word;
+      kand &= word;
       dor |= d;
       dand &= d;
+      if (prep) {
+        bad_layout |= (k >> b.prep.g.total) != 0;
+        if (b.prep.dest) b.prep.dest[e] = (int32_t)d;
+      }
     }
   }
 #pragma unroll
@@ -1145,6 +1160,7 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     s_dand[w] = dand;
   }
   __syncthreads();
+  if (prep) small_prep_levels(b.prep, s_key, kmask, n, bad_layout, s_fp, &s_flags);
   if (threadIdx.x == 0) {
     uint64_t a = 0, c = ~0ull;
     uint32_t da = 0, dc = ~0u;
@@ -1163,7 +1179,7 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
       ++np;
       vk = (lo + SORT_RADIX >= 64) ? 0ull : (vk & ~((1ull << (lo + SORT_RADIX)) - 1ull));
     }
-    uint32_t vd = da ^ dc;
+    uint32_t vd = packed ? 0u : (da ^ dc);
     const int nk = np;
     while (vd && np < nk + max_dest_windows) {
       const int lo = __builtin_ctz(vd);
@@ -1231,7 +1247,7 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     __syncthreads();
   }
   for (int e = threadIdx.x; e < n; e += SM_NT) {
-    b.out_keys[e] = s_key[e];
+    b.out_keys[e] = s_key[e] & kmask;
     b.out_vals[e] = s_val[e];
   }
 }
@@ -1277,11 +1293,17 @@ int bits_for(int64_t v) {
 // The one-workgroup sort with the fewest items per thread that holds n_max elements.
 static void launch_sort_small(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg,
                               int key_bits, hipStream_t st) {
-  const int kw = sort_max_key_windows(key_bits), dw = sort_max_dest_windows(rg);
-  if (n_max <= SM_NT) k_sort_small<1><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
-  else if (n_max <= 2 * SM_NT) k_sort_small<2><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
-  else if (n_max <= 4 * SM_NT) k_sort_small<4><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
-  else k_sort_small<SORT_SMALL_MAX / SM_NT><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw);
+  // the destination above the key bits when both fit one word
+  int dbits = 0;
+  if (rg.shift < 64 && rg.num_dest > 1)
+    while (dbits < 32 && ((uint64_t)1 << dbits) < rg.num_dest) ++dbits;
+  const bool pack = dbits > 0 && key_bits + dbits <= 64;
+  const int dshift = pack ? key_bits : -1;
+  const int kw = sort_max_key_windows(pack ? key_bits + dbits : key_bits), dw = pack ? 0 : sort_max_dest_windows(rg);
+  if (n_max <= SM_NT) k_sort_small<1><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw, dshift);
+  else if (n_max <= 2 * SM_NT) k_sort_small<2><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw, dshift);
+  else if (n_max <= 4 * SM_NT) k_sort_small<4><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw, dshift);
+  else k_sort_small<SORT_SMALL_MAX / SM_NT><<<1, SM_NT, 0, st>>>(b, n_max, n_dev, rg, kw, dw, dshift);
 }
 
 int sort_pairs(const SortBufs& b, int64_t n_max, const int64_t* n_dev, const RouteGeom& rg, int key_bits,
