@@ -1199,20 +1199,29 @@ __global__ __launch_bounds__(SM_NT) void k_sort_small(SortBufs b, int64_t n_host
     for (int i = threadIdx.x; i < SM_NW * SORT_BUCKETS; i += SM_NT) (&s_cnt[0][0])[i] = 0;
     uint64_t key[IT];
     uint32_t val[IT], dig[IT], off[IT];
+    // rows of 64 elements past the count are skipped by the whole wave (a count far
+    // below the host's bound leaves most waves without work, and the sort is bound
+    // by the one CU's vector instructions)
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
       const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       const bool valid = e < n;
-      key[j] = valid ? s_key[e] : 0ull;
-      val[j] = valid ? s_val[e] : 0u;
-      dig[j] = valid ? digit_of(ps, rg, key[j]) : 0u;
+      key[j] = 0ull;
+      val[j] = 0u;
+      dig[j] = 0u;
+      off[j] = 0u;
+      if (w * (IT * ALTO_WAVE) + j * ALTO_WAVE < n) {   // wave-uniform
+        key[j] = valid ? s_key[e] : 0ull;
+        val[j] = valid ? s_val[e] : 0u;
+        dig[j] = valid ? digit_of(ps, rg, key[j]) : 0u;
+      }
     }
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < IT; ++j) {
       const int e = w * (IT * ALTO_WAVE) + j * ALTO_WAVE + lane;
       const bool valid = e < n;
-      off[j] = wave_rank(s_cnt[w], dig[j], valid);
+      if (w * (IT * ALTO_WAVE) + j * ALTO_WAVE < n) off[j] = wave_rank(s_cnt[w], dig[j], valid);
     }
     __syncthreads();
     {
