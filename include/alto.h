@@ -249,6 +249,27 @@ int alto_stream_step_dev(alto_stream *s, const uint64_t *keys, const int32_t *fa
                          alto_groups *emitted, int32_t *status, void *ws, size_t ws_bytes,
                          hipStream_t stream);
 
+/* alto_stream_step_dev with the step's routing (its sort, the checks of its keys and
+ * counts, the fragment side of the fan fingerprint) on route_stream and the rest
+ * (merge, completion, emission, carried state) on `stream` after it, so that the
+ * routing of the next step runs beside this step's merge and emission (Section 3.1:
+ * partial outputs are streamed; the routing of a step does not depend on the
+ * carried state). Steps use ws0 and ws1 alternately (each sized as for
+ * alto_stream_step_dev, ws0 != ws1); route_stream first waits until the step two
+ * calls back, which used the same workspace, has ended on `stream` (events held by
+ * the handle, created at the first call). The inputs (keys, fan, payloads, n_dev)
+ * are read on route_stream and on `stream`: they must be ready on both (a producer
+ * on another stream: make route_stream wait for it too). perm, dest, dest_offsets
+ * and `emitted` are written on `stream`; the routing of the next call may already
+ * run when this call returns, so consecutive calls must not share input buffers
+ * that the caller rewrites in between. Errors as for alto_stream_step_dev; ALTO_E_ARG
+ * when ws0 or ws1 is null or they are equal. */
+int alto_stream_step_overlap(alto_stream *s, const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                             const int32_t *payload_i32, const float *payload_f32, int64_t n_max,
+                             const int64_t *n_dev, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
+                             alto_groups *emitted, int32_t *status, void *ws0, void *ws1, size_t ws_bytes,
+                             hipStream_t route_stream, hipStream_t stream);
+
 /* Lists the groups that have arrived leaves but were never released (incomplete,
  * or complete and waiting for an earlier sibling), by (dest, key):
  * pend_key, pend_count and counts[3] of `out`; other members are ignored. */

@@ -28,7 +28,8 @@ EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggrega
            "alto_stream_pending", "alto_stream_destroy", "alto_join_workspace_bytes", "alto_join",
            "alto_split_workspace_bytes", "alto_split", "alto_router_state_bytes", "alto_router_create",
            "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load", "alto_profile_phases",
-           "alto_read_probe", "alto_aggregate_noalloc", "alto_aggregate_dev", "alto_stream_step_dev")
+           "alto_read_probe", "alto_aggregate_noalloc", "alto_aggregate_dev", "alto_stream_step_dev",
+           "alto_stream_step_overlap")
 NOALLOC_SCRATCH_BYTES = 128 << 20   # ALTO_NOALLOC_SCRATCH_BYTES of include/alto.h
 
 
@@ -83,6 +84,9 @@ def load():
     lib.alto_stream_step_dev.restype = C.c_int
     lib.alto_stream_step_dev.argtypes = [vp, vp, vp, i64, vp, vp, i64, vp, vp, vp, vp, C.POINTER(Groups), vp,
                                          vp, C.c_size_t, vp]
+    lib.alto_stream_step_overlap.restype = C.c_int
+    lib.alto_stream_step_overlap.argtypes = [vp, vp, vp, i64, vp, vp, i64, vp, vp, vp, vp, C.POINTER(Groups), vp,
+                                             vp, vp, C.c_size_t, vp, vp]
     lib.alto_aggregate_noalloc.restype = C.c_int
     lib.alto_aggregate_noalloc.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
                                            vp, vp, vp, C.POINTER(Groups), vp, vp]
@@ -482,10 +486,14 @@ class Stream:
         _check(rc, "alto_stream_create")
 
     def step(self, keys, fan, payload_i32=None, payload_f32=None, out: Optional[GroupTensors] = None,
-             perm=None, dest_offsets=None, dest=None, status=None, stream=None, n=None, n_dev=None):
+             perm=None, dest_offsets=None, dest=None, status=None, stream=None, n=None, n_dev=None,
+             route_stream=None):
         """One step. n_dev (int64 device tensor, optional): the step's count is read
         there on the device, n (or keys.shape[0]) being its bound
-        (alto_stream_step_dev): e.g. the previous stage's out.counts[0:1]."""
+        (alto_stream_step_dev): e.g. the previous stage's out.counts[0:1].
+        route_stream (optional): the step's routing runs there and the rest on
+        `stream` (alto_stream_step_overlap, with a second workspace of this handle),
+        so that the next step's routing runs beside this step's merge and emission."""
         n = keys.shape[0] if n is None else n
         if n > self.step_max:
             raise AltoError(E_ARG, "step larger than step_max")
@@ -511,6 +519,15 @@ class Stream:
         if a.device() != self.state.device:
             a.fail(f"arguments on {a.dev}, stream state on {self.state.device}")
         G = out.struct()
+        if route_stream is not None:
+            if getattr(self, "ws2", None) is None:
+                self.ws2 = torch.empty_like(self.ws)
+            rc = self.lib.alto_stream_step_overlap(self.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32),
+                                                   _p(payload_f32), n, _p(n_dev), _p(perm), _p(dest_offsets),
+                                                   _p(dest), C.byref(G), _p(status), _p(self.ws), _p(self.ws2),
+                                                   _nbytes(self.ws), _stream(route_stream), _stream(stream))
+            _check(rc, "alto_stream_step_overlap")
+            return out, status
         rc = self.lib.alto_stream_step_dev(self.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32),
                                            _p(payload_f32), n, _p(n_dev), _p(perm), _p(dest_offsets), _p(dest),
                                            C.byref(G), _p(status), _p(self.ws), _nbytes(self.ws),

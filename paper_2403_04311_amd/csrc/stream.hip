@@ -87,14 +87,16 @@ __global__ void k_stream_begin(const StreamCtl* ctl, int32_t* status) {
 // late fragments (their group is in the emitted set), writes the step's destination
 // offsets (from its sorted keys) and does the segmentation pass's preparation for
 // the merged run (seg_prep_device), and clears the look-back words and tickets of
-// the group scan (gst, ctr[0]) and the live-set update (lst, ctr[1]).
+// the group scan (gst, ctr[0]) and the live-set update (lst, ctr[1]). When the
+// routing ran on another HIP stream, it also writes the step's permutation and
+// destinations (perm_out, dest_out; null: the routing wrote them).
 __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCtl* ctl, int64_t cap, LiveSet live,
                                                const uint64_t* __restrict__ sk, const uint32_t* __restrict__ sperm,
                                                int64_t n, int flo, int fhi, uint64_t* mkey, int32_t* msrc,
                                                uint64_t* fp_in, const int64_t* n_dev, int shiftLa,
                                                const uint64_t* __restrict__ ht, int64_t htcap, int64_t* dest_offsets,
                                                SegJob sj, uint64_t* gst, uint64_t* lst, uint32_t* ctr,
-                                               int32_t* status) {
+                                               int32_t* perm_out, int32_t* dest_out, int32_t* status) {
   n = dev_n(n_dev, n);
   int64_t Lc = ctl->live;
   Lc = Lc < 0 ? 0 : (Lc > cap ? cap : Lc);
@@ -151,6 +153,8 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
       }
       mkey[j + lo] = k;
       msrc[j + lo] = (int32_t)sperm[j];
+      if (perm_out) perm_out[j] = (int32_t)sperm[j];
+      if (dest_out) dest_out[sperm[j]] = (int32_t)dest_of_key(rg, k);
       late |= emitted_has(key_prefix(k, shiftLa), ht, htcap);
       if (dest_offsets) {
         // the step's destination offsets, where the destination changes in its sorted keys
@@ -532,6 +536,12 @@ struct alto_stream {
   int32_t* pflag;
   int32_t* ppart;
   int64_t* plen;
+  // overlapped steps (alto_stream_step_overlap): the workspace of the next step, and
+  // per workspace the end of its routing and of its step
+  int wslot;
+  bool ev_made;
+  bool ev_used[2];
+  hipEvent_t ev_routed[2], ev_done[2];
 };
 
 namespace {
@@ -641,6 +651,9 @@ int alto_stream_create(const alto_layout* layout, int32_t route_level, int32_t n
   s->cap = max_live_leaves;
   s->max_groups = max_groups;
   s->cur = 0;
+  s->wslot = 0;
+  s->ev_made = false;
+  s->ev_used[0] = s->ev_used[1] = false;
   WsCarver c{(char*)state, state_bytes, 0, true};
   carve_state(s->g, *agg, max_live_leaves, max_groups, c, s);
   if (!c.ok) {
@@ -658,10 +671,16 @@ int alto_stream_create(const alto_layout* layout, int32_t route_level, int32_t n
   return ALTO_OK;
 }
 
-int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
-                         const int32_t* payload_i32, const float* payload_f32, int64_t n, const int64_t* n_dev,
-                         int32_t* perm, int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status,
-                         void* ws, size_t ws_bytes, hipStream_t st) {
+}  // extern "C"
+
+namespace {
+
+// One step; with route_st != st (and ev), the routing runs on route_st and the rest
+// on st after it, and the merge writes the caller's perm and dest.
+int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
+                const float* payload_f32, int64_t n, const int64_t* n_dev, int32_t* perm, int64_t* dest_offsets,
+                int32_t* dest, alto_groups* emitted, int32_t* status, void* ws, size_t ws_bytes,
+                hipStream_t route_st, hipStream_t st, hipEvent_t ev_routed) {
   // n: the step's count (n_dev null) or its bound (the count is *n_dev on the device)
   if (!s || !status || !emitted || !emitted->counts || n < 0 || n > (int64_t)INT32_MAX / 2 ||
       emitted->cap_groups < 0 || emitted->cap_tokens < 0)
@@ -689,9 +708,14 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   if (!c.ok) return ALTO_E_ARG;
   // 1. route the step on its own
   // (destination offsets: written by the merge, from the step's sorted keys)
-  int rc = route_run(g, s->rg, keys, n, b, perm, dest_offsets, dest, fan, fan_ld, La, d - 1, status, st, true, false,
-                     false, n_dev);
+  const bool split = ev_routed != nullptr;
+  int rc = route_run(g, s->rg, keys, n, b, split ? nullptr : perm, dest_offsets, split ? nullptr : dest, fan, fan_ld,
+                     La, d - 1, status, split ? route_st : st, true, false, false, n_dev);
   if (rc) return rc;
+  if (split) {
+    if (hipEventRecord(ev_routed, route_st) != hipSuccess || hipStreamWaitEvent(st, ev_routed, 0) != hipSuccess)
+      return ALTO_E_HIP;
+  }
   prof_begin(PH_SEGMENT, st);
   const uint32_t* sperm = b.perm_used;
   LiveSet& old = s->live[s->cur];
@@ -735,7 +759,8 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   // destination offsets, the clearing of the step's look-back words)
   k_merge<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc,
                                                b.fp_in, n_dev, g.shift[La], s->ht, s->htcap, dest_offsets, j, gst,
-                                               lst, b.os_ctr + 1, status);
+                                               lst, b.os_ctr + 1, split ? perm : nullptr, split ? dest : nullptr,
+                                               status);
   // 3. nodes and completion over the merged run
   rc = seg_run(g, j, st);
   if (rc) return rc;
@@ -843,6 +868,44 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
   return ALTO_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
+                         const int32_t* payload_i32, const float* payload_f32, int64_t n, const int64_t* n_dev,
+                         int32_t* perm, int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status,
+                         void* ws, size_t ws_bytes, hipStream_t st) {
+  return stream_step(s, keys, fan, fan_ld, payload_i32, payload_f32, n, n_dev, perm, dest_offsets, dest, emitted,
+                     status, ws, ws_bytes, st, st, nullptr);
+}
+
+int alto_stream_step_overlap(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
+                             const int32_t* payload_i32, const float* payload_f32, int64_t n, const int64_t* n_dev,
+                             int32_t* perm, int64_t* dest_offsets, int32_t* dest, alto_groups* emitted,
+                             int32_t* status, void* ws0, void* ws1, size_t ws_bytes, hipStream_t route_stream,
+                             hipStream_t st) {
+  if (!s || !ws0 || !ws1 || ws0 == ws1) return ALTO_E_ARG;
+  if (!s->ev_made) {
+    for (int k = 0; k < 2; ++k) {
+      if (hipEventCreateWithFlags(&s->ev_routed[k], hipEventDisableTiming) != hipSuccess ||
+          hipEventCreateWithFlags(&s->ev_done[k], hipEventDisableTiming) != hipSuccess)
+        return ALTO_E_HIP;
+    }
+    s->ev_made = true;
+  }
+  const int k = s->wslot;
+  // the step two calls back used this workspace: its end on st comes first
+  if (s->ev_used[k] && hipStreamWaitEvent(route_stream, s->ev_done[k], 0) != hipSuccess) return ALTO_E_HIP;
+  const int rc = stream_step(s, keys, fan, fan_ld, payload_i32, payload_f32, n, n_dev, perm, dest_offsets, dest,
+                             emitted, status, k ? ws1 : ws0, ws_bytes, route_stream, st, s->ev_routed[k]);
+  if (rc) return rc;
+  if (hipEventRecord(s->ev_done[k], st) != hipSuccess) return ALTO_E_HIP;
+  s->ev_used[k] = true;
+  s->wslot = k ^ 1;
+  return ALTO_OK;
+}
+
 int alto_stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
                      const int32_t* payload_i32, const float* payload_f32, int64_t n, int32_t* perm,
                      int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status, void* ws,
@@ -865,6 +928,12 @@ int alto_stream_pending(alto_stream* s, alto_groups* out, int32_t* status, hipSt
 }
 
 int alto_stream_destroy(alto_stream* s) {
+  if (s && s->ev_made) {
+    for (int k = 0; k < 2; ++k) {
+      (void)hipEventDestroy(s->ev_routed[k]);
+      (void)hipEventDestroy(s->ev_done[k]);
+    }
+  }
   if (!s) return ALTO_E_ARG;
   delete s;
   return ALTO_OK;

@@ -385,3 +385,145 @@ def test_factool_stream_in_order_two_stages():
                    step_max=max(int(np.diff(cB).max()), 1), release="in_order")
     oB = oracle_steps(bB, 2, 32, 2, "concat", 1, kB, fB, pB, None, cB, release="in_order")
     compare_steps(gB, oB, "concat", 2)
+
+
+def _masked_sum(x, count):
+    """Integer sum of the first `count` rows of x (count a device scalar), as int64:
+    the same bits give the same sum in any order."""
+    n = x.shape[0]
+    keep = torch.arange(n, device=x.device) < count
+    v = x.reshape(n, -1)
+    if v.dtype == torch.float32:
+        v = v.view(torch.int32)
+    v = v.to(torch.int64)
+    return torch.where(keep[:, None], v, torch.zeros_like(v)).sum()
+
+
+def test_two_stage_stream_pipelined_on_two_hip_streams_matches_sequential():
+    """The FacTool-shaped stream's two stages with stage B of step s on a second HIP
+    stream beside stage A of step s + 1 (stage A's records double-buffered, events
+    between the stages): every step's outputs are the same bits as when the stages
+    run one after the other on one stream (checksums of the emitted document keys and
+    means, and of the claim stage's keys, token offsets and tokens, per step)."""
+    from paper_2403_04311_amd import workloads as W
+    w = W.config4("cuda", steps=300)
+    step, steps = w.step, 300
+    ring, ring_rows = w.payload_f32, w.payload_f32.shape[0]
+    keys, st = alto.pack_keys(w.path, w.bits)
+    sbB = W.CONFIG2_STAGE_B
+
+    def streams():
+        sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22,
+                         step_max=step)
+        sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
+                         step_max=step)
+        return sA, sB
+
+    def sums_a(g):
+        c = g.counts[0]
+        return torch.stack([c, _masked_sum(g.key, c), _masked_sum(g.mean, c)])
+
+    def sums_b(g):
+        c, t = g.counts[0], g.counts[1]
+        return torch.stack([c, t, _masked_sum(g.key, c), _masked_sum(g.tok_off, c), _masked_sum(g.tok, t)])
+
+    gAs = [alto.new_groups(step, 4, "mean", 768), alto.new_groups(step, 4, "mean", 768)]
+    gB = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
+    stA, stB = alto.new_status(), alto.new_status()
+    # one stream
+    sA, sB = streams()
+    seq_a, seq_b = [], []
+    for s in range(steps):
+        a, b = s * step, (s + 1) * step
+        r0 = (s * step) % ring_rows
+        g = gAs[0]
+        sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=g, status=stA)
+        seq_a.append(sums_a(g))
+        sB.step(g.key, g.fan_up.view(3, -1), g.first_i32, None, out=gB, status=stB, n=step,
+                n_dev=g.counts[0:1])
+        seq_b.append(sums_b(gB))
+    torch.cuda.synchronize()
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    sA.close()
+    sB.close()
+    # two streams
+    sA, sB = streams()
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(main)
+    a_done = [torch.cuda.Event() for _ in range(2)]
+    b_done = [torch.cuda.Event() for _ in range(2)]
+    par_a, par_b = [], []
+    for s in range(steps):
+        k = s & 1
+        a, b = s * step, (s + 1) * step
+        r0 = (s * step) % ring_rows
+        if s >= 2:
+            main.wait_event(b_done[k])
+        g = gAs[k]
+        sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=g, status=stA, stream=main)
+        par_a.append(sums_a(g))
+        a_done[k].record(main)
+        side.wait_event(a_done[k])
+        with torch.cuda.stream(side):
+            sB.step(g.key, g.fan_up.view(3, -1), g.first_i32, None, out=gB, status=stB, n=step,
+                    n_dev=g.counts[0:1], stream=side)
+            par_b.append(sums_b(gB))
+        b_done[k].record(side)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    sA.close()
+    sB.close()
+    emitted = int(torch.stack(seq_a)[:, 0].sum())
+    assert emitted > 1000
+    assert torch.equal(torch.stack(seq_a), torch.stack(par_a))
+    assert torch.equal(torch.stack(seq_b), torch.stack(par_b))
+
+
+def test_overlapped_steps_match_sequential_token_stream():
+    """alto_stream_step_overlap (each step's routing on a second HIP stream, beside
+    the previous step's merge and emission, two workspaces) gives every step the same
+    outputs as alto_stream_step_dev on one stream: the step's perm, dest and
+    dest_offsets, the emitted groups (keys, token offsets, tokens) and their counts."""
+    from paper_2403_04311_amd import workloads as W
+    w = W.config3("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n, step = w.n, w.step
+    nsteps = (n + step - 1) // step
+
+    def run(overlap):
+        s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step)
+        out = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
+        status = alto.new_status()
+        main = torch.cuda.current_stream()
+        route = torch.cuda.Stream()
+        route.wait_stream(main)
+        res = []
+        for i in range(nsteps):
+            a, b = i * step, min(n, (i + 1) * step)
+            m = b - a
+            perm = torch.full((m,), -7, dtype=torch.int32, device="cuda")
+            dest = torch.full((m,), -7, dtype=torch.int32, device="cuda")
+            offs = torch.full((65,), -7, dtype=torch.int64, device="cuda")
+            s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status, perm=perm,
+                   dest=dest, dest_offsets=offs, stream=main, route_stream=route if overlap else None)
+            c = out.counts.clone()
+            res.append((perm, dest, offs, c, out.key.clone(), out.tok_off.clone(), out.tok.clone()))
+        main.wait_stream(route)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        s.close()
+        return res
+    seq = run(False)
+    ovl = run(True)
+    total = 0
+    for i in range(nsteps):
+        (p0, d0, o0, c0, k0, t0, x0), (p1, d1, o1, c1, k1, t1, x1) = seq[i], ovl[i]
+        assert torch.equal(p0, p1) and torch.equal(d0, d1) and torch.equal(o0, o1), i
+        assert torch.equal(c0, c1), i
+        E, T = int(c0[0]), int(c0[1])
+        assert torch.equal(k0[:E], k1[:E]) and torch.equal(t0[:E + 1], t1[:E + 1]) and torch.equal(x0[:T], x1[:T]), i
+        assert (p0 >= 0).all() and (d0 >= 0).all()
+        total += E
+    assert total > 10000
