@@ -431,37 +431,44 @@ def bench_factool_stream(args):
                          step_max=step, release=args.release)
         emitted.zero_()
         main = torch.cuda.current_stream()
-        side = side_stream
+        side, rA, rB = side_stream, route_a, route_b
         a_done = [torch.cuda.Event() for _ in range(2)]
         b_done = [torch.cuda.Event() for _ in range(2)]
         t0 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
         t1 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
-        side.wait_stream(main)
+        for x in (side, rA, rB):
+            x.wait_stream(main)
         for s in range(nsteps):
             k = s & 1
             a, b = s * step, (s + 1) * step
             r0 = (s * step) % ring_rows
-            t0[s].record(main)
+            t0[s].record(rA)
             if s >= 2:
                 main.wait_event(b_done[k])
+            # stage A: routing on rA (beside the previous step), the rest on main
             sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gAs[k], status=stA,
-                    stream=main)
+                    stream=main, route_stream=rA if route_sa else None)
             a_done[k].record(main)
+            # stage B over stage A's records: routing on rB, the rest on side
+            rB.wait_event(a_done[k])
             side.wait_event(a_done[k])
             with torch.cuda.stream(side):
                 sB.step(gAs[k].key, fanAs[k], gAs[k].first_i32, None, out=gB, status=stB, n=step,
-                        n_dev=gAs[k].counts[0:1], stream=side)
+                        n_dev=gAs[k].counts[0:1], stream=side, route_stream=rB if route_sb else None)
                 emitted.add_(gAs[k].counts[0:1])
             b_done[k].record(side)
             t1[s].record(side)
-        main.wait_stream(side)
+        for x in (side, rA, rB):
+            main.wait_stream(x)
         torch.cuda.synchronize()
         sA.close()
         sB.close()
         lat = [t0[s].elapsed_time(t1[s]) for s in range(nsteps)]
         period = [t1[s - 1].elapsed_time(t1[s]) for s in range(1, nsteps)]
         return t0[0].elapsed_time(t1[nsteps - 1]), lat, period
-    side_stream = torch.cuda.Stream()
+    side_stream, route_a, route_b = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    route_sa = args.stream_overlap in ("a", "ab")
+    route_sb = args.stream_overlap in ("b", "ab")
     gAs = [gA, alto.new_groups(step, 4, "mean", 768)]
     fanAs = [g.fan_up.view(3, -1) for g in gAs]
     run(max(args.warmup, 1) * 50)
@@ -481,7 +488,8 @@ def bench_factool_stream(args):
     return _line(f"FacTool-shaped windowed stream: {steps} steps x {step} fragments, 768-d mean per document "
                  f"then document-id concat per claim (both stages each step, the claim stage reading the "
                  f"document stage's emitted count on the device; the claim stage of a step on a second HIP "
-                 f"stream beside the document stage of the next), release {args.release}",
+                 f"stream beside the document stage of the next, each stage's routing on a stream of its own), "
+                 f"release {args.release}",
                  step, ms, steps, 50, path_bytes,
                  {"stream_fragments": n, "documents_emitted": E, "window_fragments": w.info["window"],
                   "long_lived_fraction": w.info["calibrated_frac"],
@@ -753,6 +761,9 @@ def main():
                     help="write the mean kernel's HBM traffic summary from two rocprofv3 --pmc "
                          "counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--pmc-command", default="", help="the rocprofv3 commands, recorded in the summary")
+    ap.add_argument("--stream-overlap", default="none", choices=["none", "a", "b", "ab"],
+                    help="factool_stream: which stages (document a, claim b) route each step on a HIP stream of "
+                         "their own (the stages always run on two streams)")
     ap.add_argument("--release", default="complete", choices=["complete", "in_order"],
                     help="streams: a group leaves when complete, or in child order within its parent")
     ap.add_argument("--workload", default="zipf64M", choices=["zipf64M", "all"] + sorted(WORKLOADS),

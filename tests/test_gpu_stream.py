@@ -402,8 +402,9 @@ def _masked_sum(x, count):
 def test_two_stage_stream_pipelined_on_two_hip_streams_matches_sequential():
     """The FacTool-shaped stream's two stages with stage B of step s on a second HIP
     stream beside stage A of step s + 1 (stage A's records double-buffered, events
-    between the stages): every step's outputs are the same bits as when the stages
-    run one after the other on one stream (checksums of the emitted document keys and
+    between the stages), and each stage's routing on a stream of its own
+    (alto_stream_step_overlap): every step's outputs are the same bits as when the
+    stages run one after the other on one stream (checksums of the emitted document keys and
     means, and of the claim stage's keys, token offsets and tokens, per step)."""
     from paper_2403_04311_amd import workloads as W
     w = W.config4("cuda", steps=300)
@@ -446,11 +447,13 @@ def test_two_stage_stream_pipelined_on_two_hip_streams_matches_sequential():
     assert int(stA.item()) == 0 and int(stB.item()) == 0
     sA.close()
     sB.close()
-    # two streams
+    # four streams: stage A's routing (rA) and the rest (main), stage B's routing (rB)
+    # and the rest (side)
     sA, sB = streams()
     main = torch.cuda.current_stream()
-    side = torch.cuda.Stream()
-    side.wait_stream(main)
+    side, rA, rB = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    for x in (side, rA, rB):
+        x.wait_stream(main)
     a_done = [torch.cuda.Event() for _ in range(2)]
     b_done = [torch.cuda.Event() for _ in range(2)]
     par_a, par_b = [], []
@@ -461,16 +464,19 @@ def test_two_stage_stream_pipelined_on_two_hip_streams_matches_sequential():
         if s >= 2:
             main.wait_event(b_done[k])
         g = gAs[k]
-        sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=g, status=stA, stream=main)
+        sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=g, status=stA, stream=main,
+                route_stream=rA)
         par_a.append(sums_a(g))
         a_done[k].record(main)
+        rB.wait_event(a_done[k])
         side.wait_event(a_done[k])
         with torch.cuda.stream(side):
             sB.step(g.key, g.fan_up.view(3, -1), g.first_i32, None, out=gB, status=stB, n=step,
-                    n_dev=g.counts[0:1], stream=side)
+                    n_dev=g.counts[0:1], stream=side, route_stream=rB)
             par_b.append(sums_b(gB))
         b_done[k].record(side)
-    main.wait_stream(side)
+    for x in (side, rA, rB):
+        main.wait_stream(x)
     torch.cuda.synchronize()
     assert int(stA.item()) == 0 and int(stB.item()) == 0
     sA.close()
