@@ -115,14 +115,29 @@ def cpu_baseline(leaves_log2: int):
     from paper_2403_04311_amd import workloads as W
     w = W.config5("cpu", leaves=1 << leaves_log2)
     path, fan, x = w.path.numpy(), w.fan.numpy(), w.payload_f32.numpy()
-    t0 = time.perf_counter()
-    keys = O.pack_keys(path, w.bits)
-    O.aggregate(keys, fan, w.bits, w.agg_level, w.op, w.dim, w.mask_level, w.route_level, w.num_dest,
-                None, x)
-    dt = time.perf_counter() - t0
+    # one core: the process is pinned to one CPU for the timed run (numpy's own
+    # threads, if any, then share it), and the affinity is restored afterwards
+    pinned = None
+    try:
+        before = os.sched_getaffinity(0)
+        cpu = min(before)
+        os.sched_setaffinity(0, {cpu})
+        pinned = (before, cpu)
+    except (AttributeError, OSError):
+        pass
+    try:
+        t0 = time.perf_counter()
+        keys = O.pack_keys(path, w.bits)
+        O.aggregate(keys, fan, w.bits, w.agg_level, w.op, w.dim, w.mask_level, w.route_level, w.num_dest,
+                    None, x)
+        dt = time.perf_counter() - t0
+    finally:
+        if pinned:
+            os.sched_setaffinity(0, pinned[0])
     return {"value": (1 << leaves_log2) / dt, "unit": "fragments/s", "cores": 1, "kind": "oracle",
             "sample": f"same generator at 2^{leaves_log2} leaves (1/{1 << (26 - leaves_log2)} of the "
-                      f"workload): pack + route + aggregate, {dt:.1f} s single-threaded numpy",
+                      f"workload): pack + route + aggregate, {dt:.1f} s of numpy on one pinned CPU"
+                      + (f" (cpu {pinned[1]})" if pinned else " (affinity not settable: unpinned)"),
             "host": host_info()}
 
 
