@@ -779,6 +779,9 @@ def main():
     ap.add_argument("--stream-overlap", default="none", choices=["none", "a", "b", "ab"],
                     help="factool_stream: which stages (document a, claim b) route each step on a HIP stream of "
                          "their own (the stages always run on two streams)")
+    ap.add_argument("--batch-overlap", action="store_true",
+                    help="zipf64M: run each batch's gathers on a second HIP stream beside the next batch's routing "
+                         "(measured slower: the persistent mean gather fills every CU)")
     ap.add_argument("--release", default="complete", choices=["complete", "in_order"],
                     help="streams: a group leaves when complete, or in child order within its parent")
     ap.add_argument("--workload", default="zipf64M", choices=["zipf64M", "all"] + sorted(WORKLOADS),
@@ -841,9 +844,45 @@ def main():
         alto.aggregate(keys, fan, bits, La, "mean", dim, Lm, Lr, D, None, pf, ws=ws, perm=perm,
                        dest_offsets=offs, dest=dest, out=out, status=status, n=n)
 
+    # batches in flight on two HIP streams: a batch's gathers (bandwidth bound) on the
+    # gather stream beside the next batch's routing, order and completion (mostly
+    # latency bound) on the call's stream; two sets of workspace and outputs, and a
+    # batch waits until the gathers of the batch two before it, which used the same
+    # set, have ended
+    overlap = args.batch_overlap
+    gather = torch.cuda.Stream()
+    if overlap:
+        sets = [(ws, perm, offs, dest, out),
+                (alto.new_workspace(alto.workspace_bytes(bits, n, D, La, "mean", dim, Lm), dev),
+                 torch.empty(n, dtype=torch.int32, device=dev), torch.empty(D + 1, dtype=torch.int64, device=dev),
+                 torch.empty(n, dtype=torch.int32, device=dev),
+                 alto.new_groups(cap, La, "mean", dim, cap_mask=cap, device=dev, with_first=False))]
+        gathered = [torch.cuda.Event(), torch.cuda.Event()]
+        used = [False, False]
+    calls = [0]
+
+    def step_timed():
+        if not overlap:
+            step()
+            return
+        k = calls[0] & 1
+        calls[0] += 1
+        main = torch.cuda.current_stream()
+        if used[k]:
+            main.wait_event(gathered[k])
+        w_, p_, o_, d_, g_ = sets[k]
+        alto.aggregate(keys, fan, bits, La, "mean", dim, Lm, Lr, D, None, pf, ws=w_, perm=p_,
+                       dest_offsets=o_, dest=d_, out=g_, status=status, n=n, stream=main, gather_stream=gather)
+        gathered[k].record(gather)
+        used[k] = True
+
+    def settle():
+        torch.cuda.current_stream().wait_stream(gather)
+        torch.cuda.synchronize()
+
     for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+        step_timed()
+    settle()
     if int(status.item()) != 0:
         raise SystemExit(f"status {int(status.item())} from alto_aggregate")
     E, T, M, P = [int(x) for x in out.counts.cpu()]
@@ -860,10 +899,11 @@ def main():
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     evs[0].record()
+    gather.wait_stream(torch.cuda.current_stream())
     for k in range(args.steps):
-        step()
-        evs[k + 1].record()
-    torch.cuda.synchronize()
+        step_timed()
+        evs[k + 1].record(gather if overlap else torch.cuda.current_stream())   # the step's end
+    settle()
     ms_total = evs[0].elapsed_time(evs[-1])
     per_step = sorted(evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps))
     ms = (C.c_float * len(PHASES))()
@@ -873,6 +913,17 @@ def main():
     kern_ms = ms[PHASES.index("mean_kernel")] / max(calls[PHASES.index("mean_kernel")], 1)
     assert int(status.item()) == 0
     ms_step = ms_total / args.steps
+    seq_ms = None
+    if overlap:
+        # the same steps one after the other on one stream, for comparison
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for k in range(args.steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        seq_ms = e0.elapsed_time(e1) / args.steps
+        assert int(status.item()) == 0
     # one more call, untimed, with every phase recorded (diagnostics)
     assert lib.alto_profile_phases(0xFFFFFFFF) == 0
     assert lib.alto_profile_begin(32) == 0
@@ -905,8 +956,12 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"zipf depth-6 tree, 2^{args.leaves_log2} fragments, 128-d f32 mean at level 4, "
-                               "mask at level 2, 256 destinations by level-4 prefix, one batch",
+                               "mask at level 2, 256 destinations by level-4 prefix, one batch per step"
+                               + (" (a batch's gathers on a second HIP stream beside the next batch's routing)"
+                                  if overlap else ""),
                    "fragments": n, "groups": E, "mask_nodes": M, "dim": dim, "num_dest": D},
+        "batch_overlap": overlap,
+        "sequential_ms_per_step": seq_ms,
         "roofline": {"bound": "hbm", "kernel": "k_mean (fp64-accumulating row gather)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(),

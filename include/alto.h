@@ -180,6 +180,23 @@ int alto_aggregate_dev(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
                        int32_t *dest, alto_groups *out, int32_t *status, void *ws, size_t ws_bytes,
                        hipStream_t stream);
 
+/* alto_aggregate with the payload gathers (the concatenation, or the mean rows and
+ * their combination) on gather_stream and everything before them (routing, order,
+ * completion, group records) on `stream`; gather_stream waits for the records
+ * through an event the call records on `stream`. A caller with several batches
+ * runs the routing of the next batch beside this batch's gathers (the gathers are
+ * bandwidth bound, the routing mostly latency bound): give each batch in flight
+ * its own workspace, perm and `out`, and make `stream` wait for gather_stream (an
+ * event) before a batch reuses them. The inputs are read on both streams. `out`'s
+ * counts and records are written on `stream`, tok or mean on gather_stream. As
+ * alto_aggregate otherwise; gather_stream == stream is alto_aggregate. */
+int alto_aggregate_overlap(const uint64_t *keys, const int32_t *fan, int64_t fan_ld,
+                           const int32_t *payload_i32, const float *payload_f32, int64_t n,
+                           const alto_layout *layout, const alto_agg *agg, int32_t route_level,
+                           int32_t num_dest, int32_t *perm, int64_t *dest_offsets, int32_t *dest,
+                           alto_groups *out, int32_t *status, void *ws, size_t ws_bytes,
+                           hipStream_t stream, hipStream_t gather_stream);
+
 /* ---- alto_aggregate without a workspace argument ----
  * For callers that cannot allocate device memory at the time of the call (code
  * under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).

@@ -29,7 +29,7 @@ EXPORTS = ("alto_workspace_bytes", "alto_pack_keys", "alto_route", "alto_aggrega
            "alto_split_workspace_bytes", "alto_split", "alto_router_state_bytes", "alto_router_create",
            "alto_router_destroy", "alto_route_load_workspace_bytes", "alto_route_load", "alto_profile_phases",
            "alto_read_probe", "alto_aggregate_noalloc", "alto_aggregate_dev", "alto_stream_step_dev",
-           "alto_stream_step_overlap")
+           "alto_stream_step_overlap", "alto_aggregate_overlap")
 NOALLOC_SCRATCH_BYTES = 128 << 20   # ALTO_NOALLOC_SCRATCH_BYTES of include/alto.h
 
 
@@ -81,6 +81,9 @@ def load():
     lib.alto_aggregate_dev.restype = C.c_int
     lib.alto_aggregate_dev.argtypes = [vp, vp, i64, vp, vp, i64, vp, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
                                        vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp]
+    lib.alto_aggregate_overlap.restype = C.c_int
+    lib.alto_aggregate_overlap.argtypes = [vp, vp, i64, vp, vp, i64, C.POINTER(Layout), C.POINTER(Agg), i32, i32,
+                                           vp, vp, vp, C.POINTER(Groups), vp, vp, C.c_size_t, vp, vp]
     lib.alto_stream_step_dev.restype = C.c_int
     lib.alto_stream_step_dev.argtypes = [vp, vp, vp, i64, vp, vp, i64, vp, vp, vp, vp, C.POINTER(Groups), vp,
                                          vp, C.c_size_t, vp]
@@ -376,10 +379,13 @@ def new_groups(cap_groups, agg_level, op, dim=1, cap_tokens=0, cap_mask=0, devic
 
 def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0, num_dest=1,
               payload_i32=None, payload_f32=None, ws=None, perm=None, dest_offsets=None, dest=None,
-              out: Optional[GroupTensors] = None, status=None, stream=None, n=None, n_dev=None):
+              out: Optional[GroupTensors] = None, status=None, stream=None, n=None, n_dev=None,
+              gather_stream=None):
     """Routes and aggregates one batch; returns (perm, dest_offsets, dest, groups, status).
     n_dev (int64 device tensor, optional): the count is read there on the device (n,
-    or keys.shape[0], is then its bound: alto_aggregate_dev)."""
+    or keys.shape[0], is then its bound: alto_aggregate_dev). gather_stream
+    (optional): the payload gathers run there after the records
+    (alto_aggregate_overlap; not with n_dev)."""
     lib = load()
     a = _Args("alto_aggregate")
     n = keys.shape[0] if n is None else n
@@ -413,7 +419,14 @@ def aggregate(keys, fan, bits, agg_level, op, dim=1, mask_level=0, route_level=0
     L = layout(bits)
     A = agg_struct(agg_level, op, dim, mask_level)
     G = out.struct()
-    if n_dev is None:
+    if gather_stream is not None:
+        if n_dev is not None:
+            a.fail("gather_stream with n_dev")
+        rc = lib.alto_aggregate_overlap(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n,
+                                        C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
+                                        _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream),
+                                        _stream(gather_stream))
+    elif n_dev is None:
         rc = lib.alto_aggregate(_p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32), n,
                                 C.byref(L), C.byref(A), route_level, num_dest, _p(perm), _p(dest_offsets),
                                 _p(dest), C.byref(G), _p(status), _p(ws), _nbytes(ws), _stream(stream))

@@ -181,6 +181,9 @@ struct GroupsExtra {
   int64_t* emit_count;
   // the gathers the caller runs itself later (concat_chunks / mean_combine_chunks)
   int32_t defer_concat, defer_combine;
+  // the gathers on another HIP stream (gather_st, after an event recorded on the
+  // call's stream; null: the call's stream)
+  hipStream_t gather_st;
 };
 
 #define EMIT_EMPTY (~0ull)
@@ -283,7 +286,7 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
 int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
                   const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
                   int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
-                  hipStream_t st, const int64_t* n_dev = nullptr);
+                  hipStream_t st, const int64_t* n_dev = nullptr, hipStream_t gather_st = nullptr);
 void empty_outputs(const GroupOut& out, int64_t* dest_offsets, int num_dest, hipStream_t st);
 void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st);
 void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,

@@ -1105,7 +1105,7 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
 int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg& agg, const uint64_t* keys,
                   const int32_t* fan, int64_t fan_ld, const int32_t* p32, const float* pf, int64_t n, AggBufs& b,
                   int32_t* perm_out, int64_t* dest_offsets, int32_t* dest, const GroupOut& out, int32_t* status,
-                  hipStream_t st, const int64_t* n_dev) {
+                  hipStream_t st, const int64_t* n_dev, hipStream_t gather_st) {
   const int d = g.depth, La = agg.level, Lm = agg.mask_level;
   int Lt, Lseg;
   agg_levels(g, La, Lm, Lr, &Lt, &Lseg);
@@ -1217,6 +1217,7 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
   ex.xlo = b.fx_lo;
   ex.xhi = b.fx_hi;
   ex.ctl = b.ctl;
+  ex.gather_st = gather_st;
   BatchSrc src{perm, p32, fan, fan_ld, pf, agg.dim, n, status};
   return groups_run<BatchSrc>(g, rg, agg, src, b.sk, n, b, Mp, out, status, st, &ex);
 }
@@ -1252,6 +1253,16 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
                                                      status);
   ALTO_LAUNCH_CHECK();
   prof_end(PH_GROUPS, st);
+  // the gathers, on another stream if asked (after the records, through an event
+  // that is released once the device has passed it)
+  if (x.gather_st && x.gather_st != st) {
+    hipEvent_t ev;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) return ALTO_E_HIP;
+    const bool ok = hipEventRecord(ev, st) == hipSuccess && hipStreamWaitEvent(x.gather_st, ev, 0) == hipSuccess;
+    (void)hipEventDestroy(ev);
+    if (!ok) return ALTO_E_HIP;
+    st = x.gather_st;
+  }
   ProfScope ps_gather(PH_GATHER, st);
   const int64_t* NCp = b.scal + 1;   // chunk count
   if (agg.op == ALTO_CONCAT_I32) {

@@ -220,6 +220,35 @@ int alto_aggregate_dev(const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
                        dest_offsets, dest, o, status, stream, n_dev);
 }
 
+int alto_aggregate_overlap(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
+                           const float* payload_f32, int64_t n, const alto_layout* layout, const alto_agg* agg,
+                           int32_t route_level, int32_t num_dest, int32_t* perm, int64_t* dest_offsets,
+                           int32_t* dest, alto_groups* out, int32_t* status, void* ws, size_t ws_bytes,
+                           hipStream_t stream, hipStream_t gather_stream) {
+  if (!layout_ok(layout) || n < 0 || n > N_LIMIT || num_dest < 1 || num_dest > (1 << 24) || !status || !out ||
+      !out->counts || !agg_ok(layout, agg, route_level, num_dest) || out->cap_groups < 0 || out->cap_tokens < 0 ||
+      out->cap_mask < 0)
+    return ALTO_E_ARG;
+  if (agg->release != ALTO_RELEASE_COMPLETE) return ALTO_E_ARG;
+  if (agg->op == ALTO_CONCAT_I32 && !payload_i32 && n > 0) return ALTO_E_ARG;
+  if (agg->op == ALTO_MEAN_F32 && !payload_f32 && n > 0) return ALTO_E_ARG;
+  GroupOut o = to_dev_out(out);
+  if (n == 0) {
+    empty_outputs(o, dest_offsets, num_dest, stream);
+    ALTO_LAUNCH_CHECK();
+    return ALTO_OK;
+  }
+  if (!keys || !fan || fan_ld < n || !ws) return ALTO_E_ARG;
+  KeyGeom g = make_geom(layout);
+  RouteGeom rg = make_route(g, route_level, num_dest);
+  WsCarver c{(char*)ws, ws_bytes, 0, true};
+  AggBufs b;
+  plan_buffers(g, n, rg, agg, route_level, c, b);
+  if (!c.ok) return ALTO_E_ARG;
+  return aggregate_run(g, rg, route_level, *agg, keys, fan, fan_ld, payload_i32, payload_f32, n, b, perm,
+                       dest_offsets, dest, o, status, stream, nullptr, gather_stream);
+}
+
 int alto_aggregate(const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
                    const float* payload_f32, int64_t n, const alto_layout* layout, const alto_agg* agg,
                    int32_t route_level, int32_t num_dest, int32_t* perm, int64_t* dest_offsets, int32_t* dest,

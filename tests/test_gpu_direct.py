@@ -95,3 +95,73 @@ def test_direct_placement_not_taken_when_a_marker_is_missing():
     assert code == O.E_DUPLICATE
     res = U.run_aggregate(keys, fan, BITS, 4, "mean", 8, 2, 4, 256, p32, pf)
     assert res["status"] == O.E_DUPLICATE
+
+
+@pytest.mark.parametrize("seed,op,Lm,drop", [(540, "mean", 2, 0.0), (541, "mean", 0, 0.01), (542, "concat", 3, 0.0)])
+def test_gathers_on_a_second_stream_match_one_stream(seed, op, Lm, drop):
+    """alto_aggregate_overlap: the gathers of a batch on a second HIP stream beside the
+    next batch's routing (two sets of workspace and outputs, events between them), over
+    four batches in a row: every output equals alto_aggregate on one stream (direct
+    placement for the complete batches, the general path with dropped leaves)."""
+    import torch
+    from paper_2403_04311_amd import alto
+    path, fan, p32, pf = _tree(seed)
+    if drop:
+        keep = np.random.default_rng(seed + 9).random(path.shape[1]) >= drop
+        path, fan, p32, pf = path[:, keep], fan[:, keep], p32[keep], pf[keep]
+    keys = O.pack_keys(path, BITS)
+    n = len(keys)
+    dim = pf.shape[1] if op == "mean" else 1
+    tk = U.to_dev(keys.view(np.int64))
+    tf = U.to_dev(fan.astype(np.int32))
+    t32 = U.to_dev(p32)
+    tpf = U.to_dev(pf) if op == "mean" else None
+
+    def outs():
+        return (alto.new_workspace(alto.workspace_bytes(BITS, n, 256, 4, op, dim, Lm)),
+                torch.empty(n, dtype=torch.int32, device="cuda"), torch.empty(257, dtype=torch.int64, device="cuda"),
+                torch.empty(n, dtype=torch.int32, device="cuda"),
+                alto.new_groups(n, 4, op, dim, cap_tokens=n if op == "concat" else 0, cap_mask=n if Lm else 0))
+
+    def snapshot(o):
+        ws, perm, offs, dest, g = o
+        E, T, M, P = [int(x) for x in g.counts.cpu()]
+        r = [perm.cpu(), offs.cpu(), dest.cpu(), g.counts.cpu(), g.key[:E].cpu(), g.count[:E].cpu()]
+        if op == "mean":
+            r.append(g.mean[:E].cpu())
+        else:
+            r += [g.tok_off[:E + 1].cpu(), g.tok[:T].cpu()]
+        if Lm:
+            r += [g.mask_key[:M].cpu(), g.mask[:M].cpu()]
+        return r
+    ref = outs()
+    st = alto.new_status()
+    alto.aggregate(tk, tf, BITS, 4, op, dim, Lm, 4, 256, t32, tpf, ws=ref[0], perm=ref[1], dest_offsets=ref[2],
+                   dest=ref[3], out=ref[4], status=st, n=n)
+    torch.cuda.synchronize()
+    want_status = int(st.item())
+    want = snapshot(ref)
+    sets = [outs(), outs()]
+    main = torch.cuda.current_stream()
+    gather = torch.cuda.Stream()
+    gather.wait_stream(main)
+    done = [torch.cuda.Event(), torch.cuda.Event()]
+    got = []
+    for b in range(4):
+        k = b & 1
+        if b >= 2:
+            main.wait_event(done[k])
+            main.synchronize()   # the previous batch of this set is compared before it is overwritten
+            got.append(snapshot(sets[k]))
+        ws, perm, offs, dest, g = sets[k]
+        alto.aggregate(tk, tf, BITS, 4, op, dim, Lm, 4, 256, t32, tpf, ws=ws, perm=perm, dest_offsets=offs,
+                       dest=dest, out=g, status=st, n=n, stream=main, gather_stream=gather)
+        done[k].record(gather)
+    main.wait_stream(gather)
+    torch.cuda.synchronize()
+    got += [snapshot(sets[0]), snapshot(sets[1])]
+    assert int(st.item()) == want_status == O.OK
+    assert len(got) == 4
+    for r in got:
+        for a, b in zip(want, r):
+            assert torch.equal(a, b)
