@@ -273,26 +273,68 @@ def bench_factool(args):
     fanB = gA.fan_up.view(3, -1)[:, :E]
     prof = {}
 
+    offsB = torch.empty(33, dtype=torch.int64, device="cuda")
+
     def step():
         alto.aggregate(keys, w.fan, w.bits, 4, "mean", dim, 0, 2, 32, w.payload_i32, w.payload_f32, ws=ws,
                        perm=perm, dest_offsets=offs, dest=dest, out=gA, status=stA, n=n)
         alto.aggregate(gA.key, fanB, sb["bits"], 2, "concat", 1, 0, 2, 32, gA.first_i32, None, ws=wsB,
-                       perm=permB, dest_offsets=offs, dest=destB, out=gB, status=stB, n=E)
+                       perm=permB, dest_offsets=offsB, dest=destB, out=gB, status=stB, n=E)
+
+    # stage B of a step on a second HIP stream beside stage A of the next: stage A's
+    # records in one of two buffers, an event each way
+    side = torch.cuda.Stream()
+    gAs = [gA, alto.new_groups(n // 4 + 1024, 4, "mean", dim)]
+    fanBs = [g.fan_up.view(3, -1)[:, :E] for g in gAs]
+    a_done = [torch.cuda.Event(), torch.cuda.Event()]
+    b_done = [torch.cuda.Event(), torch.cuda.Event()]
+    used = [False, False]
+    cnt = [0]
+
+    def step_pipe():
+        k = cnt[0] & 1
+        cnt[0] += 1
+        main = torch.cuda.current_stream()
+        if used[k]:
+            main.wait_event(b_done[k])
+        g = gAs[k]
+        alto.aggregate(keys, w.fan, w.bits, 4, "mean", dim, 0, 2, 32, w.payload_i32, w.payload_f32, ws=ws,
+                       perm=perm, dest_offsets=offs, dest=dest, out=g, status=stA, n=n, stream=main)
+        a_done[k].record(main)
+        side.wait_event(a_done[k])
+        with torch.cuda.stream(side):
+            alto.aggregate(g.key, fanBs[k], sb["bits"], 2, "concat", 1, 0, 2, 32, g.first_i32, None, ws=wsB,
+                           perm=permB, dest_offsets=offsB, dest=destB, out=gB, status=stB, n=E, stream=side)
+        b_done[k].record(side)
+        used[k] = True
     lib = alto.load()
     import ctypes as C
     lib.alto_profile_begin.argtypes = [C.c_int32]
     lib.alto_profile_end.argtypes = [C.POINTER(C.c_float), C.POINTER(C.c_int32), C.c_int32]
+    pipe = not args.no_stage_overlap
+    run = step_pipe if pipe else step
     for _ in range(args.warmup):
-        step()
+        run()
+    torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     lib.alto_profile_phases.argtypes = [C.c_uint32]
     assert lib.alto_profile_phases(1 << PHASES.index("mean_kernel")) == 0
     assert lib.alto_profile_begin(4 * args.steps + 4) == 0
-    ms = _timed(step, args.steps, 0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    side.wait_stream(torch.cuda.current_stream())
+    for _ in range(args.steps):
+        run()
+    torch.cuda.current_stream().wait_stream(side)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
     msp = (C.c_float * len(PHASES))()
     calls = (C.c_int32 * len(PHASES))()
     assert lib.alto_profile_end(msp, calls, len(PHASES)) == 0
     assert lib.alto_profile_phases(0xFFFFFFFF) == 0
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    seq_ms = _timed(step, args.steps, 0) if pipe else ms   # both stages one after the other on one stream
     assert int(stA.item()) == 0 and int(stB.item()) == 0
     C2 = int(gB.counts[0])
     # mean gather of stage A: one launch per step (stage B has no mean)
@@ -301,8 +343,10 @@ def bench_factool(args):
     path_bytes = (n * (8 + 4 + 4 + 4 * dim + 4 + 4) + E * (8 + 4 + 8 + 4 + 12 + 4 * dim)
                   + E * (8 + 8 + 4 + 4 + 4 + 4) + C2 * (8 + 4 + 8 + 4 + 8))
     return _line("FacTool-shaped batch: 1,024 queries, depth 5, 768-d mean per document (route by claim to 32 "
-                 "destinations), then document-id concat per claim", n, ms, args.steps, args.warmup, path_bytes,
-                 {"documents": E, "claims": C2,
+                 "destinations), then document-id concat per claim"
+                 + (" (the claim stage of a batch on a second HIP stream beside the document stage of the next)"
+                    if pipe else ""), n, ms, args.steps, args.warmup, path_bytes,
+                 {"documents": E, "claims": C2, "sequential_ms_per_step": seq_ms,
                   "roofline": {"bound": "hbm", "kernel": "k_mean (first stage)", "achieved":
                                kern_bytes / (mean_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                                "frac": kern_bytes / (mean_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
@@ -779,6 +823,9 @@ def main():
     ap.add_argument("--stream-overlap", default="none", choices=["none", "a", "b", "ab"],
                     help="factool_stream: which stages (document a, claim b) route each step on a HIP stream of "
                          "their own (the stages always run on two streams)")
+    ap.add_argument("--no-stage-overlap", action="store_true",
+                    help="factool: run the claim stage after the document stage on one stream (by default the "
+                         "claim stage of a batch runs on a second HIP stream beside the next batch's first stage)")
     ap.add_argument("--batch-overlap", action="store_true",
                     help="zipf64M: run each batch's gathers on a second HIP stream beside the next batch's routing "
                          "(measured slower: the persistent mean gather fills every CU)")

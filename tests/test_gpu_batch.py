@@ -324,3 +324,70 @@ def test_flow_set_overflow_count_check(bad):
     assert res["status"] == code
     if not bad:
         U.compare(res, rt, g, "concat", Lm, La)
+
+
+def test_two_stage_batches_pipelined_on_two_hip_streams_match_one_stream():
+    """The FacTool-shaped batch's two stages with stage B of a batch on a second HIP
+    stream beside stage A of the next (stage A's records in one of two buffers, events
+    between the stages), over four batches: the outputs of every batch are the same
+    bits as with both stages on one stream."""
+    import torch
+    from paper_2403_04311_amd import alto
+    w = W.config2("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n, dim = w.n, w.dim
+    sb = W.CONFIG2_STAGE_B
+    ws = alto.new_workspace(alto.workspace_bytes(w.bits, n, 32, 4, "mean", dim))
+    stA, stB = alto.new_status(), alto.new_status()
+    gAs = [alto.new_groups(n // 4 + 1024, 4, "mean", dim), alto.new_groups(n // 4 + 1024, 4, "mean", dim)]
+    alto.aggregate(keys, w.fan, w.bits, 4, "mean", dim, 0, 2, 32, w.payload_i32, w.payload_f32, ws=ws,
+                   out=gAs[0], status=stA, n=n)
+    torch.cuda.synchronize()
+    E = int(gAs[0].counts[0])
+    assert int(stA.item()) == 0 and E > 0
+    wsB = alto.new_workspace(alto.workspace_bytes(sb["bits"], E, 32, 2, "concat"))
+    gB = alto.new_groups(E, 2, "concat", cap_tokens=E)
+
+    def snap_a(g):
+        return [g.counts.clone(), g.key[:E].clone(), g.mean[:E].clone(), g.first_i32[:E].clone()]
+
+    def snap_b(g):
+        return [g.counts.clone(), g.key.clone(), g.tok_off.clone(), g.tok.clone()]
+
+    def stage_a(g, stream):
+        alto.aggregate(keys, w.fan, w.bits, 4, "mean", dim, 0, 2, 32, w.payload_i32, w.payload_f32, ws=ws,
+                       out=g, status=stA, n=n, stream=stream)
+
+    def stage_b(g, stream):
+        alto.aggregate(g.key, g.fan_up.view(3, -1)[:, :E], sb["bits"], 2, "concat", 1, 0, 2, 32, g.first_i32,
+                       None, ws=wsB, out=gB, status=stB, n=E, stream=stream)
+    main = torch.cuda.current_stream()
+    seq = []
+    for b in range(4):
+        stage_a(gAs[0], main)
+        sa = snap_a(gAs[0])
+        stage_b(gAs[0], main)
+        seq.append((sa, snap_b(gB)))
+    side = torch.cuda.Stream()
+    side.wait_stream(main)
+    a_done = [torch.cuda.Event(), torch.cuda.Event()]
+    b_done = [torch.cuda.Event(), torch.cuda.Event()]
+    par = []
+    for b in range(4):
+        k = b & 1
+        if b >= 2:
+            main.wait_event(b_done[k])
+        stage_a(gAs[k], main)
+        sa = snap_a(gAs[k])
+        a_done[k].record(main)
+        side.wait_event(a_done[k])
+        with torch.cuda.stream(side):
+            stage_b(gAs[k], side)
+            par.append((sa, snap_b(gB)))
+        b_done[k].record(side)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    for (a0, b0), (a1, b1) in zip(seq, par):
+        for x, y in zip(a0 + b0, a1 + b1):
+            assert torch.equal(x, y)
