@@ -4,7 +4,7 @@
 #include "segment.h"
 #include "sort.h"
 
-#define GROUP_SCAN_TILE 4096   // groups per tile of the group scan (k_group_scan)
+#define GROUP_SCAN_TILE 1024   // groups per tile of the group kernel (k_groups)
 #define GROUP_SCAN_WORDS 5     // its look-back words per tile
 #define MEAN_CHUNK_ROWS 4096
 #define MEAN_SMALL_ROWS 256    // groups of at most this many rows: one chunk, gathered by one wave
@@ -116,7 +116,7 @@ struct AggBufs {
   uint64_t* fp_in;
   uint64_t* fp_nodes;
   int64_t* nnodes;
-  int64_t* scal;        // [8] device scalars: 1 = chunk count, 2 = block ticket, 3 = chunks of long groups
+  int64_t* scal;        // [8] device scalars: 1 = chunks of long groups, 2 = block ticket, 3 = short groups
   uint64_t* tmp_keys;
   uint32_t* tmp_vals;
   uint64_t* sk;
@@ -129,12 +129,10 @@ struct AggBufs {
   uint64_t* rkey;
   uint64_t* rsk;
   uint32_t* ridx;
-  int32_t* em;
-  int64_t* tokc;
-  int64_t* nch;
-  int64_t* pch;
-  int64_t* nsm;         // scanned count of small groups (one wave-gathered chunk each)
-  Chunk* chunks;
+  int32_t* em;          // [n+1] scratch of the stream's live-set update (freed arena slots)
+  int64_t* tokc;        // [n+1] the same (arena slots to fill)
+  Chunk* chunks;        // long-group chunks from 0, short-group chunks from short_base
+  int64_t short_base;
   double* part;
   uint2* gw;            // [cdiv(n_max, SEG_IT)] group-level boundary words of the segmentation pass (streams)
 };
@@ -150,19 +148,19 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
               int32_t* status, hipStream_t st, bool offsets_later = false, bool exact_flow_levels = false,
               bool allow_dp = false, const int64_t* n_dev = nullptr);
 // Work folded into the kernels of groups_run (fewer launches per call):
-//  - the comparison of the fan fingerprints, in the record kernel (fp_in null:
+//  - the comparison of the fan fingerprints, in the group kernel (fp_in null:
 //    none; levels flo..fhi, those in xlo..xhi only when ctl reports a flow-set
 //    overflow, as in k_fp_compare);
-//  - the group scan's look-back words at gst and its ticket at *gctr (null: the
+//  - the group kernel's look-back words at gst and its ticket at *gctr (null: the
 //    sort's status words and first ticket); cleared = the caller's earlier kernel
 //    cleared them (cdiv(n_max + 1, GROUP_SCAN_TILE) * GROUP_SCAN_WORDS words),
-//    else the scan's first kernel does, and also clears another look-back region
+//    else a kernel before it does, and also clears another look-back region
 //    (xst null: none) of cdiv(*xlen, xtile) * xper words and its ticket *xctr, for
 //    a scan that runs after the groups;
-//  - the emitted set (ht null: none): the record kernel inserts the key of every
+//  - the emitted set (ht null: none): the group kernel inserts the key of every
 //    emitted group into an insert-only open-addressing set of htcap (a power of
-//    two) slots, counting new keys in *emit_count; more than max_emit keys, or a
-//    full table, raise ALTO_E_CAPACITY;
+//    two) slots, counting new keys in *emit_count; a full table raises
+//    ALTO_E_CAPACITY (the caller compares the count with its own limit later);
 //  - concat / multi-chunk means left to the caller (defer_concat, defer_combine).
 struct GroupsExtra {
   const uint64_t* fp_in;
@@ -177,24 +175,34 @@ struct GroupsExtra {
   const int64_t* xlen;
   int64_t xtile, xper;
   uint64_t* ht;
-  int64_t htcap, max_emit;
+  int64_t htcap;
   int64_t* emit_count;
   // the gathers the caller runs itself later (concat_chunks / mean_combine_chunks)
   int32_t defer_concat, defer_combine;
   // the gathers on another HIP stream (gather_st, after an event recorded on the
   // call's stream; null: the call's stream)
   hipStream_t gather_st;
+  // the group kernel evaluates the completion of the group-level nodes itself (the
+  // segmentation launched no k_seg_nodes for that level): children are elements
+  // (fold_leafy) or next-level nodes; fingerprint terms of fold_level into fold_fp
+  // from the elements' keys (prefix shift fold_es)
+  int32_t fold, fold_leafy, fold_level, fold_es;
+  const uint64_t* fold_keys;
+  uint64_t* fold_fp;
 };
 
 #define EMIT_EMPTY (~0ull)
 
-// Concatenation of the chunks [c0, NC) step cstride (a block each): every row of a
-// chunk copies its int32 payload to the chunk's token range.
+// Concatenation of the chunks of the long groups (chunks[0, NB)) and the short
+// ones (chunks_s[0, NS)), chunk c0 and every cstride-th after it in that order (a
+// block each): every row of a chunk copies its int32 payload to the chunk's token
+// range.
 template <typename Src>
-__device__ inline void concat_chunks(const Chunk* __restrict__ chunks, int64_t NC, const Src& src, int32_t* tok,
-                                     int64_t cap_tokens, int64_t c0, int64_t cstride) {
-  for (int64_t c = c0; c < NC; c += cstride) {
-    const Chunk ch = chunks[c];
+__device__ inline void concat_chunks(const Chunk* __restrict__ chunks, int64_t NB, const Chunk* __restrict__ chunks_s,
+                                     int64_t NS, const Src& src, int32_t* tok, int64_t cap_tokens, int64_t c0,
+                                     int64_t cstride) {
+  for (int64_t c = c0; c < NB + NS; c += cstride) {
+    const Chunk ch = c < NB ? chunks[c] : chunks_s[c - NB];
     for (int r = threadIdx.x; r < ch.len; r += blockDim.x) {
       const int64_t o = ch.out + r;
       if (o < cap_tokens) tok[o] = src.p32_of(src.row(ch.begin + r));
@@ -204,11 +212,12 @@ __device__ inline void concat_chunks(const Chunk* __restrict__ chunks, int64_t N
 
 // The same with one wave per chunk (wave wid of nw), for chunks of a few rows.
 template <typename Src>
-__device__ inline void concat_chunks_wave(const Chunk* __restrict__ chunks, int64_t NC, const Src& src, int32_t* tok,
+__device__ inline void concat_chunks_wave(const Chunk* __restrict__ chunks, int64_t NB,
+                                          const Chunk* __restrict__ chunks_s, int64_t NS, const Src& src, int32_t* tok,
                                           int64_t cap_tokens, int64_t wid, int64_t nw) {
   const int lane = lane_id();
-  for (int64_t c = wid; c < NC; c += nw) {
-    const Chunk ch = chunks[c];
+  for (int64_t c = wid; c < NB + NS; c += nw) {
+    const Chunk ch = c < NB ? chunks[c] : chunks_s[c - NB];
     for (int r = lane; r < ch.len; r += ALTO_WAVE) {
       const int64_t o = ch.out + r;
       if (o < cap_tokens) tok[o] = src.p32_of(src.row(ch.begin + r));
@@ -217,7 +226,7 @@ __device__ inline void concat_chunks_wave(const Chunk* __restrict__ chunks, int6
 }
 
 // The mean of every group of several chunks from its chunks' partial sums (chunk
-// order), chunks [c0, NC) step cstride, a block of 256 threads each: SUBS chunk
+// order), long-group chunks [c0, NC) step cstride, a block of 256 threads each: SUBS chunk
 // subsets x COLS columns; each thread sums every SUBS-th chunk, then the subsets are
 // added in subset order. Every thread of the block calls it (it holds barriers).
 __device__ inline void mean_combine_chunks(const Chunk* __restrict__ chunks, int64_t NC,

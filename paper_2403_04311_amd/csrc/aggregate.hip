@@ -476,15 +476,25 @@ __global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, in
     if ((all || m < xlo || m > xhi) && fp_in[m] != fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
 }
 
-// Per-group scan inputs.
-// Group prefix sums in one pass: over groups u = 0..G (entry G holds the totals),
-// the exclusive sums of emitted (complete) flags, emitted tokens, mean chunks and
-// chunk partials (groups of more than one chunk). Tiles by ticket, sums across
-// tiles by look-back (64-bit words: token sums may exceed 2^30).
+// The groups of the aggregation level in one kernel. Per tile of groups: the
+// exclusive sums over groups u = 0..G (entry G holds the totals) of emitted
+// (complete) flags, emitted tokens, long-group chunks, chunk partials (groups of
+// more than one chunk) and short groups; tiles by ticket, sums across tiles by
+// look-back (64-bit words: token sums may exceed 2^30). Then, with the tile's
+// groups strided over the threads, each group's outputs: records (emitted groups)
+// or pending entries, and its chunk descriptors. Groups of more than
+// MEAN_SMALL_ROWS rows are cut into chunks of chunk_rows, at chunks[first long
+// chunk of the group ...]; each shorter group is one chunk at chunks[short_base +
+// its short-group index], so no position depends on the totals. Emitted groups
+// enter the emitted set (ex.ht). The thread holding entry G writes the call's
+// counts and the chunk totals the gathers read (capacity checked there), and,
+// unless the fold accumulates fingerprint terms in this same kernel, compares the
+// fan fingerprints.
 constexpr int GS_NT = 256;
-constexpr int GS_IT = 16;
+constexpr int GS_IT = 4;
 constexpr int GS_TILE = GS_NT * GS_IT;
 static_assert(GS_TILE == GROUP_SCAN_TILE, "group scan tile");
+static_assert(GS_IT <= 32, "a thread's groups in one flag word");
 
 constexpr int GS_NV = GROUP_SCAN_WORDS;   // scanned values per group
 
@@ -502,28 +512,124 @@ __global__ void k_group_scan_prep(const int64_t* Gp, uint64_t* st, uint32_t* ctr
   }
 }
 
-__global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_t* Gp, int32_t* em, int64_t* tokc,
-                                                     int64_t* nch, int64_t* pch, int64_t* nsm, int chunk_rows,
-                                                     uint64_t* st, uint32_t* ctr, int32_t* status) {
+// The completion of the group-level nodes, when the group kernel evaluates it (as
+// k_seg_nodes would for that level).
+struct GroupFold {
+  int32_t on, leafy, level, es;
+  uint64_t fkey;
+  const uint64_t* keys;
+  uint64_t* fp;   // nullable: fingerprint sums per level
+};
+
+template <typename Src>
+__global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int La, LevelNodes L, const int64_t* Gp,
+                                                  const uint64_t* __restrict__ sk, Src src, Chunk* chunks,
+                                                  int64_t short_base, int chunk_rows, GroupOut out, int concat,
+                                                  const int64_t* Mp, int64_t* scal, GroupsExtra ex, uint64_t* st,
+                                                  uint32_t* ctr, GroupFold f, int32_t* status) {
   const int64_t G = *Gp;
   const int64_t ntiles = cdiv(G + 1, GS_TILE);
   __shared__ int64_t s_w[GS_NT / ALTO_WAVE];
   __shared__ int64_t s_ex[GS_NV];
   __shared__ uint32_t s_tile;
+  // per group of the tile: the fold's flags and row counts, then the exclusive sums
+  __shared__ uint8_t s_okf[GS_TILE];
+  __shared__ int32_t s_cnt[GS_TILE];
+  __shared__ int32_t s_em[GS_TILE], s_cb[GS_TILE], s_pb[GS_TILE], s_sb[GS_TILE];
+  __shared__ int64_t s_tb[GS_TILE];
   if ((int64_t)blockIdx.x >= ntiles) return;   // no tile would be left for this block
+  const int lane = lane_id();
+  uint64_t fpm = 0;     // fingerprint terms of the groups this thread evaluated
+  int64_t fresh = 0;    // keys new to the emitted set
+  bool full = false;
+  bool first = true;
   while (true) {
-    if (threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
+    // a single tile is block 0's without a ticket (it waits for no other tile)
+    if (ntiles > 1 && threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
     __syncthreads();
-    const int64_t tile = (int64_t)s_tile;
+    const int64_t tile = ntiles > 1 ? (int64_t)s_tile : (first ? 0 : 1);
+    first = false;
     if (tile >= ntiles) break;   // uniform
-    const int64_t u0 = tile * GS_TILE + (int64_t)threadIdx.x * GS_IT;
+    const int64_t g0 = tile * GS_TILE;
+    const int64_t u0 = g0 + (int64_t)threadIdx.x * GS_IT;
+    // the tile's groups strided over the threads (group g0 + k GS_NT + threadIdx.x):
+    // first element and its key, for the fold and the outputs
+    int32_t sv[GS_IT];
+    uint64_t kk[GS_IT];
     int64_t v[GS_IT][GS_NV];
     int64_t sum[GS_NV] = {0, 0, 0, 0, 0};
+    uint32_t okm = 0;         // bit i: group u0 + i is complete
+    int32_t cnv[GS_IT] = {};  // rows of the groups u0 + i
+    if (f.on) {
+      // complete: as many children as declared, none of them incomplete. Every load
+      // first, then the flags, fingerprint terms and stores; the scan reads the
+      // flags and row counts back from LDS.
+      int32_t sn[GS_IT], cv[GS_IT], cn[GS_IT], nf[GS_IT];
+      uint8_t bd[GS_IT];
+#pragma unroll
+      for (int k = 0; k < GS_IT; ++k) {
+        const int64_t u = g0 + k * GS_NT + threadIdx.x;
+        const bool in = u < G;
+        sv[k] = in ? L.start[u] : 0;
+        sn[k] = in ? L.start[u + 1] : 0;
+        cv[k] = (in && !f.leafy) ? L.fc[u] : 0;
+        cn[k] = (in && !f.leafy) ? L.fc[u + 1] : 0;
+        nf[k] = in ? L.nfan[u] : 0;
+        bd[k] = in ? L.bad[u] : 1;
+      }
+#pragma unroll
+      for (int k = 0; k < GS_IT; ++k) kk[k] = g0 + k * GS_NT + threadIdx.x < G ? f.keys[sv[k]] : 0ull;
+#pragma unroll
+      for (int k = 0; k < GS_IT; ++k) {
+        const int64_t u = g0 + k * GS_NT + threadIdx.x;
+        const int idx = k * GS_NT + threadIdx.x;
+        if (u >= G) {
+          s_okf[idx] = 0;
+          s_cnt[idx] = 0;
+          continue;
+        }
+        const int32_t n0 = sn[k] - sv[k];
+        const int32_t nchild = f.leafy ? n0 : cn[k] - cv[k];
+        const bool ok = nchild == nf[k] && !bd[k];
+        s_okf[idx] = ok ? 1 : 0;
+        s_cnt[idx] = n0;
+        L.ok[u] = ok ? 1 : 0;
+        if (f.fp) fpm += (uint64_t)n0 * fan_term(f.fkey, f.level, key_prefix(kk[k], f.es), (uint32_t)nf[k]);
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < GS_IT; ++i) {
+        const int idx = threadIdx.x * GS_IT + i;
+        okm |= (uint32_t)s_okf[idx] << i;
+        cnv[i] = s_cnt[idx];
+      }
+    } else {
+      int32_t sn[GS_IT];
+#pragma unroll
+      for (int k = 0; k < GS_IT; ++k) {
+        const int64_t u = g0 + k * GS_NT + threadIdx.x;
+        const bool in = u < G;
+        sv[k] = in ? L.start[u] : 0;
+        sn[k] = in ? L.start[u + 1] : 0;
+        s_okf[k * GS_NT + threadIdx.x] = (in && L.ok[u]) ? 1 : 0;
+      }
+#pragma unroll
+      for (int k = 0; k < GS_IT; ++k) {
+        kk[k] = g0 + k * GS_NT + threadIdx.x < G ? sk[sv[k]] : 0ull;
+        s_cnt[k * GS_NT + threadIdx.x] = sn[k] - sv[k];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < GS_IT; ++i) {
+        const int idx = threadIdx.x * GS_IT + i;
+        okm |= (uint32_t)s_okf[idx] << i;
+        cnv[i] = s_cnt[idx];
+      }
+    }
 #pragma unroll
     for (int i = 0; i < GS_IT; ++i) {
-      const int64_t u = u0 + i;
-      const bool ok = u < G && L.ok[u];
-      const int64_t cnt = ok ? (int64_t)L.start[u + 1] - L.start[u] : 0;
+      const bool ok = (okm >> i) & 1u;
+      const int64_t cnt = ok ? (int64_t)cnv[i] : 0;
       const bool small = ok && cnt <= MEAN_SMALL_ROWS;
       const int64_t c = ok && !small ? cdiv(cnt, chunk_rows) : 0;
       v[i][0] = ok ? 1 : 0;
@@ -534,9 +640,9 @@ __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_
 #pragma unroll
       for (int q = 0; q < GS_NV; ++q) sum[q] += v[i][q];
     }
-    int64_t ex[GS_NV], tot[GS_NV];
+    int64_t exs[GS_NV], tot[GS_NV];
 #pragma unroll
-    for (int q = 0; q < GS_NV; ++q) ex[q] = block_excl_scan<int64_t, GS_NT>(sum[q], s_w, &tot[q]);
+    for (int q = 0; q < GS_NV; ++q) exs[q] = block_excl_scan<int64_t, GS_NT>(sum[q], s_w, &tot[q]);
     if (threadIdx.x < GS_NV) {
       const int q = threadIdx.x;
       int64_t t = tot[0];
@@ -549,123 +655,146 @@ __global__ __launch_bounds__(GS_NT) void k_group_scan(LevelNodes L, const int64_
     __syncthreads();
     int64_t run[GS_NV];
 #pragma unroll
-    for (int q = 0; q < GS_NV; ++q) run[q] = s_ex[q] + ex[q];
+    for (int q = 0; q < GS_NV; ++q) run[q] = s_ex[q] + exs[q];
 #pragma unroll
     for (int i = 0; i < GS_IT; ++i) {
       const int64_t u = u0 + i;
-      if (u <= G) {
-        em[u] = (int32_t)run[0];
-        tokc[u] = run[1];
-        nch[u] = run[2];
-        pch[u] = run[3];
-        nsm[u] = run[4];
+      const int idx = threadIdx.x * GS_IT + i;
+      s_em[idx] = (int32_t)run[0];
+      s_tb[idx] = run[1];
+      s_cb[idx] = (int32_t)run[2];
+      s_pb[idx] = (int32_t)run[3];
+      s_sb[idx] = (int32_t)run[4];
+      if (u == G) {
+        // the totals: the call's counts, the chunk totals of the gathers, capacity
+        const int64_t E = run[0], T = concat ? run[1] : 0, M = Mp ? *Mp : 0, P = G - E;
+        scal[1] = run[2];   // long-group chunks: chunks[0, scal[1])
+        scal[2] = 0;        // block tickets of the mean gather (long groups)
+        scal[3] = run[4];   // short groups: chunks[short_base, short_base + scal[3])
+        out.counts[0] = E;
+        out.counts[1] = T;
+        out.counts[2] = M;
+        out.counts[3] = P;
+        if (out.tok_off && E <= out.cap_groups) out.tok_off[E] = T;
+        if (E > out.cap_groups || P > out.cap_groups || T > out.cap_tokens || M > out.cap_mask)
+          raise_status(status, ALTO_E_CAPACITY);
+        if (ex.fp_in) {
+          const bool all = ex.ctl == nullptr || ex.ctl->flow_overflow;
+          for (int m = ex.flo; m <= ex.fhi; ++m)
+            if ((all || m < ex.xlo || m > ex.xhi) && ex.fp_in[m] != ex.fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
+        }
       }
 #pragma unroll
       for (int q = 0; q < GS_NV; ++q) run[q] += v[i][q];
     }
-    __syncthreads();   // s_ex and the ticket are reused by the next tile
-  }
-}
-
-// Group records and chunk descriptors, one thread per group; block 0 also writes
-// the call's counts and the chunk totals the gathers read (emitted groups, tokens,
-// mask nodes, pending groups; capacity) and compares the fan fingerprints.
-// Chunks: groups of more than MEAN_SMALL_ROWS rows are cut into chunks of
-// chunk_rows (their first index from the scanned chunk counts); each shorter
-// group is one chunk after those. Emitted groups enter the emitted set (ex.ht).
-template <typename Src>
-__global__ __launch_bounds__(256) void k_group_out(KeyGeom g, RouteGeom rg, int La, LevelNodes L, const int64_t* Gp,
-                                                   const uint64_t* __restrict__ sk, Src src, const int32_t* em,
-                                                   const int64_t* tokb, const int64_t* chb, const int64_t* pb,
-                                                   const int64_t* smb, Chunk* chunks, int chunk_rows, GroupOut out,
-                                                   const int64_t* tokc_or_null, const int64_t* Mp, int64_t* scal,
-                                                   GroupsExtra ex, int32_t* status) {
-  const int64_t G = *Gp;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    scal[1] = chb[G] + smb[G];   // chunks: those of long groups, then one per short group
-    scal[2] = 0;                 // block tickets of the mean gather (long groups)
-    scal[3] = chb[G];            // short groups: chunks scal[3] .. scal[1] - 1
-    const int64_t E = em[G];
-    const int64_t T = tokc_or_null ? tokc_or_null[G] : 0;
-    const int64_t M = Mp ? *Mp : 0;
-    const int64_t P = G - E;
-    out.counts[0] = E;
-    out.counts[1] = T;
-    out.counts[2] = M;
-    out.counts[3] = P;
-    if (out.tok_off && E <= out.cap_groups) out.tok_off[E] = T;
-    if (E > out.cap_groups || P > out.cap_groups || T > out.cap_tokens || M > out.cap_mask)
-      raise_status(status, ALTO_E_CAPACITY);
-    if (ex.fp_in) {
-      const bool all = ex.ctl == nullptr || ex.ctl->flow_overflow;
-      for (int m = ex.flo; m <= ex.fhi; ++m)
-        if ((all || m < ex.xlo || m > ex.xhi) && ex.fp_in[m] != ex.fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
+    __syncthreads();   // the tile's sums are in LDS
+    // the outputs of the tile's groups (strided, as loaded above): records or pending
+    // entries, the emitted set, and each complete group's first chunk by its own
+    // lane; the further chunks of long groups by the whole wave, group by group
+    const bool need_first = out.first_i32 || (out.fan_up && La > 1);
+    int64_t fr[GS_IT];
+#pragma unroll
+    for (int k = 0; k < GS_IT; ++k) {
+      const int idx = k * GS_NT + threadIdx.x;
+      fr[k] = (need_first && g0 + k * GS_NT + threadIdx.x < G && s_okf[idx]) ? src.row(sv[k]) : 0;
     }
-  }
-  const int64_t NB = chb[G];   // chunks of the long groups come first, then one per short group
-  int64_t fresh = 0;           // keys new to the emitted set
-  bool full = false;
-  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < G; u += (int64_t)gridDim.x * blockDim.x) {
-    const int32_t s = L.start[u], cnt = L.start[u + 1] - s;
-    const uint64_t k = sk[s];
-    const uint64_t gk = key_prefix(k, g.shift[La]);
-    if (L.ok[u]) {
-      const int64_t e = em[u];
-      if (e < out.cap_groups) {
-        if (out.key) out.key[e] = gk;
-        if (out.dest) out.dest[e] = (int32_t)dest_of_key(rg, k);
-        if (out.count) out.count[e] = cnt;
-        const int64_t first = src.row(s);
-        if (out.first_i32) out.first_i32[e] = src.p32_of(first);
-        if (out.fan_up)
-          for (int l = 1; l < La; ++l) out.fan_up[(int64_t)(l - 1) * out.cap_groups + e] = src.fan_of(l, first);
-        if (out.tok_off) out.tok_off[e] = tokb[u];
+#pragma unroll
+    for (int k = 0; k < GS_IT; ++k) {
+      const int64_t u = g0 + k * GS_NT + threadIdx.x;
+      const int idx = k * GS_NT + threadIdx.x;
+      const bool in = u < G;
+      const bool ok = in && s_okf[idx];
+      const int32_t s = sv[k], cnt = s_cnt[idx];
+      const int64_t e = s_em[idx], o = s_tb[idx];
+      const bool small = cnt <= MEAN_SMALL_ROWS;
+      const int64_t nc = ok ? (small ? 1 : cdiv(cnt, chunk_rows)) : 0;
+      const int64_t c0 = small ? short_base + s_sb[idx] : (int64_t)s_cb[idx];
+      const int64_t part = nc > 1 ? (int64_t)s_pb[idx] : -1;
+      if (in) {
+        const uint64_t gk = key_prefix(kk[k], g.shift[La]);
+        if (ok) {
+          if (e < out.cap_groups) {
+            if (out.key) out.key[e] = gk;
+            if (out.dest) out.dest[e] = (int32_t)dest_of_key(rg, kk[k]);
+            if (out.count) out.count[e] = cnt;
+            if (out.first_i32) out.first_i32[e] = src.p32_of(fr[k]);
+            if (out.fan_up)
+              for (int l = 1; l < La; ++l) out.fan_up[(int64_t)(l - 1) * out.cap_groups + e] = src.fan_of(l, fr[k]);
+            if (out.tok_off) out.tok_off[e] = o;
+          }
+          if (ex.ht) {
+            const int r = emitted_insert(gk, ex.ht, ex.htcap);
+            if (r < 0) full = true;
+            else fresh += r;
+          }
+          Chunk ch;
+          ch.e = e;
+          ch.begin = s;
+          ch.len = cnt < chunk_rows ? cnt : chunk_rows;
+          ch.k = 0;
+          ch.nch = (int32_t)nc;
+          ch.count = cnt;
+          ch.part = part;
+          ch.out = o;
+          ch.pad = 0;
+          chunks[c0] = ch;
+        } else {
+          const int64_t p = u - e;
+          if (p < out.cap_groups) {
+            if (out.pend_key) out.pend_key[p] = gk;
+            if (out.pend_count) out.pend_count[p] = cnt;
+          }
+        }
       }
-      if (ex.ht) {
-        const int r = emitted_insert(gk, ex.ht, ex.htcap);
-        if (r < 0) full = true;
-        else fresh += r;
-      }
-    } else {
-      const int64_t p = u - em[u];
-      if (p < out.cap_groups) {
-        if (out.pend_key) out.pend_key[p] = gk;
-        if (out.pend_count) out.pend_count[p] = cnt;
+      // chunks 1 .. nc-1 of the wave's long groups, one group at a time
+      for (uint64_t many = __ballot(nc > 1); many; many &= many - 1) {
+        const int l = __builtin_ctzll(many);
+        const int64_t le = __shfl(e, l), lo = __shfl(o, l), lc0 = __shfl(c0, l), lpart = __shfl(part, l);
+        const int32_t ls = __shfl(s, l), lcnt = __shfl(cnt, l);
+        const int64_t lnc = __shfl(nc, l);
+        for (int64_t c = 1 + lane; c < lnc; c += ALTO_WAVE) {
+          Chunk ch;
+          ch.e = le;
+          ch.begin = ls + (int32_t)(c * chunk_rows);
+          ch.len = (int32_t)((lcnt - c * chunk_rows) < chunk_rows ? (lcnt - c * chunk_rows) : chunk_rows);
+          ch.k = (int32_t)c;
+          ch.nch = (int32_t)lnc;
+          ch.count = lcnt;
+          ch.part = lpart;
+          ch.out = lo + c * chunk_rows;
+          ch.pad = 0;
+          chunks[lc0 + c] = ch;
+        }
       }
     }
-    const bool small = smb[u + 1] > smb[u];
-    const int64_t c0 = small ? NB + smb[u] : chb[u], nc = small ? 1 : chb[u + 1] - chb[u];
-    if (nc <= 0) continue;   // an incomplete group has no chunk
-    const int64_t e = em[u], part = nc > 1 ? pb[u] : -1, o = tokb[u];
-    for (int64_t c = 0; c < nc; ++c) {
-      Chunk ch;
-      ch.e = e;
-      ch.begin = s + (int32_t)(c * chunk_rows);
-      ch.len = (int32_t)((cnt - c * chunk_rows) < chunk_rows ? (cnt - c * chunk_rows) : chunk_rows);
-      ch.k = (int32_t)c;
-      ch.nch = (int32_t)nc;
-      ch.count = cnt;
-      ch.part = part;
-      ch.out = o + c * chunk_rows;
-      ch.pad = 0;
-      chunks[c0 + c] = ch;
+    __syncthreads();   // s_ex, the tile's LDS and the ticket are reused by the next tile
+  }
+  if (f.on && f.fp) {
+    // one atomic per block
+    __shared__ uint64_t s_fp[GS_NT / ALTO_WAVE];
+    const uint64_t w = wave_sum(fpm);
+    if (lane == 0) s_fp[threadIdx.x / ALTO_WAVE] = w;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      uint64_t t = 0;
+      for (int ww = 0; ww < GS_NT / ALTO_WAVE; ++ww) t += s_fp[ww];
+      if (t) atomicAdd((unsigned long long*)&f.fp[f.level], (unsigned long long)t);
     }
   }
   if (ex.ht) {
-    // one count update per wave
+    // one count update per wave (the caller's next kernel compares the total with
+    // its limit)
     const int64_t w = wave_sum(fresh);
-    if (lane_id() == 0 && w) {
-      const int64_t before = (int64_t)atomicAdd((unsigned long long*)ex.emit_count, (unsigned long long)w);
-      if (before + w > ex.max_emit) full = true;
-    }
+    if (lane == 0 && w) atomicAdd((unsigned long long*)ex.emit_count, (unsigned long long)w);
     if (full) raise_status(status, ALTO_E_CAPACITY);
   }
 }
 
 template <typename Src>
-__global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks, const int64_t* nchunks, Src src,
+__global__ __launch_bounds__(256) void k_concat(const Chunk* __restrict__ chunks, const int64_t* nlong,
+                                                const Chunk* __restrict__ chunks_s, const int64_t* nshort, Src src,
                                                 int32_t* tok, int64_t cap_tokens) {
-  concat_chunks<Src>(chunks, *nchunks, src, tok, cap_tokens, blockIdx.x, gridDim.x);
+  concat_chunks<Src>(chunks, *nlong, chunks_s, *nshort, src, tok, cap_tokens, blockIdx.x, gridDim.x);
 }
 
 // fp64 sum of the rows of one chunk of a group, in a fixed order: each lane sums
@@ -747,18 +876,19 @@ __device__ inline void mean_short_chunk(const Chunk& ch, const Src& srcp, int di
 }
 
 // Chunks [0, NB) belong to long groups and are gathered a block each (first phase);
-// chunks [NB, NC) are short groups, gathered a wave each (second phase).
+// chunks_s [0, NS) are short groups, gathered a wave each (second phase).
 template <int VEC, int CPL, typename Src>
-__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nchunks,
-                                              const int64_t* nblock, Src srcp, int dim, int lpr, double* part,
-                                              float* mean, int64_t cap_groups, unsigned long long* ticket) {
+__global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, const int64_t* nblock,
+                                              const Chunk* __restrict__ chunks_s, const int64_t* nshort, Src srcp,
+                                              int dim, int lpr, double* part, float* mean, int64_t cap_groups,
+                                              unsigned long long* ticket) {
   constexpr int NW = 4;
   constexpr int U = 2;   // row loads in flight per lane (more lowers occupancy)
   __shared__ double red[NW][64 * CPL * VEC];
   const int C = dim / VEC;
   const int lane = lane_id(), w = threadIdx.x / ALTO_WAVE;
   const int rpw = ALTO_WAVE / lpr, sub = lane / lpr, cl = lane % lpr;
-  const int64_t NC = *nchunks, NB = *nblock;
+  const int64_t NB = *nblock, NS = *nshort;
   __shared__ int64_t s_c;
   // chunks are taken by ticket: groups have very different sizes, and a block that
   // finishes early takes the next chunk (the sum of a chunk does not depend on
@@ -857,8 +987,8 @@ __global__ __launch_bounds__(256) void k_mean(const Chunk* __restrict__ chunks, 
   }
   // short groups: one wave each, assigned round robin (they have similar sizes, and
   // tickets would serialise on one counter: one atomic per short group)
-  for (int64_t c = NB + (int64_t)blockIdx.x * NW + w; c < NC; c += (int64_t)gridDim.x * NW) {
-    const Chunk ch = chunks[c];
+  for (int64_t c = (int64_t)blockIdx.x * NW + w; c < NS; c += (int64_t)gridDim.x * NW) {
+    const Chunk ch = chunks_s[c];
     mean_short_chunk<VEC, CPL, Src>(ch, srcp, dim, C, lpr, mean, cap_groups);
   }
 }
@@ -991,10 +1121,10 @@ void plan_buffers(const KeyGeom& g, int64_t n_max, const RouteGeom& rg, const al
   }
   b.em = c.take<int32_t>(n + 1);
   b.tokc = c.take<int64_t>(n + 1);
-  b.nch = c.take<int64_t>(n + 1);
-  b.pch = c.take<int64_t>(n + 1);
-  b.nsm = c.take<int64_t>(n + 1);
-  b.chunks = c.take<Chunk>(n / MEAN_CHUNK_ROWS + n + 1);
+  // long groups (more than MEAN_SMALL_ROWS rows) have at most n / MEAN_CHUNK_ROWS +
+  // n / (MEAN_SMALL_ROWS + 1) chunks; short groups (one chunk each) at most n
+  b.short_base = n / MEAN_CHUNK_ROWS + n / (MEAN_SMALL_ROWS + 1) + 1;
+  b.chunks = c.take<Chunk>(b.short_base + n + 1);
   if (agg->op == ALTO_MEAN_F32) b.part = c.take<double>((2 * cdiv(n, MEAN_CHUNK_ROWS) + 2) * (int64_t)agg->dim);
 }
 
@@ -1244,13 +1374,11 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
       return ALTO_E_ARG;   // never: words to spare
     const int64_t pb = cdiv(tiles * GS_NV, 256);
     if (!x.cleared) k_group_scan_prep<<<(int)(pb < 1024 ? pb : 1024), 256, 0, st>>>(Gp, gst, gctr, x);
-    k_group_scan<<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(GL, Gp, b.em, b.tokc, b.nch, b.pch, b.nsm,
-                                                                  MEAN_CHUNK_ROWS, gst, gctr, status);
+    GroupFold f{x.fold, x.fold_leafy, x.fold_level, x.fold_es, g.fkey, x.fold_keys, x.fold_fp};
+    k_groups<Src><<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(
+        g, rg, La, GL, Gp, sk, src, b.chunks, b.short_base, MEAN_CHUNK_ROWS, out, agg.op == ALTO_CONCAT_I32 ? 1 : 0,
+        Mp, b.scal, x, gst, gctr, f, status);
   }
-  k_group_out<Src><<<grid_for(n, 256), 256, 0, st>>>(g, rg, La, GL, Gp, sk, src, b.em, b.tokc, b.nch, b.pch, b.nsm,
-                                                     b.chunks, MEAN_CHUNK_ROWS, out,
-                                                     agg.op == ALTO_CONCAT_I32 ? b.tokc : nullptr, Mp, b.scal, x,
-                                                     status);
   ALTO_LAUNCH_CHECK();
   prof_end(PH_GROUPS, st);
   // the gathers, on another stream if asked (after the records, through an event
@@ -1264,9 +1392,12 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
     st = x.gather_st;
   }
   ProfScope ps_gather(PH_GATHER, st);
-  const int64_t* NCp = b.scal + 1;   // chunk count
+  const int64_t* NBp = b.scal + 1;   // chunks of long groups
+  const int64_t* NSp = b.scal + 3;   // short groups (one chunk each, from short_base)
   if (agg.op == ALTO_CONCAT_I32) {
-    if (out.tok && !x.defer_concat) k_concat<Src><<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, src, out.tok, out.cap_tokens);
+    if (out.tok && !x.defer_concat)
+      k_concat<Src><<<GRID_CAP, 256, 0, st>>>(b.chunks, NBp, b.chunks + b.short_base, NSp, src, out.tok,
+                                              out.cap_tokens);
   } else if (out.mean) {
     const int dim = agg.dim;
     const bool v4 = (dim % 4 == 0) && src_rows_aligned16(src);
@@ -1279,8 +1410,9 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
 #define ALTO_MEAN_CASE(V, P)                                                                                 \
   do {                                                                                                       \
     ProfScope ps_mean(PH_MEAN, st);                                                                          \
-    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NCp, b.scal + 3, src, dim, lpr, b.part, out.mean,       \
-                                            out.cap_groups, reinterpret_cast<unsigned long long*>(b.scal + 2)); \
+    k_mean<V, P, Src><<<grid, 256, 0, st>>>(b.chunks, NBp, b.chunks + b.short_base, NSp, src, dim, lpr, b.part, \
+                                            out.mean, out.cap_groups,                                          \
+                                            reinterpret_cast<unsigned long long*>(b.scal + 2));                \
   } while (0)
     if (v4) {
       if (cpl == 1) ALTO_MEAN_CASE(4, 1);
@@ -1295,7 +1427,7 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
     }
 #undef ALTO_MEAN_CASE
     if (!x.defer_combine)
-      k_mean_combine<<<GRID_CAP, 256, 0, st>>>(b.chunks, NCp, b.part, dim, out.mean, out.cap_groups);
+      k_mean_combine<<<GRID_CAP, 256, 0, st>>>(b.chunks, NBp, b.part, dim, out.mean, out.cap_groups);
   }
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;

@@ -59,6 +59,8 @@ struct SegJob {
   const SortCtl* skip_ctl;  // nullable: every kernel returns at once when skip_ctl->dp (the sort
                             // placed the elements directly and set the group level itself)
   int32_t no_prep;          // the caller's previous kernel did seg_prep_device (one launch less)
+  int32_t fold_lo;          // the completion of the level-lo nodes is evaluated by the caller's
+                            // group kernel (no k_seg_nodes launch for level lo)
   uint2* gw;                // nullable, [cdiv(n_max, SEG_IT)]: for each run of SEG_IT elements from
                             // element r * SEG_IT, x = level-lo boundaries before the run, y = its
                             // boundary bits (bit i: element r * SEG_IT + i starts a level-lo node),

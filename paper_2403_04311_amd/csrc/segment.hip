@@ -67,10 +67,13 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
   // blocks past the tile count would only contend for tickets (the grid is sized
   // for the largest count, the count may be known on the device only)
   if ((int64_t)blockIdx.x >= ntiles) return;
+  bool first = true;
   while (true) {
-    if (threadIdx.x == 0) s_tile = atomicAdd(j.lb_ctr, 1u);
+    // a single tile is block 0's without a ticket (it waits for no other tile)
+    if (ntiles > 1 && threadIdx.x == 0) s_tile = atomicAdd(j.lb_ctr, 1u);
     __syncthreads();
-    const int64_t tile = (int64_t)__builtin_amdgcn_readfirstlane(s_tile);
+    const int64_t tile = ntiles > 1 ? (int64_t)__builtin_amdgcn_readfirstlane(s_tile) : (first ? 0 : 1);
+    first = false;
     if (tile >= ntiles) break;   // uniform across the block
     const int64_t e0 = tile * TILE + (int64_t)threadIdx.x * IT;
     uint64_t k[IT];
@@ -163,20 +166,32 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
       if (q >= K) continue;
       const int m = lo + q;
       const LevelNodes& L = j.lv[m];
-      for (uint32_t r = fl[q]; r; r &= r - 1) {
-        const int i = __builtin_ctz(r);
-        const int64_t e = e0 + i;
-        const uint32_t below = (1u << i) - 1u;
-        const int32_t id = base[q] + __popc(fl[q] & below);
-        L.start[id] = (int32_t)e;
-        // a boundary of this level is one of the next: the first child starts here
-        if (q + 1 < K) L.fc[id] = base[q + 1 < KM ? q + 1 : q] + __popc(fl[q + 1 < KM ? q + 1 : q] & below);
-        if (q > 0) L.par[id] = base[q > 0 ? q - 1 : 0] + __popc(fl[q > 0 ? q - 1 : 0] & (below | (1u << i))) - 1;
-        L.nfan[id] = fan_at(j, m, e);
-        L.bad[id] = 0;
-        if (q == 0 && j.carry_fan) {
-          for (int mm = j.carry_lo; mm < lo; ++mm)
-            j.carry_fan[(int64_t)(mm - j.carry_lo) * j.carry_ld + id] = fan_at(j, mm, e);
+      for (uint32_t r = fl[q]; r;) {
+        // up to four boundaries at a time, their declared fans loaded together
+        constexpr int NBF = 4;
+        int ib[NBF];
+        int nb = 0;
+        for (; r && nb < NBF; r &= r - 1) ib[nb++] = __builtin_ctz(r);
+        int32_t fb[NBF];
+#pragma unroll
+        for (int bq = 0; bq < NBF; ++bq) fb[bq] = bq < nb ? fan_at(j, m, e0 + ib[bq]) : 0;
+#pragma unroll
+        for (int bq = 0; bq < NBF; ++bq) {
+          if (bq >= nb) break;
+          const int i = ib[bq];
+          const int64_t e = e0 + i;
+          const uint32_t below = (1u << i) - 1u;
+          const int32_t id = base[q] + __popc(fl[q] & below);
+          L.start[id] = (int32_t)e;
+          // a boundary of this level is one of the next: the first child starts here
+          if (q + 1 < K) L.fc[id] = base[q + 1 < KM ? q + 1 : q] + __popc(fl[q + 1 < KM ? q + 1 : q] & below);
+          if (q > 0) L.par[id] = base[q > 0 ? q - 1 : 0] + __popc(fl[q > 0 ? q - 1 : 0] & (below | (1u << i))) - 1;
+          L.nfan[id] = fb[bq];
+          L.bad[id] = 0;
+          if (q == 0 && j.carry_fan) {
+            for (int mm = j.carry_lo; mm < lo; ++mm)
+              j.carry_fan[(int64_t)(mm - j.carry_lo) * j.carry_ld + id] = fan_at(j, mm, e);
+          }
         }
       }
       if (j.chain_check) {
@@ -302,7 +317,8 @@ int seg_run(const KeyGeom& g, SegJob& job, hipStream_t st) {
   else if (K <= 4) k_seg_pass<4><<<grid, NT, 0, st>>>(g, job);
   else k_seg_pass<ALTO_MAX_LEVELS><<<grid, NT, 0, st>>>(g, job);
   if (job.elem_ok) k_elem_bad<<<NODE_GRID, 256, 0, st>>>(job);
-  for (int m = job.elem_level - 1; m >= job.lo; --m) k_seg_nodes<<<NODE_GRID, 256, 0, st>>>(g, job, m);
+  for (int m = job.elem_level - 1; m >= job.lo + (job.fold_lo ? 1 : 0); --m)
+    k_seg_nodes<<<NODE_GRID, 256, 0, st>>>(g, job, m);
   ALTO_LAUNCH_CHECK();
   return ALTO_OK;
 }

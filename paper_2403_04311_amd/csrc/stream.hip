@@ -42,6 +42,10 @@ constexpr int LU_NT = 256;
 constexpr int LU_IT = 8;
 constexpr int LU_TILE = LU_NT * LU_IT;
 
+// sampled keys per run in the merge's LDS search
+constexpr int MERGE_SAMPLES = 2048;
+static_assert(MERGE_SAMPLES % 256 == 0, "whole sample rows per merge block");
+
 struct LiveSet {
   uint64_t* key;
   int32_t* p32;
@@ -82,6 +86,10 @@ __global__ void k_stream_begin(const StreamCtl* ctl, int32_t* status) {
 
 // Merge path: every element finds its place by binary search in the other run.
 // Live elements go before equal step keys (which are duplicates, reported later).
+// The searches start in LDS: each block that holds merged elements first copies
+// every s-th key of both runs (at most MERGE_SAMPLES of each, s the smallest stride
+// that fits), which narrows a search to s consecutive keys before it reads global
+// memory (log2 s dependent loads instead of log2 of the run length).
 // Also adds the live leaves' terms of the fan fingerprint.
 // Also, so that the step launches fewer kernels: reports a poisoned handle, finds
 // late fragments (their group is in the emitted set), writes the step's destination
@@ -121,6 +129,39 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   if (dest_offsets && n == 0 && gtid == 0)
     for (uint32_t x = 0; x <= rg.num_dest; ++x) dest_offsets[x] = 0;
   bool late = false;
+  // this thread's first element (loaded before the samples, which it does not need)
+  const int64_t t1 = gtid;
+  uint64_t k1 = 0;
+  uint32_t p1 = 0;
+  if (t1 < Lc) {
+    k1 = live.key[t1];
+  } else if (t1 < Lc + n) {
+    k1 = sk[t1 - Lc];
+    p1 = sperm[t1 - Lc];
+  }
+  // sampled keys of both runs: the step's every s1-th (c1 of them), the live set's
+  // every s2-th (c2); blocks past the merged run load none
+  __shared__ uint64_t s_sk[MERGE_SAMPLES], s_lk[MERGE_SAMPLES];
+  const int64_t s1 = n > MERGE_SAMPLES ? cdiv(n, MERGE_SAMPLES) : 1, c1 = cdiv(n, s1);
+  const int64_t s2 = Lc > MERGE_SAMPLES ? cdiv(Lc, MERGE_SAMPLES) : 1, c2 = cdiv(Lc, s2);
+  if ((int64_t)blockIdx.x * blockDim.x < Lc + n) {   // uniform across the block
+    // all of a thread's sample loads first (independent, in flight together)
+    constexpr int PER = MERGE_SAMPLES / 256;
+    uint64_t a[PER], b[PER];
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int64_t i = threadIdx.x + r * 256;
+      a[r] = i < c1 ? sk[i * s1] : 0ull;
+      b[r] = i < c2 ? live.key[i * s2] : 0ull;
+    }
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int64_t i = threadIdx.x + r * 256;
+      if (i < c1) s_sk[i] = a[r];
+      if (i < c2) s_lk[i] = b[r];
+    }
+    __syncthreads();
+  }
   const int nl = fhi - flo + 1;
   uint64_t fp[ALTO_MAX_LEVELS];
   int sh[ALTO_MAX_LEVELS];
@@ -131,31 +172,44 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   }
   for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < Lc + n; t += (int64_t)gridDim.x * blockDim.x) {
     if (t < Lc) {
-      const uint64_t k = live.key[t];
-      int64_t lo = 0, hi = n;   // number of step keys < k
+      const uint64_t k = t == t1 ? k1 : live.key[t];
+#pragma unroll
+      for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
+        if (q < nl)
+          fp[q] += fan_term(g.fkey, flo + q, key_prefix(k, sh[q]), (uint32_t)live.fan[(int64_t)(flo + q - 1) * cap + t]);
+      // number of step keys < k: c sampled ones, so between (c - 1) s1 + 1 and c s1
+      int64_t a = 0, b = c1;
+      while (a < b) {
+        const int64_t mid = (a + b) >> 1;
+        if (dk_less(rg, s_sk[mid], k)) a = mid + 1; else b = mid;
+      }
+      int64_t lo = a == 0 ? 0 : (a - 1) * s1 + 1, hi = a < c1 ? a * s1 : n;
       while (lo < hi) {
         const int64_t mid = (lo + hi) >> 1;
         if (dk_less(rg, sk[mid], k)) lo = mid + 1; else hi = mid;
       }
       mkey[t + lo] = k;
       msrc[t + lo] = (int32_t)(-1 - t);
-#pragma unroll
-      for (int q = 0; q < ALTO_MAX_LEVELS; ++q)
-        if (q < nl)
-          fp[q] += fan_term(g.fkey, flo + q, key_prefix(k, sh[q]), (uint32_t)live.fan[(int64_t)(flo + q - 1) * cap + t]);
     } else {
       const int64_t j = t - Lc;
-      const uint64_t k = sk[j];
-      int64_t lo = 0, hi = Lc;  // number of live keys <= k
+      const uint64_t k = t == t1 ? k1 : sk[j];
+      const uint32_t pj = t == t1 ? p1 : sperm[j];
+      late |= emitted_has(key_prefix(k, shiftLa), ht, htcap);
+      // number of live keys <= k: c sampled ones, so between (c - 1) s2 + 1 and c s2
+      int64_t a = 0, b = c2;
+      while (a < b) {
+        const int64_t mid = (a + b) >> 1;
+        if (!dk_less(rg, k, s_lk[mid])) a = mid + 1; else b = mid;
+      }
+      int64_t lo = a == 0 ? 0 : (a - 1) * s2 + 1, hi = a < c2 ? a * s2 : Lc;
       while (lo < hi) {
         const int64_t mid = (lo + hi) >> 1;
         if (!dk_less(rg, k, live.key[mid])) lo = mid + 1; else hi = mid;
       }
       mkey[j + lo] = k;
-      msrc[j + lo] = (int32_t)sperm[j];
-      if (perm_out) perm_out[j] = (int32_t)sperm[j];
-      if (dest_out) dest_out[sperm[j]] = (int32_t)dest_of_key(rg, k);
-      late |= emitted_has(key_prefix(k, shiftLa), ht, htcap);
+      msrc[j + lo] = (int32_t)pj;
+      if (perm_out) perm_out[j] = (int32_t)pj;
+      if (dest_out) dest_out[pj] = (int32_t)dest_of_key(rg, k);
       if (dest_offsets) {
         // the step's destination offsets, where the destination changes in its sorted keys
         const uint32_t d = dest_of_key(rg, k);
@@ -203,14 +257,26 @@ __device__ inline void stream_poison(StreamCtl* ctl, int32_t* status) {
 static_assert(SEG_IT % LU_IT == 0, "a thread's elements lie in one boundary word");
 
 // CONCAT: the same kernel also copies the emitted groups' tokens (the chunks that
-// k_group_out listed), one wave per chunk, in the blocks that have no tile (beside
-// the tiles, not after them); only when every block has a tile, after the tiles.
+// the group kernel listed), one wave per chunk, in the blocks that have no tile
+// (beside the tiles, not after them); only when every block has a tile, after the
+// tiles.
 struct ConcatJob {
-  const Chunk* chunks;
-  const int64_t* nchunks;
+  const Chunk* chunks;     // long groups' chunks
+  const int64_t* nlong;
+  const Chunk* chunks_s;   // short groups' chunks
+  const int64_t* nshort;
   MergedSrc src;
-  int32_t* tok;           // null: no concatenation here
+  int32_t* tok;            // null: no concatenation here
   int64_t cap_tokens;
+};
+
+// The fan fingerprint comparison when the group kernel accumulated the group
+// level's node terms itself (so it cannot compare them): done by the live-set
+// update's last tile, before it ends the step (levels lo..hi, in: null = none).
+struct FpCheck {
+  const uint64_t* in;
+  const uint64_t* nodes;
+  int32_t lo, hi;
 };
 
 template <int NFP>
@@ -221,7 +287,8 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
                                                        const int32_t* __restrict__ sp32,
                                                        const int32_t* __restrict__ sfan, int64_t sfan_ld, int mean,
                                                        int32_t* fslot, int64_t* alist, uint64_t* st, uint32_t* ctr,
-                                                       ConcatJob cj, int32_t* status) {
+                                                       ConcatJob cj, FpCheck fpc, int64_t max_emit,
+                                                       int32_t* status) {
   constexpr uint64_t F21 = (1ull << 21) - 1ull;   // a tile's counts fit 21 bits (LU_TILE < 2^21)
   const int64_t M = ctl->merged;
   const int64_t ntiles = cdiv(M, LU_TILE);
@@ -231,7 +298,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   __shared__ uint32_t s_tile;
   const int64_t idle = (int64_t)gridDim.x - ntiles;   // blocks without a tile
   if (cj.tok && idle > 0 && (int64_t)blockIdx.x >= ntiles)
-    concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nchunks, cj.src, cj.tok, cj.cap_tokens,
+    concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nlong, cj.chunks_s, *cj.nshort, cj.src, cj.tok, cj.cap_tokens,
                                   ((int64_t)blockIdx.x - ntiles) * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE,
                                   idle * (LU_NT / ALTO_WAVE));
   if (ntiles == 0) {
@@ -243,14 +310,28 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
     return;
   }
   if ((int64_t)blockIdx.x < ntiles) {
+    bool first = true;
     while (true) {
-      if (threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
+      // a single tile is block 0's without a ticket (it waits for no other tile)
+      if (ntiles > 1 && threadIdx.x == 0) s_tile = atomicAdd(ctr, 1u);
       __syncthreads();
-      const int64_t tile = (int64_t)s_tile;
+      const int64_t tile = ntiles > 1 ? (int64_t)s_tile : (first ? 0 : 1);
+      first = false;
       if (tile >= ntiles) break;   // uniform
       const int64_t e0 = tile * LU_TILE + (int64_t)threadIdx.x * LU_IT;
       int32_t ms[LU_IT];
       uint32_t km = 0, fm = 0, am = 0;   // bit i: element e0 + i is kept / frees a slot / needs one
+      // the fields of a kept element are loaded with the flags (they depend on its
+      // source only), and used only if it is kept
+      uint64_t kk[LU_IT];
+      int32_t pv[LU_IT], sv[LU_IT], fv[NFP > 0 ? NFP : 1][LU_IT];
+#pragma unroll
+      for (int i = 0; i < LU_IT; ++i) {
+        kk[i] = 0;
+        pv[i] = sv[i] = 0;
+#pragma unroll
+        for (int l = 0; l < NFP; ++l) fv[l][i] = 0;
+      }
       if (e0 < M) {
         if (e0 + LU_IT <= M) {
           const int4* p = reinterpret_cast<const int4*>(msrc + e0);
@@ -266,35 +347,37 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
 #pragma unroll
           for (int i = 0; i < LU_IT; ++i) ms[i] = e0 + i < M ? msrc[e0 + i] : 0;
         }
+#pragma unroll
+        for (int i = 0; i < LU_IT; ++i) kk[i] = e0 + i < M ? mkey[e0 + i] : 0ull;
         const uint2 w = gw[e0 / SEG_IT];
         const int off = (int)(e0 % SEG_IT);
         const uint32_t fs = w.y >> off;                                          // bit i: e0 + i starts a group
         const int32_t u0 = (int32_t)w.x + __popc(w.y & ((1u << off) - 1u));      // groups started before e0
+        bool okv[LU_IT];
+#pragma unroll
+        for (int i = 0; i < LU_IT; ++i) {
+          const int32_t u = u0 + __popc(fs & ((2u << i) - 1u)) - 1;
+          const bool in = e0 + i < M;
+          okv[i] = in && u >= 0 && L.ok[u];
+          if (!in) continue;
+          const int32_t s = ms[i];
+          const bool car = s < 0;
+          const int64_t li = -1 - (int64_t)s;
+          pv[i] = car ? old.p32[li] : (sp32 ? sp32[s] : 0);
+          sv[i] = (car && mean) ? old.slot[li] : 0;
+#pragma unroll
+          for (int l = 0; l < NFP; ++l)
+            fv[l][i] = car ? old.fan[(int64_t)l * cap + li] : sfan[(int64_t)l * sfan_ld + s];
+        }
 #pragma unroll
         for (int i = 0; i < LU_IT; ++i) {
           if (e0 + i >= M) break;
-          const int32_t u = u0 + __popc(fs & ((2u << i) - 1u)) - 1;
-          const bool ok = u >= 0 && L.ok[u];
+          const bool ok = okv[i];
           const bool carried = ms[i] < 0;
           km |= (ok ? 0u : 1u) << i;
           fm |= ((mean && ok && carried) ? 1u : 0u) << i;
           am |= ((mean && !ok && !carried) ? 1u : 0u) << i;
         }
-      }
-      uint64_t kk[LU_IT];
-      int32_t pv[LU_IT], sv[LU_IT], fv[NFP > 0 ? NFP : 1][LU_IT];
-#pragma unroll
-      for (int i = 0; i < LU_IT; ++i) {
-        const bool kept = (km >> i) & 1u;
-        const int32_t s = ms[i];
-        const bool car = s < 0;
-        const int64_t li = -1 - (int64_t)s;
-        kk[i] = kept ? mkey[e0 + i] : 0ull;
-        pv[i] = kept ? (car ? old.p32[li] : (sp32 ? sp32[s] : 0)) : 0;
-        sv[i] = (car && (kept || ((fm >> i) & 1u)) && mean) ? old.slot[li] : 0;
-#pragma unroll
-        for (int l = 0; l < NFP; ++l)
-          fv[l][i] = kept ? (car ? old.fan[(int64_t)l * cap + li] : sfan[(int64_t)l * sfan_ld + s]) : 0;
       }
       const uint64_t c = (uint64_t)__popc(km) | ((uint64_t)__popc(fm) << 21) | ((uint64_t)__popc(am) << 42);
       uint64_t tot;
@@ -310,6 +393,10 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
             const int64_t T = (int64_t)(exq + tq);
             if (wv == 0) {
               if (T > cap) raise_status(status, ALTO_E_CAPACITY);
+              if (ctl->emitted > max_emit) raise_status(status, ALTO_E_CAPACITY);   // the emitted set's limit
+              if (fpc.in)
+                for (int m = fpc.lo; m <= fpc.hi; ++m)
+                  if (fpc.in[m] != fpc.nodes[m]) raise_status(status, ALTO_E_FANOUT);
               ctl->live = T > cap ? cap : T;   // read by the next step only
               if (!mean) stream_poison(ctl, status);
             } else {
@@ -360,7 +447,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
       __syncthreads();   // s_ex and the ticket are reused by the next tile
     }
     if (cj.tok && idle <= 0)
-      concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nchunks, cj.src, cj.tok, cj.cap_tokens,
+      concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nlong, cj.chunks_s, *cj.nshort, cj.src, cj.tok, cj.cap_tokens,
                                     (int64_t)blockIdx.x * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE,
                                     (int64_t)gridDim.x * (LU_NT / ALTO_WAVE));
   }
@@ -755,6 +842,9 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   j.status = status;
   j.no_prep = 1;   // done by the merge
   j.gw = b.gw;
+  // the group kernel evaluates the group level's completion (with in-order release,
+  // the release kernels read it before the scan)
+  j.fold_lo = s->pht ? 0 : 1;
   // 2. merge with the live set (also: late fragments, a poisoned handle, the step's
   // destination offsets, the clearing of the step's look-back words)
   k_merge<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc,
@@ -827,10 +917,22 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   }
   ex.ht = s->ht;
   ex.htcap = s->htcap;
-  ex.max_emit = s->max_groups;
   ex.emit_count = &s->ctl->emitted;
   ex.defer_concat = mean ? 0 : 1;   // the live-set update copies the tokens
   ex.defer_combine = mean ? 1 : 0;  // the arena-slot kernel combines the chunks
+  FpCheck fpc{nullptr, nullptr, 0, -1};
+  if (j.fold_lo) {
+    // the group kernel adds the group level's node terms: the comparison waits for
+    // the live-set update
+    fpc = FpCheck{b.fp_in, b.fp_nodes, La, d - 1};
+    ex.fp_in = nullptr;
+    ex.fold = 1;
+    ex.fold_leafy = La + 1 == d ? 1 : 0;
+    ex.fold_level = La;
+    ex.fold_es = g.shift[La] - g.shift[d];
+    ex.fold_keys = mkey;
+    ex.fold_fp = b.fp_nodes;
+  }
   rc = groups_run<MergedSrc>(g, s->rg, agg, src, mkey, ntot, b, nullptr, o, status, st, &ex);
   if (rc) return rc;
   // 5. survivors become the new live set
@@ -842,7 +944,9 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
     memset(&cj, 0, sizeof(cj));
     if (!mean && o.tok) {
       cj.chunks = b.chunks;
-      cj.nchunks = b.scal + 1;
+      cj.nlong = b.scal + 1;
+      cj.chunks_s = b.chunks + b.short_base;
+      cj.nshort = b.scal + 3;
       cj.src = src;
       cj.tok = o.tok;
       cj.cap_tokens = o.cap_tokens;
@@ -850,7 +954,8 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
 #define ALTO_LU_CASE(P)                                                                                          \
   k_live_update<P><<<grid_for(ntot, LU_TILE, 1024), LU_NT, 0, st>>>(g, b.lv[La], b.gw, mkey, msrc, s->ctl, s->cap, \
                                                                    old, nw, payload_i32, fan, fan_ld, mean ? 1 : 0, \
-                                                                   fslot, alist, lst, b.os_ctr + 2, cj, status)
+                                                                   fslot, alist, lst, b.os_ctr + 2, cj, fpc,      \
+                                                                   s->max_groups, status)
     if (nf <= 1) ALTO_LU_CASE(1);
     else if (nf == 2) ALTO_LU_CASE(2);
     else ALTO_LU_CASE(3);
