@@ -398,36 +398,54 @@ def bench_tokens(args):
         tot, per = _stream_run(nsteps, one)
         s.close()
         return tot, per
-    def run_overlapped():
+    def run_overlapped(per_step=True):
         # each step's routing on a second HIP stream, beside the previous step's merge
-        # and emission (alto_stream_step_overlap)
+        # and emission (alto_stream_step_overlap); per_step: an event pair per step
+        # (which itself costs a few microseconds on each stream), else one around all
         s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step,
                         release=args.release)
         main = torch.cuda.current_stream()
         route = route_stream
         route.wait_stream(main)
-        t0 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
-        t1 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
+        k = nsteps if per_step else 1
+        t0 = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+        t1 = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
         for i in range(nsteps):
             a, b = i * step, min(n, (i + 1) * step)
-            t0[i].record(route)
+            if per_step or i == 0:
+                t0[i if per_step else 0].record(route)
             s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status, stream=main,
                    route_stream=route)
-            t1[i].record(main)
+            if per_step or i == nsteps - 1:
+                t1[i if per_step else 0].record(main)
         main.wait_stream(route)
         torch.cuda.synchronize()
         s.close()
-        lat = [t0[i].elapsed_time(t1[i]) for i in range(nsteps)]
-        period = [t1[i - 1].elapsed_time(t1[i]) for i in range(1, nsteps)]
-        return t0[0].elapsed_time(t1[nsteps - 1]), lat, period
+        lat = [t0[i].elapsed_time(t1[i]) for i in range(k)] if per_step else []
+        period = [t1[i - 1].elapsed_time(t1[i]) for i in range(1, k)]
+        return t0[0].elapsed_time(t1[k - 1]), lat, period
     route_stream = torch.cuda.Stream()
-    for _ in range(max(args.warmup, 1)):
+    # the stream is short (96 steps, a few ms): many runs, so that the GPU clock
+    # settles first and the percentiles pool enough steps
+    reps, warm = 10, max(args.warmup, 20)
+    for _ in range(warm):
         run()
-    seq_tot, seq_per = run()
+    seq_per = []
+    seq_tot = 0.0
+    for _ in range(reps):
+        t, p = run()
+        seq_tot += t / reps
+        seq_per += p
     assert int(status.item()) == 0
-    for _ in range(max(args.warmup, 1)):
+    for _ in range(warm):
         run_overlapped()
-    tot, lat, period = run_overlapped()
+    tot, lat, period = 0.0, [], []
+    for _ in range(reps):
+        t, l, p = run_overlapped()
+        tot += t / reps
+        lat += l
+        period += p
+    bare = sum(run_overlapped(per_step=False)[0] for _ in range(reps)) / reps
     assert int(status.item()) == 0
     ms = tot / nsteps
     path_bytes = (n * (8 + 4 + 4 + 4 + 4 + 4) + 16384 * (8 + 4 + 8 + 4 + 8)) / nsteps
@@ -438,7 +456,9 @@ def bench_tokens(args):
                  path_bytes, {"stream_fragments": n, "stream_ms": tot,
                               "step_ms_p50": _pct(period, 50), "step_ms_p99": _pct(period, 99),
                               "step_ms_max": max(period),
-                              "step_ms_note": "p50/p99/max of the period between consecutive steps' ends",
+                              "step_ms_note": "p50/p99/max of the period between consecutive steps' ends, "
+                                              f"{reps} runs of {nsteps} steps pooled, an event pair per step",
+                              "uninstrumented_ms_per_step": bare / nsteps,
                               "step_latency_ms_p50": _pct(lat, 50), "step_latency_ms_p99": _pct(lat, 99),
                               "sequential_ms_per_step": seq_tot / nsteps, "sequential_step_ms_p50": _pct(seq_per, 50),
                               "sequential_step_ms_p99": _pct(seq_per, 99)})

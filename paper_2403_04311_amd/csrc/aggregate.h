@@ -259,16 +259,13 @@ __device__ inline void mean_combine_chunks(const Chunk* __restrict__ chunks, int
 }
 
 // Inserts a group key into the emitted set: 1 = new, 0 = present, -1 = table full.
+// Each probe is one compare-and-swap (no load first: one round trip per slot).
 __device__ inline int emitted_insert(uint64_t gk, uint64_t* ht, int64_t htcap) {
   int64_t h = (int64_t)(mix64(gk) & (uint64_t)(htcap - 1));
   for (int64_t p = 0; p < htcap; ++p) {
-    const uint64_t v = ht[h];
-    if (v == gk) return 0;
-    if (v == EMIT_EMPTY) {
-      const uint64_t old = atomicCAS((unsigned long long*)&ht[h], (unsigned long long)EMIT_EMPTY, (unsigned long long)gk);
-      if (old == EMIT_EMPTY) return 1;
-      if (old == gk) return 0;
-    }
+    const uint64_t old = atomicCAS((unsigned long long*)&ht[h], (unsigned long long)EMIT_EMPTY, (unsigned long long)gk);
+    if (old == EMIT_EMPTY) return 1;
+    if (old == gk) return 0;
     h = (h + 1) & (htcap - 1);
   }
   return -1;

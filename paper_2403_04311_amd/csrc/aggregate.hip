@@ -521,12 +521,43 @@ struct GroupFold {
   uint64_t* fp;   // nullable: fingerprint sums per level
 };
 
+// The node fields a thread of the group kernel reads for its groups of a tile
+// (group g0 + k GS_NT + threadIdx.x for k < GS_IT), below bound.
+struct GroupTileLoad {
+  int32_t sv[GS_IT], sn[GS_IT], cv[GS_IT], cn[GS_IT], nf[GS_IT];
+  uint8_t bd[GS_IT], okf[GS_IT];
+  uint64_t nk[GS_IT];   // first keys, when the pass recorded them
+};
+
+__device__ inline void group_tile_load(const LevelNodes& L, const GroupFold& f, int64_t g0, int64_t bound,
+                                       GroupTileLoad& t) {
+#pragma unroll
+  for (int k = 0; k < GS_IT; ++k) {
+    const int64_t u = g0 + k * GS_NT + threadIdx.x;
+    const bool in = u < bound;
+    t.sv[k] = in ? L.start[u] : 0;
+    t.sn[k] = in ? L.start[u + 1] : 0;
+    t.cv[k] = (in && f.on && !f.leafy) ? L.fc[u] : 0;
+    t.cn[k] = (in && f.on && !f.leafy) ? L.fc[u + 1] : 0;
+    t.nf[k] = (in && f.on) ? L.nfan[u] : 0;
+    t.bd[k] = (in && f.on) ? L.bad[u] : 1;
+    t.okf[k] = (in && !f.on) ? L.ok[u] : 0;
+    t.nk[k] = (in && L.nkey) ? L.nkey[u] : 0ull;
+  }
+}
+
 template <typename Src>
 __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int La, LevelNodes L, const int64_t* Gp,
                                                   const uint64_t* __restrict__ sk, Src src, Chunk* chunks,
                                                   int64_t short_base, int chunk_rows, GroupOut out, int concat,
                                                   const int64_t* Mp, int64_t* scal, GroupsExtra ex, uint64_t* st,
-                                                  uint32_t* ctr, GroupFold f, int32_t* status) {
+                                                  uint32_t* ctr, GroupFold f, int64_t ucap, int32_t* status) {
+  // the fields of the tile this block most likely takes first (its own index),
+  // loaded before the group count and the ticket have arrived (the node arrays
+  // hold ucap + 1 entries; groups past the count are not used)
+  const int64_t gt = blockIdx.x;
+  GroupTileLoad pre;
+  group_tile_load(L, f, gt * GS_TILE, ucap, pre);
   const int64_t G = *Gp;
   const int64_t ntiles = cdiv(G + 1, GS_TILE);
   __shared__ int64_t s_w[GS_NT / ALTO_WAVE];
@@ -564,21 +595,19 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
       // complete: as many children as declared, none of them incomplete. Every load
       // first, then the flags, fingerprint terms and stores; the scan reads the
       // flags and row counts back from LDS.
-      int32_t sn[GS_IT], cv[GS_IT], cn[GS_IT], nf[GS_IT];
-      uint8_t bd[GS_IT];
+      GroupTileLoad t;
+      if (tile == gt) t = pre;
+      else group_tile_load(L, f, g0, G, t);
+      const int32_t* sn = t.sn;
+      const int32_t* cv = t.cv;
+      const int32_t* cn = t.cn;
+      const int32_t* nf = t.nf;
+      const uint8_t* bd = t.bd;
 #pragma unroll
-      for (int k = 0; k < GS_IT; ++k) {
-        const int64_t u = g0 + k * GS_NT + threadIdx.x;
-        const bool in = u < G;
-        sv[k] = in ? L.start[u] : 0;
-        sn[k] = in ? L.start[u + 1] : 0;
-        cv[k] = (in && !f.leafy) ? L.fc[u] : 0;
-        cn[k] = (in && !f.leafy) ? L.fc[u + 1] : 0;
-        nf[k] = in ? L.nfan[u] : 0;
-        bd[k] = in ? L.bad[u] : 1;
-      }
+      for (int k = 0; k < GS_IT; ++k) sv[k] = t.sv[k];
 #pragma unroll
-      for (int k = 0; k < GS_IT; ++k) kk[k] = g0 + k * GS_NT + threadIdx.x < G ? f.keys[sv[k]] : 0ull;
+      for (int k = 0; k < GS_IT; ++k)
+        kk[k] = g0 + k * GS_NT + threadIdx.x < G ? (L.nkey ? t.nk[k] : f.keys[sv[k]]) : 0ull;
 #pragma unroll
       for (int k = 0; k < GS_IT; ++k) {
         const int64_t u = g0 + k * GS_NT + threadIdx.x;
@@ -604,20 +633,19 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
         cnv[i] = s_cnt[idx];
       }
     } else {
-      int32_t sn[GS_IT];
+      GroupTileLoad t;
+      if (tile == gt) t = pre;
+      else group_tile_load(L, f, g0, G, t);
 #pragma unroll
       for (int k = 0; k < GS_IT; ++k) {
-        const int64_t u = g0 + k * GS_NT + threadIdx.x;
-        const bool in = u < G;
-        sv[k] = in ? L.start[u] : 0;
-        sn[k] = in ? L.start[u + 1] : 0;
-        s_okf[k * GS_NT + threadIdx.x] = (in && L.ok[u]) ? 1 : 0;
+        const bool in = g0 + k * GS_NT + threadIdx.x < G;
+        sv[k] = t.sv[k];
+        s_okf[k * GS_NT + threadIdx.x] = (in && t.okf[k]) ? 1 : 0;
+        s_cnt[k * GS_NT + threadIdx.x] = in ? t.sn[k] - t.sv[k] : 0;
       }
 #pragma unroll
-      for (int k = 0; k < GS_IT; ++k) {
-        kk[k] = g0 + k * GS_NT + threadIdx.x < G ? sk[sv[k]] : 0ull;
-        s_cnt[k * GS_NT + threadIdx.x] = sn[k] - sv[k];
-      }
+      for (int k = 0; k < GS_IT; ++k)
+        kk[k] = g0 + k * GS_NT + threadIdx.x < G ? (L.nkey ? t.nk[k] : sk[sv[k]]) : 0ull;
       __syncthreads();
 #pragma unroll
       for (int i = 0; i < GS_IT; ++i) {
@@ -1377,7 +1405,7 @@ int groups_run(const KeyGeom& g, const RouteGeom& rg, const alto_agg& agg, const
     GroupFold f{x.fold, x.fold_leafy, x.fold_level, x.fold_es, g.fkey, x.fold_keys, x.fold_fp};
     k_groups<Src><<<grid_for(n + 1, GS_TILE, 1024), GS_NT, 0, st>>>(
         g, rg, La, GL, Gp, sk, src, b.chunks, b.short_base, MEAN_CHUNK_ROWS, out, agg.op == ALTO_CONCAT_I32 ? 1 : 0,
-        Mp, b.scal, x, gst, gctr, f, status);
+        Mp, b.scal, x, gst, gctr, f, n, status);
   }
   ALTO_LAUNCH_CHECK();
   prof_end(PH_GROUPS, st);

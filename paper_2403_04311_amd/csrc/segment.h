@@ -5,7 +5,7 @@
 #include "sort.h"
 
 #define SEG_NT 512
-#define SEG_IT 32                      // consecutive elements per thread (fewer, larger tiles: fewer look-back rounds)
+#define SEG_IT 8                       // consecutive elements per thread (a small merged run still spreads over several blocks)
 #define SEG_TILE (SEG_NT * SEG_IT)
 #define SEG_LB_STRIDE ALTO_MAX_LEVELS  // look-back words per tile (one per level)
 #define NODE_GRID 512
@@ -18,6 +18,7 @@ struct LevelNodes {
   int32_t* nfan;    // [N] declared child count (from the node's first element)
   uint8_t* ok;      // [N] 1 = the node's whole subtree is present
   uint8_t* bad;     // [N] set when some child is incomplete
+  uint64_t* nkey;   // [N] nullable: key of each node's first element (written by the pass)
 };
 
 // One segmentation run over elements sorted so that every node of the levels
@@ -59,6 +60,8 @@ struct SegJob {
   const SortCtl* skip_ctl;  // nullable: every kernel returns at once when skip_ctl->dp (the sort
                             // placed the elements directly and set the group level itself)
   int32_t no_prep;          // the caller's previous kernel did seg_prep_device (one launch less)
+  int32_t prefetch;         // keys holds n_max elements: the pass may load a tile's keys before
+                            // it knows the count
   int32_t fold_lo;          // the completion of the level-lo nodes is evaluated by the caller's
                             // group kernel (no k_seg_nodes launch for level lo)
   uint2* gw;                // nullable, [cdiv(n_max, SEG_IT)]: for each run of SEG_IT elements from

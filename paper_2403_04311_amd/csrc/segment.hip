@@ -64,6 +64,27 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
   for (int q = 0; q < KM; ++q) es[q] = q < K ? es_of(g, j, lo + q) : 64;
   const int lane = lane_id();
   const bool vec_ok = (reinterpret_cast<uintptr_t>(j.keys) & 15) == 0;
+  // with j.prefetch, the keys of the tile this block most likely takes first (its
+  // own index) are loaded before the element count and the ticket have arrived
+  // (within the key buffer's n_max elements; those past the count are masked)
+  const int64_t gt = blockIdx.x;
+  uint64_t kg[IT], pg = 0;
+  if (j.prefetch) {
+    const int64_t eg = gt * TILE + (int64_t)threadIdx.x * IT;
+    if (vec_ok && eg + IT <= j.n_max) {
+      const ulonglong2* p = reinterpret_cast<const ulonglong2*>(j.keys + eg);
+#pragma unroll
+      for (int i = 0; i < IT / 2; ++i) {
+        const ulonglong2 v = p[i];
+        kg[2 * i] = v.x;
+        kg[2 * i + 1] = v.y;
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < IT; ++i) kg[i] = eg + i < j.n_max ? j.keys[eg + i] : 0ull;
+    }
+    if (lane == 0 && eg > 0 && eg - 1 < j.n_max) pg = j.keys[eg - 1];
+  }
   // blocks past the tile count would only contend for tickets (the grid is sized
   // for the largest count, the count may be known on the device only)
   if ((int64_t)blockIdx.x >= ntiles) return;
@@ -77,7 +98,11 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
     if (tile >= ntiles) break;   // uniform across the block
     const int64_t e0 = tile * TILE + (int64_t)threadIdx.x * IT;
     uint64_t k[IT];
-    if (vec_ok && e0 + IT <= n) {
+    const bool pre = j.prefetch && tile == gt;   // uniform
+    if (pre) {
+#pragma unroll
+      for (int i = 0; i < IT; ++i) k[i] = e0 + i < n ? kg[i] : 0ull;
+    } else if (vec_ok && e0 + IT <= n) {
       const ulonglong2* p = reinterpret_cast<const ulonglong2*>(j.keys + e0);
 #pragma unroll
       for (int i = 0; i < IT / 2; ++i) {
@@ -90,7 +115,7 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
       for (int i = 0; i < IT; ++i) k[i] = e0 + i < n ? j.keys[e0 + i] : 0ull;
     }
     uint64_t prev = __shfl_up(k[IT - 1], 1);
-    if (lane == 0) prev = (e0 > 0 && e0 - 1 < n) ? j.keys[e0 - 1] : 0ull;
+    if (lane == 0) prev = (e0 > 0 && e0 - 1 < n) ? (pre ? pg : j.keys[e0 - 1]) : 0ull;
     // boundary bits of this thread's elements per level (bit i = element e0 + i),
     // route-prefix changes, duplicate keys
     uint32_t fl[KM];
@@ -169,15 +194,18 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
       for (uint32_t r = fl[q]; r;) {
         // up to four boundaries at a time, their declared fans loaded together
         constexpr int NBF = 4;
-        int ib[NBF];
-        int nb = 0;
-        for (; r && nb < NBF; r &= r - 1) ib[nb++] = __builtin_ctz(r);
-        int32_t fb[NBF];
-#pragma unroll
-        for (int bq = 0; bq < NBF; ++bq) fb[bq] = bq < nb ? fan_at(j, m, e0 + ib[bq]) : 0;
+        int ib[NBF];   // element offsets of the next boundaries (-1: none)
 #pragma unroll
         for (int bq = 0; bq < NBF; ++bq) {
-          if (bq >= nb) break;
+          ib[bq] = r ? __builtin_ctz(r) : -1;
+          r &= r - 1;
+        }
+        int32_t fb[NBF];
+#pragma unroll
+        for (int bq = 0; bq < NBF; ++bq) fb[bq] = ib[bq] >= 0 ? fan_at(j, m, e0 + ib[bq]) : 0;
+#pragma unroll
+        for (int bq = 0; bq < NBF; ++bq) {
+          if (ib[bq] < 0) break;
           const int i = ib[bq];
           const int64_t e = e0 + i;
           const uint32_t below = (1u << i) - 1u;
@@ -188,6 +216,7 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
           if (q > 0) L.par[id] = base[q > 0 ? q - 1 : 0] + __popc(fl[q > 0 ? q - 1 : 0] & (below | (1u << i))) - 1;
           L.nfan[id] = fb[bq];
           L.bad[id] = 0;
+          if (L.nkey) L.nkey[id] = k[i];
           if (q == 0 && j.carry_fan) {
             for (int mm = j.carry_lo; mm < lo; ++mm)
               j.carry_fan[(int64_t)(mm - j.carry_lo) * j.carry_ld + id] = fan_at(j, mm, e);

@@ -287,9 +287,26 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
                                                        const int32_t* __restrict__ sp32,
                                                        const int32_t* __restrict__ sfan, int64_t sfan_ld, int mean,
                                                        int32_t* fslot, int64_t* alist, uint64_t* st, uint32_t* ctr,
-                                                       ConcatJob cj, FpCheck fpc, int64_t max_emit,
+                                                       ConcatJob cj, FpCheck fpc, int64_t max_emit, int64_t ncap,
                                                        int32_t* status) {
   constexpr uint64_t F21 = (1ull << 21) - 1ull;   // a tile's counts fit 21 bits (LU_TILE < 2^21)
+  // the sources, keys and boundary word of the tile this block most likely takes
+  // first (its own index), loaded before the merged count and the ticket have
+  // arrived (the merged run's buffers hold ncap elements; those past the count are
+  // not used)
+  const int64_t gt = blockIdx.x;
+  int32_t msg[LU_IT];
+  uint64_t kkg[LU_IT];
+  uint2 wg = make_uint2(0u, 0u);
+  {
+    const int64_t eg = gt * LU_TILE + (int64_t)threadIdx.x * LU_IT;
+#pragma unroll
+    for (int i = 0; i < LU_IT; ++i) {
+      msg[i] = eg + i < ncap ? msrc[eg + i] : 0;
+      kkg[i] = eg + i < ncap ? mkey[eg + i] : 0ull;
+    }
+    if (eg < ncap) wg = gw[eg / SEG_IT];
+  }
   const int64_t M = ctl->merged;
   const int64_t ntiles = cdiv(M, LU_TILE);
   const int nf = g.depth - 1;
@@ -333,23 +350,34 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
         for (int l = 0; l < NFP; ++l) fv[l][i] = 0;
       }
       if (e0 < M) {
-        if (e0 + LU_IT <= M) {
-          const int4* p = reinterpret_cast<const int4*>(msrc + e0);
+        const bool pre = tile == gt;   // uniform
+        uint2 w;
+        if (pre) {
 #pragma unroll
-          for (int v = 0; v < LU_IT / 4; ++v) {
-            const int4 q = p[v];
-            ms[4 * v] = q.x;
-            ms[4 * v + 1] = q.y;
-            ms[4 * v + 2] = q.z;
-            ms[4 * v + 3] = q.w;
+          for (int i = 0; i < LU_IT; ++i) {
+            ms[i] = e0 + i < M ? msg[i] : 0;
+            kk[i] = e0 + i < M ? kkg[i] : 0ull;
           }
+          w = wg;
         } else {
+          if (e0 + LU_IT <= M) {
+            const int4* p = reinterpret_cast<const int4*>(msrc + e0);
 #pragma unroll
-          for (int i = 0; i < LU_IT; ++i) ms[i] = e0 + i < M ? msrc[e0 + i] : 0;
+            for (int v = 0; v < LU_IT / 4; ++v) {
+              const int4 q = p[v];
+              ms[4 * v] = q.x;
+              ms[4 * v + 1] = q.y;
+              ms[4 * v + 2] = q.z;
+              ms[4 * v + 3] = q.w;
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < LU_IT; ++i) ms[i] = e0 + i < M ? msrc[e0 + i] : 0;
+          }
+#pragma unroll
+          for (int i = 0; i < LU_IT; ++i) kk[i] = e0 + i < M ? mkey[e0 + i] : 0ull;
+          w = gw[e0 / SEG_IT];
         }
-#pragma unroll
-        for (int i = 0; i < LU_IT; ++i) kk[i] = e0 + i < M ? mkey[e0 + i] : 0ull;
-        const uint2 w = gw[e0 / SEG_IT];
         const int off = (int)(e0 % SEG_IT);
         const uint32_t fs = w.y >> off;                                          // bit i: e0 + i starts a group
         const int32_t u0 = (int32_t)w.x + __popc(w.y & ((1u << off) - 1u));      // groups started before e0
@@ -845,6 +873,13 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   // the group kernel evaluates the group level's completion (with in-order release,
   // the release kernels read it before the scan)
   j.fold_lo = s->pht ? 0 : 1;
+  j.prefetch = 1;   // mkey holds ntot = n_max keys
+  if (j.fold_lo) {
+    // the pass records each group's first key for the group kernel, in the step's
+    // sorted-key buffer (free once the merge has read it)
+    b.lv[La].nkey = b.sk;
+    j.lv[La].nkey = b.sk;
+  }
   // 2. merge with the live set (also: late fragments, a poisoned handle, the step's
   // destination offsets, the clearing of the step's look-back words)
   k_merge<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc,
@@ -955,7 +990,7 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   k_live_update<P><<<grid_for(ntot, LU_TILE, 1024), LU_NT, 0, st>>>(g, b.lv[La], b.gw, mkey, msrc, s->ctl, s->cap, \
                                                                    old, nw, payload_i32, fan, fan_ld, mean ? 1 : 0, \
                                                                    fslot, alist, lst, b.os_ctr + 2, cj, fpc,      \
-                                                                   s->max_groups, status)
+                                                                   s->max_groups, ntot, status)
     if (nf <= 1) ALTO_LU_CASE(1);
     else if (nf == 2) ALTO_LU_CASE(2);
     else ALTO_LU_CASE(3);
