@@ -495,6 +495,7 @@ constexpr int GS_IT = 4;
 constexpr int GS_TILE = GS_NT * GS_IT;
 static_assert(GS_TILE == GROUP_SCAN_TILE, "group scan tile");
 static_assert(GS_IT <= 32, "a thread's groups in one flag word");
+static_assert(GS_NT * GS_IT < (1 << 21), "a tile's group counts fit 21 bits");
 
 constexpr int GS_NV = GROUP_SCAN_WORDS;   // scanned values per group
 
@@ -560,7 +561,7 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
   group_tile_load(L, f, gt * GS_TILE, ucap, pre);
   const int64_t G = *Gp;
   const int64_t ntiles = cdiv(G + 1, GS_TILE);
-  __shared__ int64_t s_w[GS_NT / ALTO_WAVE];
+  __shared__ uint64_t s_w[GS_NT / ALTO_WAVE];
   __shared__ int64_t s_ex[GS_NV];
   __shared__ uint32_t s_tile;
   // per group of the tile: the fold's flags and row counts, then the exclusive sums
@@ -668,9 +669,27 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
 #pragma unroll
       for (int q = 0; q < GS_NV; ++q) sum[q] += v[i][q];
     }
+    // two block scans of packed words: emitted groups, short groups and long-group
+    // chunks in 21-bit fields (a tile holds GS_TILE < 2^21 groups and fewer than
+    // 2^31 / MEAN_CHUNK_ROWS + GS_TILE < 2^21 chunks), rows (below 2^31) and partial
+    // slots (below 2^21) in 32-bit fields: no field carries into the next
+    constexpr uint64_t F21 = (1ull << 21) - 1ull, F32 = (1ull << 32) - 1ull;
+    const uint64_t wa = (uint64_t)sum[0] | ((uint64_t)sum[4] << 21) | ((uint64_t)sum[2] << 42);
+    const uint64_t wb = (uint64_t)sum[1] | ((uint64_t)sum[3] << 32);
+    uint64_t ta, tb;
+    const uint64_t xa = block_excl_scan<uint64_t, GS_NT>(wa, s_w, &ta);
+    const uint64_t xb = block_excl_scan<uint64_t, GS_NT>(wb, s_w, &tb);
     int64_t exs[GS_NV], tot[GS_NV];
-#pragma unroll
-    for (int q = 0; q < GS_NV; ++q) exs[q] = block_excl_scan<int64_t, GS_NT>(sum[q], s_w, &tot[q]);
+    exs[0] = (int64_t)(xa & F21);
+    exs[1] = (int64_t)(xb & F32);
+    exs[2] = (int64_t)(xa >> 42);
+    exs[3] = (int64_t)(xb >> 32);
+    exs[4] = (int64_t)((xa >> 21) & F21);
+    tot[0] = (int64_t)(ta & F21);
+    tot[1] = (int64_t)(tb & F32);
+    tot[2] = (int64_t)(ta >> 42);
+    tot[3] = (int64_t)(tb >> 32);
+    tot[4] = (int64_t)((ta >> 21) & F21);
     if (threadIdx.x < GS_NV) {
       const int q = threadIdx.x;
       int64_t t = tot[0];

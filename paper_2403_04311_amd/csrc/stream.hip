@@ -261,14 +261,34 @@ static_assert(SEG_IT % LU_IT == 0, "a thread's elements lie in one boundary word
 // (beside the tiles, not after them); only when every block has a tile, after the
 // tiles.
 struct ConcatJob {
-  const Chunk* chunks;     // long groups' chunks
+  const Chunk* chunks;     // long groups' chunks (long_cap entries)
   const int64_t* nlong;
-  const Chunk* chunks_s;   // short groups' chunks
+  const Chunk* chunks_s;   // short groups' chunks (short_cap entries)
   const int64_t* nshort;
+  int64_t long_cap, short_cap;
   MergedSrc src;
   int32_t* tok;            // null: no concatenation here
   int64_t cap_tokens;
 };
+
+// The concatenation by the blocks without a tile: wave cw of nw (numbered from the
+// grid's end) copies chunks cw, cw + nw, ... of the long then the short groups;
+// its first chunk was loaded before the counts were known (c0l = chunks[cw],
+// c0s = chunks_s[cw]: used when the counts place chunk cw there).
+__device__ inline void concat_role(const ConcatJob& cj, int64_t cw, int64_t nw, const Chunk& c0l, const Chunk& c0s) {
+  const int64_t NB = *cj.nlong, NS = *cj.nshort;
+  const int lane = lane_id();
+  for (int64_t c = cw; c < NB + NS; c += nw) {
+    Chunk ch;
+    if (c == cw && c < NB) ch = c0l;
+    else if (c == cw && NB == 0) ch = c0s;
+    else ch = c < NB ? cj.chunks[c] : cj.chunks_s[c - NB];
+    for (int r = lane; r < ch.len; r += ALTO_WAVE) {
+      const int64_t o = ch.out + r;
+      if (o < cj.cap_tokens) cj.tok[o] = cj.src.p32_of(cj.src.row(ch.begin + r));
+    }
+  }
+}
 
 // The fan fingerprint comparison when the group kernel accumulated the group
 // level's node terms itself (so it cannot compare them): done by the live-set
@@ -295,6 +315,13 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   // arrived (the merged run's buffers hold ncap elements; those past the count are
   // not used)
   const int64_t gt = blockIdx.x;
+  // the first chunk of this block's waves in the concatenation, if it has no tile
+  const int64_t cw = ((int64_t)gridDim.x - 1 - (int64_t)blockIdx.x) * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE;
+  Chunk c0l{}, c0s{};
+  if (cj.tok) {
+    if (cw < cj.long_cap) c0l = cj.chunks[cw];
+    if (cw < cj.short_cap) c0s = cj.chunks_s[cw];
+  }
   int32_t msg[LU_IT];
   uint64_t kkg[LU_IT];
   uint2 wg = make_uint2(0u, 0u);
@@ -314,10 +341,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   __shared__ int64_t s_ex[3];
   __shared__ uint32_t s_tile;
   const int64_t idle = (int64_t)gridDim.x - ntiles;   // blocks without a tile
-  if (cj.tok && idle > 0 && (int64_t)blockIdx.x >= ntiles)
-    concat_chunks_wave<MergedSrc>(cj.chunks, *cj.nlong, cj.chunks_s, *cj.nshort, cj.src, cj.tok, cj.cap_tokens,
-                                  ((int64_t)blockIdx.x - ntiles) * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE,
-                                  idle * (LU_NT / ALTO_WAVE));
+  if (cj.tok && idle > 0 && (int64_t)blockIdx.x >= ntiles) concat_role(cj, cw, idle * (LU_NT / ALTO_WAVE), c0l, c0s);
   if (ntiles == 0) {
     // nothing carried and nothing arrived
     if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -982,6 +1006,8 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
       cj.nlong = b.scal + 1;
       cj.chunks_s = b.chunks + b.short_base;
       cj.nshort = b.scal + 3;
+      cj.long_cap = b.short_base;
+      cj.short_cap = ntot + 1;
       cj.src = src;
       cj.tok = o.tok;
       cj.cap_tokens = o.cap_tokens;
