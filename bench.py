@@ -113,7 +113,7 @@ def cpu_baseline(leaves_log2: int):
     import numpy as np
     from oracle import alto_oracle as O
     from paper_2403_04311_amd import workloads as W
-    w = W.config5("cpu", leaves=1 << leaves_log2)
+    w = W.zipf_tree("cpu", leaves=1 << leaves_log2)
     path, fan, x = w.path.numpy(), w.fan.numpy(), w.payload_f32.numpy()
     # one core: the process is pinned to one CPU for the timed run (numpy's own
     # threads, if any, then share it), and the affinity is restored afterwards
@@ -221,7 +221,7 @@ def bench_tiny(args):
     token concat per sentence); launch-latency bound."""
     import torch
     from paper_2403_04311_amd import alto, workloads as W
-    w = W.config1("cuda")
+    w = W.tiny_tree("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     n = w.n
     ws = alto.new_workspace(alto.workspace_bytes(w.bits, n, w.num_dest, w.agg_level, "concat"))
@@ -251,10 +251,10 @@ def bench_factool(args):
     over the first stage's records."""
     import torch
     from paper_2403_04311_amd import alto, workloads as W
-    w = W.config2("cuda")
+    w = W.factool_batch("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     n, dim = w.n, w.dim
-    sb = W.CONFIG2_STAGE_B
+    sb = W.FACTOOL_CLAIM_STAGE
     ws = alto.new_workspace(alto.workspace_bytes(w.bits, n, 32, 4, "mean", dim))
     perm = torch.empty(n, dtype=torch.int32, device="cuda")
     offs = torch.empty(33, dtype=torch.int64, device="cuda")
@@ -381,7 +381,7 @@ def bench_tokens(args):
     sentences carried across steps and emitted when their last token arrives."""
     import torch
     from paper_2403_04311_amd import alto, workloads as W
-    w = W.config3("cuda")
+    w = W.token_stream("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     n, step = w.n, w.step
     nsteps = (n + step - 1) // step
@@ -470,11 +470,11 @@ def bench_factool_stream(args):
     reads the first stage's emitted count on the device (no host read per step)."""
     import torch
     from paper_2403_04311_amd import alto, workloads as W
-    w = W.config4("cuda")
+    w = W.factool_stream("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     step, steps = w.step, min(w.info["steps"], args.stream_steps)
     ring, ring_rows = w.payload_f32, w.payload_f32.shape[0]
-    sbB = W.CONFIG2_STAGE_B
+    sbB = W.FACTOOL_CLAIM_STAGE
     gA = alto.new_groups(step, 4, "mean", 768)
     gB = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
     stA, stB = alto.new_status(), alto.new_status()
@@ -605,11 +605,11 @@ def bench_join(args):
         assert int(st.item()) == 0 and int(counts[0]) == nr
         return nl, nr, ms
 
-    w2 = W.config2("cuda")
+    w2 = W.factool_batch("cuda")
     k2, _ = alto.pack_keys(w2.path, w2.bits)
     nl2, nr2, ms2 = one(k2, w2.bits, 3, args.steps * 10, args.warmup)
     del w2, k2
-    w5 = W.config5("cuda", leaves=1 << args.leaves_log2)
+    w5 = W.zipf_tree("cuda", leaves=1 << args.leaves_log2)
     k5, _ = alto.pack_keys(w5.path, w5.bits)
     del w5
     torch.cuda.empty_cache()
@@ -649,10 +649,10 @@ def bench_split(args):
         assert int(st.item()) == 0 and int(counts[2]) == 0
         return n, ms
 
-    t3 = W.config3_text("cuda")
+    t3 = W.token_stream_text("cuda")
     n3, ms3 = one(t3, args.steps * 10, args.warmup)
     del t3
-    t = W.config3_text("cuda", generators=16384)
+    t = W.token_stream_text("cuda", generators=16384)
     n, ms = one(t, args.steps, args.warmup)
     # in: key, stream length, token; out per placed token: key, two counts, token, input index
     per = 8 + 4 + 4 + 8 + 4 + 4 + 4 + 4
@@ -674,7 +674,7 @@ def bench_route_load(args):
     import time as T
     import torch
     from paper_2403_04311_amd import alto, workloads as W
-    w5 = W.config5("cuda", leaves=1 << args.leaves_log2)
+    w5 = W.zipf_tree("cuda", leaves=1 << args.leaves_log2)
     keys, _ = alto.pack_keys(w5.path, w5.bits)
     bits = w5.bits
     del w5
@@ -718,7 +718,7 @@ def bench_route_load(args):
     torch.cuda.empty_cache()
 
     # the FacTool-shaped stream: claims as flows, 32 destinations, 128 fragments drained per step
-    w = W.config4("cuda")
+    w = W.factool_stream("cuda")
     skeys, _ = alto.pack_keys(w.path, w.bits)
     step, steps = w.step, min(w.info["steps"], args.stream_steps)
     Ds, service = 32, 128
@@ -766,7 +766,7 @@ def bench_route_load(args):
 
 def bench_live_scaling(args):
     """Per-step cost of a stream step against the size of the carried state. A token
-    stream in config 3's layout (31, 6, 12) whose 256 sentences stay open (each
+    stream in the token stream's layout (31, 6, 12) whose 256 sentences stay open (each
     declares 4,095 tokens): every 4,096-fragment step adds 16 tokens to each, so the
     live set grows by 4,096 leaves a step, to 1,044,480 after 255 steps. Reports the
     device time per step at several live-set sizes and the least-squares slope."""
@@ -778,7 +778,7 @@ def bench_live_scaling(args):
     rng = np.random.default_rng(20240307)
     roots = rng.choice(1 << 31, size=G, replace=False).astype(np.int64)
     # step s: tokens s*16 .. s*16+15 of every generator's sentence 0, generator-major
-    # within a tick (round robin), as config 3 arrives
+    # within a tick (round robin), as the token stream arrives
     t = np.arange(steps * per, dtype=np.int64)
     tick, gen = np.meshgrid(t, np.arange(G), indexing="ij")
     path = np.stack([roots[gen.ravel()], np.zeros(gen.size, np.int64), tick.ravel()]).astype(np.int32)
@@ -811,7 +811,7 @@ def bench_live_scaling(args):
         sel = (live >= lo) & (live < lo + (1 << 16))
         if sel.any():
             at[str(lo)] = float(np.median(np.asarray(per_ms)[sel]) * 1e3)
-    return _line("open token stream (live set growing 4,096 leaves a step to 1,044,480), config 3 layout, "
+    return _line("open token stream (live set growing 4,096 leaves a step to 1,044,480), token-stream layout, "
                  "concat per sentence, 64 destinations", step, tot / steps, steps, 1, 0,
                  {"step_us_p50_at_live": at, "step_us_per_1k_live": float(slope * 1e3), "step_us_at_live_0": float(icpt)})
 
@@ -889,7 +889,7 @@ def main():
     n = 1 << args.leaves_log2
     log(f"generating workload: 2^{args.leaves_log2} fragments")
     t0 = time.time()
-    w = W.config5(dev, leaves=n)
+    w = W.zipf_tree(dev, leaves=n)
     keys, st = alto.pack_keys(w.path, w.bits)
     torch.cuda.synchronize()
     assert int(st.item()) == 0

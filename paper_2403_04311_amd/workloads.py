@@ -217,10 +217,10 @@ def tokens(rng: np.random.Generator, n: int) -> np.ndarray:
 
 
 # ----------------------------------------------------------------------------
-# the five configurations
+# the benchmarked workloads
 # ----------------------------------------------------------------------------
 
-def config1(device="cpu", seed: int = SEED_BASE + 1) -> Workload:
+def tiny_tree(device="cpu", seed: int = SEED_BASE + 1) -> Workload:
     """Tiny depth-4 tree: query / doc / sentence / token, concat at sentence level."""
     rng = np.random.default_rng(seed)
     roots = distinct_ids(rng, 64)
@@ -228,7 +228,7 @@ def config1(device="cpu", seed: int = SEED_BASE + 1) -> Workload:
     path, fan = expand_tree(fans, roots)
     tok = tokens(rng, path.shape[1])
     p, f, t, _ = shuffle_arrival(path, fan, tok, seed + 101, device)
-    return Workload("cfg1_tiny_concat", (31, 2, 3, 4), 1, 8, 3, "concat", 1, 0, p, f,
+    return Workload("tiny_concat", (31, 2, 3, 4), 1, 8, 3, "concat", 1, 0, p, f,
                     payload_i32=t)
 
 
@@ -245,11 +245,11 @@ def doc_ids_per_sentence(rng, fans) -> np.ndarray:
     return np.repeat(ids, fans[3].astype(np.int64))
 
 
-def config2(device="cpu", seed: int = SEED_BASE + 2, queries: int = 1024) -> Workload:
+def factool_batch(device="cpu", seed: int = SEED_BASE + 2, queries: int = 1024) -> Workload:
     """FacTool-shaped depth-5 tree; mean-pool 768-d sentence vectors per document.
 
     The follow-on stage (concat of document ids per claim) consumes the records the
-    first stage emits; see ``CONFIG2_STAGE_B``.
+    first stage emits; see ``FACTOOL_CLAIM_STAGE``.
     """
     rng = np.random.default_rng(seed)
     roots = distinct_ids(rng, queries)
@@ -258,16 +258,16 @@ def config2(device="cpu", seed: int = SEED_BASE + 2, queries: int = 1024) -> Wor
     docid = doc_ids_per_sentence(rng, fans)
     p, f, t, _ = shuffle_arrival(path, fan, docid, seed + 101, device)
     x = randn_rows(path.shape[1], 768, seed + 202, device)
-    return Workload("cfg2_factool_mean_concat", (31, 3, 2, 3, 8), 2, 32, 4, "mean", 768, 0,
+    return Workload("factool_mean_concat", (31, 3, 2, 3, 8), 2, 32, 4, "mean", 768, 0,
                     p, f, payload_i32=t, payload_f32=x)
 
 
-# second stage of configurations 2 and 4: records of level-4 groups (depth-4 keys)
-CONFIG2_STAGE_B = dict(bits=(31, 3, 2, 3), route_level=2, num_dest=32, agg_level=2,
+# second stage of the FacTool batch and stream: records of level-4 groups (depth-4 keys)
+FACTOOL_CLAIM_STAGE = dict(bits=(31, 3, 2, 3), route_level=2, num_dest=32, agg_level=2,
                        op="concat", dim=1, mask_level=0)
 
 
-def config3(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
+def token_stream(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
             sentences: int = 64, step: int = 4096) -> Workload:
     """Token stream: request / sentence / token, round-robin over generators."""
     rng = np.random.default_rng(seed)
@@ -281,7 +281,7 @@ def config3(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
     gen = np.repeat(np.arange(generators, dtype=np.int64), per_gen)
     tick = np.arange(path.shape[1], dtype=np.int64) - np.repeat(np.cumsum(per_gen) - per_gen, per_gen)
     order = np.lexsort((gen, tick))
-    w = Workload("cfg3_token_stream", (31, 6, 12), 2, 64, 2, "concat", 1, 0,
+    w = Workload("token_stream", (31, 6, 12), 2, 64, 2, "concat", 1, 0,
                  _to_dev(path[:, order], device), _to_dev(fan[:, order], device),
                  payload_i32=_to_dev(tok[order], device), step=step)
     w.info["generators"] = generators
@@ -319,11 +319,11 @@ class TextStreams:
         return int(self.path.shape[1])
 
 
-def config3_text(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
+def token_stream_text(device="cpu", seed: int = SEED_BASE + 3, generators: int = 256,
                  sentences: int = 64) -> TextStreams:
-    """The token streams config 3's sentences come from: every generator writes its
+    """The token streams the token stream's sentences come from: every generator writes its
     sentences as one stream, each sentence followed by a delimiter token, and a pmap
-    entry cuts the streams back into sentences. Same draws as config 3 (same seed,
+    entry cuts the streams back into sentences. Same draws as token_stream (same seed,
     same generators: the same requests, sentence lengths and token ids).
     Layout (request 31 bits, position 18 bits) -> (request, sentence 6, token 12);
     arrival round-robin over generators, in order within each. The streams are laid
@@ -375,7 +375,7 @@ def random_text(seed: int, depth: int, roots: int, max_fan: Sequence[int], bits:
     return path, fan, tok
 
 
-def config4(device="cpu", seed: int = SEED_BASE + 4, steps: int = 10000, step: int = 4096,
+def factool_stream(device="cpu", seed: int = SEED_BASE + 4, steps: int = 10000, step: int = 4096,
             target_frac: float = 0.30, ring_steps: int = 256) -> Workload:
     """FacTool-shaped trees as a continuous windowed stream of ``steps`` x ``step``.
 
@@ -423,7 +423,7 @@ def config4(device="cpu", seed: int = SEED_BASE + 4, steps: int = 10000, step: i
     f = _to_dev(fan, device)[:, order].contiguous()
     t = _to_dev(docid, device)[order].contiguous()
     x = randn_rows(ring_steps * step, 768, seed + 202, device)
-    w = Workload("cfg4_factool_stream", (31, 3, 2, 3, 8), 2, 32, 4, "mean", 768, 0, p, f,
+    w = Workload("factool_stream", (31, 3, 2, 3, 8), 2, 32, 4, "mean", 768, 0, p, f,
                  payload_i32=t, payload_f32=x, step=step)
     w.info.update(window=W, ring_steps=ring_steps, steps=steps, calibrated_frac=frac(W))
     return w
@@ -438,7 +438,7 @@ def _leaves_per_root(fans):
     return c
 
 
-def config5_tree(seed: int = SEED_BASE + 5, leaves: int = 1 << 26, s: float = 1.2,
+def zipf_tree_fans(seed: int = SEED_BASE + 5, leaves: int = 1 << 26, s: float = 1.2,
                  cap: int = 4096, depth: int = 6):
     """Skewed depth-6 tree built bottom-up from truncated Zipf child counts."""
     rng = np.random.default_rng(seed)
@@ -453,15 +453,15 @@ def config5_tree(seed: int = SEED_BASE + 5, leaves: int = 1 << 26, s: float = 1.
     return fans, roots
 
 
-def config5(device="cpu", seed: int = SEED_BASE + 5, leaves: int = 1 << 26,
+def zipf_tree(device="cpu", seed: int = SEED_BASE + 5, leaves: int = 1 << 26,
             with_payload: bool = True) -> Workload:
     """Skewed Zipf depth-6 tree, 128-d mean at level 4, completion mask at level 2."""
-    fans, roots = config5_tree(seed, leaves)
+    fans, roots = zipf_tree_fans(seed, leaves)
     path, fan = expand_tree(fans, roots)
     p, f, _, _ = shuffle_arrival(path, fan, None, seed + 101, device)
     del path, fan
     x = randn_rows(leaves, 128, seed + 202, device) if with_payload else None
-    w = Workload("cfg5_zipf_mean_mask", (3, 12, 12, 12, 12, 12), 4, 256, 4, "mean", 128, 2,
+    w = Workload("zipf_mean_mask", (3, 12, 12, 12, 12, 12), 4, 256, 4, "mean", 128, 2,
                  p, f, payload_f32=x)
     w.info["level_nodes"] = [len(roots)] + [int(x.sum()) for x in fans]
     return w

@@ -156,8 +156,8 @@ def test_route_duplicate_and_layout():
     assert int(st.item()) == O.E_LAYOUT
 
 
-def test_config1_full():
-    w = W.config1("cpu")
+def test_tiny_tree_full():
+    w = W.tiny_tree("cpu")
     path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
     keys = O.pack_keys(path, w.bits)
     code, rt, g = U.oracle_aggregate(keys, fan, w.bits, w.agg_level, w.op, 1, 0, w.route_level,
@@ -333,10 +333,10 @@ def test_two_stage_batches_pipelined_on_two_hip_streams_match_one_stream():
     bits as with both stages on one stream."""
     import torch
     from paper_2403_04311_amd import alto
-    w = W.config2("cuda")
+    w = W.factool_batch("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     n, dim = w.n, w.dim
-    sb = W.CONFIG2_STAGE_B
+    sb = W.FACTOOL_CLAIM_STAGE
     ws = alto.new_workspace(alto.workspace_bytes(w.bits, n, 32, 4, "mean", dim))
     stA, stB = alto.new_status(), alto.new_status()
     gAs = [alto.new_groups(n // 4 + 1024, 4, "mean", dim), alto.new_groups(n // 4 + 1024, 4, "mean", dim)]

@@ -51,7 +51,7 @@ def _zipf_call(w, keys, n):
 
 def test_zipf_64M_mean_mask():
     log("config: zipf depth-6, 2^26 fragments, 128-d mean at level 4, mask at level 2")
-    w = W.config5("cuda")
+    w = W.zipf_tree("cuda")
     n = w.n
     keys, st = alto.pack_keys(w.path, w.bits)
     torch.cuda.synchronize()
@@ -118,7 +118,7 @@ def test_zipf_64M_mean_mask():
 
 def test_factool_batch_two_stages():
     log("config: FacTool depth-5, 1,024 queries, 768-d mean per doc, then doc-id concat per claim")
-    w = W.config2("cuda")
+    w = W.factool_batch("cuda")
     path, fan, docid = w.path.cpu().numpy(), w.fan.cpu().numpy(), w.payload_i32.cpu().numpy()
     keys = O.pack_keys(path, w.bits)
     pf = w.payload_f32.cpu().numpy()
@@ -127,7 +127,7 @@ def test_factool_batch_two_stages():
     res = U.run_aggregate(keys, fan, w.bits, 4, "mean", 768, 0, 2, 32, docid, pf)
     assert res["status"] == O.OK
     U.compare(res, rt, g, "mean", 0, 4)
-    sb = W.CONFIG2_STAGE_B
+    sb = W.FACTOOL_CLAIM_STAGE
     kB, fB, pB = res["key"], res["fan_up"], res["first_i32"]
     code, rtB, gB = U.oracle_aggregate(kB, fB, sb["bits"], 2, "concat", 1, 0, 2, 32, pB)
     assert code == O.OK
@@ -138,7 +138,7 @@ def test_factool_batch_two_stages():
 
 def test_factool_stream_10000_steps():
     log("config: FacTool windowed stream, 10,000 steps x 4,096 fragments, two stages chained on the device")
-    w = W.config4("cuda")
+    w = W.factool_stream("cuda")
     log(f"generated: window {w.info['window']:.0f}, long-lived fraction {w.info['calibrated_frac']:.3f}")
     step, steps = w.step, w.info["steps"]
     ring = w.payload_f32
@@ -150,7 +150,7 @@ def test_factool_stream_10000_steps():
     hdoc = w.payload_i32.cpu().numpy()
     assert np.array_equal(keys_d.cpu().numpy().view(np.uint64), hkeys)
     sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22, step_max=step)
-    sbB = W.CONFIG2_STAGE_B
+    sbB = W.FACTOOL_CLAIM_STAGE
     sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
                      step_max=step)
     # expected: a document is emitted in the step of its last sentence, if all arrived

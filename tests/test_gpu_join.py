@@ -61,7 +61,7 @@ def test_join_parity(case):
 def test_join_factool_search_queries():
     """Search-query objects (level 3 of the FacTool-shaped tree, e.g. query embeddings)
     joined with every sentence below them (908,008 fragments)."""
-    w = W.config2("cpu")
+    w = W.factool_batch("cpu")
     keys = O.pack_keys(w.path.numpy(), w.bits)
     rng = np.random.default_rng(5)
     left = np.unique(O.prefix(keys, w.bits, 3))

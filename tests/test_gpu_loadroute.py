@@ -118,7 +118,7 @@ def test_load_route_zipf_tree_full_size():
     """All 2^26 fragments of the Zipf depth-6 tree, flows at level 4 (1,452 of them)
     to 256 destinations from empty queues, in the launch configuration the benchmark
     times: destinations and queues against the oracle, perm by its defining order."""
-    w = W.config5("cuda")
+    w = W.zipf_tree("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     del w
     torch.cuda.empty_cache()

@@ -154,10 +154,10 @@ def test_split_rejects_bad_arguments():
     assert rc == 1           # workspace too small
 
 
-def test_split_config3_streams_against_oracle():
+def test_split_token_streams_against_oracle():
     """The 256 generator streams of the token-stream workload (408,190 positions), in
     the launch configuration the benchmark times, element by element."""
-    t = W.config3_text("cpu")
+    t = W.token_stream_text("cpu")
     path, fan, tok = t.path.numpy(), t.fan.numpy(), t.tokens.numpy()
     w = check(path, fan, tok, t.bits, t.delim, t.seg_bits, t.tok_bits)
     assert w.counts.tolist() == [t.n - 16384, 16384, 0, 16384]
@@ -168,7 +168,7 @@ def test_split_scaled_streams_give_back_their_tree():
     the new fragments are exactly the (request, sentence, index) tags the streams
     were written from, with their (sentences, sentence length) counts and tokens, in
     key order; sampled parents are checked against the oracle."""
-    t = W.config3_text("cuda", generators=16384)
+    t = W.token_stream_text("cuda", generators=16384)
     keys, st = alto.pack_keys(t.path, t.bits)
     ok, of, otok, oidx, rest, c, st2 = alto.split(keys, t.fan, t.tokens, t.bits, t.delim, t.seg_bits, t.tok_bits)
     torch.cuda.synchronize()

@@ -142,8 +142,8 @@ def test_stream_parity(case, op):
     compare_steps(gpu, ora, op, La)
 
 
-def test_config3_token_stream_full():
-    w = W.config3("cpu")
+def test_token_stream_full():
+    w = W.token_stream("cpu")
     path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
     keys = O.pack_keys(path, w.bits)
     cuts = list(range(0, w.n, w.step)) + [w.n]
@@ -184,7 +184,7 @@ def gpu_chain(bits, keys, fan, p32, pf, cuts, step_max, max_live, max_groups, re
     """The two FacTool stages on the device, step by step, stage B reading stage A's
     emitted count on the device (alto_stream_step_dev): no host read between the
     stages. Returns per-step (stage A dict, stage B dict)."""
-    bB = W.CONFIG2_STAGE_B["bits"]
+    bB = W.FACTOOL_CLAIM_STAGE["bits"]
     sA = alto.Stream(bits, 2, 32, 4, "mean", 768, max_live_leaves=max_live, max_groups=max_groups,
                      step_max=step_max, release=release)
     sB = alto.Stream(bB, 2, 32, 2, "concat", 1, max_live_leaves=max_live, max_groups=max_groups,
@@ -245,12 +245,12 @@ def test_factool_stream_two_stages():
     # stage B consumes stage A's emitted records step by step, on the device
     got = gpu_chain(bits, keys, fan, docid, pf, cuts, 256, 8192, 1 << 14)
     oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts)
-    compare_chain(got, oA, W.CONFIG2_STAGE_B["bits"], "complete")
+    compare_chain(got, oA, W.FACTOOL_CLAIM_STAGE["bits"], "complete")
     # and through host-side copies of stage A's records, with per-step routing outputs
     gA = gpu_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, max_live=8192,
                    max_groups=1 << 14, step_max=256)
     compare_steps(gA, oA, "mean", 4)
-    bB = W.CONFIG2_STAGE_B["bits"]
+    bB = W.FACTOOL_CLAIM_STAGE["bits"]
     kB, fB, pB, cB = [], [], [], [0]
     for r in gA[0]:
         kB.append(r["key"])
@@ -369,11 +369,11 @@ def test_factool_stream_in_order_two_stages():
     cuts = sorted(set(list(range(0, n, 256)) + [n]))
     oA = oracle_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, release="in_order")
     got = gpu_chain(bits, keys, fan, docid, pf, cuts, 256, 8192, 1 << 14, release="in_order")
-    compare_chain(got, oA, W.CONFIG2_STAGE_B["bits"], "in_order")
+    compare_chain(got, oA, W.FACTOOL_CLAIM_STAGE["bits"], "in_order")
     gA = gpu_steps(bits, 2, 32, 4, "mean", 768, keys, fan, docid, pf, cuts, max_live=8192,
                    max_groups=1 << 14, step_max=256, release="in_order")
     compare_steps(gA, oA, "mean", 4)
-    bB = W.CONFIG2_STAGE_B["bits"]
+    bB = W.FACTOOL_CLAIM_STAGE["bits"]
     kB, fB, pB, cB = [], [], [], [0]
     for r in gA[0]:
         kB.append(r["key"])
@@ -407,11 +407,11 @@ def test_two_stage_stream_pipelined_on_two_hip_streams_matches_sequential():
     stages run one after the other on one stream (checksums of the emitted document keys and
     means, and of the claim stage's keys, token offsets and tokens, per step)."""
     from paper_2403_04311_amd import workloads as W
-    w = W.config4("cuda", steps=300)
+    w = W.factool_stream("cuda", steps=300)
     step, steps = w.step, 300
     ring, ring_rows = w.payload_f32, w.payload_f32.shape[0]
     keys, st = alto.pack_keys(w.path, w.bits)
-    sbB = W.CONFIG2_STAGE_B
+    sbB = W.FACTOOL_CLAIM_STAGE
 
     def streams():
         sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22,
@@ -493,7 +493,7 @@ def test_overlapped_steps_match_sequential_token_stream():
     outputs as alto_stream_step_dev on one stream: the step's perm, dest and
     dest_offsets, the emitted groups (keys, token offsets, tokens) and their counts."""
     from paper_2403_04311_amd import workloads as W
-    w = W.config3("cuda")
+    w = W.token_stream("cuda")
     keys, st = alto.pack_keys(w.path, w.bits)
     n, step = w.n, w.step
     nsteps = (n + step - 1) // step

@@ -504,10 +504,10 @@ def test_stream_late_and_duplicate():
         assert e.value.code == O.E_DUPLICATE
 
 
-def test_config3_emission_step_closed_form():
+def test_token_stream_emission_step_closed_form():
     # Tokens of a generator arrive in order, so a sentence is emitted in the step of
     # its last token: floor(arrival index of the last token / step).
-    w = W.config3(generators=16, sentences=8, step=256)
+    w = W.token_stream(generators=16, sentences=8, step=256)
     path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
     keys = O.pack_keys(path, w.bits)
     s = O.Stream(w.bits, w.route_level, w.num_dest, w.agg_level, "concat")
@@ -580,7 +580,7 @@ def test_stream_in_order_release_brute_force():
 def test_in_order_release_token_stream_matches_completion():
     # Tokens of a generator arrive in order, so its sentences also complete in order:
     # in-order release changes nothing (floor(last token's arrival index / step)).
-    w = W.config3(generators=16, sentences=8, step=256)
+    w = W.token_stream(generators=16, sentences=8, step=256)
     path, fan, tok = w.path.numpy(), w.fan.numpy(), w.payload_i32.numpy()
     keys = O.pack_keys(path, w.bits)
     s = O.Stream(w.bits, w.route_level, w.num_dest, w.agg_level, "concat", release="in_order")
