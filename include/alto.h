@@ -204,9 +204,10 @@ int alto_aggregate_overlap(const uint64_t *keys, const int32_t *fan, int64_t fan
  * ws_bytes: the workspace is a fixed array of ALTO_NOALLOC_SCRATCH_BYTES in the
  * library's own device memory, one per GPU, held from the first call on that GPU
  * until the process ends. Calls with alto_workspace_bytes(layout, n, num_dest,
- * agg) > ALTO_NOALLOC_SCRATCH_BYTES return ALTO_E_ARG (nothing is enqueued); for
- * the layouts of this library that is about 600k fragments with a 128-float mean,
- * 900k with a 768-float one. The call allocates nothing. Every call on one GPU
+ * agg) > ALTO_NOALLOC_SCRATCH_BYTES return ALTO_E_ARG (nothing is enqueued); that
+ * is about 600k fragments for a six-level layout with a 128-float mean and a
+ * completion mask, 1.1M for a five-level one with a 768-float mean. The call
+ * allocates nothing. Every call on one GPU
  * shares that GPU's array, and it keeps what the last call left there: calls on
  * one GPU that overlap in time (different streams, or different host threads)
  * race on it and give undefined outputs; serialise them. ALTO_E_HIP if the
