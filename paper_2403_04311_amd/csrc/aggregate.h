@@ -149,8 +149,8 @@ int route_run(const KeyGeom& g, const RouteGeom& rg, const uint64_t* keys, int64
               bool allow_dp = false, const int64_t* n_dev = nullptr);
 // Work folded into the kernels of groups_run (fewer launches per call):
 //  - the comparison of the fan fingerprints, in the group kernel (fp_in null:
-//    none; levels flo..fhi, those in xlo..xhi only when ctl reports a flow-set
-//    overflow, as in k_fp_compare);
+//    none; levels flo..fhi, those in xlo..xhi, which the flow set checked exactly,
+//    only when ctl reports that the flow set overflowed);
 //  - the group kernel's look-back words at gst and its ticket at *gctr (null: the
 //    sort's status words and first ticket); cleared = the caller's earlier kernel
 //    cleared them (cdiv(n_max + 1, GROUP_SCAN_TILE) * GROUP_SCAN_WORDS words),
@@ -295,5 +295,3 @@ int aggregate_run(const KeyGeom& g, const RouteGeom& rg, int Lr, const alto_agg&
                   hipStream_t st, const int64_t* n_dev = nullptr, hipStream_t gather_st = nullptr);
 void empty_outputs(const GroupOut& out, int64_t* dest_offsets, int num_dest, hipStream_t st);
 void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st);
-void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,
-                       hipStream_t st);

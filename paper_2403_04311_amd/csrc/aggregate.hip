@@ -462,20 +462,6 @@ __global__ __launch_bounds__(256) void k_dest_offsets(const uint64_t* __restrict
   if (dup) raise_status(status, ALTO_E_DUPLICATE);
 }
 
-__global__ void k_fill_i64(int64_t* p, int64_t count, int64_t v) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
-}
-
-// Levels xlo..xhi were checked exactly per flow and have no fragment-side
-// fingerprint, unless the flow set overflowed (then k_prep_fp added it).
-__global__ void k_fp_compare(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int xlo, int xhi,
-                             const SortCtl* ctl, int32_t* status) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  const bool all = ctl == nullptr || ctl->flow_overflow;
-  for (int m = flo; m <= fhi; ++m)
-    if ((all || m < xlo || m > xhi) && fp_in[m] != fp_nodes[m]) raise_status(status, ALTO_E_FANOUT);
-}
-
 // The groups of the aggregation level in one kernel. Per tile of groups: the
 // exclusive sums over groups u = 0..G (entry G holds the totals) of emitted
 // (complete) flags, emitted tokens, long-group chunks, chunk partials (groups of
@@ -1512,7 +1498,3 @@ void zero_offsets(int64_t* dest_offsets, int num_dest, hipStream_t st) {
   if (dest_offsets) k_zero_offsets<<<1, 256, 0, st>>>(dest_offsets, num_dest);
 }
 
-void fp_compare_launch(const uint64_t* fp_in, const uint64_t* fp_nodes, int flo, int fhi, int32_t* status,
-                       hipStream_t st) {
-  k_fp_compare<<<1, 1, 0, st>>>(fp_in, fp_nodes, flo, fhi, 1, 0, nullptr, status);
-}
