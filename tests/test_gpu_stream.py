@@ -266,6 +266,26 @@ def test_factool_stream_two_stages():
     compare_steps(gB, oB, "concat", 2)
 
 
+@pytest.mark.parametrize("op", ["concat", "mean"])
+@pytest.mark.parametrize("drop", [0.0, 0.0002])
+def test_stream_long_groups(op, drop):
+    """Groups of up to 6,000 leaves carried across steps: long groups (chunks of
+    4,096 rows after the first, written by the whole wave; means combined from
+    partial sums), next to short ones, element by element against the oracle."""
+    bits = (8, 4, 13)
+    keys, fan, p32, pf = _tiny(640 + int(drop * 10000), 3, bits, (12, 6000), 2, drop, 8)
+    n = len(keys)
+    assert n > 4 * 4096
+    rng = np.random.default_rng(641)
+    cuts = [0] + sorted(rng.choice(np.arange(1, n), size=5, replace=False).tolist()) + [n]
+    pfa = pf if op == "mean" else None
+    gpu = gpu_steps(bits, 1, 4, 2, op, 8, keys, fan, p32, pfa, cuts, max_live=1 << 16, max_groups=1 << 10)
+    ora = oracle_steps(bits, 1, 4, 2, op, 8, keys, fan, p32, pfa, cuts)
+    long_emitted = [int((r.groups.count > 4096).sum()) for c, r in ora[0] if c == O.OK]
+    assert sum(long_emitted) > 0
+    compare_steps(gpu, ora, op, 2)
+
+
 def _cross_step_case():
     bits = (6, 3, 4)
     path, fan = W.random_tree(41, 3, 6, (4, 9), bits)
@@ -273,7 +293,7 @@ def _cross_step_case():
     return bits, keys, fan, np.arange(len(keys), dtype=np.int32)
 
 
-@pytest.mark.parametrize("kind", ["late", "dup_across", "fan_across", "live_capacity"])
+@pytest.mark.parametrize("kind", ["late", "dup_across", "fan_across", "live_capacity", "emit_capacity"])
 def test_stream_errors_and_poison(kind):
     bits, keys, fan, p32 = _cross_step_case()
     n = len(keys)
@@ -302,16 +322,29 @@ def test_stream_errors_and_poison(kind):
         fan[1, idx_g[1]] += 1
         order = np.concatenate([idx_g[:1], idx_g[1:], rest])
         cuts = [0, 1, len(idx_g), len(order)]
-    else:
+    elif kind == "live_capacity":
         max_live = 4
         order = np.random.default_rng(3).permutation(n)
         cuts = [0, n // 2, n]
+    else:
+        # more groups emitted than the stream's max_groups: the live-set update of
+        # the step that passes the limit reports it
+        max_groups = 2
+        order = np.random.default_rng(4).permutation(n)
+        cuts = [0, n // 3, 2 * n // 3, n]
     k, f, p = keys[order], fan[:, order], p32[order]
-    gpu = gpu_steps(bits, 1, 5, 2, "concat", 1, k, f, p, None, cuts, max_live=max_live, max_groups=1024)
+    gpu = gpu_steps(bits, 1, 5, 2, "concat", 1, k, f, p, None, cuts, max_live=max_live,
+                    max_groups=max_groups if kind == "emit_capacity" else 1024)
     ora = oracle_steps(bits, 1, 5, 2, "concat", 1, k, f, p, None, cuts)
     codes_g = [r["status"] for r in gpu[0]]
     codes_o = [c for c, _ in ora[0]]
-    if kind == "live_capacity":
+    if kind in ("live_capacity", "emit_capacity"):
+        if kind == "emit_capacity":
+            # the step whose emissions first take the total past the limit reports it
+            assert all(c == O.OK for c in codes_o)
+            total = np.cumsum([len(r.groups.key) for _, r in ora[0]])
+            assert total[-1] > max_groups
+            assert codes_g.index(O.E_CAPACITY) == int(np.argmax(total > max_groups)), (codes_g, total)
         assert O.E_CAPACITY in codes_g
         first = codes_g.index(O.E_CAPACITY)
         assert all(c == O.E_CAPACITY for c in codes_g[first:])       # poisoned
