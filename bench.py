@@ -398,32 +398,33 @@ def bench_tokens(args):
         tot, per = _stream_run(nsteps, one)
         s.close()
         return tot, per
-    def run_overlapped(per_step=True):
+    def run_overlapped(ends=True, starts=True):
         # each step's routing on a second HIP stream, beside the previous step's merge
-        # and emission (alto_stream_step_overlap); per_step: an event pair per step
-        # (which itself costs a few microseconds on each stream), else one around all
+        # and emission (alto_stream_step_overlap). ends: an event at every step's end
+        # (on the merge stream), starts: one at every step's start (on the routing
+        # stream); each event itself costs a few microseconds on its stream, so the
+        # period is taken with ends only, the latency with both, the rate with neither
         s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step,
                         release=args.release)
         main = torch.cuda.current_stream()
         route = route_stream
         route.wait_stream(main)
-        k = nsteps if per_step else 1
-        t0 = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
-        t1 = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+        t0 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
+        t1 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
         for i in range(nsteps):
             a, b = i * step, min(n, (i + 1) * step)
-            if per_step or i == 0:
-                t0[i if per_step else 0].record(route)
+            if (ends and starts) or i == 0:
+                t0[i].record(route)
             s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status, stream=main,
                    route_stream=route)
-            if per_step or i == nsteps - 1:
-                t1[i if per_step else 0].record(main)
+            if ends or i == nsteps - 1:
+                t1[i].record(main)
         main.wait_stream(route)
         torch.cuda.synchronize()
         s.close()
-        lat = [t0[i].elapsed_time(t1[i]) for i in range(k)] if per_step else []
-        period = [t1[i - 1].elapsed_time(t1[i]) for i in range(1, k)]
-        return t0[0].elapsed_time(t1[k - 1]), lat, period
+        lat = [t0[i].elapsed_time(t1[i]) for i in range(nsteps)] if (ends and starts) else []
+        period = [t1[i - 1].elapsed_time(t1[i]) for i in range(1, nsteps)] if ends else []
+        return t0[0].elapsed_time(t1[nsteps - 1]), lat, period
     route_stream = torch.cuda.Stream()
     # the stream is short (96 steps, a few ms): many runs, so that the GPU clock
     # settles first and the percentiles pool enough steps
@@ -441,11 +442,11 @@ def bench_tokens(args):
         run_overlapped()
     tot, lat, period = 0.0, [], []
     for _ in range(reps):
-        t, l, p = run_overlapped()
+        t, _, p = run_overlapped(starts=False)
         tot += t / reps
-        lat += l
         period += p
-    bare = sum(run_overlapped(per_step=False)[0] for _ in range(reps)) / reps
+        lat += run_overlapped()[1]
+    bare = sum(run_overlapped(ends=False, starts=False)[0] for _ in range(reps)) / reps
     assert int(status.item()) == 0
     ms = tot / nsteps
     path_bytes = (n * (8 + 4 + 4 + 4 + 4 + 4) + 16384 * (8 + 4 + 8 + 4 + 8)) / nsteps
@@ -457,7 +458,8 @@ def bench_tokens(args):
                               "step_ms_p50": _pct(period, 50), "step_ms_p99": _pct(period, 99),
                               "step_ms_max": max(period),
                               "step_ms_note": "p50/p99/max of the period between consecutive steps' ends, "
-                                              f"{reps} runs of {nsteps} steps pooled, an event pair per step",
+                                              f"{reps} runs of {nsteps} steps pooled, an event at each step's end; "
+                                              "latency from runs with an event at each step's start as well",
                               "uninstrumented_ms_per_step": bare / nsteps,
                               "step_latency_ms_p50": _pct(lat, 50), "step_latency_ms_p99": _pct(lat, 99),
                               "sequential_ms_per_step": seq_tot / nsteps, "sequential_step_ms_p50": _pct(seq_per, 50),
