@@ -484,6 +484,7 @@ static_assert(GS_IT <= 32, "a thread's groups in one flag word");
 static_assert(GS_NT * GS_IT < (1 << 21), "a tile's group counts fit 21 bits");
 
 constexpr int GS_NV = GROUP_SCAN_WORDS;   // scanned values per group
+constexpr int GS_SPEC_BLOCKS = 8;         // blocks that load their tile before the count arrives
 
 __global__ void k_group_scan_prep(const int64_t* Gp, uint64_t* st, uint32_t* ctr, GroupsExtra ex) {
   const int64_t len = cdiv(*Gp + 1, GS_TILE) * GS_NV;
@@ -541,10 +542,13 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
                                                   uint32_t* ctr, GroupFold f, int64_t ucap, int32_t* status) {
   // the fields of the tile this block most likely takes first (its own index),
   // loaded before the group count and the ticket have arrived (the node arrays
-  // hold ucap + 1 entries; groups past the count are not used)
+  // hold ucap + 1 entries; groups past the count are not used). Only the first
+  // GS_SPEC_BLOCKS blocks do so: the grid is sized for the largest count, and
+  // blocks past the actual tile count would only load in vain.
   const int64_t gt = blockIdx.x;
+  const bool spec = blockIdx.x < GS_SPEC_BLOCKS;
   GroupTileLoad pre;
-  group_tile_load(L, f, gt * GS_TILE, ucap, pre);
+  if (spec) group_tile_load(L, f, gt * GS_TILE, ucap, pre);
   const int64_t G = *Gp;
   const int64_t ntiles = cdiv(G + 1, GS_TILE);
   __shared__ uint64_t s_w[GS_NT / ALTO_WAVE];
@@ -583,7 +587,7 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
       // first, then the flags, fingerprint terms and stores; the scan reads the
       // flags and row counts back from LDS.
       GroupTileLoad t;
-      if (tile == gt) t = pre;
+      if (spec && tile == gt) t = pre;
       else group_tile_load(L, f, g0, G, t);
       const int32_t* sn = t.sn;
       const int32_t* cv = t.cv;
@@ -621,7 +625,7 @@ __global__ __launch_bounds__(GS_NT) void k_groups(KeyGeom g, RouteGeom rg, int L
       }
     } else {
       GroupTileLoad t;
-      if (tile == gt) t = pre;
+      if (spec && tile == gt) t = pre;
       else group_tile_load(L, f, g0, G, t);
 #pragma unroll
       for (int k = 0; k < GS_IT; ++k) {

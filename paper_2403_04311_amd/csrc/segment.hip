@@ -18,6 +18,7 @@ namespace {
 constexpr int NT = SEG_NT;
 constexpr int IT = SEG_IT;
 constexpr int TILE = SEG_TILE;
+constexpr int SEG_SPEC_BLOCKS = 64;   // blocks that load their tile before the count arrives
 
 __device__ inline int64_t nelem(const SegJob& j) { return j.n_dev ? *j.n_dev : j.n_host; }
 
@@ -68,8 +69,9 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
   // own index) are loaded before the element count and the ticket have arrived
   // (within the key buffer's n_max elements; those past the count are masked)
   const int64_t gt = blockIdx.x;
+  const bool spec = j.prefetch && blockIdx.x < SEG_SPEC_BLOCKS;   // the grid is sized for the largest count
   uint64_t kg[IT], pg = 0;
-  if (j.prefetch) {
+  if (spec) {
     const int64_t eg = gt * TILE + (int64_t)threadIdx.x * IT;
     if (vec_ok && eg + IT <= j.n_max) {
       const ulonglong2* p = reinterpret_cast<const ulonglong2*>(j.keys + eg);
@@ -98,7 +100,7 @@ __global__ __launch_bounds__(NT) void k_seg_pass(KeyGeom g, SegJob j) {
     if (tile >= ntiles) break;   // uniform across the block
     const int64_t e0 = tile * TILE + (int64_t)threadIdx.x * IT;
     uint64_t k[IT];
-    const bool pre = j.prefetch && tile == gt;   // uniform
+    const bool pre = spec && tile == gt;   // uniform
     if (pre) {
 #pragma unroll
       for (int i = 0; i < IT; ++i) k[i] = e0 + i < n ? kg[i] : 0ull;

@@ -41,6 +41,7 @@ struct StreamCtl {
 constexpr int LU_NT = 256;
 constexpr int LU_IT = 8;
 constexpr int LU_TILE = LU_NT * LU_IT;
+constexpr int LU_SPEC_BLOCKS = 64;   // blocks that load their tile before the merged count arrives
 
 // sampled keys per run in the merge's LDS search
 constexpr int MERGE_SAMPLES = 2048;
@@ -315,6 +316,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   // arrived (the merged run's buffers hold ncap elements; those past the count are
   // not used)
   const int64_t gt = blockIdx.x;
+  const bool spec = blockIdx.x < LU_SPEC_BLOCKS;   // the grid is sized for the largest count
   // the first chunk of this block's waves in the concatenation, if it has no tile
   const int64_t cw = ((int64_t)gridDim.x - 1 - (int64_t)blockIdx.x) * (LU_NT / ALTO_WAVE) + threadIdx.x / ALTO_WAVE;
   Chunk c0l{}, c0s{};
@@ -325,7 +327,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
   int32_t msg[LU_IT];
   uint64_t kkg[LU_IT];
   uint2 wg = make_uint2(0u, 0u);
-  {
+  if (spec) {
     const int64_t eg = gt * LU_TILE + (int64_t)threadIdx.x * LU_IT;
 #pragma unroll
     for (int i = 0; i < LU_IT; ++i) {
@@ -374,7 +376,7 @@ __global__ __launch_bounds__(LU_NT) void k_live_update(KeyGeom g, LevelNodes L, 
         for (int l = 0; l < NFP; ++l) fv[l][i] = 0;
       }
       if (e0 < M) {
-        const bool pre = tile == gt;   // uniform
+        const bool pre = spec && tile == gt;   // uniform
         uint2 w;
         if (pre) {
 #pragma unroll
