@@ -85,6 +85,41 @@ __global__ void k_stream_begin(const StreamCtl* ctl, int32_t* status) {
   if (threadIdx.x == 0 && blockIdx.x == 0 && ctl->error) raise_status(status, ctl->error);
 }
 
+// Steps routed on another HIP stream: the routing's end is published in a word of
+// the handle's state (one per workspace, each on its own 256-byte line) rather
+// than with a HIP event, whose cross-queue wait costs the host about 10 us per
+// step and the step's queue a barrier packet. The signal kernel runs on the
+// routing stream after the routing's kernels, whose writes are released at their
+// ends; the merge waits for the word to hold the step's sequence number (a
+// per-handle random base plus a count, compared for equality, so a stale word of
+// an earlier handle in the same memory never matches) and then acquires.
+constexpr int64_t ROUTE_FLAG_STRIDE = 32;      // uint64 words: 256 bytes
+constexpr int ROUTE_WAIT_LIMIT = 1 << 24;      // polls of ~0.2-1 us: seconds, then ALTO_E_INTERNAL
+
+__global__ void k_route_signal(uint64_t* flag, uint64_t seq) {
+  if (threadIdx.x == 0) __hip_atomic_store(flag, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bounded wait of a block for its step's routing (rflag null: the routing ran
+// before on the same stream). On giving up the status word gets ALTO_E_INTERNAL
+// and the block goes on; whatever it then reads of the routing's outputs is used
+// only within bounds (the merge clamps the permutation's source indices).
+__device__ inline void route_wait(const uint64_t* rflag, uint64_t rseq, int32_t* status) {
+  if (!rflag) return;
+  if (threadIdx.x == 0) {
+    int spin = 0;
+    while (__hip_atomic_load(rflag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != rseq) {
+      if (++spin > ROUTE_WAIT_LIMIT) {
+        raise_status(status, ALTO_E_INTERNAL);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(8);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+  __syncthreads();
+}
+
 // Merge path: every element finds its place by binary search in the other run.
 // Live elements go before equal step keys (which are duplicates, reported later).
 // The searches start in LDS: each block that holds merged elements first copies
@@ -98,18 +133,43 @@ __global__ void k_stream_begin(const StreamCtl* ctl, int32_t* status) {
 // the merged run (seg_prep_device), and clears the look-back words and tickets of
 // the group scan (gst, ctr[0]) and the live-set update (lst, ctr[1]). When the
 // routing ran on another HIP stream, it also writes the step's permutation and
-// destinations (perm_out, dest_out; null: the routing wrote them).
+// destinations (perm_out, dest_out; null: the routing wrote them), after waiting
+// for the routing's signal (rflag, rseq; null: no wait).
 __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCtl* ctl, int64_t cap, LiveSet live,
                                                const uint64_t* __restrict__ sk, const uint32_t* __restrict__ sperm,
                                                int64_t n, int flo, int fhi, uint64_t* mkey, int32_t* msrc,
                                                uint64_t* fp_in, const int64_t* n_dev, int shiftLa,
                                                const uint64_t* __restrict__ ht, int64_t htcap, int64_t* dest_offsets,
                                                SegJob sj, uint64_t* gst, uint64_t* lst, uint32_t* ctr,
-                                               int32_t* perm_out, int32_t* dest_out, int32_t* status) {
+                                               int32_t* perm_out, int32_t* dest_out, const uint64_t* rflag,
+                                               uint64_t rseq, int32_t* status) {
   n = dev_n(n_dev, n);
   int64_t Lc = ctl->live;
   Lc = Lc < 0 ? 0 : (Lc > cap ? cap : Lc);
   const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = (int64_t)gridDim.x * blockDim.x;
+  // the live set's loads first (this thread's first element, the sampled keys): they
+  // do not depend on the routing, whose signal may still be on its way; nothing in
+  // the workspace is read or written before the wait
+  const int64_t t1 = gtid;
+  uint64_t k1 = 0;
+  uint32_t p1 = 0;
+  if (t1 < Lc) k1 = live.key[t1];
+  // sampled keys of both runs: the step's every s1-th (c1 of them), the live set's
+  // every s2-th (c2); blocks past the merged run load none
+  __shared__ uint64_t s_sk[MERGE_SAMPLES], s_lk[MERGE_SAMPLES];
+  const int64_t s1 = n > MERGE_SAMPLES ? cdiv(n, MERGE_SAMPLES) : 1, c1 = cdiv(n, s1);
+  const int64_t s2 = Lc > MERGE_SAMPLES ? cdiv(Lc, MERGE_SAMPLES) : 1, c2 = cdiv(Lc, s2);
+  const bool sampling = (int64_t)blockIdx.x * blockDim.x < Lc + n;   // uniform across the block
+  constexpr int PER = MERGE_SAMPLES / 256;
+  uint64_t a[PER], b[PER];
+  if (sampling) {
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+      const int64_t i = threadIdx.x + r * 256;
+      b[r] = i < c2 ? live.key[i * s2] : 0ull;
+    }
+  }
+  route_wait(rflag, rseq, status);
   if (gtid == 0) {
     ctl->merged = Lc + n;
     ctl->merged1 = Lc + n + 1;
@@ -130,30 +190,17 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   if (dest_offsets && n == 0 && gtid == 0)
     for (uint32_t x = 0; x <= rg.num_dest; ++x) dest_offsets[x] = 0;
   bool late = false;
-  // this thread's first element (loaded before the samples, which it does not need)
-  const int64_t t1 = gtid;
-  uint64_t k1 = 0;
-  uint32_t p1 = 0;
-  if (t1 < Lc) {
-    k1 = live.key[t1];
-  } else if (t1 < Lc + n) {
+  if (t1 >= Lc && t1 < Lc + n) {
     k1 = sk[t1 - Lc];
     p1 = sperm[t1 - Lc];
+    p1 = p1 < (uint32_t)n ? p1 : 0u;
   }
-  // sampled keys of both runs: the step's every s1-th (c1 of them), the live set's
-  // every s2-th (c2); blocks past the merged run load none
-  __shared__ uint64_t s_sk[MERGE_SAMPLES], s_lk[MERGE_SAMPLES];
-  const int64_t s1 = n > MERGE_SAMPLES ? cdiv(n, MERGE_SAMPLES) : 1, c1 = cdiv(n, s1);
-  const int64_t s2 = Lc > MERGE_SAMPLES ? cdiv(Lc, MERGE_SAMPLES) : 1, c2 = cdiv(Lc, s2);
-  if ((int64_t)blockIdx.x * blockDim.x < Lc + n) {   // uniform across the block
+  if (sampling) {
     // all of a thread's sample loads first (independent, in flight together)
-    constexpr int PER = MERGE_SAMPLES / 256;
-    uint64_t a[PER], b[PER];
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
       const int64_t i = threadIdx.x + r * 256;
       a[r] = i < c1 ? sk[i * s1] : 0ull;
-      b[r] = i < c2 ? live.key[i * s2] : 0ull;
     }
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
@@ -194,7 +241,8 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
     } else {
       const int64_t j = t - Lc;
       const uint64_t k = t == t1 ? k1 : sk[j];
-      const uint32_t pj = t == t1 ? p1 : sperm[j];
+      const uint32_t pr = t == t1 ? p1 : sperm[j];
+      const uint32_t pj = pr < (uint32_t)n ? pr : 0u;   // always, unless a routing wait gave up
       late |= emitted_has(key_prefix(k, shiftLa), ht, htcap);
       // number of live keys <= k: c sampled ones, so between (c - 1) s2 + 1 and c s2
       int64_t a = 0, b = c2;
@@ -677,12 +725,15 @@ struct alto_stream {
   int32_t* pflag;
   int32_t* ppart;
   int64_t* plen;
-  // overlapped steps (alto_stream_step_overlap): the workspace of the next step, and
-  // per workspace the end of its routing and of its step
+  // overlapped steps (alto_stream_step_overlap): the workspace of the next step,
+  // per workspace the end of its step, the routing-done words (device, one per
+  // workspace) and the last sequence number
   int wslot;
   bool ev_made;
   bool ev_used[2];
-  hipEvent_t ev_routed[2], ev_done[2];
+  hipEvent_t ev_done[2];
+  uint64_t* rflag;
+  uint64_t rseq;
 };
 
 namespace {
@@ -721,6 +772,7 @@ void carve_state(const KeyGeom& g, const alto_agg& agg, int64_t cap, int64_t max
   s->pflag = c.take<int32_t>(cap + 1);
   s->ppart = c.take<int32_t>(SCAN_MAX_BLOCKS + 1);
   s->plen = c.take<int64_t>(4);
+  s->rflag = c.take<uint64_t>(2 * ROUTE_FLAG_STRIDE);
 }
 
 bool layout_valid(const alto_layout* l) {
@@ -795,6 +847,7 @@ int alto_stream_create(const alto_layout* layout, int32_t route_level, int32_t n
   s->wslot = 0;
   s->ev_made = false;
   s->ev_used[0] = s->ev_used[1] = false;
+  s->rseq = fresh_fp_key();   // random base of the routing sequence numbers
   WsCarver c{(char*)state, state_bytes, 0, true};
   carve_state(s->g, *agg, max_live_leaves, max_groups, c, s);
   if (!c.ok) {
@@ -816,12 +869,13 @@ int alto_stream_create(const alto_layout* layout, int32_t route_level, int32_t n
 
 namespace {
 
-// One step; with route_st != st (and ev), the routing runs on route_st and the rest
-// on st after it, and the merge writes the caller's perm and dest.
+// One step; with rslot >= 0, the routing runs on route_st and the rest on st after
+// it (the merge waits for routing-done word rslot), and the merge writes the
+// caller's perm and dest.
 int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld, const int32_t* payload_i32,
                 const float* payload_f32, int64_t n, const int64_t* n_dev, int32_t* perm, int64_t* dest_offsets,
                 int32_t* dest, alto_groups* emitted, int32_t* status, void* ws, size_t ws_bytes,
-                hipStream_t route_st, hipStream_t st, hipEvent_t ev_routed) {
+                hipStream_t route_st, hipStream_t st, int rslot) {
   // n: the step's count (n_dev null) or its bound (the count is *n_dev on the device)
   if (!s || !status || !emitted || !emitted->counts || n < 0 || n > (int64_t)INT32_MAX / 2 ||
       emitted->cap_groups < 0 || emitted->cap_tokens < 0)
@@ -849,13 +903,15 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   if (!c.ok) return ALTO_E_ARG;
   // 1. route the step on its own
   // (destination offsets: written by the merge, from the step's sorted keys)
-  const bool split = ev_routed != nullptr;
+  const bool split = rslot >= 0;
   int rc = route_run(g, s->rg, keys, n, b, split ? nullptr : perm, dest_offsets, split ? nullptr : dest, fan, fan_ld,
                      La, d - 1, status, split ? route_st : st, true, false, false, n_dev);
   if (rc) return rc;
+  uint64_t* rflag = nullptr;
+  const uint64_t rseq = split ? ++s->rseq : 0;
   if (split) {
-    if (hipEventRecord(ev_routed, route_st) != hipSuccess || hipStreamWaitEvent(st, ev_routed, 0) != hipSuccess)
-      return ALTO_E_HIP;
+    rflag = s->rflag + rslot * ROUTE_FLAG_STRIDE;
+    k_route_signal<<<1, 64, 0, route_st>>>(rflag, rseq);
   }
   prof_begin(PH_SEGMENT, st);
   const uint32_t* sperm = b.perm_used;
@@ -908,10 +964,12 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   }
   // 2. merge with the live set (also: late fragments, a poisoned handle, the step's
   // destination offsets, the clearing of the step's look-back words)
-  k_merge<<<grid_for(ntot, 256), 256, 0, st>>>(g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc,
-                                               b.fp_in, n_dev, g.shift[La], s->ht, s->htcap, dest_offsets, j, gst,
-                                               lst, b.os_ctr + 1, split ? perm : nullptr, split ? dest : nullptr,
-                                               status);
+  // (with the routing on another stream, at most two blocks per CU: the merge's
+  // blocks wait for the routing, whose kernels need room on the CUs)
+  k_merge<<<grid_for(ntot, 256, split ? 512 : 4096), 256, 0, st>>>(
+      g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc, b.fp_in, n_dev, g.shift[La], s->ht,
+      s->htcap, dest_offsets, j, gst, lst, b.os_ctr + 1, split ? perm : nullptr, split ? dest : nullptr, rflag, rseq,
+      status);
   // 3. nodes and completion over the merged run
   rc = seg_run(g, j, st);
   if (rc) return rc;
@@ -1045,7 +1103,7 @@ int alto_stream_step_dev(alto_stream* s, const uint64_t* keys, const int32_t* fa
                          int32_t* perm, int64_t* dest_offsets, int32_t* dest, alto_groups* emitted, int32_t* status,
                          void* ws, size_t ws_bytes, hipStream_t st) {
   return stream_step(s, keys, fan, fan_ld, payload_i32, payload_f32, n, n_dev, perm, dest_offsets, dest, emitted,
-                     status, ws, ws_bytes, st, st, nullptr);
+                     status, ws, ws_bytes, st, st, -1);
 }
 
 int alto_stream_step_overlap(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_t fan_ld,
@@ -1055,18 +1113,15 @@ int alto_stream_step_overlap(alto_stream* s, const uint64_t* keys, const int32_t
                              hipStream_t st) {
   if (!s || !ws0 || !ws1 || ws0 == ws1) return ALTO_E_ARG;
   if (!s->ev_made) {
-    for (int k = 0; k < 2; ++k) {
-      if (hipEventCreateWithFlags(&s->ev_routed[k], hipEventDisableTiming) != hipSuccess ||
-          hipEventCreateWithFlags(&s->ev_done[k], hipEventDisableTiming) != hipSuccess)
-        return ALTO_E_HIP;
-    }
+    for (int k = 0; k < 2; ++k)
+      if (hipEventCreateWithFlags(&s->ev_done[k], hipEventDisableTiming) != hipSuccess) return ALTO_E_HIP;
     s->ev_made = true;
   }
   const int k = s->wslot;
   // the step two calls back used this workspace: its end on st comes first
   if (s->ev_used[k] && hipStreamWaitEvent(route_stream, s->ev_done[k], 0) != hipSuccess) return ALTO_E_HIP;
   const int rc = stream_step(s, keys, fan, fan_ld, payload_i32, payload_f32, n, n_dev, perm, dest_offsets, dest,
-                             emitted, status, k ? ws1 : ws0, ws_bytes, route_stream, st, s->ev_routed[k]);
+                             emitted, status, k ? ws1 : ws0, ws_bytes, route_stream, st, k);
   if (rc) return rc;
   if (hipEventRecord(s->ev_done[k], st) != hipSuccess) return ALTO_E_HIP;
   s->ev_used[k] = true;
@@ -1097,10 +1152,7 @@ int alto_stream_pending(alto_stream* s, alto_groups* out, int32_t* status, hipSt
 
 int alto_stream_destroy(alto_stream* s) {
   if (s && s->ev_made) {
-    for (int k = 0; k < 2; ++k) {
-      (void)hipEventDestroy(s->ev_routed[k]);
-      (void)hipEventDestroy(s->ev_done[k]);
-    }
+    for (int k = 0; k < 2; ++k) (void)hipEventDestroy(s->ev_done[k]);
   }
   if (!s) return ALTO_E_ARG;
   delete s;
