@@ -278,9 +278,9 @@ int alto_stream_step_dev(alto_stream *s, const uint64_t *keys, const int32_t *fa
  * the handle, created at the first call). The merge's first kernel waits on the
  * device for the routing: a one-thread kernel on route_stream, after the routing
  * and whatever the caller enqueued there before, stores the step's sequence number
- * in a word of the handle's state, and the merge's blocks (at most 512, so that
- * the routing finds room on the CUs) poll it before they read the routing's
- * outputs. The wait is bounded (seconds; then ALTO_E_INTERNAL in `status`), so
+ * in a word of the handle's state, and the merge's blocks that hold elements (at
+ * most 256, one per CU, so that the routing finds room beside them) poll it
+ * before they read the routing's outputs. The wait is bounded (seconds; then ALTO_E_INTERNAL in `status`), so
  * route_stream must not wait for work that the caller enqueues on `stream` after
  * this call. The inputs (keys, fan, payloads, n_dev)
  * are read on route_stream and on `stream`: they must be ready on both (a producer

@@ -146,7 +146,13 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   n = dev_n(n_dev, n);
   int64_t Lc = ctl->live;
   Lc = Lc < 0 ? 0 : (Lc > cap ? cap : Lc);
-  const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = (int64_t)gridDim.x * blockDim.x;
+  // blocks past the merged run (the grid is sized for the largest count) leave at
+  // once: only blocks that hold elements wait for the routing, and they also do the
+  // grid-stride clearing below
+  const int64_t nwork_ = cdiv(Lc + n, (int64_t)blockDim.x);
+  const int64_t nwork = nwork_ < 1 ? 1 : (nwork_ > (int64_t)gridDim.x ? (int64_t)gridDim.x : nwork_);
+  if ((int64_t)blockIdx.x >= nwork) return;
+  const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = nwork * blockDim.x;
   // the live set's loads first (this thread's first element, the sampled keys): they
   // do not depend on the routing, whose signal may still be on its way; nothing in
   // the workspace is read or written before the wait
@@ -964,9 +970,10 @@ int stream_step(alto_stream* s, const uint64_t* keys, const int32_t* fan, int64_
   }
   // 2. merge with the live set (also: late fragments, a poisoned handle, the step's
   // destination offsets, the clearing of the step's look-back words)
-  // (with the routing on another stream, at most two blocks per CU: the merge's
-  // blocks wait for the routing, whose kernels need room on the CUs)
-  k_merge<<<grid_for(ntot, 256, split ? 512 : 4096), 256, 0, st>>>(
+  // (with the routing on another stream at most one block per CU: the merge's
+  // blocks wait for the routing, whose kernels need room on the CUs, e.g. the
+  // one-workgroup sort's 1,024 threads and up to 107 KB of LDS)
+  k_merge<<<grid_for(ntot, 256, split ? 256 : 4096), 256, 0, st>>>(
       g, s->rg, s->ctl, s->cap, old, b.sk, sperm, n, La, d - 1, mkey, msrc, b.fp_in, n_dev, g.shift[La], s->ht,
       s->htcap, dest_offsets, j, gst, lst, b.os_ctr + 1, split ? perm : nullptr, split ? dest : nullptr, rflag, rseq,
       status);
