@@ -551,15 +551,14 @@ def bench_factool_stream(args):
         side, rA, rB = side_stream, route_a, route_b
         a_done = [torch.cuda.Event() for _ in range(2)]
         b_done = [torch.cuda.Event() for _ in range(2)]
-        t0 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
-        t1 = [torch.cuda.Event(enable_timing=True) for _ in range(nsteps)]
+        ev = _LightEvents(2 * nsteps)   # step s: start s, end nsteps + s
         for x in (side, rA, rB):
             x.wait_stream(main)
         for s in range(nsteps):
             k = s & 1
             a, b = s * step, (s + 1) * step
             r0 = (s * step) % ring_rows
-            t0[s].record(rA)
+            ev.record(s, rA)
             if s >= 2:
                 main.wait_event(b_done[k])
             # stage A: routing on rA (beside the previous step), the rest on main
@@ -574,15 +573,17 @@ def bench_factool_stream(args):
                         n_dev=gAs[k].counts[0:1], stream=side, route_stream=rB if route_sb else None)
                 emitted.add_(gAs[k].counts[0:1])
             b_done[k].record(side)
-            t1[s].record(side)
+            ev.record(nsteps + s, side)
         for x in (side, rA, rB):
             main.wait_stream(x)
         torch.cuda.synchronize()
         sA.close()
         sB.close()
-        lat = [t0[s].elapsed_time(t1[s]) for s in range(nsteps)]
-        period = [t1[s - 1].elapsed_time(t1[s]) for s in range(1, nsteps)]
-        return t0[0].elapsed_time(t1[nsteps - 1]), lat, period
+        lat = [ev.elapsed_ms(s, nsteps + s) for s in range(nsteps)]
+        period = [ev.elapsed_ms(nsteps + s - 1, nsteps + s) for s in range(1, nsteps)]
+        tot = ev.elapsed_ms(0, 2 * nsteps - 1)
+        ev.close()
+        return tot, lat, period
     side_stream, route_a, route_b = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     route_sa = args.stream_overlap in ("a", "ab")
     route_sb = args.stream_overlap in ("b", "ab")
@@ -605,7 +606,10 @@ def bench_factool_stream(args):
     return _line(f"FacTool-shaped windowed stream: {steps} steps x {step} fragments, 768-d mean per document "
                  f"then document-id concat per claim (both stages each step, the claim stage reading the "
                  f"document stage's emitted count on the device; the claim stage of a step on a second HIP "
-                 f"stream beside the document stage of the next, each stage's routing on a stream of its own), "
+                 f"stream beside the document stage of the next"
+                 + {"ab": ", each stage's routing on a stream of its own", "a": ", the document stage's routing on "
+                    "a stream of its own", "b": ", the claim stage's routing on a stream of its own",
+                    "none": ""}[args.stream_overlap] + "), "
                  f"release {args.release}",
                  step, ms, steps, 50, path_bytes,
                  {"stream_fragments": n, "documents_emitted": E, "window_fragments": w.info["window"],
@@ -878,7 +882,7 @@ def main():
                     help="write the mean kernel's HBM traffic summary from two rocprofv3 --pmc "
                          "counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) and exit")
     ap.add_argument("--pmc-command", default="", help="the rocprofv3 commands, recorded in the summary")
-    ap.add_argument("--stream-overlap", default="none", choices=["none", "a", "b", "ab"],
+    ap.add_argument("--stream-overlap", default="ab", choices=["none", "a", "b", "ab"],
                     help="factool_stream: which stages (document a, claim b) route each step on a HIP stream of "
                          "their own (the stages always run on two streams)")
     ap.add_argument("--no-stage-overlap", action="store_true",
