@@ -445,14 +445,16 @@ def bench_tokens(args):
         route = route_stream
         route.wait_stream(main)
         ev = _LightEvents(2 * nsteps)   # t0[i] = i, t1[i] = nsteps + i
+        one = s.prepare(out, status, stream=main, route_stream=route)   # fixed arguments checked once
+        h0 = time.perf_counter()
         for i in range(nsteps):
             a, b = i * step, min(n, (i + 1) * step)
             if (ends and starts) or i == 0:
                 ev.record(i, route)
-            s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status, stream=main,
-                   route_stream=route)
+            one(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b])
             if ends or i == nsteps - 1:
                 ev.record(nsteps + i, main)
+        host_us[0] = (time.perf_counter() - h0) * 1e6 / nsteps
         main.wait_stream(route)
         torch.cuda.synchronize()
         s.close()
@@ -462,6 +464,7 @@ def bench_tokens(args):
         ev.close()
         return tot, lat, period
     route_stream = torch.cuda.Stream()
+    host_us = [0.0]   # the host's time to enqueue a step (the last run)
     # the stream is short (96 steps, a few ms): many runs, so that the GPU clock
     # settles first and the percentiles pool enough steps
     reps, warm = 10, max(args.warmup, 20)
@@ -482,7 +485,8 @@ def bench_tokens(args):
         tot += t / reps
         period += p
         lat += run_overlapped()[1]
-    bare = sum(run_overlapped(ends=False, starts=False)[0] for _ in range(reps)) / reps
+    bare_runs = sorted(run_overlapped(ends=False, starts=False)[0] / nsteps for _ in range(reps))
+    host_bare = host_us[0]
     assert int(status.item()) == 0
     ms = tot / nsteps
     path_bytes = (n * (8 + 4 + 4 + 4 + 4 + 4) + 16384 * (8 + 4 + 8 + 4 + 8)) / nsteps
@@ -496,7 +500,9 @@ def bench_tokens(args):
                               "step_ms_note": "p50/p99/max of the period between consecutive steps' ends, "
                                               f"{reps} runs of {nsteps} steps pooled, an event at each step's end; "
                                               "latency from runs with an event at each step's start as well",
-                              "uninstrumented_ms_per_step": bare / nsteps,
+                              "uninstrumented_ms_per_step": _pct(bare_runs, 50),
+                              "uninstrumented_ms_per_step_min_max": [bare_runs[0], bare_runs[-1]],
+                              "host_enqueue_us_per_step": host_bare,
                               "step_latency_ms_p50": _pct(lat, 50), "step_latency_ms_p99": _pct(lat, 99),
                               "sequential_ms_per_step": seq_tot / nsteps, "sequential_step_ms_p50": _pct(seq_per, 50),
                               "sequential_step_ms_p99": _pct(seq_per, 99)})
@@ -538,10 +544,12 @@ def bench_factool_stream(args):
         sA.close()
         sB.close()
         return tot, per
-    def run_pipelined(nsteps):
+    def run_pipelined(nsteps, count=False):
         # stage B of step s on a second HIP stream, beside stage A of step s + 1:
         # stage A writes its records into one of two buffers, stage B waits for them
-        # (an event), stage A waits before reusing a buffer until stage B has read it
+        # (an event), stage A waits before reusing a buffer until stage B has read it.
+        # count: also add up the emitted documents (a torch kernel per step on the
+        # second stream, and its launch on the host: bookkeeping, so not in timed runs)
         sA = alto.Stream(w.bits, 2, 32, 4, "mean", 768, max_live_leaves=1 << 17, max_groups=1 << 22,
                          step_max=step, release=args.release)
         sB = alto.Stream(sbB["bits"], 2, 32, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 20,
@@ -554,6 +562,11 @@ def bench_factool_stream(args):
         ev = _LightEvents(2 * nsteps)   # step s: start s, end nsteps + s
         for x in (side, rA, rB):
             x.wait_stream(main)
+        # the per-step calls with their fixed arguments checked once (Stream.prepare)
+        stepA = [sA.prepare(gAs[k], stA, stream=main, route_stream=rA if route_sa else None) for k in range(2)]
+        stepB = sB.prepare(gB, stB, stream=side, route_stream=rB if route_sb else None)
+        nA = [g.counts[0:1] for g in gAs]
+        h0 = time.perf_counter()
         for s in range(nsteps):
             k = s & 1
             a, b = s * step, (s + 1) * step
@@ -562,18 +575,18 @@ def bench_factool_stream(args):
             if s >= 2:
                 main.wait_event(b_done[k])
             # stage A: routing on rA (beside the previous step), the rest on main
-            sA.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step], out=gAs[k], status=stA,
-                    stream=main, route_stream=rA if route_sa else None)
+            stepA[k](keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step])
             a_done[k].record(main)
             # stage B over stage A's records: routing on rB, the rest on side
             rB.wait_event(a_done[k])
             side.wait_event(a_done[k])
-            with torch.cuda.stream(side):
-                sB.step(gAs[k].key, fanAs[k], gAs[k].first_i32, None, out=gB, status=stB, n=step,
-                        n_dev=gAs[k].counts[0:1], stream=side, route_stream=rB if route_sb else None)
-                emitted.add_(gAs[k].counts[0:1])
+            stepB(gAs[k].key, fanAs[k], gAs[k].first_i32, None, n=step, n_dev=nA[k])
+            if count:
+                with torch.cuda.stream(side):
+                    emitted.add_(nA[k])
             b_done[k].record(side)
             ev.record(nsteps + s, side)
+        host_us[0] = (time.perf_counter() - h0) * 1e6 / nsteps
         for x in (side, rA, rB):
             main.wait_stream(x)
         torch.cuda.synchronize()
@@ -585,6 +598,7 @@ def bench_factool_stream(args):
         ev.close()
         return tot, lat, period
     side_stream, route_a, route_b = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    host_us = [0.0]   # the host's time to enqueue a step (the last run)
     route_sa = args.stream_overlap in ("a", "ab")
     route_sb = args.stream_overlap in ("b", "ab")
     gAs = [gA, alto.new_groups(step, 4, "mean", 768)]
@@ -595,6 +609,9 @@ def bench_factool_stream(args):
     E_seq = int(emitted.item())
     run_pipelined(max(args.warmup, 1) * 50)
     total, lat, period = run_pipelined(steps)
+    host_timed = host_us[0]
+    assert int(stA.item()) == 0 and int(stB.item()) == 0
+    run_pipelined(steps, count=True)   # untimed: the same documents as on one stream
     assert int(stA.item()) == 0 and int(stB.item()) == 0
     E = int(emitted.item())
     assert E == E_seq
@@ -617,6 +634,7 @@ def bench_factool_stream(args):
                   "step_ms_p50": _pct(period, 50), "step_ms_p99": _pct(period, 99), "step_ms_max": max(period),
                   "step_ms_note": "p50/p99/max of the period between consecutive steps' ends (two stages in flight)",
                   "step_latency_ms_p50": _pct(lat, 50), "step_latency_ms_p99": _pct(lat, 99),
+                  "host_enqueue_us_per_step": host_timed,
                   "sequential_ms_per_step": seq_total / steps, "sequential_step_ms_p50": _pct(seq_dev, 50),
                   "sequential_step_ms_p99": _pct(seq_dev, 99)})
 

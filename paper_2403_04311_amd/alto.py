@@ -548,6 +548,19 @@ class Stream:
         _check(rc, "alto_stream_step")
         return out, status
 
+    def prepare(self, out: GroupTensors, status, perm=None, dest_offsets=None, dest=None, stream=None,
+                route_stream=None) -> "PreparedStep":
+        """The arguments that stay the same from step to step, checked once: returns
+        a callable that takes only a step's inputs (keys, fan, payloads, n, n_dev)
+        and calls the same entry point as step() (alto_stream_step_overlap with a
+        route_stream, else alto_stream_step_dev). For callers that run many short
+        steps, whose per-call argument checks would otherwise cost the host about as
+        much as the step's launches. perm and dest must hold step_max elements. The
+        tensors given here (and those of `out`) must stay allocated, in place and
+        unresized while the returned object is used; prepare again after changing
+        any of them."""
+        return PreparedStep(self, out, status, perm, dest_offsets, dest, stream, route_stream)
+
     def pending(self, out: Optional[GroupTensors] = None, status=None, stream=None, cap=None):
         dev = self.state.device
         if out is None:
@@ -742,3 +755,60 @@ def split(keys: torch.Tensor, fan: torch.Tensor, tokens: torch.Tensor, bits, del
                         _p(counts), _p(status), _p(ws), _nbytes(ws), _stream(stream))
     _check(rc, "alto_split")
     return out_keys, out_fan, out_tokens, out_idx, rest_idx, counts, status
+
+
+class PreparedStep:
+    """Stream.step with its fixed arguments checked and marshalled once (Stream.prepare)."""
+
+    def __init__(self, s: Stream, out: GroupTensors, status, perm, dest_offsets, dest, stream, route_stream):
+        a = _Args("alto_stream_step (prepared)")
+        if out is None or status is None:
+            a.fail("out and status are required")
+        a.t(perm, "perm", torch.int32, s.step_max, optional=True)
+        a.t(dest_offsets, "dest_offsets", torch.int64, s.D + 1, optional=True)
+        a.t(dest, "dest", torch.int32, s.step_max, optional=True)
+        out.check(a, s.op, s.La, s.dim)
+        a.t(status, "status", torch.int32, 1)
+        a.t(s.ws, "workspace", torch.uint8)
+        if a.device() != s.state.device:
+            a.fail(f"arguments on {a.dev}, stream state on {s.state.device}")
+        if route_stream is not None and getattr(s, "ws2", None) is None:
+            s.ws2 = torch.empty_like(s.ws)
+        self.s, self.dev = s, s.state.device
+        self.keep = (out, status, perm, dest_offsets, dest, stream, route_stream)   # alive while prepared
+        self.G = out.struct()
+        self.Gp = C.byref(self.G)
+        self.fixed = (_p(perm), _p(dest_offsets), _p(dest))
+        self.status = _p(status)
+        self.ws, self.ws2 = _p(s.ws), _p(getattr(s, "ws2", None) if route_stream is not None else None)
+        self.nbytes = _nbytes(s.ws)
+        self.stream, self.route = _stream(stream), (_stream(route_stream) if route_stream is not None else None)
+        self.out, self.status_t = out, status
+        self.nrows = len(s.bits) - 1
+
+    def __call__(self, keys, fan, payload_i32=None, payload_f32=None, n=None, n_dev=None):
+        s = self.s
+        n = keys.shape[0] if n is None else n
+        if n > s.step_max:
+            raise AltoError(E_ARG, "step larger than step_max")
+        a = _Args("alto_stream_step (prepared)")
+        a.t(keys, "keys", _KEY_DTYPES, n)
+        fan_ld = a.rows(fan, "fan", torch.int32, self.nrows, n)
+        a.t(payload_i32, "payload_i32", torch.int32, n, optional=s.op != "concat")
+        a.payload(payload_f32, "payload_f32", n, s.dim, optional=s.op != "mean")
+        a.t(n_dev, "n_dev", torch.int64, 1, optional=True)
+        if a.device() != self.dev:
+            a.fail(f"inputs on {a.dev}, prepared arguments on {self.dev}")
+        perm, offs, dest = self.fixed
+        if self.route is not None:
+            rc = s.lib.alto_stream_step_overlap(s.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32),
+                                                _p(payload_f32), n, _p(n_dev), perm, offs, dest, self.Gp,
+                                                self.status, self.ws, self.ws2, self.nbytes, self.route,
+                                                self.stream)
+            _check(rc, "alto_stream_step_overlap")
+        else:
+            rc = s.lib.alto_stream_step_dev(s.handle, _p(keys), _p(fan), fan_ld, _p(payload_i32), _p(payload_f32),
+                                            n, _p(n_dev), perm, offs, dest, self.Gp, self.status, self.ws,
+                                            self.nbytes, self.stream)
+            _check(rc, "alto_stream_step")
+        return self.out, self.status_t

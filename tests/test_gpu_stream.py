@@ -566,3 +566,65 @@ def test_overlapped_steps_match_sequential_token_stream():
         assert (p0 >= 0).all() and (d0 >= 0).all()
         total += E
     assert total > 10000
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("overlap", [False, True])
+def test_prepared_steps_match_step(overlap):
+    """Stream.prepare (fixed arguments checked once, per-step inputs only) calls the
+    same entry point as Stream.step: every step's perm, dest, dest_offsets and
+    emitted groups are the same bits, on one stream and with the routing on a
+    second one; and it refuses inputs on the wrong device or a step above step_max."""
+    from paper_2403_04311_amd import workloads as W
+    w = W.token_stream("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n, step = w.n, w.step
+    nsteps = (n + step - 1) // step
+
+    def run(prepared):
+        s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step)
+        out = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
+        status = alto.new_status()
+        perm = torch.empty(step, dtype=torch.int32, device="cuda")
+        dest = torch.empty(step, dtype=torch.int32, device="cuda")
+        offs = torch.empty(65, dtype=torch.int64, device="cuda")
+        main = torch.cuda.current_stream()
+        route = torch.cuda.Stream() if overlap else None
+        if route is not None:
+            route.wait_stream(main)
+        one = s.prepare(out, status, perm=perm, dest_offsets=offs, dest=dest, stream=main,
+                        route_stream=route) if prepared else None
+        res = []
+        for i in range(nsteps):
+            a, b = i * step, min(n, (i + 1) * step)
+            m = b - a
+            if prepared:
+                one(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b])
+            else:
+                s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status, perm=perm,
+                       dest=dest, dest_offsets=offs, stream=main, route_stream=route)
+            c = out.counts.clone()
+            res.append((perm[:m].clone(), dest[:m].clone(), offs.clone(), c, out.key.clone(), out.tok_off.clone(),
+                        out.tok.clone()))
+        if route is not None:
+            main.wait_stream(route)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        if prepared:
+            with pytest.raises(alto.AltoError):
+                one(keys[:step + 1], w.fan[:, :step + 1], w.payload_i32[:step + 1])
+            with pytest.raises(alto.AltoError):
+                one(keys[:8].cpu(), w.fan[:, :8].cpu(), w.payload_i32[:8].cpu())
+        s.close()
+        return res
+    ref = run(False)
+    got = run(True)
+    total = 0
+    for i in range(nsteps):
+        (p0, d0, o0, c0, k0, t0, x0), (p1, d1, o1, c1, k1, t1, x1) = ref[i], got[i]
+        assert torch.equal(p0, p1) and torch.equal(d0, d1) and torch.equal(o0, o1), i
+        assert torch.equal(c0, c1), i
+        E, T = int(c0[0]), int(c0[1])
+        assert torch.equal(k0[:E], k1[:E]) and torch.equal(t0[:E + 1], t1[:E + 1]) and torch.equal(x0[:T], x1[:T]), i
+        total += E
+    assert total > 10000
