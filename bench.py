@@ -571,7 +571,7 @@ def bench_factool_stream(args):
             k = s & 1
             a, b = s * step, (s + 1) * step
             r0 = (s * step) % ring_rows
-            ev.record(s, rA)
+            ev.record(s, rA if route_sa else main)
             if s >= 2:
                 main.wait_event(b_done[k])
             # stage A: routing on rA (beside the previous step), the rest on main
