@@ -555,7 +555,8 @@ class Stream:
         and calls the same entry point as step() (alto_stream_step_overlap with a
         route_stream, else alto_stream_step_dev). For callers that run many short
         steps, whose per-call argument checks would otherwise cost the host about as
-        much as the step's launches. perm and dest must hold step_max elements. The
+        much as the step's launches. perm and dest must hold step_max elements;
+        stream None is the current stream at this call. The
         tensors given here (and those of `out`) must stay allocated, in place and
         unresized while the returned object is used; prepare again after changing
         any of them."""
