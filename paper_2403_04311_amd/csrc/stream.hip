@@ -94,7 +94,7 @@ __global__ void k_stream_begin(const StreamCtl* ctl, int32_t* status) {
 // per-handle random base plus a count, compared for equality, so a stale word of
 // an earlier handle in the same memory never matches) and then acquires.
 constexpr int64_t ROUTE_FLAG_STRIDE = 32;      // uint64 words: 256 bytes
-constexpr int ROUTE_WAIT_LIMIT = 1 << 24;      // polls of ~0.2-1 us: seconds, then ALTO_E_INTERNAL
+constexpr int ROUTE_WAIT_LIMIT = 1 << 22;      // polls of ~0.3-1.2 us: 1-5 s, then ALTO_E_INTERNAL
 
 __global__ void k_route_signal(uint64_t* flag, uint64_t seq) {
   if (threadIdx.x == 0) __hip_atomic_store(flag, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
