@@ -628,3 +628,54 @@ def test_prepared_steps_match_step(overlap):
         assert torch.equal(k0[:E], k1[:E]) and torch.equal(t0[:E + 1], t1[:E + 1]) and torch.equal(x0[:T], x1[:T]), i
         total += E
     assert total > 10000
+
+
+@pytest.mark.gpu
+def test_overlapped_steps_with_empty_steps_match_sequential():
+    """alto_stream_step_overlap with empty steps between non-empty ones (a host
+    count of 0: nothing is routed and no routing word is signalled for them) keeps
+    the workspace alternation and the routing join of the following steps: every
+    step's emitted groups are the same bits as on one stream."""
+    from paper_2403_04311_amd import workloads as W
+    w = W.token_stream("cuda")
+    keys, st = alto.pack_keys(w.path, w.bits)
+    n, step = w.n, w.step
+    nsteps = min((n + step - 1) // step, 40)
+    order = []
+    for i in range(nsteps):
+        order.append(i)
+        if i % 3 == 1:
+            order.append(None)   # an empty step
+            if i % 2 == 1:
+                order.append(None)
+
+    def run(overlap):
+        s = alto.Stream(w.bits, 2, 64, 2, "concat", 1, max_live_leaves=1 << 16, max_groups=1 << 16, step_max=step)
+        out = alto.new_groups(step, 2, "concat", cap_tokens=(1 << 16) + step)
+        status = alto.new_status()
+        main = torch.cuda.current_stream()
+        route = torch.cuda.Stream() if overlap else None
+        if route is not None:
+            route.wait_stream(main)
+        res = []
+        for i in order:
+            a, b = (0, 0) if i is None else (i * step, min(n, (i + 1) * step))
+            s.step(keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], None, out=out, status=status, stream=main,
+                   route_stream=route)
+            c = out.counts.clone()
+            res.append((c, out.key.clone(), out.tok_off.clone(), out.tok.clone()))
+        if route is not None:
+            main.wait_stream(route)
+        torch.cuda.synchronize()
+        assert int(status.item()) == 0
+        s.close()
+        return res
+    ref, got = run(False), run(True)
+    total = 0
+    for j in range(len(order)):
+        (c0, k0, t0, x0), (c1, k1, t1, x1) = ref[j], got[j]
+        assert torch.equal(c0, c1), j
+        E, T = int(c0[0]), int(c0[1])
+        assert torch.equal(k0[:E], k1[:E]) and torch.equal(t0[:E + 1], t1[:E + 1]) and torch.equal(x0[:T], x1[:T]), j
+        total += E
+    assert total > 1000
