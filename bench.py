@@ -577,9 +577,11 @@ def bench_factool_stream(args):
             # stage A: routing on rA (beside the previous step), the rest on main
             stepA[k](keys[a:b], w.fan[:, a:b], w.payload_i32[a:b], ring[r0:r0 + step])
             a_done[k].record(main)
-            # stage B over stage A's records: routing on rB, the rest on side
+            # stage B over stage A's records: routing on rB, the rest on side (which
+            # reads them only after the routing's signal when the routing is on rB)
             rB.wait_event(a_done[k])
-            side.wait_event(a_done[k])
+            if not route_sb:
+                side.wait_event(a_done[k])
             stepB(gAs[k].key, fanAs[k], gAs[k].first_i32, None, n=step, n_dev=nA[k])
             if count:
                 with torch.cuda.stream(side):

@@ -282,10 +282,11 @@ int alto_stream_step_dev(alto_stream *s, const uint64_t *keys, const int32_t *fa
  * most 256, one per CU, so that the routing finds room beside them) poll it
  * before they read the routing's outputs. The wait is bounded (seconds; then ALTO_E_INTERNAL in `status`), so
  * route_stream must not wait for work that the caller enqueues on `stream` after
- * this call. The inputs (keys, fan, payloads, n_dev)
- * are read on route_stream and on `stream`: they must be ready on both (a producer
- * on another stream: make route_stream wait for it too). perm, dest, dest_offsets
- * and `emitted` are written on `stream`; the routing of the next call may already
+ * this call. The inputs (keys, fan, payloads, n_dev) are read on route_stream,
+ * and on `stream` only after the routing's word (by kernels that follow the
+ * merge's wait): they must be ready on route_stream; a producer on another stream
+ * needs only route_stream to wait for it. perm, dest, dest_offsets and `emitted`
+ * are written on `stream`; the routing of the next call may already
  * run when this call returns, so consecutive calls must not share input buffers
  * that the caller rewrites in between. Errors as for alto_stream_step_dev; ALTO_E_ARG
  * when ws0 or ws1 is null or they are equal. */

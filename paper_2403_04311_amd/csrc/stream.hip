@@ -143,19 +143,20 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
                                                SegJob sj, uint64_t* gst, uint64_t* lst, uint32_t* ctr,
                                                int32_t* perm_out, int32_t* dest_out, const uint64_t* rflag,
                                                uint64_t rseq, int32_t* status) {
-  n = dev_n(n_dev, n);
+  const int64_t nb = n;   // the host's count, or with n_dev its bound
   int64_t Lc = ctl->live;
   Lc = Lc < 0 ? 0 : (Lc > cap ? cap : Lc);
   // blocks past the merged run (the grid is sized for the largest count) leave at
-  // once: only blocks that hold elements wait for the routing, and they also do the
-  // grid-stride clearing below
-  const int64_t nwork_ = cdiv(Lc + n, (int64_t)blockDim.x);
+  // once: only blocks that may hold elements wait for the routing, and they also do
+  // the grid-stride clearing below
+  const int64_t nwork_ = cdiv(Lc + nb, (int64_t)blockDim.x);
   const int64_t nwork = nwork_ < 1 ? 1 : (nwork_ > (int64_t)gridDim.x ? (int64_t)gridDim.x : nwork_);
   if ((int64_t)blockIdx.x >= nwork) return;
   const int64_t gtid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x, gstride = nwork * blockDim.x;
   // the live set's loads first (this thread's first element, the sampled keys): they
   // do not depend on the routing, whose signal may still be on its way; nothing in
-  // the workspace is read or written before the wait
+  // the workspace and none of the step's inputs (not even its device count) is read
+  // or written before the wait
   const int64_t t1 = gtid;
   uint64_t k1 = 0;
   uint32_t p1 = 0;
@@ -163,12 +164,10 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
   // sampled keys of both runs: the step's every s1-th (c1 of them), the live set's
   // every s2-th (c2); blocks past the merged run load none
   __shared__ uint64_t s_sk[MERGE_SAMPLES], s_lk[MERGE_SAMPLES];
-  const int64_t s1 = n > MERGE_SAMPLES ? cdiv(n, MERGE_SAMPLES) : 1, c1 = cdiv(n, s1);
   const int64_t s2 = Lc > MERGE_SAMPLES ? cdiv(Lc, MERGE_SAMPLES) : 1, c2 = cdiv(Lc, s2);
-  const bool sampling = (int64_t)blockIdx.x * blockDim.x < Lc + n;   // uniform across the block
   constexpr int PER = MERGE_SAMPLES / 256;
   uint64_t a[PER], b[PER];
-  if (sampling) {
+  if ((int64_t)blockIdx.x * blockDim.x < Lc + nb) {   // uniform across the block
 #pragma unroll
     for (int r = 0; r < PER; ++r) {
       const int64_t i = threadIdx.x + r * 256;
@@ -176,6 +175,9 @@ __global__ __launch_bounds__(256) void k_merge(KeyGeom g, RouteGeom rg, StreamCt
     }
   }
   route_wait(rflag, rseq, status);
+  n = dev_n(n_dev, nb);
+  const int64_t s1 = n > MERGE_SAMPLES ? cdiv(n, MERGE_SAMPLES) : 1, c1 = cdiv(n, s1);
+  const bool sampling = (int64_t)blockIdx.x * blockDim.x < Lc + n;   // uniform across the block
   if (gtid == 0) {
     ctl->merged = Lc + n;
     ctl->merged1 = Lc + n + 1;

@@ -501,8 +501,9 @@ def test_two_stage_stream_pipelined_on_two_hip_streams_matches_sequential():
                 route_stream=rA)
         par_a.append(sums_a(g))
         a_done[k].record(main)
+        # stage B's merge side reads stage A's records only after stage B's routing
+        # (on rB, which waits for them) has signalled: side needs no wait of its own
         rB.wait_event(a_done[k])
-        side.wait_event(a_done[k])
         with torch.cuda.stream(side):
             sB.step(g.key, g.fan_up.view(3, -1), g.first_i32, None, out=gB, status=stB, n=step,
                     n_dev=g.counts[0:1], stream=side, route_stream=rB)
